@@ -1,0 +1,229 @@
+"""float64 CPU oracle for the event-driven LIF layer (test infrastructure).
+
+Only the test suite, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg
+of ``bench.py`` may import this package.  The GPU library never links,
+imports or calls it, and this package never imports the GPU library.
+
+Two independent implementations live here:
+
+* ``lif_oracle.c`` (compiled with gcc into ``liblif_oracle.so``): the serial
+  event loop of the paper in float64, threaded over (sample, neuron) items;
+  forward, backward (implicit differentiation through the resets) and the
+  layer merge.  Wrapped below with ctypes + numpy.
+* ``ref.py``: the same definitions in pure Python loops for tiny inputs.
+
+Functions whose results cannot be pinned independently would say
+"parity unpinned" here; at present every output (spike times, counts, I at
+spike, weight and input-time gradients, merged queues) has an independent pin
+in ``tests/test_oracle_pins.py``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "lif_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liblif_oracle.so")
+_lib = None
+
+TIE_BAND = 1e-6
+
+
+def build(force: bool = True) -> str:
+    """Compile the C oracle with gcc (plain -O2, no fast-math)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-pthread",
+                               "-D_DEFAULT_SOURCE", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+class _Params(ctypes.Structure):
+    _fields_ = [("tau_mem", ctypes.c_double), ("tau_syn", ctypes.c_double),
+                ("v_th", ctypes.c_double), ("v_reset", ctypes.c_double),
+                ("t_end", ctypes.c_double), ("s_max", ctypes.c_int32),
+                ("solver_reg", ctypes.c_double), ("tie_band", ctypes.c_double)]
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+            build()
+        _lib = ctypes.CDLL(_LIB_PATH)
+        P = ctypes.c_void_p
+        _lib.or_forward.argtypes = [P, P, P, ctypes.c_int, ctypes.c_int, P, ctypes.c_int, ctypes.c_int,
+                                    ctypes.POINTER(_Params), ctypes.c_int, P, P, P, P, P, P]
+        _lib.or_forward.restype = ctypes.c_int
+        _lib.or_backward.argtypes = [P, P, P, ctypes.c_int, ctypes.c_int, P, ctypes.c_int, ctypes.c_int,
+                                     ctypes.POINTER(_Params), ctypes.c_int, P, P, P, P, P, P]
+        _lib.or_backward.restype = ctypes.c_int
+        _lib.or_trace.argtypes = [P, P, ctypes.c_int, P, ctypes.c_int, ctypes.c_int,
+                                  ctypes.POINTER(_Params), P, P]
+        _lib.or_trace.restype = ctypes.c_int
+        _lib.or_merge.argtypes = [P, P, ctypes.c_int, ctypes.c_int, ctypes.c_int, P, P, P, P, ctypes.c_int]
+        _lib.or_merge.restype = ctypes.c_int
+        D = ctypes.c_double
+        _lib.or_check_interval.argtypes = [ctypes.POINTER(_Params), D, D, D, ctypes.POINTER(D), ctypes.POINTER(D)]
+        _lib.or_check_interval.restype = ctypes.c_int
+        _lib.or_solve_root.argtypes = [ctypes.POINTER(_Params), D, D, D]
+        _lib.or_solve_root.restype = D
+    return _lib
+
+
+@dataclass
+class LifParams:
+    tau_mem: float = 0.02
+    tau_syn: float = 0.005
+    v_th: float = 1.0
+    v_reset: float = 0.0
+    t_end: float = float("inf")
+    s_max: int = 64
+    solver_reg: float = 0.01
+    tie_band: float = TIE_BAND
+
+    def c(self) -> _Params:
+        return _Params(self.tau_mem, self.tau_syn, self.v_th, self.v_reset, self.t_end,
+                       int(self.s_max), self.solver_reg, self.tie_band)
+
+
+@dataclass
+class ForwardResult:
+    out_t: np.ndarray    # float64 [B, N, s_max], +inf padding
+    out_i: np.ndarray    # float64 [B, N, s_max], I at each spike
+    out_n: np.ndarray    # int32 [B, N]
+    capped: np.ndarray   # int32 [B, N]
+    tie_t: np.ndarray    # float64 [B, N]: start of first near-tie interval, +inf if none
+    min_gap: np.ndarray  # float64 [B, N]: smallest |V_max - V_th| over checked intervals
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _nthreads(n: Optional[int]) -> int:
+    if n is None:
+        n = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    return max(1, int(n))
+
+
+def forward(ev_t, ev_src, ev_n, WT, params: LifParams = LifParams(), nthreads: Optional[int] = None) -> ForwardResult:
+    """Serial float64 forward pass of one LIF layer over a padded batch."""
+    lib = _load()
+    ev_t = np.ascontiguousarray(ev_t, dtype=np.float32)
+    ev_src = np.ascontiguousarray(ev_src, dtype=np.int32)
+    ev_n = np.ascontiguousarray(ev_n, dtype=np.int32)
+    WT = np.ascontiguousarray(WT, dtype=np.float32)
+    B, E = ev_t.shape
+    C, N = WT.shape
+    S = int(params.s_max)
+    out_t = np.empty((B, N, S), np.float64)
+    out_i = np.empty((B, N, S), np.float64)
+    out_n = np.empty((B, N), np.int32)
+    capped = np.empty((B, N), np.int32)
+    tie_t = np.empty((B, N), np.float64)
+    min_gap = np.empty((B, N), np.float64)
+    p = params.c()
+    rc = lib.or_forward(_ptr(ev_t), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(WT), C, N, ctypes.byref(p),
+                        _nthreads(nthreads), _ptr(out_t), _ptr(out_i), _ptr(out_n), _ptr(capped),
+                        _ptr(tie_t), _ptr(min_gap))
+    if rc != 0:
+        raise ValueError(f"oracle forward rejected its arguments (rc={rc})")
+    return ForwardResult(out_t, out_i, out_n, capped, tie_t, min_gap)
+
+
+def backward(ev_t, ev_src, ev_n, WT, fwd: ForwardResult, grad_out_t, params: LifParams = LifParams(),
+             nthreads: Optional[int] = None):
+    """float64 gradients (grad_WT [C_in, N], grad_ev_t [B, E_max]) of
+    L = sum grad_out_t * out_t through the oracle's own forward result."""
+    lib = _load()
+    ev_t = np.ascontiguousarray(ev_t, dtype=np.float32)
+    ev_src = np.ascontiguousarray(ev_src, dtype=np.int32)
+    ev_n = np.ascontiguousarray(ev_n, dtype=np.int32)
+    WT = np.ascontiguousarray(WT, dtype=np.float32)
+    B, E = ev_t.shape
+    C, N = WT.shape
+    g = np.ascontiguousarray(grad_out_t, dtype=np.float64)
+    gW = np.empty((C, N), np.float64)
+    gT = np.empty((B, E), np.float64)
+    p = params.c()
+    rc = lib.or_backward(_ptr(ev_t), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(WT), C, N, ctypes.byref(p),
+                         _nthreads(nthreads), _ptr(np.ascontiguousarray(fwd.out_t)),
+                         _ptr(np.ascontiguousarray(fwd.out_i)), _ptr(np.ascontiguousarray(fwd.out_n)),
+                         _ptr(g), _ptr(gW), _ptr(gT))
+    if rc != 0:
+        raise RuntimeError(f"oracle backward failed (rc={rc})")
+    return gW, gT
+
+
+def trace(ev_t_row, ev_src_row, n, WT, i, params: LifParams = LifParams()):
+    """(V, I) just after each of the first n events for neuron i of one sample."""
+    lib = _load()
+    ev_t_row = np.ascontiguousarray(ev_t_row, dtype=np.float32)
+    ev_src_row = np.ascontiguousarray(ev_src_row, dtype=np.int32)
+    WT = np.ascontiguousarray(WT, dtype=np.float32)
+    V = np.zeros(max(n, 1), np.float64)
+    I = np.zeros(max(n, 1), np.float64)
+    p = params.c()
+    ns = lib.or_trace(_ptr(ev_t_row), _ptr(ev_src_row), int(n), _ptr(WT), WT.shape[1], int(i),
+                      ctypes.byref(p), _ptr(V), _ptr(I))
+    return V[:n], I[:n], int(ns)
+
+
+def check_interval(V0: float, I0: float, length: float, params: LifParams = LifParams()):
+    """Interval rule of Sec. 3.2.2 from state (V0, I0): (crossing, bracket_hi, V_max)."""
+    lib = _load()
+    hi = ctypes.c_double()
+    vmax = ctypes.c_double()
+    p = params.c()
+    c = lib.or_check_interval(ctypes.byref(p), float(V0), float(I0), float(length), ctypes.byref(hi),
+                              ctypes.byref(vmax))
+    return bool(c), hi.value, vmax.value
+
+
+def solve_root(V0: float, I0: float, hi: float, params: LifParams = LifParams()) -> float:
+    """Smallest float64 offset tau in (0, hi] with V(tau) >= V_th."""
+    p = params.c()
+    return float(_load().or_solve_root(ctypes.byref(p), float(V0), float(I0), float(hi)))
+
+
+def merge(out_t32, out_n, E2_max: int):
+    """Per-sample merge of spike lists (float32 times) into sorted queues.
+    Returns (ev_t2, ev_src2, ev_n2, perm, overflow)."""
+    lib = _load()
+    out_t32 = np.ascontiguousarray(out_t32, dtype=np.float32)
+    out_n = np.ascontiguousarray(out_n, dtype=np.int32)
+    B, N, S = out_t32.shape
+    ev_t2 = np.empty((B, E2_max), np.float32)
+    ev_src2 = np.empty((B, E2_max), np.int32)
+    ev_n2 = np.empty(B, np.int32)
+    perm = np.empty((B, E2_max), np.int32)
+    rc = lib.or_merge(_ptr(out_t32), _ptr(out_n), B, N, S, _ptr(ev_t2), _ptr(ev_src2), _ptr(ev_n2),
+                      _ptr(perm), int(E2_max))
+    return ev_t2, ev_src2, ev_n2, perm, bool(rc)
+
+
+def first_spike_ce(out_t_first, spiked, labels, tau0: float, t_silent: float):
+    """Readout loss: logits_c = -t_c / tau0 with t_c the first spike time of
+    readout neuron c (t_silent if it never fires); mean softmax
+    cross-entropy over the batch.  Returns (loss, dL/dt_first) in float64;
+    silent neurons get a zero gradient (their time is a constant)."""
+    t = np.where(spiked, np.asarray(out_t_first, np.float64), t_silent)
+    z = -t / tau0
+    z = z - z.max(axis=1, keepdims=True)
+    pz = np.exp(z)
+    pz /= pz.sum(axis=1, keepdims=True)
+    B = t.shape[0]
+    loss = -np.mean(np.log(pz[np.arange(B), labels]))
+    onehot = np.zeros_like(pz)
+    onehot[np.arange(B), labels] = 1.0
+    g = (pz - onehot) / B * (-1.0 / tau0)
+    g = np.where(spiked, g, 0.0)
+    return float(loss), g

@@ -1,0 +1,458 @@
+/*
+ * lif_oracle.c -- float64 CPU oracle for the event-driven current-based LIF
+ * layer with exact hard reset ("Bullet Trains", arXiv 2603.13283).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the plain, slow, sequential
+ * reference that the GPU path is checked against.  Only the test suite, the
+ * smoke check and the CPU-baseline leg of the benchmark may load it.  It
+ * shares no code, header, table or constant generator with the GPU library.
+ *
+ * Every (sample, neuron) pair is simulated independently, one event at a
+ * time, exactly as the paper's serial semantics describe (Sec. 4 baseline,
+ * Appendix E.2 and E.3): before each input event the neuron checks whether
+ * it fires in the interval up to that event (Sec. 3.2.2 interval rule); if so
+ * the spike time is solved, the voltage is hard-reset and the same interval
+ * is tested again from the spike time.  All arithmetic is IEEE float64 on the
+ * float32 input values widened to float64.
+ *
+ * Readings where the paper is silent (each is also listed in the design
+ * notes of the repository):
+ *   - the neuron starts at V = 0, I = 0 at t = 0;
+ *   - the reset acts on V only; I keeps decaying (Eq. curr_dyn);
+ *   - the threshold test is V >= V_th;
+ *   - an interior maximum needs I0 > V0 *and* D = V0 (tm - ts) + I0 ts > 0,
+ *     otherwise the log argument of Eq. t_vmax is not > 1;
+ *   - the root bracket is [0, min(t_Vmax, interval length)];
+ *   - the root is the smallest float64 offset tau with V(tau) >= V_th;
+ *   - the interval after the last event extends to t_end (default +inf);
+ *   - after the s_max-th spike the neuron stops (it is reported as capped).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <pthread.h>
+
+typedef struct {
+    double tau_mem;    /* membrane time constant tau_m (s)                   */
+    double tau_syn;    /* synaptic time constant tau_s (s), tau_s < tau_m    */
+    double v_th;       /* threshold V_th                                     */
+    double v_reset;    /* reset potential V_reset                            */
+    double t_end;      /* end of the last interval (+inf: unbounded)         */
+    int32_t s_max;     /* output spike capacity per neuron                   */
+    double solver_reg; /* backward: floor on dV/dt at a spike (0: off)       */
+    double tie_band;   /* |V_max - V_th| below this marks a near-tie         */
+} or_params;
+
+/* ---------------------------------------------------------------------- */
+/* Closed-form sub-threshold solution (Appendix A, Eq. mem_pot and curr).  */
+/* ---------------------------------------------------------------------- */
+
+static double kappa(const or_params* p) { return p->tau_syn / (p->tau_mem - p->tau_syn); }
+
+/* V(t) from (V0, I0) after time t >= 0 (Eq. mem_pot). */
+static double v_at(const or_params* p, double V0, double I0, double t)
+{
+    if (isinf(t)) return 0.0;
+    double em = exp(-t / p->tau_mem), es = exp(-t / p->tau_syn);
+    return V0 * em + I0 * kappa(p) * (em - es);
+}
+
+/* I(t) from I0 after time t (Eq. curr). */
+static double i_at(const or_params* p, double I0, double t)
+{
+    if (isinf(t)) return 0.0;
+    return I0 * exp(-t / p->tau_syn);
+}
+
+/* dV/dt from the ODE itself (Eq. mem_dyn): tau_m dV/dt = -V + I. */
+static double dvdt(const or_params* p, double V, double I) { return (I - V) / p->tau_mem; }
+
+/* ---------------------------------------------------------------------- */
+/* Interval check (Sec. 3.2.2 rule; t_Vmax from Appendix D.1, Eq. t_vmax). */
+/* ---------------------------------------------------------------------- */
+
+typedef struct {
+    int crossing;    /* 1 if V reaches V_th inside (0, len]                 */
+    double hi;       /* right end of the root bracket: min(t_Vmax, len)     */
+    double vmax;     /* maximum of V over [0, len] (for the near-tie flag)  */
+} or_check;
+
+static or_check check_interval(const or_params* p, double V0, double I0, double len)
+{
+    or_check r = {0, len, V0};
+    double vend = v_at(p, V0, I0, len);
+    if (vend > r.vmax) r.vmax = vend;
+    /* Interior maximum: dV/dt = 0 has its root at Eq. t_vmax when the log
+     * argument I0 tm / (V0 (tm - ts) + I0 ts) exceeds 1. */
+    double D = V0 * (p->tau_mem - p->tau_syn) + I0 * p->tau_syn;
+    int has_max = (I0 > V0) && (D > 0.0);
+    double tv = INFINITY;
+    if (has_max) {
+        tv = (p->tau_mem * p->tau_syn / (p->tau_mem - p->tau_syn)) * log(I0 * p->tau_mem / D);
+        if (tv < len) {
+            double vv = v_at(p, V0, I0, tv);
+            if (vv > r.vmax) r.vmax = vv;
+        }
+    }
+    /* The literal rule: a spike if V(t_next) >= V_th, or if t_Vmax lies in the
+     * interval and V(t_Vmax) >= V_th. */
+    if (vend >= p->v_th) {
+        r.crossing = 1;
+        r.hi = has_max && tv < len ? tv : len;
+    } else if (has_max && tv < len && v_at(p, V0, I0, tv) >= p->v_th) {
+        r.crossing = 1;
+        r.hi = tv;
+    }
+    return r;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Spike-time root (Appendix D.1 Newton-Raphson, bracketed and clamped to   */
+/* the search interval; D.2 bisection as the fallback step).                */
+/* ---------------------------------------------------------------------- */
+
+/* Smallest float64 tau in (0, hi] with V(tau) >= V_th, where V(hi) >= V_th
+ * and V is increasing on [0, hi]. */
+static double solve_root(const or_params* p, double V0, double I0, double hi)
+{
+    const double hi0 = hi;
+    double lo = 0.0;
+    double t = 0.5 * hi;                      /* t0 = t_Vmax / 2 (App. D.1) */
+    for (int it = 0; it < 200; ++it) {
+        double v = v_at(p, V0, I0, t);
+        if (v >= p->v_th) hi = t; else lo = t;
+        double d = dvdt(p, v, i_at(p, I0, t));
+        double tn = (d > 0.0) ? t - (v - p->v_th) / d : 0.5 * (lo + hi);
+        if (!(tn > lo && tn < hi)) tn = 0.5 * (lo + hi);   /* clamp: bisect */
+        if (tn == t || hi - lo <= 2.0 * (nextafter(hi, INFINITY) - hi)) break;
+        t = tn;
+    }
+    /* Polish to the smallest float64 with V >= V_th: step up from the last
+     * iterate until the threshold is met, then down while it still is. */
+    double r = t;
+    for (int it = 0; it < 256 && r < hi0 && v_at(p, V0, I0, r) < p->v_th; ++it)
+        r = nextafter(r, INFINITY);
+    if (v_at(p, V0, I0, r) < p->v_th) r = hi;        /* bracket end satisfies it */
+    for (int it = 0; it < 256; ++it) {
+        double q = nextafter(r, 0.0);
+        if (q <= 0.0 || v_at(p, V0, I0, q) < p->v_th) break;
+        r = q;
+    }
+    return r;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Forward: one neuron, serial event loop with restart after each spike.    */
+/* ---------------------------------------------------------------------- */
+
+typedef struct {
+    int32_t n_spikes;
+    int32_t capped;
+    double tie_t;       /* start time of the first near-tie interval (+inf) */
+    double min_gap;     /* min over checked intervals of |V_max - V_th|     */
+} or_neuron_result;
+
+static or_neuron_result simulate_neuron(const or_params* p, const float* ev_t, const int32_t* ev_src,
+                                        int n, const float* WT, int N, int i,
+                                        double* st, double* si)
+{
+    or_neuron_result res = {0, 0, INFINITY, INFINITY};
+    double t_cur = 0.0, V = 0.0, I = 0.0;
+    int k = 0;
+    for (;;) {
+        double t_hi = (k < n) ? (double)ev_t[k] : p->t_end;
+        double len = t_hi - t_cur;
+        if (len > 0.0) {
+            or_check c = check_interval(p, V, I, len);
+            double gap = fabs(c.vmax - p->v_th);
+            if (gap < res.min_gap) res.min_gap = gap;
+            if (gap < p->tie_band && t_cur < res.tie_t) res.tie_t = t_cur;
+            if (c.crossing) {
+                double tau = solve_root(p, V, I, c.hi);
+                double Istar = i_at(p, I, tau);
+                st[res.n_spikes] = t_cur + tau;
+                si[res.n_spikes] = Istar;
+                res.n_spikes++;
+                if (res.n_spikes >= p->s_max) { res.capped = 1; return res; }
+                /* Hard reset of V only; the interval is tested again from t*. */
+                V = p->v_reset;
+                I = Istar;
+                t_cur = t_cur + tau;
+                continue;
+            }
+        }
+        if (k >= n) break;
+        /* Eq. affine: s_k = M(dt) s_{k-1} + (0, w). */
+        if (len > 0.0) {
+            double Vn = v_at(p, V, I, len);
+            I = i_at(p, I, len);
+            V = Vn;
+        }
+        I += (double)WT[(size_t)ev_src[k] * (size_t)N + (size_t)i];
+        t_cur = t_hi;
+        ++k;
+    }
+    return res;
+}
+
+/* Work split over (sample, neuron) items with plain pthreads. */
+typedef struct {
+    const or_params* p;
+    const float* ev_t; const int32_t* ev_src; const int32_t* ev_n;
+    int B, E_max; const float* WT; int C_in, N;
+    double* out_t; double* out_i; int32_t* out_n; int32_t* capped; double* tie_t; double* min_gap;
+    int tid, nthreads;
+} fwd_job;
+
+static void* fwd_worker(void* arg)
+{
+    fwd_job* j = (fwd_job*)arg;
+    size_t total = (size_t)j->B * (size_t)j->N;
+    for (size_t item = (size_t)j->tid; item < total; item += (size_t)j->nthreads) {
+        int b = (int)(item / (size_t)j->N), i = (int)(item % (size_t)j->N);
+        size_t o = item * (size_t)j->p->s_max;
+        for (int s = 0; s < j->p->s_max; ++s) { j->out_t[o + s] = INFINITY; j->out_i[o + s] = 0.0; }
+        or_neuron_result r = simulate_neuron(j->p, j->ev_t + (size_t)b * j->E_max,
+                                             j->ev_src + (size_t)b * j->E_max, j->ev_n[b],
+                                             j->WT, j->N, i, j->out_t + o, j->out_i + o);
+        j->out_n[item] = r.n_spikes;
+        j->capped[item] = r.capped;
+        j->tie_t[item] = r.tie_t;
+        j->min_gap[item] = r.min_gap;
+    }
+    return NULL;
+}
+
+static int run_threads(void* (*fn)(void*), void* jobs, size_t job_size, int nthreads)
+{
+    pthread_t* th = (pthread_t*)malloc(sizeof(pthread_t) * (size_t)nthreads);
+    if (!th) return -1;
+    for (int t = 0; t < nthreads; ++t)
+        pthread_create(&th[t], NULL, fn, (char*)jobs + (size_t)t * job_size);
+    for (int t = 0; t < nthreads; ++t) pthread_join(th[t], NULL);
+    free(th);
+    return 0;
+}
+
+/* Forward over a batch.  Outputs are [B][N][s_max] (times, I at spike; +inf
+ * and 0 padding), [B][N] counts, capped flags, first near-tie interval start
+ * and the smallest |V_max - V_th| seen. */
+int or_forward(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
+               const float* WT, int C_in, int N, const or_params* p, int nthreads,
+               double* out_t, double* out_i, int32_t* out_n, int32_t* capped,
+               double* tie_t, double* min_gap)
+{
+    if (!(p->tau_mem > p->tau_syn && p->tau_syn > 0.0) || !(p->v_reset < p->v_th) || p->s_max < 1)
+        return -1;
+    if (nthreads < 1) nthreads = 1;
+    fwd_job* jobs = (fwd_job*)calloc((size_t)nthreads, sizeof(fwd_job));
+    if (!jobs) return -2;
+    for (int t = 0; t < nthreads; ++t) {
+        fwd_job j = {p, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N,
+                     out_t, out_i, out_n, capped, tie_t, min_gap, t, nthreads};
+        jobs[t] = j;
+    }
+    int rc = run_threads(fwd_worker, jobs, sizeof(fwd_job), nthreads);
+    free(jobs);
+    return rc;
+}
+
+/* Membrane trace of one neuron right after every input event (no spikes
+ * beyond what the full forward finds); used by the closed-form pins.
+ * V_after[k], I_after[k] are the true (reset-including) state just after
+ * event k. */
+int or_trace(const float* ev_t, const int32_t* ev_src, int n, const float* WT, int N, int i,
+             const or_params* p, double* V_after, double* I_after)
+{
+    double t_cur = 0.0, V = 0.0, I = 0.0;
+    int k = 0, ns = 0;
+    for (;;) {
+        double t_hi = (k < n) ? (double)ev_t[k] : p->t_end;
+        double len = t_hi - t_cur;
+        if (len > 0.0 && ns < p->s_max) {
+            or_check c = check_interval(p, V, I, len);
+            if (c.crossing) {
+                double tau = solve_root(p, V, I, c.hi);
+                I = i_at(p, I, tau);
+                V = p->v_reset;
+                t_cur += tau;
+                ++ns;
+                continue;
+            }
+        }
+        if (k >= n) break;
+        if (len > 0.0) {
+            double Vn = v_at(p, V, I, len);
+            I = i_at(p, I, len);
+            V = Vn;
+        }
+        I += (double)WT[(size_t)ev_src[k] * (size_t)N + (size_t)i];
+        t_cur = t_hi;
+        V_after[k] = V;
+        I_after[k] = I;
+        ++k;
+    }
+    return ns;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Backward (Appendix D.3 implicit differentiation, chained through the     */
+/* hard resets).                                                            */
+/*                                                                          */
+/* With the resets written as subtractions, spike s satisfies              */
+/*   F_s = sum_{k: t_k < t_s} w_k K(t_s - t_k)                              */
+/*         - (V_th - V_reset) sum_{s' < s} exp(-(t_s - t_s')/tm) - V_th = 0 */
+/* with K(u) = kappa (exp(-u/tm) - exp(-u/ts)).  The implicit function      */
+/* theorem (Eq. ift_vjp) gives dt_s = -(dF_s/dt_s)^-1 dF_s, where           */
+/* dF_s/dt_s = dV/dt at the spike = (I(t_s) - V_th)/tm (Eq. mem_dyn),       */
+/* floored by the solver regularisation.  The adjoints are taken by a       */
+/* reverse pass over the spikes of each neuron, then every input event      */
+/* collects its weight and time gradients directly from the sums.           */
+/* ---------------------------------------------------------------------- */
+
+typedef struct {
+    const or_params* p;
+    const float* ev_t; const int32_t* ev_src; const int32_t* ev_n;
+    int B, E_max; const float* WT; int C_in, N;
+    const double* out_t; const double* out_i; const int32_t* out_n; const double* grad_out_t;
+    double* gW_part;   /* [nthreads][C_in][N] partial weight gradients       */
+    double* gT_part;   /* [nthreads][B][E_max] partial time gradients        */
+    int tid, nthreads;
+} bwd_job;
+
+static void* bwd_worker(void* arg)
+{
+    bwd_job* j = (bwd_job*)arg;
+    const or_params* p = j->p;
+    const double tm = p->tau_mem, ts = p->tau_syn, ka = kappa(p);
+    const int smax = p->s_max;
+    double* mu = (double*)malloc(sizeof(double) * (size_t)smax);
+    double* gW = j->gW_part + (size_t)j->tid * (size_t)j->C_in * (size_t)j->N;
+    double* gT = j->gT_part + (size_t)j->tid * (size_t)j->B * (size_t)j->E_max;
+    size_t total = (size_t)j->B * (size_t)j->N;
+    for (size_t item = (size_t)j->tid; item < total; item += (size_t)j->nthreads) {
+        int b = (int)(item / (size_t)j->N), i = (int)(item % (size_t)j->N);
+        int ns = j->out_n[item];
+        if (ns <= 0) continue;
+        const double* ts_ = j->out_t + item * (size_t)smax;
+        const double* is_ = j->out_i + item * (size_t)smax;
+        const double* g = j->grad_out_t + item * (size_t)smax;
+        /* Reverse pass over the spikes: lambda_s = dL/dt_s (total),
+         * mu_s = -lambda_s / V'_s is the multiplier of constraint F_s. */
+        for (int s = ns - 1; s >= 0; --s) {
+            double lam = g[s];
+            for (int s2 = s + 1; s2 < ns; ++s2)
+                lam -= (p->v_th - p->v_reset) / tm * mu[s2] * exp(-(ts_[s2] - ts_[s]) / tm);
+            double vp = dvdt(p, p->v_th, is_[s]);
+            if (vp < p->solver_reg) vp = p->solver_reg;
+            mu[s] = -lam / vp;
+        }
+        /* Each event before a spike: dF_s/dw_src = K(t_s - t_k),
+         * dF_s/dt_k = -w K'(t_s - t_k). */
+        const float* et = j->ev_t + (size_t)b * j->E_max;
+        const int32_t* es = j->ev_src + (size_t)b * j->E_max;
+        int n = j->ev_n[b];
+        for (int k = 0; k < n; ++k) {
+            double tk = (double)et[k];
+            if (!(tk < ts_[ns - 1])) break;
+            double a = 0.0, ad = 0.0;
+            for (int s = 0; s < ns; ++s) {
+                double u = ts_[s] - tk;
+                if (!(u > 0.0)) continue;
+                double em = exp(-u / tm), es2 = exp(-u / ts);
+                a += mu[s] * ka * (em - es2);
+                ad += mu[s] * ka * (-em / tm + es2 / ts);
+            }
+            double w = (double)j->WT[(size_t)es[k] * (size_t)j->N + (size_t)i];
+            gW[(size_t)es[k] * (size_t)j->N + (size_t)i] += a;
+            gT[(size_t)b * j->E_max + k] += -w * ad;
+        }
+    }
+    free(mu);
+    return NULL;
+}
+
+/* Backward over a batch: grad_WT [C_in][N] and grad_ev_t [B][E_max] are
+ * overwritten.  out_t/out_i/out_n are the oracle's own forward outputs. */
+int or_backward(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
+                const float* WT, int C_in, int N, const or_params* p, int nthreads,
+                const double* out_t, const double* out_i, const int32_t* out_n,
+                const double* grad_out_t, double* grad_WT, double* grad_ev_t)
+{
+    if (nthreads < 1) nthreads = 1;
+    size_t wsz = (size_t)C_in * (size_t)N, tsz = (size_t)B * (size_t)E_max;
+    double* gW_part = (double*)calloc(wsz * (size_t)nthreads, sizeof(double));
+    double* gT_part = (double*)calloc(tsz * (size_t)nthreads, sizeof(double));
+    bwd_job* jobs = (bwd_job*)calloc((size_t)nthreads, sizeof(bwd_job));
+    if (!gW_part || !gT_part || !jobs) { free(gW_part); free(gT_part); free(jobs); return -2; }
+    for (int t = 0; t < nthreads; ++t) {
+        bwd_job j = {p, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, out_t, out_i, out_n, grad_out_t,
+                     gW_part, gT_part, t, nthreads};
+        jobs[t] = j;
+    }
+    run_threads(bwd_worker, jobs, sizeof(bwd_job), nthreads);
+    for (size_t x = 0; x < wsz; ++x) {
+        double s = 0.0;
+        for (int t = 0; t < nthreads; ++t) s += gW_part[(size_t)t * wsz + x];
+        grad_WT[x] = s;
+    }
+    for (size_t x = 0; x < tsz; ++x) {
+        double s = 0.0;
+        for (int t = 0; t < nthreads; ++t) s += gT_part[(size_t)t * tsz + x];
+        grad_ev_t[x] = s;
+    }
+    free(gW_part); free(gT_part); free(jobs);
+    return 0;
+}
+
+/* Per-sample merge of a layer's output spikes into the next layer's sorted
+ * event queue (Appendix E.2): order by (time, neuron).  Times are the
+ * float32-rounded spike times that the next layer consumes. */
+int or_merge(const float* out_t, const int32_t* out_n, int B, int N, int s_max,
+             float* ev_t2, int32_t* ev_src2, int32_t* ev_n2, int32_t* perm, int E2_max)
+{
+    int rc = 0;
+    for (int b = 0; b < B; ++b) {
+        int cnt = 0;
+        for (int i = 0; i < N; ++i) cnt += out_n[(size_t)b * N + i];
+        if (cnt > E2_max) { rc = 1; cnt = E2_max; }
+        /* Selection of the (time, neuron)-smallest remaining head, one list
+         * pointer per neuron: a plain k-way merge. */
+        int* head = (int*)calloc((size_t)N, sizeof(int));
+        for (int e = 0; e < E2_max; ++e) {
+            size_t o = (size_t)b * E2_max + e;
+            ev_t2[o] = INFINITY; ev_src2[o] = 0; if (perm) perm[o] = -1;
+        }
+        for (int e = 0; e < cnt; ++e) {
+            int best = -1; float bt = INFINITY;
+            for (int i = 0; i < N; ++i) {
+                int h = head[i];
+                if (h >= out_n[(size_t)b * N + i]) continue;
+                float t = out_t[((size_t)b * N + i) * s_max + h];
+                if (best < 0 || t < bt) { best = i; bt = t; }
+            }
+            size_t o = (size_t)b * E2_max + e;
+            ev_t2[o] = bt; ev_src2[o] = best;
+            if (perm) perm[o] = best * s_max + head[best];
+            head[best]++;
+        }
+        ev_n2[b] = cnt;
+        free(head);
+    }
+    return rc;
+}
+
+/* Direct access to the interval rule and the root for the unit pins. */
+int or_check_interval(const or_params* p, double V0, double I0, double len, double* hi, double* vmax)
+{
+    or_check c = check_interval(p, V0, I0, len);
+    *hi = c.hi;
+    *vmax = c.vmax;
+    return c.crossing;
+}
+
+double or_solve_root(const or_params* p, double V0, double I0, double hi)
+{
+    return solve_root(p, V0, I0, hi);
+}
