@@ -1,0 +1,197 @@
+/*
+ * lif.h -- C ABI of the MI355X (gfx950) event-driven LIF layer library
+ * (liblif.so), after "Bullet Trains: Parallelizing Training of Temporally
+ * Precise Spiking Neural Networks" (arXiv 2603.13283).
+ *
+ * Conventions shared by every entry point
+ *   - Array arguments are DEVICE pointers unless stated otherwise; the caller
+ *     allocates and owns every buffer (outputs and workspace included).  The
+ *     library never allocates device memory, never synchronises the stream
+ *     and keeps no state between calls (except the optional kernel timer,
+ *     see lif_timer_*).
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL is the null stream)
+ *     and the call returns at once.  Calls on different streams with
+ *     distinct buffers may run concurrently.
+ *   - Argument errors are detected on the host before anything is launched;
+ *     the call then returns a negative LIF_ERR_* code and enqueues nothing.
+ *     Conditions that depend on the data (spike cap reached, unsorted input
+ *     under LIF_VALIDATE, merge overflow) are reported in the device status
+ *     words (int32[LIF_STATUS_WORDS]), which the call resets itself.
+ *     Malformed queues never make a kernel address outside its buffers:
+ *     event counts are clamped into [0, E_max] and sources into [0, C_in).
+ *   - Times are in seconds relative to the sample start t = 0, where every
+ *     neuron is at rest (V = I = 0).  Index layouts are row-major.
+ *   - Input events of one sample are sorted by time (ties in any order);
+ *     entries k >= ev_n[b] are padding and are never read as events.
+ *
+ * Model (paper Sec. 3.1, Appendix A): tau_m dV/dt = -V + I,
+ * tau_s dI/dt = -I; an input event from channel c adds w_{i c} to I of
+ * neuron i (Eq. spike_input, no delays); neuron i emits a spike when
+ * V >= V_th and V is then hard-reset to V_reset (I is not reset).
+ */
+#ifndef LIF_H
+#define LIF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Same type as hipStream_t. */
+typedef struct ihipStream_t* lif_stream_t;
+
+/* Return codes. */
+#define LIF_OK              0
+#define LIF_ERR_ARG        -1  /* null pointer, bad size, s_max < 1          */
+#define LIF_ERR_TAU        -2  /* require tau_mem > tau_syn > 0 (App. D.1)   */
+#define LIF_ERR_THRESHOLD  -3  /* require v_reset < v_th                     */
+#define LIF_ERR_WORKSPACE  -4  /* ws_bytes below the *_workspace_size value  */
+#define LIF_ERR_HIP        -5  /* a kernel launch failed                     */
+#define LIF_ERR_SIZE       -6  /* a size exceeds a documented limit          */
+
+/* lif_params.flags */
+#define LIF_VALIDATE  1u  /* check sorted times, finite values, source range */
+
+/* Device status words written by every forward call (int32 each). */
+#define LIF_STATUS_WORDS     8
+#define LIF_ST_FLAGS         0  /* OR of LIF_WARN_* bits                     */
+#define LIF_ST_CAPPED        1  /* neurons that reached s_max spikes         */
+#define LIF_ST_SPIKES        2  /* output spikes emitted                     */
+#define LIF_ST_CAND_BLOCKS   3  /* event sub-blocks flagged by the scan      */
+#define LIF_ST_WALKED_BLOCKS 4  /* sub-blocks re-walked exactly to resolve   */
+#define LIF_ST_ROOT_SOLVES   5  /* spike-time root solves                    */
+#define LIF_ST_EVENTS        6  /* input events consumed (sum of ev_n)       */
+
+#define LIF_WARN_SPIKE_CAP   1  /* a neuron stopped at s_max spikes          */
+#define LIF_WARN_UNSORTED    2  /* LIF_VALIDATE: times decrease in a sample  */
+#define LIF_WARN_BAD_SOURCE  4  /* LIF_VALIDATE: source outside [0, C_in)    */
+#define LIF_WARN_NONFINITE   8  /* LIF_VALIDATE: NaN/inf event time          */
+#define LIF_WARN_MERGE_FULL 16  /* merge: more spikes than E2_max            */
+#define LIF_WARN_BAD_COUNT  32  /* LIF_VALIDATE: ev_n[b] outside [0, E_max]  */
+
+typedef struct lif_params {
+    double   tau_mem;    /* tau_m (s); must exceed tau_syn (paper: 0.02)        */
+    double   tau_syn;    /* tau_s (s); > 0 (paper: 0.005)                       */
+    double   v_th;       /* threshold V_th (paper: 1.0)                         */
+    double   v_reset;    /* reset potential, < v_th (paper: 0.0)                */
+    double   t_end;      /* end of the interval after the last event; +INFINITY
+                            (events later than t_end are still consumed; the
+                            open interval is then empty)                        */
+    int32_t  s_max;      /* output spike capacity per neuron, >= 1 (App. E.2)   */
+    uint32_t flags;      /* LIF_VALIDATE                                        */
+    double   solver_reg; /* backward floor on dV/dt at a spike (paper 0.01,
+                            Table 4 "Solver Regularization"); 0 disables it     */
+} lif_params;
+
+/* Library version string (static storage). */
+const char* lif_version(void);
+
+/* --------------------------------------------------------------------- */
+/* Forward pass of one layer (paper Sec. 3.2.1 parallel scan of the affine  */
+/* event maps, Eq. affine and the Combine operator; Sec. 3.2.2 interval    */
+/* rule with t_Vmax of Eq. t_vmax; Appendix D.1 Newton spike-time solve;   */
+/* Appendix E.2 single commit + restart after each spike).                 */
+/*                                                                         */
+/*   ev_t   float [B][E_max]   event times, sorted per sample              */
+/*   ev_src int32 [B][E_max]   source channel of each event, in [0, C_in)  */
+/*   ev_n   int32 [B]          events per sample, 0 <= ev_n[b] <= E_max    */
+/*   WT     float [C_in][N_out] weights, WT[c*N_out + i] = w_{i c}         */
+/*   out_t  float [B][N_out][s_max] spike times in increasing order,       */
+/*                             +INFINITY after the last spike              */
+/*   out_n  int32 [B][N_out]   spike counts                                */
+/*   out_i  float [B][N_out][s_max] synaptic current I at each spike (the  */
+/*                             backward pass needs it); 0 padding; may be  */
+/*                             NULL                                        */
+/*   status int32 [LIF_STATUS_WORDS]                                       */
+/*   ws     device workspace of ws_bytes >= lif_layer_forward_workspace_size */
+/* The spike times are exact up to float64 rounding of the closed-form     */
+/* dynamics and are returned rounded to float32.                           */
+/* --------------------------------------------------------------------- */
+size_t lif_layer_forward_workspace_size(int B, int E_max, int C_in, int N_out, const lif_params* p);
+
+int lif_layer_forward(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
+                      const float* WT, int C_in, int N_out, const lif_params* p,
+                      float* out_t, int32_t* out_n, float* out_i, int32_t* status,
+                      void* ws, size_t ws_bytes, lif_stream_t stream);
+
+/* The sequential baseline (paper Appendix E.3): one GPU thread per
+ * (sample, neuron) consumes every event in order and runs the same interval
+ * rule and root solve.  Same arguments and results as lif_layer_forward;
+ * its workspace size is lif_layer_forward_workspace_size as well. */
+int lif_layer_forward_sequential(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B,
+                                 int E_max, const float* WT, int C_in, int N_out, const lif_params* p,
+                                 float* out_t, int32_t* out_n, float* out_i, int32_t* status,
+                                 void* ws, size_t ws_bytes, lif_stream_t stream);
+
+/* --------------------------------------------------------------------- */
+/* Backward pass (paper Appendix D.3, Eq. ift_vjp, chained through the     */
+/* hard resets): given dL/dt for every output spike, returns dL/dW and     */
+/* dL/d(event time).                                                       */
+/*                                                                         */
+/*   out_t, out_n, out_i  the forward results for the same inputs          */
+/*                        (out_i is required here)                         */
+/*   grad_out_t float [B][N_out][s_max]  dL/dt_s; padding entries ignored  */
+/*   grad_WT    float [C_in][N_out]      overwritten with dL/dWT           */
+/*   grad_ev_t  float [B][E_max]         overwritten with dL/dev_t (0 on   */
+/*                                       padding); may be NULL             */
+/* dV/dt at each spike is floored at p->solver_reg.  grad_WT sums over     */
+/* samples with float atomics, so its last bits depend on timing.          */
+/* --------------------------------------------------------------------- */
+size_t lif_layer_backward_workspace_size(int B, int E_max, int C_in, int N_out, const lif_params* p);
+
+int lif_layer_backward(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
+                       const float* WT, int C_in, int N_out, const lif_params* p,
+                       const float* out_t, const int32_t* out_n, const float* out_i,
+                       const float* grad_out_t, float* grad_WT, float* grad_ev_t,
+                       void* ws, size_t ws_bytes, lif_stream_t stream);
+
+/* --------------------------------------------------------------------- */
+/* Layer merge (paper Appendix E.2): the spikes of a layer become the next */
+/* layer's sorted per-sample event queue, ordered by (time, neuron).       */
+/*                                                                         */
+/*   out_t, out_n   a forward result, [B][N][s_max] and [B][N]             */
+/*   ev_t2   float [B][E2_max]  merged times (+INFINITY padding)           */
+/*   ev_src2 int32 [B][E2_max]  source = emitting neuron index             */
+/*   ev_n2   int32 [B]          merged counts (clipped at E2_max)          */
+/*   perm    int32 [B][E2_max]  i*s_max + s of each merged spike, -1 on    */
+/*                              padding; may be NULL                       */
+/*   status  int32 [LIF_STATUS_WORDS] (LIF_WARN_MERGE_FULL on overflow)    */
+/* Limit: E2_max <= LIF_MERGE_MAX (LIF_ERR_SIZE otherwise).                */
+/* --------------------------------------------------------------------- */
+#define LIF_MERGE_MAX 16384
+size_t lif_merge_workspace_size(int B, int N, int s_max, int E2_max);
+
+int lif_merge_spikes(const float* out_t, const int32_t* out_n, int B, int N, int s_max,
+                     float* ev_t2, int32_t* ev_src2, int32_t* ev_n2, int32_t* perm, int E2_max,
+                     int32_t* status, void* ws, size_t ws_bytes, lif_stream_t stream);
+
+/* --------------------------------------------------------------------- */
+/* First-spike readout loss: logits_c = -t_c / tau0 from the first spike   */
+/* time t_c of readout neuron c (t_silent when it never fires), mean       */
+/* softmax cross-entropy over the batch, and dL/dt written into the s = 0  */
+/* slot of grad_out_t (all other slots and silent neurons get 0).          */
+/*   labels int32 [B] in [0, N); loss float [1] (device)                   */
+/* --------------------------------------------------------------------- */
+int lif_first_spike_ce(const float* out_t, const int32_t* out_n, int B, int N, int s_max,
+                       const int32_t* labels, double tau0, double t_silent,
+                       float* loss, float* grad_out_t, lif_stream_t stream);
+
+/* --------------------------------------------------------------------- */
+/* Optional kernel timer (host-side state, off by default).  When enabled, */
+/* every kernel launched by this library is bracketed by HIP events on its */
+/* stream; lif_timer_read synchronises on the recorded events and returns  */
+/* per-kernel totals.                                                      */
+/*   lif_timer_enable(1) resets and starts recording, (0) stops.           */
+/*   lif_timer_read fills up to `cap` entries: names[j] (static strings),  */
+/*   total_ms[j], launches[j]; returns the number of kernels seen.         */
+/* --------------------------------------------------------------------- */
+void lif_timer_enable(int on);
+int lif_timer_read(const char** names, double* total_ms, int32_t* launches, int cap);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LIF_H */

@@ -1,0 +1,294 @@
+"""Python binding of liblif.so, the MI355X (gfx950) event-driven LIF layer.
+
+Argument marshalling only: every step of the forward and backward passes runs
+in the library's HIP kernels.  PyTorch supplies device memory and the current
+HIP stream.  The entry points carry the C names of ``include/lif.h``
+(``lif_layer_forward``, ``lif_layer_forward_sequential``,
+``lif_layer_backward``, ``lif_merge_spikes``, ``lif_first_spike_ce``, the
+workspace-size queries, ``lif_version``); ``forward``/``backward``/``merge``
+are conveniences that allocate outputs and workspace as torch tensors and
+call them.
+
+Importing this module does not touch the GPU.  Loading the library fails
+loudly (``LibraryMissing``) if ``liblif.so`` has not been built: there is no
+fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "liblif.so")
+
+LIF_OK = 0
+LIF_ERR_ARG = -1
+LIF_ERR_TAU = -2
+LIF_ERR_THRESHOLD = -3
+LIF_ERR_WORKSPACE = -4
+LIF_ERR_HIP = -5
+LIF_ERR_SIZE = -6
+ERR_NAMES = {LIF_ERR_ARG: "LIF_ERR_ARG", LIF_ERR_TAU: "LIF_ERR_TAU", LIF_ERR_THRESHOLD: "LIF_ERR_THRESHOLD",
+             LIF_ERR_WORKSPACE: "LIF_ERR_WORKSPACE", LIF_ERR_HIP: "LIF_ERR_HIP", LIF_ERR_SIZE: "LIF_ERR_SIZE"}
+
+LIF_VALIDATE = 1
+LIF_STATUS_WORDS = 8
+ST_FLAGS, ST_CAPPED, ST_SPIKES, ST_CAND_BLOCKS, ST_WALKED_BLOCKS, ST_ROOT_SOLVES, ST_EVENTS = range(7)
+WARN_SPIKE_CAP, WARN_UNSORTED, WARN_BAD_SOURCE, WARN_NONFINITE, WARN_MERGE_FULL, WARN_BAD_COUNT = 1, 2, 4, 8, 16, 32
+LIF_MERGE_MAX = 16384
+
+EXPORTED = ["lif_version", "lif_layer_forward_workspace_size", "lif_layer_forward",
+            "lif_layer_forward_sequential", "lif_layer_backward_workspace_size", "lif_layer_backward",
+            "lif_merge_workspace_size", "lif_merge_spikes", "lif_first_spike_ce", "lif_timer_enable",
+            "lif_timer_read"]
+
+
+class LibraryMissing(RuntimeError):
+    pass
+
+
+class LifError(RuntimeError):
+    def __init__(self, fn: str, code: int):
+        super().__init__(f"{fn} returned {ERR_NAMES.get(code, code)}")
+        self.code = code
+
+
+class lif_params(ctypes.Structure):
+    _fields_ = [("tau_mem", ctypes.c_double), ("tau_syn", ctypes.c_double), ("v_th", ctypes.c_double),
+                ("v_reset", ctypes.c_double), ("t_end", ctypes.c_double), ("s_max", ctypes.c_int32),
+                ("flags", ctypes.c_uint32), ("solver_reg", ctypes.c_double)]
+
+
+@dataclass
+class Params:
+    """Layer constants (defaults: paper Table 4, SHD/SSC columns)."""
+    tau_mem: float = 0.02
+    tau_syn: float = 0.005
+    v_th: float = 1.0
+    v_reset: float = 0.0
+    t_end: float = math.inf
+    s_max: int = 64
+    solver_reg: float = 0.01
+    validate: bool = False
+
+    def c(self) -> lif_params:
+        return lif_params(self.tau_mem, self.tau_syn, self.v_th, self.v_reset, self.t_end, int(self.s_max),
+                          LIF_VALIDATE if self.validate else 0, self.solver_reg)
+
+
+_lib = None
+_P = ctypes.c_void_p
+_I = ctypes.c_int
+_SZ = ctypes.c_size_t
+_PP = ctypes.POINTER(lif_params)
+
+
+def load(path: Optional[str] = None):
+    """Load liblif.so (raises LibraryMissing if it was not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = path or LIB_PATH
+    if not os.path.exists(path):
+        raise LibraryMissing(f"{path} not found: build it with `python -c 'import __graft_entry__ as g; g.build()'`")
+    lib = ctypes.CDLL(path)
+    lib.lif_version.restype = ctypes.c_char_p
+    lib.lif_version.argtypes = []
+    for name in ("lif_layer_forward_workspace_size", "lif_layer_backward_workspace_size"):
+        f = getattr(lib, name)
+        f.restype = _SZ
+        f.argtypes = [_I, _I, _I, _I, _PP]
+    fwd_args = [_P, _P, _P, _I, _I, _P, _I, _I, _PP, _P, _P, _P, _P, _P, _SZ, _P]
+    for name in ("lif_layer_forward", "lif_layer_forward_sequential"):
+        f = getattr(lib, name)
+        f.restype = _I
+        f.argtypes = fwd_args
+    lib.lif_layer_backward.restype = _I
+    lib.lif_layer_backward.argtypes = [_P, _P, _P, _I, _I, _P, _I, _I, _PP, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]
+    lib.lif_merge_workspace_size.restype = _SZ
+    lib.lif_merge_workspace_size.argtypes = [_I, _I, _I, _I]
+    lib.lif_merge_spikes.restype = _I
+    lib.lif_merge_spikes.argtypes = [_P, _P, _I, _I, _I, _P, _P, _P, _P, _I, _P, _P, _SZ, _P]
+    lib.lif_first_spike_ce.restype = _I
+    lib.lif_first_spike_ce.argtypes = [_P, _P, _I, _I, _I, _P, ctypes.c_double, ctypes.c_double, _P, _P, _P]
+    lib.lif_timer_enable.restype = None
+    lib.lif_timer_enable.argtypes = [_I]
+    lib.lif_timer_read.restype = _I
+    lib.lif_timer_read.argtypes = [ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_double),
+                                   ctypes.POINTER(ctypes.c_int32), _I]
+    _lib = lib
+    return lib
+
+
+# ---------------------------------------------------------------------------
+# C entry points under their own names (raw pointers / ints)
+# ---------------------------------------------------------------------------
+
+def lif_version() -> str:
+    return load().lif_version().decode()
+
+
+def lif_layer_forward_workspace_size(B, E_max, C_in, N_out, p: lif_params) -> int:
+    return int(load().lif_layer_forward_workspace_size(B, E_max, C_in, N_out, ctypes.byref(p)))
+
+
+def lif_layer_backward_workspace_size(B, E_max, C_in, N_out, p: lif_params) -> int:
+    return int(load().lif_layer_backward_workspace_size(B, E_max, C_in, N_out, ctypes.byref(p)))
+
+
+def lif_merge_workspace_size(B, N, s_max, E2_max) -> int:
+    return int(load().lif_merge_workspace_size(B, N, s_max, E2_max))
+
+
+def lif_layer_forward(*args) -> int:
+    return load().lif_layer_forward(*args)
+
+
+def lif_layer_forward_sequential(*args) -> int:
+    return load().lif_layer_forward_sequential(*args)
+
+
+def lif_layer_backward(*args) -> int:
+    return load().lif_layer_backward(*args)
+
+
+def lif_merge_spikes(*args) -> int:
+    return load().lif_merge_spikes(*args)
+
+
+def lif_first_spike_ce(*args) -> int:
+    return load().lif_first_spike_ce(*args)
+
+
+def lif_timer_enable(on: bool) -> None:
+    load().lif_timer_enable(1 if on else 0)
+
+
+def lif_timer_read(cap: int = 32):
+    names = (ctypes.c_char_p * cap)()
+    ms = (ctypes.c_double * cap)()
+    cnt = (ctypes.c_int32 * cap)()
+    n = load().lif_timer_read(names, ms, cnt, cap)
+    return {names[j].decode(): (ms[j], cnt[j]) for j in range(min(n, cap))}
+
+
+# ---------------------------------------------------------------------------
+# torch conveniences
+# ---------------------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> int:
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _check(fn: str, rc: int):
+    if rc != LIF_OK:
+        raise LifError(fn, rc)
+
+
+def _dev_inputs(ev_t, ev_src, ev_n, WT):
+    torch = _torch()
+    for name, t, dt in (("ev_t", ev_t, torch.float32), ("ev_src", ev_src, torch.int32),
+                        ("ev_n", ev_n, torch.int32), ("WT", WT, torch.float32)):
+        if t.dtype != dt or not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous {dt} CUDA tensor")
+    if ev_t.dim() != 2 or ev_src.shape != ev_t.shape or ev_n.dim() != 1 or ev_n.shape[0] != ev_t.shape[0]:
+        raise ValueError("ev_t/ev_src must be [B, E_max] and ev_n [B]")
+    if WT.dim() != 2:
+        raise ValueError("WT must be [C_in, N_out]")
+    return ev_t.shape[0], ev_t.shape[1], WT.shape[0], WT.shape[1]
+
+
+@dataclass
+class ForwardOut:
+    out_t: "object"     # float32 [B, N, s_max]
+    out_n: "object"     # int32 [B, N]
+    out_i: "object"     # float32 [B, N, s_max]
+    status: "object"    # int32 [LIF_STATUS_WORDS]
+
+
+def forward(ev_t, ev_src, ev_n, WT, params: Params = Params(), sequential: bool = False, stream=None,
+            ws=None, out: Optional[ForwardOut] = None) -> ForwardOut:
+    """Run lif_layer_forward (or the sequential baseline) on device tensors."""
+    torch = _torch()
+    B, E, C, N = _dev_inputs(ev_t, ev_src, ev_n, WT)
+    p = params.c()
+    dev = ev_t.device
+    if out is None:
+        out = ForwardOut(torch.empty((B, N, params.s_max), dtype=torch.float32, device=dev),
+                         torch.empty((B, N), dtype=torch.int32, device=dev),
+                         torch.empty((B, N, params.s_max), dtype=torch.float32, device=dev),
+                         torch.empty(LIF_STATUS_WORDS, dtype=torch.int32, device=dev))
+    need = lif_layer_forward_workspace_size(B, E, C, N, p)
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    fn = lif_layer_forward_sequential if sequential else lif_layer_forward
+    rc = fn(_ptr(ev_t), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(WT), C, N, ctypes.byref(p), _ptr(out.out_t),
+            _ptr(out.out_n), _ptr(out.out_i), _ptr(out.status), _ptr(ws), ws.numel(), _stream(stream))
+    _check(fn.__name__, rc)
+    return out
+
+
+def backward(ev_t, ev_src, ev_n, WT, fwd: ForwardOut, grad_out_t, params: Params = Params(), stream=None,
+             want_time_grad: bool = True, ws=None):
+    """Run lif_layer_backward; returns (grad_WT, grad_ev_t or None)."""
+    torch = _torch()
+    B, E, C, N = _dev_inputs(ev_t, ev_src, ev_n, WT)
+    p = params.c()
+    dev = ev_t.device
+    gW = torch.empty((C, N), dtype=torch.float32, device=dev)
+    gT = torch.empty((B, E), dtype=torch.float32, device=dev) if want_time_grad else None
+    need = lif_layer_backward_workspace_size(B, E, C, N, p)
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    g = grad_out_t.contiguous().to(torch.float32)
+    rc = lif_layer_backward(_ptr(ev_t), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(WT), C, N, ctypes.byref(p),
+                            _ptr(fwd.out_t), _ptr(fwd.out_n), _ptr(fwd.out_i), _ptr(g), _ptr(gW), _ptr(gT),
+                            _ptr(ws), ws.numel(), _stream(stream))
+    _check("lif_layer_backward", rc)
+    return gW, gT
+
+
+def merge(fwd: ForwardOut, E2_max: int, stream=None):
+    """Run lif_merge_spikes; returns (ev_t2, ev_src2, ev_n2, perm, status)."""
+    torch = _torch()
+    B, N, S = fwd.out_t.shape
+    dev = fwd.out_t.device
+    ev_t2 = torch.empty((B, E2_max), dtype=torch.float32, device=dev)
+    ev_src2 = torch.empty((B, E2_max), dtype=torch.int32, device=dev)
+    ev_n2 = torch.empty(B, dtype=torch.int32, device=dev)
+    perm = torch.empty((B, E2_max), dtype=torch.int32, device=dev)
+    status = torch.empty(LIF_STATUS_WORDS, dtype=torch.int32, device=dev)
+    need = lif_merge_workspace_size(B, N, S, E2_max)
+    ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    rc = lif_merge_spikes(_ptr(fwd.out_t), _ptr(fwd.out_n), B, N, S, _ptr(ev_t2), _ptr(ev_src2), _ptr(ev_n2),
+                          _ptr(perm), E2_max, _ptr(status), _ptr(ws), ws.numel(), _stream(stream))
+    _check("lif_merge_spikes", rc)
+    return ev_t2, ev_src2, ev_n2, perm, status
+
+
+def first_spike_ce(fwd: ForwardOut, labels, tau0: float, t_silent: float, stream=None):
+    """Run lif_first_spike_ce; returns (loss [1], grad_out_t [B, N, s_max])."""
+    torch = _torch()
+    B, N, S = fwd.out_t.shape
+    dev = fwd.out_t.device
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    g = torch.empty((B, N, S), dtype=torch.float32, device=dev)
+    lab = labels.to(device=dev, dtype=torch.int32).contiguous()
+    rc = lif_first_spike_ce(_ptr(fwd.out_t), _ptr(fwd.out_n), B, N, S, _ptr(lab), float(tau0), float(t_silent),
+                            _ptr(loss), _ptr(g), _stream(stream))
+    _check("lif_first_spike_ce", rc)
+    return loss, g

@@ -1,0 +1,103 @@
+"""Host-side checks of the C ABI (no GPU needed): every symbol declared in
+include/lif.h is exported by liblif.so, and argument errors are rejected on
+the host before any launch."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2603_13283_amd as L
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+F = ctypes.c_void_p(0x1000)      # never dereferenced: validation fails first
+
+
+def declared_symbols():
+    txt = open(os.path.join(ROOT, "include", "lif.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(lif_[a-z_]+)\s*\(", txt)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return L.load()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_symbols()
+    assert len(names) >= 10
+    for name in names:
+        assert hasattr(lib, name), name
+    assert set(names) == set(L.EXPORTED)
+
+
+def test_version_and_workspace_sizes(lib):
+    assert "gfx950" in L.lif_version()
+    p = L.Params().c()
+    small = L.lif_layer_forward_workspace_size(1, 10, 4, 8, p)
+    big = L.lif_layer_forward_workspace_size(32, 5200, 700, 256, p)
+    assert 0 < small < big < 2 ** 31
+    assert L.lif_layer_forward_workspace_size(-1, 10, 4, 8, p) == 0
+    assert L.lif_layer_backward_workspace_size(4, 100, 10, 20, p) > 0
+    assert L.lif_merge_workspace_size(4, 20, 8, 100) > 0
+
+
+def _fwd(fn, p, B=2, E=10, C=4, N=8, ws_bytes=10 ** 9, null=None):
+    args = [F, F, F, B, E, F, C, N, ctypes.byref(p), F, F, F, F, F, ws_bytes, None]
+    if null is not None:
+        args[null] = None
+    return fn(*args)
+
+
+@pytest.mark.parametrize("fn", [L.lif_layer_forward, L.lif_layer_forward_sequential])
+def test_forward_argument_errors(lib, fn):
+    assert _fwd(fn, L.Params(tau_mem=0.005, tau_syn=0.005).c()) == L.LIF_ERR_TAU
+    assert _fwd(fn, L.Params(tau_mem=0.005, tau_syn=0.01).c()) == L.LIF_ERR_TAU
+    assert _fwd(fn, L.Params(tau_syn=0.0).c()) == L.LIF_ERR_TAU
+    assert _fwd(fn, L.Params(v_th=0.0, v_reset=0.0).c()) == L.LIF_ERR_THRESHOLD
+    assert _fwd(fn, L.Params(v_th=1.0, v_reset=2.0).c()) == L.LIF_ERR_THRESHOLD
+    assert _fwd(fn, L.Params(s_max=0).c()) == L.LIF_ERR_ARG
+    assert _fwd(fn, L.Params(t_end=math.nan).c()) == L.LIF_ERR_ARG
+    assert _fwd(fn, L.Params(solver_reg=-1.0).c()) == L.LIF_ERR_ARG
+    p = L.Params().c()
+    assert _fwd(fn, p, B=-1) == L.LIF_ERR_ARG
+    assert _fwd(fn, p, N=0) == L.LIF_ERR_ARG
+    assert _fwd(fn, p, C=0) == L.LIF_ERR_ARG
+    for null in (0, 1, 2, 5, 9, 10, 12, 13):       # ev_t, ev_src, ev_n, WT, out_t, out_n, status, ws
+        assert _fwd(fn, p, null=null) == L.LIF_ERR_ARG, null
+    assert _fwd(fn, p, ws_bytes=10) == L.LIF_ERR_WORKSPACE
+    assert fn(F, F, F, 2, 10, F, 4, 8, None, F, F, F, F, F, 10 ** 9, None) == L.LIF_ERR_ARG
+
+
+def test_backward_and_merge_argument_errors(lib):
+    p = L.Params().c()
+    base = [F, F, F, 2, 10, F, 4, 8, ctypes.byref(p), F, F, F, F, F, F, F, 10 ** 9, None]
+    assert L.lif_layer_backward(*base[:11], None, *base[12:]) == L.LIF_ERR_ARG      # out_i required
+    bad = L.Params(tau_mem=0.001).c()
+    assert L.lif_layer_backward(*base[:8], ctypes.byref(bad), *base[9:]) == L.LIF_ERR_TAU
+    small = list(base)
+    small[16] = 10
+    assert L.lif_layer_backward(*small) == L.LIF_ERR_WORKSPACE
+    margs = [F, F, 2, 8, 4, F, F, F, F, 100, F, F, 10 ** 6, None]
+    m2 = list(margs)
+    m2[9] = L.LIF_MERGE_MAX + 1
+    assert L.lif_merge_spikes(*m2) == L.LIF_ERR_SIZE
+    m3 = list(margs)
+    m3[9] = 0
+    assert L.lif_merge_spikes(*m3) == L.LIF_ERR_ARG
+    assert L.lif_first_spike_ce(F, F, 0, 20, 4, F, 0.02, 1.0, F, F, None) == L.LIF_ERR_ARG
+    assert L.lif_first_spike_ce(F, F, 2, 20, 4, F, 0.0, 1.0, F, F, None) == L.LIF_ERR_ARG
+
+
+def test_library_missing_fails_loudly(tmp_path):
+    import importlib
+    mod = importlib.import_module("paper_2603_13283_amd")
+    saved = mod._lib
+    try:
+        mod._lib = None
+        with pytest.raises(mod.LibraryMissing):
+            mod.load(str(tmp_path / "nope.so"))
+    finally:
+        mod._lib = saved

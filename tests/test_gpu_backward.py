@@ -1,0 +1,130 @@
+"""GPU backward, merge and readout-loss parity against the float64 oracle."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+import copy
+
+from tests.parity import E2E_ELEM_RTOL, compare_grad, compare_spikes
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def env():
+    import torch
+    import paper_2603_13283_amd as lif
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    lif.load()
+    return torch, lif
+
+
+def _dev(torch, a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda:0")
+
+
+def _fwd_bwd(env, ev, WT, seed, s_max=64, reg=0.01, **kw):
+    torch, lif = env
+    P = lif.Params(s_max=s_max, solver_reg=reg, **kw)
+    OP = oracle.LifParams(s_max=s_max, solver_reg=reg, **kw)
+    d = [_dev(torch, a) for a in (ev.ev_t, ev.ev_src, ev.ev_n, WT)]
+    out = lif.forward(*d, P)
+    ref = oracle.forward(ev.ev_t, ev.ev_src, ev.ev_n, WT, OP)
+    torch.cuda.synchronize()
+    compare_spikes(out.out_t.cpu().numpy(), out.out_n.cpu().numpy(), ref)
+    rng = np.random.default_rng(seed)
+    valid = np.isfinite(ref.out_t)
+    g = (rng.standard_normal(ref.out_t.shape) * valid).astype(np.float32)
+    gW, gT = lif.backward(*d, out, _dev(torch, g), P)
+    torch.cuda.synchronize()
+    oW, oT = oracle.backward(ev.ev_t, ev.ev_src, ev.ev_n, WT, ref, g.astype(np.float64), OP)
+    # neurons with a flagged near-tie are excluded from the comparison
+    okN = ~np.isfinite(ref.tie_t).any(axis=0)
+    okB = ~np.isfinite(ref.tie_t).any(axis=1)
+    rW = compare_grad(gW.cpu().numpy()[:, okN], oW[:, okN], label="grad_WT", elem_rtol=E2E_ELEM_RTOL)
+    rT = compare_grad(gT.cpu().numpy()[okB], oT[okB], label="grad_ev_t", elem_rtol=E2E_ELEM_RTOL)
+    # The backward kernels alone, on identical inputs: the oracle's spikes
+    # rounded to float32 go to both sides.
+    r32 = copy.deepcopy(ref)
+    r32.out_t = ref.out_t.astype(np.float32).astype(np.float64)
+    r32.out_i = ref.out_i.astype(np.float32).astype(np.float64)
+    fwd32 = lif.ForwardOut(_dev(torch, ref.out_t.astype(np.float32)), _dev(torch, ref.out_n),
+                           _dev(torch, ref.out_i.astype(np.float32)), None)
+    hW, hT = lif.backward(*d, fwd32, _dev(torch, g), P)
+    torch.cuda.synchronize()
+    qW, qT = oracle.backward(ev.ev_t, ev.ev_src, ev.ev_n, WT, r32, g.astype(np.float64), OP)
+    sW = compare_grad(hW.cpu().numpy(), qW, label="grad_WT (same inputs)")
+    sT = compare_grad(hT.cpu().numpy(), qT, label="grad_ev_t (same inputs)")
+    print(f"[case] spikes={int(ref.out_n.sum())} e2e rel(gW)={rW:.2e} rel(gT)={rT:.2e}; "
+          f"same-input rel(gW)={sW:.2e} rel(gT)={sT:.2e}", flush=True)
+    return gW, gT, oW, oT
+
+
+@pytest.mark.parametrize("seed,N", [(21, 64), (22, 90), (23, 20)])
+def test_backward_small(env, seed, N):
+    cfg = W.random_small(seed, B=4, C=25, N=N, n_events=600, T=0.4, gain=14.0)
+    _fwd_bwd(env, cfg.events, cfg.layers[0].WT, seed)
+
+
+def test_backward_no_regularisation_and_reset(env):
+    cfg = W.random_small(24, B=3, C=25, N=70, n_events=500, T=0.4, gain=14.0)
+    _fwd_bwd(env, cfg.events, cfg.layers[0].WT, 24, reg=0.0, v_reset=-0.2)
+
+
+def test_backward_config2_driven(env):
+    cfg = W.config2(B=4)
+    _fwd_bwd(env, cfg.events, cfg.layers[0].WT, 25, v_th=0.5)
+
+
+def test_backward_silent_layer_is_zero(env):
+    torch, lif = env
+    cfg = W.config1()
+    _, _, oW, oT = _fwd_bwd(env, cfg.events, cfg.layers[0].WT, 26)
+    assert np.all(oW == 0) and np.all(oT == 0)
+
+
+def test_merge_bit_exact(env):
+    torch, lif = env
+    cfg = W.random_small(27, B=5, C=25, N=150, n_events=600, T=0.4, gain=14.0)
+    ev, WT = cfg.events, cfg.layers[0].WT
+    d = [_dev(torch, a) for a in (ev.ev_t, ev.ev_src, ev.ev_n, WT)]
+    out = lif.forward(*d, lif.Params(s_max=16))
+    torch.cuda.synchronize()
+    t32 = out.out_t.cpu().numpy()
+    n = out.out_n.cpu().numpy()
+    E2 = int(n.sum(1).max()) + 5
+    t2, s2, n2, perm, st = lif.merge(out, E2)
+    torch.cuda.synchronize()
+    rt, rs, rn, rp, ovf = oracle.merge(t32, n, E2)
+    assert not ovf and st.cpu().numpy()[0] == 0
+    assert np.array_equal(n2.cpu().numpy(), rn)
+    assert np.array_equal(t2.cpu().numpy(), rt)
+    assert np.array_equal(s2.cpu().numpy(), rs)
+    assert np.array_equal(perm.cpu().numpy(), rp)
+    # overflow: keep the E2 smallest and flag it
+    t2, s2, n2, perm, st = lif.merge(out, 3)
+    torch.cuda.synchronize()
+    rt, rs, rn, rp, ovf = oracle.merge(t32, n, 3)
+    assert ovf and st.cpu().numpy()[0] & lif.WARN_MERGE_FULL
+    assert np.array_equal(t2.cpu().numpy(), rt) and np.array_equal(s2.cpu().numpy(), rs)
+
+
+def test_first_spike_ce(env):
+    torch, lif = env
+    rng = np.random.default_rng(28)
+    B, N, S = 7, 20, 4
+    n = rng.integers(0, 3, (B, N)).astype(np.int32)
+    t = np.full((B, N, S), np.inf, np.float32)
+    for b in range(B):
+        for i in range(N):
+            t[b, i, : n[b, i]] = np.sort(rng.uniform(0.01, 0.3, n[b, i]))
+    y = rng.integers(0, N, B)
+    fwd = lif.ForwardOut(_dev(torch, t), _dev(torch, n), None, None)
+    loss, g = lif.first_spike_ce(fwd, torch.from_numpy(y), 0.02, 1.0)
+    torch.cuda.synchronize()
+    rl, rg = oracle.first_spike_ce(t[:, :, 0], n > 0, y, 0.02, 1.0)
+    assert abs(loss.item() - rl) <= 1e-5 * abs(rl)
+    gg = g.cpu().numpy()
+    assert np.allclose(gg[:, :, 0], rg, rtol=1e-5, atol=1e-6)
+    assert np.all(gg[:, :, 1:] == 0)

@@ -1,0 +1,154 @@
+"""GPU forward parity: liblif.so (through the C ABI) against the float64
+oracle on identical seeded float32 inputs."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from tests.parity import compare_spikes
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def env():
+    import torch
+    import paper_2603_13283_amd as lif
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    lif.load()
+    return torch, lif
+
+
+def _dev(torch, a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda:0")
+
+
+def run_both(env, ev, WT, s_max=64, sequential=False, **kw):
+    torch, lif = env
+    P = lif.Params(s_max=s_max, **kw)
+    OP = oracle.LifParams(s_max=s_max, **{k: v for k, v in kw.items() if k != "validate"})
+    out = lif.forward(_dev(torch, ev.ev_t), _dev(torch, ev.ev_src), _dev(torch, ev.ev_n), _dev(torch, WT), P,
+                      sequential=sequential)
+    torch.cuda.synchronize()
+    ref = oracle.forward(ev.ev_t, ev.ev_src, ev.ev_n, WT, OP)
+    return out, ref
+
+
+def check(env, ev, WT, label, s_max=64, both=True, **kw):
+    print(f"[case] {label} B={ev.B} E_max={ev.E_max} C={WT.shape[0]} N={WT.shape[1]}", flush=True)
+    stats = {}
+    for seq in ((False, True) if both else (False,)):
+        out, ref = run_both(env, ev, WT, s_max=s_max, sequential=seq, **kw)
+        st = out.status.cpu().numpy()
+        s = compare_spikes(out.out_t.cpu().numpy(), out.out_n.cpu().numpy(), ref, out.out_i.cpu().numpy(),
+                           label=f"{label}{' seq' if seq else ''}")
+        assert st[2] == out.out_n.cpu().numpy().sum()
+        assert st[6] == int(ev.ev_n.sum())
+        assert st[1] == int(ref.capped.sum())
+        s["status"] = st.tolist()
+        stats["seq" if seq else "par"] = s
+    print(f"    {stats}", flush=True)
+    return stats
+
+
+def test_config1_silent_and_driven(env):
+    cfg = W.config1()
+    s = check(env, cfg.events, cfg.layers[0].WT, "c1")
+    assert s["par"]["spikes"] == 0
+    cfgd = W.config1(gain=30.0)
+    s = check(env, cfgd.events, cfgd.layers[0].WT, "c1x10")
+    assert s["par"]["spikes"] > 100
+
+
+@pytest.mark.parametrize("seed,N", [(1, 64), (2, 70), (3, 20), (4, 200)])
+def test_small_ragged(env, seed, N):
+    cfg = W.random_small(seed, B=5, C=30, N=N, n_events=700, T=0.5, gain=14.0)
+    assert (cfg.events.ev_n == 0).any() or cfg.events.ev_n.min() < cfg.events.E_max
+    s = check(env, cfg.events, cfg.layers[0].WT, f"small{seed}")
+    assert s["par"]["spikes"] > 20
+
+
+def test_empty_inputs(env):
+    ev = W.pack_events([np.array([]), np.array([])], [np.array([], int), np.array([], int)], e_max=3)
+    WT = np.ones((4, 5), np.float32)
+    s = check(env, ev, WT, "empty")
+    assert s["par"]["spikes"] == 0
+    ev1 = W.pack_events([np.array([0.1])], [np.array([2])])
+    WT1 = np.full((4, 3), 50.0, np.float32)
+    s = check(env, ev1, WT1, "one-event")
+    assert s["par"]["spikes"] > 3
+
+
+def test_equal_times_and_exact_boundaries(env):
+    rng = np.random.default_rng(5)
+    t = np.sort(np.repeat(rng.random(150) * 0.2, 3))            # every time three times
+    src = rng.integers(0, 12, t.size)
+    ev = W.pack_events([t], [src])
+    WT = (rng.standard_normal((12, 66)) * 3.0).astype(np.float32)
+    s = check(env, ev, WT, "dup-times")
+    assert s["par"]["spikes"] > 10
+
+
+def test_reset_nonzero_threshold_and_t_end(env):
+    cfg = W.random_small(6, B=3, C=30, N=100, n_events=500, T=0.4, gain=14.0)
+    check(env, cfg.events, cfg.layers[0].WT, "vr", v_reset=-0.25)
+    check(env, cfg.events, cfg.layers[0].WT, "th0.5", v_th=0.5)
+    check(env, cfg.events, cfg.layers[0].WT, "tend", t_end=0.3)
+    check(env, cfg.events, cfg.layers[0].WT, "taus", tau_mem=0.03, tau_syn=0.002)
+
+
+def test_spike_cap(env):
+    cfg = W.random_small(7, B=3, C=30, N=100, n_events=500, T=0.4, gain=20.0)
+    s = check(env, cfg.events, cfg.layers[0].WT, "cap1", s_max=1)
+    assert s["par"]["status"][1] > 0 and s["par"]["status"][0] & 1
+    check(env, cfg.events, cfg.layers[0].WT, "cap3", s_max=3)
+
+
+def test_config2_full(env):
+    cfg = W.config2()
+    s = check(env, cfg.events, cfg.layers[0].WT, "c2")
+    assert s["par"]["spikes"] > 100
+    assert s["par"]["status"][1] == 0              # the cap never binds
+
+
+def test_config2_driven(env):
+    cfg = W.config2(B=8)
+    s = check(env, cfg.events, cfg.layers[0].WT, "c2-th0.5", v_th=0.5)
+    assert s["par"]["spikes"] > 1000
+
+
+def test_config4_bursts_sampled(env):
+    cfg = W.config4(B=4)
+    WT = cfg.layers[0].WT[:, :192]
+    s = check(env, cfg.events, WT, "c4", both=False)
+    assert s["par"]["spikes"] > 100
+
+
+def test_config3_layer1_sampled(env):
+    cfg = W.config3(B=6)
+    check(env, cfg.events, cfg.layers[0].WT, "c3-l1", both=False)
+
+
+def test_determinism(env):
+    torch, lif = env
+    cfg = W.random_small(8, B=4, C=30, N=130, n_events=900, T=0.5, gain=14.0)
+    ev, WT = cfg.events, cfg.layers[0].WT
+    a = lif.forward(_dev(torch, ev.ev_t), _dev(torch, ev.ev_src), _dev(torch, ev.ev_n), _dev(torch, WT))
+    b = lif.forward(_dev(torch, ev.ev_t), _dev(torch, ev.ev_src), _dev(torch, ev.ev_n), _dev(torch, WT))
+    torch.cuda.synchronize()
+    assert torch.equal(a.out_t, b.out_t) and torch.equal(a.out_n, b.out_n) and torch.equal(a.out_i, b.out_i)
+
+
+def test_validation_flags(env):
+    torch, lif = env
+    ev = W.pack_events([np.array([0.1, 0.2, 0.3])], [np.array([0, 1, 2])])
+    ev.ev_t[0, 1] = 0.5                      # unsorted
+    ev.ev_src[0, 2] = 9                      # out of range for C_in = 4
+    WT = np.ones((4, 8), np.float32)
+    out = lif.forward(_dev(torch, ev.ev_t), _dev(torch, ev.ev_src), _dev(torch, ev.ev_n),
+                      _dev(torch, WT), lif.Params(validate=True))
+    torch.cuda.synchronize()
+    st = out.status.cpu().numpy()
+    assert st[0] & lif.WARN_UNSORTED and st[0] & lif.WARN_BAD_SOURCE
