@@ -1,0 +1,182 @@
+"""Benchmark of the event-driven LIF layer forward pass on one MI355X.
+
+Workload: one LIF layer, 700 input channels -> 256 neurons, batch 32, 1 s per
+sample, lognormal-rate Poisson input channels (~5k events per sample),
+W ~ N(0,1) * 4/sqrt(700), tau_m = 20 ms, tau_s = 5 ms, threshold 1, hard
+reset to 0 (synthetic, seeded).  A step is one forward pass of the layer
+(decays, weight gather, segment scan, interval checks, root solves, resets,
+outputs) over the batch, with all inputs resident in HBM.
+
+Prints one JSON line: throughput in neuron-events/s (N_out * sum of events
+per sample, per second), the roofline of the dominant kernel, the speedup
+over the sequential one-thread-per-neuron GPU event loop, the backward time,
+and the float64 CPU oracle timed on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0     # MI355X HBM3E, GB/s
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--seq-steps", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-repeats", type=int, default=3)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the layer shards over samples "
+              "with no exchange in the forward pass, and multi-GPU runs are not part of this build.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2603_13283_amd as lif
+    import workloads as W
+
+    dev = torch.device("cuda:0")
+    cfg = W.config2()
+    ev, WT = cfg.events, cfg.layers[0].WT
+    B, E = ev.ev_t.shape
+    C, N = WT.shape
+    total_ev = int(ev.ev_n.sum())
+    neuron_events = N * total_ev
+    P = lif.Params(s_max=64)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    d_t, d_s, d_n, d_W = t(ev.ev_t), t(ev.ev_src), t(ev.ev_n), t(WT)
+    pc = P.c()
+    ws = torch.empty(lif.lif_layer_forward_workspace_size(B, E, C, N, pc), dtype=torch.uint8, device=dev)
+    out = lif.forward(d_t, d_s, d_n, d_W, P, ws=ws)
+    torch.cuda.synchronize()
+    log(f"[bench] {cfg.name}: B={B} E_max={E} events={total_ev} N={N} neuron-events={neuron_events} "
+        f"lib={lif.lif_version()}")
+
+    # ---- warmup (also fills the kernel timer's event pool)
+    lif.lif_timer_enable(True)
+    for _ in range(args.warmup):
+        lif.forward(d_t, d_s, d_n, d_W, P, ws=ws, out=out)
+    torch.cuda.synchronize()
+
+    # ---- timed forward steps, kernel timer live on the same stream
+    lif.lif_timer_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        lif.forward(d_t, d_s, d_n, d_W, P, ws=ws, out=out)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    kern = lif.lif_timer_read()
+    lif.lif_timer_enable(False)
+    ms_step = elapsed / args.steps * 1e3
+    value = neuron_events * args.steps / elapsed
+    status = out.status.cpu().numpy().tolist()
+    n_spikes = int(out.out_n.sum().item())
+    log(f"[bench] forward {ms_step * 1e3:.1f} us/step, {value:.3e} neuron-events/s, status {status}")
+    log(f"[bench] kernels: " + ", ".join(f"{k}={v[0] / v[1] * 1e3:.1f}us" for k, v in kern.items()))
+
+    # ---- roofline of the dominant kernel: algorithmic bytes are the event
+    # record (time + source, 8 B per event) and one float32 weight per
+    # neuron-event, plus the spike outputs for the resolve pass.
+    dom = max(kern.items(), key=lambda kv: kv[1][0])
+    dom_name, (dom_ms, dom_n) = dom
+    dom_us = dom_ms / dom_n * 1e3
+    alg_bytes = total_ev * (8 + 4 * N)
+    achieved = alg_bytes / (dom_us * 1e-6) / 1e9
+    fwd_alg_bytes = total_ev * (8 + 4 * N) + B * N * 4 + n_spikes * 8
+
+    # ---- sequential GPU baseline (same ABI, same inputs)
+    seq = lif.forward(d_t, d_s, d_n, d_W, P, sequential=True, ws=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(seq.out_n, out.out_n), "sequential and parallel spike counts differ"
+    ts0 = time.perf_counter()
+    for _ in range(args.seq_steps):
+        lif.forward(d_t, d_s, d_n, d_W, P, sequential=True, ws=ws, out=seq)
+    torch.cuda.synchronize()
+    seq_ms = (time.perf_counter() - ts0) / args.seq_steps * 1e3
+    log(f"[bench] sequential {seq_ms:.3f} ms/step, speedup {seq_ms / ms_step:.1f}x")
+
+    # ---- backward pass on the same batch (dL/dt ~ N(0,1) on every spike)
+    rng = np.random.default_rng(1)
+    valid = np.isfinite(out.out_t.cpu().numpy())
+    g = t((rng.standard_normal(valid.shape) * valid).astype(np.float32))
+    bws = torch.empty(lif.lif_layer_backward_workspace_size(B, E, C, N, pc), dtype=torch.uint8, device=dev)
+    for _ in range(3):
+        lif.backward(d_t, d_s, d_n, d_W, out, g, P, ws=bws)
+    torch.cuda.synchronize()
+    tb0 = time.perf_counter()
+    nb = max(5, args.steps // 5)
+    for _ in range(nb):
+        lif.backward(d_t, d_s, d_n, d_W, out, g, P, ws=bws)
+    torch.cuda.synchronize()
+    bwd_ms = (time.perf_counter() - tb0) / nb * 1e3
+    log(f"[bench] backward {bwd_ms * 1e3:.1f} us/step")
+
+    # ---- float64 CPU oracle on the host cores (full batch, repeated)
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        ncores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+        ncores = max(1, min(int(ncores), 16))
+        OP = oracle.LifParams(s_max=64)
+        oracle.forward(ev.ev_t[:1], ev.ev_src[:1], ev.ev_n[:1], WT, OP, nthreads=ncores)
+        c0 = time.perf_counter()
+        for _ in range(args.cpu_repeats):
+            oracle.forward(ev.ev_t, ev.ev_src, ev.ev_n, WT, OP, nthreads=ncores)
+        cpu_s = (time.perf_counter() - c0) / args.cpu_repeats
+        cpu = {"value": neuron_events / cpu_s, "unit": "neuron-events/s", "cores": ncores, "kind": "oracle",
+               "sample": f"full batch (32 samples x 256 neurons, {total_ev} events), "
+                         f"{args.cpu_repeats} repeats, {cpu_s:.3f} s each"}
+        log(f"[bench] cpu oracle {cpu_s:.3f} s/forward on {ncores} threads")
+
+    line = {
+        "metric": "neuron-events/s fwd (700->256, B=32)",
+        "value": value,
+        "unit": "neuron-events/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "io_dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "LIF layer 700->256, B=32, 1 s lognormal-Poisson input (~5k events/sample), "
+                               "tau_m 20 ms, tau_s 5 ms, threshold 1, reset 0",
+                   "batch": B, "c_in": C, "n_out": N, "events": total_ev, "e_max": E,
+                   "neuron_events": neuron_events, "spikes": n_spikes, "s_max": P.s_max},
+        "roofline": {"bound": "hbm", "kernel": dom_name, "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "alg_bytes_per_launch": alg_bytes, "kernel_us": dom_us},
+        "hbm_frac_forward": fwd_alg_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "kernels_us": {k: v[0] / v[1] * 1e3 for k, v in kern.items()},
+        "sequential_ms": seq_ms,
+        "speedup_vs_sequential": seq_ms / ms_step,
+        "backward_ms": bwd_ms,
+        "status": status,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()
