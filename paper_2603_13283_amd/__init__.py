@@ -36,7 +36,7 @@ ERR_NAMES = {LIF_ERR_ARG: "LIF_ERR_ARG", LIF_ERR_TAU: "LIF_ERR_TAU", LIF_ERR_THR
 
 LIF_VALIDATE = 1
 LIF_STATUS_WORDS = 8
-ST_FLAGS, ST_CAPPED, ST_SPIKES, ST_CAND_BLOCKS, ST_WALKED_BLOCKS, ST_ROOT_SOLVES, ST_EVENTS = range(7)
+ST_FLAGS, ST_CAPPED, ST_SPIKES, ST_CAND_BLOCKS, ST_WALKED_BLOCKS, ST_ROOT_SOLVES, ST_EVENTS, ST_POOL_FALLBACK = range(8)
 WARN_SPIKE_CAP, WARN_UNSORTED, WARN_BAD_SOURCE, WARN_NONFINITE, WARN_MERGE_FULL, WARN_BAD_COUNT = 1, 2, 4, 8, 16, 32
 LIF_MERGE_MAX = 16384
 

@@ -70,6 +70,7 @@ __device__ __forceinline__ double v_after(const Model& m, double V0, double I0, 
 struct Crossing {
     bool hit;      // V reaches th inside (0, len]
     double hi;     // right end of the root bracket, min(t_Vmax, len)
+    double vhi;    // V(hi)
 };
 
 // Interval rule of Sec. 3.2.2 for an interval of length len (may be +inf)
@@ -83,34 +84,47 @@ struct Crossing {
 __device__ __forceinline__ Crossing interval_rule(const Model& m, double V0, double I0, double len,
                                                   double eA, double eD, double vend, double th)
 {
-    Crossing c{false, len};
+    Crossing c{false, len, vend};
     double Dd = V0 * (m.tm - m.ts) + I0 * m.ts;
     bool has_max = (I0 > V0) && (Dd > 0.0);
     bool max_inside = has_max && (isinf(len) || I0 * m.tm * eD < Dd * eA);
     if (vend >= th) {
         c.hit = true;
-        if (max_inside) c.hi = fmin(m.c_tv * log(I0 * m.tm / Dd), len);
+        if (max_inside) {
+            double tv = m.c_tv * log(I0 * m.tm / Dd);
+            if (tv < len) { c.hi = tv; c.vhi = v_after(m, V0, I0, tv); }
+        }
         return c;
     }
     if (max_inside) {
         double tv = m.c_tv * log(I0 * m.tm / Dd);
-        if (tv < len && v_after(m, V0, I0, tv) >= th) {
-            c.hit = true;
-            c.hi = tv;
+        if (tv < len) {
+            double vv = v_after(m, V0, I0, tv);
+            if (vv >= th) {
+                c.hit = true;
+                c.hi = tv;
+                c.vhi = vv;
+            }
         }
     }
     return c;
 }
 
 // Bracketed Newton-Raphson for the first time tau in (0, hi] with
-// V(tau) = th (Appendix D.1): start at hi/2, keep [lo, hi] with V(lo) < th
-// <= V(hi), fall back to the midpoint whenever a step leaves the bracket
-// (the clamp of D.1, i.e. a bisection step of D.2), stop when the step no
-// longer changes the float64 iterate.  dV/dt comes from Eq. mem_dyn.
-__device__ __forceinline__ double newton_root(const Model& m, double V0, double I0, double hi, int* iters)
+// V(tau) = th (Appendix D.1), keeping [lo, hi] with V(lo) < th <= V(hi) and
+// falling back to the midpoint whenever a step leaves the bracket (the
+// clamp of D.1, i.e. a bisection step of D.2); it stops when a step no longer
+// moves the float64 iterate.  dV/dt comes from Eq. mem_dyn.  The start is the
+// root of the chord from (0, V0) to (hi, V(hi)) instead of the paper's hi/2:
+// V is concave on [0, hi] (it rises to its only maximum, whose inflection
+// comes later), so the chord lies below V and its root is a tight upper
+// bound of the crossing; from there Newton converges in a few steps.
+__device__ __forceinline__ double newton_root(const Model& m, double V0, double I0, double hi, double vhi,
+                                              int* iters)
 {
     double lo = 0.0;
-    double t = 0.5 * hi;
+    double t = (vhi > V0) ? hi * ((m.th - V0) / (vhi - V0)) : 0.5 * hi;
+    if (!(t > 0.0 && t <= hi)) t = 0.5 * hi;
     int it = 0;
     for (; it < 96; ++it) {
         double em = exp(-t * m.inv_tm);
@@ -118,10 +132,11 @@ __device__ __forceinline__ double newton_root(const Model& m, double V0, double 
         double v = V0 * em + I0 * m.kappa * (em - es);
         if (v >= m.th) hi = t; else lo = t;
         double d = (I0 * es - v) * m.inv_tm;
-        double tn = (d > 0.0) ? t - (v - m.th) / d : 0.5 * (lo + hi);
+        double step = (d > 0.0) ? (v - m.th) / d : INFINITY;
+        if (fabs(step) <= 2e-16 * t) { t -= step; break; }   // converged to the ulp
+        double tn = t - step;
         if (!(tn > lo && tn < hi)) tn = 0.5 * (lo + hi);
-        if (tn == t) break;                               // converged to the ulp
-        if (hi - lo <= 4e-16 * hi) { t = hi; break; }     // bracket collapsed
+        if (hi - lo <= 4e-16 * hi) { t = hi; break; }        // bracket collapsed
         t = tn;
     }
     if (iters) *iters = it;

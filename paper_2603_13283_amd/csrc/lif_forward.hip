@@ -35,11 +35,24 @@
 
 namespace lif {
 
-struct alignas(32) SubCarry {
-    double V, I;    // no-reset state entering the sub-block
-    double ub;      // upper bound of the no-reset V over the flagged intervals
-    double pad;
+// Record of one flagged sub-block of one neuron: the no-reset state (V, I)
+// entering it and right after each of its kSub events.  With the reset
+// deficit of the spikes found so far, these give the true state at every
+// interval boundary of the sub-block in O(1), so the resolve pass can test
+// all of its intervals at once.  Records live in a pool; each wave allocates
+// the records of one sub-block with one atomic and notes (lane mask, first
+// slot).
+struct alignas(16) Record {
+    double2 s[kSub + 1];    // s[0]: entering state; s[j + 1]: after event j
 };
+static_assert(sizeof(Record) == 16 * (kSub + 1), "record layout");
+
+struct alignas(16) WaveInfo {
+    unsigned long long lanes;   // lanes of the wave with a record for this sub-block
+    uint32_t base;              // pool slot of the lowest such lane, kNoSlot if the pool was full
+    uint32_t pad;
+};
+constexpr uint32_t kNoSlot = 0xffffffffu;
 
 // Workgroup index -> work index such that each of the 8 XCDs (which receive
 // workgroups round-robin) processes a contiguous, sample-major range: the
@@ -58,10 +71,12 @@ __device__ __forceinline__ int xcd_remap(int wg, int total)
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_decay(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_n,
                                                int B, int E_max, int S, Model m, Decay* __restrict__ dec,
-                                               Decay* __restrict__ segm, int32_t* __restrict__ status)
+                                               Decay* __restrict__ segm, int32_t* __restrict__ status,
+                                               uint32_t* __restrict__ pool_count)
 {
     size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (idx < LIF_STATUS_WORDS && status) status[idx] = 0;
+    if (idx == 0 && pool_count) *pool_count = 0;
     if (idx >= (size_t)B * (size_t)E_max) return;
     int b = (int)(idx / (size_t)E_max), k = (int)(idx % (size_t)E_max);
     int n = clamp_count(ev_n[b], E_max);
@@ -158,7 +173,10 @@ __global__ __launch_bounds__(64) void k_aggregate(const int32_t* __restrict__ ev
 }
 
 // Exclusive scan over segments of the Combine of Eq. affine:
-// s_in(j+1) = M(T_j) s_in(j) + b_j, with s_in(0) = (0, 0).
+// s_in(j+1) = M(T_j) s_in(j) + b_j, with s_in(0) = (0, 0).  The segment
+// aggregates are fetched kCarryBatch at a time so their loads overlap.
+constexpr int kCarryBatch = 8;
+
 __global__ __launch_bounds__(256) void k_carry(const int32_t* __restrict__ ev_n, int B, int E_max, int N, int S,
                                                const Decay* __restrict__ segm, const double2* __restrict__ agg,
                                                double2* __restrict__ carry)
@@ -168,71 +186,42 @@ __global__ __launch_bounds__(256) void k_carry(const int32_t* __restrict__ ev_n,
     int b = (int)(idx / (size_t)N), n = (int)(idx % (size_t)N);
     int Sb = (clamp_count(ev_n[b], E_max) + kSeg - 1) / kSeg;
     double V = 0.0, I = 0.0;
-    for (int j = 0; j < Sb; ++j) {
-        size_t o = ((size_t)b * S + j) * N + n;
-        carry[o] = make_double2(V, I);
-        Decay M = segm[(size_t)b * S + j];
-        double2 a = agg[o];
-        double Vn = M.A * V + M.C * I + a.x;
-        I = M.D * I + a.y;
-        V = Vn;
-    }
-}
-
-// Exact interval test of one no-reset sub-block walk, run only for lanes
-// whose cheap bound fired somewhere in the sub-block.  Returns whether any
-// interval of the sub-block satisfies the interval rule at th_lo and the
-// largest bound value of such intervals.
-__device__ __noinline__ bool subblock_exact(const Model& m, const float* __restrict__ tt,
-                                            const int32_t* __restrict__ src, const Decay* __restrict__ d,
-                                            const float* __restrict__ wcol, int C_in, int N, int kq0, int kq1, int nb,
-                                            double V, double I, double* ub_out)
-{
-    bool cand = false;
-    double ub = -INFINITY;
-    for (int k = kq0; k < kq1; ++k) {
-        Decay e = d[k];
-        double u = fmax(V, 0.0) + fmax(I, 0.0) * e.g;
-        double Vn = e.A * V + e.C * I;
-        if (u >= m.th_lo) {
-            double len = (double)tt[k] - (k > 0 ? (double)tt[k - 1] : 0.0);
-            Crossing c = interval_rule(m, V, I, len, e.A, e.D, Vn, m.th_lo);
-            if (c.hit) { cand = true; ub = fmax(ub, u); }
+    for (int j0 = 0; j0 < Sb; j0 += kCarryBatch) {
+        double2 a[kCarryBatch];
+        Decay M[kCarryBatch];
+#pragma unroll
+        for (int j = 0; j < kCarryBatch; ++j) {
+            int jj = min(j0 + j, Sb - 1);
+            a[j] = agg[((size_t)b * S + jj) * N + n];
+            M[j] = segm[(size_t)b * S + jj];
         }
-        I = e.D * I + (double)wcol[(size_t)clamp_src(src[k], C_in) * (size_t)N];
-        V = Vn;
-    }
-    if (kq1 == nb) {
-        // Interval after the last event, up to t_end (default +inf).
-        double len = m.t_end - (double)tt[nb - 1];
-        if (len > 0.0) {
-            double eA = isinf(len) ? 0.0 : exp(-len * m.inv_tm);
-            double eD = isinf(len) ? 0.0 : exp(-len * m.inv_ts);
-            double C = isinf(len) ? 0.0 : unit_kernel(m, len, eA);
-            double gl = fmin(len, m.t_peak);
-            double g = unit_kernel(m, gl, exp(-gl * m.inv_tm)) * (1.0 + 1e-12);
-            double u = fmax(V, 0.0) + fmax(I, 0.0) * g;
-            if (u >= m.th_lo) {
-                Crossing c = interval_rule(m, V, I, len, eA, eD, V * eA + C * I, m.th_lo);
-                if (c.hit) { cand = true; ub = fmax(ub, u); }
+#pragma unroll
+        for (int j = 0; j < kCarryBatch; ++j) {
+            if (j0 + j < Sb) {
+                carry[((size_t)b * S + j0 + j) * N + n] = make_double2(V, I);
+                double Vn = M[j].A * V + M[j].C * I + a[j].x;
+                I = M[j].D * I + a[j].y;
+                V = Vn;
             }
         }
     }
-    *ub_out = ub;
-    return cand;
 }
 
-// Re-walk with the interval check.  Bound: V(t) = V0 e^{-t/tm} + I0 K(t)
-// <= max(V0, 0) + max(I0, 0) K(min(dt, t_peak)) since 0 <= K <= that value
-// on [0, dt].  The hot loop only records whether the bound reached th_lo in
-// a sub-block (one compare per event); such sub-blocks, rare except right
-// around spikes, are walked again with the exact interval rule.
+// Re-walk from the carried no-reset state with a cheap exact bound per
+// interval: V(t) = V0 e^{-t/tm} + I0 K(t) <= max(V0, 0) + max(I0, 0)
+// K(min(dt, t_peak)) since 0 <= K(t) <= K(min(dt, t_peak)) on [0, dt].
+// Resets only lower V (each is the subtraction of a positive decaying
+// term), so a sub-block whose no-reset bound stays below the threshold holds
+// no spike whatever happened before it.  Sub-blocks whose bound reaches it
+// get a record for the resolve pass, which applies the exact interval rule.
 __global__ __launch_bounds__(64) void k_check(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src,
                                               const int32_t* __restrict__ ev_n, int E_max,
                                               const float* __restrict__ WT, int C_in, int N, int tiles, int S,
                                               int total, Model m, const Decay* __restrict__ dec,
                                               const double2* __restrict__ carry, uint32_t* __restrict__ mask,
-                                              SubCarry* __restrict__ subc, int32_t* __restrict__ status)
+                                              WaveInfo* __restrict__ winfo, Record* __restrict__ pool,
+                                              double* __restrict__ pool_ub, uint32_t* __restrict__ pool_count,
+                                              uint32_t pool_cap, int32_t* __restrict__ status)
 {
     int lin = xcd_remap(blockIdx.x, total);
     int tile = lin % tiles;
@@ -243,7 +232,8 @@ __global__ __launch_bounds__(64) void k_check(const float* __restrict__ ev_t, co
     int k0 = seg * kSeg;
     if (k0 >= nb) return;
     int k1 = min(k0 + kSeg, nb);
-    int n = tile * kWave + (int)threadIdx.x;
+    const int lane = (int)threadIdx.x;
+    int n = tile * kWave + lane;
     int nc = min(n, N - 1);
     const float* wcol = WT + nc;
     const float* tt = ev_t + (size_t)b * E_max;
@@ -254,40 +244,61 @@ __global__ __launch_bounds__(64) void k_check(const float* __restrict__ ev_t, co
     double V = c0.x, I = c0.y;
     uint32_t msk = 0;
     int ncand = 0;
+    const unsigned long long below = (1ull << lane) - 1ull;
     for (int q = 0; q < kSubPerSeg; ++q) {
         int kq0 = k0 + q * kSub;
         if (kq0 >= k1) break;
-        int kq1 = min(kq0 + kSub, k1);
-        double Vin = V, Iin = I;
-        bool surv = kq1 == nb;           // the open last interval is always tested exactly
-        if (kq1 - kq0 == kSub) {
-            float w[kSub];
+        int cnt = min(kSub, k1 - kq0);
+        double Vin = V, Iin = I, ub = -INFINITY;
+        float w[kSub];
+        double Vs[kSub], Is[kSub];
 #pragma unroll
-            for (int j = 0; j < kSub; ++j) w[j] = wcol[(size_t)clamp_src(src[kq0 + j], C_in) * (size_t)N];
+        for (int j = 0; j < kSub; ++j) w[j] = j < cnt ? wcol[(size_t)clamp_src(src[kq0 + j], C_in) * (size_t)N] : 0.0f;
 #pragma unroll
-            for (int j = 0; j < kSub; ++j) {
+        for (int j = 0; j < kSub; ++j) {
+            if (j < cnt) {
                 Decay e = d[kq0 + j];
-                surv |= fmax(V, 0.0) + fmax(I, 0.0) * e.g >= m.th_lo;
+                ub = fmax(ub, fmax(V, 0.0) + fmax(I, 0.0) * e.g);
                 double Vn = e.A * V + e.C * I;
                 I = e.D * I + (double)w[j];
                 V = Vn;
             }
-        } else {
-            for (int k = kq0; k < kq1; ++k) {
-                float w = wcol[(size_t)clamp_src(src[k], C_in) * (size_t)N];
-                Decay e = d[k];
-                surv |= fmax(V, 0.0) + fmax(I, 0.0) * e.g >= m.th_lo;
-                double Vn = e.A * V + e.C * I;
-                I = e.D * I + (double)w;
-                V = Vn;
+            Vs[j] = V;
+            Is[j] = I;
+        }
+        if (kq0 + cnt == nb) {
+            // Interval after the last event, up to t_end (default +inf).
+            double len = m.t_end - (double)tt[nb - 1];
+            if (len > 0.0) {
+                double gl = fmin(len, m.t_peak);
+                double g = unit_kernel(m, gl, exp(-gl * m.inv_tm)) * (1.0 + 1e-12);
+                ub = fmax(ub, fmax(V, 0.0) + fmax(I, 0.0) * g);
             }
         }
-        if (surv && n < N) {
-            double ub;
-            if (subblock_exact(m, tt, src, d, wcol, C_in, N, kq0, kq1, nb, Vin, Iin, &ub)) {
-                SubCarry sc;
-                sc.V = Vin; sc.I = Iin; sc.ub = ub; sc.pad = 0.0;
-                subc[row * kSubPerSeg + (size_t)q * N + n] = sc;
+        bool surv = ub >= m.th_lo && n < N;
+        unsigned long long lanes = __ballot(surv);
+        if (lanes) {
+            int cntl = __popcll(lanes);
+            uint32_t base = 0;
+            if (lane == 0) base = atomicAdd(pool_count, (uint32_t)cntl);
+            base = __shfl(base, 0, kWave);
+            bool ok = (unsigned long long)base + (unsigned long long)cntl <= (unsigned long long)pool_cap;
+            if (lane == 0) {
+                WaveInfo wi;
+                wi.lanes = lanes;
+                wi.base = ok ? base : kNoSlot;
+                wi.pad = 0;
+                winfo[(((size_t)b * S + seg) * tiles + tile) * kSubPerSeg + q] = wi;
+            }
+            if (surv) {
+                if (ok) {
+                    uint32_t slot = base + (uint32_t)__popcll(lanes & below);
+                    pool_ub[slot] = ub;
+                    Record* r = pool + slot;
+                    r->s[0] = make_double2(Vin, Iin);
+#pragma unroll
+                    for (int j = 0; j < kSub; ++j) r->s[j + 1] = make_double2(Vs[j], Is[j]);
+                }
                 msk |= 1u << q;
                 ++ncand;
             }
@@ -340,7 +351,7 @@ __device__ bool advance_interval(const Model& m, double& V, double& I, double& t
             Crossing c = interval_rule(m, V, I, len, eA, eD, vend, m.th);
             if (c.hit) {
                 int it = 0;
-                double tau = newton_root(m, V, I, c.hi, &it);
+                double tau = newton_root(m, V, I, c.hi, c.vhi, &it);
                 double Istar = I * exp(-tau * m.inv_ts);
                 double tsp = t_cur + tau;
                 sk.st[sk.ns] = (float)tsp;
@@ -380,62 +391,257 @@ __device__ __forceinline__ void finish_neuron(const Model& m, Sink& sk, int32_t*
     if (sk.roots) atomicAdd(&status[LIF_ST_ROOT_SOLVES], sk.roots);
 }
 
-__global__ __launch_bounds__(256) void k_resolve(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src,
-                                                 const int32_t* __restrict__ ev_n, int B, int E_max,
-                                                 const float* __restrict__ WT, int C_in, int N, int S, Model m,
-                                                 const Decay* __restrict__ dec, const uint32_t* __restrict__ mask,
-                                                 const SubCarry* __restrict__ subc, float* __restrict__ out_t,
-                                                 int32_t* __restrict__ out_n, float* __restrict__ out_i,
-                                                 int32_t* __restrict__ status)
+// Rebuild a sub-block's entering no-reset state from its segment carry by
+// walking the earlier sub-blocks of the segment (used only when the record
+// pool was full).
+__device__ __noinline__ double2 entering_state(const double2* __restrict__ carry, size_t row, int n, int k0, int kq0,
+                                               const int32_t* __restrict__ src, const Decay* __restrict__ d,
+                                               const float* __restrict__ WT, int C_in, int N)
 {
-    size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= (size_t)B * (size_t)N) return;
-    int b = (int)(idx / (size_t)N), n = (int)(idx % (size_t)N);
-    int nb = clamp_count(ev_n[b], E_max);
-    if (n == 0) atomicAdd(&status[LIF_ST_EVENTS], nb);
+    double2 c = carry[row + n];
+    double V = c.x, I = c.y;
+    for (int k = k0; k < kq0; ++k) {
+        Decay e = d[k];
+        double Vn = e.A * V + e.C * I;
+        I = e.D * I + (double)WT[(size_t)clamp_src(src[k], C_in) * (size_t)N + n];
+        V = Vn;
+    }
+    return make_double2(V, I);
+}
+
+// Resolve pass: one wave per (sample, neuron), the paper's chunked
+// speculative scheme applied to the neuron's flagged sub-blocks only.
+// kGroup flagged sub-blocks are staged in LDS (kSub lanes each, one lane per
+// interval).  Since every reset subtracts (V_th - V_reset) e^{-(t - t_s)/tm}
+// from the no-reset trajectory, the true state entering interval k is the
+// record's no-reset state minus the reset deficit at t_{k-1}; all intervals
+// of the group are tested at once with the interval rule, the earliest
+// crossing (ballot) is solved by its lane with bracketed Newton, reset and
+// re-tested until its interval is clear, the deficit is updated and the
+// later intervals are tested again.  Intervals before the first flagged
+// sub-block, and between flagged sub-blocks, provably hold no spike.
+constexpr int kGroup = kWave / kSub;
+
+// Wave-uniform spike bookkeeping of the neuron being resolved.
+struct NeuronSpikes {
+    int ns, roots;
+    double dref, tref;    // reset deficit dref at time tref
+    bool capped;
+};
+
+__device__ __forceinline__ double deficit_at(const NeuronSpikes& ns_, const Model& m, double t)
+{
+    return ns_.ns > 0 ? ns_.dref * exp(-(t - ns_.tref) * m.inv_tm) : 0.0;
+}
+
+__global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src,
+                                                   const int32_t* __restrict__ ev_n, int E_max,
+                                                   const float* __restrict__ WT, int C_in, int N, int tiles, int S,
+                                                   Model m, const Decay* __restrict__ dec,
+                                                   const double2* __restrict__ carry,
+                                                   const uint32_t* __restrict__ mask,
+                                                   const WaveInfo* __restrict__ winfo,
+                                                   const Record* __restrict__ pool,
+                                                   const double* __restrict__ pool_ub, float* __restrict__ out_t,
+                                                   int32_t* __restrict__ out_n, float* __restrict__ out_i,
+                                                   int32_t* __restrict__ status)
+{
+    __shared__ double2 stg[kGroup][kSub + 1];
+    __shared__ int g_seg[kGroup], g_q[kGroup];
+    __shared__ int w_seg[kWave], w_q[kWave];
+    const int b = blockIdx.x / N;
+    const int n = blockIdx.x % N;
+    const int tile = n / kWave;
+    const unsigned long long below_n = (1ull << (n % kWave)) - 1ull;
+    const int lane = (int)threadIdx.x;
+    const int nb = clamp_count(ev_n[b], E_max);
+    if (n == 0 && lane == 0) atomicAdd(&status[LIF_ST_EVENTS], nb);
     const float* tt = ev_t + (size_t)b * E_max;
     const int32_t* src = ev_src + (size_t)b * E_max;
     const Decay* d = dec + (size_t)b * E_max;
-    Sink sk;
-    sk.st = out_t + idx * (size_t)m.s_max;
-    sk.si = out_i ? out_i + idx * (size_t)m.s_max : nullptr;
-    sk.ns = 0; sk.roots = 0; sk.dref = 0.0; sk.tref = 0.0;
-    bool capped = false;
-    int walked = 0;
-    int Sb = (nb + kSeg - 1) / kSeg;
-    for (int seg = 0; seg < Sb && !capped; ++seg) {
-        size_t row = ((size_t)b * S + seg) * N;
-        uint32_t msk = mask[row + n];
-        while (msk && !capped) {
-            int q = __builtin_ctz(msk);
-            msk &= msk - 1;
-            SubCarry sc = subc[row * kSubPerSeg + (size_t)q * N + n];
+    const size_t idx = (size_t)b * N + n;
+    float* st = out_t + idx * (size_t)m.s_max;
+    float* si = out_i ? out_i + idx * (size_t)m.s_max : nullptr;
+    NeuronSpikes sp{0, 0, 0.0, 0.0, false};
+    int walked = 0, fallback = 0;
+    const int Sb = (nb + kSeg - 1) / kSeg;
+    int G = 0;
+
+    auto process_group = [&]() {
+        __syncthreads();                      // g_seg / g_q written by lane 0
+        // ---- stage the group's no-reset states in LDS
+        for (int r = 0; r < G; ++r) {
+            int seg = g_seg[r], q = g_q[r];
             int kq0 = seg * kSeg + q * kSub;
-            int kq1 = min(kq0 + kSub, nb);
-            bool last = kq1 == nb;
-            double t_in = kq0 > 0 ? (double)tt[kq0 - 1] : 0.0;
-            // End of the sub-block's last interval (the open interval after the
-            // final event ends at t_end, or is empty if t_end is earlier).
-            double t_out = last ? fmax(m.t_end, (double)tt[kq1 - 1]) : (double)tt[kq1 - 1];
-            double def_in = 0.0;
-            if (sk.ns > 0) {
-                double def_out = isinf(t_out) ? 0.0 : sk.dref * exp(-(t_out - sk.tref) * m.inv_tm);
-                if (sc.ub - def_out < m.th_lo) continue;    // certified by the deficit
-                def_in = sk.dref * exp(-(t_in - sk.tref) * m.inv_tm);
+            WaveInfo wi = winfo[(((size_t)b * S + seg) * tiles + tile) * kSubPerSeg + q];
+            if (wi.base != kNoSlot) {
+                const Record* rec = pool + wi.base + (uint32_t)__popcll(wi.lanes & below_n);
+                if (lane <= kSub) stg[r][lane] = rec->s[lane];
+            } else {
+                if (lane == 0) {
+                    size_t row = ((size_t)b * S + seg) * N;
+                    double2 cs = entering_state(carry, row, n, seg * kSeg, kq0, src, d, WT, C_in, N);
+                    double V = cs.x, I = cs.y;
+                    stg[r][0] = cs;
+                    int cnt = min(kSub, nb - kq0);
+                    for (int j = 0; j < cnt; ++j) {
+                        Decay e = d[kq0 + j];
+                        double Vn = e.A * V + e.C * I;
+                        I = e.D * I + (double)WT[(size_t)clamp_src(src[kq0 + j], C_in) * (size_t)N + n];
+                        V = Vn;
+                        stg[r][j + 1] = make_double2(V, I);
+                    }
+                }
+                ++fallback;
             }
-            ++walked;
-            double V = sc.V - def_in, I = sc.I, t_cur = t_in;
-            for (int k = kq0; k < kq1; ++k) {
-                if (!advance_interval(m, V, I, t_cur, (double)tt[k], &d[k], sk)) { capped = true; break; }
-                I += (double)WT[(size_t)clamp_src(src[k], C_in) * (size_t)N + n];
+        }
+        __syncthreads();
+        walked += G;
+        // ---- this lane's interval: the one before event k of sub-block r
+        const int r = lane / kSub, j = lane % kSub;
+        int kq0 = 0, cnt = 0;
+        if (r < G) { kq0 = g_seg[r] * kSeg + g_q[r] * kSub; cnt = min(kSub, nb - kq0); }
+        const bool valid = r < G && j < cnt;
+        const int k = valid ? kq0 + j : 0;
+        const Decay e = valid ? d[k] : Decay{1.0, 0.0, 1.0, 0.0};
+        const double t1 = valid ? (double)tt[k] : 0.0;
+        const double t0 = valid && k > 0 ? (double)tt[k - 1] : 0.0;
+        const double2 s0 = valid ? stg[r][j] : make_double2(0.0, 0.0);
+        const double2 s1 = valid ? stg[r][j + 1] : make_double2(0.0, 0.0);
+        bool pending = valid && t1 > t0;
+        while (!sp.capped) {
+            bool cross = false;
+            double V0 = 0.0, I0 = 0.0;
+            if (pending) {
+                double def0 = deficit_at(sp, m, t0);
+                V0 = s0.x - def0;
+                I0 = s0.y;
+                double u = fmax(V0, 0.0) + fmax(I0, 0.0) * e.g;
+                if (u >= m.th_lo) {
+                    double vend = s1.x - def0 * e.A;
+                    cross = interval_rule(m, V0, I0, t1 - t0, e.A, e.D, vend, m.th).hit;
+                }
             }
-            if (!capped && last) {
-                if (!advance_interval(m, V, I, t_cur, m.t_end, nullptr, sk)) capped = true;
+            unsigned long long cm = __ballot(cross);
+            if (!cm) break;
+            const int kl = __ffsll((long long)cm) - 1;
+            if (lane == kl) {
+                Sink sk;
+                sk.st = st; sk.si = si;
+                sk.ns = sp.ns; sk.roots = sp.roots; sk.dref = sp.dref; sk.tref = sp.tref;
+                double V = V0, I = I0, tc = t0;
+                bool ok = advance_interval(m, V, I, tc, t1, &e, sk);
+                sp.ns = sk.ns; sp.roots = sk.roots; sp.dref = sk.dref; sp.tref = sk.tref;
+                sp.capped = !ok;
+            }
+            sp.ns = __shfl(sp.ns, kl, kWave);
+            sp.roots = __shfl(sp.roots, kl, kWave);
+            sp.dref = __shfl(sp.dref, kl, kWave);
+            sp.tref = __shfl(sp.tref, kl, kWave);
+            sp.capped = __shfl((int)sp.capped, kl, kWave) != 0;
+            if (lane <= kl) pending = false;
+        }
+        // ---- the open interval after the stream's last event
+        if (!sp.capped && G > 0) {
+            int rl = G - 1;
+            int kql = g_seg[rl] * kSeg + g_q[rl] * kSub;
+            int cl = min(kSub, nb - kql);
+            if (kql + cl == nb && lane == 0) {
+                double tl = (double)tt[nb - 1];
+                double2 sl = stg[rl][cl];
+                Sink sk;
+                sk.st = st; sk.si = si;
+                sk.ns = sp.ns; sk.roots = sp.roots; sk.dref = sp.dref; sk.tref = sp.tref;
+                double V = sl.x - deficit_at(sp, m, tl), I = sl.y, tc = tl;
+                bool ok = advance_interval(m, V, I, tc, m.t_end, nullptr, sk);
+                sp.ns = sk.ns; sp.roots = sk.roots; sp.dref = sk.dref; sp.tref = sk.tref;
+                sp.capped = !ok;
+            }
+            sp.ns = __shfl(sp.ns, 0, kWave);
+            sp.roots = __shfl(sp.roots, 0, kWave);
+            sp.dref = __shfl(sp.dref, 0, kWave);
+            sp.tref = __shfl(sp.tref, 0, kWave);
+            sp.capped = __shfl((int)sp.capped, 0, kWave) != 0;
+        }
+        __syncthreads();
+        G = 0;
+    };
+
+    // Flagged sub-blocks are gathered in windows of up to kWave (one lane
+    // each).  Every pass over a window first certifies, in parallel, the
+    // sub-blocks whose no-reset bound minus the current reset deficit at
+    // their end stays below the threshold (more spikes only deepen the
+    // deficit, so certification is final), then resolves the earliest kGroup
+    // uncertified ones.
+    int W = 0;
+    auto process_window = [&]() {
+        __syncthreads();                      // w_seg / w_q written by lane 0
+        bool done = lane >= W;
+        double ub = 0.0, t_out = 0.0;
+        if (!done) {
+            int seg = w_seg[lane], q = w_q[lane];
+            int kq0 = seg * kSeg + q * kSub;
+            int cnt = min(kSub, nb - kq0);
+            WaveInfo wi = winfo[(((size_t)b * S + seg) * tiles + tile) * kSubPerSeg + q];
+            ub = wi.base != kNoSlot ? pool_ub[wi.base + (uint32_t)__popcll(wi.lanes & below_n)] : INFINITY;
+            double tl = (double)tt[kq0 + cnt - 1];
+            t_out = kq0 + cnt == nb ? fmax(m.t_end, tl) : tl;
+        }
+        while (!sp.capped) {
+            if (!done && sp.ns > 0) {
+                double def_out = isinf(t_out) ? 0.0 : deficit_at(sp, m, t_out);
+                if (ub - def_out < m.th_lo) done = true;
+            }
+            unsigned long long rem = __ballot(!done);
+            if (!rem) break;
+            G = 0;
+            while (rem && G < kGroup) {
+                int c = __ffsll((long long)rem) - 1;
+                rem &= rem - 1ull;
+                if (lane == 0) { g_seg[G] = w_seg[c]; g_q[G] = w_q[c]; }
+                if (lane == c) done = true;
+                ++G;
+            }
+            process_group();
+        }
+        __syncthreads();
+        W = 0;
+    };
+
+    for (int seg0 = 0; seg0 < Sb && !sp.capped; seg0 += kWave) {
+        int sj = seg0 + lane;
+        uint32_t mv = sj < Sb ? mask[((size_t)b * S + sj) * N + n] : 0u;
+        unsigned long long nz = __ballot(mv != 0u);
+        while (nz && !sp.capped) {
+            int l = __ffsll((long long)nz) - 1;
+            nz &= nz - 1ull;
+            uint32_t mm = (uint32_t)__shfl((int)mv, l, kWave);
+            while (mm && !sp.capped) {
+                int q = __builtin_ctz(mm);
+                mm &= mm - 1u;
+                if (lane == 0) { w_seg[W] = seg0 + l; w_q[W] = q; }
+                ++W;
+                if (W == kWave) process_window();
             }
         }
     }
-    if (walked) atomicAdd(&status[LIF_ST_WALKED_BLOCKS], walked);
-    finish_neuron(m, sk, out_n + idx, capped, status);
+    if (W > 0 && !sp.capped) process_window();
+
+    if (lane == 0) {
+        if (walked) atomicAdd(&status[LIF_ST_WALKED_BLOCKS], walked);
+        if (fallback) atomicAdd(&status[LIF_ST_POOL_FALLBACK], fallback);
+        out_n[idx] = sp.ns;
+        if (sp.capped) {
+            atomicAdd(&status[LIF_ST_CAPPED], 1);
+            atomicOr(&status[LIF_ST_FLAGS], LIF_WARN_SPIKE_CAP);
+        }
+        if (sp.ns) atomicAdd(&status[LIF_ST_SPIKES], sp.ns);
+        if (sp.roots) atomicAdd(&status[LIF_ST_ROOT_SOLVES], sp.roots);
+    }
+    for (int s2 = sp.ns + lane; s2 < m.s_max; s2 += kWave) {
+        st[s2] = INFINITY;
+        if (si) si[s2] = 0.0f;
+    }
 }
 
 // Sequential baseline: one thread per (sample, neuron), every event in order.
@@ -482,7 +688,19 @@ FwdLayout fwd_layout(int B, int E_max, int N)
     L.agg = take((size_t)B * L.S * N * sizeof(double2));
     L.carry = take((size_t)B * L.S * N * sizeof(double2));
     L.mask = take((size_t)B * L.S * N * sizeof(uint32_t));
-    L.subc = take((size_t)B * L.S * kSubPerSeg * N * sizeof(SubCarry));
+    int tiles = (N + kWave - 1) / kWave;
+    L.winfo = take((size_t)B * L.S * tiles * kSubPerSeg * sizeof(WaveInfo));
+    L.counters = take(256);
+    // Record pool: one record per flagged (sub-block, neuron).  Sized at a
+    // sixteenth of the dense bound (far above what spiking activity needs); a
+    // full pool only sends the excess sub-blocks through a slower re-walk.
+    size_t dense = (size_t)B * L.S * kSubPerSeg * N;
+    size_t cap = dense / 16 > 65536 ? dense / 16 : (dense < 65536 ? dense : 65536);
+    if (const char* env = getenv("LIF_POOL_CAP")) cap = (size_t)strtoull(env, nullptr, 10);
+    if (cap > 0xfffffff0ull) cap = 0xfffffff0ull;
+    L.pool_cap = cap;
+    L.pool = take(cap * sizeof(Record));
+    L.pool_ub = take(cap * sizeof(double));
     L.total = off + 256;
     return L;
 }
@@ -502,22 +720,25 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     double2* agg = (double2*)(base + L.agg);
     double2* carry = (double2*)(base + L.carry);
     uint32_t* mask = (uint32_t*)(base + L.mask);
-    SubCarry* subc = (SubCarry*)(base + L.subc);
+    WaveInfo* winfo = (WaveInfo*)(base + L.winfo);
+    uint32_t* pool_count = (uint32_t*)(base + L.counters);
+    Record* pool = (Record*)(base + L.pool);
+    double* pool_ub = (double*)(base + L.pool_ub);
 
     size_t nev = (size_t)B * E_max;
     size_t dec_threads = nev > LIF_STATUS_WORDS ? nev : LIF_STATUS_WORDS;
     TIMED_LAUNCH("decay", k_decay, dim3((unsigned)((dec_threads + 255) / 256)), dim3(256), 0, stream,
-                 ev_t, ev_n, B, E_max, L.S, m, dec, segm, status);
+                 ev_t, ev_n, B, E_max, L.S, m, dec, segm, status, pool_count);
     if ((p->flags & LIF_VALIDATE) && nev)
         TIMED_LAUNCH("validate", k_validate, dim3((unsigned)((nev + 255) / 256)), dim3(256), 0, stream,
                      ev_t, ev_src, ev_n, B, E_max, C_in, status);
     size_t nn = (size_t)B * N;
+    int tiles = (N + kWave - 1) / kWave;
     if (sequential) {
         TIMED_LAUNCH("sequential", k_sequential, dim3((unsigned)((nn + 63) / 64)), dim3(64), 0, stream,
                      ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, dec, out_t, out_n, out_i, status);
         return check_launch();
     }
-    int tiles = (N + kWave - 1) / kWave;
     size_t total = (size_t)B * L.S * tiles;
     if (total > 0x7fffffff) return LIF_ERR_SIZE;
     if (total) {
@@ -526,10 +747,13 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
         TIMED_LAUNCH("carry", k_carry, dim3((unsigned)((nn + 255) / 256)), dim3(256), 0, stream,
                      ev_n, B, E_max, N, L.S, segm, agg, carry);
         TIMED_LAUNCH("check", k_check, dim3((unsigned)total), dim3(kWave), 0, stream,
-                     ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, L.S, (int)total, m, dec, carry, mask, subc, status);
+                     ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, L.S, (int)total, m, dec, carry, mask, winfo,
+                     pool, pool_ub, pool_count, (uint32_t)L.pool_cap, status);
     }
-    TIMED_LAUNCH("resolve", k_resolve, dim3((unsigned)((nn + 255) / 256)), dim3(256), 0, stream,
-                 ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, L.S, m, dec, mask, subc, out_t, out_n, out_i, status);
+    if (nn > 0x7fffffff) return LIF_ERR_SIZE;
+    if (nn) TIMED_LAUNCH("resolve", k_resolve, dim3((unsigned)nn), dim3(kWave), 0, stream,
+                         ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, L.S, m, dec, carry, mask, winfo, pool,
+                         pool_ub, out_t, out_n, out_i, status);
     return check_launch();
 }
 

@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 
 #include "../../include/lif.h"
 #include "lif_common.hpp"
@@ -13,7 +14,8 @@ namespace lif {
 
 struct FwdLayout {
     int S;                                   // segments per sample
-    size_t dec, segm, agg, carry, mask, subc, total;
+    size_t dec, segm, agg, carry, mask, winfo, counters, pool, pool_ub, total;
+    size_t pool_cap;                         // records in the pool
 };
 FwdLayout fwd_layout(int B, int E_max, int N);
 
