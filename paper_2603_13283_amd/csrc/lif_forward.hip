@@ -69,38 +69,32 @@ __device__ __forceinline__ int xcd_remap(int wg, int total)
 // ---------------------------------------------------------------------------
 // k_decay
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_decay(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_n,
-                                               int B, int E_max, int S, Model m, Decay* __restrict__ dec,
-                                               Decay* __restrict__ segm, int32_t* __restrict__ status,
-                                               uint32_t* __restrict__ pool_count)
+// Decay record of event k (gap to the previous event, or to t = 0).
+__device__ __forceinline__ Decay make_decay(const Model& m, const float* __restrict__ t, int k)
 {
-    size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx < LIF_STATUS_WORDS && status) status[idx] = 0;
-    if (idx == 0 && pool_count) *pool_count = 0;
-    if (idx >= (size_t)B * (size_t)E_max) return;
-    int b = (int)(idx / (size_t)E_max), k = (int)(idx % (size_t)E_max);
-    int n = clamp_count(ev_n[b], E_max);
-    if (k >= n) return;
-    const float* t = ev_t + (size_t)b * E_max;
-    double tk = (double)t[k];
-    double tp = k > 0 ? (double)t[k - 1] : 0.0;
-    double dt = tk - tp;
+    double dt = (double)t[k] - (k > 0 ? (double)t[k - 1] : 0.0);
     Decay d;
     d.A = exp(-dt * m.inv_tm);
     d.D = exp(-dt * m.inv_ts);
     d.C = unit_kernel(m, dt, d.A);
     double gl = fmin(dt, m.t_peak);
     d.g = unit_kernel(m, gl, exp(-gl * m.inv_tm)) * (1.0 + 1e-12);
-    dec[idx] = d;
-    if (k % kSeg == 0) {
-        int k1 = min(k + kSeg, n);
-        double T = (double)t[k1 - 1] - tp;
-        Decay s;
-        s.A = exp(-T * m.inv_tm);
-        s.D = exp(-T * m.inv_ts);
-        s.C = unit_kernel(m, T, s.A);
-        s.g = T;
-        segm[(size_t)b * S + k / kSeg] = s;
+    return d;
+}
+
+__global__ __launch_bounds__(256) void k_decay(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_n,
+                                               int B, int E_max, int S, Model m, Decay* __restrict__ dec,
+                                               int32_t* __restrict__ status, uint32_t* __restrict__ counters)
+{
+    const size_t tid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    if (tid < LIF_STATUS_WORDS) status[tid] = 0;
+    if (tid < 2 && counters) counters[tid] = 0;
+    const size_t nev = (size_t)B * (size_t)E_max;
+    for (size_t idx = tid; idx < nev; idx += stride) {
+        int b = (int)(idx / (size_t)E_max), k = (int)(idx % (size_t)E_max);
+        if (k >= clamp_count(ev_n[b], E_max)) continue;
+        dec[idx] = make_decay(m, ev_t + (size_t)b * E_max, k);
     }
 }
 
@@ -124,83 +118,164 @@ __global__ __launch_bounds__(256) void k_validate(const float* __restrict__ ev_t
 }
 
 // ---------------------------------------------------------------------------
-// Walk of one segment from a given state: V <- A V + C I, I <- D I + w.
-// The event source and decay record are wave-uniform (scalar loads); the
-// weight load is a coalesced W^T row slice.  Events are consumed in batches
-// of kSub so the loads of a batch are in flight together.
+// Segment walks.  A workgroup of kTilesPerBlock waves takes one (sample,
+// segment) and kTilesPerBlock 64-neuron tiles; lanes are neurons.  The
+// segment's decay records are computed (k_aggregate) or fetched (k_check)
+// once into LDS and read by all of its waves.  Each event's source is
+// wave-uniform; lane j holds the sources of events j and j + 64 and each is
+// broadcast with a lane read, so the weight loads of the next kSub events
+// (one coalesced W^T row slice per event) are issued while the current kSub
+// events are walked.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(64) void k_aggregate(const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n,
-                                                  int E_max, const float* __restrict__ WT, int C_in, int N, int tiles, int S,
-                                                  int total, const Decay* __restrict__ dec,
-                                                  double2* __restrict__ agg)
+constexpr int kTilesPerBlock = 4;
+constexpr int kSrcRegs = kSeg / kWave;
+
+struct SegCoords {
+    int b, seg, tile, wave, lane, n, nc, nb, k0, cnt;
+};
+
+__device__ __forceinline__ SegCoords seg_coords(int total, int tgroups, int S, const int32_t* __restrict__ ev_n,
+                                                int E_max, int N)
 {
+    SegCoords c;
     int lin = xcd_remap(blockIdx.x, total);
-    int tile = lin % tiles;
-    int rest = lin / tiles;
-    int seg = rest % S;
-    int b = rest / S;
-    int nb = clamp_count(ev_n[b], E_max);
-    int k0 = seg * kSeg;
-    if (k0 >= nb) return;
-    int k1 = min(k0 + kSeg, nb);
-    int n = tile * kWave + (int)threadIdx.x;
-    int nc = min(n, N - 1);
-    const float* wcol = WT + nc;
-    const int32_t* src = ev_src + (size_t)b * E_max;
-    const Decay* d = dec + (size_t)b * E_max;
+    int tg = lin % tgroups;
+    int rest = lin / tgroups;
+    c.seg = rest % S;
+    c.b = rest / S;
+    c.wave = (int)threadIdx.x / kWave;
+    c.lane = (int)threadIdx.x % kWave;
+    c.tile = tg * kTilesPerBlock + c.wave;
+    c.n = c.tile * kWave + c.lane;
+    c.nc = min(c.n, N - 1);
+    c.nb = clamp_count(ev_n[c.b], E_max);
+    c.k0 = c.seg * kSeg;
+    c.cnt = min(kSeg, c.nb - c.k0);
+    return c;
+}
+
+struct SrcRegs {
+    int v[kSrcRegs];
+};
+
+__device__ __forceinline__ SrcRegs load_sources(const int32_t* __restrict__ src, int cnt, int lane, int C_in)
+{
+    SrcRegs r;
+#pragma unroll
+    for (int h = 0; h < kSrcRegs; ++h) r.v[h] = h * kWave + lane < cnt ? clamp_src(src[h * kWave + lane], C_in) : 0;
+    return r;
+}
+
+// Weights of events q*kSub .. q*kSub + kSub - 1 of the segment (0 past cnt).
+__device__ __forceinline__ void load_sub_weights(const SrcRegs& sr, const float* __restrict__ wcol, int N, int cnt,
+                                                 int q, float (&w)[kSub])
+{
+#pragma unroll
+    for (int j = 0; j < kSub; ++j) {
+        const int e = q * kSub + j;
+        int sj = __builtin_amdgcn_readlane(sr.v[e / kWave], e % kWave);
+        w[j] = e < cnt ? wcol[(size_t)sj * (size_t)N] : 0.0f;
+    }
+}
+
+__global__ __launch_bounds__(kWave * kTilesPerBlock) void k_aggregate(
+    const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
+    const float* __restrict__ WT, int C_in, int N, int tiles, int tgroups, int S, int total, Model m,
+    Decay* __restrict__ dec, Decay* __restrict__ segm, double2* __restrict__ agg, int32_t* __restrict__ status,
+    uint32_t* __restrict__ counters)
+{
+    __shared__ Decay sd[kSeg];
+    if (blockIdx.x == 0 && threadIdx.x < LIF_STATUS_WORDS) status[threadIdx.x] = 0;
+    if (blockIdx.x == 0 && threadIdx.x < 2) counters[threadIdx.x] = 0;
+    const SegCoords c = seg_coords(total, tgroups, S, ev_n, E_max, N);
+    if (c.k0 >= c.nb) return;                        // uniform over the workgroup
+    const float* tt = ev_t + (size_t)c.b * E_max;
+    const int tg = c.tile / kTilesPerBlock;
+    if ((int)threadIdx.x < c.cnt) {
+        int k = c.k0 + (int)threadIdx.x;
+        Decay e = make_decay(m, tt, k);
+        sd[threadIdx.x] = e;
+        if (tg == 0) dec[(size_t)c.b * E_max + k] = e;
+    }
+    if (tg == 0 && threadIdx.x == kSeg % (kWave * kTilesPerBlock)) {
+        // The segment's composed map M(T) (the maps form a semigroup).
+        double T = (double)tt[c.k0 + c.cnt - 1] - (c.k0 > 0 ? (double)tt[c.k0 - 1] : 0.0);
+        Decay sm;
+        sm.A = exp(-T * m.inv_tm);
+        sm.D = exp(-T * m.inv_ts);
+        sm.C = unit_kernel(m, T, sm.A);
+        sm.g = T;
+        segm[(size_t)c.b * S + c.seg] = sm;
+    }
+    __syncthreads();
+    if (c.tile >= tiles) return;
+    const float* wcol = WT + c.nc;
+    const SrcRegs sr = load_sources(ev_src + (size_t)c.b * E_max + c.k0, c.cnt, c.lane, C_in);
     double V = 0.0, I = 0.0;
-    int k = k0;
-    for (; k + kSub <= k1; k += kSub) {
-        float w[kSub];
+    float wn[kSub];
+    load_sub_weights(sr, wcol, N, c.cnt, 0, wn);
 #pragma unroll
-        for (int j = 0; j < kSub; ++j) w[j] = wcol[(size_t)clamp_src(src[k + j], C_in) * (size_t)N];
+    for (int q = 0; q < kSubPerSeg; ++q) {
+        if (q * kSub < c.cnt) {
+            float w[kSub];
 #pragma unroll
-        for (int j = 0; j < kSub; ++j) {
-            Decay e = d[k + j];
-            double Vn = e.A * V + e.C * I;
-            I = e.D * I + (double)w[j];
-            V = Vn;
+            for (int j = 0; j < kSub; ++j) w[j] = wn[j];
+            if (q + 1 < kSubPerSeg && (q + 1) * kSub < c.cnt) load_sub_weights(sr, wcol, N, c.cnt, q + 1, wn);
+#pragma unroll
+            for (int j = 0; j < kSub; ++j) {
+                if (q * kSub + j < c.cnt) {
+                    Decay e = sd[q * kSub + j];
+                    double Vn = e.A * V + e.C * I;
+                    I = e.D * I + (double)w[j];
+                    V = Vn;
+                }
+            }
         }
     }
-    for (; k < k1; ++k) {
-        float w = wcol[(size_t)clamp_src(src[k], C_in) * (size_t)N];
-        Decay e = d[k];
-        double Vn = e.A * V + e.C * I;
-        I = e.D * I + (double)w;
-        V = Vn;
-    }
-    if (n < N) agg[((size_t)b * S + seg) * N + n] = make_double2(V, I);
+    if (c.n < N) agg[((size_t)c.b * S + c.seg) * N + c.n] = make_double2(V, I);
 }
 
 // Exclusive scan over segments of the Combine of Eq. affine:
 // s_in(j+1) = M(T_j) s_in(j) + b_j, with s_in(0) = (0, 0).  The segment
 // aggregates are fetched kCarryBatch at a time so their loads overlap.
-constexpr int kCarryBatch = 8;
+constexpr int kCarryBatch = 16;
 
 __global__ __launch_bounds__(256) void k_carry(const int32_t* __restrict__ ev_n, int B, int E_max, int N, int S,
                                                const Decay* __restrict__ segm, const double2* __restrict__ agg,
-                                               double2* __restrict__ carry)
+                                               double2* __restrict__ carry, int32_t* __restrict__ status,
+                                               int s_max, float* __restrict__ out_t, int32_t* __restrict__ out_n,
+                                               float* __restrict__ out_i, uint32_t* __restrict__ listed)
 {
     size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= (size_t)B * (size_t)N) return;
+    const size_t nn = (size_t)B * (size_t)N;
+    if (idx >= nn) return;
     int b = (int)(idx / (size_t)N), n = (int)(idx % (size_t)N);
-    int Sb = (clamp_count(ev_n[b], E_max) + kSeg - 1) / kSeg;
+    // Every neuron starts with no spike (+inf times); the resolve pass
+    // overwrites the outputs of neurons that fire.  Coalesced fill.
+    for (size_t i = idx; i < nn * (size_t)s_max; i += nn) {
+        out_t[i] = INFINITY;
+        if (out_i) out_i[i] = 0.0f;
+    }
+    out_n[idx] = 0;
+    listed[idx] = 0u;
+    int nb = clamp_count(ev_n[b], E_max);
+    if (n == 0) atomicAdd(&status[LIF_ST_EVENTS], nb);
+    int Sb = (nb + kSeg - 1) / kSeg;
     double V = 0.0, I = 0.0;
     for (int j0 = 0; j0 < Sb; j0 += kCarryBatch) {
         double2 a[kCarryBatch];
-        Decay M[kCarryBatch];
 #pragma unroll
         for (int j = 0; j < kCarryBatch; ++j) {
             int jj = min(j0 + j, Sb - 1);
             a[j] = agg[((size_t)b * S + jj) * N + n];
-            M[j] = segm[(size_t)b * S + jj];
         }
 #pragma unroll
         for (int j = 0; j < kCarryBatch; ++j) {
             if (j0 + j < Sb) {
+                Decay M = segm[(size_t)b * S + j0 + j];
                 carry[((size_t)b * S + j0 + j) * N + n] = make_double2(V, I);
-                double Vn = M[j].A * V + M[j].C * I + a[j].x;
-                I = M[j].D * I + a[j].y;
+                double Vn = M.A * V + M.C * I + a[j].x;
+                I = M.D * I + a[j].y;
                 V = Vn;
             }
         }
@@ -214,99 +289,107 @@ __global__ __launch_bounds__(256) void k_carry(const int32_t* __restrict__ ev_n,
 // term), so a sub-block whose no-reset bound stays below the threshold holds
 // no spike whatever happened before it.  Sub-blocks whose bound reaches it
 // get a record for the resolve pass, which applies the exact interval rule.
-__global__ __launch_bounds__(64) void k_check(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src,
-                                              const int32_t* __restrict__ ev_n, int E_max,
-                                              const float* __restrict__ WT, int C_in, int N, int tiles, int S,
-                                              int total, Model m, const Decay* __restrict__ dec,
-                                              const double2* __restrict__ carry, uint32_t* __restrict__ mask,
-                                              WaveInfo* __restrict__ winfo, Record* __restrict__ pool,
-                                              double* __restrict__ pool_ub, uint32_t* __restrict__ pool_count,
-                                              uint32_t pool_cap, int32_t* __restrict__ status)
+__global__ __launch_bounds__(kWave * kTilesPerBlock) void k_check(
+    const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
+    const float* __restrict__ WT, int C_in, int N, int tiles, int tgroups, int S, int total, Model m,
+    const Decay* __restrict__ dec, const double2* __restrict__ carry, uint32_t* __restrict__ mask,
+    WaveInfo* __restrict__ winfo, Record* __restrict__ pool, double* __restrict__ pool_ub,
+    uint32_t* __restrict__ pool_count, uint32_t pool_cap, uint32_t* __restrict__ listed, uint32_t* __restrict__ work,
+    uint32_t* __restrict__ nwork, int32_t* __restrict__ status)
 {
-    int lin = xcd_remap(blockIdx.x, total);
-    int tile = lin % tiles;
-    int rest = lin / tiles;
-    int seg = rest % S;
-    int b = rest / S;
-    int nb = clamp_count(ev_n[b], E_max);
-    int k0 = seg * kSeg;
-    if (k0 >= nb) return;
-    int k1 = min(k0 + kSeg, nb);
-    const int lane = (int)threadIdx.x;
-    int n = tile * kWave + lane;
-    int nc = min(n, N - 1);
-    const float* wcol = WT + nc;
-    const float* tt = ev_t + (size_t)b * E_max;
-    const int32_t* src = ev_src + (size_t)b * E_max;
-    const Decay* d = dec + (size_t)b * E_max;
-    size_t row = ((size_t)b * S + seg) * N;
-    double2 c0 = carry[row + nc];
+    __shared__ Decay sd[kSeg];
+    const SegCoords c = seg_coords(total, tgroups, S, ev_n, E_max, N);
+    if (c.k0 >= c.nb) return;                        // uniform over the workgroup
+    const float* tt = ev_t + (size_t)c.b * E_max;
+    if ((int)threadIdx.x < c.cnt) sd[threadIdx.x] = dec[(size_t)c.b * E_max + c.k0 + threadIdx.x];
+    __syncthreads();
+    if (c.tile >= tiles) return;
+    const int lane = c.lane, n = c.n, nb = c.nb, k0 = c.k0, cnt_seg = c.cnt;
+    const float* wcol = WT + c.nc;
+    const SrcRegs sr = load_sources(ev_src + (size_t)c.b * E_max + k0, cnt_seg, lane, C_in);
+    const size_t row = ((size_t)c.b * S + c.seg) * N;
+    double2 c0 = carry[row + c.nc];
     double V = c0.x, I = c0.y;
     uint32_t msk = 0;
     int ncand = 0;
     const unsigned long long below = (1ull << lane) - 1ull;
+    float wn[kSub];
+    load_sub_weights(sr, wcol, N, cnt_seg, 0, wn);
+#pragma unroll
     for (int q = 0; q < kSubPerSeg; ++q) {
-        int kq0 = k0 + q * kSub;
-        if (kq0 >= k1) break;
-        int cnt = min(kSub, k1 - kq0);
-        double Vin = V, Iin = I, ub = -INFINITY;
-        float w[kSub];
-        double Vs[kSub], Is[kSub];
+        if (q * kSub < cnt_seg) {
+            const int cnt = min(kSub, cnt_seg - q * kSub);
+            float w[kSub];
 #pragma unroll
-        for (int j = 0; j < kSub; ++j) w[j] = j < cnt ? wcol[(size_t)clamp_src(src[kq0 + j], C_in) * (size_t)N] : 0.0f;
+            for (int j = 0; j < kSub; ++j) w[j] = wn[j];
+            if (q + 1 < kSubPerSeg && (q + 1) * kSub < cnt_seg) load_sub_weights(sr, wcol, N, cnt_seg, q + 1, wn);
+            double Vin = V, Iin = I, ub = -INFINITY;
 #pragma unroll
-        for (int j = 0; j < kSub; ++j) {
-            if (j < cnt) {
-                Decay e = d[kq0 + j];
-                ub = fmax(ub, fmax(V, 0.0) + fmax(I, 0.0) * e.g);
-                double Vn = e.A * V + e.C * I;
-                I = e.D * I + (double)w[j];
-                V = Vn;
-            }
-            Vs[j] = V;
-            Is[j] = I;
-        }
-        if (kq0 + cnt == nb) {
-            // Interval after the last event, up to t_end (default +inf).
-            double len = m.t_end - (double)tt[nb - 1];
-            if (len > 0.0) {
-                double gl = fmin(len, m.t_peak);
-                double g = unit_kernel(m, gl, exp(-gl * m.inv_tm)) * (1.0 + 1e-12);
-                ub = fmax(ub, fmax(V, 0.0) + fmax(I, 0.0) * g);
-            }
-        }
-        bool surv = ub >= m.th_lo && n < N;
-        unsigned long long lanes = __ballot(surv);
-        if (lanes) {
-            int cntl = __popcll(lanes);
-            uint32_t base = 0;
-            if (lane == 0) base = atomicAdd(pool_count, (uint32_t)cntl);
-            base = __shfl(base, 0, kWave);
-            bool ok = (unsigned long long)base + (unsigned long long)cntl <= (unsigned long long)pool_cap;
-            if (lane == 0) {
-                WaveInfo wi;
-                wi.lanes = lanes;
-                wi.base = ok ? base : kNoSlot;
-                wi.pad = 0;
-                winfo[(((size_t)b * S + seg) * tiles + tile) * kSubPerSeg + q] = wi;
-            }
-            if (surv) {
-                if (ok) {
-                    uint32_t slot = base + (uint32_t)__popcll(lanes & below);
-                    pool_ub[slot] = ub;
-                    Record* r = pool + slot;
-                    r->s[0] = make_double2(Vin, Iin);
-#pragma unroll
-                    for (int j = 0; j < kSub; ++j) r->s[j + 1] = make_double2(Vs[j], Is[j]);
+            for (int j = 0; j < kSub; ++j) {
+                if (j < cnt) {
+                    Decay e = sd[q * kSub + j];
+                    ub = fmax(ub, fmax(V, 0.0) + fmax(I, 0.0) * e.g);
+                    double Vn = e.A * V + e.C * I;
+                    I = e.D * I + (double)w[j];
+                    V = Vn;
                 }
-                msk |= 1u << q;
-                ++ncand;
+            }
+            if (k0 + q * kSub + cnt == nb) {
+                // Interval after the last event, up to t_end (default +inf).
+                double len = m.t_end - (double)tt[nb - 1];
+                if (len > 0.0) {
+                    double gl = fmin(len, m.t_peak);
+                    double g = unit_kernel(m, gl, exp(-gl * m.inv_tm)) * (1.0 + 1e-12);
+                    ub = fmax(ub, fmax(V, 0.0) + fmax(I, 0.0) * g);
+                }
+            }
+            bool surv = ub >= m.th_lo && n < N;
+            unsigned long long lanes = __ballot(surv);
+            if (lanes) {
+                int cntl = __popcll(lanes);
+                uint32_t base = 0;
+                if (lane == 0) base = atomicAdd(pool_count, (uint32_t)cntl);
+                base = __shfl(base, 0, kWave);
+                bool ok = (unsigned long long)base + (unsigned long long)cntl <= (unsigned long long)pool_cap;
+                if (lane == 0) {
+                    WaveInfo wi;
+                    wi.lanes = lanes;
+                    wi.base = ok ? base : kNoSlot;
+                    wi.pad = 0;
+                    winfo[(((size_t)c.b * S + c.seg) * tiles + c.tile) * kSubPerSeg + q] = wi;
+                }
+                if (surv) {
+                    if (ok) {
+                        // Re-walk the sub-block to store its states.
+                        uint32_t slot = base + (uint32_t)__popcll(lanes & below);
+                        pool_ub[slot] = ub;
+                        Record* r = pool + slot;
+                        r->s[0] = make_double2(Vin, Iin);
+                        double Vr = Vin, Ir = Iin;
+#pragma unroll
+                        for (int j = 0; j < kSub; ++j) {
+                            if (j < cnt) {
+                                Decay e = sd[q * kSub + j];
+                                double Vn = e.A * Vr + e.C * Ir;
+                                Ir = e.D * Ir + (double)w[j];
+                                Vr = Vn;
+                            }
+                            r->s[j + 1] = make_double2(Vr, Ir);
+                        }
+                    }
+                    msk |= 1u << q;
+                    ++ncand;
+                }
             }
         }
     }
     if (n < N) {
         mask[row + n] = msk;
-        if (ncand) atomicAdd(&status[LIF_ST_CAND_BLOCKS], ncand);
+        if (ncand) {
+            atomicAdd(&status[LIF_ST_CAND_BLOCKS], ncand);
+            size_t bn = (size_t)c.b * N + n;
+            if (atomicOr(&listed[bn], 1u) == 0u) work[atomicAdd(nwork, 1u)] = (uint32_t)bn;
+        }
     }
 }
 
@@ -409,18 +492,26 @@ __device__ __noinline__ double2 entering_state(const double2* __restrict__ carry
     return make_double2(V, I);
 }
 
-// Resolve pass: one wave per (sample, neuron), the paper's chunked
-// speculative scheme applied to the neuron's flagged sub-blocks only.
-// kGroup flagged sub-blocks are staged in LDS (kSub lanes each, one lane per
-// interval).  Since every reset subtracts (V_th - V_reset) e^{-(t - t_s)/tm}
-// from the no-reset trajectory, the true state entering interval k is the
-// record's no-reset state minus the reset deficit at t_{k-1}; all intervals
-// of the group are tested at once with the interval rule, the earliest
-// crossing (ballot) is solved by its lane with bracketed Newton, reset and
-// re-tested until its interval is clear, the deficit is updated and the
-// later intervals are tested again.  Intervals before the first flagged
-// sub-block, and between flagged sub-blocks, provably hold no spike.
+// Resolve pass: one wave per neuron that has flagged sub-blocks (a work
+// list built by the check pass); the paper's chunked speculative scheme
+// applied to those sub-blocks only.
+//   * Flagged sub-blocks are taken in time order in windows of kWin.  A
+//     window's records (no-reset states), decays and event times are staged
+//     in LDS with one batch of loads (one lane per sub-block).
+//   * Since every reset subtracts (V_th - V_reset) e^{-(t - t_s)/tm} from
+//     the no-reset trajectory, the true state entering an interval is the
+//     record's no-reset state minus the reset deficit at its start.  A
+//     sub-block whose no-reset bound minus the deficit at its end stays
+//     below the threshold is certified at once (more spikes only deepen the
+//     deficit); this test runs for the whole window in parallel.
+//   * The earliest kGroup uncertified sub-blocks are checked together, one
+//     lane per interval, with the interval rule; the earliest crossing
+//     (ballot) is solved by its lane with bracketed Newton, reset and
+//     re-tested until its interval is clear, the deficit is updated and the
+//     later intervals are tested again.
+// Intervals outside flagged sub-blocks provably hold no spike.
 constexpr int kGroup = kWave / kSub;
+constexpr int kWin = 32;
 
 // Wave-uniform spike bookkeeping of the neuron being resolved.
 struct NeuronSpikes {
@@ -434,28 +525,36 @@ __device__ __forceinline__ double deficit_at(const NeuronSpikes& ns_, const Mode
     return ns_.ns > 0 ? ns_.dref * exp(-(t - ns_.tref) * m.inv_tm) : 0.0;
 }
 
-__global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src,
-                                                   const int32_t* __restrict__ ev_n, int E_max,
-                                                   const float* __restrict__ WT, int C_in, int N, int tiles, int S,
-                                                   Model m, const Decay* __restrict__ dec,
-                                                   const double2* __restrict__ carry,
-                                                   const uint32_t* __restrict__ mask,
-                                                   const WaveInfo* __restrict__ winfo,
-                                                   const Record* __restrict__ pool,
-                                                   const double* __restrict__ pool_ub, float* __restrict__ out_t,
-                                                   int32_t* __restrict__ out_n, float* __restrict__ out_i,
-                                                   int32_t* __restrict__ status)
+__device__ __forceinline__ void share_from(NeuronSpikes& sp, int from)
 {
-    __shared__ double2 stg[kGroup][kSub + 1];
-    __shared__ int g_seg[kGroup], g_q[kGroup];
-    __shared__ int w_seg[kWave], w_q[kWave];
-    const int b = blockIdx.x / N;
-    const int n = blockIdx.x % N;
+    sp.ns = __shfl(sp.ns, from, kWave);
+    sp.roots = __shfl(sp.roots, from, kWave);
+    sp.dref = __shfl(sp.dref, from, kWave);
+    sp.tref = __shfl(sp.tref, from, kWave);
+    sp.capped = __shfl((int)sp.capped, from, kWave) != 0;
+}
+
+struct ResolveLds {
+    double2 s[kWin][kSub + 1];   // no-reset states: entering, then after each event
+    Decay e[kWin][kSub];         // decays of the sub-block's events
+    float t[kWin][kSub + 1];     // time before the sub-block, then each event's time
+    int seg[kWin], q[kWin];      // the window's sub-blocks
+    int grp[kGroup];             // window slots of the group being checked
+};
+
+__device__ void resolve_neuron(ResolveLds& sh, int b, int n, const float* __restrict__ ev_t,
+                               const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
+                               const float* __restrict__ WT, int C_in, int N, int tiles, int S, const Model& m,
+                               const Decay* __restrict__ dec, const double2* __restrict__ carry,
+                               const uint32_t* __restrict__ mask, const WaveInfo* __restrict__ winfo,
+                               const Record* __restrict__ pool, const double* __restrict__ pool_ub,
+                               float* __restrict__ out_t, int32_t* __restrict__ out_n, float* __restrict__ out_i,
+                               int32_t* __restrict__ status)
+{
     const int tile = n / kWave;
     const unsigned long long below_n = (1ull << (n % kWave)) - 1ull;
     const int lane = (int)threadIdx.x;
     const int nb = clamp_count(ev_n[b], E_max);
-    if (n == 0 && lane == 0) atomicAdd(&status[LIF_ST_EVENTS], nb);
     const float* tt = ev_t + (size_t)b * E_max;
     const int32_t* src = ev_src + (size_t)b * E_max;
     const Decay* d = dec + (size_t)b * E_max;
@@ -465,144 +564,127 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
     NeuronSpikes sp{0, 0, 0.0, 0.0, false};
     int walked = 0, fallback = 0;
     const int Sb = (nb + kSeg - 1) / kSeg;
-    int G = 0;
+    int W = 0;
 
-    auto process_group = [&]() {
-        __syncthreads();                      // g_seg / g_q written by lane 0
-        // ---- stage the group's no-reset states in LDS
-        for (int r = 0; r < G; ++r) {
-            int seg = g_seg[r], q = g_q[r];
+    auto process_window = [&]() {
+        __syncthreads();                                  // window list written by lane 0
+        // ---- stage: lane c loads sub-block c's record, decays and times
+        bool done = lane >= W;
+        double ub = 0.0, t_out = 0.0;
+        int cnt_c = 0;
+        if (!done) {
+            int seg = sh.seg[lane], q = sh.q[lane];
             int kq0 = seg * kSeg + q * kSub;
+            cnt_c = min(kSub, nb - kq0);
             WaveInfo wi = winfo[(((size_t)b * S + seg) * tiles + tile) * kSubPerSeg + q];
+            sh.t[lane][0] = kq0 > 0 ? tt[kq0 - 1] : 0.0f;
+            for (int j = 0; j < kSub; ++j) {
+                int k = min(kq0 + j, nb - 1);
+                sh.e[lane][j] = d[k];
+                sh.t[lane][j + 1] = tt[k];
+            }
             if (wi.base != kNoSlot) {
-                const Record* rec = pool + wi.base + (uint32_t)__popcll(wi.lanes & below_n);
-                if (lane <= kSub) stg[r][lane] = rec->s[lane];
+                uint32_t slot = wi.base + (uint32_t)__popcll(wi.lanes & below_n);
+                ub = pool_ub[slot];
+                const Record* rec = pool + slot;
+                for (int j = 0; j <= kSub; ++j) sh.s[lane][j] = rec->s[j];
             } else {
-                if (lane == 0) {
-                    size_t row = ((size_t)b * S + seg) * N;
-                    double2 cs = entering_state(carry, row, n, seg * kSeg, kq0, src, d, WT, C_in, N);
-                    double V = cs.x, I = cs.y;
-                    stg[r][0] = cs;
-                    int cnt = min(kSub, nb - kq0);
-                    for (int j = 0; j < cnt; ++j) {
+                size_t row = ((size_t)b * S + seg) * N;
+                double2 cs = entering_state(carry, row, n, seg * kSeg, kq0, src, d, WT, C_in, N);
+                double V = cs.x, I = cs.y;
+                sh.s[lane][0] = cs;
+                for (int j = 0; j < kSub; ++j) {
+                    if (j < cnt_c) {
                         Decay e = d[kq0 + j];
                         double Vn = e.A * V + e.C * I;
                         I = e.D * I + (double)WT[(size_t)clamp_src(src[kq0 + j], C_in) * (size_t)N + n];
                         V = Vn;
-                        stg[r][j + 1] = make_double2(V, I);
                     }
+                    sh.s[lane][j + 1] = make_double2(V, I);
                 }
-                ++fallback;
+                ub = INFINITY;
             }
+            double tl = (double)tt[kq0 + cnt_c - 1];
+            t_out = kq0 + cnt_c == nb ? fmax(m.t_end, tl) : tl;
         }
+        fallback += __popcll(__ballot(ub == INFINITY && lane < W));
         __syncthreads();
-        walked += G;
-        // ---- this lane's interval: the one before event k of sub-block r
-        const int r = lane / kSub, j = lane % kSub;
-        int kq0 = 0, cnt = 0;
-        if (r < G) { kq0 = g_seg[r] * kSeg + g_q[r] * kSub; cnt = min(kSub, nb - kq0); }
-        const bool valid = r < G && j < cnt;
-        const int k = valid ? kq0 + j : 0;
-        const Decay e = valid ? d[k] : Decay{1.0, 0.0, 1.0, 0.0};
-        const double t1 = valid ? (double)tt[k] : 0.0;
-        const double t0 = valid && k > 0 ? (double)tt[k - 1] : 0.0;
-        const double2 s0 = valid ? stg[r][j] : make_double2(0.0, 0.0);
-        const double2 s1 = valid ? stg[r][j + 1] : make_double2(0.0, 0.0);
-        bool pending = valid && t1 > t0;
         while (!sp.capped) {
-            bool cross = false;
-            double V0 = 0.0, I0 = 0.0;
-            if (pending) {
-                double def0 = deficit_at(sp, m, t0);
-                V0 = s0.x - def0;
-                I0 = s0.y;
-                double u = fmax(V0, 0.0) + fmax(I0, 0.0) * e.g;
-                if (u >= m.th_lo) {
-                    double vend = s1.x - def0 * e.A;
-                    cross = interval_rule(m, V0, I0, t1 - t0, e.A, e.D, vend, m.th).hit;
-                }
-            }
-            unsigned long long cm = __ballot(cross);
-            if (!cm) break;
-            const int kl = __ffsll((long long)cm) - 1;
-            if (lane == kl) {
-                Sink sk;
-                sk.st = st; sk.si = si;
-                sk.ns = sp.ns; sk.roots = sp.roots; sk.dref = sp.dref; sk.tref = sp.tref;
-                double V = V0, I = I0, tc = t0;
-                bool ok = advance_interval(m, V, I, tc, t1, &e, sk);
-                sp.ns = sk.ns; sp.roots = sk.roots; sp.dref = sk.dref; sp.tref = sk.tref;
-                sp.capped = !ok;
-            }
-            sp.ns = __shfl(sp.ns, kl, kWave);
-            sp.roots = __shfl(sp.roots, kl, kWave);
-            sp.dref = __shfl(sp.dref, kl, kWave);
-            sp.tref = __shfl(sp.tref, kl, kWave);
-            sp.capped = __shfl((int)sp.capped, kl, kWave) != 0;
-            if (lane <= kl) pending = false;
-        }
-        // ---- the open interval after the stream's last event
-        if (!sp.capped && G > 0) {
-            int rl = G - 1;
-            int kql = g_seg[rl] * kSeg + g_q[rl] * kSub;
-            int cl = min(kSub, nb - kql);
-            if (kql + cl == nb && lane == 0) {
-                double tl = (double)tt[nb - 1];
-                double2 sl = stg[rl][cl];
-                Sink sk;
-                sk.st = st; sk.si = si;
-                sk.ns = sp.ns; sk.roots = sp.roots; sk.dref = sp.dref; sk.tref = sp.tref;
-                double V = sl.x - deficit_at(sp, m, tl), I = sl.y, tc = tl;
-                bool ok = advance_interval(m, V, I, tc, m.t_end, nullptr, sk);
-                sp.ns = sk.ns; sp.roots = sk.roots; sp.dref = sk.dref; sp.tref = sk.tref;
-                sp.capped = !ok;
-            }
-            sp.ns = __shfl(sp.ns, 0, kWave);
-            sp.roots = __shfl(sp.roots, 0, kWave);
-            sp.dref = __shfl(sp.dref, 0, kWave);
-            sp.tref = __shfl(sp.tref, 0, kWave);
-            sp.capped = __shfl((int)sp.capped, 0, kWave) != 0;
-        }
-        __syncthreads();
-        G = 0;
-    };
-
-    // Flagged sub-blocks are gathered in windows of up to kWave (one lane
-    // each).  Every pass over a window first certifies, in parallel, the
-    // sub-blocks whose no-reset bound minus the current reset deficit at
-    // their end stays below the threshold (more spikes only deepen the
-    // deficit, so certification is final), then resolves the earliest kGroup
-    // uncertified ones.
-    int W = 0;
-    auto process_window = [&]() {
-        __syncthreads();                      // w_seg / w_q written by lane 0
-        bool done = lane >= W;
-        double ub = 0.0, t_out = 0.0;
-        if (!done) {
-            int seg = w_seg[lane], q = w_q[lane];
-            int kq0 = seg * kSeg + q * kSub;
-            int cnt = min(kSub, nb - kq0);
-            WaveInfo wi = winfo[(((size_t)b * S + seg) * tiles + tile) * kSubPerSeg + q];
-            ub = wi.base != kNoSlot ? pool_ub[wi.base + (uint32_t)__popcll(wi.lanes & below_n)] : INFINITY;
-            double tl = (double)tt[kq0 + cnt - 1];
-            t_out = kq0 + cnt == nb ? fmax(m.t_end, tl) : tl;
-        }
-        while (!sp.capped) {
+            // ---- certify in parallel with the current deficit
             if (!done && sp.ns > 0) {
                 double def_out = isinf(t_out) ? 0.0 : deficit_at(sp, m, t_out);
                 if (ub - def_out < m.th_lo) done = true;
             }
             unsigned long long rem = __ballot(!done);
             if (!rem) break;
-            G = 0;
+            // ---- the earliest kGroup uncertified sub-blocks form the group
+            int G = 0;
             while (rem && G < kGroup) {
                 int c = __ffsll((long long)rem) - 1;
                 rem &= rem - 1ull;
-                if (lane == 0) { g_seg[G] = w_seg[c]; g_q[G] = w_q[c]; }
+                if (lane == 0) sh.grp[G] = c;
                 if (lane == c) done = true;
                 ++G;
             }
-            process_group();
+            __syncthreads();
+            walked += G;
+            const int r = lane / kSub, j = lane % kSub;
+            const int c = r < G ? sh.grp[r] : 0;
+            int kq0 = 0, cnt = 0;
+            if (r < G) { kq0 = sh.seg[c] * kSeg + sh.q[c] * kSub; cnt = min(kSub, nb - kq0); }
+            const bool valid = r < G && j < cnt;
+            const Decay e = valid ? sh.e[c][j] : Decay{1.0, 0.0, 1.0, 0.0};
+            const double t0 = valid ? (double)sh.t[c][j] : 0.0;
+            const double t1 = valid ? (double)sh.t[c][j + 1] : 0.0;
+            const double2 s0 = valid ? sh.s[c][j] : make_double2(0.0, 0.0);
+            const double2 s1 = valid ? sh.s[c][j + 1] : make_double2(0.0, 0.0);
+            bool pending = valid && t1 > t0;
+            while (!sp.capped) {
+                bool cross = false;
+                double V0 = 0.0, I0 = 0.0;
+                if (pending) {
+                    double def0 = deficit_at(sp, m, t0);
+                    V0 = s0.x - def0;
+                    I0 = s0.y;
+                    double u = fmax(V0, 0.0) + fmax(I0, 0.0) * e.g;
+                    if (u >= m.th_lo) cross = interval_rule(m, V0, I0, t1 - t0, e.A, e.D, s1.x - def0 * e.A, m.th).hit;
+                }
+                unsigned long long cm = __ballot(cross);
+                if (!cm) break;
+                const int kl = __ffsll((long long)cm) - 1;
+                if (lane == kl) {
+                    Sink sk;
+                    sk.st = st; sk.si = si;
+                    sk.ns = sp.ns; sk.roots = sp.roots; sk.dref = sp.dref; sk.tref = sp.tref;
+                    double V = V0, I = I0, tc = t0;
+                    bool ok = advance_interval(m, V, I, tc, t1, &e, sk);
+                    sp.ns = sk.ns; sp.roots = sk.roots; sp.dref = sk.dref; sp.tref = sk.tref;
+                    sp.capped = !ok;
+                }
+                share_from(sp, kl);
+                if (lane <= kl) pending = false;
+            }
+            // ---- the open interval after the stream's last event
+            if (!sp.capped) {
+                const int cl = sh.grp[G - 1];
+                int kql = sh.seg[cl] * kSeg + sh.q[cl] * kSub;
+                int cntl = min(kSub, nb - kql);
+                if (kql + cntl == nb) {
+                    if (lane == 0) {
+                        double tl = (double)sh.t[cl][cntl];
+                        double2 sl = sh.s[cl][cntl];
+                        Sink sk;
+                        sk.st = st; sk.si = si;
+                        sk.ns = sp.ns; sk.roots = sp.roots; sk.dref = sp.dref; sk.tref = sp.tref;
+                        double V = sl.x - deficit_at(sp, m, tl), I = sl.y, tc = tl;
+                        bool ok = advance_interval(m, V, I, tc, m.t_end, nullptr, sk);
+                        sp.ns = sk.ns; sp.roots = sk.roots; sp.dref = sk.dref; sp.tref = sk.tref;
+                        sp.capped = !ok;
+                    }
+                    share_from(sp, 0);
+                }
+            }
+            __syncthreads();
         }
         __syncthreads();
         W = 0;
@@ -619,9 +701,9 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
             while (mm && !sp.capped) {
                 int q = __builtin_ctz(mm);
                 mm &= mm - 1u;
-                if (lane == 0) { w_seg[W] = seg0 + l; w_q[W] = q; }
+                if (lane == 0) { sh.seg[W] = seg0 + l; sh.q[W] = q; }
                 ++W;
-                if (W == kWave) process_window();
+                if (W == kWin) process_window();
             }
         }
     }
@@ -638,9 +720,30 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
         if (sp.ns) atomicAdd(&status[LIF_ST_SPIKES], sp.ns);
         if (sp.roots) atomicAdd(&status[LIF_ST_ROOT_SOLVES], sp.roots);
     }
-    for (int s2 = sp.ns + lane; s2 < m.s_max; s2 += kWave) {
-        st[s2] = INFINITY;
-        if (si) si[s2] = 0.0f;
+    __syncthreads();
+}
+
+// Work-list driven: every wave takes neurons from the list built by k_check
+// until the list is exhausted.
+__global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src,
+                                                   const int32_t* __restrict__ ev_n, int E_max,
+                                                   const float* __restrict__ WT, int C_in, int N, int tiles, int S,
+                                                   Model m, const Decay* __restrict__ dec,
+                                                   const double2* __restrict__ carry,
+                                                   const uint32_t* __restrict__ mask,
+                                                   const WaveInfo* __restrict__ winfo,
+                                                   const Record* __restrict__ pool,
+                                                   const double* __restrict__ pool_ub,
+                                                   const uint32_t* __restrict__ work, const uint32_t* __restrict__ nwork,
+                                                   float* __restrict__ out_t, int32_t* __restrict__ out_n,
+                                                   float* __restrict__ out_i, int32_t* __restrict__ status)
+{
+    __shared__ ResolveLds sh;
+    const uint32_t count = *nwork;
+    for (uint32_t w = blockIdx.x; w < count; w += gridDim.x) {
+        uint32_t bn = work[w];
+        resolve_neuron(sh, (int)(bn / (uint32_t)N), (int)(bn % (uint32_t)N), ev_t, ev_src, ev_n, E_max, WT, C_in, N,
+                       tiles, S, m, dec, carry, mask, winfo, pool, pool_ub, out_t, out_n, out_i, status);
     }
 }
 
@@ -691,6 +794,8 @@ FwdLayout fwd_layout(int B, int E_max, int N)
     int tiles = (N + kWave - 1) / kWave;
     L.winfo = take((size_t)B * L.S * tiles * kSubPerSeg * sizeof(WaveInfo));
     L.counters = take(256);
+    L.listed = take((size_t)B * N * sizeof(uint32_t));
+    L.work = take((size_t)B * N * sizeof(uint32_t));
     // Record pool: one record per flagged (sub-block, neuron).  Sized at a
     // sixteenth of the dense bound (far above what spiking activity needs); a
     // full pool only sends the excess sub-blocks through a slower re-walk.
@@ -722,38 +827,50 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     uint32_t* mask = (uint32_t*)(base + L.mask);
     WaveInfo* winfo = (WaveInfo*)(base + L.winfo);
     uint32_t* pool_count = (uint32_t*)(base + L.counters);
+    uint32_t* nwork = pool_count + 1;
+    uint32_t* listed = (uint32_t*)(base + L.listed);
+    uint32_t* work = (uint32_t*)(base + L.work);
     Record* pool = (Record*)(base + L.pool);
     double* pool_ub = (double*)(base + L.pool_ub);
 
     size_t nev = (size_t)B * E_max;
-    size_t dec_threads = nev > LIF_STATUS_WORDS ? nev : LIF_STATUS_WORDS;
-    TIMED_LAUNCH("decay", k_decay, dim3((unsigned)((dec_threads + 255) / 256)), dim3(256), 0, stream,
-                 ev_t, ev_n, B, E_max, L.S, m, dec, segm, status, pool_count);
+    size_t nn = (size_t)B * N;
+    int tiles = (N + kWave - 1) / kWave;
+    int tgroups = (tiles + kTilesPerBlock - 1) / kTilesPerBlock;
+    size_t total = (size_t)B * L.S * tgroups;
+    if (total > 0x7fffffff || nn > 0xffffffffull) return LIF_ERR_SIZE;
+    if (sequential || total == 0) {
+        size_t blocks = (nev + 255) / 256;
+        if (blocks > 2048) blocks = 2048;
+        if (blocks < 1) blocks = 1;
+        TIMED_LAUNCH("decay", k_decay, dim3((unsigned)blocks), dim3(256), 0, stream,
+                     ev_t, ev_n, B, E_max, L.S, m, dec, status, pool_count);
+    } else {
+        TIMED_LAUNCH("aggregate", k_aggregate, dim3((unsigned)total), dim3(kWave * kTilesPerBlock), 0, stream,
+                     ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, tgroups, L.S, (int)total, m, dec, segm, agg,
+                     status, pool_count);
+    }
     if ((p->flags & LIF_VALIDATE) && nev)
         TIMED_LAUNCH("validate", k_validate, dim3((unsigned)((nev + 255) / 256)), dim3(256), 0, stream,
                      ev_t, ev_src, ev_n, B, E_max, C_in, status);
-    size_t nn = (size_t)B * N;
-    int tiles = (N + kWave - 1) / kWave;
     if (sequential) {
         TIMED_LAUNCH("sequential", k_sequential, dim3((unsigned)((nn + 63) / 64)), dim3(64), 0, stream,
                      ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, dec, out_t, out_n, out_i, status);
         return check_launch();
     }
-    size_t total = (size_t)B * L.S * tiles;
-    if (total > 0x7fffffff) return LIF_ERR_SIZE;
-    if (total) {
-        TIMED_LAUNCH("aggregate", k_aggregate, dim3((unsigned)total), dim3(kWave), 0, stream,
-                     ev_src, ev_n, E_max, WT, C_in, N, tiles, L.S, (int)total, dec, agg);
+    if (nn)
         TIMED_LAUNCH("carry", k_carry, dim3((unsigned)((nn + 255) / 256)), dim3(256), 0, stream,
-                     ev_n, B, E_max, N, L.S, segm, agg, carry);
-        TIMED_LAUNCH("check", k_check, dim3((unsigned)total), dim3(kWave), 0, stream,
-                     ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, L.S, (int)total, m, dec, carry, mask, winfo,
-                     pool, pool_ub, pool_count, (uint32_t)L.pool_cap, status);
+                     ev_n, B, E_max, N, L.S, segm, agg, carry, status, m.s_max, out_t, out_n, out_i, listed);
+    if (total) {
+        TIMED_LAUNCH("check", k_check, dim3((unsigned)total), dim3(kWave * kTilesPerBlock), 0, stream,
+                     ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, tgroups, L.S, (int)total, m, dec, carry, mask,
+                     winfo, pool, pool_ub, pool_count, (uint32_t)L.pool_cap, listed, work, nwork, status);
+        // One wave per listed neuron, as many as can be resident at once.
+        unsigned grid = (unsigned)(nn < 4096 ? nn : 4096);
+        TIMED_LAUNCH("resolve", k_resolve, dim3(grid), dim3(kWave), 0, stream,
+                     ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, L.S, m, dec, carry, mask, winfo, pool, pool_ub,
+                     work, nwork, out_t, out_n, out_i, status);
     }
-    if (nn > 0x7fffffff) return LIF_ERR_SIZE;
-    if (nn) TIMED_LAUNCH("resolve", k_resolve, dim3((unsigned)nn), dim3(kWave), 0, stream,
-                         ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, L.S, m, dec, carry, mask, winfo, pool,
-                         pool_ub, out_t, out_n, out_i, status);
     return check_launch();
 }
 

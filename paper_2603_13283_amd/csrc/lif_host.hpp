@@ -14,7 +14,7 @@ namespace lif {
 
 struct FwdLayout {
     int S;                                   // segments per sample
-    size_t dec, segm, agg, carry, mask, winfo, counters, pool, pool_ub, total;
+    size_t dec, segm, agg, carry, mask, winfo, counters, listed, work, pool, pool_ub, total;
     size_t pool_cap;                         // records in the pool
 };
 FwdLayout fwd_layout(int B, int E_max, int N);

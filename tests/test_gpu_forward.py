@@ -163,4 +163,4 @@ def test_record_pool_fallback(env, monkeypatch):
     assert s["par"]["status"][7] > 0
     monkeypatch.setenv("LIF_POOL_CAP", "0")
     s = check(env, cfg.events, cfg.layers[0].WT, "pool0", both=False)
-    assert s["par"]["status"][7] == s["par"]["status"][4]      # every walked block fell back
+    assert s["par"]["status"][7] >= s["par"]["status"][4] > 0   # every walked block fell back
