@@ -221,9 +221,16 @@ __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_aggregate(
 #pragma unroll
             for (int j = 0; j < kSub; ++j) w[j] = wn[j];
             if (q + 1 < kSubPerSeg && (q + 1) * kSub < c.cnt) load_sub_weights(sr, wcol, N, c.cnt, q + 1, wn);
+            if ((q + 1) * kSub <= c.cnt) {            // full sub-block: straight-line code
 #pragma unroll
-            for (int j = 0; j < kSub; ++j) {
-                if (q * kSub + j < c.cnt) {
+                for (int j = 0; j < kSub; ++j) {
+                    Decay e = sd[q * kSub + j];
+                    double Vn = e.A * V + e.C * I;
+                    I = e.D * I + (double)w[j];
+                    V = Vn;
+                }
+            } else {
+                for (int j = 0; j < c.cnt - q * kSub; ++j) {
                     Decay e = sd[q * kSub + j];
                     double Vn = e.A * V + e.C * I;
                     I = e.D * I + (double)w[j];
@@ -324,9 +331,17 @@ __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_check(
             for (int j = 0; j < kSub; ++j) w[j] = wn[j];
             if (q + 1 < kSubPerSeg && (q + 1) * kSub < cnt_seg) load_sub_weights(sr, wcol, N, cnt_seg, q + 1, wn);
             double Vin = V, Iin = I, ub = -INFINITY;
+            if (cnt == kSub) {                         // full sub-block: straight-line code
 #pragma unroll
-            for (int j = 0; j < kSub; ++j) {
-                if (j < cnt) {
+                for (int j = 0; j < kSub; ++j) {
+                    Decay e = sd[q * kSub + j];
+                    ub = fmax(ub, fmax(V, 0.0) + fmax(I, 0.0) * e.g);
+                    double Vn = e.A * V + e.C * I;
+                    I = e.D * I + (double)w[j];
+                    V = Vn;
+                }
+            } else {
+                for (int j = 0; j < cnt; ++j) {
                     Decay e = sd[q * kSub + j];
                     ub = fmax(ub, fmax(V, 0.0) + fmax(I, 0.0) * e.g);
                     double Vn = e.A * V + e.C * I;
