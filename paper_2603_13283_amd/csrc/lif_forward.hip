@@ -89,7 +89,6 @@ __global__ __launch_bounds__(256) void k_decay(const float* __restrict__ ev_t, c
     const size_t tid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     const size_t stride = (size_t)gridDim.x * blockDim.x;
     if (tid < LIF_STATUS_WORDS) status[tid] = 0;
-    if (tid < 2 && counters) counters[tid] = 0;
     const size_t nev = (size_t)B * (size_t)E_max;
     for (size_t idx = tid; idx < nev; idx += stride) {
         int b = (int)(idx / (size_t)E_max), k = (int)(idx % (size_t)E_max);
@@ -186,7 +185,6 @@ __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_aggregate(
 {
     __shared__ Decay sd[kSeg];
     if (blockIdx.x == 0 && threadIdx.x < LIF_STATUS_WORDS) status[threadIdx.x] = 0;
-    if (blockIdx.x == 0 && threadIdx.x < 2) counters[threadIdx.x] = 0;
     const SegCoords c = seg_coords(total, tgroups, S, ev_n, E_max, N);
     if (c.k0 >= c.nb) return;                        // uniform over the workgroup
     const float* tt = ev_t + (size_t)c.b * E_max;
@@ -212,15 +210,16 @@ __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_aggregate(
     const float* wcol = WT + c.nc;
     const SrcRegs sr = load_sources(ev_src + (size_t)c.b * E_max + c.k0, c.cnt, c.lane, C_in);
     double V = 0.0, I = 0.0;
-    float wn[kSub];
+    float wn[kSub], wn2[kSub];
     load_sub_weights(sr, wcol, N, c.cnt, 0, wn);
+    if (kSub < c.cnt) load_sub_weights(sr, wcol, N, c.cnt, 1, wn2);
 #pragma unroll
     for (int q = 0; q < kSubPerSeg; ++q) {
         if (q * kSub < c.cnt) {
             float w[kSub];
 #pragma unroll
-            for (int j = 0; j < kSub; ++j) w[j] = wn[j];
-            if (q + 1 < kSubPerSeg && (q + 1) * kSub < c.cnt) load_sub_weights(sr, wcol, N, c.cnt, q + 1, wn);
+            for (int j = 0; j < kSub; ++j) { w[j] = wn[j]; wn[j] = wn2[j]; }
+            if (q + 2 < kSubPerSeg && (q + 2) * kSub < c.cnt) load_sub_weights(sr, wcol, N, c.cnt, q + 2, wn2);
             if ((q + 1) * kSub <= c.cnt) {            // full sub-block: straight-line code
 #pragma unroll
                 for (int j = 0; j < kSub; ++j) {
@@ -251,7 +250,8 @@ __global__ __launch_bounds__(256) void k_carry(const int32_t* __restrict__ ev_n,
                                                const Decay* __restrict__ segm, const double2* __restrict__ agg,
                                                double2* __restrict__ carry, int32_t* __restrict__ status,
                                                int s_max, float* __restrict__ out_t, int32_t* __restrict__ out_n,
-                                               float* __restrict__ out_i, uint32_t* __restrict__ listed)
+                                               float* __restrict__ out_i, uint32_t* __restrict__ listed,
+                                               uint32_t* __restrict__ counters)
 {
     size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     const size_t nn = (size_t)B * (size_t)N;
@@ -265,6 +265,8 @@ __global__ __launch_bounds__(256) void k_carry(const int32_t* __restrict__ ev_n,
     }
     out_n[idx] = 0;
     listed[idx] = 0u;
+    if (n == 0) counters[1 + b] = 0u;          // record pool use of sample b
+    if (idx == 0) counters[0] = 0u;            // work-list length
     int nb = clamp_count(ev_n[b], E_max);
     if (n == 0) atomicAdd(&status[LIF_ST_EVENTS], nb);
     int Sb = (nb + kSeg - 1) / kSeg;
@@ -320,16 +322,17 @@ __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_check(
     uint32_t msk = 0;
     int ncand = 0;
     const unsigned long long below = (1ull << lane) - 1ull;
-    float wn[kSub];
+    float wn[kSub], wn2[kSub];
     load_sub_weights(sr, wcol, N, cnt_seg, 0, wn);
+    if (kSub < cnt_seg) load_sub_weights(sr, wcol, N, cnt_seg, 1, wn2);
 #pragma unroll
     for (int q = 0; q < kSubPerSeg; ++q) {
         if (q * kSub < cnt_seg) {
             const int cnt = min(kSub, cnt_seg - q * kSub);
             float w[kSub];
 #pragma unroll
-            for (int j = 0; j < kSub; ++j) w[j] = wn[j];
-            if (q + 1 < kSubPerSeg && (q + 1) * kSub < cnt_seg) load_sub_weights(sr, wcol, N, cnt_seg, q + 1, wn);
+            for (int j = 0; j < kSub; ++j) { w[j] = wn[j]; wn[j] = wn2[j]; }
+            if (q + 2 < kSubPerSeg && (q + 2) * kSub < cnt_seg) load_sub_weights(sr, wcol, N, cnt_seg, q + 2, wn2);
             double Vin = V, Iin = I, ub = -INFINITY;
             if (cnt == kSub) {                         // full sub-block: straight-line code
 #pragma unroll
@@ -362,10 +365,13 @@ __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_check(
             unsigned long long lanes = __ballot(surv);
             if (lanes) {
                 int cntl = __popcll(lanes);
+                // Records of sample b live in their own slice of the pool, so
+                // the allocation atomics of different samples do not contend.
                 uint32_t base = 0;
-                if (lane == 0) base = atomicAdd(pool_count, (uint32_t)cntl);
+                if (lane == 0) base = atomicAdd(&pool_count[c.b], (uint32_t)cntl);
                 base = __shfl(base, 0, kWave);
                 bool ok = (unsigned long long)base + (unsigned long long)cntl <= (unsigned long long)pool_cap;
+                base += (uint32_t)c.b * pool_cap;
                 if (lane == 0) {
                     WaveInfo wi;
                     wi.lanes = lanes;
@@ -401,11 +407,14 @@ __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_check(
     if (n < N) {
         mask[row + n] = msk;
         if (ncand) {
-            atomicAdd(&status[LIF_ST_CAND_BLOCKS], ncand);
             size_t bn = (size_t)c.b * N + n;
             if (atomicOr(&listed[bn], 1u) == 0u) work[atomicAdd(nwork, 1u)] = (uint32_t)bn;
         }
     }
+    int tot = ncand;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) tot += __shfl_xor(tot, off, kWave);
+    if (lane == 0 && tot) atomicAdd(&status[LIF_ST_CAND_BLOCKS], tot);
 }
 
 // ---------------------------------------------------------------------------
@@ -808,7 +817,7 @@ FwdLayout fwd_layout(int B, int E_max, int N)
     L.mask = take((size_t)B * L.S * N * sizeof(uint32_t));
     int tiles = (N + kWave - 1) / kWave;
     L.winfo = take((size_t)B * L.S * tiles * kSubPerSeg * sizeof(WaveInfo));
-    L.counters = take(256);
+    L.counters = take(((size_t)B + 1) * sizeof(uint32_t));
     L.listed = take((size_t)B * N * sizeof(uint32_t));
     L.work = take((size_t)B * N * sizeof(uint32_t));
     // Record pool: one record per flagged (sub-block, neuron).  Sized at a
@@ -841,8 +850,9 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     double2* carry = (double2*)(base + L.carry);
     uint32_t* mask = (uint32_t*)(base + L.mask);
     WaveInfo* winfo = (WaveInfo*)(base + L.winfo);
-    uint32_t* pool_count = (uint32_t*)(base + L.counters);
-    uint32_t* nwork = pool_count + 1;
+    uint32_t* counters = (uint32_t*)(base + L.counters);
+    uint32_t* nwork = counters;
+    uint32_t* pool_count = counters + 1;
     uint32_t* listed = (uint32_t*)(base + L.listed);
     uint32_t* work = (uint32_t*)(base + L.work);
     Record* pool = (Record*)(base + L.pool);
@@ -859,11 +869,11 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
         if (blocks > 2048) blocks = 2048;
         if (blocks < 1) blocks = 1;
         TIMED_LAUNCH("decay", k_decay, dim3((unsigned)blocks), dim3(256), 0, stream,
-                     ev_t, ev_n, B, E_max, L.S, m, dec, status, pool_count);
+                     ev_t, ev_n, B, E_max, L.S, m, dec, status, counters);
     } else {
         TIMED_LAUNCH("aggregate", k_aggregate, dim3((unsigned)total), dim3(kWave * kTilesPerBlock), 0, stream,
                      ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, tgroups, L.S, (int)total, m, dec, segm, agg,
-                     status, pool_count);
+                     status, counters);
     }
     if ((p->flags & LIF_VALIDATE) && nev)
         TIMED_LAUNCH("validate", k_validate, dim3((unsigned)((nev + 255) / 256)), dim3(256), 0, stream,
@@ -875,11 +885,13 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     }
     if (nn)
         TIMED_LAUNCH("carry", k_carry, dim3((unsigned)((nn + 255) / 256)), dim3(256), 0, stream,
-                     ev_n, B, E_max, N, L.S, segm, agg, carry, status, m.s_max, out_t, out_n, out_i, listed);
+                     ev_n, B, E_max, N, L.S, segm, agg, carry, status, m.s_max, out_t, out_n, out_i, listed,
+                     counters);
     if (total) {
         TIMED_LAUNCH("check", k_check, dim3((unsigned)total), dim3(kWave * kTilesPerBlock), 0, stream,
                      ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, tgroups, L.S, (int)total, m, dec, carry, mask,
-                     winfo, pool, pool_ub, pool_count, (uint32_t)L.pool_cap, listed, work, nwork, status);
+                     winfo, pool, pool_ub, pool_count, (uint32_t)(L.pool_cap / (B > 0 ? B : 1)), listed, work, nwork,
+                     status);
         // One wave per listed neuron, as many as can be resident at once.
         unsigned grid = (unsigned)(nn < 4096 ? nn : 4096);
         TIMED_LAUNCH("resolve", k_resolve, dim3(grid), dim3(kWave), 0, stream,
