@@ -84,11 +84,18 @@ __device__ __forceinline__ Decay make_decay(const Model& m, const float* __restr
 
 __global__ __launch_bounds__(256) void k_decay(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_n,
                                                int B, int E_max, int S, Model m, Decay* __restrict__ dec,
-                                               int32_t* __restrict__ status, uint32_t* __restrict__ counters)
+                                               int32_t* __restrict__ status, uint32_t* __restrict__ counters,
+                                               float* __restrict__ out_t, float* __restrict__ out_i, size_t n_out)
 {
     const size_t tid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     const size_t stride = (size_t)gridDim.x * blockDim.x;
     if (tid < LIF_STATUS_WORDS) status[tid] = 0;
+    if (out_t) {
+        for (size_t i = tid; i < n_out; i += stride) {
+            out_t[i] = INFINITY;
+            if (out_i) out_i[i] = 0.0f;
+        }
+    }
     const size_t nev = (size_t)B * (size_t)E_max;
     for (size_t idx = tid; idx < nev; idx += stride) {
         int b = (int)(idx / (size_t)E_max), k = (int)(idx % (size_t)E_max);
@@ -181,10 +188,20 @@ __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_aggregate(
     const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
     const float* __restrict__ WT, int C_in, int N, int tiles, int tgroups, int S, int total, Model m,
     Decay* __restrict__ dec, Decay* __restrict__ segm, double2* __restrict__ agg, int32_t* __restrict__ status,
-    uint32_t* __restrict__ counters)
+    uint32_t* __restrict__ counters, float* __restrict__ out_t, float* __restrict__ out_i, size_t n_out)
 {
     __shared__ Decay sd[kSeg];
     if (blockIdx.x == 0 && threadIdx.x < LIF_STATUS_WORDS) status[threadIdx.x] = 0;
+    {
+        // Every neuron starts with no spike (+inf times); the resolve pass
+        // overwrites the outputs of neurons that fire.  Coalesced fill spread
+        // over the whole launch.
+        const size_t stride = (size_t)gridDim.x * blockDim.x;
+        for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_out; i += stride) {
+            out_t[i] = INFINITY;
+            if (out_i) out_i[i] = 0.0f;
+        }
+    }
     const SegCoords c = seg_coords(total, tgroups, S, ev_n, E_max, N);
     if (c.k0 >= c.nb) return;                        // uniform over the workgroup
     const float* tt = ev_t + (size_t)c.b * E_max;
@@ -246,7 +263,7 @@ __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_aggregate(
 // aggregates are fetched kCarryBatch at a time so their loads overlap.
 constexpr int kCarryBatch = 16;
 
-__global__ __launch_bounds__(256) void k_carry(const int32_t* __restrict__ ev_n, int B, int E_max, int N, int S,
+__global__ __launch_bounds__(64) void k_carry(const int32_t* __restrict__ ev_n, int B, int E_max, int N, int S,
                                                const Decay* __restrict__ segm, const double2* __restrict__ agg,
                                                double2* __restrict__ carry, int32_t* __restrict__ status,
                                                int s_max, float* __restrict__ out_t, int32_t* __restrict__ out_n,
@@ -257,12 +274,6 @@ __global__ __launch_bounds__(256) void k_carry(const int32_t* __restrict__ ev_n,
     const size_t nn = (size_t)B * (size_t)N;
     if (idx >= nn) return;
     int b = (int)(idx / (size_t)N), n = (int)(idx % (size_t)N);
-    // Every neuron starts with no spike (+inf times); the resolve pass
-    // overwrites the outputs of neurons that fire.  Coalesced fill.
-    for (size_t i = idx; i < nn * (size_t)s_max; i += nn) {
-        out_t[i] = INFINITY;
-        if (out_i) out_i[i] = 0.0f;
-    }
     out_n[idx] = 0;
     listed[idx] = 0u;
     if (n == 0) counters[1 + b] = 0u;          // record pool use of sample b
@@ -865,15 +876,16 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     size_t total = (size_t)B * L.S * tgroups;
     if (total > 0x7fffffff || nn > 0xffffffffull) return LIF_ERR_SIZE;
     if (sequential || total == 0) {
-        size_t blocks = (nev + 255) / 256;
+        size_t blocks = ((nev > nn * (size_t)p->s_max ? nev : nn * (size_t)p->s_max) + 255) / 256;
         if (blocks > 2048) blocks = 2048;
         if (blocks < 1) blocks = 1;
         TIMED_LAUNCH("decay", k_decay, dim3((unsigned)blocks), dim3(256), 0, stream,
-                     ev_t, ev_n, B, E_max, L.S, m, dec, status, counters);
+                     ev_t, ev_n, B, E_max, L.S, m, dec, status, counters, sequential ? nullptr : out_t, out_i,
+                     nn * (size_t)p->s_max);
     } else {
         TIMED_LAUNCH("aggregate", k_aggregate, dim3((unsigned)total), dim3(kWave * kTilesPerBlock), 0, stream,
                      ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, tgroups, L.S, (int)total, m, dec, segm, agg,
-                     status, counters);
+                     status, counters, out_t, out_i, nn * (size_t)p->s_max);
     }
     if ((p->flags & LIF_VALIDATE) && nev)
         TIMED_LAUNCH("validate", k_validate, dim3((unsigned)((nev + 255) / 256)), dim3(256), 0, stream,
@@ -884,7 +896,7 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
         return check_launch();
     }
     if (nn)
-        TIMED_LAUNCH("carry", k_carry, dim3((unsigned)((nn + 255) / 256)), dim3(256), 0, stream,
+        TIMED_LAUNCH("carry", k_carry, dim3((unsigned)((nn + 63) / 64)), dim3(64), 0, stream,
                      ev_n, B, E_max, N, L.S, segm, agg, carry, status, m.s_max, out_t, out_n, out_i, listed,
                      counters);
     if (total) {
