@@ -85,17 +85,15 @@ __device__ __forceinline__ Crossing interval_rule(const Model& m, double V0, dou
                                                   double eA, double eD, double vend, double th)
 {
     Crossing c{false, len, vend};
+    // If V(len) >= th the crossing lies in (0, len]: V is unimodal, so V < th
+    // before the crossing and V >= th from it to len; [0, len] brackets it.
+    if (vend >= th) {
+        c.hit = true;
+        return c;
+    }
     double Dd = V0 * (m.tm - m.ts) + I0 * m.ts;
     bool has_max = (I0 > V0) && (Dd > 0.0);
     bool max_inside = has_max && (isinf(len) || I0 * m.tm * eD < Dd * eA);
-    if (vend >= th) {
-        c.hit = true;
-        if (max_inside) {
-            double tv = m.c_tv * log(I0 * m.tm / Dd);
-            if (tv < len) { c.hi = tv; c.vhi = v_after(m, V0, I0, tv); }
-        }
-        return c;
-    }
     if (max_inside) {
         double tv = m.c_tv * log(I0 * m.tm / Dd);
         if (tv < len) {
@@ -113,12 +111,12 @@ __device__ __forceinline__ Crossing interval_rule(const Model& m, double V0, dou
 // Bracketed Newton-Raphson for the first time tau in (0, hi] with
 // V(tau) = th (Appendix D.1), keeping [lo, hi] with V(lo) < th <= V(hi) and
 // falling back to the midpoint whenever a step leaves the bracket (the
-// clamp of D.1, i.e. a bisection step of D.2); it stops when a step no longer
-// moves the float64 iterate.  dV/dt comes from Eq. mem_dyn.  The start is the
-// root of the chord from (0, V0) to (hi, V(hi)) instead of the paper's hi/2:
-// V is concave on [0, hi] (it rises to its only maximum, whose inflection
-// comes later), so the chord lies below V and its root is a tight upper
-// bound of the crossing; from there Newton converges in a few steps.
+// clamp of D.1, i.e. a bisection step of D.2).  dV/dt comes from
+// Eq. mem_dyn.  The start is the root of the chord from (0, V0) to
+// (hi, V(hi)) instead of the paper's hi/2.  The iteration runs in float32
+// (hardware exp) until its step is below float32 resolution, then float64
+// steps finish it to float64 precision; the float64 bracket is kept
+// throughout, so the float32 phase only supplies a starting point.
 __device__ __forceinline__ double newton_root(const Model& m, double V0, double I0, double hi, double vhi,
                                               int* iters)
 {
@@ -126,6 +124,24 @@ __device__ __forceinline__ double newton_root(const Model& m, double V0, double 
     double t = (vhi > V0) ? hi * ((m.th - V0) / (vhi - V0)) : 0.5 * hi;
     if (!(t > 0.0 && t <= hi)) t = 0.5 * hi;
     int it = 0;
+    {
+        const float V0f = (float)V0, I0f = (float)I0, thf = (float)m.th, kf = (float)m.kappa;
+        const float itm = (float)m.inv_tm, its = (float)m.inv_ts;
+        float tf = (float)t, lof = 0.0f, hif = (float)hi;
+        for (int k = 0; k < 24; ++k) {
+            float em = __expf(-tf * itm), es = __expf(-tf * its);
+            float v = V0f * em + I0f * kf * (em - es);
+            if (v >= thf) hif = tf; else lof = tf;
+            float dv = (I0f * es - v) * itm;
+            float step = dv > 0.0f ? (v - thf) / dv : 0.0f;
+            float tn = tf - step;
+            if (!(tn > lof && tn < hif)) tn = 0.5f * (lof + hif);
+            if (fabsf(tn - tf) <= 2e-7f * tf) { tf = tn; break; }
+            tf = tn;
+        }
+        double tc = (double)tf;
+        if (tc > 0.0 && tc < hi) t = tc;
+    }
     for (; it < 96; ++it) {
         double em = exp(-t * m.inv_tm);
         double es = exp(-t * m.inv_ts);

@@ -450,22 +450,23 @@ __device__ bool advance_interval(const Model& m, double& V, double& I, double& t
     for (;;) {
         double len = t_hi - t_cur;
         if (!(len > 0.0)) return true;
-        double eA, eD, C, g;
+        // Decays of the whole gap from the table while no spike split it;
+        // after a spike (or for the open last interval) they are computed
+        // and the cheap bound is skipped (the exact rule is applied).
+        double eA, eD, C;
+        bool test = true;
         if (fresh) {
-            eA = tab->A; eD = tab->D; C = tab->C; g = tab->g;
+            eA = tab->A; eD = tab->D; C = tab->C;
+            test = fmax(V, 0.0) + fmax(I, 0.0) * tab->g >= m.th_lo;
         } else if (isinf(len)) {
             eA = 0.0; eD = 0.0; C = 0.0;
-            g = unit_kernel(m, m.t_peak, exp(-m.t_peak * m.inv_tm)) * (1.0 + 1e-12);
         } else {
             eA = exp(-len * m.inv_tm);
             eD = exp(-len * m.inv_ts);
-            C = unit_kernel(m, len, eA);
-            double gl = fmin(len, m.t_peak);
-            g = unit_kernel(m, gl, exp(-gl * m.inv_tm)) * (1.0 + 1e-12);
+            C = m.kappa * (eA - eD);
         }
         double vend = V * eA + C * I;
-        double u = fmax(V, 0.0) + fmax(I, 0.0) * g;
-        if (u >= m.th_lo) {
+        if (test) {
             Crossing c = interval_rule(m, V, I, len, eA, eD, vend, m.th);
             if (c.hit) {
                 int it = 0;
@@ -612,17 +613,30 @@ __device__ void resolve_neuron(ResolveLds& sh, int b, int n, const float* __rest
             int kq0 = seg * kSeg + q * kSub;
             cnt_c = min(kSub, nb - kq0);
             WaveInfo wi = winfo[(((size_t)b * S + seg) * tiles + tile) * kSubPerSeg + q];
-            sh.t[lane][0] = kq0 > 0 ? tt[kq0 - 1] : 0.0f;
-            for (int j = 0; j < kSub; ++j) {
-                int k = min(kq0 + j, nb - 1);
-                sh.e[lane][j] = d[k];
-                sh.t[lane][j + 1] = tt[k];
+            {
+                float tv[kSub + 1];
+                Decay ev[kSub];
+                tv[0] = kq0 > 0 ? tt[kq0 - 1] : 0.0f;
+#pragma unroll
+                for (int j = 0; j < kSub; ++j) {
+                    int k = min(kq0 + j, nb - 1);
+                    ev[j] = d[k];
+                    tv[j + 1] = tt[k];
+                }
+#pragma unroll
+                for (int j = 0; j < kSub; ++j) sh.e[lane][j] = ev[j];
+#pragma unroll
+                for (int j = 0; j <= kSub; ++j) sh.t[lane][j] = tv[j];
             }
             if (wi.base != kNoSlot) {
                 uint32_t slot = wi.base + (uint32_t)__popcll(wi.lanes & below_n);
                 ub = pool_ub[slot];
                 const Record* rec = pool + slot;
-                for (int j = 0; j <= kSub; ++j) sh.s[lane][j] = rec->s[j];
+                double2 rs[kSub + 1];
+#pragma unroll
+                for (int j = 0; j <= kSub; ++j) rs[j] = rec->s[j];
+#pragma unroll
+                for (int j = 0; j <= kSub; ++j) sh.s[lane][j] = rs[j];
             } else {
                 size_t row = ((size_t)b * S + seg) * N;
                 double2 cs = entering_state(carry, row, n, seg * kSeg, kq0, src, d, WT, C_in, N);
@@ -644,11 +658,18 @@ __device__ void resolve_neuron(ResolveLds& sh, int b, int n, const float* __rest
         }
         fallback += __popcll(__ballot(ub == INFINITY && lane < W));
         __syncthreads();
+        // Deficits are evaluated as dw * e^{-(t - tw)/tm}: the per-lane factor
+        // is computed once per window (or group), the uniform dw only after
+        // a spike.
+        const double tw = (double)sh.t[0][0];
+        const double f_out = isinf(t_out) ? 0.0 : exp(-(t_out - tw) * m.inv_tm);
+        double dw = deficit_at(sp, m, tw);
+        int dw_ns = sp.ns;
         while (!sp.capped) {
+            if (sp.ns != dw_ns) { dw = deficit_at(sp, m, tw); dw_ns = sp.ns; }
             // ---- certify in parallel with the current deficit
             if (!done && sp.ns > 0) {
-                double def_out = isinf(t_out) ? 0.0 : deficit_at(sp, m, t_out);
-                if (ub - def_out < m.th_lo) done = true;
+                if (ub - dw * f_out < m.th_lo) done = true;
             }
             unsigned long long rem = __ballot(!done);
             if (!rem) break;
@@ -674,11 +695,13 @@ __device__ void resolve_neuron(ResolveLds& sh, int b, int n, const float* __rest
             const double2 s0 = valid ? sh.s[c][j] : make_double2(0.0, 0.0);
             const double2 s1 = valid ? sh.s[c][j + 1] : make_double2(0.0, 0.0);
             bool pending = valid && t1 > t0;
+            const double f0 = exp(-(t0 - tw) * m.inv_tm);
             while (!sp.capped) {
+                if (sp.ns != dw_ns) { dw = deficit_at(sp, m, tw); dw_ns = sp.ns; }
                 bool cross = false;
                 double V0 = 0.0, I0 = 0.0;
                 if (pending) {
-                    double def0 = deficit_at(sp, m, t0);
+                    double def0 = dw * f0;
                     V0 = s0.x - def0;
                     I0 = s0.y;
                     double u = fmax(V0, 0.0) + fmax(I0, 0.0) * e.g;
