@@ -46,7 +46,7 @@ typedef struct ihipStream_t* lif_stream_t;
 #define LIF_OK              0
 #define LIF_ERR_ARG        -1  /* null pointer, bad size, s_max < 1          */
 #define LIF_ERR_TAU        -2  /* require tau_mem > tau_syn > 0 (App. D.1)   */
-#define LIF_ERR_THRESHOLD  -3  /* require v_reset < v_th                     */
+#define LIF_ERR_THRESHOLD  -3  /* require 0 < v_th and v_reset < v_th        */
 #define LIF_ERR_WORKSPACE  -4  /* ws_bytes below the *_workspace_size value  */
 #define LIF_ERR_HIP        -5  /* a kernel launch failed                     */
 #define LIF_ERR_SIZE       -6  /* a size exceeds a documented limit          */
@@ -76,7 +76,7 @@ typedef struct ihipStream_t* lif_stream_t;
 typedef struct lif_params {
     double   tau_mem;    /* tau_m (s); must exceed tau_syn (paper: 0.02)        */
     double   tau_syn;    /* tau_s (s); > 0 (paper: 0.005)                       */
-    double   v_th;       /* threshold V_th (paper: 1.0)                         */
+    double   v_th;       /* threshold V_th > 0, above rest (paper: 1.0)         */
     double   v_reset;    /* reset potential, < v_th (paper: 0.0)                */
     double   t_end;      /* end of the interval after the last event; +INFINITY
                             (events later than t_end are still consumed; the

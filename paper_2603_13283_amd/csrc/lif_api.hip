@@ -12,7 +12,9 @@ int check_params(const lif_params* p)
 {
     if (!p) return LIF_ERR_ARG;
     if (!(p->tau_syn > 0.0) || !(p->tau_mem > p->tau_syn) || !isfinite(p->tau_mem)) return LIF_ERR_TAU;
-    if (!(p->v_reset < p->v_th) || !isfinite(p->v_th) || !isfinite(p->v_reset)) return LIF_ERR_THRESHOLD;
+    // The neuron rests at V = 0 below its threshold: 0 < v_th, v_reset < v_th.
+    if (!(p->v_reset < p->v_th) || !(p->v_th > 0.0) || !isfinite(p->v_th) || !isfinite(p->v_reset))
+        return LIF_ERR_THRESHOLD;
     if (p->s_max < 1) return LIF_ERR_ARG;
     if (isnan(p->t_end) || !(p->solver_reg >= 0.0)) return LIF_ERR_ARG;
     return LIF_OK;
@@ -35,6 +37,10 @@ Model make_model(const lif_params& p)
     // The cheap bound is evaluated in float64 with relative error ~1e-15; the
     // margin keeps it conservative for thresholds of any sign.
     m.th_lo = p.v_th - 1e-9 * fmax(1.0, fabs(p.v_th));
+    m.inv_th = 1.0 / p.v_th;
+    m.th_1k = p.v_th * (1.0 + m.kappa);
+    m.ts_tm = p.tau_syn / p.tau_mem;
+    m.dth = p.v_th - p.v_reset;
     m.reg = p.solver_reg;
     m.s_max = p.s_max;
     m.flags = p.flags;

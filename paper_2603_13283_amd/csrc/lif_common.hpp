@@ -30,6 +30,10 @@ struct Model {
     double inv_tm, inv_ts;
     double t_peak;     // argmax of the unit kernel K(u) = kappa (e^-u/tm - e^-u/ts)
     double th_lo;      // survival threshold of the cheap upper bound (slightly below th)
+    double inv_th;     // 1 / th
+    double th_1k;      // th (1 + kappa)
+    double ts_tm;      // tau_s / tau_m
+    double dth;        // th - vr: the drop of V at a reset
     double reg;        // backward floor on dV/dt
     int s_max;
     uint32_t flags;
@@ -58,105 +62,108 @@ __device__ __forceinline__ double unit_kernel(const Model& m, double u, double e
     return -m.kappa * eA * expm1(-u * m.a_rate);
 }
 
-// Closed-form V after time t from (V0, I0) (Appendix A, Eq. mem_pot).
-__device__ __forceinline__ double v_after(const Model& m, double V0, double I0, double t)
-{
-    if (isinf(t)) return 0.0;
-    double em = exp(-t * m.inv_tm);
-    return V0 * em + I0 * unit_kernel(m, t, em);
-}
-
-// Result of the interval rule.
-struct Crossing {
-    bool hit;      // V reaches th inside (0, len]
-    double hi;     // right end of the root bracket, min(t_Vmax, len)
-    double vhi;    // V(hi)
+// Interval test in deficit form.  Every spike at t_s lowers V afterwards by
+// (th - vr) e^{-(t - t_s)/tm} (hard reset of a linear system, Sec. 3.1 and
+// Eq. mem_pot), so on an interval that starts at the no-reset state
+// (V0, I0) with the spikes so far amounting to a deficit D at its start, the
+// true potential is V_lin(u) - D e^{-u/tm}, u in [0, L].  It reaches th
+// inside (0, L] iff D <= max h over (0, L] with
+//   h(u) = (V_lin(u) - th) e^{u/tm}
+//        = V0 - th e^{u/tm} + kappa I0 (1 - e^{-u r}),   r = 1/ts - 1/tm.
+// h'(u) = (I0 e^{-u r} - th e^{u/tm}) / tm: for th > 0 the only stationary
+// point is u* = ts ln(I0/th), a maximum, where h(u*) =
+// V0 + kappa I0 - th (1 + kappa) (I0/th)^{ts/tm}; it lies inside (0, L) iff
+// I0 > th and I0 e^{-L/ts} < th.  Otherwise h is monotone on the interval
+// and the test is the end value, D e^{-L/tm} <= V_lin(L) - th.  This is the
+// interval rule of Sec. 3.2.2 (t_Vmax of Eq. t_vmax, V at the maximum or at
+// the end) applied to V_lin - D e^{-u/tm}, with the maximum taken of h so
+// that the deficit enters as a single multiply: the test does not change as
+// D grows, and a spike in the interval re-tests the rest of it (the maximum
+// over (u_s, L] is the same, since u_s <= u*).
+struct IntervalMax {
+    double g;     // crossing iff D * a <= g
+    double a;     // 1 (interior maximum) or e^{-L/tm} (end value)
+    double hi;    // right end of the root bracket: u* or L
+    double Fhi;   // h(hi); F(hi) = h(hi) - D starts the root solve
 };
 
-// Interval rule of Sec. 3.2.2 for an interval of length len (may be +inf)
-// starting at (V0, I0); eA = e^{-len/tm}, eD = e^{-len/ts}, vend = V(len).
-// A spike occurs iff V(len) >= th, or the maximum (Eq. t_vmax) lies inside
-// the interval and V(t_Vmax) >= th.  The maximum exists only if I0 > V0 and
-// D = V0 (tm - ts) + I0 ts > 0; it lies before len iff
-// I0 tm e^{-len/ts} < D e^{-len/tm} (the log of Eq. t_vmax compared with
-// len without evaluating it).  `th` is passed so the scan can use a
-// conservative threshold.
-__device__ __forceinline__ Crossing interval_rule(const Model& m, double V0, double I0, double len,
-                                                  double eA, double eD, double vend, double th)
+__device__ __forceinline__ IntervalMax interval_max(const Model& m, double V0, double I0, double V1, double L,
+                                                    double A, double D)
 {
-    Crossing c{false, len, vend};
-    // If V(len) >= th the crossing lies in (0, len]: V is unimodal, so V < th
-    // before the crossing and V >= th from it to len; [0, len] brackets it.
-    if (vend >= th) {
-        c.hit = true;
-        return c;
+    IntervalMax r;
+    if (I0 > m.th && I0 * D < m.th) {
+        double lr = log(I0 * m.inv_th);
+        r.g = V0 + m.kappa * I0 - m.th_1k * exp(m.ts_tm * lr);
+        r.a = 1.0;
+        r.hi = m.ts * lr;
+        r.Fhi = r.g;
+    } else {
+        r.g = V1 - m.th;
+        r.a = A;
+        r.hi = L;
+        r.Fhi = A > 0.0 ? r.g / A : -INFINITY;
     }
-    double Dd = V0 * (m.tm - m.ts) + I0 * m.ts;
-    bool has_max = (I0 > V0) && (Dd > 0.0);
-    bool max_inside = has_max && (isinf(len) || I0 * m.tm * eD < Dd * eA);
-    if (max_inside) {
-        double tv = m.c_tv * log(I0 * m.tm / Dd);
-        if (tv < len) {
-            double vv = v_after(m, V0, I0, tv);
-            if (vv >= th) {
-                c.hit = true;
-                c.hi = tv;
-                c.vhi = vv;
-            }
-        }
-    }
-    return c;
+    return r;
 }
 
-// Bracketed Newton-Raphson for the first time tau in (0, hi] with
-// V(tau) = th (Appendix D.1), keeping [lo, hi] with V(lo) < th <= V(hi) and
-// falling back to the midpoint whenever a step leaves the bracket (the
-// clamp of D.1, i.e. a bisection step of D.2).  dV/dt comes from
-// Eq. mem_dyn.  The start is the root of the chord from (0, V0) to
-// (hi, V(hi)) instead of the paper's hi/2.  The iteration runs in float32
-// (hardware exp) until its step is below float32 resolution, then float64
-// steps finish it to float64 precision; the float64 bracket is kept
-// throughout, so the float32 phase only supplies a starting point.
-__device__ __forceinline__ double newton_root(const Model& m, double V0, double I0, double hi, double vhi,
-                                              int* iters)
+// e^x for |x| <= 4e-3 by its Taylor series to x^6 (relative error < 1e-17).
+__device__ __forceinline__ double exp_small(double x)
 {
-    double lo = 0.0;
-    double t = (vhi > V0) ? hi * ((m.th - V0) / (vhi - V0)) : 0.5 * hi;
-    if (!(t > 0.0 && t <= hi)) t = 0.5 * hi;
+    return 1.0 + x * (1.0 + x * (0.5 + x * (1.0 / 6.0 + x * (1.0 / 24.0 + x * (1.0 / 120.0 + x * (1.0 / 720.0))))));
+}
+
+// Spike time inside a crossing interval (Appendix D.1, bracketed
+// Newton-Raphson): the smallest u in (lo, hi] with F(u) = h(u) - D = 0,
+//   F(u) = c0 - th e^{u/tm} - kI e^{-u r},  c0 = V0 - D + kappa I0, kI = kappa I0,
+// given F(lo) = Flo < 0 <= F(hi) = Fhi.  F is concave wherever it can cross
+// (I0 > 0), so it increases through its first root.  The iteration starts at
+// the root of the chord from (lo, Flo) to (hi, Fhi) instead of the paper's
+// midpoint, keeps [lo, hi] with F(lo) < 0 <= F(hi) and takes the midpoint
+// whenever a Newton step leaves it (the clamp of D.1).  The two
+// exponentials are evaluated once at the start and then carried along by
+// the factor e^{step} (Taylor series) while steps are small, so a typical
+// solve costs one pair of exponentials.  Stops when a step falls below
+// 1e-9 ts (with quadratic convergence the error left is far below float64
+// resolution of the spike time) or the bracket collapses.  On return
+// *E1 = e^{u/tm} and *E2 = e^{-u r} at the returned u.
+__device__ __forceinline__ double root_h(const Model& m, double c0, double kI, double lo, double Flo, double hi,
+                                         double Fhi, double* E1o, double* E2o, int* iters)
+{
+    double u = (Fhi > Flo && Fhi < INFINITY) ? lo + (hi - lo) * (-Flo / (Fhi - Flo)) : 0.5 * (lo + hi);
+    if (!(u > lo && u <= hi)) u = 0.5 * (lo + hi);
+    double E1 = exp(u * m.inv_tm), E2 = exp(-u * m.a_rate);
+    const double tol = 1e-9 * m.ts;
+    const double dF1 = kI * m.a_rate, dF2 = m.th * m.inv_tm;
+    const double rmax = fmax(m.inv_tm, m.a_rate);
     int it = 0;
-    {
-        const float V0f = (float)V0, I0f = (float)I0, thf = (float)m.th, kf = (float)m.kappa;
-        const float itm = (float)m.inv_tm, its = (float)m.inv_ts;
-        float tf = (float)t, lof = 0.0f, hif = (float)hi;
-        for (int k = 0; k < 24; ++k) {
-            float em = __expf(-tf * itm), es = __expf(-tf * its);
-            float v = V0f * em + I0f * kf * (em - es);
-            if (v >= thf) hif = tf; else lof = tf;
-            float dv = (I0f * es - v) * itm;
-            float step = dv > 0.0f ? (v - thf) / dv : 0.0f;
-            float tn = tf - step;
-            if (!(tn > lof && tn < hif)) tn = 0.5f * (lof + hif);
-            if (fabsf(tn - tf) <= 2e-7f * tf) { tf = tn; break; }
-            tf = tn;
+    while (it < 80) {
+        ++it;
+        double F = c0 - m.th * E1 - kI * E2;
+        if (F >= 0.0) {
+            hi = u;
+            if (F == 0.0) break;
+        } else {
+            lo = u;
         }
-        double tc = (double)tf;
-        if (tc > 0.0 && tc < hi) t = tc;
+        if (!(hi - lo > 4e-16 * hi)) break;             // bracket collapsed onto u
+        double dF = dF1 * E2 - dF2 * E1;
+        double un = dF > 0.0 ? u - F / dF : 0.5 * (lo + hi);
+        if (!(un > lo && un < hi)) un = 0.5 * (lo + hi);
+        double d = un - u;
+        if (fabs(d) * rmax <= 4e-3) {
+            E1 *= exp_small(d * m.inv_tm);
+            E2 *= exp_small(-d * m.a_rate);
+        } else {
+            E1 = exp(un * m.inv_tm);
+            E2 = exp(-un * m.a_rate);
+        }
+        u = un;
+        if (fabs(d) <= tol) break;
     }
-    for (; it < 96; ++it) {
-        double em = exp(-t * m.inv_tm);
-        double es = exp(-t * m.inv_ts);
-        double v = V0 * em + I0 * m.kappa * (em - es);
-        if (v >= m.th) hi = t; else lo = t;
-        double d = (I0 * es - v) * m.inv_tm;
-        double step = (d > 0.0) ? (v - m.th) / d : INFINITY;
-        if (fabs(step) <= 2e-16 * t) { t -= step; break; }   // converged to the ulp
-        double tn = t - step;
-        if (!(tn > lo && tn < hi)) tn = 0.5 * (lo + hi);
-        if (hi - lo <= 4e-16 * hi) { t = hi; break; }        // bracket collapsed
-        t = tn;
-    }
-    if (iters) *iters = it;
-    return t;
+    *E1o = E1;
+    *E2o = E2;
+    if (iters) *iters += it;
+    return u;
 }
 
 }  // namespace lif

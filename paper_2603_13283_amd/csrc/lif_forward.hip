@@ -429,90 +429,40 @@ __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_check(
 }
 
 // ---------------------------------------------------------------------------
-// Exact advance of one neuron across [t_cur, t_hi]: every spike inside is
-// solved and followed by a hard reset and a re-test of the rest of the same
-// interval.  `tab` holds the decays of the whole gap and is used while no
-// spike has split the interval.  Returns false once the neuron is capped.
+// Resolve pass: one wave per neuron that has flagged sub-blocks (a work list
+// built by the check pass).  Intervals outside flagged sub-blocks provably
+// hold no spike.  The flagged sub-blocks are taken in time order:
+//   * Candidate list: the segments' sub-block masks are compacted into a
+//     time-ordered list in LDS with one wave prefix sum per 64 segments.
+//   * Windows of 64 candidates, one lane each, hold each sub-block's record
+//     slot, its upper bound of the no-reset V (from the check pass) and its
+//     end time.  Since every spike lowers V afterwards by
+//     (th - vr) e^{-(t - t_s)/tm}, a sub-block whose bound minus the deficit
+//     at its end stays below the threshold is certified without a walk
+//     (later spikes only deepen the deficit); this test runs on the whole
+//     window in parallel.
+//   * The earliest kGroup uncertified sub-blocks form a group, one lane per
+//     interval.  Each lane derives the interval's maximum of
+//     h(u) = (V_lin(u) - th) e^{u/tm} in closed form once (interval_max);
+//     with D the lane's deficit at its interval start, the interval crosses
+//     iff D a <= g.  A round takes the earliest crossing lane (ballot), which
+//     solves its spike time (root_h), emits the spike and raises its own
+//     deficit (the same lane is tested again for a second spike in its
+//     interval, Appendix E.2 restart); the later lanes take the new deficit
+//     with one exponential.  Rounds repeat until no lane crosses.
+// Wave-uniform state: spike count, reset deficit dref at the latest spike
+// time tref.
 // ---------------------------------------------------------------------------
-struct Sink {
-    float* st;      // this neuron's s_max time slots
-    float* si;      // this neuron's s_max current slots, may be null
-    int ns;         // spikes so far
-    int roots;      // root solves
-    double dref;    // reset deficit at tref (sum of (th - vr) e^{-(t - t_s)/tm})
-    double tref;
+constexpr int kGroup = kWave / kSub;             // sub-blocks per group
+constexpr int kCandCap = kWave * kSubPerSeg;     // candidates of 64 segments
+
+struct ResolveLds {
+    uint32_t cand[kCandCap];                     // (segment in chunk << 3) | sub-block
 };
 
-__device__ bool advance_interval(const Model& m, double& V, double& I, double& t_cur, double t_hi,
-                                 const Decay* tab, Sink& sk)
-{
-    bool fresh = tab != nullptr;
-    for (;;) {
-        double len = t_hi - t_cur;
-        if (!(len > 0.0)) return true;
-        // Decays of the whole gap from the table while no spike split it;
-        // after a spike (or for the open last interval) they are computed
-        // and the cheap bound is skipped (the exact rule is applied).
-        double eA, eD, C;
-        bool test = true;
-        if (fresh) {
-            eA = tab->A; eD = tab->D; C = tab->C;
-            test = fmax(V, 0.0) + fmax(I, 0.0) * tab->g >= m.th_lo;
-        } else if (isinf(len)) {
-            eA = 0.0; eD = 0.0; C = 0.0;
-        } else {
-            eA = exp(-len * m.inv_tm);
-            eD = exp(-len * m.inv_ts);
-            C = m.kappa * (eA - eD);
-        }
-        double vend = V * eA + C * I;
-        if (test) {
-            Crossing c = interval_rule(m, V, I, len, eA, eD, vend, m.th);
-            if (c.hit) {
-                int it = 0;
-                double tau = newton_root(m, V, I, c.hi, c.vhi, &it);
-                double Istar = I * exp(-tau * m.inv_ts);
-                double tsp = t_cur + tau;
-                sk.st[sk.ns] = (float)tsp;
-                if (sk.si) sk.si[sk.ns] = (float)Istar;
-                sk.ns++;
-                sk.roots++;
-                sk.dref = sk.dref * exp(-(tsp - sk.tref) * m.inv_tm) + (m.th - m.vr);
-                sk.tref = tsp;
-                V = m.vr;
-                I = Istar;
-                t_cur = tsp;
-                fresh = false;
-                if (sk.ns >= m.s_max) return false;
-                continue;
-            }
-        }
-        V = vend;
-        I = I * eD;
-        t_cur = t_hi;
-        return true;
-    }
-}
-
-__device__ __forceinline__ void finish_neuron(const Model& m, Sink& sk, int32_t* out_n_slot, bool capped,
-                                              int32_t* status)
-{
-    *out_n_slot = sk.ns;
-    for (int s = sk.ns; s < m.s_max; ++s) {
-        sk.st[s] = INFINITY;
-        if (sk.si) sk.si[s] = 0.0f;
-    }
-    if (capped) {
-        atomicAdd(&status[LIF_ST_CAPPED], 1);
-        atomicOr(&status[LIF_ST_FLAGS], LIF_WARN_SPIKE_CAP);
-    }
-    if (sk.ns) atomicAdd(&status[LIF_ST_SPIKES], sk.ns);
-    if (sk.roots) atomicAdd(&status[LIF_ST_ROOT_SOLVES], sk.roots);
-}
-
 // Rebuild a sub-block's entering no-reset state from its segment carry by
-// walking the earlier sub-blocks of the segment (used only when the record
-// pool was full).
+// walking the earlier events of the segment (used only when the record pool
+// was full).
 __device__ __noinline__ double2 entering_state(const double2* __restrict__ carry, size_t row, int n, int k0, int kq0,
                                                const int32_t* __restrict__ src, const Decay* __restrict__ d,
                                                const float* __restrict__ WT, int C_in, int N)
@@ -528,55 +478,15 @@ __device__ __noinline__ double2 entering_state(const double2* __restrict__ carry
     return make_double2(V, I);
 }
 
-// Resolve pass: one wave per neuron that has flagged sub-blocks (a work
-// list built by the check pass); the paper's chunked speculative scheme
-// applied to those sub-blocks only.
-//   * Flagged sub-blocks are taken in time order in windows of kWin.  A
-//     window's records (no-reset states), decays and event times are staged
-//     in LDS with one batch of loads (one lane per sub-block).
-//   * Since every reset subtracts (V_th - V_reset) e^{-(t - t_s)/tm} from
-//     the no-reset trajectory, the true state entering an interval is the
-//     record's no-reset state minus the reset deficit at its start.  A
-//     sub-block whose no-reset bound minus the deficit at its end stays
-//     below the threshold is certified at once (more spikes only deepen the
-//     deficit); this test runs for the whole window in parallel.
-//   * The earliest kGroup uncertified sub-blocks are checked together, one
-//     lane per interval, with the interval rule; the earliest crossing
-//     (ballot) is solved by its lane with bracketed Newton, reset and
-//     re-tested until its interval is clear, the deficit is updated and the
-//     later intervals are tested again.
-// Intervals outside flagged sub-blocks provably hold no spike.
-constexpr int kGroup = kWave / kSub;
-constexpr int kWin = 32;
+__device__ __forceinline__ int rl_int(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
 
-// Wave-uniform spike bookkeeping of the neuron being resolved.
-struct NeuronSpikes {
-    int ns, roots;
-    double dref, tref;    // reset deficit dref at time tref
-    bool capped;
-};
-
-__device__ __forceinline__ double deficit_at(const NeuronSpikes& ns_, const Model& m, double t)
+__device__ __forceinline__ double rl_double(double v, int l)
 {
-    return ns_.ns > 0 ? ns_.dref * exp(-(t - ns_.tref) * m.inv_tm) : 0.0;
+    unsigned long long u = (unsigned long long)__double_as_longlong(v);
+    unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)u, l);
+    unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(u >> 32), l);
+    return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
-
-__device__ __forceinline__ void share_from(NeuronSpikes& sp, int from)
-{
-    sp.ns = __shfl(sp.ns, from, kWave);
-    sp.roots = __shfl(sp.roots, from, kWave);
-    sp.dref = __shfl(sp.dref, from, kWave);
-    sp.tref = __shfl(sp.tref, from, kWave);
-    sp.capped = __shfl((int)sp.capped, from, kWave) != 0;
-}
-
-struct ResolveLds {
-    double2 s[kWin][kSub + 1];   // no-reset states: entering, then after each event
-    Decay e[kWin][kSub];         // decays of the sub-block's events
-    float t[kWin][kSub + 1];     // time before the sub-block, then each event's time
-    int seg[kWin], q[kWin];      // the window's sub-blocks
-    int grp[kGroup];             // window slots of the group being checked
-};
 
 __device__ void resolve_neuron(ResolveLds& sh, int b, int n, const float* __restrict__ ev_t,
                                const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
@@ -597,188 +507,211 @@ __device__ void resolve_neuron(ResolveLds& sh, int b, int n, const float* __rest
     const size_t idx = (size_t)b * N + n;
     float* st = out_t + idx * (size_t)m.s_max;
     float* si = out_i ? out_i + idx * (size_t)m.s_max : nullptr;
-    NeuronSpikes sp{0, 0, 0.0, 0.0, false};
-    int walked = 0, fallback = 0;
     const int Sb = (nb + kSeg - 1) / kSeg;
-    int W = 0;
+    const int r = lane / kSub, j = lane % kSub;
 
-    auto process_window = [&]() {
-        __syncthreads();                                  // window list written by lane 0
-        // ---- stage: lane c loads sub-block c's record, decays and times
-        bool done = lane >= W;
-        double ub = 0.0, t_out = 0.0;
-        int cnt_c = 0;
-        if (!done) {
-            int seg = sh.seg[lane], q = sh.q[lane];
-            int kq0 = seg * kSeg + q * kSub;
-            cnt_c = min(kSub, nb - kq0);
-            WaveInfo wi = winfo[(((size_t)b * S + seg) * tiles + tile) * kSubPerSeg + q];
-            {
-                float tv[kSub + 1];
-                Decay ev[kSub];
-                tv[0] = kq0 > 0 ? tt[kq0 - 1] : 0.0f;
-#pragma unroll
-                for (int j = 0; j < kSub; ++j) {
-                    int k = min(kq0 + j, nb - 1);
-                    ev[j] = d[k];
-                    tv[j + 1] = tt[k];
-                }
-#pragma unroll
-                for (int j = 0; j < kSub; ++j) sh.e[lane][j] = ev[j];
-#pragma unroll
-                for (int j = 0; j <= kSub; ++j) sh.t[lane][j] = tv[j];
-            }
-            if (wi.base != kNoSlot) {
-                uint32_t slot = wi.base + (uint32_t)__popcll(wi.lanes & below_n);
-                ub = pool_ub[slot];
-                const Record* rec = pool + slot;
-                double2 rs[kSub + 1];
-#pragma unroll
-                for (int j = 0; j <= kSub; ++j) rs[j] = rec->s[j];
-#pragma unroll
-                for (int j = 0; j <= kSub; ++j) sh.s[lane][j] = rs[j];
-            } else {
-                size_t row = ((size_t)b * S + seg) * N;
-                double2 cs = entering_state(carry, row, n, seg * kSeg, kq0, src, d, WT, C_in, N);
-                double V = cs.x, I = cs.y;
-                sh.s[lane][0] = cs;
-                for (int j = 0; j < kSub; ++j) {
-                    if (j < cnt_c) {
-                        Decay e = d[kq0 + j];
-                        double Vn = e.A * V + e.C * I;
-                        I = e.D * I + (double)WT[(size_t)clamp_src(src[kq0 + j], C_in) * (size_t)N + n];
-                        V = Vn;
-                    }
-                    sh.s[lane][j + 1] = make_double2(V, I);
-                }
-                ub = INFINITY;
-            }
-            double tl = (double)tt[kq0 + cnt_c - 1];
-            t_out = kq0 + cnt_c == nb ? fmax(m.t_end, tl) : tl;
-        }
-        fallback += __popcll(__ballot(ub == INFINITY && lane < W));
-        __syncthreads();
-        // Deficits are evaluated as dw * e^{-(t - tw)/tm}: the per-lane factor
-        // is computed once per window (or group), the uniform dw only after
-        // a spike.
-        const double tw = (double)sh.t[0][0];
-        const double f_out = isinf(t_out) ? 0.0 : exp(-(t_out - tw) * m.inv_tm);
-        double dw = deficit_at(sp, m, tw);
-        int dw_ns = sp.ns;
-        while (!sp.capped) {
-            if (sp.ns != dw_ns) { dw = deficit_at(sp, m, tw); dw_ns = sp.ns; }
-            // ---- certify in parallel with the current deficit
-            if (!done && sp.ns > 0) {
-                if (ub - dw * f_out < m.th_lo) done = true;
-            }
-            unsigned long long rem = __ballot(!done);
-            if (!rem) break;
-            // ---- the earliest kGroup uncertified sub-blocks form the group
-            int G = 0;
-            while (rem && G < kGroup) {
-                int c = __ffsll((long long)rem) - 1;
-                rem &= rem - 1ull;
-                if (lane == 0) sh.grp[G] = c;
-                if (lane == c) done = true;
-                ++G;
-            }
-            __syncthreads();
-            walked += G;
-            const int r = lane / kSub, j = lane % kSub;
-            const int c = r < G ? sh.grp[r] : 0;
-            int kq0 = 0, cnt = 0;
-            if (r < G) { kq0 = sh.seg[c] * kSeg + sh.q[c] * kSub; cnt = min(kSub, nb - kq0); }
-            const bool valid = r < G && j < cnt;
-            const Decay e = valid ? sh.e[c][j] : Decay{1.0, 0.0, 1.0, 0.0};
-            const double t0 = valid ? (double)sh.t[c][j] : 0.0;
-            const double t1 = valid ? (double)sh.t[c][j + 1] : 0.0;
-            const double2 s0 = valid ? sh.s[c][j] : make_double2(0.0, 0.0);
-            const double2 s1 = valid ? sh.s[c][j + 1] : make_double2(0.0, 0.0);
-            bool pending = valid && t1 > t0;
-            const double f0 = exp(-(t0 - tw) * m.inv_tm);
-            while (!sp.capped) {
-                if (sp.ns != dw_ns) { dw = deficit_at(sp, m, tw); dw_ns = sp.ns; }
-                bool cross = false;
-                double V0 = 0.0, I0 = 0.0;
-                if (pending) {
-                    double def0 = dw * f0;
-                    V0 = s0.x - def0;
-                    I0 = s0.y;
-                    double u = fmax(V0, 0.0) + fmax(I0, 0.0) * e.g;
-                    if (u >= m.th_lo) cross = interval_rule(m, V0, I0, t1 - t0, e.A, e.D, s1.x - def0 * e.A, m.th).hit;
-                }
-                unsigned long long cm = __ballot(cross);
-                if (!cm) break;
-                const int kl = __ffsll((long long)cm) - 1;
-                if (lane == kl) {
-                    Sink sk;
-                    sk.st = st; sk.si = si;
-                    sk.ns = sp.ns; sk.roots = sp.roots; sk.dref = sp.dref; sk.tref = sp.tref;
-                    double V = V0, I = I0, tc = t0;
-                    bool ok = advance_interval(m, V, I, tc, t1, &e, sk);
-                    sp.ns = sk.ns; sp.roots = sk.roots; sp.dref = sk.dref; sp.tref = sk.tref;
-                    sp.capped = !ok;
-                }
-                share_from(sp, kl);
-                if (lane <= kl) pending = false;
-            }
-            // ---- the open interval after the stream's last event
-            if (!sp.capped) {
-                const int cl = sh.grp[G - 1];
-                int kql = sh.seg[cl] * kSeg + sh.q[cl] * kSub;
-                int cntl = min(kSub, nb - kql);
-                if (kql + cntl == nb) {
-                    if (lane == 0) {
-                        double tl = (double)sh.t[cl][cntl];
-                        double2 sl = sh.s[cl][cntl];
-                        Sink sk;
-                        sk.st = st; sk.si = si;
-                        sk.ns = sp.ns; sk.roots = sp.roots; sk.dref = sp.dref; sk.tref = sp.tref;
-                        double V = sl.x - deficit_at(sp, m, tl), I = sl.y, tc = tl;
-                        bool ok = advance_interval(m, V, I, tc, m.t_end, nullptr, sk);
-                        sp.ns = sk.ns; sp.roots = sk.roots; sp.dref = sk.dref; sp.tref = sk.tref;
-                        sp.capped = !ok;
-                    }
-                    share_from(sp, 0);
-                }
-            }
-            __syncthreads();
-        }
-        __syncthreads();
-        W = 0;
-    };
+    int ns = 0, walked = 0, fallback = 0;
+    bool capped = false;
+    double dref = 0.0, tref = 0.0;     // deficit right after the latest spike, its time
 
-    for (int seg0 = 0; seg0 < Sb && !sp.capped; seg0 += kWave) {
-        int sj = seg0 + lane;
-        uint32_t mv = sj < Sb ? mask[((size_t)b * S + sj) * N + n] : 0u;
-        unsigned long long nz = __ballot(mv != 0u);
-        while (nz && !sp.capped) {
-            int l = __ffsll((long long)nz) - 1;
-            nz &= nz - 1ull;
-            uint32_t mm = (uint32_t)__shfl((int)mv, l, kWave);
-            while (mm && !sp.capped) {
-                int q = __builtin_ctz(mm);
+    for (int seg0 = 0; seg0 < Sb && !capped; seg0 += kWave) {
+        // ---- compact this chunk's flagged sub-blocks into a time-ordered list
+        const int sj = seg0 + lane;
+        const uint32_t mv = sj < Sb ? mask[((size_t)b * S + sj) * N + n] : 0u;
+        const int pc = __popc(mv);
+        int ex = pc;
+#pragma unroll
+        for (int off = 1; off < kWave; off <<= 1) {
+            int v = __shfl_up(ex, off, kWave);
+            if (lane >= off) ex += v;
+        }
+        const int tot = __shfl(ex, kWave - 1, kWave);
+        ex -= pc;
+        {
+            uint32_t mm = mv;
+            int o = ex;
+            while (mm) {
+                sh.cand[o++] = ((uint32_t)lane << 3) | (uint32_t)__builtin_ctz(mm);
                 mm &= mm - 1u;
-                if (lane == 0) { sh.seg[W] = seg0 + l; sh.q[W] = q; }
-                ++W;
-                if (W == kWin) process_window();
             }
         }
+        __syncthreads();
+
+        for (int w0 = 0; w0 < tot && !capped; w0 += kWave) {
+            // ---- window: lane c holds candidate w0 + c
+            const bool has = w0 + lane < tot;
+            int kq0 = 0, cnt = 0, seg = 0;
+            uint32_t slot = kNoSlot;
+            double ub = INFINITY, t_out = 0.0;
+            bool last = false;
+            if (has) {
+                uint32_t cw = sh.cand[w0 + lane];
+                seg = seg0 + (int)(cw >> 3);
+                int q = (int)(cw & 7u);
+                kq0 = seg * kSeg + q * kSub;
+                cnt = min(kSub, nb - kq0);
+                WaveInfo wi = winfo[(((size_t)b * S + seg) * tiles + tile) * kSubPerSeg + q];
+                if (wi.base != kNoSlot) {
+                    slot = wi.base + (uint32_t)__popcll(wi.lanes & below_n);
+                    ub = pool_ub[slot];
+                }
+                last = kq0 + cnt == nb;
+                double tl = (double)tt[kq0 + cnt - 1];
+                t_out = last ? fmax(m.t_end, tl) : tl;
+            }
+            fallback += __popcll(__ballot(has && slot == kNoSlot));
+            bool done = !has;
+            int cert_ns = 0;            // spike count the certification last saw
+            bool open_next = false;     // the open interval after the last event is due
+            int oc = 0;                 // window lane of the sample's last sub-block
+            while (!capped) {
+                // ---- pick the next group (or the open interval)
+                bool open_grp = open_next;
+                open_next = false;
+                int c0 = 0, c1 = 0, c2 = 0, c3 = 0, G = 0;
+                if (!open_grp) {
+                    if (ns != cert_ns) {
+                        if (!done) {
+                            double dout = dref * exp(-(t_out - tref) * m.inv_tm);
+                            if (ub - dout < m.th_lo) done = true;
+                        }
+                        cert_ns = ns;
+                    }
+                    unsigned long long rem = __ballot(!done);
+                    if (!rem) break;
+                    c0 = __ffsll((long long)rem) - 1; rem &= rem - 1ull; G = 1;
+                    if (rem) { c1 = __ffsll((long long)rem) - 1; rem &= rem - 1ull; G = 2; }
+                    if (rem) { c2 = __ffsll((long long)rem) - 1; rem &= rem - 1ull; G = 3; }
+                    if (rem) { c3 = __ffsll((long long)rem) - 1; G = 4; }
+                    if (lane == c0 || (G > 1 && lane == c1) || (G > 2 && lane == c2) || (G > 3 && lane == c3))
+                        done = true;
+                    walked += G;
+                }
+                // ---- this lane's interval
+                const int c = open_grp ? oc : r == 0 ? c0 : r == 1 ? c1 : r == 2 ? c2 : c3;
+                const int g_kq0 = __shfl(kq0, c, kWave);
+                const int g_cnt = __shfl(cnt, c, kWave);
+                const uint32_t g_slot = (uint32_t)__shfl((int)slot, c, kWave);
+                const int g_seg = __shfl(seg, c, kWave);
+                bool valid;
+                double t0, L, V0 = 0.0, I0 = 0.0, V1 = 0.0, A, Dd, gb;
+                if (!open_grp) {
+                    valid = r < G && j < g_cnt;
+                    const int k = g_kq0 + (valid ? j : 0);
+                    t0 = k > 0 ? (double)tt[k - 1] : 0.0;
+                    L = (double)tt[k] - t0;
+                    Decay e = d[k];
+                    A = e.A; Dd = e.D; gb = e.g;
+                    if (valid && g_slot != kNoSlot) {
+                        const Record* rec = pool + g_slot;
+                        double2 s0 = rec->s[j];
+                        V0 = s0.x; I0 = s0.y;
+                        V1 = rec->s[j + 1].x;
+                    }
+                    if (__ballot(valid && g_slot == kNoSlot)) {
+                        if (valid && g_slot == kNoSlot) {
+                            double2 cs = entering_state(carry, ((size_t)b * S + g_seg) * N, n, g_seg * kSeg, g_kq0,
+                                                        src, d, WT, C_in, N);
+                            double V = cs.x, I = cs.y;
+                            V0 = V; I0 = I;
+                            for (int q = 0; q < kSub; ++q) {
+                                if (q < g_cnt) {
+                                    Decay eq = d[g_kq0 + q];
+                                    double Vn = eq.A * V + eq.C * I;
+                                    I = eq.D * I + (double)WT[(size_t)clamp_src(src[g_kq0 + q], C_in) * (size_t)N + n];
+                                    V = Vn;
+                                }
+                                if (q + 1 == j) { V0 = V; I0 = I; }
+                                if (q == j) V1 = V;
+                            }
+                        }
+                    }
+                } else {
+                    // Open interval (t_last, t_end] of the last sub-block, lane 0.
+                    valid = lane == 0;
+                    t0 = (double)tt[nb - 1];
+                    L = m.t_end - t0;
+                    if (g_slot != kNoSlot) {
+                        double2 s0 = pool[g_slot].s[g_cnt];
+                        V0 = s0.x; I0 = s0.y;
+                    } else {
+                        double2 s0 = entering_state(carry, ((size_t)b * S + g_seg) * N, n, g_seg * kSeg, nb, src, d,
+                                                    WT, C_in, N);
+                        V0 = s0.x; I0 = s0.y;
+                    }
+                    if (isinf(L)) {
+                        A = 0.0; Dd = 0.0; V1 = 0.0;
+                    } else {
+                        A = exp(-L * m.inv_tm);
+                        Dd = exp(-L * m.inv_ts);
+                        V1 = V0 * A + unit_kernel(m, L, A) * I0;
+                    }
+                    double gl = fmin(L, m.t_peak);
+                    gb = unit_kernel(m, gl, exp(-gl * m.inv_tm)) * (1.0 + 1e-12);
+                }
+                if (!open_grp) {
+                    // The open interval follows the group holding the last sub-block.
+                    const int lc = G > 0 ? (G == 1 ? c0 : G == 2 ? c1 : G == 3 ? c2 : c3) : 0;
+                    if (G > 0 && rl_int((int)last, lc) && m.t_end > (double)tt[nb - 1]) {
+                        open_next = true;
+                        oc = lc;
+                    }
+                }
+                // ---- deficit at the interval start, cheap bound, interval maximum
+                double Dl = (ns > 0 && valid) ? dref * exp(-(t0 - tref) * m.inv_tm) : 0.0;
+                bool pending = valid && L > 0.0 && fmax(V0 - Dl, 0.0) + fmax(I0, 0.0) * gb >= m.th_lo;
+                if (!__ballot(pending)) {
+                    if (open_grp) break;
+                    continue;
+                }
+                IntervalMax im{0.0, 1.0, 0.0, 0.0};
+                if (pending) im = interval_max(m, V0, I0, V1, L, A, Dd);
+                double lo = 0.0, Flo = V0 - m.th - Dl;
+                // ---- rounds: earliest crossing lane solves, the rest re-test
+                for (;;) {
+                    unsigned long long cm = __ballot(pending && Dl * im.a <= im.g);
+                    if (!cm) break;
+                    const int kl = __ffsll((long long)cm) - 1;
+                    double tsp = 0.0, dnew = 0.0;
+                    if (lane == kl) {
+                        double E1, E2;
+                        const double kI = m.kappa * I0;
+                        double u = root_h(m, V0 - Dl + kI, kI, lo, Flo, im.hi, im.Fhi - Dl, &E1, &E2,
+                                          nullptr);
+                        tsp = t0 + u;
+                        st[ns] = (float)tsp;
+                        if (si) si[ns] = (float)(I0 * (E2 / E1));
+                        dnew = Dl / E1 + m.dth;
+                        Dl += m.dth * E1;
+                        lo = u;
+                        Flo = -m.dth * E1;
+                    }
+                    ++ns;
+                    dref = rl_double(dnew, kl);
+                    tref = rl_double(tsp, kl);
+                    if (ns >= m.s_max) { capped = true; break; }
+                    if (lane < kl) pending = false;
+                    if (pending && lane > kl) Dl = dref * exp(-(t0 - tref) * m.inv_tm);
+                }
+                if (open_grp) break;
+            }
+        }
+        __syncthreads();                              // the list is rewritten by the next chunk
     }
-    if (W > 0 && !sp.capped) process_window();
 
     if (lane == 0) {
         if (walked) atomicAdd(&status[LIF_ST_WALKED_BLOCKS], walked);
         if (fallback) atomicAdd(&status[LIF_ST_POOL_FALLBACK], fallback);
-        out_n[idx] = sp.ns;
-        if (sp.capped) {
+        out_n[idx] = ns;
+        if (capped) {
             atomicAdd(&status[LIF_ST_CAPPED], 1);
             atomicOr(&status[LIF_ST_FLAGS], LIF_WARN_SPIKE_CAP);
         }
-        if (sp.ns) atomicAdd(&status[LIF_ST_SPIKES], sp.ns);
-        if (sp.roots) atomicAdd(&status[LIF_ST_ROOT_SOLVES], sp.roots);
+        if (ns) {
+            atomicAdd(&status[LIF_ST_SPIKES], ns);
+            atomicAdd(&status[LIF_ST_ROOT_SOLVES], ns);
+        }
     }
-    __syncthreads();
 }
 
 // Work-list driven: every wave takes neurons from the list built by k_check
@@ -805,7 +738,11 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
     }
 }
 
-// Sequential baseline: one thread per (sample, neuron), every event in order.
+// Sequential baseline (Appendix E.3): one thread per (sample, neuron)
+// consumes every event in order with the same interval test and root solve.
+// The state (V, I) is the true one, so each interval starts with deficit 0;
+// spikes inside it raise the deficit and the rest of the interval is
+// re-tested.
 __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src,
                                                    const int32_t* __restrict__ ev_n, int B, int E_max,
                                                    const float* __restrict__ WT, int C_in, int N, Model m,
@@ -821,18 +758,67 @@ __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_
     const float* tt = ev_t + (size_t)b * E_max;
     const int32_t* src = ev_src + (size_t)b * E_max;
     const Decay* d = dec + (size_t)b * E_max;
-    Sink sk;
-    sk.st = out_t + idx * (size_t)m.s_max;
-    sk.si = out_i ? out_i + idx * (size_t)m.s_max : nullptr;
-    sk.ns = 0; sk.roots = 0; sk.dref = 0.0; sk.tref = 0.0;
-    double V = 0.0, I = 0.0, t_cur = 0.0;
+    float* st = out_t + idx * (size_t)m.s_max;
+    float* si = out_i ? out_i + idx * (size_t)m.s_max : nullptr;
+    int ns = 0;
     bool capped = false;
-    for (int k = 0; k < nb; ++k) {
-        if (!advance_interval(m, V, I, t_cur, (double)tt[k], &d[k], sk)) { capped = true; break; }
-        I += (double)WT[(size_t)clamp_src(src[k], C_in) * (size_t)N + n];
+    double V = 0.0, I = 0.0, t_prev = 0.0;
+    for (int k = 0; k <= nb && !capped; ++k) {
+        double L, A, C, Dd, gb;
+        if (k < nb) {
+            Decay e = d[k];
+            A = e.A; C = e.C; Dd = e.D; gb = e.g;
+            L = (double)tt[k] - t_prev;
+        } else {
+            L = m.t_end - t_prev;                      // open interval after the last event
+            if (!(L > 0.0)) break;
+            if (isinf(L)) {
+                A = 0.0; C = 0.0; Dd = 0.0;
+            } else {
+                A = exp(-L * m.inv_tm);
+                Dd = exp(-L * m.inv_ts);
+                C = unit_kernel(m, L, A);
+            }
+            double gl = fmin(L, m.t_peak);
+            gb = unit_kernel(m, gl, exp(-gl * m.inv_tm)) * (1.0 + 1e-12);
+        }
+        double V1 = A * V + C * I;
+        if (L > 0.0 && fmax(V, 0.0) + fmax(I, 0.0) * gb >= m.th_lo) {
+            IntervalMax im = interval_max(m, V, I, V1, L, A, Dd);
+            double Dk = 0.0, lo = 0.0, Flo = V - m.th;
+            const double kI = m.kappa * I;
+            while (Dk * im.a <= im.g) {
+                double E1, E2;
+                double u = root_h(m, V - Dk + kI, kI, lo, Flo, im.hi, im.Fhi - Dk, &E1, &E2, nullptr);
+                st[ns] = (float)(t_prev + u);
+                if (si) si[ns] = (float)(I * (E2 / E1));
+                ++ns;
+                Dk += m.dth * E1;
+                lo = u;
+                Flo = -m.dth * E1;
+                if (ns >= m.s_max) { capped = true; break; }
+            }
+            V1 -= Dk * A;                               // true V at the end of the interval
+        }
+        V = V1;
+        if (k < nb) {
+            I = Dd * I + (double)WT[(size_t)clamp_src(src[k], C_in) * (size_t)N + n];
+            t_prev = (double)tt[k];
+        }
     }
-    if (!capped && !advance_interval(m, V, I, t_cur, m.t_end, nullptr, sk)) capped = true;
-    finish_neuron(m, sk, out_n + idx, capped, status);
+    out_n[idx] = ns;
+    for (int s = ns; s < m.s_max; ++s) {
+        st[s] = INFINITY;
+        if (si) si[s] = 0.0f;
+    }
+    if (capped) {
+        atomicAdd(&status[LIF_ST_CAPPED], 1);
+        atomicOr(&status[LIF_ST_FLAGS], LIF_WARN_SPIKE_CAP);
+    }
+    if (ns) {
+        atomicAdd(&status[LIF_ST_SPIKES], ns);
+        atomicAdd(&status[LIF_ST_ROOT_SOLVES], ns);
+    }
 }
 
 // ---------------------------------------------------------------------------

@@ -58,6 +58,7 @@ def test_forward_argument_errors(lib, fn):
     assert _fwd(fn, L.Params(tau_syn=0.0).c()) == L.LIF_ERR_TAU
     assert _fwd(fn, L.Params(v_th=0.0, v_reset=0.0).c()) == L.LIF_ERR_THRESHOLD
     assert _fwd(fn, L.Params(v_th=1.0, v_reset=2.0).c()) == L.LIF_ERR_THRESHOLD
+    assert _fwd(fn, L.Params(v_th=-0.5, v_reset=-1.0).c()) == L.LIF_ERR_THRESHOLD
     assert _fwd(fn, L.Params(s_max=0).c()) == L.LIF_ERR_ARG
     assert _fwd(fn, L.Params(t_end=math.nan).c()) == L.LIF_ERR_ARG
     assert _fwd(fn, L.Params(solver_reg=-1.0).c()) == L.LIF_ERR_ARG
