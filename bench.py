@@ -41,6 +41,9 @@ def main():
     ap.add_argument("--seq-steps", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-repeats", type=int, default=3)
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="only run one plain device-to-device copy of BYTES bytes (calibrates the HBM byte "
+                         "counters of a profiler against a kernel of known traffic) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the layer shards over samples "
@@ -53,6 +56,15 @@ def main():
     import workloads as W
 
     dev = torch.device("cuda:0")
+    if args.copy_probe:
+        n = args.copy_probe // 4
+        a = torch.ones(n, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        log(f"[bench] copy probe: {n * 4} bytes read, {n * 4} bytes written")
+        return
     cfg = W.config2()
     ev, WT = cfg.events, cfg.layers[0].WT
     B, E = ev.ev_t.shape

@@ -41,6 +41,11 @@ Model make_model(const lif_params& p)
     m.th_1k = p.v_th * (1.0 + m.kappa);
     m.ts_tm = p.tau_syn / p.tau_mem;
     m.dth = p.v_th - p.v_reset;
+    m.f_th = (float)m.th;
+    m.f_kappa = (float)m.kappa;
+    m.f_th1k = (float)m.th_1k;
+    m.f_ts_tm = (float)m.ts_tm;
+    m.f_inv_th = (float)m.inv_th;
     m.reg = p.solver_reg;
     m.s_max = p.s_max;
     m.flags = p.flags;

@@ -35,6 +35,7 @@ struct Model {
     double ts_tm;      // tau_s / tau_m
     double dth;        // th - vr: the drop of V at a reset
     double reg;        // backward floor on dV/dt
+    float f_th, f_kappa, f_th1k, f_ts_tm, f_inv_th;   // float32 copies for screening
     int s_max;
     uint32_t flags;
 };
@@ -112,6 +113,38 @@ __device__ __forceinline__ double exp_small(double x)
     return 1.0 + x * (1.0 + x * (0.5 + x * (1.0 / 6.0 + x * (1.0 / 24.0 + x * (1.0 / 120.0 + x * (1.0 / 720.0))))));
 }
 
+// 1/x from the hardware reciprocal refined by one Newton step (error of a
+// few ulp; used where a quotient only has to be accurate to ~1e-15).
+__device__ __forceinline__ double rcp_refined(double x)
+{
+    double r = __builtin_amdgcn_rcp(x);
+    return r * (2.0 - x * r);
+}
+
+// One step of the bracketed Newton iteration of root_h, written without
+// branches except for the rare exact re-evaluation of the exponentials.
+__device__ __forceinline__ void newton_step(const Model& m, double c0, double kI, double dF1, double dF2, double rmax,
+                                            double& u, double& lo, double& hi, double& E1, double& E2, double& d)
+{
+    const double F = c0 - m.th * E1 - kI * E2;
+    const bool pos = F >= 0.0;
+    hi = pos ? u : hi;
+    lo = pos ? lo : u;
+    const double dF = dF1 * E2 - dF2 * E1;
+    double un = u - F * rcp_refined(dF);
+    un = (dF > 0.0 && un > lo && un < hi) ? un : 0.5 * (lo + hi);
+    un = (F == 0.0 || !(hi - lo > 4e-16 * hi)) ? u : un;     // exact root, or bracket collapsed onto u
+    d = un - u;
+    if (fabs(d) * rmax <= 4e-3) {
+        E1 *= exp_small(d * m.inv_tm);
+        E2 *= exp_small(-d * m.a_rate);
+    } else {
+        E1 = exp(un * m.inv_tm);
+        E2 = exp(-un * m.a_rate);
+    }
+    u = un;
+}
+
 // Spike time inside a crossing interval (Appendix D.1, bracketed
 // Newton-Raphson): the smallest u in (lo, hi] with F(u) = h(u) - D = 0,
 //   F(u) = c0 - th e^{u/tm} - kI e^{-u r},  c0 = V0 - D + kappa I0, kI = kappa I0,
@@ -122,43 +155,28 @@ __device__ __forceinline__ double exp_small(double x)
 // whenever a Newton step leaves it (the clamp of D.1).  The two
 // exponentials are evaluated once at the start and then carried along by
 // the factor e^{step} (Taylor series) while steps are small, so a typical
-// solve costs one pair of exponentials.  Stops when a step falls below
-// 1e-9 ts (with quadratic convergence the error left is far below float64
-// resolution of the spike time) or the bracket collapses.  On return
-// *E1 = e^{u/tm} and *E2 = e^{-u r} at the returned u.
+// solve costs one pair of exponentials.  Three steps are always taken (the
+// typical count from a chord start); further steps run until a step falls
+// below 1e-9 ts (with quadratic convergence the error left is far below
+// float64 resolution of the spike time) or the bracket collapses.  On
+// return *E1 = e^{u/tm} and *E2 = e^{-u r} at the returned u.
 __device__ __forceinline__ double root_h(const Model& m, double c0, double kI, double lo, double Flo, double hi,
                                          double Fhi, double* E1o, double* E2o, int* iters)
 {
-    double u = (Fhi > Flo && Fhi < INFINITY) ? lo + (hi - lo) * (-Flo / (Fhi - Flo)) : 0.5 * (lo + hi);
+    double u = (Fhi > Flo && Fhi < INFINITY) ? lo + (hi - lo) * (-Flo * rcp_refined(Fhi - Flo)) : 0.5 * (lo + hi);
     if (!(u > lo && u <= hi)) u = 0.5 * (lo + hi);
     double E1 = exp(u * m.inv_tm), E2 = exp(-u * m.a_rate);
     const double tol = 1e-9 * m.ts;
     const double dF1 = kI * m.a_rate, dF2 = m.th * m.inv_tm;
     const double rmax = fmax(m.inv_tm, m.a_rate);
-    int it = 0;
-    while (it < 80) {
+    double d = 0.0;
+    newton_step(m, c0, kI, dF1, dF2, rmax, u, lo, hi, E1, E2, d);
+    newton_step(m, c0, kI, dF1, dF2, rmax, u, lo, hi, E1, E2, d);
+    newton_step(m, c0, kI, dF1, dF2, rmax, u, lo, hi, E1, E2, d);
+    int it = 3;
+    while (fabs(d) > tol && it < 96) {
+        newton_step(m, c0, kI, dF1, dF2, rmax, u, lo, hi, E1, E2, d);
         ++it;
-        double F = c0 - m.th * E1 - kI * E2;
-        if (F >= 0.0) {
-            hi = u;
-            if (F == 0.0) break;
-        } else {
-            lo = u;
-        }
-        if (!(hi - lo > 4e-16 * hi)) break;             // bracket collapsed onto u
-        double dF = dF1 * E2 - dF2 * E1;
-        double un = dF > 0.0 ? u - F / dF : 0.5 * (lo + hi);
-        if (!(un > lo && un < hi)) un = 0.5 * (lo + hi);
-        double d = un - u;
-        if (fabs(d) * rmax <= 4e-3) {
-            E1 *= exp_small(d * m.inv_tm);
-            E2 *= exp_small(-d * m.a_rate);
-        } else {
-            E1 = exp(un * m.inv_tm);
-            E2 = exp(-un * m.a_rate);
-        }
-        u = un;
-        if (fabs(d) <= tol) break;
     }
     *E1o = E1;
     *E2o = E2;

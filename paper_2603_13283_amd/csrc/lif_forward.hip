@@ -283,19 +283,26 @@ __global__ __launch_bounds__(64) void k_carry(const int32_t* __restrict__ ev_n, 
     int Sb = (nb + kSeg - 1) / kSeg;
     double V = 0.0, I = 0.0;
     for (int j0 = 0; j0 < Sb; j0 += kCarryBatch) {
+        // All loads of the batch are issued before the first is used (the
+        // segment maps are read as vector loads so that they do not
+        // serialise on the scalar cache).
         double2 a[kCarryBatch];
+        double mA[kCarryBatch], mC[kCarryBatch], mD[kCarryBatch];
 #pragma unroll
         for (int j = 0; j < kCarryBatch; ++j) {
             int jj = min(j0 + j, Sb - 1);
             a[j] = agg[((size_t)b * S + jj) * N + n];
+            const Decay* M = segm + (size_t)b * S + jj;
+            mA[j] = __builtin_nontemporal_load(&M->A);
+            mC[j] = __builtin_nontemporal_load(&M->C);
+            mD[j] = __builtin_nontemporal_load(&M->D);
         }
 #pragma unroll
         for (int j = 0; j < kCarryBatch; ++j) {
             if (j0 + j < Sb) {
-                Decay M = segm[(size_t)b * S + j0 + j];
                 carry[((size_t)b * S + j0 + j) * N + n] = make_double2(V, I);
-                double Vn = M.A * V + M.C * I + a[j].x;
-                I = M.D * I + a[j].y;
+                double Vn = mA[j] * V + mC[j] * I + a[j].x;
+                I = mD[j] * I + a[j].y;
                 V = Vn;
             }
         }
@@ -434,27 +441,25 @@ __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_check(
 // hold no spike.  The flagged sub-blocks are taken in time order:
 //   * Candidate list: the segments' sub-block masks are compacted into a
 //     time-ordered list in LDS with one wave prefix sum per 64 segments.
-//   * Windows of 64 candidates, one lane each, hold each sub-block's record
-//     slot, its upper bound of the no-reset V (from the check pass) and its
-//     end time.  Since every spike lowers V afterwards by
-//     (th - vr) e^{-(t - t_s)/tm}, a sub-block whose bound minus the deficit
-//     at its end stays below the threshold is certified without a walk
-//     (later spikes only deepen the deficit); this test runs on the whole
-//     window in parallel.
-//   * The earliest kGroup uncertified sub-blocks form a group, one lane per
-//     interval.  Each lane derives the interval's maximum of
-//     h(u) = (V_lin(u) - th) e^{u/tm} in closed form once (interval_max);
-//     with D the lane's deficit at its interval start, the interval crosses
-//     iff D a <= g.  A round takes the earliest crossing lane (ballot), which
-//     solves its spike time (root_h), emits the spike and raises its own
-//     deficit (the same lane is tested again for a second spike in its
-//     interval, Appendix E.2 restart); the later lanes take the new deficit
-//     with one exponential.  Rounds repeat until no lane crosses.
-// Wave-uniform state: spike count, reset deficit dref at the latest spike
-// time tref.
+//   * Chunks of kChunk candidates are processed one after the other, with
+//     the loads of the next chunk in flight meanwhile.  Lane l holds
+//     interval l % kSub of candidate 4 i + l / kSub of the chunk, i < 4 (the
+//     four "slices"), so time order is (slice, lane).
+//   * Each interval's maximum of h(u) = (V_lin(u) - th) e^{u/tm} is derived
+//     in closed form once (interval_max); with D the deficit of the spikes
+//     so far at the interval start, it crosses iff D a <= g.  A round takes
+//     the earliest crossing interval (ballots), solves its spike time
+//     (root_h) on its lane, emits the spike and raises that interval's own
+//     deficit (so it is tested again for a second spike, Appendix E.2
+//     restart); every later interval takes the new deficit with one
+//     exponential.  Rounds repeat until no interval of the chunk crosses.
+//   * The open interval after the last event is resolved last, on lane 0.
+// Wave-uniform state: spike count, reset deficit dref right after the
+// latest spike, at time tref.
 // ---------------------------------------------------------------------------
-constexpr int kGroup = kWave / kSub;             // sub-blocks per group
 constexpr int kCandCap = kWave * kSubPerSeg;     // candidates of 64 segments
+constexpr int kSlices = 4;                       // intervals per lane in a chunk
+constexpr int kChunk = kSlices * (kWave / kSub); // candidates per chunk
 
 struct ResolveLds {
     uint32_t cand[kCandCap];                     // (segment in chunk << 3) | sub-block
@@ -478,6 +483,26 @@ __device__ __noinline__ double2 entering_state(const double2* __restrict__ carry
     return make_double2(V, I);
 }
 
+// No-reset states at the start and end of interval j of a sub-block whose
+// record was not stored (pool full): walk from the segment carry.
+__device__ __noinline__ double3 walked_interval(const double2* __restrict__ carry, size_t row, int n, int seg,
+                                                int kq0, int cnt, int j, const int32_t* __restrict__ src,
+                                                const Decay* __restrict__ d, const float* __restrict__ WT, int C_in,
+                                                int N)
+{
+    double2 cs = entering_state(carry, row, n, seg * kSeg, kq0, src, d, WT, C_in, N);
+    double V = cs.x, I = cs.y, V0 = V, I0 = I, V1 = V;
+    for (int q = 0; q < kSub && q < cnt; ++q) {
+        Decay eq = d[kq0 + q];
+        double Vn = eq.A * V + eq.C * I;
+        I = eq.D * I + (double)WT[(size_t)clamp_src(src[kq0 + q], C_in) * (size_t)N + n];
+        V = Vn;
+        if (q + 1 == j) { V0 = V; I0 = I; }
+        if (q == j) V1 = V;
+    }
+    return make_double3(V0, I0, V1);
+}
+
 __device__ __forceinline__ int rl_int(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
 
 __device__ __forceinline__ double rl_double(double v, int l)
@@ -488,18 +513,128 @@ __device__ __forceinline__ double rl_double(double v, int l)
     return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
 
+// One lane's interval: start time and length, no-reset state at its start
+// (V0, I0) and end (V1), decays of its gap.
+struct Iv {
+    double t0, L, V0, I0, V1, A, D;
+    bool valid;
+};
+
+// The raw loads of one lane's interval.  Every load is unconditional (from
+// a clamped, valid address) and nothing is derived from the loaded values
+// until the interval is used: a branch around a load, or a select of its
+// value, would make the compiler wait for every outstanding load at that
+// point, which defeats the prefetch of the next chunk.
+struct IvRaw {
+    float tp, tb;       // time of the previous event and of this interval's event
+    double A, D;        // decays of the gap
+    double2 s0;         // record: no-reset state at the interval start
+    double v1;          // record: no-reset V at the interval end
+    int k, seg, kq0, cnt, j;
+    bool valid, fb;     // fb: the record pool was full for this sub-block
+};
+
+// The window's per-candidate values (one candidate per lane).
+struct WinLane {
+    int kq0, cnt, seg;
+    uint32_t slot;
+};
+
+__device__ __forceinline__ IvRaw load_slice(int cw, int nwin, const WinLane& w, int j, const float* __restrict__ tt,
+                                            const Decay* __restrict__ d, const Record* __restrict__ pool)
+{
+    IvRaw v;
+    const int c = min(cw, kWave - 1);
+    v.kq0 = __shfl(w.kq0, c, kWave);
+    v.cnt = __shfl(w.cnt, c, kWave);
+    v.seg = __shfl(w.seg, c, kWave);
+    const uint32_t slot = (uint32_t)__shfl((int)w.slot, c, kWave);
+    v.j = j;
+    v.valid = cw < nwin && j < v.cnt;
+    v.fb = v.valid && slot == kNoSlot;
+    v.k = v.kq0 + (v.valid ? j : 0);
+    v.tp = tt[max(v.k - 1, 0)];
+    v.tb = tt[v.k];
+    v.A = d[v.k].A;
+    v.D = d[v.k].D;
+    const Record* rec = pool + (v.valid && slot != kNoSlot ? slot : 0u);   // pool holds at least one record
+    v.s0 = rec->s[j];
+    v.v1 = rec->s[j + 1].x;
+    return v;
+}
+
+__device__ __forceinline__ Iv finish_slice(const IvRaw& r, int b, int n, int S, int N, int C_in,
+                                           const int32_t* __restrict__ src, const Decay* __restrict__ d,
+                                           const float* __restrict__ WT, const double2* __restrict__ carry)
+{
+    Iv v;
+    v.valid = r.valid;
+    v.t0 = r.k > 0 ? (double)r.tp : 0.0;
+    v.L = (double)r.tb - v.t0;
+    v.A = r.A;
+    v.D = r.D;
+    v.V0 = r.s0.x;
+    v.I0 = r.s0.y;
+    v.V1 = r.v1;
+    if (__ballot(r.fb) && r.fb) {
+        double3 w = walked_interval(carry, ((size_t)b * S + r.seg) * N, n, r.seg, r.kq0, r.cnt, r.j, src, d, WT,
+                                    C_in, N);
+        v.V0 = w.x; v.I0 = w.y; v.V1 = w.z;
+    }
+    return v;
+}
+
+// Float32 screen of the interval test D a <= g.  An interval whose float32
+// evaluation misses the test by more than 1e-4 of the magnitude of the
+// terms involved cannot cross: the float32 rounding of these few operations
+// and of the hardware exp/log stays below 1e-5 of that magnitude.  Only the
+// intervals that pass are evaluated in float64.
+struct Screen {
+    float g, a, s;    // g and a of the test in float32, s the magnitude of the terms of g
+};
+
+__device__ __forceinline__ Screen screen32(const Model& m, const Iv& v)
+{
+    const float V0 = (float)v.V0, I0 = (float)v.I0;
+    Screen c;
+    if (I0 > m.f_th && I0 * (float)v.D < m.f_th) {
+        const float p = __expf(m.f_ts_tm * __logf(I0 * m.f_inv_th));
+        c.g = V0 + m.f_kappa * I0 - m.f_th1k * p;
+        c.a = 1.0f;
+        c.s = fabsf(V0) + m.f_kappa * fabsf(I0) + m.f_th1k * p;
+    } else {
+        const float V1 = (float)v.V1;
+        c.g = V1 - m.f_th;
+        c.a = (float)v.A;
+        c.s = fabsf(V1) + m.f_th;
+    }
+    return c;
+}
+
+// Reset deficit at time t0 in float32 (0 before the first spike).
+__device__ __forceinline__ float deficit32(int ns, double dref, double tref, double t0, const Model& m)
+{
+    return ns > 0 ? (float)dref * __expf((float)(-(t0 - tref) * m.inv_tm)) : 0.0f;
+}
+
+__device__ __forceinline__ bool may_cross(const Screen& c, float D32)
+{
+    const float da = D32 * c.a;
+    return !(da - c.g > 1e-4f * (c.s + da));     // NaN passes (evaluated in float64)
+}
+
 __device__ void resolve_neuron(ResolveLds& sh, int b, int n, const float* __restrict__ ev_t,
                                const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
                                const float* __restrict__ WT, int C_in, int N, int tiles, int S, const Model& m,
                                const Decay* __restrict__ dec, const double2* __restrict__ carry,
                                const uint32_t* __restrict__ mask, const WaveInfo* __restrict__ winfo,
-                               const Record* __restrict__ pool, const double* __restrict__ pool_ub,
-                               float* __restrict__ out_t, int32_t* __restrict__ out_n, float* __restrict__ out_i,
-                               int32_t* __restrict__ status)
+                               const Record* __restrict__ pool, float* __restrict__ out_t, int32_t* __restrict__ out_n,
+                               float* __restrict__ out_i, int32_t* __restrict__ status)
 {
     const int tile = n / kWave;
     const unsigned long long below_n = (1ull << (n % kWave)) - 1ull;
     const int lane = (int)threadIdx.x;
+    const int j = lane % kSub, r = lane / kSub;
     const int nb = clamp_count(ev_n[b], E_max);
     const float* tt = ev_t + (size_t)b * E_max;
     const int32_t* src = ev_src + (size_t)b * E_max;
@@ -508,10 +643,11 @@ __device__ void resolve_neuron(ResolveLds& sh, int b, int n, const float* __rest
     float* st = out_t + idx * (size_t)m.s_max;
     float* si = out_i ? out_i + idx * (size_t)m.s_max : nullptr;
     const int Sb = (nb + kSeg - 1) / kSeg;
-    const int r = lane / kSub, j = lane % kSub;
 
     int ns = 0, walked = 0, fallback = 0;
-    bool capped = false;
+    bool capped = false, last_seen = false;
+    int last_seg = 0, last_cnt = 0;
+    uint32_t last_slot = kNoSlot;
     double dref = 0.0, tref = 0.0;     // deficit right after the latest spike, its time
 
     for (int seg0 = 0; seg0 < Sb && !capped; seg0 += kWave) {
@@ -525,7 +661,7 @@ __device__ void resolve_neuron(ResolveLds& sh, int b, int n, const float* __rest
             int v = __shfl_up(ex, off, kWave);
             if (lane >= off) ex += v;
         }
-        const int tot = __shfl(ex, kWave - 1, kWave);
+        const int tot = rl_int(ex, kWave - 1);
         ex -= pc;
         {
             uint32_t mm = mv;
@@ -539,165 +675,138 @@ __device__ void resolve_neuron(ResolveLds& sh, int b, int n, const float* __rest
 
         for (int w0 = 0; w0 < tot && !capped; w0 += kWave) {
             // ---- window: lane c holds candidate w0 + c
-            const bool has = w0 + lane < tot;
-            int kq0 = 0, cnt = 0, seg = 0;
-            uint32_t slot = kNoSlot;
-            double ub = INFINITY, t_out = 0.0;
+            const int nwin = min(kWave, tot - w0);
+            WinLane w{0, 0, 0, kNoSlot};
             bool last = false;
-            if (has) {
+            if (lane < nwin) {
                 uint32_t cw = sh.cand[w0 + lane];
-                seg = seg0 + (int)(cw >> 3);
+                w.seg = seg0 + (int)(cw >> 3);
                 int q = (int)(cw & 7u);
-                kq0 = seg * kSeg + q * kSub;
-                cnt = min(kSub, nb - kq0);
-                WaveInfo wi = winfo[(((size_t)b * S + seg) * tiles + tile) * kSubPerSeg + q];
-                if (wi.base != kNoSlot) {
-                    slot = wi.base + (uint32_t)__popcll(wi.lanes & below_n);
-                    ub = pool_ub[slot];
-                }
-                last = kq0 + cnt == nb;
-                double tl = (double)tt[kq0 + cnt - 1];
-                t_out = last ? fmax(m.t_end, tl) : tl;
+                w.kq0 = w.seg * kSeg + q * kSub;
+                w.cnt = min(kSub, nb - w.kq0);
+                WaveInfo wi = winfo[(((size_t)b * S + w.seg) * tiles + tile) * kSubPerSeg + q];
+                if (wi.base != kNoSlot) w.slot = wi.base + (uint32_t)__popcll(wi.lanes & below_n);
+                last = w.kq0 + w.cnt == nb;
             }
-            fallback += __popcll(__ballot(has && slot == kNoSlot));
-            bool done = !has;
-            int cert_ns = 0;            // spike count the certification last saw
-            bool open_next = false;     // the open interval after the last event is due
-            int oc = 0;                 // window lane of the sample's last sub-block
-            while (!capped) {
-                // ---- pick the next group (or the open interval)
-                bool open_grp = open_next;
-                open_next = false;
-                int c0 = 0, c1 = 0, c2 = 0, c3 = 0, G = 0;
-                if (!open_grp) {
-                    if (ns != cert_ns) {
-                        if (!done) {
-                            double dout = dref * exp(-(t_out - tref) * m.inv_tm);
-                            if (ub - dout < m.th_lo) done = true;
-                        }
-                        cert_ns = ns;
-                    }
-                    unsigned long long rem = __ballot(!done);
-                    if (!rem) break;
-                    c0 = __ffsll((long long)rem) - 1; rem &= rem - 1ull; G = 1;
-                    if (rem) { c1 = __ffsll((long long)rem) - 1; rem &= rem - 1ull; G = 2; }
-                    if (rem) { c2 = __ffsll((long long)rem) - 1; rem &= rem - 1ull; G = 3; }
-                    if (rem) { c3 = __ffsll((long long)rem) - 1; G = 4; }
-                    if (lane == c0 || (G > 1 && lane == c1) || (G > 2 && lane == c2) || (G > 3 && lane == c3))
-                        done = true;
-                    walked += G;
+            fallback += __popcll(__ballot(lane < nwin && w.slot == kNoSlot));
+            {
+                unsigned long long lm = __ballot(last);
+                if (lm) {
+                    const int ll = __ffsll((long long)lm) - 1;
+                    last_seen = true;
+                    last_seg = rl_int(w.seg, ll);
+                    last_cnt = rl_int(w.cnt, ll);
+                    last_slot = (uint32_t)rl_int((int)w.slot, ll);
                 }
-                // ---- this lane's interval
-                const int c = open_grp ? oc : r == 0 ? c0 : r == 1 ? c1 : r == 2 ? c2 : c3;
-                const int g_kq0 = __shfl(kq0, c, kWave);
-                const int g_cnt = __shfl(cnt, c, kWave);
-                const uint32_t g_slot = (uint32_t)__shfl((int)slot, c, kWave);
-                const int g_seg = __shfl(seg, c, kWave);
-                bool valid;
-                double t0, L, V0 = 0.0, I0 = 0.0, V1 = 0.0, A, Dd, gb;
-                if (!open_grp) {
-                    valid = r < G && j < g_cnt;
-                    const int k = g_kq0 + (valid ? j : 0);
-                    t0 = k > 0 ? (double)tt[k - 1] : 0.0;
-                    L = (double)tt[k] - t0;
-                    Decay e = d[k];
-                    A = e.A; Dd = e.D; gb = e.g;
-                    if (valid && g_slot != kNoSlot) {
-                        const Record* rec = pool + g_slot;
-                        double2 s0 = rec->s[j];
-                        V0 = s0.x; I0 = s0.y;
-                        V1 = rec->s[j + 1].x;
+            }
+
+            IvRaw nx[kSlices];
+#pragma unroll
+            for (int i = 0; i < kSlices; ++i) nx[i] = load_slice(i * (kWave / kSub) + r, nwin, w, j, tt, d, pool);
+            for (int c0 = 0; c0 < nwin && !capped; c0 += kChunk) {
+                IvRaw raw[kSlices];
+#pragma unroll
+                for (int i = 0; i < kSlices; ++i) raw[i] = nx[i];
+                walked += min(kChunk, nwin - c0);
+                // ---- prefetch the next chunk
+                if (c0 + kChunk < nwin) {
+#pragma unroll
+                    for (int i = 0; i < kSlices; ++i)
+                        nx[i] = load_slice(c0 + kChunk + i * (kWave / kSub) + r, nwin, w, j, tt, d, pool);
+                }
+                Iv v[kSlices];
+#pragma unroll
+                for (int i = 0; i < kSlices; ++i) v[i] = finish_slice(raw[i], b, n, S, N, C_in, src, d, WT, carry);
+                // ---- slices in time order: screen in float32 with the current
+                // deficit, then the deficit and the maximum in float64 where
+                // an interval may cross, then rounds
+#pragma unroll
+                for (int i = 0; i < kSlices; ++i) {
+                    if (capped) break;
+                    const Iv& x = v[i];
+                    const Screen sc = screen32(m, x);
+                    bool pend = x.valid && x.L > 0.0 && may_cross(sc, deficit32(ns, dref, tref, x.t0, m));
+                    if (!__ballot(pend)) continue;
+                    double Dl = 0.0, lo = 0.0, Flo = 0.0;
+                    IntervalMax im{-1.0, 1.0, 0.0, 0.0};
+                    if (pend) {
+                        Dl = ns > 0 ? dref * exp(-(x.t0 - tref) * m.inv_tm) : 0.0;
+                        im = interval_max(m, x.V0, x.I0, x.V1, x.L, x.A, x.D);
+                        Flo = x.V0 - m.th - Dl;
                     }
-                    if (__ballot(valid && g_slot == kNoSlot)) {
-                        if (valid && g_slot == kNoSlot) {
-                            double2 cs = entering_state(carry, ((size_t)b * S + g_seg) * N, n, g_seg * kSeg, g_kq0,
-                                                        src, d, WT, C_in, N);
-                            double V = cs.x, I = cs.y;
-                            V0 = V; I0 = I;
-                            for (int q = 0; q < kSub; ++q) {
-                                if (q < g_cnt) {
-                                    Decay eq = d[g_kq0 + q];
-                                    double Vn = eq.A * V + eq.C * I;
-                                    I = eq.D * I + (double)WT[(size_t)clamp_src(src[g_kq0 + q], C_in) * (size_t)N + n];
-                                    V = Vn;
-                                }
-                                if (q + 1 == j) { V0 = V; I0 = I; }
-                                if (q == j) V1 = V;
+                    // ---- rounds: the earliest crossing lane solves, the later
+                    // ones re-test
+                    for (;;) {
+                        const unsigned long long cm = __ballot(pend && Dl * im.a <= im.g);
+                        if (!cm) break;
+                        const int kl = __ffsll((long long)cm) - 1;
+                        double tsp = 0.0, dnew = 0.0;
+                        if (lane == kl) {
+                            double E1, E2;
+                            const double kI = m.kappa * x.I0;
+                            const double u = root_h(m, x.V0 - Dl + kI, kI, lo, Flo, im.hi, im.Fhi - Dl, &E1, &E2,
+                                                    nullptr);
+                            const double iE1 = rcp_refined(E1);
+                            tsp = x.t0 + u;
+                            st[ns] = (float)tsp;
+                            if (si) si[ns] = (float)(x.I0 * (E2 * iE1));
+                            dnew = Dl * iE1 + m.dth;
+                            // the same interval is tested again with the raised deficit
+                            Dl += m.dth * E1;
+                            lo = u;
+                            Flo = -m.dth * E1;
+                        }
+                        ++ns;
+                        dref = rl_double(dnew, kl);
+                        tref = rl_double(tsp, kl);
+                        if (ns >= m.s_max) { capped = true; break; }
+                        if (lane < kl) pend = false;
+                        if (pend && lane > kl) {
+                            pend = may_cross(sc, deficit32(ns, dref, tref, x.t0, m));
+                            if (__ballot(pend) && pend) {
+                                Dl = dref * exp(-(x.t0 - tref) * m.inv_tm);
+                                Flo = x.V0 - m.th - Dl;
                             }
                         }
                     }
-                } else {
-                    // Open interval (t_last, t_end] of the last sub-block, lane 0.
-                    valid = lane == 0;
-                    t0 = (double)tt[nb - 1];
-                    L = m.t_end - t0;
-                    if (g_slot != kNoSlot) {
-                        double2 s0 = pool[g_slot].s[g_cnt];
-                        V0 = s0.x; I0 = s0.y;
-                    } else {
-                        double2 s0 = entering_state(carry, ((size_t)b * S + g_seg) * N, n, g_seg * kSeg, nb, src, d,
-                                                    WT, C_in, N);
-                        V0 = s0.x; I0 = s0.y;
-                    }
-                    if (isinf(L)) {
-                        A = 0.0; Dd = 0.0; V1 = 0.0;
-                    } else {
-                        A = exp(-L * m.inv_tm);
-                        Dd = exp(-L * m.inv_ts);
-                        V1 = V0 * A + unit_kernel(m, L, A) * I0;
-                    }
-                    double gl = fmin(L, m.t_peak);
-                    gb = unit_kernel(m, gl, exp(-gl * m.inv_tm)) * (1.0 + 1e-12);
                 }
-                if (!open_grp) {
-                    // The open interval follows the group holding the last sub-block.
-                    const int lc = G > 0 ? (G == 1 ? c0 : G == 2 ? c1 : G == 3 ? c2 : c3) : 0;
-                    if (G > 0 && rl_int((int)last, lc) && m.t_end > (double)tt[nb - 1]) {
-                        open_next = true;
-                        oc = lc;
-                    }
-                }
-                // ---- deficit at the interval start, cheap bound, interval maximum
-                double Dl = (ns > 0 && valid) ? dref * exp(-(t0 - tref) * m.inv_tm) : 0.0;
-                bool pending = valid && L > 0.0 && fmax(V0 - Dl, 0.0) + fmax(I0, 0.0) * gb >= m.th_lo;
-                if (!__ballot(pending)) {
-                    if (open_grp) break;
-                    continue;
-                }
-                IntervalMax im{0.0, 1.0, 0.0, 0.0};
-                if (pending) im = interval_max(m, V0, I0, V1, L, A, Dd);
-                double lo = 0.0, Flo = V0 - m.th - Dl;
-                // ---- rounds: earliest crossing lane solves, the rest re-test
-                for (;;) {
-                    unsigned long long cm = __ballot(pending && Dl * im.a <= im.g);
-                    if (!cm) break;
-                    const int kl = __ffsll((long long)cm) - 1;
-                    double tsp = 0.0, dnew = 0.0;
-                    if (lane == kl) {
-                        double E1, E2;
-                        const double kI = m.kappa * I0;
-                        double u = root_h(m, V0 - Dl + kI, kI, lo, Flo, im.hi, im.Fhi - Dl, &E1, &E2,
-                                          nullptr);
-                        tsp = t0 + u;
-                        st[ns] = (float)tsp;
-                        if (si) si[ns] = (float)(I0 * (E2 / E1));
-                        dnew = Dl / E1 + m.dth;
-                        Dl += m.dth * E1;
-                        lo = u;
-                        Flo = -m.dth * E1;
-                    }
-                    ++ns;
-                    dref = rl_double(dnew, kl);
-                    tref = rl_double(tsp, kl);
-                    if (ns >= m.s_max) { capped = true; break; }
-                    if (lane < kl) pending = false;
-                    if (pending && lane > kl) Dl = dref * exp(-(t0 - tref) * m.inv_tm);
-                }
-                if (open_grp) break;
             }
         }
         __syncthreads();                              // the list is rewritten by the next chunk
     }
+
+    // ---- the open interval (t_last, t_end] after the last event, lane 0
+    const double t_last = nb > 0 ? (double)tt[nb - 1] : 0.0;
+    if (!capped && last_seen && m.t_end > t_last && lane == 0) {
+        double2 s0 = last_slot != kNoSlot
+                         ? pool[last_slot].s[last_cnt]
+                         : entering_state(carry, ((size_t)b * S + last_seg) * N, n, last_seg * kSeg, nb, src, d, WT,
+                                          C_in, N);
+        const double V0 = s0.x, I0 = s0.y, L = m.t_end - t_last;
+        double A = 0.0, Dd = 0.0, V1 = 0.0;
+        if (!isinf(L)) {
+            A = exp(-L * m.inv_tm);
+            Dd = exp(-L * m.inv_ts);
+            V1 = V0 * A + unit_kernel(m, L, A) * I0;
+        }
+        const IntervalMax im = interval_max(m, V0, I0, V1, L, A, Dd);
+        double Dk = ns > 0 ? dref * exp(-(t_last - tref) * m.inv_tm) : 0.0;
+        double lo = 0.0, Flo = V0 - m.th - Dk;
+        const double kI = m.kappa * I0;
+        while (Dk * im.a <= im.g) {
+            double E1, E2;
+            double u = root_h(m, V0 - Dk + kI, kI, lo, Flo, im.hi, im.Fhi - Dk, &E1, &E2, nullptr);
+            st[ns] = (float)(t_last + u);
+            if (si) si[ns] = (float)(I0 * (E2 * rcp_refined(E1)));
+            ++ns;
+            Dk += m.dth * E1;
+            lo = u;
+            Flo = -m.dth * E1;
+            if (ns >= m.s_max) { capped = true; break; }
+        }
+    }
+    ns = rl_int(ns, 0);
+    capped = rl_int((int)capped, 0) != 0;
 
     if (lane == 0) {
         if (walked) atomicAdd(&status[LIF_ST_WALKED_BLOCKS], walked);
@@ -724,7 +833,6 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
                                                    const uint32_t* __restrict__ mask,
                                                    const WaveInfo* __restrict__ winfo,
                                                    const Record* __restrict__ pool,
-                                                   const double* __restrict__ pool_ub,
                                                    const uint32_t* __restrict__ work, const uint32_t* __restrict__ nwork,
                                                    float* __restrict__ out_t, int32_t* __restrict__ out_n,
                                                    float* __restrict__ out_i, int32_t* __restrict__ status)
@@ -734,7 +842,7 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
     for (uint32_t w = blockIdx.x; w < count; w += gridDim.x) {
         uint32_t bn = work[w];
         resolve_neuron(sh, (int)(bn / (uint32_t)N), (int)(bn % (uint32_t)N), ev_t, ev_src, ev_n, E_max, WT, C_in, N,
-                       tiles, S, m, dec, carry, mask, winfo, pool, pool_ub, out_t, out_n, out_i, status);
+                       tiles, S, m, dec, carry, mask, winfo, pool, out_t, out_n, out_i, status);
     }
 }
 
@@ -848,7 +956,7 @@ FwdLayout fwd_layout(int B, int E_max, int N)
     if (const char* env = getenv("LIF_POOL_CAP")) cap = (size_t)strtoull(env, nullptr, 10);
     if (cap > 0xfffffff0ull) cap = 0xfffffff0ull;
     L.pool_cap = cap;
-    L.pool = take(cap * sizeof(Record));
+    L.pool = take((cap > 0 ? cap : 1) * sizeof(Record));   // at least one record (a safe load address)
     L.pool_ub = take(cap * sizeof(double));
     L.total = off + 256;
     return L;
@@ -916,7 +1024,7 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
         // One wave per listed neuron, as many as can be resident at once.
         unsigned grid = (unsigned)(nn < 4096 ? nn : 4096);
         TIMED_LAUNCH("resolve", k_resolve, dim3(grid), dim3(kWave), 0, stream,
-                     ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, L.S, m, dec, carry, mask, winfo, pool, pool_ub,
+                     ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, L.S, m, dec, carry, mask, winfo, pool,
                      work, nwork, out_t, out_n, out_i, status);
     }
     return check_launch();
