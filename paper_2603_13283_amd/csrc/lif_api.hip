@@ -42,10 +42,7 @@ Model make_model(const lif_params& p)
     m.ts_tm = p.tau_syn / p.tau_mem;
     m.dth = p.v_th - p.v_reset;
     m.f_th = (float)m.th;
-    m.f_kappa = (float)m.kappa;
-    m.f_th1k = (float)m.th_1k;
-    m.f_ts_tm = (float)m.ts_tm;
-    m.f_inv_th = (float)m.inv_th;
+    m.f_inv_tm = (float)m.inv_tm;
     m.reg = p.solver_reg;
     m.s_max = p.s_max;
     m.flags = p.flags;

@@ -35,7 +35,7 @@ struct Model {
     double ts_tm;      // tau_s / tau_m
     double dth;        // th - vr: the drop of V at a reset
     double reg;        // backward floor on dV/dt
-    float f_th, f_kappa, f_th1k, f_ts_tm, f_inv_th;   // float32 copies for screening
+    float f_th, f_inv_tm;   // float32 copies for screening
     int s_max;
     uint32_t flags;
 };

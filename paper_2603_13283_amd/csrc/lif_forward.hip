@@ -584,30 +584,32 @@ __device__ __forceinline__ Iv finish_slice(const IvRaw& r, int b, int n, int S, 
     return v;
 }
 
-// Float32 screen of the interval test D a <= g.  An interval whose float32
-// evaluation misses the test by more than 1e-4 of the magnitude of the
-// terms involved cannot cross: the float32 rounding of these few operations
-// and of the hardware exp/log stays below 1e-5 of that magnitude.  Only the
-// intervals that pass are evaluated in float64.
+// Float32 screen of the interval test D a <= g, with no transcendental
+// function.  The crossing condition is D <= max of h over the interval.
+// h(L) = (V_lin(L) - th) e^{L/tm} is known exactly (the end test
+// D e^{-L/tm} <= V_lin(L) - th); when I0 > th, h is concave with
+// h'(0) = (I0 - th)/tm > 0, so its tangent at 0 bounds it over the whole
+// interval: max h <= V0 - th + (I0 - th) L / tm.  An interval that misses
+// both tests by more than 1e-4 of the magnitude of their terms (far above
+// float32 rounding of these few operations and of the hardware exp used for
+// D) cannot cross; only the others are tested exactly in float64.
 struct Screen {
-    float g, a, s;    // g and a of the test in float32, s the magnitude of the terms of g
+    float e_rhs, e_a, e_s;   // end test:     D e_a <= e_rhs  (+ margin on e_s)
+    float i_rhs, i_s;        // tangent test: D <= i_rhs      (+ margin on i_s), when I0 > th
+    bool tangent;
 };
 
 __device__ __forceinline__ Screen screen32(const Model& m, const Iv& v)
 {
-    const float V0 = (float)v.V0, I0 = (float)v.I0;
+    const float V0 = (float)v.V0, I0 = (float)v.I0, V1 = (float)v.V1, L = (float)v.L;
+    const float th = m.f_th, Lt = L * m.f_inv_tm;
     Screen c;
-    if (I0 > m.f_th && I0 * (float)v.D < m.f_th) {
-        const float p = __expf(m.f_ts_tm * __logf(I0 * m.f_inv_th));
-        c.g = V0 + m.f_kappa * I0 - m.f_th1k * p;
-        c.a = 1.0f;
-        c.s = fabsf(V0) + m.f_kappa * fabsf(I0) + m.f_th1k * p;
-    } else {
-        const float V1 = (float)v.V1;
-        c.g = V1 - m.f_th;
-        c.a = (float)v.A;
-        c.s = fabsf(V1) + m.f_th;
-    }
+    c.e_rhs = V1 - th;
+    c.e_a = (float)v.A;
+    c.e_s = fabsf(V1) + th;
+    c.tangent = I0 > th * (1.0f - 1e-5f);
+    c.i_rhs = (V0 - th) + (I0 - th) * Lt;
+    c.i_s = fabsf(V0) + th + fabsf(I0) * Lt;
     return c;
 }
 
@@ -617,10 +619,12 @@ __device__ __forceinline__ float deficit32(int ns, double dref, double tref, dou
     return ns > 0 ? (float)dref * __expf((float)(-(t0 - tref) * m.inv_tm)) : 0.0f;
 }
 
-__device__ __forceinline__ bool may_cross(const Screen& c, float D32)
+__device__ __forceinline__ bool may_cross(const Screen& c, float D)
 {
-    const float da = D32 * c.a;
-    return !(da - c.g > 1e-4f * (c.s + da));     // NaN passes (evaluated in float64)
+    const float da = D * c.e_a;
+    const bool end_miss = da - c.e_rhs > 1e-4f * (c.e_s + da);
+    const bool tan_miss = !c.tangent || D - c.i_rhs > 1e-4f * (c.i_s + D);
+    return !(end_miss && tan_miss);      // NaN passes (tested in float64)
 }
 
 __device__ void resolve_neuron(ResolveLds& sh, int b, int n, const float* __restrict__ ev_t,
