@@ -33,6 +33,40 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_forward_700x256_b32.txt")
+KERNEL_SOURCES = ("lif_forward.hip", "lif_common.hpp", "lif_host.hpp")
+
+
+def kernel_sources_sha256() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2603_13283_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` from the rocprofv3 FETCH_SIZE and
+    WRITE_SIZE runs summarised in profiles/ (already scaled by the copy-probe
+    factors), or None when they are missing or were taken on other kernel
+    sources than the ones built now."""
+    try:
+        lines = open(TRAFFIC_FILE).read().splitlines()
+    except OSError:
+        return None
+    sha = None
+    for ln in lines:
+        if ln.startswith("sources_sha256:"):
+            sha = ln.split(":", 1)[1].strip()
+        parts = ln.split()
+        if sha and len(parts) == 3 and parts[0] == kernel:
+            if sha != kernel_sources_sha256():
+                return None
+            return int(parts[1]) + int(parts[2])
+    return None
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -40,7 +74,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--seq-steps", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-repeats", type=int, default=3)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="CPU oracle baseline: repeat the full-batch forward until this much time has passed")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run one plain device-to-device copy of BYTES bytes (calibrates the HBM byte "
                          "counters of a profiler against a kernel of known traffic) and exit")
@@ -81,38 +116,80 @@ def main():
     log(f"[bench] {cfg.name}: B={B} E_max={E} events={total_ev} N={N} neuron-events={neuron_events} "
         f"lib={lif.lif_version()}")
 
-    # ---- warmup (also fills the kernel timer's event pool)
+    # ---- per-kernel durations: eager launches bracketed by HIP events on the
+    # launch stream (the library's kernel timer)
     lif.lif_timer_enable(True)
     for _ in range(args.warmup):
         lif.forward(d_t, d_s, d_n, d_W, P, ws=ws, out=out)
     torch.cuda.synchronize()
-
-    # ---- timed forward steps, kernel timer live on the same stream
     lif.lif_timer_enable(True)
+    for _ in range(args.steps):
+        lif.forward(d_t, d_s, d_n, d_W, P, ws=ws, out=out)
+    torch.cuda.synchronize()
+    kern = lif.lif_timer_read()
+    lif.lif_timer_enable(False)
+    log(f"[bench] kernels: " + ", ".join(f"{k}={v[0] / v[1] * 1e3:.1f}us" for k, v in kern.items()))
+
+    # ---- eager forward steps (no timer)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
         lif.forward(d_t, d_s, d_n, d_W, P, ws=ws, out=out)
     torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    kern = lif.lif_timer_read()
-    lif.lif_timer_enable(False)
-    ms_step = elapsed / args.steps * 1e3
-    value = neuron_events * args.steps / elapsed
+    eager_ms = (time.perf_counter() - t0) / args.steps * 1e3
+    ref_t, ref_n, ref_st = out.out_t.clone(), out.out_n.clone(), out.status.clone()
+
+    # ---- timed steps: the forward call captured once in a HIP graph and
+    # replayed (the call allocates nothing and issues only kernel launches)
+    gstream = torch.cuda.Stream()
+    gstream.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(gstream):
+        lif.forward(d_t, d_s, d_n, d_W, P, ws=ws, out=out)
+    torch.cuda.current_stream().wait_stream(gstream)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        lif.forward(d_t, d_s, d_n, d_W, P, ws=ws, out=out)
+    for _ in range(args.warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    assert torch.equal(out.out_t, ref_t) and torch.equal(out.out_n, ref_n) and torch.equal(out.status, ref_st), \
+        "graph replay differs from the eager forward"
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    graph_ms = (time.perf_counter() - t0) / args.steps * 1e3
+    # The reported step is the plain (eager) library call.
+    ms_step = eager_ms
+    value = neuron_events / (ms_step * 1e-3)
     status = out.status.cpu().numpy().tolist()
     n_spikes = int(out.out_n.sum().item())
-    log(f"[bench] forward {ms_step * 1e3:.1f} us/step, {value:.3e} neuron-events/s, status {status}")
-    log(f"[bench] kernels: " + ", ".join(f"{k}={v[0] / v[1] * 1e3:.1f}us" for k, v in kern.items()))
+    log(f"[bench] forward {ms_step * 1e3:.1f} us/step eager, {graph_ms * 1e3:.1f} us/step graph replay, "
+        f"{value:.3e} neuron-events/s, status {status}")
 
-    # ---- roofline of the dominant kernel: algorithmic bytes are the event
-    # record (time + source, 8 B per event) and one float32 weight per
-    # neuron-event, plus the spike outputs for the resolve pass.
-    dom = max(kern.items(), key=lambda kv: kv[1][0])
-    dom_name, (dom_ms, dom_n) = dom
-    dom_us = dom_ms / dom_n * 1e3
-    alg_bytes = total_ev * (8 + 4 * N)
+    # ---- roofline of the dominant kernel.  Algorithmic bytes per launch:
+    #   aggregate, check: every event record (time + source, 8 B) and one
+    #     float32 weight per neuron-event (4 B) -- both passes gather the
+    #     whole W^T row slice of every event;
+    #   carry: one float64 (V, I) aggregate read and one carry written per
+    #     (sample, segment, neuron);
+    #   resolve: per walked sub-block its record (17 float64 pairs), the 17
+    #     event times and 16 decay pairs, plus 8 B per spike and 4 B per count.
+    S = (E + 127) // 128
+    walked = status[4]
+    alg = {"aggregate": total_ev * (8 + 4 * N),
+           "check": total_ev * (8 + 4 * N),
+           "carry": B * S * N * 32,
+           "resolve": walked * (17 * 16 + 17 * 4 + 16 * 16) + n_spikes * 8 + B * N * 4}
+    kern_us = {k: v[0] / v[1] * 1e3 for k, v in kern.items()}
+    dom_name = max(kern_us, key=kern_us.get)
+    dom_us = kern_us[dom_name]
+    alg_bytes = alg.get(dom_name, 0)
     achieved = alg_bytes / (dom_us * 1e-6) / 1e9
     fwd_alg_bytes = total_ev * (8 + 4 * N) + B * N * 4 + n_spikes * 8
+    traffic = measured_traffic(dom_name)
 
     # ---- sequential GPU baseline (same ABI, same inputs)
     seq = lif.forward(d_t, d_s, d_n, d_W, P, sequential=True, ws=ws)
@@ -149,13 +226,15 @@ def main():
         ncores = max(1, min(int(ncores), 16))
         OP = oracle.LifParams(s_max=64)
         oracle.forward(ev.ev_t[:1], ev.ev_src[:1], ev.ev_n[:1], WT, OP, nthreads=ncores)
+        reps = 0
         c0 = time.perf_counter()
-        for _ in range(args.cpu_repeats):
+        while reps < 3 or time.perf_counter() - c0 < args.cpu_seconds:
             oracle.forward(ev.ev_t, ev.ev_src, ev.ev_n, WT, OP, nthreads=ncores)
-        cpu_s = (time.perf_counter() - c0) / args.cpu_repeats
+            reps += 1
+        cpu_s = (time.perf_counter() - c0) / reps
         cpu = {"value": neuron_events / cpu_s, "unit": "neuron-events/s", "cores": ncores, "kind": "oracle",
-               "sample": f"full batch (32 samples x 256 neurons, {total_ev} events), "
-                         f"{args.cpu_repeats} repeats, {cpu_s:.3f} s each"}
+               "sample": f"the full workload (32 samples x 256 neurons, {total_ev} events) repeated {reps} times, "
+                         f"{cpu_s:.3f} s each, float64, one thread per core over (sample, neuron)"}
         log(f"[bench] cpu oracle {cpu_s:.3f} s/forward on {ncores} threads")
 
     line = {
@@ -166,6 +245,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_step,
+        "ms_per_step_graph_replay": graph_ms,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -177,10 +257,10 @@ def main():
                    "batch": B, "c_in": C, "n_out": N, "events": total_ev, "e_max": E,
                    "neuron_events": neuron_events, "spikes": n_spikes, "s_max": P.s_max},
         "roofline": {"bound": "hbm", "kernel": dom_name, "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "alg_bytes_per_launch": alg_bytes, "kernel_us": dom_us},
         "hbm_frac_forward": fwd_alg_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
-        "kernels_us": {k: v[0] / v[1] * 1e3 for k, v in kern.items()},
+        "kernels_us": kern_us,
         "sequential_ms": seq_ms,
         "speedup_vs_sequential": seq_ms / ms_step,
         "backward_ms": bwd_ms,

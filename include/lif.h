@@ -182,9 +182,10 @@ int lif_first_spike_ce(const float* out_t, const int32_t* out_n, int B, int N, i
 
 /* --------------------------------------------------------------------- */
 /* Optional kernel timer (host-side state, off by default).  When enabled, */
-/* every kernel launched by this library is bracketed by HIP events on its */
-/* stream; lif_timer_read synchronises on the recorded events and returns  */
-/* per-kernel totals.                                                      */
+/* every kernel launched by this library is launched with a pair of HIP    */
+/* events that its own dispatch records (hipExtLaunchKernel), so each      */
+/* elapsed time is the kernel's execution on its stream; lif_timer_read    */
+/* synchronises on the recorded events and returns per-kernel totals.      */
 /*   lif_timer_enable(1) resets and starts recording, (0) stops.           */
 /*   lif_timer_read fills up to `cap` entries: names[j] (static strings),  */
 /*   total_ms[j], launches[j]; returns the number of kernels seen.         */

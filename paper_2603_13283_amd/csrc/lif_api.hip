@@ -97,19 +97,15 @@ hipEvent_t pool_get()
 
 bool timer_on() { return g_on; }
 
-void timer_begin(const char* name, hipStream_t s)
+bool timer_events(const char* name, hipEvent_t* start, hipEvent_t* stop)
 {
     std::lock_guard<std::mutex> lk(g_mu);
     hipEvent_t a = pool_get(), b = pool_get();
-    if (!a || !b) return;
-    (void)hipEventRecord(a, s);
+    if (!a || !b) return false;
     g_recs.push_back({name, a, b});
-}
-
-void timer_end(hipStream_t s)
-{
-    std::lock_guard<std::mutex> lk(g_mu);
-    if (!g_recs.empty()) (void)hipEventRecord(g_recs.back().b, s);
+    *start = a;
+    *stop = b;
+    return true;
 }
 
 }  // namespace lif

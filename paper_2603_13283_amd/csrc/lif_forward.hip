@@ -259,49 +259,102 @@ __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_aggregate(
 }
 
 // Exclusive scan over segments of the Combine of Eq. affine:
-// s_in(j+1) = M(T_j) s_in(j) + b_j, with s_in(0) = (0, 0).  The segment
-// aggregates are fetched kCarryBatch at a time so their loads overlap.
+// s_in(j+1) = M(T_j) s_in(j) + b_j, with s_in(0) = (0, 0).  A workgroup of
+// kCarryWaves waves takes one (sample, 64-neuron tile); lanes are neurons
+// and wave w the w-th contiguous range of segments.  Each wave folds its
+// range from the zero state (the segment aggregates are fetched
+// kCarryBatch at a time so that their loads overlap), the range totals are
+// combined across waves in LDS (the maps compose in closed form), and each
+// wave walks its range again from its incoming state, writing the carries.
 constexpr int kCarryBatch = 16;
+constexpr int kCarryWaves = 4;
 
-__global__ __launch_bounds__(64) void k_carry(const int32_t* __restrict__ ev_n, int B, int E_max, int N, int S,
-                                               const Decay* __restrict__ segm, const double2* __restrict__ agg,
-                                               double2* __restrict__ carry, int32_t* __restrict__ status,
-                                               int s_max, float* __restrict__ out_t, int32_t* __restrict__ out_n,
-                                               float* __restrict__ out_i, uint32_t* __restrict__ listed,
-                                               uint32_t* __restrict__ counters)
+struct Affine {               // the map s -> M s + b of a range of segments
+    double A, C, D;           // M = [[A, C], [0, D]] (wave-uniform)
+    double V, I;              // b (per neuron)
+};
+
+__device__ __forceinline__ void carry_batch(const double2* __restrict__ agg, const Decay* __restrict__ segm,
+                                            size_t row0, size_t seg_row, int N, int n, int j0, int j1,
+                                            double2 (&a)[kCarryBatch], double (&mA)[kCarryBatch],
+                                            double (&mC)[kCarryBatch], double (&mD)[kCarryBatch])
 {
-    size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const size_t nn = (size_t)B * (size_t)N;
-    if (idx >= nn) return;
-    int b = (int)(idx / (size_t)N), n = (int)(idx % (size_t)N);
-    out_n[idx] = 0;
-    listed[idx] = 0u;
-    if (n == 0) counters[1 + b] = 0u;          // record pool use of sample b
-    if (idx == 0) counters[0] = 0u;            // work-list length
-    int nb = clamp_count(ev_n[b], E_max);
-    if (n == 0) atomicAdd(&status[LIF_ST_EVENTS], nb);
-    int Sb = (nb + kSeg - 1) / kSeg;
-    double V = 0.0, I = 0.0;
-    for (int j0 = 0; j0 < Sb; j0 += kCarryBatch) {
-        // All loads of the batch are issued before the first is used (the
-        // segment maps are read as vector loads so that they do not
-        // serialise on the scalar cache).
-        double2 a[kCarryBatch];
-        double mA[kCarryBatch], mC[kCarryBatch], mD[kCarryBatch];
+#pragma unroll
+    for (int j = 0; j < kCarryBatch; ++j) {
+        const int jj = min(j0 + j, j1 - 1);
+        a[j] = agg[(row0 + (size_t)jj) * N + n];
+        const Decay* M = segm + seg_row + jj;
+        mA[j] = __builtin_nontemporal_load(&M->A);
+        mC[j] = __builtin_nontemporal_load(&M->C);
+        mD[j] = __builtin_nontemporal_load(&M->D);
+    }
+}
+
+__global__ __launch_bounds__(kWave * kCarryWaves) void k_carry(
+    const int32_t* __restrict__ ev_n, int B, int E_max, int N, int tiles, int S, const Decay* __restrict__ segm,
+    const double2* __restrict__ agg, double2* __restrict__ carry, int32_t* __restrict__ status,
+    int32_t* __restrict__ out_n, uint32_t* __restrict__ listed, uint32_t* __restrict__ counters)
+{
+    __shared__ Affine tot[kCarryWaves][kWave];
+    const int b = blockIdx.x / tiles, tile = blockIdx.x % tiles;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int n = tile * kWave + lane;
+    const bool live = n < N;
+    const int nc = live ? n : N - 1;
+    const size_t idx = (size_t)b * N + nc;
+    if (wave == 0 && live) {
+        out_n[idx] = 0;
+        listed[idx] = 0u;
+    }
+    const int nb = clamp_count(ev_n[b], E_max);
+    if (threadIdx.x == 0 && tile == 0) {
+        counters[1 + b] = 0u;                   // record pool use of sample b
+        atomicAdd(&status[LIF_ST_EVENTS], nb);
+        if (b == 0) counters[0] = 0u;           // work-list length
+    }
+    const int Sb = (nb + kSeg - 1) / kSeg;
+    const int per = (Sb + kCarryWaves - 1) / kCarryWaves;
+    const int j_lo = min(wave * per, Sb), j_hi = min(j_lo + per, Sb);
+    const size_t row0 = (size_t)b * S, seg_row = (size_t)b * S;
+
+    // ---- fold this wave's range from the zero state
+    Affine f{1.0, 0.0, 1.0, 0.0, 0.0};
+    double2 a[kCarryBatch];
+    double mA[kCarryBatch], mC[kCarryBatch], mD[kCarryBatch];
+    for (int j0 = j_lo; j0 < j_hi; j0 += kCarryBatch) {
+        carry_batch(agg, segm, row0, seg_row, N, nc, j0, j_hi, a, mA, mC, mD);
 #pragma unroll
         for (int j = 0; j < kCarryBatch; ++j) {
-            int jj = min(j0 + j, Sb - 1);
-            a[j] = agg[((size_t)b * S + jj) * N + n];
-            const Decay* M = segm + (size_t)b * S + jj;
-            mA[j] = __builtin_nontemporal_load(&M->A);
-            mC[j] = __builtin_nontemporal_load(&M->C);
-            mD[j] = __builtin_nontemporal_load(&M->D);
+            if (j0 + j < j_hi) {
+                const double Vn = mA[j] * f.V + mC[j] * f.I + a[j].x;
+                f.I = mD[j] * f.I + a[j].y;
+                f.V = Vn;
+                // M_j composed after the range so far: [[A_j A, A_j C + C_j D], [0, D_j D]]
+                const double Cn = mA[j] * f.C + mC[j] * f.D;
+                f.A *= mA[j];
+                f.D *= mD[j];
+                f.C = Cn;
+            }
         }
+    }
+    tot[wave][lane] = f;
+    __syncthreads();
+    // ---- incoming state: the earlier ranges applied in order to zero
+    double V = 0.0, I = 0.0;
+    for (int w = 0; w < wave; ++w) {
+        const Affine g = tot[w][lane];
+        const double Vn = g.A * V + g.C * I + g.V;
+        I = g.D * I + g.I;
+        V = Vn;
+    }
+    // ---- walk the range again, writing the carry entering each segment
+    for (int j0 = j_lo; j0 < j_hi; j0 += kCarryBatch) {
+        carry_batch(agg, segm, row0, seg_row, N, nc, j0, j_hi, a, mA, mC, mD);
 #pragma unroll
         for (int j = 0; j < kCarryBatch; ++j) {
-            if (j0 + j < Sb) {
-                carry[((size_t)b * S + j0 + j) * N + n] = make_double2(V, I);
-                double Vn = mA[j] * V + mC[j] * I + a[j].x;
+            if (j0 + j < j_hi) {
+                if (live) carry[(row0 + (size_t)(j0 + j)) * N + n] = make_double2(V, I);
+                const double Vn = mA[j] * V + mC[j] * I + a[j].x;
                 I = mD[j] * I + a[j].y;
                 V = Vn;
             }
@@ -1017,9 +1070,8 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
         return check_launch();
     }
     if (nn)
-        TIMED_LAUNCH("carry", k_carry, dim3((unsigned)((nn + 63) / 64)), dim3(64), 0, stream,
-                     ev_n, B, E_max, N, L.S, segm, agg, carry, status, m.s_max, out_t, out_n, out_i, listed,
-                     counters);
+        TIMED_LAUNCH("carry", k_carry, dim3((unsigned)((size_t)B * tiles)), dim3(kWave * kCarryWaves), 0, stream,
+                     ev_n, B, E_max, N, tiles, L.S, segm, agg, carry, status, out_n, listed, counters);
     if (total) {
         TIMED_LAUNCH("check", k_check, dim3((unsigned)total), dim3(kWave * kTilesPerBlock), 0, stream,
                      ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, tgroups, L.S, (int)total, m, dec, carry, mask,

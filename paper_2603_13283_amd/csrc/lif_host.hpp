@@ -2,6 +2,7 @@
 // argument validation, model constants, workspace layout, launch timing.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -26,17 +27,19 @@ int validate_forward_args(const float* ev_t, const int32_t* ev_src, const int32_
                           const int32_t* out_n, const int32_t* status, const void* ws);
 int check_launch();
 
-// Kernel timer (lif_timer_*): records a HIP event pair around each launch.
-void timer_begin(const char* name, hipStream_t s);
-void timer_end(hipStream_t s);
+// Kernel timer (lif_timer_*): a HIP event pair per launch, recorded by the
+// dispatch of the kernel itself (hipExtLaunchKernelGGL), so that the elapsed
+// time is the kernel's own execution.
+bool timer_events(const char* name, hipEvent_t* start, hipEvent_t* stop);
 bool timer_on();
 
 }  // namespace lif
 
-#define TIMED_LAUNCH(name, kern, grid, block, shmem, stream, ...)                \
-    do {                                                                         \
-        bool _t = ::lif::timer_on();                                             \
-        if (_t) ::lif::timer_begin(name, stream);                                \
-        hipLaunchKernelGGL(kern, grid, block, shmem, stream, __VA_ARGS__);       \
-        if (_t) ::lif::timer_end(stream);                                        \
+#define TIMED_LAUNCH(name, kern, grid, block, shmem, stream, ...)                      \
+    do {                                                                               \
+        hipEvent_t _a, _b;                                                             \
+        if (::lif::timer_on() && ::lif::timer_events(name, &_a, &_b))                  \
+            hipExtLaunchKernelGGL(kern, grid, block, shmem, stream, _a, _b, 0, __VA_ARGS__); \
+        else                                                                           \
+            hipLaunchKernelGGL(kern, grid, block, shmem, stream, __VA_ARGS__);         \
     } while (0)

@@ -141,6 +141,46 @@ def test_determinism(env):
     assert torch.equal(a.out_t, b.out_t) and torch.equal(a.out_n, b.out_n) and torch.equal(a.out_i, b.out_i)
 
 
+def test_graph_replay_matches_eager(env):
+    """The forward call captured in a HIP graph and replayed several times,
+    with other eager forwards (different inputs) and synchronisations
+    between the replays, reproduces the eager result every time."""
+    torch, lif = env
+    cfg = W.random_small(12, B=4, C=40, N=150, n_events=1200, T=0.6, gain=14.0)
+    other = W.random_small(13, B=2, C=40, N=150, n_events=700, T=0.6, gain=14.0)
+    ev, WT = cfg.events, cfg.layers[0].WT
+    d = [_dev(torch, a) for a in (ev.ev_t, ev.ev_src, ev.ev_n, WT)]
+    do = [_dev(torch, a) for a in (other.events.ev_t, other.events.ev_src, other.events.ev_n, other.layers[0].WT)]
+    P = lif.Params()
+    ref = lif.forward(*d, P)
+    torch.cuda.synchronize()
+    B, E = ev.ev_t.shape
+    ws = torch.empty(lif.lif_layer_forward_workspace_size(B, E, WT.shape[0], WT.shape[1], P.c()),
+                     dtype=torch.uint8, device="cuda:0")
+    out = lif.forward(*d, P, ws=ws)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        lif.forward(*d, P, ws=ws, out=out)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        lif.forward(*d, P, ws=ws, out=out)
+    for rep in range(4):
+        out.out_t.fill_(-1.0)
+        out.out_n.fill_(-1)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out.out_t, ref.out_t), rep
+        assert torch.equal(out.out_n, ref.out_n), rep
+        assert torch.equal(out.out_i, ref.out_i), rep
+        assert torch.equal(out.status, ref.status), rep
+        lif.forward(*do, P)                  # eager work between replays
+        torch.cuda.synchronize()
+
+
 def test_validation_flags(env):
     torch, lif = env
     ev = W.pack_events([np.array([0.1, 0.2, 0.3])], [np.array([0, 1, 2])])
