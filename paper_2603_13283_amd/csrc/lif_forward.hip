@@ -53,6 +53,7 @@ struct alignas(16) WaveInfo {
     uint32_t pad;
 };
 constexpr uint32_t kNoSlot = 0xffffffffu;
+constexpr uint32_t kInvalid = 0xffffffffu;   // work-list entry of a neuron already listed
 
 // Workgroup index -> work index such that each of the 8 XCDs (which receive
 // workgroups round-robin) processes a contiguous, sample-major range: the
@@ -134,6 +135,7 @@ __global__ __launch_bounds__(256) void k_validate(const float* __restrict__ ev_t
 // events are walked.
 // ---------------------------------------------------------------------------
 constexpr int kTilesPerBlock = 4;
+constexpr int kPoolLocal = 16;     // record slots owned by each check wave
 constexpr int kSrcRegs = kSeg / kWave;
 
 struct SegCoords {
@@ -182,6 +184,22 @@ __device__ __forceinline__ void load_sub_weights(const SrcRegs& sr, const float*
         int sj = __builtin_amdgcn_readlane(sr.v[e / kWave], e % kWave);
         w[j] = e < cnt ? wcol[(size_t)sj * (size_t)N] : 0.0f;
     }
+}
+
+// The same, with the sources read as wave-uniform (scalar) loads.  All
+// sixteen source loads are issued before the first is used (past cnt the
+// last event is read again and its weight discarded).
+__device__ __forceinline__ void load_sub_weights_s(const int32_t* __restrict__ sseg, const float* __restrict__ wcol,
+                                                   int N, int C_in, int cnt, int q, float (&w)[kSub])
+{
+    int sj[kSub];
+#pragma unroll
+    for (int j = 0; j < kSub; ++j) sj[j] = sseg[min(q * kSub + j, cnt - 1)];
+#pragma unroll
+    for (int j = 0; j < kSub; ++j) w[j] = wcol[(size_t)clamp_src(sj[j], C_in) * (size_t)N];
+#pragma unroll
+    for (int j = 0; j < kSub; ++j)
+        if (q * kSub + j >= cnt) w[j] = 0.0f;
 }
 
 __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_aggregate(
@@ -369,33 +387,40 @@ __global__ __launch_bounds__(kWave * kCarryWaves) void k_carry(
 // term), so a sub-block whose no-reset bound stays below the threshold holds
 // no spike whatever happened before it.  Sub-blocks whose bound reaches it
 // get a record for the resolve pass, which applies the exact interval rule.
+__device__ __forceinline__ int B_of(int total, int tgroups, int S) { return total / (tgroups * S); }
+
 __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_check(
     const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
     const float* __restrict__ WT, int C_in, int N, int tiles, int tgroups, int S, int total, Model m,
     const Decay* __restrict__ dec, const double2* __restrict__ carry, uint32_t* __restrict__ mask,
-    WaveInfo* __restrict__ winfo, Record* __restrict__ pool, double* __restrict__ pool_ub,
-    uint32_t* __restrict__ pool_count, uint32_t pool_cap, uint32_t* __restrict__ listed, uint32_t* __restrict__ work,
-    uint32_t* __restrict__ nwork, int32_t* __restrict__ status)
+    WaveInfo* __restrict__ winfo, Record* __restrict__ pool,
+    uint32_t* __restrict__ pool_count, uint32_t pool_local, uint32_t pool_cap, uint32_t* __restrict__ listed,
+    uint32_t* __restrict__ work, uint32_t* __restrict__ nwork, int32_t* __restrict__ status)
 {
-    __shared__ Decay sd[kSeg];
+    // The segment's decays and sources are wave-uniform: they are read with
+    // scalar loads and used as scalar operands.
     const SegCoords c = seg_coords(total, tgroups, S, ev_n, E_max, N);
-    if (c.k0 >= c.nb) return;                        // uniform over the workgroup
+    if (c.k0 >= c.nb || c.tile >= tiles) return;
     const float* tt = ev_t + (size_t)c.b * E_max;
-    if ((int)threadIdx.x < c.cnt) sd[threadIdx.x] = dec[(size_t)c.b * E_max + c.k0 + threadIdx.x];
-    __syncthreads();
-    if (c.tile >= tiles) return;
     const int lane = c.lane, n = c.n, nb = c.nb, k0 = c.k0, cnt_seg = c.cnt;
     const float* wcol = WT + c.nc;
-    const SrcRegs sr = load_sources(ev_src + (size_t)c.b * E_max + k0, cnt_seg, lane, C_in);
+    const Decay* __restrict__ sd = dec + (size_t)c.b * E_max + k0;
+    const int32_t* __restrict__ sseg = ev_src + (size_t)c.b * E_max + k0;
     const size_t row = ((size_t)c.b * S + c.seg) * N;
     double2 c0 = carry[row + c.nc];
     double V = c0.x, I = c0.y;
     uint32_t msk = 0;
     int ncand = 0;
     const unsigned long long below = (1ull << lane) - 1ull;
+    // Records go first to this wave's own block of pool_local slots (no
+    // atomic), then to the per-sample overflow slices (one atomic each).
+    const uint32_t wave_id = (uint32_t)(((size_t)c.b * S + c.seg) * tiles + c.tile);
+    const uint32_t local0 = wave_id * pool_local;
+    const uint32_t overflow0 = (uint32_t)((size_t)B_of(total, tgroups, S) * S * tiles * pool_local);
+    uint32_t used = 0;
     float wn[kSub], wn2[kSub];
-    load_sub_weights(sr, wcol, N, cnt_seg, 0, wn);
-    if (kSub < cnt_seg) load_sub_weights(sr, wcol, N, cnt_seg, 1, wn2);
+    load_sub_weights_s(sseg, wcol, N, C_in, cnt_seg, 0, wn);
+    if (kSub < cnt_seg) load_sub_weights_s(sseg, wcol, N, C_in, cnt_seg, 1, wn2);
 #pragma unroll
     for (int q = 0; q < kSubPerSeg; ++q) {
         if (q * kSub < cnt_seg) {
@@ -403,7 +428,8 @@ __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_check(
             float w[kSub];
 #pragma unroll
             for (int j = 0; j < kSub; ++j) { w[j] = wn[j]; wn[j] = wn2[j]; }
-            if (q + 2 < kSubPerSeg && (q + 2) * kSub < cnt_seg) load_sub_weights(sr, wcol, N, cnt_seg, q + 2, wn2);
+            if (q + 2 < kSubPerSeg && (q + 2) * kSub < cnt_seg)
+                load_sub_weights_s(sseg, wcol, N, C_in, cnt_seg, q + 2, wn2);
             double Vin = V, Iin = I, ub = -INFINITY;
             if (cnt == kSub) {                         // full sub-block: straight-line code
 #pragma unroll
@@ -435,14 +461,22 @@ __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_check(
             bool surv = ub >= m.th_lo && n < N;
             unsigned long long lanes = __ballot(surv);
             if (lanes) {
-                int cntl = __popcll(lanes);
-                // Records of sample b live in their own slice of the pool, so
-                // the allocation atomics of different samples do not contend.
-                uint32_t base = 0;
-                if (lane == 0) base = atomicAdd(&pool_count[c.b], (uint32_t)cntl);
-                base = __shfl(base, 0, kWave);
-                bool ok = (unsigned long long)base + (unsigned long long)cntl <= (unsigned long long)pool_cap;
-                base += (uint32_t)c.b * pool_cap;
+                const uint32_t cntl = (uint32_t)__popcll(lanes);
+                uint32_t base;
+                bool ok;
+                if (used + cntl <= pool_local) {
+                    base = local0 + used;
+                    used += cntl;
+                    ok = true;
+                } else {
+                    // Overflow records of sample b live in their own slice, so
+                    // the allocation atomics of different samples do not contend.
+                    uint32_t ob = 0;
+                    if (lane == 0) ob = atomicAdd(&pool_count[c.b], cntl);
+                    ob = __shfl(ob, 0, kWave);
+                    ok = (unsigned long long)ob + cntl <= (unsigned long long)pool_cap;
+                    base = overflow0 + (uint32_t)c.b * pool_cap + ob;
+                }
                 if (lane == 0) {
                     WaveInfo wi;
                     wi.lanes = lanes;
@@ -454,7 +488,6 @@ __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_check(
                     if (ok) {
                         // Re-walk the sub-block to store its states.
                         uint32_t slot = base + (uint32_t)__popcll(lanes & below);
-                        pool_ub[slot] = ub;
                         Record* r = pool + slot;
                         r->s[0] = make_double2(Vin, Iin);
                         double Vr = Vin, Ir = Iin;
@@ -475,12 +508,20 @@ __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_check(
             }
         }
     }
-    if (n < N) {
-        mask[row + n] = msk;
-        if (ncand) {
-            size_t bn = (size_t)c.b * N + n;
-            if (atomicOr(&listed[bn], 1u) == 0u) work[atomicAdd(nwork, 1u)] = (uint32_t)bn;
-        }
+    if (n < N) mask[row + n] = msk;
+    const bool want = ncand > 0 && n < N;
+    const unsigned long long wm = __ballot(want);
+    if (wm) {
+        // Work list: every lane with candidates takes an entry; the first
+        // segment to list a neuron writes it, later ones write kInvalid.  The
+        // per-lane OR is issued before the wave's single counter update, so
+        // the two round trips overlap.
+        const size_t bn = (size_t)c.b * N + c.nc;
+        const uint32_t old = atomicOr(&listed[bn], want ? 1u : 0u);
+        uint32_t wbase = 0;
+        if (lane == 0) wbase = atomicAdd(nwork, (uint32_t)__popcll(wm));
+        wbase = __shfl(wbase, 0, kWave);
+        if (want) work[wbase + (uint32_t)__popcll(wm & below)] = old == 0u ? (uint32_t)bn : kInvalid;
     }
     int tot = ncand;
 #pragma unroll
@@ -897,7 +938,8 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
     __shared__ ResolveLds sh;
     const uint32_t count = *nwork;
     for (uint32_t w = blockIdx.x; w < count; w += gridDim.x) {
-        uint32_t bn = work[w];
+        const uint32_t bn = work[w];
+        if (bn == kInvalid) continue;
         resolve_neuron(sh, (int)(bn / (uint32_t)N), (int)(bn % (uint32_t)N), ev_t, ev_src, ev_n, E_max, WT, C_in, N,
                        tiles, S, m, dec, carry, mask, winfo, pool, out_t, out_n, out_i, status);
     }
@@ -1004,17 +1046,25 @@ FwdLayout fwd_layout(int B, int E_max, int N)
     L.winfo = take((size_t)B * L.S * tiles * kSubPerSeg * sizeof(WaveInfo));
     L.counters = take(((size_t)B + 1) * sizeof(uint32_t));
     L.listed = take((size_t)B * N * sizeof(uint32_t));
-    L.work = take((size_t)B * N * sizeof(uint32_t));
-    // Record pool: one record per flagged (sub-block, neuron).  Sized at a
-    // sixteenth of the dense bound (far above what spiking activity needs); a
-    // full pool only sends the excess sub-blocks through a slower re-walk.
-    size_t dense = (size_t)B * L.S * kSubPerSeg * N;
-    size_t cap = dense / 16 > 65536 ? dense / 16 : (dense < 65536 ? dense : 65536);
+    L.work = take((size_t)B * L.S * N * sizeof(uint32_t));   // one entry per (segment, neuron) with candidates
+    // Record pool: one record per flagged (sub-block, neuron).  Each check
+    // wave (sample, segment, tile) owns kPoolLocal slots; the overflow is
+    // shared per sample and sized at a 64th of the dense bound (far above
+    // what spiking activity needs).  A full pool only sends the excess
+    // sub-blocks through a slower re-walk.  LIF_POOL_LOCAL / LIF_POOL_CAP
+    // override the two sizes (used by tests of the re-walk path).
+    size_t local = kPoolLocal;
+    if (const char* env = getenv("LIF_POOL_LOCAL")) local = (size_t)strtoull(env, nullptr, 10);
+    size_t waves = (size_t)B * L.S * tiles;
+    size_t dense = waves * kSubPerSeg * kWave;
+    size_t cap = dense / 64 > 65536 ? dense / 64 : (dense < 65536 ? dense : 65536);
     if (const char* env = getenv("LIF_POOL_CAP")) cap = (size_t)strtoull(env, nullptr, 10);
-    if (cap > 0xfffffff0ull) cap = 0xfffffff0ull;
+    if (local > 64) local = 64;
+    if (waves * local + cap > 0xfffffff0ull) cap = 0xfffffff0ull - waves * local;   // slot indices are 32-bit
+    L.pool_local = local;
     L.pool_cap = cap;
-    L.pool = take((cap > 0 ? cap : 1) * sizeof(Record));   // at least one record (a safe load address)
-    L.pool_ub = take(cap * sizeof(double));
+    size_t recs = waves * local + cap;
+    L.pool = take((recs > 0 ? recs : 1) * sizeof(Record));   // at least one record (a safe load address)
     L.total = off + 256;
     return L;
 }
@@ -1041,7 +1091,6 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     uint32_t* listed = (uint32_t*)(base + L.listed);
     uint32_t* work = (uint32_t*)(base + L.work);
     Record* pool = (Record*)(base + L.pool);
-    double* pool_ub = (double*)(base + L.pool_ub);
 
     size_t nev = (size_t)B * E_max;
     size_t nn = (size_t)B * N;
@@ -1075,7 +1124,8 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     if (total) {
         TIMED_LAUNCH("check", k_check, dim3((unsigned)total), dim3(kWave * kTilesPerBlock), 0, stream,
                      ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, tgroups, L.S, (int)total, m, dec, carry, mask,
-                     winfo, pool, pool_ub, pool_count, (uint32_t)(L.pool_cap / (B > 0 ? B : 1)), listed, work, nwork,
+                     winfo, pool, pool_count, (uint32_t)L.pool_local, (uint32_t)(L.pool_cap / (B > 0 ? B : 1)),
+                     listed, work, nwork,
                      status);
         // One wave per listed neuron, as many as can be resident at once.
         unsigned grid = (unsigned)(nn < 4096 ? nn : 4096);

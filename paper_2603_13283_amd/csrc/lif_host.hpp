@@ -15,8 +15,9 @@ namespace lif {
 
 struct FwdLayout {
     int S;                                   // segments per sample
-    size_t dec, segm, agg, carry, mask, winfo, counters, listed, work, pool, pool_ub, total;
-    size_t pool_cap;                         // records in the pool
+    size_t dec, segm, agg, carry, mask, winfo, counters, listed, work, pool, total;
+    size_t pool_local;                       // record slots per check wave
+    size_t pool_cap;                         // overflow records shared per sample
 };
 FwdLayout fwd_layout(int B, int E_max, int N);
 

@@ -198,9 +198,13 @@ def test_record_pool_fallback(env, monkeypatch):
     """With a tiny record pool the overflowing sub-blocks are resolved by the
     re-walk fallback; results are unchanged."""
     cfg = W.random_small(9, B=3, C=30, N=130, n_events=600, T=0.4, gain=14.0)
+    monkeypatch.setenv("LIF_POOL_LOCAL", "0")
     monkeypatch.setenv("LIF_POOL_CAP", "5")
     s = check(env, cfg.events, cfg.layers[0].WT, "pool5", both=False)
     assert s["par"]["status"][7] > 0
     monkeypatch.setenv("LIF_POOL_CAP", "0")
     s = check(env, cfg.events, cfg.layers[0].WT, "pool0", both=False)
     assert s["par"]["status"][7] >= s["par"]["status"][4] > 0   # every walked block fell back
+    monkeypatch.setenv("LIF_POOL_LOCAL", "1")
+    s = check(env, cfg.events, cfg.layers[0].WT, "local1-pool0", both=False)
+    assert s["par"]["status"][7] > 0
