@@ -22,38 +22,54 @@ def compare_spikes(out_t_gpu, out_n_gpu, ref, out_i_gpu=None, label=""):
     Returns a dict of statistics."""
     tg = np.asarray(out_t_gpu, dtype=np.float64)
     ng = np.asarray(out_n_gpu)
+    ig = None if out_i_gpu is None else np.asarray(out_i_gpu, dtype=np.float64)
     B, N, S = ref.out_t.shape
-    flagged = 0
-    compared = 0
+    tie = np.isfinite(ref.tie_t)
     worst = 0.0
     worst_i = 0.0
-    for b in range(B):
-        for i in range(N):
-            tie = ref.tie_t[b, i]
-            ro = ref.out_t[b, i, : ref.out_n[b, i]]
-            go = tg[b, i, : ng[b, i]]
-            if np.isfinite(tie):
-                flagged += 1
-                ro = ro[ro < tie]
-                go = go[go < tie]
-            assert len(go) == len(ro), f"{label} count mismatch at (b={b}, i={i}): gpu {ng[b, i]} oracle {ref.out_n[b, i]}"
-            if len(ro):
-                assert np.all(np.diff(go) > 0) or len(go) == 1, f"{label} order at ({b},{i})"
-                err = np.abs(go - ro) / np.abs(ro)
-                worst = max(worst, float(err.max()))
-                assert err.max() <= TIME_RTOL, f"{label} time mismatch at ({b},{i}): {go} vs {ro}"
-                if out_i_gpu is not None:
-                    gi = np.asarray(out_i_gpu, dtype=np.float64)[b, i, : len(ro)]
-                    ri = ref.out_i[b, i, : len(ro)]
-                    e = np.abs(gi - ri) / np.maximum(np.abs(ri), 1e-3)
-                    worst_i = max(worst_i, float(e.max()))
-                    assert e.max() <= TIME_RTOL, f"{label} I* mismatch at ({b},{i})"
-            compared += 1
-            if not np.isfinite(tie):
-                assert ng[b, i] == ref.out_n[b, i]
-                rest = tg[b, i, ng[b, i]:]
-                assert np.all(np.isinf(rest)), f"{label} padding at ({b},{i})"
-    return {"flagged": flagged, "compared": compared, "worst_time_rel": worst, "worst_i_rel": worst_i,
+    # ---- neurons without a flagged tie: every slot, vectorised
+    nt = ~tie
+    bad = np.argwhere(nt & (ng != ref.out_n))
+    if len(bad):
+        b, i = bad[0]
+        raise AssertionError(f"{label} count mismatch at (b={b}, i={i}): gpu {ng[b, i]} oracle {ref.out_n[b, i]}")
+    slot = np.arange(S)[None, None, :]
+    valid = (slot < ref.out_n[..., None]) & nt[..., None]
+    if valid.any():
+        ro = ref.out_t[valid]
+        err = np.abs(tg[valid] - ro) / np.abs(ro)
+        worst = float(err.max())
+        if worst > TIME_RTOL:
+            b, i, s = np.argwhere(valid)[int(err.argmax())]
+            raise AssertionError(f"{label} time mismatch at ({b},{i}) spike {s}: {tg[b, i, s]} vs {ref.out_t[b, i, s]}")
+        later = valid[..., 1:]
+        assert np.all(tg[..., 1:][later] > tg[..., :-1][later]), f"{label} spike order"
+        if ig is not None:
+            ri = ref.out_i[valid]
+            e = np.abs(ig[valid] - ri) / np.maximum(np.abs(ri), 1e-3)
+            worst_i = float(e.max())
+            assert worst_i <= TIME_RTOL, f"{label} I* mismatch (worst {worst_i:.3e})"
+    pad = (slot >= ref.out_n[..., None]) & nt[..., None]
+    assert np.all(np.isinf(tg[pad])), f"{label} padding"
+    # ---- flagged neurons: the spikes before the tie
+    for b, i in np.argwhere(tie):
+        t_tie = ref.tie_t[b, i]
+        ro = ref.out_t[b, i, : ref.out_n[b, i]]
+        go = tg[b, i, : ng[b, i]]
+        ro = ro[ro < t_tie]
+        go = go[go < t_tie]
+        assert len(go) == len(ro), f"{label} count mismatch before a tie at (b={b}, i={i})"
+        if len(ro):
+            assert np.all(np.diff(go) > 0), f"{label} order at ({b},{i})"
+            err = np.abs(go - ro) / np.abs(ro)
+            worst = max(worst, float(err.max()))
+            assert err.max() <= TIME_RTOL, f"{label} time mismatch at ({b},{i}): {go} vs {ro}"
+            if ig is not None:
+                e = np.abs(ig[b, i, : len(ro)] - ref.out_i[b, i, : len(ro)]) / np.maximum(
+                    np.abs(ref.out_i[b, i, : len(ro)]), 1e-3)
+                worst_i = max(worst_i, float(e.max()))
+                assert e.max() <= TIME_RTOL, f"{label} I* mismatch at ({b},{i})"
+    return {"flagged": int(tie.sum()), "compared": int(B * N), "worst_time_rel": worst, "worst_i_rel": worst_i,
             "spikes": int(ref.out_n.sum())}
 
 

@@ -1,0 +1,172 @@
+"""Multi-layer parity at the shapes of the two-layer workloads: layer 1,
+the spike merge into the next layer's queue, layer 2 (fed the oracle's
+layer-1 output, and chained on the GPU), the first-spike readout loss and
+the gradients chained back through the merge."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from tests.parity import E2E_ELEM_RTOL, compare_grad, compare_spikes
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def env():
+    import torch
+    import paper_2603_13283_amd as lif
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    lif.load()
+    return torch, lif
+
+
+def _dev(torch, a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda:0")
+
+
+def _tie_free(ref):
+    """(sample, neuron) pairs without a flagged near-threshold tie."""
+    return ~np.isfinite(ref.tie_t)
+
+
+def _gpu_fwd(env, ev_t, ev_src, ev_n, WT, P):
+    torch, lif = env
+    d = [_dev(torch, a) for a in (ev_t, ev_src, ev_n, WT)]
+    out = lif.forward(*d, P)
+    torch.cuda.synchronize()
+    return d, out
+
+
+def test_config3_two_layers(env):
+    """700 -> 512 -> 512, batch 128, ~10k input events per sample."""
+    torch, lif = env
+    cfg = W.config3()
+    ev, W1, W2 = cfg.events, cfg.layers[0].WT, cfg.layers[1].WT
+    # The strongest-driven neurons fire ~100 times per second: the spike
+    # capacity is set so that it never binds.
+    P, OP = lif.Params(s_max=128), oracle.LifParams(s_max=128)
+    print(f"[case] c3 layer 1 B={ev.B} E_max={ev.E_max}", flush=True)
+    d1, o1 = _gpu_fwd(env, ev.ev_t, ev.ev_src, ev.ev_n, W1, P)
+    r1 = oracle.forward(ev.ev_t, ev.ev_src, ev.ev_n, W1, OP)
+    s1 = compare_spikes(o1.out_t.cpu().numpy(), o1.out_n.cpu().numpy(), r1, o1.out_i.cpu().numpy(), label="c3-l1")
+    assert int(o1.status.cpu().numpy()[1]) == 0 and not r1.capped.any()
+    o1_n = o1.out_n.cpu().numpy()
+    # merge of the GPU's layer-1 spikes: bit-exact against the oracle's merge
+    n1 = o1.out_n.cpu().numpy()
+    E2 = int(n1.sum(1).max()) + 8
+    t2, s2, n2, perm, st = lif.merge(o1, E2)
+    torch.cuda.synchronize()
+    rt, rs, rn, rp, ovf = oracle.merge(o1.out_t.cpu().numpy(), n1, E2)
+    assert not ovf
+    assert np.array_equal(n2.cpu().numpy(), rn) and np.array_equal(t2.cpu().numpy(), rt)
+    assert np.array_equal(s2.cpu().numpy(), rs) and np.array_equal(perm.cpu().numpy(), rp)
+    # layer 2 isolated: both sides read the oracle's merged layer-1 output
+    E2o = int(r1.out_n.sum(1).max()) + 8
+    ot, os_, on, _, ovf = oracle.merge(r1.out_t.astype(np.float32), r1.out_n, E2o)
+    assert not ovf
+    print(f"[case] c3 layer 2 isolated E_max={E2o} events={int(on.sum())}", flush=True)
+    _, o2 = _gpu_fwd(env, ot, os_, on, W2, P)
+    r2 = oracle.forward(ot, os_, on, W2, OP)
+    s2i = compare_spikes(o2.out_t.cpu().numpy(), o2.out_n.cpu().numpy(), r2, o2.out_i.cpu().numpy(),
+                         label="c3-l2 isolated")
+    assert int(o2.status.cpu().numpy()[1]) == 0 and not r2.capped.any()
+    # layer 2 at the stated gain is nearly silent: also a driven variant
+    # (weights x3) on the same merged queue
+    W2d = (W2 * 3.0).astype(np.float32)
+    _, o2d = _gpu_fwd(env, ot, os_, on, W2d, P)
+    r2d = oracle.forward(ot, os_, on, W2d, OP)
+    s2d = compare_spikes(o2d.out_t.cpu().numpy(), o2d.out_n.cpu().numpy(), r2d, o2d.out_i.cpu().numpy(),
+                         label="c3-l2 driven")
+    assert s2d["spikes"] > 1000
+    # layer 2 chained on the GPU (GPU layer 1 -> GPU merge -> GPU layer 2)
+    # against the oracle's chain (r2 above).  Where the GPU's merged queue of
+    # a sample is bit-identical to the oracle's (layer-1 spike times that
+    # round to the same float32) and layer 1 had no flagged tie, the chains
+    # see the same input; those samples are compared.
+    o2c = lif.forward(t2, s2, n2, _dev(torch, W2), P)
+    torch.cuda.synchronize()
+    gt, gs, gn = t2.cpu().numpy(), s2.cpu().numpy(), n2.cpu().numpy()
+    keep = np.array([gn[b] == on[b] and np.array_equal(gt[b, :gn[b]], ot[b, :on[b]])
+                     and np.array_equal(gs[b, :gn[b]], os_[b, :on[b]]) and not np.isfinite(r1.tie_t[b]).any()
+                     for b in range(ev.B)])
+    sub = oracle.ForwardResult(r2.out_t[keep], r2.out_i[keep], r2.out_n[keep], r2.capped[keep], r2.tie_t[keep],
+                               r2.min_gap)
+    s2c = compare_spikes(o2c.out_t.cpu().numpy()[keep], o2c.out_n.cpu().numpy()[keep], sub, label="c3-l2 chained")
+    print(f"    l1 {s1} l2-isolated {s2i} l2-driven {s2d} l2-chained {s2c} samples chained "
+          f"{int(keep.sum())}/{ev.B}", flush=True)
+    assert keep.sum() >= ev.B // 2
+
+
+def test_config5_forward_backward_driven(env):
+    """32768 -> 2048 -> 20 readout, one sample of ~100k events, hidden gain
+    16 and readout gain 10 (the stated gains leave both layers silent and
+    every gradient zero); first-spike-time cross-entropy; gradients chained
+    from the loss back through the merge to the hidden weights."""
+    torch, lif = env
+    cfg = W.config5(B=1, g1=16.0, g2=10.0)
+    ev, W1, W2 = cfg.events, cfg.layers[0].WT, cfg.layers[1].WT
+    P, OP = lif.Params(), oracle.LifParams()
+    print(f"[case] c5 hidden B=1 events={int(ev.ev_n.sum())}", flush=True)
+    d1, o1 = _gpu_fwd(env, ev.ev_t, ev.ev_src, ev.ev_n, W1, P)
+    r1 = oracle.forward(ev.ev_t, ev.ev_src, ev.ev_n, W1, OP)
+    s1 = compare_spikes(o1.out_t.cpu().numpy(), o1.out_n.cpu().numpy(), r1, o1.out_i.cpu().numpy(), label="c5-hidden")
+    assert (r1.out_n > 0).mean() > 0.5 and not r1.capped.any()
+    # readout on the oracle's merged hidden spikes (same queue on both sides)
+    E2 = int(r1.out_n.sum()) + 8
+    qt, qs, qn, qperm, ovf = oracle.merge(r1.out_t.astype(np.float32), r1.out_n, E2)
+    assert not ovf
+    d2, o2 = _gpu_fwd(env, qt, qs, qn, W2, P)
+    r2 = oracle.forward(qt, qs, qn, W2, OP)
+    s2 = compare_spikes(o2.out_t.cpu().numpy(), o2.out_n.cpu().numpy(), r2, o2.out_i.cpu().numpy(), label="c5-readout")
+    assert (r2.out_n > 0).mean() >= 0.5
+    # first-spike loss and its gradient, GPU against oracle
+    labels = cfg.labels
+    loss, g2 = lif.first_spike_ce(o2, torch.from_numpy(labels), 0.02, 1.0)
+    torch.cuda.synchronize()
+    rl, rg = oracle.first_spike_ce(r2.out_t[:, :, 0], r2.out_n > 0, labels, 0.02, 1.0)
+    assert abs(loss.item() - rl) <= 1e-5 * abs(rl)
+    assert np.allclose(g2.cpu().numpy()[:, :, 0], rg, rtol=1e-5, atol=1e-6 * np.abs(rg).max())
+    # readout backward on identical inputs (the oracle's spikes in float32)
+    gout2 = np.zeros(r2.out_t.shape)
+    gout2[:, :, 0] = rg
+    f2 = lif.ForwardOut(_dev(torch, r2.out_t.astype(np.float32)), _dev(torch, r2.out_n),
+                        _dev(torch, r2.out_i.astype(np.float32)), None)
+    gW2, gT2 = lif.backward(*d2, f2, _dev(torch, gout2.astype(np.float32)), P)
+    torch.cuda.synchronize()
+    r2_32 = oracle.ForwardResult(r2.out_t.astype(np.float32).astype(np.float64),
+                                 r2.out_i.astype(np.float32).astype(np.float64), r2.out_n, r2.capped, r2.tie_t,
+                                 r2.min_gap)
+    qW2, qT2 = oracle.backward(qt, qs, qn, W2, r2_32, gout2.astype(np.float32).astype(np.float64), OP)
+    compare_grad(gW2.cpu().numpy(), qW2, label="c5 grad_W readout")
+    compare_grad(gT2.cpu().numpy(), qT2, label="c5 grad_t readout")
+    # dL/d(hidden spike time) through the merge permutation
+    S = r1.out_t.shape[2]
+
+    def to_hidden(gt):
+        g = np.zeros(r1.out_t.shape)
+        k = np.arange(int(qn[0]))
+        p = qperm[0, k]
+        g[0, p // S, p % S] = gt[0, k]
+        return g
+
+    gout1 = to_hidden(qT2)
+    assert np.count_nonzero(gout1) > 0
+    f1 = lif.ForwardOut(_dev(torch, r1.out_t.astype(np.float32)), _dev(torch, r1.out_n),
+                        _dev(torch, r1.out_i.astype(np.float32)), None)
+    gW1, _ = lif.backward(*d1, f1, _dev(torch, gout1.astype(np.float32)), P, want_time_grad=False)
+    torch.cuda.synchronize()
+    r1_32 = oracle.ForwardResult(r1.out_t.astype(np.float32).astype(np.float64),
+                                 r1.out_i.astype(np.float32).astype(np.float64), r1.out_n, r1.capped, r1.tie_t,
+                                 r1.min_gap)
+    qW1, _ = oracle.backward(ev.ev_t, ev.ev_src, ev.ev_n, W1, r1_32, gout1.astype(np.float32).astype(np.float64), OP)
+    okN = _tie_free(r1)[0]
+    rel = compare_grad(gW1.cpu().numpy()[:, okN], qW1[:, okN], label="c5 grad_W hidden")
+    # chained on the GPU's own upstream gradient (end-to-end tolerance)
+    gW1c, _ = lif.backward(*d1, f1, _dev(torch, to_hidden(gT2.cpu().numpy()).astype(np.float32)), P,
+                           want_time_grad=False)
+    torch.cuda.synchronize()
+    relc = compare_grad(gW1c.cpu().numpy()[:, okN], qW1[:, okN], label="c5 grad_W hidden chained",
+                        elem_rtol=E2E_ELEM_RTOL)
+    print(f"    hidden {s1} readout {s2} loss {loss.item():.6f} vs {rl:.6f}; rel(gW1) {rel:.2e} chained {relc:.2e}",
+          flush=True)
