@@ -53,7 +53,6 @@ struct alignas(16) WaveInfo {
     uint32_t pad;
 };
 constexpr uint32_t kNoSlot = 0xffffffffu;
-constexpr uint32_t kInvalid = 0xffffffffu;   // work-list entry of a neuron already listed
 
 // Workgroup index -> work index such that each of the 8 XCDs (which receive
 // workgroups round-robin) processes a contiguous, sample-major range: the
@@ -326,9 +325,9 @@ __global__ __launch_bounds__(kWave * kCarryWaves) void k_carry(
     }
     const int nb = clamp_count(ev_n[b], E_max);
     if (threadIdx.x == 0 && tile == 0) {
-        counters[1 + b] = 0u;                   // record pool use of sample b
+        counters[b] = 0u;                       // record pool use of sample b
+        counters[B + b] = 0u;                   // work-list length of sample b
         atomicAdd(&status[LIF_ST_EVENTS], nb);
-        if (b == 0) counters[0] = 0u;           // work-list length
     }
     const int Sb = (nb + kSeg - 1) / kSeg;
     const int per = (Sb + kCarryWaves - 1) / kCarryWaves;
@@ -392,10 +391,12 @@ __device__ __forceinline__ int B_of(int total, int tgroups, int S) { return tota
 __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_check(
     const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
     const float* __restrict__ WT, int C_in, int N, int tiles, int tgroups, int S, int total, Model m,
-    const Decay* __restrict__ dec, const double2* __restrict__ carry, uint32_t* __restrict__ mask,
-    WaveInfo* __restrict__ winfo, Record* __restrict__ pool,
+    const Decay* __restrict__ dec, const double2* __restrict__ carry, double2* __restrict__ ent,
+    uint32_t* __restrict__ mask, WaveInfo* __restrict__ winfo, Record* __restrict__ pool,
     uint32_t* __restrict__ pool_count, uint32_t pool_local, uint32_t pool_cap, uint32_t* __restrict__ listed,
     uint32_t* __restrict__ work, uint32_t* __restrict__ nwork, int32_t* __restrict__ status)
+// work: per-sample lists of the neurons with candidates (capacity N each);
+// nwork: per-sample list lengths.
 {
     // The segment's decays and sources are wave-uniform: they are read with
     // scalar loads and used as scalar operands.
@@ -485,6 +486,10 @@ __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_check(
                     winfo[(((size_t)c.b * S + c.seg) * tiles + c.tile) * kSubPerSeg + q] = wi;
                 }
                 if (surv) {
+                    // The entering state always; the full record if the pool
+                    // had room (otherwise the resolve pass rebuilds the
+                    // sub-block's states from the entering state).
+                    ent[(((size_t)c.b * S + c.seg) * kSubPerSeg + q) * N + n] = make_double2(Vin, Iin);
                     if (ok) {
                         // Re-walk the sub-block to store its states.
                         uint32_t slot = base + (uint32_t)__popcll(lanes & below);
@@ -510,24 +515,20 @@ __global__ __launch_bounds__(kWave * kTilesPerBlock) void k_check(
     }
     if (n < N) mask[row + n] = msk;
     const bool want = ncand > 0 && n < N;
-    const unsigned long long wm = __ballot(want);
-    if (wm) {
-        // Work list: every lane with candidates takes an entry; the first
-        // segment to list a neuron writes it, later ones write kInvalid.  The
-        // per-lane OR is issued before the wave's single counter update, so
-        // the two round trips overlap.
+    if (__ballot(want)) {
+        // Work list of sample b: the first segment to flag a neuron appends
+        // it (one OR per flagged lane, then one counter update per wave).
         const size_t bn = (size_t)c.b * N + c.nc;
         const uint32_t old = atomicOr(&listed[bn], want ? 1u : 0u);
-        uint32_t wbase = 0;
-        if (lane == 0) wbase = atomicAdd(nwork, (uint32_t)__popcll(wm));
-        wbase = __shfl(wbase, 0, kWave);
-        if (want) work[wbase + (uint32_t)__popcll(wm & below)] = old == 0u ? (uint32_t)bn : kInvalid;
-    }
-    int tot = ncand;
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) tot += __shfl_xor(tot, off, kWave);
-    if (lane == 0 && tot) atomicAdd(&status[LIF_ST_CAND_BLOCKS], tot);
-}
+        const bool first = want && old == 0u;
+        const unsigned long long fm = __ballot(first);
+        if (fm) {
+            uint32_t wbase = 0;
+            if (lane == 0) wbase = atomicAdd(&nwork[c.b], (uint32_t)__popcll(fm));
+            wbase = __shfl(wbase, 0, kWave);
+            if (first) work[(size_t)c.b * N + wbase + (uint32_t)__popcll(fm & below)] = (uint32_t)bn;
+        }
+    }}
 
 // ---------------------------------------------------------------------------
 // Resolve pass: one wave per neuron that has flagged sub-blocks (a work list
@@ -577,24 +578,60 @@ __device__ __noinline__ double2 entering_state(const double2* __restrict__ carry
     return make_double2(V, I);
 }
 
-// No-reset states at the start and end of interval j of a sub-block whose
-// record was not stored (pool full): walk from the segment carry.
-__device__ __noinline__ double3 walked_interval(const double2* __restrict__ carry, size_t row, int n, int seg,
-                                                int kq0, int cnt, int j, const int32_t* __restrict__ src,
-                                                const Decay* __restrict__ d, const float* __restrict__ WT, int C_in,
-                                                int N)
+// Lane shift by n within rows of 16 lanes (DPP row_shr): lanes whose
+// source lies outside the row keep `old`.
+template <int n>
+__device__ __forceinline__ double row_shr(double v, double old)
 {
-    double2 cs = entering_state(carry, row, n, seg * kSeg, kq0, src, d, WT, C_in, N);
-    double V = cs.x, I = cs.y, V0 = V, I0 = I, V1 = V;
-    for (int q = 0; q < kSub && q < cnt; ++q) {
-        Decay eq = d[kq0 + q];
-        double Vn = eq.A * V + eq.C * I;
-        I = eq.D * I + (double)WT[(size_t)clamp_src(src[kq0 + q], C_in) * (size_t)N + n];
-        V = Vn;
-        if (q + 1 == j) { V0 = V; I0 = I; }
-        if (q == j) V1 = V;
-    }
-    return make_double3(V0, I0, V1);
+    static_assert(n >= 1 && n <= 15, "row shift");
+    const unsigned long long u = (unsigned long long)__double_as_longlong(v);
+    const unsigned long long o = (unsigned long long)__double_as_longlong(old);
+    const int lo = __builtin_amdgcn_update_dpp((int)(unsigned)o, (int)(unsigned)u, 0x110 + n, 0xf, 0xf, false);
+    const int hi = __builtin_amdgcn_update_dpp((int)(unsigned)(o >> 32), (int)(unsigned)(u >> 32), 0x110 + n, 0xf,
+                                               0xf, false);
+    return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
+}
+
+// Affine map s -> (A V + C I + bV, D I + bI) of a run of events.
+struct Map {
+    double A, C, D, bV, bI;
+};
+
+// `late` applied after `early`.
+__device__ __forceinline__ Map compose(const Map& late, const Map& early)
+{
+    Map r;
+    r.A = late.A * early.A;
+    r.C = late.A * early.C + late.C * early.D;
+    r.D = late.D * early.D;
+    r.bV = late.A * early.bV + late.C * early.bI + late.bV;
+    r.bI = late.D * early.bI + late.bI;
+    return r;
+}
+
+template <int n>
+__device__ __forceinline__ Map row_shr_map(const Map& m)
+{
+    return Map{row_shr<n>(m.A, 1.0), row_shr<n>(m.C, 0.0), row_shr<n>(m.D, 1.0), row_shr<n>(m.bV, 0.0),
+               row_shr<n>(m.bI, 0.0)};
+}
+
+// No-reset states of a sub-block whose record was not stored (pool full):
+// lane j of each row of 16 lanes holds event j's map (Eq. affine: decay
+// then jump), an inclusive scan over the row (Hillis-Steele with DPP row
+// shifts; all 64 lanes take part) composes the maps of events 0..j, and the
+// sub-block's entering state s0 gives the state after event j.  Lane j
+// returns the state entering interval j (after event j - 1) and V at its end.
+__device__ __forceinline__ double3 scan_interval(double2 s0, double A, double C, double D, double w)
+{
+    Map m{A, C, D, 0.0, w};
+    m = compose(m, row_shr_map<1>(m));
+    m = compose(m, row_shr_map<2>(m));
+    m = compose(m, row_shr_map<4>(m));
+    m = compose(m, row_shr_map<8>(m));
+    const double Va = m.A * s0.x + m.C * s0.y + m.bV;     // after event j
+    const double Ia = m.D * s0.y + m.bI;
+    return make_double3(row_shr<1>(Va, s0.x), row_shr<1>(Ia, s0.y), Va);
 }
 
 __device__ __forceinline__ int rl_int(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
@@ -626,6 +663,7 @@ struct IvRaw {
     double v1;          // record: no-reset V at the interval end
     int k, seg, kq0, cnt, j;
     bool valid, fb;     // fb: the record pool was full for this sub-block
+    bool rowfb;         // the same for the lane's row, valid or not
 };
 
 // The window's per-candidate values (one candidate per lane).
@@ -646,6 +684,7 @@ __device__ __forceinline__ IvRaw load_slice(int cw, int nwin, const WinLane& w, 
     v.j = j;
     v.valid = cw < nwin && j < v.cnt;
     v.fb = v.valid && slot == kNoSlot;
+    v.rowfb = cw < nwin && slot == kNoSlot;
     v.k = v.kq0 + (v.valid ? j : 0);
     v.tp = tt[max(v.k - 1, 0)];
     v.tb = tt[v.k];
@@ -659,7 +698,7 @@ __device__ __forceinline__ IvRaw load_slice(int cw, int nwin, const WinLane& w, 
 
 __device__ __forceinline__ Iv finish_slice(const IvRaw& r, int b, int n, int S, int N, int C_in,
                                            const int32_t* __restrict__ src, const Decay* __restrict__ d,
-                                           const float* __restrict__ WT, const double2* __restrict__ carry)
+                                           const float* __restrict__ WT, const double2* __restrict__ ent)
 {
     Iv v;
     v.valid = r.valid;
@@ -670,10 +709,17 @@ __device__ __forceinline__ Iv finish_slice(const IvRaw& r, int b, int n, int S, 
     v.V0 = r.s0.x;
     v.I0 = r.s0.y;
     v.V1 = r.v1;
-    if (__ballot(r.fb) && r.fb) {
-        double3 w = walked_interval(carry, ((size_t)b * S + r.seg) * N, n, r.seg, r.kq0, r.cnt, r.j, src, d, WT,
-                                    C_in, N);
-        v.V0 = w.x; v.I0 = w.y; v.V1 = w.z;
+    if (__ballot(r.rowfb)) {
+        // No record: rebuild the row's states from its entering state (every
+        // lane takes part in the row scan; past cnt the maps are identities).
+        const int q = (r.kq0 % kSeg) / kSub;
+        const double2 s0 = r.rowfb ? ent[(((size_t)b * S + r.seg) * kSubPerSeg + q) * N + n] : make_double2(0.0, 0.0);
+        const bool in = r.j < r.cnt;
+        const int k = r.kq0 + min(r.j, max(r.cnt - 1, 0));
+        const Decay e = d[k];
+        const double w = in ? (double)WT[(size_t)clamp_src(src[k], C_in) * (size_t)N + n] : 0.0;
+        const double3 sc = scan_interval(s0, in ? e.A : 1.0, in ? e.C : 0.0, in ? e.D : 1.0, w);
+        if (r.fb) { v.V0 = sc.x; v.I0 = sc.y; v.V1 = sc.z; }
     }
     return v;
 }
@@ -721,13 +767,19 @@ __device__ __forceinline__ bool may_cross(const Screen& c, float D)
     return !(end_miss && tan_miss);      // NaN passes (tested in float64)
 }
 
-__device__ void resolve_neuron(ResolveLds& sh, int b, int n, const float* __restrict__ ev_t,
+// Status counts of one wave, added to the status words once per wave.
+struct ResolveStats {
+    int walked, fallback, capped, spikes;
+};
+
+__device__ void resolve_neuron(ResolveLds& sh, ResolveStats& acc, int b, int n, const float* __restrict__ ev_t,
                                const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
                                const float* __restrict__ WT, int C_in, int N, int tiles, int S, const Model& m,
                                const Decay* __restrict__ dec, const double2* __restrict__ carry,
+                               const double2* __restrict__ ent,
                                const uint32_t* __restrict__ mask, const WaveInfo* __restrict__ winfo,
                                const Record* __restrict__ pool, float* __restrict__ out_t, int32_t* __restrict__ out_n,
-                               float* __restrict__ out_i, int32_t* __restrict__ status)
+                               float* __restrict__ out_i)
 {
     const int tile = n / kWave;
     const unsigned long long below_n = (1ull << (n % kWave)) - 1ull;
@@ -814,7 +866,7 @@ __device__ void resolve_neuron(ResolveLds& sh, int b, int n, const float* __rest
                 }
                 Iv v[kSlices];
 #pragma unroll
-                for (int i = 0; i < kSlices; ++i) v[i] = finish_slice(raw[i], b, n, S, N, C_in, src, d, WT, carry);
+                for (int i = 0; i < kSlices; ++i) v[i] = finish_slice(raw[i], b, n, S, N, C_in, src, d, WT, ent);
                 // ---- slices in time order: screen in float32 with the current
                 // deficit, then the deficit and the maximum in float64 where
                 // an interval may cross, then rounds
@@ -906,28 +958,22 @@ __device__ void resolve_neuron(ResolveLds& sh, int b, int n, const float* __rest
     ns = rl_int(ns, 0);
     capped = rl_int((int)capped, 0) != 0;
 
-    if (lane == 0) {
-        if (walked) atomicAdd(&status[LIF_ST_WALKED_BLOCKS], walked);
-        if (fallback) atomicAdd(&status[LIF_ST_POOL_FALLBACK], fallback);
-        out_n[idx] = ns;
-        if (capped) {
-            atomicAdd(&status[LIF_ST_CAPPED], 1);
-            atomicOr(&status[LIF_ST_FLAGS], LIF_WARN_SPIKE_CAP);
-        }
-        if (ns) {
-            atomicAdd(&status[LIF_ST_SPIKES], ns);
-            atomicAdd(&status[LIF_ST_ROOT_SOLVES], ns);
-        }
-    }
+    if (lane == 0) out_n[idx] = ns;
+    acc.walked += walked;
+    acc.fallback += fallback;
+    acc.capped += capped ? 1 : 0;
+    acc.spikes += ns;
 }
 
-// Work-list driven: every wave takes neurons from the list built by k_check
-// until the list is exhausted.
+// Work-list driven: workgroup (b, k) takes entries k, k + K, ... of sample
+// b's list of neurons built by k_check (K workgroups per sample).  Status
+// counts are added once per workgroup.
 __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src,
-                                                   const int32_t* __restrict__ ev_n, int E_max,
+                                                   const int32_t* __restrict__ ev_n, int B, int E_max,
                                                    const float* __restrict__ WT, int C_in, int N, int tiles, int S,
                                                    Model m, const Decay* __restrict__ dec,
                                                    const double2* __restrict__ carry,
+                                                   const double2* __restrict__ ent,
                                                    const uint32_t* __restrict__ mask,
                                                    const WaveInfo* __restrict__ winfo,
                                                    const Record* __restrict__ pool,
@@ -936,12 +982,30 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
                                                    float* __restrict__ out_i, int32_t* __restrict__ status)
 {
     __shared__ ResolveLds sh;
-    const uint32_t count = *nwork;
-    for (uint32_t w = blockIdx.x; w < count; w += gridDim.x) {
-        const uint32_t bn = work[w];
-        if (bn == kInvalid) continue;
-        resolve_neuron(sh, (int)(bn / (uint32_t)N), (int)(bn % (uint32_t)N), ev_t, ev_src, ev_n, E_max, WT, C_in, N,
-                       tiles, S, m, dec, carry, mask, winfo, pool, out_t, out_n, out_i, status);
+    const int K = (int)gridDim.x / B;
+    const int b = (int)blockIdx.x / K, k = (int)blockIdx.x % K;
+    const uint32_t count = nwork[b];
+    const uint32_t* list = work + (size_t)b * N;
+    ResolveStats acc{0, 0, 0, 0};
+    for (uint32_t w = (uint32_t)k; w < count; w += (uint32_t)K) {
+        const uint32_t bn = list[w];
+        resolve_neuron(sh, acc, (int)(bn / (uint32_t)N), (int)(bn % (uint32_t)N), ev_t, ev_src, ev_n, E_max, WT,
+                       C_in, N, tiles, S, m, dec, carry, ent, mask, winfo, pool, out_t, out_n, out_i);
+    }
+    if (threadIdx.x == 0) {
+        if (acc.walked) {
+            atomicAdd(&status[LIF_ST_WALKED_BLOCKS], acc.walked);
+            atomicAdd(&status[LIF_ST_CAND_BLOCKS], acc.walked);
+        }
+        if (acc.fallback) atomicAdd(&status[LIF_ST_POOL_FALLBACK], acc.fallback);
+        if (acc.capped) {
+            atomicAdd(&status[LIF_ST_CAPPED], acc.capped);
+            atomicOr(&status[LIF_ST_FLAGS], LIF_WARN_SPIKE_CAP);
+        }
+        if (acc.spikes) {
+            atomicAdd(&status[LIF_ST_SPIKES], acc.spikes);
+            atomicAdd(&status[LIF_ST_ROOT_SOLVES], acc.spikes);
+        }
     }
 }
 
@@ -957,11 +1021,12 @@ __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_
                                                    int32_t* __restrict__ out_n, float* __restrict__ out_i,
                                                    int32_t* __restrict__ status)
 {
-    size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= (size_t)B * (size_t)N) return;
+    const size_t idx_raw = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const bool live = idx_raw < (size_t)B * (size_t)N;
+    const size_t idx = live ? idx_raw : 0;            // lanes past the end run neuron 0 and write nothing
     int b = (int)(idx / (size_t)N), n = (int)(idx % (size_t)N);
     int nb = clamp_count(ev_n[b], E_max);
-    if (n == 0) atomicAdd(&status[LIF_ST_EVENTS], nb);
+    if (live && n == 0) atomicAdd(&status[LIF_ST_EVENTS], nb);
     const float* tt = ev_t + (size_t)b * E_max;
     const int32_t* src = ev_src + (size_t)b * E_max;
     const Decay* d = dec + (size_t)b * E_max;
@@ -997,8 +1062,10 @@ __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_
             while (Dk * im.a <= im.g) {
                 double E1, E2;
                 double u = root_h(m, V - Dk + kI, kI, lo, Flo, im.hi, im.Fhi - Dk, &E1, &E2, nullptr);
-                st[ns] = (float)(t_prev + u);
-                if (si) si[ns] = (float)(I * (E2 / E1));
+                if (live) {
+                    st[ns] = (float)(t_prev + u);
+                    if (si) si[ns] = (float)(I * (E2 / E1));
+                }
                 ++ns;
                 Dk += m.dth * E1;
                 lo = u;
@@ -1013,18 +1080,29 @@ __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_
             t_prev = (double)tt[k];
         }
     }
-    out_n[idx] = ns;
-    for (int s = ns; s < m.s_max; ++s) {
-        st[s] = INFINITY;
-        if (si) si[s] = 0.0f;
+    if (live) {
+        out_n[idx] = ns;
+        for (int s = ns; s < m.s_max; ++s) {
+            st[s] = INFINITY;
+            if (si) si[s] = 0.0f;
+        }
     }
-    if (capped) {
-        atomicAdd(&status[LIF_ST_CAPPED], 1);
-        atomicOr(&status[LIF_ST_FLAGS], LIF_WARN_SPIKE_CAP);
+    // status counts: one atomic per wave
+    int nsw = live ? ns : 0, cw = live && capped ? 1 : 0;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        nsw += __shfl_xor(nsw, off, kWave);
+        cw += __shfl_xor(cw, off, kWave);
     }
-    if (ns) {
-        atomicAdd(&status[LIF_ST_SPIKES], ns);
-        atomicAdd(&status[LIF_ST_ROOT_SOLVES], ns);
+    if (threadIdx.x % kWave == 0) {
+        if (cw) {
+            atomicAdd(&status[LIF_ST_CAPPED], cw);
+            atomicOr(&status[LIF_ST_FLAGS], LIF_WARN_SPIKE_CAP);
+        }
+        if (nsw) {
+            atomicAdd(&status[LIF_ST_SPIKES], nsw);
+            atomicAdd(&status[LIF_ST_ROOT_SOLVES], nsw);
+        }
     }
 }
 
@@ -1042,11 +1120,12 @@ FwdLayout fwd_layout(int B, int E_max, int N)
     L.agg = take((size_t)B * L.S * N * sizeof(double2));
     L.carry = take((size_t)B * L.S * N * sizeof(double2));
     L.mask = take((size_t)B * L.S * N * sizeof(uint32_t));
+    L.ent = take((size_t)B * L.S * kSubPerSeg * N * sizeof(double2));
     int tiles = (N + kWave - 1) / kWave;
     L.winfo = take((size_t)B * L.S * tiles * kSubPerSeg * sizeof(WaveInfo));
-    L.counters = take(((size_t)B + 1) * sizeof(uint32_t));
+    L.counters = take(2 * (size_t)B * sizeof(uint32_t));   // per sample: pool use, work-list length
     L.listed = take((size_t)B * N * sizeof(uint32_t));
-    L.work = take((size_t)B * L.S * N * sizeof(uint32_t));   // one entry per (segment, neuron) with candidates
+    L.work = take((size_t)B * N * sizeof(uint32_t));
     // Record pool: one record per flagged (sub-block, neuron).  Each check
     // wave (sample, segment, tile) owns kPoolLocal slots; the overflow is
     // shared per sample and sized at a 64th of the dense bound (far above
@@ -1083,11 +1162,12 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     Decay* segm = (Decay*)(base + L.segm);
     double2* agg = (double2*)(base + L.agg);
     double2* carry = (double2*)(base + L.carry);
+    double2* ent = (double2*)(base + L.ent);
     uint32_t* mask = (uint32_t*)(base + L.mask);
     WaveInfo* winfo = (WaveInfo*)(base + L.winfo);
     uint32_t* counters = (uint32_t*)(base + L.counters);
-    uint32_t* nwork = counters;
-    uint32_t* pool_count = counters + 1;
+    uint32_t* pool_count = counters;
+    uint32_t* nwork = counters + B;
     uint32_t* listed = (uint32_t*)(base + L.listed);
     uint32_t* work = (uint32_t*)(base + L.work);
     Record* pool = (Record*)(base + L.pool);
@@ -1123,14 +1203,16 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
                      ev_n, B, E_max, N, tiles, L.S, segm, agg, carry, status, out_n, listed, counters);
     if (total) {
         TIMED_LAUNCH("check", k_check, dim3((unsigned)total), dim3(kWave * kTilesPerBlock), 0, stream,
-                     ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, tgroups, L.S, (int)total, m, dec, carry, mask,
+                     ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, tgroups, L.S, (int)total, m, dec, carry, ent, mask,
                      winfo, pool, pool_count, (uint32_t)L.pool_local, (uint32_t)(L.pool_cap / (B > 0 ? B : 1)),
                      listed, work, nwork,
                      status);
-        // One wave per listed neuron, as many as can be resident at once.
-        unsigned grid = (unsigned)(nn < 4096 ? nn : 4096);
-        TIMED_LAUNCH("resolve", k_resolve, dim3(grid), dim3(kWave), 0, stream,
-                     ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, L.S, m, dec, carry, mask, winfo, pool,
+        // K single-wave workgroups per sample, about 4096 in all.
+        int K = B > 0 ? 4096 / B : 1;
+        if (K > N) K = N;
+        if (K < 1) K = 1;
+        TIMED_LAUNCH("resolve", k_resolve, dim3((unsigned)((size_t)B * K)), dim3(kWave), 0, stream,
+                     ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, tiles, L.S, m, dec, carry, ent, mask, winfo, pool,
                      work, nwork, out_t, out_n, out_i, status);
     }
     return check_launch();

@@ -15,7 +15,7 @@ namespace lif {
 
 struct FwdLayout {
     int S;                                   // segments per sample
-    size_t dec, segm, agg, carry, mask, winfo, counters, listed, work, pool, total;
+    size_t dec, segm, agg, carry, mask, ent, winfo, counters, listed, work, pool, total;
     size_t pool_local;                       // record slots per check wave
     size_t pool_cap;                         // overflow records shared per sample
 };
