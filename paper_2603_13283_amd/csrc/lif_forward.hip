@@ -965,8 +965,9 @@ __device__ void resolve_neuron(ResolveLds& sh, ResolveStats& acc, int b, int n, 
     acc.spikes += ns;
 }
 
-// Work-list driven: workgroup (b, k) takes entries k, k + K, ... of sample
-// b's list of neurons built by k_check (K workgroups per sample).  Status
+// Work-list driven: the per-sample lists of neurons built by k_check are
+// taken as one concatenated list, entry w by workgroup w mod gridDim.x, so
+// that samples with many listed neurons spread over the whole grid.  Status
 // counts are added once per workgroup.
 __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src,
                                                    const int32_t* __restrict__ ev_n, int B, int E_max,
@@ -982,13 +983,38 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
                                                    float* __restrict__ out_i, int32_t* __restrict__ status)
 {
     __shared__ ResolveLds sh;
-    const int K = (int)gridDim.x / B;
-    const int b = (int)blockIdx.x / K, k = (int)blockIdx.x % K;
-    const uint32_t count = nwork[b];
-    const uint32_t* list = work + (size_t)b * N;
+    const int lane = (int)threadIdx.x;
     ResolveStats acc{0, 0, 0, 0};
-    for (uint32_t w = (uint32_t)k; w < count; w += (uint32_t)K) {
-        const uint32_t bn = list[w];
+    // Running sum of the list lengths over groups of 64 samples (one load
+    // per lane, a wave prefix sum): entry w of the concatenated lists belongs
+    // to the first sample whose running sum exceeds w.
+    int b0 = 0;               // first sample of the current group
+    uint32_t base = 0;        // entries of the samples before the group
+    uint32_t incl = 0;        // running sum up to and including sample b0 + lane
+    auto load_group = [&]() {
+        uint32_t c = b0 + lane < B ? nwork[b0 + lane] : 0u;
+#pragma unroll
+        for (int off = 1; off < kWave; off <<= 1) {
+            const uint32_t v = (uint32_t)__shfl_up((int)c, off, kWave);
+            if (lane >= off) c += v;
+        }
+        incl = base + c;
+    };
+    load_group();
+    for (uint32_t w = blockIdx.x;; w += gridDim.x) {
+        unsigned long long past = __ballot(b0 + lane < B && incl <= w);
+        while (past == ~0ull) {              // w lies beyond the whole group
+            base = (uint32_t)__shfl((int)incl, kWave - 1, kWave);
+            b0 += kWave;
+            if (b0 >= B) break;
+            load_group();
+            past = __ballot(b0 + lane < B && incl <= w);
+        }
+        const int l = __popcll(past);        // samples of the group whose entries end at or before w
+        const int b = b0 + l;
+        if (b0 >= B || l >= kWave || b >= B) break;
+        const uint32_t before = l > 0 ? (uint32_t)__shfl((int)incl, l - 1, kWave) : base;
+        const uint32_t bn = work[(size_t)b * N + (w - before)];
         resolve_neuron(sh, acc, (int)(bn / (uint32_t)N), (int)(bn % (uint32_t)N), ev_t, ev_src, ev_n, E_max, WT,
                        C_in, N, tiles, S, m, dec, carry, ent, mask, winfo, pool, out_t, out_n, out_i);
     }
@@ -1207,11 +1233,9 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
                      winfo, pool, pool_count, (uint32_t)L.pool_local, (uint32_t)(L.pool_cap / (B > 0 ? B : 1)),
                      listed, work, nwork,
                      status);
-        // K single-wave workgroups per sample, about 4096 in all.
-        int K = B > 0 ? 4096 / B : 1;
-        if (K > N) K = N;
-        if (K < 1) K = 1;
-        TIMED_LAUNCH("resolve", k_resolve, dim3((unsigned)((size_t)B * K)), dim3(kWave), 0, stream,
+        // Single-wave workgroups over the concatenated per-sample lists.
+        const unsigned rgrid = (unsigned)(nn < 4096 ? nn : 4096);
+        TIMED_LAUNCH("resolve", k_resolve, dim3(rgrid), dim3(kWave), 0, stream,
                      ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, tiles, L.S, m, dec, carry, ent, mask, winfo, pool,
                      work, nwork, out_t, out_n, out_i, status);
     }
