@@ -119,16 +119,21 @@ def test_config2_driven(env):
     assert s["par"]["spikes"] > 1000
 
 
-def test_config4_bursts_sampled(env):
-    cfg = W.config4(B=4)
-    WT = cfg.layers[0].WT[:, :192]
-    s = check(env, cfg.events, WT, "c4", both=False)
-    assert s["par"]["spikes"] > 100
+def test_config4_bursts_full(env):
+    """2312 -> 1024, batch 64, ~20k events per sample in three bursts."""
+    cfg = W.config4()
+    s = check(env, cfg.events, cfg.layers[0].WT, "c4")
+    assert s["par"]["spikes"] > 10000
+    assert s["par"]["status"][1] == 0
 
 
-def test_config3_layer1_sampled(env):
-    cfg = W.config3(B=6)
-    check(env, cfg.events, cfg.layers[0].WT, "c3-l1", both=False)
+def test_config5_full_stated_gain(env):
+    """32768 -> 2048 at the stated gain, batch 16, ~100k events per sample:
+    the hidden layer stays silent on both sides (the driven variant is in
+    the two-layer tests)."""
+    cfg = W.config5()
+    s = check(env, cfg.events, cfg.layers[0].WT, "c5-hidden", both=False)
+    assert s["par"]["spikes"] == 0 and s["par"]["status"][6] == int(cfg.events.ev_n.sum())
 
 
 def test_determinism(env):
