@@ -64,7 +64,10 @@ typedef struct ihipStream_t* lif_stream_t;
 #define LIF_ST_ROOT_SOLVES   5  /* spike-time root solves                    */
 #define LIF_ST_EVENTS        6  /* input events consumed (sum of ev_n)       */
 #define LIF_ST_POOL_FALLBACK 7  /* flagged sub-blocks that found the record
-                                   pool full (resolved by a slower re-walk)  */
+                                   pool full (resolved by a slower re-walk);
+                                   which ones do depends on the order in
+                                   which sub-blocks claim pool slots, so
+                                   this count may differ between calls      */
 
 #define LIF_WARN_SPIKE_CAP   1  /* a neuron stopped at s_max spikes          */
 #define LIF_WARN_UNSORTED    2  /* LIF_VALIDATE: times decrease in a sample  */

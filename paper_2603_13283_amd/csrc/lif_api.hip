@@ -34,9 +34,11 @@ Model make_model(const lif_params& p)
     m.a_rate = m.inv_ts - m.inv_tm;
     m.c_tv = p.tau_mem * p.tau_syn / (p.tau_mem - p.tau_syn);
     m.t_peak = m.c_tv * log(p.tau_mem / p.tau_syn);
-    // The cheap bound is evaluated in float64 with relative error ~1e-15; the
-    // margin keeps it conservative for thresholds of any sign.
+    // The no-crossing screen is evaluated in float64 with relative error
+    // ~1e-15; the margin keeps it conservative.
     m.th_lo = p.v_th - 1e-9 * fmax(1.0, fabs(p.v_th));
+    m.thk_lo = m.th_lo / m.kappa;
+    m.inv_ktm = 1.0 / (m.kappa * p.tau_mem);
     m.inv_th = 1.0 / p.v_th;
     m.th_1k = p.v_th * (1.0 + m.kappa);
     m.ts_tm = p.tau_syn / p.tau_mem;

@@ -59,7 +59,7 @@ __global__ __launch_bounds__(256) void k_bwd_decay(const float* __restrict__ ev_
     d.A = exp(-dt * m.inv_tm);
     d.D = exp(-dt * m.inv_ts);
     d.C = 0.0;
-    d.g = 0.0;
+    d.lk = 0.0;
     dec[idx] = d;
 }
 

@@ -29,7 +29,9 @@ struct Model {
     double c_tv;       // tau_m tau_s / (tau_m - tau_s)               (Eq. t_vmax)
     double inv_tm, inv_ts;
     double t_peak;     // argmax of the unit kernel K(u) = kappa (e^-u/tm - e^-u/ts)
-    double th_lo;      // survival threshold of the cheap upper bound (slightly below th)
+    double th_lo;      // survival threshold of the no-crossing screen (slightly below th)
+    double thk_lo;     // th_lo / kappa: the same threshold in the eigen-coordinates of the walks
+    double inv_ktm;    // 1 / (kappa tau_m)
     double inv_th;     // 1 / th
     double th_1k;      // th (1 + kappa)
     double ts_tm;      // tau_s / tau_m
@@ -42,12 +44,37 @@ struct Model {
 
 // Per-event decay record, shared by every neuron of a sample (the matrix
 // M(dt) of Eq. affine depends only on the gap dt to the previous event):
-//   A = e^{-dt/tm}, C = kappa (e^{-dt/tm} - e^{-dt/ts}), D = e^{-dt/ts},
-//   g = K(min(dt, t_peak)): the largest value the unit kernel reaches inside
-//       the gap, used by the no-crossing bound V <= max(V0,0) + max(I0,0) g.
+//   A = e^{-dt/tm}, D = e^{-dt/ts}, C = kappa (e^{-dt/tm} - e^{-dt/ts}),
+//   lk = dt / (kappa tm): the slope factor of the no-crossing screen.
+// Padding entries past a sample's last event hold the identity map
+// (A = D = 1, C = lk = 0).
 struct alignas(32) Decay {
-    double A, C, D, g;
+    double A, D, C, lk;
 };
+
+// Eigen-coordinates of the event map.  M(dt) = [[A, C], [0, D]] has the
+// eigenvalues A and D; with U = V / kappa + I and J = I the state decays as
+// two independent exponentials, U -> A U and J -> D J, an input of weight w
+// adds w to both (it raises I and leaves V unchanged), and
+// V = kappa (U - J), I = J.  This is Eq. mem_pot (V = (V0 + kappa I0)
+// e^{-t/tm} - kappa I0 e^{-t/ts}) with both terms divided by kappa.
+__device__ __forceinline__ double v_of(const Model& m, double U, double J) { return m.kappa * (U - J); }
+__device__ __forceinline__ double u_of(const Model& m, double V, double I) { return V / m.kappa + I; }
+
+// No-crossing screen of one interval of length L = lk kappa tm that starts
+// in the no-reset state (U, J): the interval can reach the threshold only if
+//   (U - J) + max(J - th, 0) lk >= th_lo / kappa,
+// i.e. V0 + max(I0 - th, 0) L / tm >= th_lo.  Proof: with
+// h(u) = (V_lin(u) - th) e^{u/tm}, h'(u) = (I0 e^{-u (1/ts - 1/tm)} - th
+// e^{u/tm}) / tm; for I0 > th, h is concave and lies below its tangent at 0,
+// h(0) + h'(0) u = V0 - th + (I0 - th) u / tm; for I0 <= th, h is
+// decreasing and its maximum is h(0) = V0 - th.  Resets only lower V
+// (Sec. 3.1: the reset subtracts a positive decaying term), so an interval
+// that fails the screen for the no-reset state holds no spike.
+__device__ __forceinline__ double screen_value(const Model& m, double U, double J, double lk)
+{
+    return fma(fmax(J - m.th, 0.0), lk, U - J);
+}
 
 // Source channel of an event, clamped into [0, C_in) so that a malformed
 // queue can never address outside W (LIF_VALIDATE reports such events).

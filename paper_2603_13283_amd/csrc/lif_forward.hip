@@ -1,33 +1,36 @@
 // lif_forward.hip -- forward pass of the event-driven LIF layer on gfx950.
 //
-// Pipeline for one call (one sample = one event queue; N neurons share it):
-//   k_decay      per (sample, event): the event's affine map M(dt) of
-//                Eq. affine depends only on the gap to the previous event, so
-//                its three entries (and a no-crossing bound factor) are
-//                computed once per sample and shared by every neuron; per
-//                segment of kSeg events also the composed map M(T_seg)
-//                (the maps form a semigroup: M(a) M(b) = M(a + b)).
-//   k_aggregate  per (sample, 64-neuron tile, segment): one wave walks the
-//                segment's events from the zero state; lanes are neurons and
-//                read their weight of each event from the event's W^T row
-//                (one coalesced 256-byte row slice per event).  The result is
-//                the b-part of the Combine of the segment's maps.
-//   k_carry      per (sample, neuron): exclusive Combine scan over segments,
-//                giving the no-reset state entering every segment.
-//   k_check      per (sample, tile, segment): re-walk from the carried state
-//                and test every inter-event interval with the paper's
-//                interval rule (Sec. 3.2.2) behind a cheap exact upper bound.
-//                Because resets only lower V, a segment whose no-reset
-//                trajectory never reaches threshold cannot hold a spike, so
-//                only flagged sub-blocks of kSub events are kept (with their
-//                entering state and an upper bound of V over them).
-//   k_resolve    per (sample, neuron): walks only its flagged sub-blocks in
-//                time order.  Spikes found so far lower V by a known decaying
-//                amount (the reset deficit), which both corrects the entering
-//                state and certifies later sub-blocks without walking them.
-//                A walked sub-block resolves spikes exactly: interval rule,
-//                bracketed Newton (Appendix D.1), hard reset of V, re-test of
-//                the same interval from the spike (Appendix E.2).
+// Pipeline for one call (a sample is one sorted event queue, shared by the
+// N neurons of the layer):
+//   k_prep       per (sample, event): the affine map M(dt) of Eq. affine
+//                depends only on the gap to the previous event, so its
+//                entries are computed once per sample and shared by every
+//                neuron; per segment of kSeg events also the composed map
+//                (the maps form a semigroup, M(a) M(b) = M(a + b)).  Also
+//                resets the outputs, status words and counters.
+//   k_aggregate  per (sample, segment, tile of 64 NPL neurons): one wave walks
+//                the segment from the zero state in the eigen-coordinates
+//                (U, J) of the maps (two FMAs per neuron-event, the decays as
+//                scalar operands).  Lane l holds NPL adjacent neurons and
+//                reads their weights of an event with one vector load from
+//                the event's W^T row.  The result is the b-part of the
+//                Combine of the segment's maps.
+//   k_carry      per (sample, 64 neurons): exclusive Combine scan over the
+//                segments (diagonal maps in (U, J)), giving the no-reset
+//                state entering every segment.
+//   k_check      per (sample, segment, tile): re-walk from the carried state
+//                with a no-crossing screen per inter-event interval
+//                (screen_value).  Resets only lower V, so a sub-block of kSub
+//                events whose no-reset trajectory passes every screen holds
+//                no spike whatever happened before it; flagged sub-blocks
+//                get a record of their no-reset states for the resolve pass.
+//   k_resolve    per (sample, neuron) with flagged sub-blocks: walks only
+//                those, in time order.  Spikes found so far lower V by a
+//                known decaying amount (the reset deficit), which corrects
+//                the recorded states exactly.  Each interval is tested with
+//                the interval rule (Sec. 3.2.2), the spike time is solved by
+//                bracketed Newton (Appendix D.1), V is hard-reset and the
+//                same interval is tested again from the spike (Appendix E.2).
 // The sequential baseline k_sequential (Appendix E.3) runs the same interval
 // rule and root solve one event at a time per (sample, neuron).
 #include "lif_common.hpp"
@@ -39,19 +42,12 @@ namespace lif {
 // entering it and right after each of its kSub events.  With the reset
 // deficit of the spikes found so far, these give the true state at every
 // interval boundary of the sub-block in O(1), so the resolve pass can test
-// all of its intervals at once.  Records live in a pool; each wave allocates
-// the records of one sub-block with one atomic and notes (lane mask, first
-// slot).
+// all of its intervals at once.  Records live in per-sample pools; each
+// wave allocates the records of one sub-block with one atomic.
 struct alignas(16) Record {
     double2 s[kSub + 1];    // s[0]: entering state; s[j + 1]: after event j
 };
 static_assert(sizeof(Record) == 16 * (kSub + 1), "record layout");
-
-struct alignas(16) WaveInfo {
-    unsigned long long lanes;   // lanes of the wave with a record for this sub-block
-    uint32_t base;              // pool slot of the lowest such lane, kNoSlot if the pool was full
-    uint32_t pad;
-};
 constexpr uint32_t kNoSlot = 0xffffffffu;
 
 // Workgroup index -> work index such that each of the 8 XCDs (which receive
@@ -67,7 +63,7 @@ __device__ __forceinline__ int xcd_remap(int wg, int total)
 }
 
 // ---------------------------------------------------------------------------
-// k_decay
+// k_prep
 // ---------------------------------------------------------------------------
 // Decay record of event k (gap to the previous event, or to t = 0).
 __device__ __forceinline__ Decay make_decay(const Model& m, const float* __restrict__ t, int k)
@@ -77,30 +73,55 @@ __device__ __forceinline__ Decay make_decay(const Model& m, const float* __restr
     d.A = exp(-dt * m.inv_tm);
     d.D = exp(-dt * m.inv_ts);
     d.C = unit_kernel(m, dt, d.A);
-    double gl = fmin(dt, m.t_peak);
-    d.g = unit_kernel(m, gl, exp(-gl * m.inv_tm)) * (1.0 + 1e-12);
+    d.lk = dt * m.inv_ktm;
     return d;
 }
 
-__global__ __launch_bounds__(256) void k_decay(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_n,
-                                               int B, int E_max, int S, Model m, Decay* __restrict__ dec,
-                                               int32_t* __restrict__ status, uint32_t* __restrict__ counters,
-                                               float* __restrict__ out_t, float* __restrict__ out_i, size_t n_out)
+// Decays dec[B][E_pad] (identity maps past each sample's last event, so
+// that the walks run whole sub-blocks), the composed maps (A, D) of every
+// segment, and the reset of status words, counters and outputs (out_t is
+// filled with +inf when given: the resolve pass writes only neurons that
+// fire).
+__global__ __launch_bounds__(256) void k_prep(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_n,
+                                              int B, int E_max, int E_pad, int S, Model m, Decay* __restrict__ dec,
+                                              double2* __restrict__ segm, int32_t* __restrict__ status,
+                                              uint32_t* __restrict__ counters, size_t n_counters,
+                                              int32_t* __restrict__ out_n, uint32_t* __restrict__ listed, size_t nn,
+                                              float* __restrict__ out_t, float* __restrict__ out_i, size_t n_out)
 {
     const size_t tid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     const size_t stride = (size_t)gridDim.x * blockDim.x;
     if (tid < LIF_STATUS_WORDS) status[tid] = 0;
+    for (size_t i = tid; i < n_counters; i += stride) counters[i] = 0u;
+    for (size_t i = tid; i < nn; i += stride) {
+        out_n[i] = 0;
+        if (listed) listed[i] = 0u;
+    }
     if (out_t) {
         for (size_t i = tid; i < n_out; i += stride) {
             out_t[i] = INFINITY;
             if (out_i) out_i[i] = 0.0f;
         }
     }
-    const size_t nev = (size_t)B * (size_t)E_max;
+    const size_t nev = (size_t)B * (size_t)E_pad;
     for (size_t idx = tid; idx < nev; idx += stride) {
-        int b = (int)(idx / (size_t)E_max), k = (int)(idx % (size_t)E_max);
-        if (k >= clamp_count(ev_n[b], E_max)) continue;
-        dec[idx] = make_decay(m, ev_t + (size_t)b * E_max, k);
+        const int b = (int)(idx / (size_t)E_pad), k = (int)(idx % (size_t)E_pad);
+        Decay d{1.0, 1.0, 0.0, 0.0};
+        if (k < clamp_count(ev_n[b], E_max)) d = make_decay(m, ev_t + (size_t)b * E_max, k);
+        dec[idx] = d;
+    }
+    if (segm) {
+        for (size_t idx = tid; idx < (size_t)B * S; idx += stride) {
+            const int b = (int)(idx / (size_t)S), j = (int)(idx % (size_t)S);
+            const int nb = clamp_count(ev_n[b], E_max), k0 = j * kSeg;
+            double2 r = make_double2(1.0, 1.0);
+            if (k0 < nb) {
+                const float* tt = ev_t + (size_t)b * E_max;
+                const double T = (double)tt[min(k0 + kSeg, nb) - 1] - (k0 > 0 ? (double)tt[k0 - 1] : 0.0);
+                r = make_double2(exp(-T * m.inv_tm), exp(-T * m.inv_ts));
+            }
+            segm[idx] = r;
+        }
     }
 }
 
@@ -124,412 +145,520 @@ __global__ __launch_bounds__(256) void k_validate(const float* __restrict__ ev_t
 }
 
 // ---------------------------------------------------------------------------
-// Segment walks.  A workgroup of kTilesPerBlock waves takes one (sample,
-// segment) and kTilesPerBlock 64-neuron tiles; lanes are neurons.  The
-// segment's decay records are computed (k_aggregate) or fetched (k_check)
-// once into LDS and read by all of its waves.  Each event's source is
-// wave-uniform; lane j holds the sources of events j and j + 64 and each is
-// broadcast with a lane read, so the weight loads of the next kSub events
-// (one coalesced W^T row slice per event) are issued while the current kSub
-// events are walked.
+// Segment walks (k_aggregate, k_check).  A work item is (sample, segment,
+// tile of 64 NPL neurons) and takes one wave; a workgroup runs kWalkWaves
+// consecutive items.  Lane l holds neurons tile * 64 NPL + l NPL + i,
+// i < NPL, and reads their weights of an event with one NPL-wide load from
+// the event's W^T row (the wave reads 256 NPL contiguous bytes).  Sources
+// and decays are wave-uniform and are read with scalar loads; the weights of
+// the next kSub events are loaded while the current kSub events are walked.
 // ---------------------------------------------------------------------------
-constexpr int kTilesPerBlock = 4;
-constexpr int kPoolLocal = 16;     // record slots owned by each check wave
-constexpr int kSrcRegs = kSeg / kWave;
+constexpr int kWalkWaves = 4;
 
-struct SegCoords {
-    int b, seg, tile, wave, lane, n, nc, nb, k0, cnt;
+struct WalkCoords {
+    int b, seg, tile, lane, n0, nb, k0, cnt;
+    bool live;                    // the lane holds neurons (n0 < N)
 };
 
-__device__ __forceinline__ SegCoords seg_coords(int total, int tgroups, int S, const int32_t* __restrict__ ev_n,
-                                                int E_max, int N)
+template <int NPL>
+__device__ __forceinline__ bool walk_coords(int items, int tiles, int S, const int32_t* __restrict__ ev_n, int E_max,
+                                            int N, WalkCoords& c)
 {
-    SegCoords c;
-    int lin = xcd_remap(blockIdx.x, total);
-    int tg = lin % tgroups;
-    int rest = lin / tgroups;
+    // wave-uniform by construction; readfirstlane lets the compiler keep
+    // everything derived from it (sources, decays) in scalar registers
+    const int item = __builtin_amdgcn_readfirstlane(xcd_remap(blockIdx.x, gridDim.x) * kWalkWaves +
+                                                    (int)threadIdx.x / kWave);
+    if (item >= items) return false;
+    c.tile = item % tiles;
+    const int rest = item / tiles;
     c.seg = rest % S;
     c.b = rest / S;
-    c.wave = (int)threadIdx.x / kWave;
     c.lane = (int)threadIdx.x % kWave;
-    c.tile = tg * kTilesPerBlock + c.wave;
-    c.n = c.tile * kWave + c.lane;
-    c.nc = min(c.n, N - 1);
     c.nb = clamp_count(ev_n[c.b], E_max);
     c.k0 = c.seg * kSeg;
+    if (c.k0 >= c.nb) return false;
     c.cnt = min(kSeg, c.nb - c.k0);
-    return c;
+    const int n0 = c.tile * (kWave * NPL) + c.lane * NPL;
+    c.live = n0 < N;
+    c.n0 = c.live ? n0 : 0;
+    return true;
 }
 
-struct SrcRegs {
-    int v[kSrcRegs];
+template <int NPL>
+__device__ __forceinline__ void load_w(const float* __restrict__ p, float (&w)[NPL])
+{
+    if constexpr (NPL == 4) {
+        const float4 v = *reinterpret_cast<const float4*>(p);
+        w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+    } else if constexpr (NPL == 2) {
+        const float2 v = *reinterpret_cast<const float2*>(p);
+        w[0] = v.x; w[1] = v.y;
+    } else {
+        w[0] = *p;
+    }
+}
+
+// Per-wave staging of a segment.  The sources of its events go to VGPRs
+// (lane l holds those of events l and l + 64) and are broadcast with one lane
+// read per event; the decays (A, D) and screen slopes lk go to the wave's
+// slice of LDS and are read back as wave-wide broadcasts; for the check pass
+// also the largest slope of each group of kGrp intervals.  The weights are
+// read with buffer loads whose per-event row offset is a scalar operand, so
+// a load in flight holds no address registers.
+constexpr int kGrp = 8;
+constexpr int kGrpPerSeg = kSeg / kGrp;
+static_assert(kSub == 2 * kGrp && kWave % kGrp == 0, "a sub-block is two groups; groups tile lane ranges");
+constexpr int kSrcRegs = kSeg / kWave;
+
+struct Stage {
+    int off[kSrcRegs];                 // W^T row byte offsets of events lane, lane + 64
+    __amdgpu_buffer_rsrc_t rsrc;       // W^T as a raw buffer
+    uint32_t lane_off;                 // byte offset of the lane's first neuron in a row
 };
 
-__device__ __forceinline__ SrcRegs load_sources(const int32_t* __restrict__ src, int cnt, int lane, int C_in)
+__device__ __forceinline__ void wave_lds_sync()
 {
-    SrcRegs r;
-#pragma unroll
-    for (int h = 0; h < kSrcRegs; ++h) r.v[h] = h * kWave + lane < cnt ? clamp_src(src[h * kWave + lane], C_in) : 0;
-    return r;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Weights of events q*kSub .. q*kSub + kSub - 1 of the segment (0 past cnt).
-__device__ __forceinline__ void load_sub_weights(const SrcRegs& sr, const float* __restrict__ wcol, int N, int cnt,
-                                                 int q, float (&w)[kSub])
+// The buffer descriptor's fourth word for raw 32-bit-element buffers on gfx9.
+constexpr int kRsrcWord3 = 0x00020000;
+
+__device__ __forceinline__ Stage stage_segment(const WalkCoords& c, const int32_t* __restrict__ ss,
+                                               const Decay* __restrict__ sd, const float* __restrict__ WT, int C_in,
+                                               int N, double2* __restrict__ lad, double* __restrict__ llk,
+                                               double* __restrict__ lgk)
 {
+    Stage st;
+    st.rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)WT, (short)0, (int)((uint32_t)C_in * (uint32_t)N * 4u),
+                                                kRsrcWord3);
+    st.lane_off = (uint32_t)c.n0 * 4u;
 #pragma unroll
-    for (int j = 0; j < kSub; ++j) {
-        const int e = q * kSub + j;
-        int sj = __builtin_amdgcn_readlane(sr.v[e / kWave], e % kWave);
-        w[j] = e < cnt ? wcol[(size_t)sj * (size_t)N] : 0.0f;
+    for (int h = 0; h < kSrcRegs; ++h) {
+        const int e = h * kWave + c.lane;
+        st.off[h] = clamp_src(ss[min(e, c.cnt - 1)], C_in) * N * 4;
+        const Decay d = sd[e];
+        lad[e] = make_double2(d.A, d.D);
+        if (llk) llk[e] = d.lk;
     }
-}
-
-// The same, with the sources read as wave-uniform (scalar) loads.  All
-// sixteen source loads are issued before the first is used (past cnt the
-// last event is read again and its weight discarded).
-__device__ __forceinline__ void load_sub_weights_s(const int32_t* __restrict__ sseg, const float* __restrict__ wcol,
-                                                   int N, int C_in, int cnt, int q, float (&w)[kSub])
-{
-    int sj[kSub];
+    wave_lds_sync();
+    if (lgk) {
+        if (c.lane < kGrpPerSeg) {
+            double g = 0.0;
 #pragma unroll
-    for (int j = 0; j < kSub; ++j) sj[j] = sseg[min(q * kSub + j, cnt - 1)];
-#pragma unroll
-    for (int j = 0; j < kSub; ++j) w[j] = wcol[(size_t)clamp_src(sj[j], C_in) * (size_t)N];
-#pragma unroll
-    for (int j = 0; j < kSub; ++j)
-        if (q * kSub + j >= cnt) w[j] = 0.0f;
-}
-
-__global__ __launch_bounds__(kWave * kTilesPerBlock) void k_aggregate(
-    const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
-    const float* __restrict__ WT, int C_in, int N, int tiles, int tgroups, int S, int total, Model m,
-    Decay* __restrict__ dec, Decay* __restrict__ segm, double2* __restrict__ agg, int32_t* __restrict__ status,
-    uint32_t* __restrict__ counters, float* __restrict__ out_t, float* __restrict__ out_i, size_t n_out)
-{
-    __shared__ Decay sd[kSeg];
-    if (blockIdx.x == 0 && threadIdx.x < LIF_STATUS_WORDS) status[threadIdx.x] = 0;
-    {
-        // Every neuron starts with no spike (+inf times); the resolve pass
-        // overwrites the outputs of neurons that fire.  Coalesced fill spread
-        // over the whole launch.
-        const size_t stride = (size_t)gridDim.x * blockDim.x;
-        for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_out; i += stride) {
-            out_t[i] = INFINITY;
-            if (out_i) out_i[i] = 0.0f;
+            for (int j = 0; j < kGrp; ++j) g = fmax(g, llk[c.lane * kGrp + j]);
+            lgk[c.lane] = g;
         }
+        wave_lds_sync();
     }
-    const SegCoords c = seg_coords(total, tgroups, S, ev_n, E_max, N);
-    if (c.k0 >= c.nb) return;                        // uniform over the workgroup
-    const float* tt = ev_t + (size_t)c.b * E_max;
-    const int tg = c.tile / kTilesPerBlock;
-    if ((int)threadIdx.x < c.cnt) {
-        int k = c.k0 + (int)threadIdx.x;
-        Decay e = make_decay(m, tt, k);
-        sd[threadIdx.x] = e;
-        if (tg == 0) dec[(size_t)c.b * E_max + k] = e;
+    return st;
+}
+
+template <int NPL>
+__device__ __forceinline__ void load_w(const Stage& st, int soff, float (&w)[NPL])
+{
+    if constexpr (NPL == 4) {
+        const float4 v = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(st.rsrc, st.lane_off, soff, 0));
+        w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+    } else if constexpr (NPL == 2) {
+        const float2 v = __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(st.rsrc, st.lane_off, soff, 0));
+        w[0] = v.x; w[1] = v.y;
+    } else {
+        w[0] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(st.rsrc, st.lane_off, soff, 0));
     }
-    if (tg == 0 && threadIdx.x == kSeg % (kWave * kTilesPerBlock)) {
-        // The segment's composed map M(T) (the maps form a semigroup).
-        double T = (double)tt[c.k0 + c.cnt - 1] - (c.k0 > 0 ? (double)tt[c.k0 - 1] : 0.0);
-        Decay sm;
-        sm.A = exp(-T * m.inv_tm);
-        sm.D = exp(-T * m.inv_ts);
-        sm.C = unit_kernel(m, T, sm.A);
-        sm.g = T;
-        segm[(size_t)c.b * S + c.seg] = sm;
+}
+
+// Weights of events e0 .. e0 + kGrp - 1 of the segment (past the last event
+// the last event's row is read again; the walks never use those).
+template <int NPL>
+__device__ __forceinline__ void load_grp(const Stage& st, int e0, float (&w)[kGrp][NPL])
+{
+    const int oreg = e0 < kWave ? st.off[0] : st.off[kSrcRegs - 1];
+#pragma unroll
+    for (int j = 0; j < kGrp; ++j) load_w<NPL>(st, __builtin_amdgcn_readlane(oreg, (e0 + j) & (kWave - 1)), w[j]);
+}
+
+// One event in eigen-coordinates: decay over the gap, then the jump.
+template <int NPL>
+__device__ __forceinline__ void step(double A, double D, const float (&w)[NPL], double (&U)[NPL], double (&J)[NPL])
+{
+#pragma unroll
+    for (int i = 0; i < NPL; ++i) {
+        const double x = (double)w[i];
+        U[i] = fma(A, U[i], x);
+        J[i] = fma(D, J[i], x);
     }
-    __syncthreads();
-    if (c.tile >= tiles) return;
-    const float* wcol = WT + c.nc;
-    const SrcRegs sr = load_sources(ev_src + (size_t)c.b * E_max + c.k0, c.cnt, c.lane, C_in);
-    double V = 0.0, I = 0.0;
-    float wn[kSub], wn2[kSub];
-    load_sub_weights(sr, wcol, N, c.cnt, 0, wn);
-    if (kSub < c.cnt) load_sub_weights(sr, wcol, N, c.cnt, 1, wn2);
+}
+
+// Walk the n events of a group starting at e0 (n = kGrp on every group but
+// a sample's last).
+template <int NPL>
+__device__ __forceinline__ void walk_grp(const double2* __restrict__ lad, int e0, int n, const float (&w)[kGrp][NPL],
+                                         double (&U)[NPL], double (&J)[NPL])
+{
+    if (n >= kGrp) {
 #pragma unroll
-    for (int q = 0; q < kSubPerSeg; ++q) {
-        if (q * kSub < c.cnt) {
-            float w[kSub];
+        for (int j = 0; j < kGrp; ++j) {
+            const double2 ad = lad[e0 + j];
+            step<NPL>(ad.x, ad.y, w[j], U, J);
+        }
+    } else {
 #pragma unroll
-            for (int j = 0; j < kSub; ++j) { w[j] = wn[j]; wn[j] = wn2[j]; }
-            if (q + 2 < kSubPerSeg && (q + 2) * kSub < c.cnt) load_sub_weights(sr, wcol, N, c.cnt, q + 2, wn2);
-            if ((q + 1) * kSub <= c.cnt) {            // full sub-block: straight-line code
-#pragma unroll
-                for (int j = 0; j < kSub; ++j) {
-                    Decay e = sd[q * kSub + j];
-                    double Vn = e.A * V + e.C * I;
-                    I = e.D * I + (double)w[j];
-                    V = Vn;
-                }
-            } else {
-                for (int j = 0; j < c.cnt - q * kSub; ++j) {
-                    Decay e = sd[q * kSub + j];
-                    double Vn = e.A * V + e.C * I;
-                    I = e.D * I + (double)w[j];
-                    V = Vn;
-                }
+        for (int j = 0; j < kGrp; ++j)
+            if (j < n) {
+                const double2 ad = lad[e0 + j];
+                step<NPL>(ad.x, ad.y, w[j], U, J);
             }
-        }
     }
-    if (c.n < N) agg[((size_t)c.b * S + c.seg) * N + c.n] = make_double2(V, I);
 }
 
-// Exclusive scan over segments of the Combine of Eq. affine:
-// s_in(j+1) = M(T_j) s_in(j) + b_j, with s_in(0) = (0, 0).  A workgroup of
-// kCarryWaves waves takes one (sample, 64-neuron tile); lanes are neurons
-// and wave w the w-th contiguous range of segments.  Each wave folds its
-// range from the zero state (the segment aggregates are fetched
-// kCarryBatch at a time so that their loads overlap), the range totals are
-// combined across waves in LDS (the maps compose in closed form), and each
-// wave walks its range again from its incoming state, writing the carries.
-constexpr int kCarryBatch = 16;
-constexpr int kCarryWaves = 4;
-
-struct Affine {               // the map s -> M s + b of a range of segments
-    double A, C, D;           // M = [[A, C], [0, D]] (wave-uniform)
-    double V, I;              // b (per neuron)
-};
-
-__device__ __forceinline__ void carry_batch(const double2* __restrict__ agg, const Decay* __restrict__ segm,
-                                            size_t row0, size_t seg_row, int N, int n, int j0, int j1,
-                                            double2 (&a)[kCarryBatch], double (&mA)[kCarryBatch],
-                                            double (&mC)[kCarryBatch], double (&mD)[kCarryBatch])
+template <int NPL>
+__global__ __launch_bounds__(kWave * kWalkWaves) void k_aggregate(
+    const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max, int E_pad,
+    const float* __restrict__ WT, int C_in, int N, int tiles, int S, int items, const Decay* __restrict__ dec,
+    double2* __restrict__ agg)
 {
+    __shared__ double2 s_ad[kWalkWaves][kSeg];
+    WalkCoords c;
+    if (!walk_coords<NPL>(items, tiles, S, ev_n, E_max, N, c)) return;
+    double2* lad = s_ad[threadIdx.x / kWave];
+    const Stage st = stage_segment(c, ev_src + (size_t)c.b * E_max + c.k0, dec + (size_t)c.b * E_pad + c.k0, WT,
+                                   C_in, N, lad, nullptr, nullptr);
+    double U[NPL], J[NPL];
 #pragma unroll
-    for (int j = 0; j < kCarryBatch; ++j) {
-        const int jj = min(j0 + j, j1 - 1);
-        a[j] = agg[(row0 + (size_t)jj) * N + n];
-        const Decay* M = segm + seg_row + jj;
-        mA[j] = __builtin_nontemporal_load(&M->A);
-        mC[j] = __builtin_nontemporal_load(&M->C);
-        mD[j] = __builtin_nontemporal_load(&M->D);
+    for (int i = 0; i < NPL; ++i) U[i] = J[i] = 0.0;
+    // Two weight buffers in alternation (no register copies): wa holds the
+    // even and wb the odd groups.
+    float wa[kGrp][NPL], wb[kGrp][NPL];
+    load_grp<NPL>(st, 0, wa);
+    for (int e0 = 0; e0 < c.cnt; e0 += 2 * kGrp) {
+        load_grp<NPL>(st, e0 + kGrp, wb);
+        walk_grp<NPL>(lad, e0, c.cnt - e0, wa, U, J);
+        if (e0 + kGrp >= c.cnt) break;
+        load_grp<NPL>(st, e0 + 2 * kGrp, wa);
+        walk_grp<NPL>(lad, e0 + kGrp, c.cnt - e0 - kGrp, wb, U, J);
+    }
+    if (c.live) {
+        const size_t row = ((size_t)c.b * S + c.seg) * N + c.n0;
+#pragma unroll
+        for (int i = 0; i < NPL; ++i) agg[row + i] = make_double2(U[i], J[i]);
     }
 }
+
+// Exclusive scan over segments of the Combine of Eq. affine in (U, J):
+// s_in(j + 1) = M(T_j) s_in(j) + agg_j, s_in(0) = 0, where M(T_j) =
+// diag(A_j, D_j) (segm).  A workgroup of kCarryWaves waves takes one
+// (sample, 64-neuron tile); lanes are neurons and wave w the w-th contiguous
+// range of at most kCarryBatch segments per round.  Each wave folds its range
+// from the zero state (its aggregates loaded at once and kept), the range
+// totals are combined across waves in LDS, and each wave walks its range
+// again from its incoming state, writing the carries.
+constexpr int kCarryWaves = 4;
+constexpr int kCarryBatch = 16;
 
 __global__ __launch_bounds__(kWave * kCarryWaves) void k_carry(
-    const int32_t* __restrict__ ev_n, int B, int E_max, int N, int tiles, int S, const Decay* __restrict__ segm,
-    const double2* __restrict__ agg, double2* __restrict__ carry, int32_t* __restrict__ status,
-    int32_t* __restrict__ out_n, uint32_t* __restrict__ listed, uint32_t* __restrict__ counters)
+    const int32_t* __restrict__ ev_n, int B, int E_max, int N, int tiles, int S, const double2* __restrict__ segm,
+    const double2* __restrict__ agg, double2* __restrict__ carry, int32_t* __restrict__ status)
 {
-    __shared__ Affine tot[kCarryWaves][kWave];
+    __shared__ double2 tot[kCarryWaves][kWave];      // range map b-part
+    __shared__ double2 dec_tot[kCarryWaves];         // range map diagonal
     const int b = blockIdx.x / tiles, tile = blockIdx.x % tiles;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int n = tile * kWave + lane;
     const bool live = n < N;
     const int nc = live ? n : N - 1;
-    const size_t idx = (size_t)b * N + nc;
-    if (wave == 0 && live) {
-        out_n[idx] = 0;
-        listed[idx] = 0u;
-    }
     const int nb = clamp_count(ev_n[b], E_max);
-    if (threadIdx.x == 0 && tile == 0) {
-        counters[b] = 0u;                       // record pool use of sample b
-        counters[B + b] = 0u;                   // work-list length of sample b
-        atomicAdd(&status[LIF_ST_EVENTS], nb);
-    }
+    if (threadIdx.x == 0 && tile == 0) atomicAdd(&status[LIF_ST_EVENTS], nb);
     const int Sb = (nb + kSeg - 1) / kSeg;
-    const int per = (Sb + kCarryWaves - 1) / kCarryWaves;
-    const int j_lo = min(wave * per, Sb), j_hi = min(j_lo + per, Sb);
-    const size_t row0 = (size_t)b * S, seg_row = (size_t)b * S;
-
-    // ---- fold this wave's range from the zero state
-    Affine f{1.0, 0.0, 1.0, 0.0, 0.0};
-    double2 a[kCarryBatch];
-    double mA[kCarryBatch], mC[kCarryBatch], mD[kCarryBatch];
-    for (int j0 = j_lo; j0 < j_hi; j0 += kCarryBatch) {
-        carry_batch(agg, segm, row0, seg_row, N, nc, j0, j_hi, a, mA, mC, mD);
+    double U = 0.0, J = 0.0;                         // state entering the current round
+    for (int r0 = 0; r0 < Sb; r0 += kCarryWaves * kCarryBatch) {
+        const int per = min(kCarryBatch, (Sb - r0 + kCarryWaves - 1) / kCarryWaves);
+        const int j_lo = min(r0 + wave * per, Sb), j_hi = min(j_lo + per, Sb);
+        double2 a[kCarryBatch], M[kCarryBatch];
 #pragma unroll
         for (int j = 0; j < kCarryBatch; ++j) {
-            if (j0 + j < j_hi) {
-                const double Vn = mA[j] * f.V + mC[j] * f.I + a[j].x;
-                f.I = mD[j] * f.I + a[j].y;
-                f.V = Vn;
-                // M_j composed after the range so far: [[A_j A, A_j C + C_j D], [0, D_j D]]
-                const double Cn = mA[j] * f.C + mC[j] * f.D;
-                f.A *= mA[j];
-                f.D *= mD[j];
-                f.C = Cn;
+            const int jj = min(j_lo + j, Sb - 1);
+            a[j] = agg[((size_t)b * S + jj) * N + nc];
+            M[j] = segm[(size_t)b * S + jj];
+        }
+        // fold the range from zero
+        double fU = 0.0, fJ = 0.0, pA = 1.0, pD = 1.0;
+#pragma unroll
+        for (int j = 0; j < kCarryBatch; ++j) {
+            if (j_lo + j < j_hi) {
+                fU = fma(M[j].x, fU, a[j].x);
+                fJ = fma(M[j].y, fJ, a[j].y);
+                pA *= M[j].x;
+                pD *= M[j].y;
             }
         }
-    }
-    tot[wave][lane] = f;
-    __syncthreads();
-    // ---- incoming state: the earlier ranges applied in order to zero
-    double V = 0.0, I = 0.0;
-    for (int w = 0; w < wave; ++w) {
-        const Affine g = tot[w][lane];
-        const double Vn = g.A * V + g.C * I + g.V;
-        I = g.D * I + g.I;
-        V = Vn;
-    }
-    // ---- walk the range again, writing the carry entering each segment
-    for (int j0 = j_lo; j0 < j_hi; j0 += kCarryBatch) {
-        carry_batch(agg, segm, row0, seg_row, N, nc, j0, j_hi, a, mA, mC, mD);
+        tot[wave][lane] = make_double2(fU, fJ);
+        if (lane == 0) dec_tot[wave] = make_double2(pA, pD);
+        __syncthreads();
+        // incoming state of this wave's range: the earlier ranges applied in order
+        double iU = U, iJ = J;
+        for (int w = 0; w < wave; ++w) {
+            const double2 g = tot[w][lane], gd = dec_tot[w];
+            iU = fma(gd.x, iU, g.x);
+            iJ = fma(gd.y, iJ, g.y);
+        }
+        // state after the whole round (for the next round)
+        for (int w = 0; w < kCarryWaves; ++w) {
+            const double2 g = tot[w][lane], gd = dec_tot[w];
+            U = fma(gd.x, U, g.x);
+            J = fma(gd.y, J, g.y);
+        }
+        __syncthreads();
+        // walk the range again, writing the carry entering each segment
 #pragma unroll
         for (int j = 0; j < kCarryBatch; ++j) {
-            if (j0 + j < j_hi) {
-                if (live) carry[(row0 + (size_t)(j0 + j)) * N + n] = make_double2(V, I);
-                const double Vn = mA[j] * V + mC[j] * I + a[j].x;
-                I = mD[j] * I + a[j].y;
-                V = Vn;
+            if (j_lo + j < j_hi) {
+                if (live) carry[((size_t)b * S + j_lo + j) * N + n] = make_double2(iU, iJ);
+                iU = fma(M[j].x, iU, a[j].x);
+                iJ = fma(M[j].y, iJ, a[j].y);
             }
         }
     }
 }
 
-// Re-walk from the carried no-reset state with a cheap exact bound per
-// interval: V(t) = V0 e^{-t/tm} + I0 K(t) <= max(V0, 0) + max(I0, 0)
-// K(min(dt, t_peak)) since 0 <= K(t) <= K(min(dt, t_peak)) on [0, dt].
-// Resets only lower V (each is the subtraction of a positive decaying
-// term), so a sub-block whose no-reset bound stays below the threshold holds
-// no spike whatever happened before it.  Sub-blocks whose bound reaches it
-// get a record for the resolve pass, which applies the exact interval rule.
-__device__ __forceinline__ int B_of(int total, int tgroups, int S) { return total / (tgroups * S); }
-
-__global__ __launch_bounds__(kWave * kTilesPerBlock) void k_check(
-    const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
-    const float* __restrict__ WT, int C_in, int N, int tiles, int tgroups, int S, int total, Model m,
-    const Decay* __restrict__ dec, const double2* __restrict__ carry, double2* __restrict__ ent,
-    uint32_t* __restrict__ mask, WaveInfo* __restrict__ winfo, Record* __restrict__ pool,
-    uint32_t* __restrict__ pool_count, uint32_t pool_local, uint32_t pool_cap, uint32_t* __restrict__ listed,
-    uint32_t* __restrict__ work, uint32_t* __restrict__ nwork, int32_t* __restrict__ status)
-// work: per-sample lists of the neurons with candidates (capacity N each);
-// nwork: per-sample list lengths.
+// Records of a flagged sub-block: one pool allocation for the wave, then a
+// second walk of the sub-block (its weights loaded again) storing the
+// no-reset states (V, I) of the flagged neurons.
+template <int NPL>
+__device__ __forceinline__ void record_subblock(const WalkCoords& c, const Model& m, int q, int S, int N,
+                                                const Stage& st, const double2* __restrict__ lad, double (&U0)[NPL],
+                                                double (&J0)[NPL], const bool (&f)[NPL],
+                                                const unsigned long long (&fm)[NPL], double2* __restrict__ ent,
+                                                uint32_t* __restrict__ slotmap, Record* __restrict__ pool,
+                                                uint32_t* __restrict__ pool_count, uint32_t pool_cap,
+                                                uint32_t (&msk)[NPL])
 {
-    // The segment's decays and sources are wave-uniform: they are read with
-    // scalar loads and used as scalar operands.
-    const SegCoords c = seg_coords(total, tgroups, S, ev_n, E_max, N);
-    if (c.k0 >= c.nb || c.tile >= tiles) return;
-    const float* tt = ev_t + (size_t)c.b * E_max;
-    const int lane = c.lane, n = c.n, nb = c.nb, k0 = c.k0, cnt_seg = c.cnt;
-    const float* wcol = WT + c.nc;
-    const Decay* __restrict__ sd = dec + (size_t)c.b * E_max + k0;
-    const int32_t* __restrict__ sseg = ev_src + (size_t)c.b * E_max + k0;
-    const size_t row = ((size_t)c.b * S + c.seg) * N;
-    double2 c0 = carry[row + c.nc];
-    double V = c0.x, I = c0.y;
-    uint32_t msk = 0;
-    int ncand = 0;
+    const int lane = c.lane;
     const unsigned long long below = (1ull << lane) - 1ull;
-    // Records go first to this wave's own block of pool_local slots (no
-    // atomic), then to the per-sample overflow slices (one atomic each).
-    const uint32_t wave_id = (uint32_t)(((size_t)c.b * S + c.seg) * tiles + c.tile);
-    const uint32_t local0 = wave_id * pool_local;
-    const uint32_t overflow0 = (uint32_t)((size_t)B_of(total, tgroups, S) * S * tiles * pool_local);
-    uint32_t used = 0;
-    float wn[kSub], wn2[kSub];
-    load_sub_weights_s(sseg, wcol, N, C_in, cnt_seg, 0, wn);
-    if (kSub < cnt_seg) load_sub_weights_s(sseg, wcol, N, C_in, cnt_seg, 1, wn2);
+    uint32_t total = 0;
 #pragma unroll
+    for (int i = 0; i < NPL; ++i) total += (uint32_t)__popcll(fm[i]);
+    uint32_t base = 0;
+    if (lane == 0) base = atomicAdd(&pool_count[c.b], total);
+    base = (uint32_t)__shfl((int)base, 0, kWave);
+    const bool ok = (unsigned long long)base + total <= (unsigned long long)pool_cap;
+    uint32_t slot[NPL];
+    uint32_t before = 0;
+#pragma unroll
+    for (int i = 0; i < NPL; ++i) {
+        slot[i] = ok ? (uint32_t)c.b * pool_cap + base + before + (uint32_t)__popcll(fm[i] & below) : kNoSlot;
+        before += (uint32_t)__popcll(fm[i]);
+    }
+    const size_t srow = (((size_t)c.b * S + c.seg) * kSubPerSeg + q) * N + c.n0;
+#pragma unroll
+    for (int i = 0; i < NPL; ++i) {
+        if (f[i]) {
+            slotmap[srow + i] = slot[i];
+            if (!ok) ent[srow + i] = make_double2(U0[i], J0[i]);
+            msk[i] |= 1u << q;
+        }
+    }
+    if (!ok) return;
+#pragma unroll
+    for (int i = 0; i < NPL; ++i)
+        if (f[i]) pool[slot[i]].s[0] = make_double2(v_of(m, U0[i], J0[i]), J0[i]);
+#pragma unroll
+    for (int g = 0; g < kSub / kGrp; ++g) {
+        const int e0 = q * kSub + g * kGrp;
+        float w[kGrp][NPL];
+        load_grp<NPL>(st, e0, w);
+#pragma unroll
+        for (int j = 0; j < kGrp; ++j) {
+            if (e0 + j < c.cnt) {
+                const double2 ad = lad[e0 + j];
+                step<NPL>(ad.x, ad.y, w[j], U0, J0);
+            }
+#pragma unroll
+            for (int i = 0; i < NPL; ++i)
+                if (f[i]) pool[slot[i]].s[g * kGrp + j + 1] = make_double2(v_of(m, U0[i], J0[i]), J0[i]);
+        }
+    }
+}
+
+// Screen of one group of intervals.  The coarse test bounds every interval
+// of the group at once: with X = U - J at each interval start, the largest X
+// and J over the group and the group's largest slope glk,
+//   max_j [X_j + max(J_j - th, 0) lk_j] <= max X + max(max J - th, 0) glk,
+// so a group that fails it holds no interval that passes screen_value.  The
+// (rare) groups that pass are walked again from their entering state with
+// the exact per-interval screen.  Returns the largest exact screen value
+// (-inf when the coarse test rejects the group for every lane).
+template <int NPL>
+__device__ __forceinline__ void screen_grp(const Model& m, const double2* __restrict__ lad,
+                                           const double* __restrict__ llk, double glk, int e0, int n,
+                                           const float (&w)[kGrp][NPL], double (&U)[NPL], double (&J)[NPL],
+                                           double (&z)[NPL])
+{
+    double Ug[NPL], Jg[NPL], xm[NPL], jm[NPL];
+#pragma unroll
+    for (int i = 0; i < NPL; ++i) {
+        Ug[i] = U[i];
+        Jg[i] = J[i];
+        xm[i] = -INFINITY;
+        jm[i] = -INFINITY;
+    }
+    auto track = [&](int j) {
+        const double2 ad = lad[e0 + j];
+#pragma unroll
+        for (int i = 0; i < NPL; ++i) {
+            xm[i] = fmax(xm[i], U[i] - J[i]);
+            jm[i] = fmax(jm[i], J[i]);
+        }
+        step<NPL>(ad.x, ad.y, w[j], U, J);
+    };
+    if (n >= kGrp) {
+#pragma unroll
+        for (int j = 0; j < kGrp; ++j) track(j);
+    } else {
+#pragma unroll
+        for (int j = 0; j < kGrp; ++j)
+            if (j < n) track(j);
+    }
+    bool pass = false;
+#pragma unroll
+    for (int i = 0; i < NPL; ++i) pass |= fma(fmax(jm[i] - m.th, 0.0), glk, xm[i]) >= m.thk_lo;
+    if (__ballot(pass) == 0ull) return;
+#pragma unroll
+    for (int j = 0; j < kGrp; ++j) {
+        if (j < n) {
+            const double lk = llk[e0 + j];
+            const double2 ad = lad[e0 + j];
+#pragma unroll
+            for (int i = 0; i < NPL; ++i) z[i] = fmax(z[i], screen_value(m, Ug[i], Jg[i], lk));
+            step<NPL>(ad.x, ad.y, w[j], Ug, Jg);
+        }
+    }
+}
+
+// Re-walk from the carried no-reset state with the no-crossing screen on
+// every interval: the interval before each event of the sub-block and, in
+// the sub-block holding the sample's last event, the open interval after it
+// (up to t_end).  A flagged (sub-block, neuron) gets a record of its no-reset
+// states (V, I) in the sample's pool, its slot in slotmap and a bit in the
+// neuron's sub-block mask of the segment; the first segment to flag a neuron
+// appends it to the sample's work list.  When the pool is full, the
+// sub-block's entering state (U, J) goes to ent instead (the resolve pass
+// then rebuilds its states from it).
+template <int NPL>
+__global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
+    const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
+    int E_pad, const float* __restrict__ WT, int C_in, int N, int tiles, int S, int items, Model m,
+    const Decay* __restrict__ dec, const double2* __restrict__ carry, double2* __restrict__ ent,
+    uint32_t* __restrict__ mask, uint32_t* __restrict__ slotmap, Record* __restrict__ pool,
+    uint32_t* __restrict__ pool_count, uint32_t pool_cap, uint32_t* __restrict__ listed,
+    uint32_t* __restrict__ work, uint32_t* __restrict__ nwork)
+// work: per-sample lists of the neurons with flagged sub-blocks (capacity N
+// each); nwork: per-sample list lengths.
+{
+    __shared__ double2 s_ad[kWalkWaves][kSeg];
+    __shared__ double s_lk[kWalkWaves][kSeg];
+    __shared__ double s_gk[kWalkWaves][kGrpPerSeg];
+    WalkCoords c;
+    if (!walk_coords<NPL>(items, tiles, S, ev_n, E_max, N, c)) return;
+    const int lane = c.lane;
+    const int wv = threadIdx.x / kWave;
+    double2* lad = s_ad[wv];
+    double* llk = s_lk[wv];
+    double* lgk = s_gk[wv];
+    const Stage st = stage_segment(c, ev_src + (size_t)c.b * E_max + c.k0, dec + (size_t)c.b * E_pad + c.k0, WT,
+                                   C_in, N, lad, llk, lgk);
+    const size_t row = ((size_t)c.b * S + c.seg) * N + c.n0;
+    const unsigned long long below = (1ull << lane) - 1ull;
+    double U[NPL], J[NPL];
+#pragma unroll
+    for (int i = 0; i < NPL; ++i) {
+        const double2 s0 = carry[row + i];
+        U[i] = s0.x;
+        J[i] = s0.y;
+    }
+    uint32_t msk[NPL];
+#pragma unroll
+    for (int i = 0; i < NPL; ++i) msk[i] = 0u;
+    // The open interval after the sample's last event, up to t_end.
+    const bool last_seg = c.k0 + c.cnt == c.nb;
+    const double open_lk = last_seg ? (m.t_end - (double)ev_t[(size_t)c.b * E_max + c.nb - 1]) * m.inv_ktm : 0.0;
+    // Two weight buffers in alternation: wa holds the first and wb the second
+    // group of each sub-block.
+    float wa[kGrp][NPL], wb[kGrp][NPL];
+    load_grp<NPL>(st, 0, wa);
     for (int q = 0; q < kSubPerSeg; ++q) {
-        if (q * kSub < cnt_seg) {
-            const int cnt = min(kSub, cnt_seg - q * kSub);
-            float w[kSub];
+        const int q0 = q * kSub;
+        if (q0 >= c.cnt) break;
+        double U0[NPL], J0[NPL], z[NPL];
 #pragma unroll
-            for (int j = 0; j < kSub; ++j) { w[j] = wn[j]; wn[j] = wn2[j]; }
-            if (q + 2 < kSubPerSeg && (q + 2) * kSub < cnt_seg)
-                load_sub_weights_s(sseg, wcol, N, C_in, cnt_seg, q + 2, wn2);
-            double Vin = V, Iin = I, ub = -INFINITY;
-            if (cnt == kSub) {                         // full sub-block: straight-line code
+        for (int i = 0; i < NPL; ++i) {
+            U0[i] = U[i];
+            J0[i] = J[i];
+            z[i] = -INFINITY;
+        }
+        load_grp<NPL>(st, q0 + kGrp, wb);
+        screen_grp<NPL>(m, lad, llk, lgk[2 * q], q0, c.cnt - q0, wa, U, J, z);
+        if (q0 + kGrp < c.cnt) {
+            load_grp<NPL>(st, q0 + kSub, wa);
+            screen_grp<NPL>(m, lad, llk, lgk[2 * q + 1], q0 + kGrp, c.cnt - q0 - kGrp, wb, U, J, z);
+        }
+        if (last_seg && q0 + kSub >= c.cnt && open_lk > 0.0) {
 #pragma unroll
-                for (int j = 0; j < kSub; ++j) {
-                    Decay e = sd[q * kSub + j];
-                    ub = fmax(ub, fmax(V, 0.0) + fmax(I, 0.0) * e.g);
-                    double Vn = e.A * V + e.C * I;
-                    I = e.D * I + (double)w[j];
-                    V = Vn;
-                }
-            } else {
-                for (int j = 0; j < cnt; ++j) {
-                    Decay e = sd[q * kSub + j];
-                    ub = fmax(ub, fmax(V, 0.0) + fmax(I, 0.0) * e.g);
-                    double Vn = e.A * V + e.C * I;
-                    I = e.D * I + (double)w[j];
-                    V = Vn;
-                }
-            }
-            if (k0 + q * kSub + cnt == nb) {
-                // Interval after the last event, up to t_end (default +inf).
-                double len = m.t_end - (double)tt[nb - 1];
-                if (len > 0.0) {
-                    double gl = fmin(len, m.t_peak);
-                    double g = unit_kernel(m, gl, exp(-gl * m.inv_tm)) * (1.0 + 1e-12);
-                    ub = fmax(ub, fmax(V, 0.0) + fmax(I, 0.0) * g);
-                }
-            }
-            bool surv = ub >= m.th_lo && n < N;
-            unsigned long long lanes = __ballot(surv);
-            if (lanes) {
-                const uint32_t cntl = (uint32_t)__popcll(lanes);
-                uint32_t base;
-                bool ok;
-                if (used + cntl <= pool_local) {
-                    base = local0 + used;
-                    used += cntl;
-                    ok = true;
-                } else {
-                    // Overflow records of sample b live in their own slice, so
-                    // the allocation atomics of different samples do not contend.
-                    uint32_t ob = 0;
-                    if (lane == 0) ob = atomicAdd(&pool_count[c.b], cntl);
-                    ob = __shfl(ob, 0, kWave);
-                    ok = (unsigned long long)ob + cntl <= (unsigned long long)pool_cap;
-                    base = overflow0 + (uint32_t)c.b * pool_cap + ob;
-                }
-                if (lane == 0) {
-                    WaveInfo wi;
-                    wi.lanes = lanes;
-                    wi.base = ok ? base : kNoSlot;
-                    wi.pad = 0;
-                    winfo[(((size_t)c.b * S + c.seg) * tiles + c.tile) * kSubPerSeg + q] = wi;
-                }
-                if (surv) {
-                    // The entering state always; the full record if the pool
-                    // had room (otherwise the resolve pass rebuilds the
-                    // sub-block's states from the entering state).
-                    ent[(((size_t)c.b * S + c.seg) * kSubPerSeg + q) * N + n] = make_double2(Vin, Iin);
-                    if (ok) {
-                        // Re-walk the sub-block to store its states.
-                        uint32_t slot = base + (uint32_t)__popcll(lanes & below);
-                        Record* r = pool + slot;
-                        r->s[0] = make_double2(Vin, Iin);
-                        double Vr = Vin, Ir = Iin;
+            for (int i = 0; i < NPL; ++i)
+                z[i] = fmax(z[i], J[i] > m.th ? fma(J[i] - m.th, open_lk, U[i] - J[i]) : U[i] - J[i]);
+        }
+        bool f[NPL];
+        unsigned long long fm[NPL];
+        unsigned long long any = 0ull;
 #pragma unroll
-                        for (int j = 0; j < kSub; ++j) {
-                            if (j < cnt) {
-                                Decay e = sd[q * kSub + j];
-                                double Vn = e.A * Vr + e.C * Ir;
-                                Ir = e.D * Ir + (double)w[j];
-                                Vr = Vn;
-                            }
-                            r->s[j + 1] = make_double2(Vr, Ir);
-                        }
-                    }
-                    msk |= 1u << q;
-                    ++ncand;
-                }
+        for (int i = 0; i < NPL; ++i) {
+            f[i] = c.live && z[i] >= m.thk_lo;
+            fm[i] = __ballot(f[i]);
+            any |= fm[i];
+        }
+        if (any) record_subblock<NPL>(c, m, q, S, N, st, lad, U0, J0, f, fm, ent, slotmap, pool, pool_count,
+                                      pool_cap, msk);
+    }
+    if (c.live) {
+#pragma unroll
+        for (int i = 0; i < NPL; ++i) mask[row + i] = msk[i];
+    }
+    // Work list of the sample: the first segment to flag a neuron appends it
+    // (one OR per flagged neuron, one counter update per wave).
+    bool want[NPL], first[NPL];
+    unsigned long long wm = 0ull;
+#pragma unroll
+    for (int i = 0; i < NPL; ++i) {
+        want[i] = c.live && msk[i] != 0u;
+        wm |= __ballot(want[i]);
+    }
+    if (wm) {
+        unsigned long long fmk[NPL];
+        uint32_t tot = 0;
+#pragma unroll
+        for (int i = 0; i < NPL; ++i) {
+            first[i] = false;
+            if (want[i]) first[i] = atomicOr(&listed[(size_t)c.b * N + c.n0 + i], 1u) == 0u;
+            fmk[i] = __ballot(first[i]);
+            tot += (uint32_t)__popcll(fmk[i]);
+        }
+        if (tot) {
+            uint32_t wbase = 0;
+            if (lane == 0) wbase = atomicAdd(&nwork[c.b], tot);
+            wbase = (uint32_t)__shfl((int)wbase, 0, kWave);
+            uint32_t before = 0;
+#pragma unroll
+            for (int i = 0; i < NPL; ++i) {
+                if (first[i])
+                    work[(size_t)c.b * N + wbase + before + (uint32_t)__popcll(fmk[i] & below)] =
+                        (uint32_t)((size_t)c.b * N + c.n0 + i);
+                before += (uint32_t)__popcll(fmk[i]);
             }
         }
     }
-    if (n < N) mask[row + n] = msk;
-    const bool want = ncand > 0 && n < N;
-    if (__ballot(want)) {
-        // Work list of sample b: the first segment to flag a neuron appends
-        // it (one OR per flagged lane, then one counter update per wave).
-        const size_t bn = (size_t)c.b * N + c.nc;
-        const uint32_t old = atomicOr(&listed[bn], want ? 1u : 0u);
-        const bool first = want && old == 0u;
-        const unsigned long long fm = __ballot(first);
-        if (fm) {
-            uint32_t wbase = 0;
-            if (lane == 0) wbase = atomicAdd(&nwork[c.b], (uint32_t)__popcll(fm));
-            wbase = __shfl(wbase, 0, kWave);
-            if (first) work[(size_t)c.b * N + wbase + (uint32_t)__popcll(fm & below)] = (uint32_t)bn;
-        }
-    }}
-
+}
 // ---------------------------------------------------------------------------
 // Resolve pass: one wave per neuron that has flagged sub-blocks (a work list
 // built by the check pass).  Intervals outside flagged sub-blocks provably
@@ -560,78 +689,22 @@ struct ResolveLds {
     uint32_t cand[kCandCap];                     // (segment in chunk << 3) | sub-block
 };
 
-// Rebuild a sub-block's entering no-reset state from its segment carry by
-// walking the earlier events of the segment (used only when the record pool
-// was full).
-__device__ __noinline__ double2 entering_state(const double2* __restrict__ carry, size_t row, int n, int k0, int kq0,
-                                               const int32_t* __restrict__ src, const Decay* __restrict__ d,
-                                               const float* __restrict__ WT, int C_in, int N)
+// No-reset state (V, I) after the events [k0, kq0) of a segment, from its
+// carry (used only for the open interval when the record pool was full):
+// the check pass's walk, operation for operation.
+__device__ __noinline__ double2 entering_state(const Model& m, const double2* __restrict__ carry, size_t row, int n,
+                                               int k0, int kq0, const int32_t* __restrict__ src,
+                                               const Decay* __restrict__ d, const float* __restrict__ WT, int C_in,
+                                               int N)
 {
-    double2 c = carry[row + n];
-    double V = c.x, I = c.y;
+    const double2 c = carry[row + n];            // (U, J) eigen-coordinates
+    double U = c.x, J = c.y;
     for (int k = k0; k < kq0; ++k) {
-        Decay e = d[k];
-        double Vn = e.A * V + e.C * I;
-        I = e.D * I + (double)WT[(size_t)clamp_src(src[k], C_in) * (size_t)N + n];
-        V = Vn;
+        const double w = (double)WT[(size_t)clamp_src(src[k], C_in) * (size_t)N + n];
+        U = fma(d[k].A, U, w);
+        J = fma(d[k].D, J, w);
     }
-    return make_double2(V, I);
-}
-
-// Lane shift by n within rows of 16 lanes (DPP row_shr): lanes whose
-// source lies outside the row keep `old`.
-template <int n>
-__device__ __forceinline__ double row_shr(double v, double old)
-{
-    static_assert(n >= 1 && n <= 15, "row shift");
-    const unsigned long long u = (unsigned long long)__double_as_longlong(v);
-    const unsigned long long o = (unsigned long long)__double_as_longlong(old);
-    const int lo = __builtin_amdgcn_update_dpp((int)(unsigned)o, (int)(unsigned)u, 0x110 + n, 0xf, 0xf, false);
-    const int hi = __builtin_amdgcn_update_dpp((int)(unsigned)(o >> 32), (int)(unsigned)(u >> 32), 0x110 + n, 0xf,
-                                               0xf, false);
-    return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
-}
-
-// Affine map s -> (A V + C I + bV, D I + bI) of a run of events.
-struct Map {
-    double A, C, D, bV, bI;
-};
-
-// `late` applied after `early`.
-__device__ __forceinline__ Map compose(const Map& late, const Map& early)
-{
-    Map r;
-    r.A = late.A * early.A;
-    r.C = late.A * early.C + late.C * early.D;
-    r.D = late.D * early.D;
-    r.bV = late.A * early.bV + late.C * early.bI + late.bV;
-    r.bI = late.D * early.bI + late.bI;
-    return r;
-}
-
-template <int n>
-__device__ __forceinline__ Map row_shr_map(const Map& m)
-{
-    return Map{row_shr<n>(m.A, 1.0), row_shr<n>(m.C, 0.0), row_shr<n>(m.D, 1.0), row_shr<n>(m.bV, 0.0),
-               row_shr<n>(m.bI, 0.0)};
-}
-
-// No-reset states of a sub-block whose record was not stored (pool full):
-// lane j of each row of 16 lanes holds event j's map (Eq. affine: decay
-// then jump), an inclusive scan over the row (Hillis-Steele with DPP row
-// shifts; all 64 lanes take part) composes the maps of events 0..j, and the
-// sub-block's entering state s0 gives the state after event j.  Lane j
-// returns the state entering interval j (after event j - 1) and V at its end.
-__device__ __forceinline__ double3 scan_interval(double2 s0, double A, double C, double D, double w)
-{
-    Map m{A, C, D, 0.0, w};
-    m = compose(m, row_shr_map<1>(m));
-    m = compose(m, row_shr_map<2>(m));
-    m = compose(m, row_shr_map<4>(m));
-    m = compose(m, row_shr_map<8>(m));
-    const double Va = m.A * s0.x + m.C * s0.y + m.bV;     // after event j
-    const double Ia = m.D * s0.y + m.bI;
-    return make_double3(row_shr<1>(Va, s0.x), row_shr<1>(Ia, s0.y), Va);
+    return make_double2(v_of(m, U, J), J);
 }
 
 __device__ __forceinline__ int rl_int(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
@@ -696,7 +769,7 @@ __device__ __forceinline__ IvRaw load_slice(int cw, int nwin, const WinLane& w, 
     return v;
 }
 
-__device__ __forceinline__ Iv finish_slice(const IvRaw& r, int b, int n, int S, int N, int C_in,
+__device__ __forceinline__ Iv finish_slice(const Model& m, const IvRaw& r, int b, int n, int S, int N, int C_in,
                                            const int32_t* __restrict__ src, const Decay* __restrict__ d,
                                            const float* __restrict__ WT, const double2* __restrict__ ent)
 {
@@ -710,16 +783,25 @@ __device__ __forceinline__ Iv finish_slice(const IvRaw& r, int b, int n, int S, 
     v.I0 = r.s0.y;
     v.V1 = r.v1;
     if (__ballot(r.rowfb)) {
-        // No record: rebuild the row's states from its entering state (every
-        // lane takes part in the row scan; past cnt the maps are identities).
+        // No record: rebuild the states from the sub-block's entering state
+        // (U, J).  Lane j walks events 0 .. j of its sub-block with the same
+        // float64 operations, in the same order, as the check pass's record
+        // walk, so the rebuilt states equal the recorded ones bit for bit.
         const int q = (r.kq0 % kSeg) / kSub;
         const double2 s0 = r.rowfb ? ent[(((size_t)b * S + r.seg) * kSubPerSeg + q) * N + n] : make_double2(0.0, 0.0);
-        const bool in = r.j < r.cnt;
-        const int k = r.kq0 + min(r.j, max(r.cnt - 1, 0));
-        const Decay e = d[k];
-        const double w = in ? (double)WT[(size_t)clamp_src(src[k], C_in) * (size_t)N + n] : 0.0;
-        const double3 sc = scan_interval(s0, in ? e.A : 1.0, in ? e.C : 0.0, in ? e.D : 1.0, w);
-        if (r.fb) { v.V0 = sc.x; v.I0 = sc.y; v.V1 = sc.z; }
+        double U = s0.x, J = s0.y, V0 = 0.0, I0 = 0.0;
+        for (int e = 0; e < kSub; ++e) {
+            if (e == r.j) { V0 = v_of(m, U, J); I0 = J; }
+            const int k = r.kq0 + min(e, max(r.cnt - 1, 0));
+            const bool step_in = e <= r.j && e < r.cnt;
+            const double w = step_in ? (double)WT[(size_t)clamp_src(src[k], C_in) * (size_t)N + n] : 0.0;
+            const Decay dk = d[k];
+            if (step_in) {
+                U = fma(dk.A, U, w);
+                J = fma(dk.D, J, w);
+            }
+        }
+        if (r.fb) { v.V0 = V0; v.I0 = I0; v.V1 = v_of(m, U, J); }
     }
     return v;
 }
@@ -774,21 +856,19 @@ struct ResolveStats {
 
 __device__ void resolve_neuron(ResolveLds& sh, ResolveStats& acc, int b, int n, const float* __restrict__ ev_t,
                                const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
-                               const float* __restrict__ WT, int C_in, int N, int tiles, int S, const Model& m,
+                               const float* __restrict__ WT, int C_in, int N, int E_pad, int S, const Model& m,
                                const Decay* __restrict__ dec, const double2* __restrict__ carry,
                                const double2* __restrict__ ent,
-                               const uint32_t* __restrict__ mask, const WaveInfo* __restrict__ winfo,
+                               const uint32_t* __restrict__ mask, const uint32_t* __restrict__ slotmap,
                                const Record* __restrict__ pool, float* __restrict__ out_t, int32_t* __restrict__ out_n,
                                float* __restrict__ out_i)
 {
-    const int tile = n / kWave;
-    const unsigned long long below_n = (1ull << (n % kWave)) - 1ull;
     const int lane = (int)threadIdx.x;
     const int j = lane % kSub, r = lane / kSub;
     const int nb = clamp_count(ev_n[b], E_max);
     const float* tt = ev_t + (size_t)b * E_max;
     const int32_t* src = ev_src + (size_t)b * E_max;
-    const Decay* d = dec + (size_t)b * E_max;
+    const Decay* d = dec + (size_t)b * E_pad;
     const size_t idx = (size_t)b * N + n;
     float* st = out_t + idx * (size_t)m.s_max;
     float* si = out_i ? out_i + idx * (size_t)m.s_max : nullptr;
@@ -834,8 +914,7 @@ __device__ void resolve_neuron(ResolveLds& sh, ResolveStats& acc, int b, int n, 
                 int q = (int)(cw & 7u);
                 w.kq0 = w.seg * kSeg + q * kSub;
                 w.cnt = min(kSub, nb - w.kq0);
-                WaveInfo wi = winfo[(((size_t)b * S + w.seg) * tiles + tile) * kSubPerSeg + q];
-                if (wi.base != kNoSlot) w.slot = wi.base + (uint32_t)__popcll(wi.lanes & below_n);
+                w.slot = slotmap[(((size_t)b * S + w.seg) * kSubPerSeg + q) * N + n];
                 last = w.kq0 + w.cnt == nb;
             }
             fallback += __popcll(__ballot(lane < nwin && w.slot == kNoSlot));
@@ -866,7 +945,7 @@ __device__ void resolve_neuron(ResolveLds& sh, ResolveStats& acc, int b, int n, 
                 }
                 Iv v[kSlices];
 #pragma unroll
-                for (int i = 0; i < kSlices; ++i) v[i] = finish_slice(raw[i], b, n, S, N, C_in, src, d, WT, ent);
+                for (int i = 0; i < kSlices; ++i) v[i] = finish_slice(m, raw[i], b, n, S, N, C_in, src, d, WT, ent);
                 // ---- slices in time order: screen in float32 with the current
                 // deficit, then the deficit and the maximum in float64 where
                 // an interval may cross, then rounds
@@ -930,7 +1009,7 @@ __device__ void resolve_neuron(ResolveLds& sh, ResolveStats& acc, int b, int n, 
     if (!capped && last_seen && m.t_end > t_last && lane == 0) {
         double2 s0 = last_slot != kNoSlot
                          ? pool[last_slot].s[last_cnt]
-                         : entering_state(carry, ((size_t)b * S + last_seg) * N, n, last_seg * kSeg, nb, src, d, WT,
+                         : entering_state(m, carry, ((size_t)b * S + last_seg) * N, n, last_seg * kSeg, nb, src, d, WT,
                                           C_in, N);
         const double V0 = s0.x, I0 = s0.y, L = m.t_end - t_last;
         double A = 0.0, Dd = 0.0, V1 = 0.0;
@@ -971,12 +1050,12 @@ __device__ void resolve_neuron(ResolveLds& sh, ResolveStats& acc, int b, int n, 
 // counts are added once per workgroup.
 __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src,
                                                    const int32_t* __restrict__ ev_n, int B, int E_max,
-                                                   const float* __restrict__ WT, int C_in, int N, int tiles, int S,
+                                                   const float* __restrict__ WT, int C_in, int N, int E_pad, int S,
                                                    Model m, const Decay* __restrict__ dec,
                                                    const double2* __restrict__ carry,
                                                    const double2* __restrict__ ent,
                                                    const uint32_t* __restrict__ mask,
-                                                   const WaveInfo* __restrict__ winfo,
+                                                   const uint32_t* __restrict__ slotmap,
                                                    const Record* __restrict__ pool,
                                                    const uint32_t* __restrict__ work, const uint32_t* __restrict__ nwork,
                                                    float* __restrict__ out_t, int32_t* __restrict__ out_n,
@@ -1016,7 +1095,7 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
         const uint32_t before = l > 0 ? (uint32_t)__shfl((int)incl, l - 1, kWave) : base;
         const uint32_t bn = work[(size_t)b * N + (w - before)];
         resolve_neuron(sh, acc, (int)(bn / (uint32_t)N), (int)(bn % (uint32_t)N), ev_t, ev_src, ev_n, E_max, WT,
-                       C_in, N, tiles, S, m, dec, carry, ent, mask, winfo, pool, out_t, out_n, out_i);
+                       C_in, N, E_pad, S, m, dec, carry, ent, mask, slotmap, pool, out_t, out_n, out_i);
     }
     if (threadIdx.x == 0) {
         if (acc.walked) {
@@ -1043,7 +1122,7 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
 __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src,
                                                    const int32_t* __restrict__ ev_n, int B, int E_max,
                                                    const float* __restrict__ WT, int C_in, int N, Model m,
-                                                   const Decay* __restrict__ dec, float* __restrict__ out_t,
+                                                   int E_pad, const Decay* __restrict__ dec, float* __restrict__ out_t,
                                                    int32_t* __restrict__ out_n, float* __restrict__ out_i,
                                                    int32_t* __restrict__ status)
 {
@@ -1055,17 +1134,17 @@ __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_
     if (live && n == 0) atomicAdd(&status[LIF_ST_EVENTS], nb);
     const float* tt = ev_t + (size_t)b * E_max;
     const int32_t* src = ev_src + (size_t)b * E_max;
-    const Decay* d = dec + (size_t)b * E_max;
+    const Decay* d = dec + (size_t)b * E_pad;
     float* st = out_t + idx * (size_t)m.s_max;
     float* si = out_i ? out_i + idx * (size_t)m.s_max : nullptr;
     int ns = 0;
     bool capped = false;
     double V = 0.0, I = 0.0, t_prev = 0.0;
     for (int k = 0; k <= nb && !capped; ++k) {
-        double L, A, C, Dd, gb;
+        double L, A, C, Dd;
         if (k < nb) {
             Decay e = d[k];
-            A = e.A; C = e.C; Dd = e.D; gb = e.g;
+            A = e.A; C = e.C; Dd = e.D;
             L = (double)tt[k] - t_prev;
         } else {
             L = m.t_end - t_prev;                      // open interval after the last event
@@ -1077,11 +1156,10 @@ __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_
                 Dd = exp(-L * m.inv_ts);
                 C = unit_kernel(m, L, A);
             }
-            double gl = fmin(L, m.t_peak);
-            gb = unit_kernel(m, gl, exp(-gl * m.inv_tm)) * (1.0 + 1e-12);
         }
         double V1 = A * V + C * I;
-        if (L > 0.0 && fmax(V, 0.0) + fmax(I, 0.0) * gb >= m.th_lo) {
+        // no-crossing screen V0 + max(I0 - th, 0) L / tm >= th_lo (screen_value)
+        if (L > 0.0 && V + (I > m.th ? (I - m.th) * (L * m.inv_tm) : 0.0) >= m.th_lo) {
             IntervalMax im = interval_max(m, V, I, V1, L, A, Dd);
             double Dk = 0.0, lo = 0.0, Flo = V - m.th;
             const double kI = m.kappa * I;
@@ -1139,39 +1217,75 @@ FwdLayout fwd_layout(int B, int E_max, int N)
 {
     FwdLayout L{};
     L.S = (E_max + kSeg - 1) / kSeg;
+    L.E_pad = L.S * kSeg;
     size_t off = 0;
     auto take = [&](size_t bytes) { size_t o = off; off += (bytes + 255) & ~(size_t)255; return o; };
-    L.dec = take((size_t)B * E_max * sizeof(Decay));
-    L.segm = take((size_t)B * L.S * sizeof(Decay));
-    L.agg = take((size_t)B * L.S * N * sizeof(double2));
-    L.carry = take((size_t)B * L.S * N * sizeof(double2));
-    L.mask = take((size_t)B * L.S * N * sizeof(uint32_t));
-    L.ent = take((size_t)B * L.S * kSubPerSeg * N * sizeof(double2));
-    int tiles = (N + kWave - 1) / kWave;
-    L.winfo = take((size_t)B * L.S * tiles * kSubPerSeg * sizeof(WaveInfo));
-    L.counters = take(2 * (size_t)B * sizeof(uint32_t));   // per sample: pool use, work-list length
+    const size_t BS = (size_t)B * L.S;
+    L.dec = take((size_t)B * L.E_pad * sizeof(Decay));
+    L.segm = take(BS * sizeof(double2));
+    L.agg = take(BS * N * sizeof(double2));
+    L.carry = take(BS * N * sizeof(double2));
+    L.mask = take(BS * N * sizeof(uint32_t));
+    L.slotmap = take(BS * kSubPerSeg * N * sizeof(uint32_t));
+    L.ent = take(BS * kSubPerSeg * N * sizeof(double2));
+    // per sample: record-pool use, work-list length
+    L.n_counters = 2 * (size_t)B;
+    L.counters = take(L.n_counters * sizeof(uint32_t));
     L.listed = take((size_t)B * N * sizeof(uint32_t));
     L.work = take((size_t)B * N * sizeof(uint32_t));
-    // Record pool: one record per flagged (sub-block, neuron).  Each check
-    // wave (sample, segment, tile) owns kPoolLocal slots; the overflow is
-    // shared per sample and sized at a 64th of the dense bound (far above
-    // what spiking activity needs).  A full pool only sends the excess
-    // sub-blocks through a slower re-walk.  LIF_POOL_LOCAL / LIF_POOL_CAP
-    // override the two sizes (used by tests of the re-walk path).
-    size_t local = kPoolLocal;
-    if (const char* env = getenv("LIF_POOL_LOCAL")) local = (size_t)strtoull(env, nullptr, 10);
-    size_t waves = (size_t)B * L.S * tiles;
-    size_t dense = waves * kSubPerSeg * kWave;
-    size_t cap = dense / 64 > 65536 ? dense / 64 : (dense < 65536 ? dense : 65536);
+    // Record pool: one record per flagged (sub-block, neuron), in per-sample
+    // slices sized at a 16th of the dense bound (every sub-block of every
+    // neuron flagged), at least 4096 records (or the dense bound when
+    // smaller).  A full slice only sends the excess sub-blocks through a
+    // slower re-walk.  LIF_POOL_CAP overrides the slice size (tests of the
+    // re-walk path).
+    const size_t dense = (size_t)L.S * kSubPerSeg * N;
+    size_t cap = dense / 16 > 4096 ? dense / 16 : (dense < 4096 ? dense : 4096);
     if (const char* env = getenv("LIF_POOL_CAP")) cap = (size_t)strtoull(env, nullptr, 10);
-    if (local > 64) local = 64;
-    if (waves * local + cap > 0xfffffff0ull) cap = 0xfffffff0ull - waves * local;   // slot indices are 32-bit
-    L.pool_local = local;
+    if (B > 0 && (size_t)B * cap > 0xfffffff0ull) cap = 0xfffffff0ull / (size_t)B;   // slot indices are 32-bit
     L.pool_cap = cap;
-    size_t recs = waves * local + cap;
+    const size_t recs = (size_t)B * cap;
     L.pool = take((recs > 0 ? recs : 1) * sizeof(Record));   // at least one record (a safe load address)
     L.total = off + 256;
     return L;
+}
+
+// Neurons per lane of the segment walks: NPL-wide weight loads need W^T rows
+// of a multiple of NPL floats and an aligned base.  LIF_NPL (1, 2 or 4)
+// restricts the choice.
+static int pick_npl(const float* WT, int N)
+{
+    int lim = 4;
+    if (const char* env = getenv("LIF_NPL")) lim = atoi(env);
+    const uintptr_t a = (uintptr_t)WT;
+    if (lim >= 4 && N % 4 == 0 && a % 16 == 0) return 4;
+    if (lim >= 2 && N % 2 == 0 && a % 8 == 0) return 2;
+    return 1;
+}
+
+struct FwdPtrs {
+    Decay* dec;
+    double2 *segm, *agg, *carry, *ent;
+    uint32_t *mask, *slotmap, *counters, *pool_count, *nwork, *listed, *work;
+    Record* pool;
+};
+
+template <int NPL>
+static void launch_walks(const FwdLayout& L, const FwdPtrs& P, const float* ev_t, const int32_t* ev_src,
+                         const int32_t* ev_n, int B, int E_max, const float* WT, int C_in, int N, const Model& m,
+                         int32_t* status, hipStream_t stream)
+{
+    const int tiles = (N + kWave * NPL - 1) / (kWave * NPL);
+    const size_t items = (size_t)B * L.S * tiles;
+    const unsigned blocks = (unsigned)((items + kWalkWaves - 1) / kWalkWaves);
+    TIMED_LAUNCH("aggregate", k_aggregate<NPL>, dim3(blocks), dim3(kWave * kWalkWaves), 0, stream,
+                 ev_src, ev_n, E_max, L.E_pad, WT, C_in, N, tiles, L.S, (int)items, P.dec, P.agg);
+    const int ctiles = (N + kWave - 1) / kWave;
+    TIMED_LAUNCH("carry", k_carry, dim3((unsigned)((size_t)B * ctiles)), dim3(kWave * kCarryWaves), 0, stream,
+                 ev_n, B, E_max, N, ctiles, L.S, P.segm, P.agg, P.carry, status);
+    TIMED_LAUNCH("check", k_check<NPL>, dim3(blocks), dim3(kWave * kWalkWaves), 0, stream,
+                 ev_t, ev_src, ev_n, E_max, L.E_pad, WT, C_in, N, tiles, L.S, (int)items, m, P.dec, P.carry, P.ent,
+                 P.mask, P.slotmap, P.pool, P.pool_count, (uint32_t)L.pool_cap, P.listed, P.work, P.nwork);
 }
 
 int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
@@ -1184,61 +1298,56 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     if (ws_bytes < L.total) return LIF_ERR_WORKSPACE;
     Model m = make_model(*p);
     char* base = (char*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
-    Decay* dec = (Decay*)(base + L.dec);
-    Decay* segm = (Decay*)(base + L.segm);
-    double2* agg = (double2*)(base + L.agg);
-    double2* carry = (double2*)(base + L.carry);
-    double2* ent = (double2*)(base + L.ent);
-    uint32_t* mask = (uint32_t*)(base + L.mask);
-    WaveInfo* winfo = (WaveInfo*)(base + L.winfo);
-    uint32_t* counters = (uint32_t*)(base + L.counters);
-    uint32_t* pool_count = counters;
-    uint32_t* nwork = counters + B;
-    uint32_t* listed = (uint32_t*)(base + L.listed);
-    uint32_t* work = (uint32_t*)(base + L.work);
-    Record* pool = (Record*)(base + L.pool);
+    FwdPtrs P;
+    P.dec = (Decay*)(base + L.dec);
+    P.segm = (double2*)(base + L.segm);
+    P.agg = (double2*)(base + L.agg);
+    P.carry = (double2*)(base + L.carry);
+    P.ent = (double2*)(base + L.ent);
+    P.mask = (uint32_t*)(base + L.mask);
+    P.slotmap = (uint32_t*)(base + L.slotmap);
+    P.counters = (uint32_t*)(base + L.counters);
+    P.pool_count = P.counters;
+    P.nwork = P.counters + B;
+    P.listed = (uint32_t*)(base + L.listed);
+    P.work = (uint32_t*)(base + L.work);
+    P.pool = (Record*)(base + L.pool);
 
-    size_t nev = (size_t)B * E_max;
-    size_t nn = (size_t)B * N;
-    int tiles = (N + kWave - 1) / kWave;
-    int tgroups = (tiles + kTilesPerBlock - 1) / kTilesPerBlock;
-    size_t total = (size_t)B * L.S * tgroups;
-    if (total > 0x7fffffff || nn > 0xffffffffull) return LIF_ERR_SIZE;
-    if (sequential || total == 0) {
-        size_t blocks = ((nev > nn * (size_t)p->s_max ? nev : nn * (size_t)p->s_max) + 255) / 256;
+    const size_t nev = (size_t)B * L.E_pad;
+    const size_t nn = (size_t)B * N;
+    const size_t items_max = (size_t)B * L.S * ((N + kWave - 1) / kWave);
+    if (items_max > 0x7fffffff || nn > 0xffffffffull) return LIF_ERR_SIZE;
+    {
+        const size_t n_out = nn * (size_t)p->s_max;
+        size_t work_items = nev > n_out ? nev : n_out;
+        size_t blocks = (work_items + 255) / 256;
         if (blocks > 2048) blocks = 2048;
         if (blocks < 1) blocks = 1;
-        TIMED_LAUNCH("decay", k_decay, dim3((unsigned)blocks), dim3(256), 0, stream,
-                     ev_t, ev_n, B, E_max, L.S, m, dec, status, counters, sequential ? nullptr : out_t, out_i,
-                     nn * (size_t)p->s_max);
-    } else {
-        TIMED_LAUNCH("aggregate", k_aggregate, dim3((unsigned)total), dim3(kWave * kTilesPerBlock), 0, stream,
-                     ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, tgroups, L.S, (int)total, m, dec, segm, agg,
-                     status, counters, out_t, out_i, nn * (size_t)p->s_max);
+        TIMED_LAUNCH("prep", k_prep, dim3((unsigned)blocks), dim3(256), 0, stream,
+                     ev_t, ev_n, B, E_max, L.E_pad, L.S, m, P.dec, sequential ? nullptr : P.segm, status, P.counters,
+                     L.n_counters, out_n, sequential ? nullptr : P.listed, nn, sequential ? nullptr : out_t, out_i,
+                     n_out);
     }
-    if ((p->flags & LIF_VALIDATE) && nev)
-        TIMED_LAUNCH("validate", k_validate, dim3((unsigned)((nev + 255) / 256)), dim3(256), 0, stream,
-                     ev_t, ev_src, ev_n, B, E_max, C_in, status);
+    if ((p->flags & LIF_VALIDATE) && (size_t)B * E_max)
+        TIMED_LAUNCH("validate", k_validate, dim3((unsigned)(((size_t)B * E_max + 255) / 256)), dim3(256), 0,
+                     stream, ev_t, ev_src, ev_n, B, E_max, C_in, status);
     if (sequential) {
-        TIMED_LAUNCH("sequential", k_sequential, dim3((unsigned)((nn + 63) / 64)), dim3(64), 0, stream,
-                     ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, dec, out_t, out_n, out_i, status);
+        if (nn)
+            TIMED_LAUNCH("sequential", k_sequential, dim3((unsigned)((nn + 63) / 64)), dim3(64), 0, stream,
+                         ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, L.E_pad, P.dec, out_t, out_n, out_i, status);
         return check_launch();
     }
-    if (nn)
-        TIMED_LAUNCH("carry", k_carry, dim3((unsigned)((size_t)B * tiles)), dim3(kWave * kCarryWaves), 0, stream,
-                     ev_n, B, E_max, N, tiles, L.S, segm, agg, carry, status, out_n, listed, counters);
-    if (total) {
-        TIMED_LAUNCH("check", k_check, dim3((unsigned)total), dim3(kWave * kTilesPerBlock), 0, stream,
-                     ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, tgroups, L.S, (int)total, m, dec, carry, ent, mask,
-                     winfo, pool, pool_count, (uint32_t)L.pool_local, (uint32_t)(L.pool_cap / (B > 0 ? B : 1)),
-                     listed, work, nwork,
-                     status);
-        // Single-wave workgroups over the concatenated per-sample lists.
-        const unsigned rgrid = (unsigned)(nn < 4096 ? nn : 4096);
-        TIMED_LAUNCH("resolve", k_resolve, dim3(rgrid), dim3(kWave), 0, stream,
-                     ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, tiles, L.S, m, dec, carry, ent, mask, winfo, pool,
-                     work, nwork, out_t, out_n, out_i, status);
+    if (items_max == 0) return check_launch();
+    switch (pick_npl(WT, N)) {
+    case 4: launch_walks<4>(L, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, status, stream); break;
+    case 2: launch_walks<2>(L, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, status, stream); break;
+    default: launch_walks<1>(L, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, status, stream); break;
     }
+    // Single-wave workgroups over the concatenated per-sample lists.
+    const unsigned rgrid = (unsigned)(nn < 4096 ? nn : 4096);
+    TIMED_LAUNCH("resolve", k_resolve, dim3(rgrid), dim3(kWave), 0, stream,
+                 ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, L.E_pad, L.S, m, P.dec, P.carry, P.ent, P.mask,
+                 P.slotmap, P.pool, P.work, P.nwork, out_t, out_n, out_i, status);
     return check_launch();
 }
 

@@ -15,9 +15,10 @@ namespace lif {
 
 struct FwdLayout {
     int S;                                   // segments per sample
-    size_t dec, segm, agg, carry, mask, ent, winfo, counters, listed, work, pool, total;
-    size_t pool_local;                       // record slots per check wave
-    size_t pool_cap;                         // overflow records shared per sample
+    int E_pad;                               // S * kSeg: row length of the decay table
+    size_t dec, segm, agg, carry, mask, slotmap, ent, counters, listed, work, pool, total;
+    size_t n_counters;                       // uint32 counters reset by every call
+    size_t pool_cap;                         // record slots per sample
 };
 FwdLayout fwd_layout(int B, int E_max, int N);
 

@@ -181,7 +181,9 @@ def test_graph_replay_matches_eager(env):
         assert torch.equal(out.out_t, ref.out_t), rep
         assert torch.equal(out.out_n, ref.out_n), rep
         assert torch.equal(out.out_i, ref.out_i), rep
-        assert torch.equal(out.status, ref.status), rep
+        # every status word but the pool-fallback count, which depends on
+        # the order in which sub-blocks claim record slots
+        assert torch.equal(out.status[:7], ref.status[:7]), rep
         lif.forward(*do, P)                  # eager work between replays
         torch.cuda.synchronize()
 
@@ -203,13 +205,27 @@ def test_record_pool_fallback(env, monkeypatch):
     """With a tiny record pool the overflowing sub-blocks are resolved by the
     re-walk fallback; results are unchanged."""
     cfg = W.random_small(9, B=3, C=30, N=130, n_events=600, T=0.4, gain=14.0)
-    monkeypatch.setenv("LIF_POOL_LOCAL", "0")
     monkeypatch.setenv("LIF_POOL_CAP", "5")
     s = check(env, cfg.events, cfg.layers[0].WT, "pool5", both=False)
     assert s["par"]["status"][7] > 0
     monkeypatch.setenv("LIF_POOL_CAP", "0")
     s = check(env, cfg.events, cfg.layers[0].WT, "pool0", both=False)
     assert s["par"]["status"][7] >= s["par"]["status"][4] > 0   # every walked block fell back
-    monkeypatch.setenv("LIF_POOL_LOCAL", "1")
-    s = check(env, cfg.events, cfg.layers[0].WT, "local1-pool0", both=False)
-    assert s["par"]["status"][7] > 0
+
+
+@pytest.mark.parametrize("npl", [1, 2, 4])
+def test_neurons_per_lane_variants(env, monkeypatch, npl):
+    """The segment walks hold 1, 2 or 4 adjacent neurons per lane; every
+    variant matches the oracle (N = 264 is a multiple of 4 but not of 256, so
+    the last tile is partial in each)."""
+    monkeypatch.setenv("LIF_NPL", str(npl))
+    cfg = W.random_small(31, B=2, C=50, N=264, n_events=700, T=0.35, gain=12.0)
+    s = check(env, cfg.events, cfg.layers[0].WT, f"npl{npl}", both=False)
+    assert s["par"]["spikes"] > 0
+
+
+def test_odd_neuron_count(env):
+    """An odd N forces one neuron per lane (no vector weight loads)."""
+    cfg = W.random_small(32, B=2, C=40, N=77, n_events=500, T=0.3, gain=12.0)
+    s = check(env, cfg.events, cfg.layers[0].WT, "odd-N", both=False)
+    assert s["par"]["spikes"] > 0
