@@ -118,6 +118,7 @@ struct IntervalMax {
 __device__ __forceinline__ IntervalMax interval_max(const Model& m, double V0, double I0, double V1, double L,
                                                     double A, double D)
 {
+#pragma clang fp contract(off)      // the same IEEE operations wherever it is inlined
     IntervalMax r;
     if (I0 > m.th && I0 * D < m.th) {
         double lr = log(I0 * m.inv_th);
@@ -176,34 +177,55 @@ __device__ __forceinline__ void newton_step(const Model& m, double c0, double kI
 // Newton-Raphson): the smallest u in (lo, hi] with F(u) = h(u) - D = 0,
 //   F(u) = c0 - th e^{u/tm} - kI e^{-u r},  c0 = V0 - D + kappa I0, kI = kappa I0,
 // given F(lo) = Flo < 0 <= F(hi) = Fhi.  F is concave wherever it can cross
-// (I0 > 0), so it increases through its first root.  The iteration starts at
-// the root of the chord from (lo, Flo) to (hi, Fhi) instead of the paper's
-// midpoint, keeps [lo, hi] with F(lo) < 0 <= F(hi) and takes the midpoint
-// whenever a Newton step leaves it (the clamp of D.1).  The two
-// exponentials are evaluated once at the start and then carried along by
-// the factor e^{step} (Taylor series) while steps are small, so a typical
-// solve costs one pair of exponentials.  Three steps are always taken (the
-// typical count from a chord start); further steps run until a step falls
-// below 1e-9 ts (with quadratic convergence the error left is far below
-// float64 resolution of the spike time) or the bracket collapses.  On
-// return *E1 = e^{u/tm} and *E2 = e^{-u r} at the returned u.
+// (I0 > 0), so it increases through its first root.  The iteration keeps
+// [lo, hi] with F(lo) < 0 <= F(hi) and takes the midpoint whenever a Newton
+// step leaves it (the clamp of D.1).  Instead of the paper's midpoint start:
+//   * a float32 Newton phase (hardware exponentials) from the root of the
+//     chord from (lo, Flo) to (hi, Fhi) brings u to float32 accuracy;
+//   * float64 Newton steps then run from there with the two exponentials
+//     evaluated exactly once and carried along by the factor e^{step}
+//     (Taylor series) while steps are small.  The iteration stops when a
+//     step is below 1e-9 ts, or below 1e-7 ts and at most 1/100 of the step
+//     before it (quadratic convergence: the error left is then far below
+//     float64 resolution of the spike time), or the bracket collapses.
+// On return *E1 = e^{u/tm} and *E2 = e^{-u r} at the returned u.
 __device__ __forceinline__ double root_h(const Model& m, double c0, double kI, double lo, double Flo, double hi,
                                          double Fhi, double* E1o, double* E2o, int* iters)
 {
     double u = (Fhi > Flo && Fhi < INFINITY) ? lo + (hi - lo) * (-Flo * rcp_refined(Fhi - Flo)) : 0.5 * (lo + hi);
     if (!(u > lo && u <= hi)) u = 0.5 * (lo + hi);
+    {
+        // float32 phase (a start value only: the float64 phase below is
+        // bracketed and does not rely on it)
+        const float c0f = (float)c0, kIf = (float)kI, thf = (float)m.th, itm = (float)m.inv_tm,
+                    ar = (float)m.a_rate;
+        float lf = (float)lo, hf = (float)hi, uf = (float)u;
+#pragma unroll 1
+        for (int i = 0; i < 3; ++i) {
+            const float e1 = __expf(uf * itm), e2 = __expf(-uf * ar);
+            const float F = c0f - thf * e1 - kIf * e2;
+            const float dF = kIf * ar * e2 - thf * itm * e1;
+            if (F >= 0.0f) hf = uf; else lf = uf;
+            float un = uf - F / dF;
+            if (!(dF > 0.0f && un > lf && un < hf)) un = 0.5f * (lf + hf);
+            uf = un;
+        }
+        const double ud = (double)uf;
+        if (ud > lo && ud <= hi) u = ud;
+    }
     double E1 = exp(u * m.inv_tm), E2 = exp(-u * m.a_rate);
-    const double tol = 1e-9 * m.ts;
+    const double tol = 1e-9 * m.ts, tol_q = 1e-7 * m.ts;
     const double dF1 = kI * m.a_rate, dF2 = m.th * m.inv_tm;
     const double rmax = fmax(m.inv_tm, m.a_rate);
-    double d = 0.0;
-    newton_step(m, c0, kI, dF1, dF2, rmax, u, lo, hi, E1, E2, d);
-    newton_step(m, c0, kI, dF1, dF2, rmax, u, lo, hi, E1, E2, d);
-    newton_step(m, c0, kI, dF1, dF2, rmax, u, lo, hi, E1, E2, d);
-    int it = 3;
-    while (fabs(d) > tol && it < 96) {
+    double d = 0.0, dprev = INFINITY;
+    int it = 0;
+#pragma unroll 1
+    while (it < 96) {
         newton_step(m, c0, kI, dF1, dF2, rmax, u, lo, hi, E1, E2, d);
         ++it;
+        const double ad = fabs(d);
+        if (ad <= tol || (ad <= tol_q && ad <= 0.01 * dprev)) break;
+        dprev = ad;
     }
     *E1o = E1;
     *E2o = E2;

@@ -39,15 +39,22 @@
 namespace lif {
 
 // Record of one flagged sub-block of one neuron: the no-reset state (V, I)
-// entering it and right after each of its kSub events.  With the reset
-// deficit of the spikes found so far, these give the true state at every
-// interval boundary of the sub-block in O(1), so the resolve pass can test
-// all of its intervals at once.  Records live in per-sample pools; each
+// entering it and right after each of its kSub events, written by the check
+// pass; and, per interval, its crossing data written by k_intervals.  With
+// the reset deficit of the spikes found so far these give the true state at
+// every interval boundary of the sub-block in O(1), so the resolve pass can
+// test all of its intervals at once.  Records live in per-sample pools; each
 // wave allocates the records of one sub-block with one atomic.
 struct alignas(16) Record {
     double2 s[kSub + 1];    // s[0]: entering state; s[j + 1]: after event j
+    double crit[kSub + 1];  // interval j crosses iff the deficit at its start is <= crit[j] (< 0: never);
+                            // entry kSub: the open interval after the sample's last event (in the
+                            // record of the sub-block that holds it)
+    double hi[kSub + 1];    // right end of interval j's root bracket (u* or its length)
+    double fhi[kSub + 1];   // h(hi) of interval j (F(hi) = fhi - deficit)
+    int32_t kq0, cnt;       // first event of the sub-block (index in the sample), events in it
 };
-static_assert(sizeof(Record) == 16 * (kSub + 1), "record layout");
+static_assert(sizeof(Record) == 16 * (kSub + 1) + 24 * (kSub + 1) + 8, "record layout");
 constexpr uint32_t kNoSlot = 0xffffffffu;
 
 // Workgroup index -> work index such that each of the 8 XCDs (which receive
@@ -460,10 +467,23 @@ __device__ __forceinline__ void record_subblock(const WalkCoords& c, const Model
             msk[i] |= 1u << q;
         }
     }
-    if (!ok) return;
+    if (!ok) {
+        // Slots of this allocation that still lie inside the pool are marked
+        // empty, so that k_intervals (which takes every slot below the pool
+        // counter) sees only records written by this call.
+        const uint32_t hi = min(base + total, pool_cap);
+        for (uint32_t t = base + (uint32_t)lane; t < hi; t += kWave) pool[(size_t)c.b * pool_cap + t].cnt = 0;
+        return;
+    }
+    const int kq0 = c.k0 + q * kSub;
 #pragma unroll
     for (int i = 0; i < NPL; ++i)
-        if (f[i]) pool[slot[i]].s[0] = make_double2(v_of(m, U0[i], J0[i]), J0[i]);
+        if (f[i]) {
+            Record* r = pool + slot[i];
+            r->s[0] = make_double2(v_of(m, U0[i], J0[i]), J0[i]);
+            r->kq0 = kq0;
+            r->cnt = min(kSub, c.nb - kq0);
+        }
 #pragma unroll
     for (int g = 0; g < kSub / kGrp; ++g) {
         const int e0 = q * kSub + g * kGrp;
@@ -663,48 +683,129 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
 // Resolve pass: one wave per neuron that has flagged sub-blocks (a work list
 // built by the check pass).  Intervals outside flagged sub-blocks provably
 // hold no spike.  The flagged sub-blocks are taken in time order:
-//   * Candidate list: the segments' sub-block masks are compacted into a
-//     time-ordered list in LDS with one wave prefix sum per 64 segments.
-//   * Chunks of kChunk candidates are processed one after the other, with
-//     the loads of the next chunk in flight meanwhile.  Lane l holds
-//     interval l % kSub of candidate 4 i + l / kSub of the chunk, i < 4 (the
-//     four "slices"), so time order is (slice, lane).
-//   * Each interval's maximum of h(u) = (V_lin(u) - th) e^{u/tm} is derived
-//     in closed form once (interval_max); with D the deficit of the spikes
-//     so far at the interval start, it crosses iff D a <= g.  A round takes
-//     the earliest crossing interval (ballots), solves its spike time
-//     (root_h) on its lane, emits the spike and raises that interval's own
-//     deficit (so it is tested again for a second spike, Appendix E.2
-//     restart); every later interval takes the new deficit with one
-//     exponential.  Rounds repeat until no interval of the chunk crosses.
-//   * The open interval after the last event is resolved last, on lane 0.
+//   * Candidate list: per 64 segments, the sub-block masks are compacted into
+//     a time-ordered list in LDS with one wave prefix sum, and the record
+//     slot of every candidate is looked up once.
+//   * Windows of kWinCand candidates are staged in LDS: the loads of the next
+//     window are in flight (registers) while the current one is resolved.
+//   * Steps of kWave / kSub = 4 candidates: lane l takes interval l % kSub of
+//     candidate l / kSub, so time order is lane order.  Each interval
+//     carries its crossing data (k_intervals): it crosses iff the reset
+//     deficit at its start is <= crit.  A round takes the earliest crossing
+//     interval (ballot), solves its spike time (root_h) on its lane, emits
+//     the spike and raises that interval's own deficit (so it is tested again
+//     for a second spike, Appendix E.2 restart); every later interval takes
+//     the new deficit with one exponential.  Rounds repeat until no interval
+//     of the step crosses.
+//   * The open interval after the sample's last event is one more step (one
+//     lane) after the last window.
+//   * Spikes are buffered in LDS and written out kWave at a time.
+// The resolve kernel runs few waves per compute unit, so nearly all of its
+// code is fetched cold: every path is written once (no unrolled copies of
+// the solver or of the rare rebuild of sub-blocks without a record).
 // Wave-uniform state: spike count, reset deficit dref right after the
 // latest spike, at time tref.
 // ---------------------------------------------------------------------------
 constexpr int kCandCap = kWave * kSubPerSeg;     // candidates of 64 segments
-constexpr int kSlices = 4;                       // intervals per lane in a chunk
-constexpr int kChunk = kSlices * (kWave / kSub); // candidates per chunk
+constexpr int kStep = kWave / kSub;              // candidates per step
+constexpr int kWinCand = 32;                     // candidates per window
+constexpr int kWinIv = kWinCand * kSub;          // intervals per window
+constexpr int kIvPerLane = kWinIv / kWave;       // window intervals staged by each lane
+constexpr int kWinSteps = kWinCand / kStep;
+constexpr int kOpenIv = kWinIv;                  // window slot of the open interval
 
 struct ResolveLds {
     uint32_t cand[kCandCap];                     // (segment in chunk << 3) | sub-block
+    uint32_t slot[kCandCap];                     // record slot of each candidate (kNoSlot: none)
+    // the current window, interval i = candidate * kSub + j; slot kOpenIv:
+    // the open interval
+    double crit[kWinIv + 1], hi[kWinIv + 1], fhi[kWinIv + 1];
+    double2 s0[kWinIv + 1];                      // (V0, I0)
+    double t0[kWinIv + 1];                       // interval start
+    float st[kWave], si[kWave];                  // spike buffer
 };
 
-// No-reset state (V, I) after the events [k0, kq0) of a segment, from its
-// carry (used only for the open interval when the record pool was full):
-// the check pass's walk, operation for operation.
-__device__ __noinline__ double2 entering_state(const Model& m, const double2* __restrict__ carry, size_t row, int n,
-                                               int k0, int kq0, const int32_t* __restrict__ src,
-                                               const Decay* __restrict__ d, const float* __restrict__ WT, int C_in,
-                                               int N)
+// Crossing data of one interval of length L that starts in the no-reset
+// state (V0, I0) and ends with V1 (A, D: its decays): the interval reaches
+// the threshold iff the reset deficit at its start is <= crit (crit < 0:
+// never), by interval_max's test D a <= g; the spike then lies in
+// (lo, hi] with F(hi) = fhi - deficit.  Zero-length intervals never cross.
+// k_intervals (records) and the resolve pass (sub-blocks without a record)
+// both evaluate it; with floating-point contraction off here and in
+// interval_max, every inlined copy performs the same IEEE operations, so
+// both give the same bits whichever path a sub-block takes.
+__device__ __forceinline__ void crossing_data(const Model& m, double V0, double I0, double V1, double L, double A,
+                                              double D, double& crit, double& hi, double& fhi)
 {
-    const double2 c = carry[row + n];            // (U, J) eigen-coordinates
-    double U = c.x, J = c.y;
-    for (int k = k0; k < kq0; ++k) {
-        const double w = (double)WT[(size_t)clamp_src(src[k], C_in) * (size_t)N + n];
-        U = fma(d[k].A, U, w);
-        J = fma(d[k].D, J, w);
+#pragma clang fp contract(off)
+    crit = -1.0;
+    hi = 0.0;
+    fhi = -INFINITY;
+    if (!(L > 0.0)) return;
+    const IntervalMax im = interval_max(m, V0, I0, V1, L, A, D);
+    if (im.g >= 0.0) crit = im.a > 0.0 ? im.g / im.a : INFINITY;
+    hi = im.hi;
+    fhi = im.Fhi;
+}
+
+// Crossing data of the open interval (t_last, t_end] after a sample's last
+// event, from the state (V, I) right after it.
+__device__ __forceinline__ void open_interval_data(const Model& m, double V, double I, double L, double& crit,
+                                                   double& hi, double& fhi)
+{
+    double A = 0.0, D = 0.0, V1 = 0.0;
+    if (!isinf(L)) {
+        A = exp(-L * m.inv_tm);
+        D = exp(-L * m.inv_ts);
+        V1 = V * A + unit_kernel(m, L, A) * I;
     }
-    return make_double2(v_of(m, U, J), J);
+    crossing_data(m, V, I, V1, L, A, D, crit, hi, fhi);
+}
+
+// k_intervals: crossing data of every interval of every record, in
+// parallel (lanes are intervals, 4 records per wave), and of the open
+// interval in the record of each sample's last sub-block.  This takes the
+// closed-form maximum of each interval (a log and an exp) off the resolve
+// pass's per-neuron serial chain.  Grid: (blocks per sample, B); the records
+// of sample blockIdx.y are spread over that sample's blocks.
+__global__ __launch_bounds__(256) void k_intervals(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_n,
+                                                   int E_max, int E_pad, Model m, const Decay* __restrict__ dec,
+                                                   Record* __restrict__ pool, const uint32_t* __restrict__ pool_count,
+                                                   uint32_t pool_cap)
+{
+    const int lane = (int)threadIdx.x % kWave;
+    const int j = lane % kSub;
+    const uint32_t gw = (blockIdx.x * blockDim.x + threadIdx.x) / kWave;
+    const uint32_t nw = gridDim.x * blockDim.x / kWave;
+    constexpr uint32_t kRecPerWave = kWave / kSub;
+    const int b = blockIdx.y;
+    const int nb = clamp_count(ev_n[b], E_max);
+    const uint32_t used = min(pool_count[b], pool_cap);
+    const float* tt = ev_t + (size_t)b * E_max;
+    const Decay* d = dec + (size_t)b * E_pad;
+    for (uint32_t r0 = gw * kRecPerWave; r0 < used; r0 += nw * kRecPerWave) {
+        const uint32_t r = r0 + (uint32_t)(lane / kSub);
+        if (r >= used) continue;
+        Record* rec = pool + (size_t)b * pool_cap + r;
+        const int kq0 = rec->kq0, cnt = rec->cnt;
+        if (j >= cnt || kq0 < 0 || kq0 + j >= nb) continue;
+        const int k = kq0 + j;
+        const double t0 = k > 0 ? (double)tt[k - 1] : 0.0;
+        const double2 s0 = rec->s[j];
+        double crit, hi, fhi;
+        crossing_data(m, s0.x, s0.y, rec->s[j + 1].x, (double)tt[k] - t0, d[k].A, d[k].D, crit, hi, fhi);
+        rec->crit[j] = crit;
+        rec->hi[j] = hi;
+        rec->fhi[j] = fhi;
+        if (j == cnt - 1 && k == nb - 1) {
+            // the open interval after the sample's last event
+            const double2 s1 = rec->s[cnt];
+            open_interval_data(m, s1.x, s1.y, m.t_end - (double)tt[k], crit, hi, fhi);
+            rec->crit[kSub] = crit;
+            rec->hi[kSub] = hi;
+            rec->fhi[kSub] = fhi;
+        }
+    }
 }
 
 __device__ __forceinline__ int rl_int(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
@@ -717,83 +818,62 @@ __device__ __forceinline__ double rl_double(double v, int l)
     return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
 
-// One lane's interval: start time and length, no-reset state at its start
-// (V0, I0) and end (V1), decays of its gap.
-struct Iv {
-    double t0, L, V0, I0, V1, A, D;
-    bool valid;
+// Loads of window interval h kWave + lane: candidate c = c0 + h kStep +
+// lane / kSub, interval j = lane % kSub (unconditional loads from clamped
+// addresses; nothing derived from the loaded values here).
+struct StageIv {
+    double crit, hi, fhi;
+    double2 s0;
+    float tp;
 };
 
-// The raw loads of one lane's interval.  Every load is unconditional (from
-// a clamped, valid address) and nothing is derived from the loaded values
-// until the interval is used: a branch around a load, or a select of its
-// value, would make the compiler wait for every outstanding load at that
-// point, which defeats the prefetch of the next chunk.
-struct IvRaw {
-    float tp, tb;       // time of the previous event and of this interval's event
-    double A, D;        // decays of the gap
-    double2 s0;         // record: no-reset state at the interval start
-    double v1;          // record: no-reset V at the interval end
-    int k, seg, kq0, cnt, j;
-    bool valid, fb;     // fb: the record pool was full for this sub-block
-    bool rowfb;         // the same for the lane's row, valid or not
-};
-
-// The window's per-candidate values (one candidate per lane).
-struct WinLane {
-    int kq0, cnt, seg;
-    uint32_t slot;
-};
-
-__device__ __forceinline__ IvRaw load_slice(int cw, int nwin, const WinLane& w, int j, const float* __restrict__ tt,
-                                            const Decay* __restrict__ d, const Record* __restrict__ pool)
+__device__ __forceinline__ StageIv stage_load(const ResolveLds& sh, int c, int tot, int seg0, int nb, int j,
+                                              const float* __restrict__ tt, const Record* __restrict__ pool)
 {
-    IvRaw v;
-    const int c = min(cw, kWave - 1);
-    v.kq0 = __shfl(w.kq0, c, kWave);
-    v.cnt = __shfl(w.cnt, c, kWave);
-    v.seg = __shfl(w.seg, c, kWave);
-    const uint32_t slot = (uint32_t)__shfl((int)w.slot, c, kWave);
-    v.j = j;
-    v.valid = cw < nwin && j < v.cnt;
-    v.fb = v.valid && slot == kNoSlot;
-    v.rowfb = cw < nwin && slot == kNoSlot;
-    v.k = v.kq0 + (v.valid ? j : 0);
-    v.tp = tt[max(v.k - 1, 0)];
-    v.tb = tt[v.k];
-    v.A = d[v.k].A;
-    v.D = d[v.k].D;
-    const Record* rec = pool + (v.valid && slot != kNoSlot ? slot : 0u);   // pool holds at least one record
+    StageIv v;
+    const int cc = min(c, tot - 1);
+    const uint32_t cw = sh.cand[cc];
+    const uint32_t slot = sh.slot[cc];
+    const int kq0 = (seg0 + (int)(cw >> 3)) * kSeg + (int)(cw & 7u) * kSub;
+    const int k = min(kq0 + j, nb - 1);
+    v.tp = tt[max(k - 1, 0)];
+    const Record* rec = pool + (slot != kNoSlot ? slot : 0u);   // pool holds at least one record
     v.s0 = rec->s[j];
-    v.v1 = rec->s[j + 1].x;
+    v.crit = rec->crit[j];
+    v.hi = rec->hi[j];
+    v.fhi = rec->fhi[j];
     return v;
 }
 
-__device__ __forceinline__ Iv finish_slice(const Model& m, const IvRaw& r, int b, int n, int S, int N, int C_in,
-                                           const int32_t* __restrict__ src, const Decay* __restrict__ d,
-                                           const float* __restrict__ WT, const double2* __restrict__ ent)
+// Sub-blocks without a record (the pool was full): rebuild the window's
+// interval i from the sub-block's entering state (U, J).  Lane j walks
+// events 0 .. j of its sub-block with the same float64 operations, in the
+// same order, as the check pass's record walk, so the rebuilt states equal
+// the recorded ones bit for bit; then the crossing data as k_intervals
+// computes it (and the open interval's, on the lane of the sample's last
+// event).
+__device__ __forceinline__ void rebuild_window(ResolveLds& sh, const Model& m, int c0, int tot, int seg0, int b, int n,
+                                            int nb, int S, int N, int C_in, const float* __restrict__ tt,
+                                            const int32_t* __restrict__ src, const Decay* __restrict__ d,
+                                            const float* __restrict__ WT, const double2* __restrict__ ent)
 {
-    Iv v;
-    v.valid = r.valid;
-    v.t0 = r.k > 0 ? (double)r.tp : 0.0;
-    v.L = (double)r.tb - v.t0;
-    v.A = r.A;
-    v.D = r.D;
-    v.V0 = r.s0.x;
-    v.I0 = r.s0.y;
-    v.V1 = r.v1;
-    if (__ballot(r.rowfb)) {
-        // No record: rebuild the states from the sub-block's entering state
-        // (U, J).  Lane j walks events 0 .. j of its sub-block with the same
-        // float64 operations, in the same order, as the check pass's record
-        // walk, so the rebuilt states equal the recorded ones bit for bit.
-        const int q = (r.kq0 % kSeg) / kSub;
-        const double2 s0 = r.rowfb ? ent[(((size_t)b * S + r.seg) * kSubPerSeg + q) * N + n] : make_double2(0.0, 0.0);
-        double U = s0.x, J = s0.y, V0 = 0.0, I0 = 0.0;
+    const int lane = (int)threadIdx.x;
+    const int j = lane % kSub;
+    for (int h = 0; h < kIvPerLane; ++h) {
+        const int c = c0 + h * kStep + lane / kSub;
+        const bool in = c < tot;
+        const int cc = min(c, tot - 1);
+        const bool fb = in && sh.slot[cc] == kNoSlot;
+        if (!__ballot(fb)) continue;
+        const uint32_t cw = sh.cand[cc];
+        const int seg = seg0 + (int)(cw >> 3), q = (int)(cw & 7u);
+        const int kq0 = seg * kSeg + q * kSub, cnt = min(kSub, nb - kq0);
+        const double2 e0 = fb ? ent[(((size_t)b * S + seg) * kSubPerSeg + q) * N + n] : make_double2(0.0, 0.0);
+        double U = e0.x, J = e0.y, V0 = 0.0, I0 = 0.0;
         for (int e = 0; e < kSub; ++e) {
-            if (e == r.j) { V0 = v_of(m, U, J); I0 = J; }
-            const int k = r.kq0 + min(e, max(r.cnt - 1, 0));
-            const bool step_in = e <= r.j && e < r.cnt;
+            if (e == j) { V0 = v_of(m, U, J); I0 = J; }
+            const int k = kq0 + min(e, max(cnt - 1, 0));
+            const bool step_in = e <= j && e < cnt;
             const double w = step_in ? (double)WT[(size_t)clamp_src(src[k], C_in) * (size_t)N + n] : 0.0;
             const Decay dk = d[k];
             if (step_in) {
@@ -801,52 +881,33 @@ __device__ __forceinline__ Iv finish_slice(const Model& m, const IvRaw& r, int b
                 J = fma(dk.D, J, w);
             }
         }
-        if (r.fb) { v.V0 = V0; v.I0 = I0; v.V1 = v_of(m, U, J); }
+        if (fb && j < cnt) {
+            const int i = h * kWave + lane;
+            const int k = kq0 + j;
+            const double t0 = k > 0 ? (double)tt[k - 1] : 0.0;
+            const Decay dk = d[k];
+            crossing_data(m, V0, I0, v_of(m, U, J), (double)tt[k] - t0, dk.A, dk.D, sh.crit[i], sh.hi[i],
+                          sh.fhi[i]);
+            sh.s0[i] = make_double2(V0, I0);
+            if (k == nb - 1) {
+                open_interval_data(m, v_of(m, U, J), J, m.t_end - (double)tt[k], sh.crit[kOpenIv], sh.hi[kOpenIv],
+                                   sh.fhi[kOpenIv]);
+                sh.s0[kOpenIv] = make_double2(v_of(m, U, J), J);
+            }
+        }
     }
-    return v;
 }
 
-// Float32 screen of the interval test D a <= g, with no transcendental
-// function.  The crossing condition is D <= max of h over the interval.
-// h(L) = (V_lin(L) - th) e^{L/tm} is known exactly (the end test
-// D e^{-L/tm} <= V_lin(L) - th); when I0 > th, h is concave with
-// h'(0) = (I0 - th)/tm > 0, so its tangent at 0 bounds it over the whole
-// interval: max h <= V0 - th + (I0 - th) L / tm.  An interval that misses
-// both tests by more than 1e-4 of the magnitude of their terms (far above
-// float32 rounding of these few operations and of the hardware exp used for
-// D) cannot cross; only the others are tested exactly in float64.
-struct Screen {
-    float e_rhs, e_a, e_s;   // end test:     D e_a <= e_rhs  (+ margin on e_s)
-    float i_rhs, i_s;        // tangent test: D <= i_rhs      (+ margin on i_s), when I0 > th
-    bool tangent;
-};
-
-__device__ __forceinline__ Screen screen32(const Model& m, const Iv& v)
+// Float32 screen of the deficit test D <= crit at an interval start t0 with
+// the deficit dref e^{-(t0 - tref)/tm} of the spikes so far: the hardware
+// exponential and the float32 products err by a few 1e-7 relative, far
+// inside the 1e-4 margin, so an interval that fails the screen cannot cross.
+__device__ __forceinline__ bool deficit_may_cross(int ns, double dref, double tref, double t0, double crit,
+                                                  const Model& m)
 {
-    const float V0 = (float)v.V0, I0 = (float)v.I0, V1 = (float)v.V1, L = (float)v.L;
-    const float th = m.f_th, Lt = L * m.f_inv_tm;
-    Screen c;
-    c.e_rhs = V1 - th;
-    c.e_a = (float)v.A;
-    c.e_s = fabsf(V1) + th;
-    c.tangent = I0 > th * (1.0f - 1e-5f);
-    c.i_rhs = (V0 - th) + (I0 - th) * Lt;
-    c.i_s = fabsf(V0) + th + fabsf(I0) * Lt;
-    return c;
-}
-
-// Reset deficit at time t0 in float32 (0 before the first spike).
-__device__ __forceinline__ float deficit32(int ns, double dref, double tref, double t0, const Model& m)
-{
-    return ns > 0 ? (float)dref * __expf((float)(-(t0 - tref) * m.inv_tm)) : 0.0f;
-}
-
-__device__ __forceinline__ bool may_cross(const Screen& c, float D)
-{
-    const float da = D * c.e_a;
-    const bool end_miss = da - c.e_rhs > 1e-4f * (c.e_s + da);
-    const bool tan_miss = !c.tangent || D - c.i_rhs > 1e-4f * (c.i_s + D);
-    return !(end_miss && tan_miss);      // NaN passes (tested in float64)
+    if (ns == 0) return true;
+    const float D = (float)dref * __expf((float)(-(t0 - tref) * m.inv_tm));
+    return D <= (float)crit * 1.0001f;
 }
 
 // Status counts of one wave, added to the status words once per wave.
@@ -854,11 +915,85 @@ struct ResolveStats {
     int walked, fallback, capped, spikes;
 };
 
+// Wave-uniform resolve state of one neuron.
+struct Chain {
+    int ns;              // spikes so far
+    double dref, tref;   // deficit right after the latest spike, its time
+    bool capped;
+};
+
+// Spikes [from, to) from the LDS buffer to the outputs (coalesced).
+__device__ __forceinline__ void flush_spikes(ResolveLds& sh, int from, int to, float* __restrict__ st,
+                                             float* __restrict__ si)
+{
+    const int lane = (int)threadIdx.x;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (from + lane < to) {
+        st[from + lane] = sh.st[(from + lane) % kWave];
+        if (si) si[from + lane] = sh.si[(from + lane) % kWave];
+    }
+    __builtin_amdgcn_wave_barrier();
+}
+
+// Rounds over one step (see the section comment): lane l takes window
+// interval i0 + l if l < nlanes.
+__device__ __forceinline__ void resolve_step(ResolveLds& sh, const Model& m, int i0, int nlanes, Chain& ch,
+                                          float* __restrict__ st, float* __restrict__ si)
+{
+    const int lane = (int)threadIdx.x;
+    const int i = lane < nlanes ? i0 + lane : i0;
+    const double crit = sh.crit[i];
+    const double t0 = sh.t0[i];
+    bool pend = lane < nlanes && crit >= 0.0 && deficit_may_cross(ch.ns, ch.dref, ch.tref, t0, crit, m);
+    if (!__ballot(pend)) return;
+    const double2 s0 = sh.s0[i];
+    const double hi = sh.hi[i], fhi = sh.fhi[i];
+    double Dl = 0.0, lo = 0.0, Flo = 0.0;
+    if (pend) {
+        Dl = ch.ns > 0 ? ch.dref * exp(-(t0 - ch.tref) * m.inv_tm) : 0.0;
+        Flo = s0.x - m.th - Dl;
+    }
+    for (;;) {
+        const unsigned long long cm = __ballot(pend && Dl <= crit);
+        if (!cm) return;
+        const int kl = __ffsll((long long)cm) - 1;
+        double tsp = 0.0, dnew = 0.0;
+        if (lane == kl) {
+            double E1, E2;
+            const double kI = m.kappa * s0.y;
+            const double u = root_h(m, s0.x - Dl + kI, kI, lo, Flo, hi, fhi - Dl, &E1, &E2, nullptr);
+            const double iE1 = rcp_refined(E1);
+            tsp = t0 + u;
+            sh.st[ch.ns % kWave] = (float)tsp;
+            sh.si[ch.ns % kWave] = (float)(s0.y * (E2 * iE1));
+            dnew = Dl * iE1 + m.dth;
+            // the same interval is tested again with the raised deficit
+            Dl += m.dth * E1;
+            lo = u;
+            Flo = -m.dth * E1;
+        }
+        ++ch.ns;
+        ch.dref = rl_double(dnew, kl);
+        ch.tref = rl_double(tsp, kl);
+        if (ch.ns % kWave == 0) flush_spikes(sh, ch.ns - kWave, ch.ns, st, si);
+        if (ch.ns >= m.s_max) { ch.capped = true; return; }
+        if (lane < kl) pend = false;
+        if (pend && lane > kl) {
+            pend = deficit_may_cross(ch.ns, ch.dref, ch.tref, t0, crit, m);
+            if (__ballot(pend) && pend) {
+                Dl = ch.dref * exp(-(t0 - ch.tref) * m.inv_tm);
+                Flo = s0.x - m.th - Dl;
+            }
+        }
+    }
+}
+
 __device__ void resolve_neuron(ResolveLds& sh, ResolveStats& acc, int b, int n, const float* __restrict__ ev_t,
                                const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
                                const float* __restrict__ WT, int C_in, int N, int E_pad, int S, const Model& m,
-                               const Decay* __restrict__ dec, const double2* __restrict__ carry,
-                               const double2* __restrict__ ent,
+                               const Decay* __restrict__ dec, const double2* __restrict__ ent,
                                const uint32_t* __restrict__ mask, const uint32_t* __restrict__ slotmap,
                                const Record* __restrict__ pool, float* __restrict__ out_t, int32_t* __restrict__ out_n,
                                float* __restrict__ out_i)
@@ -873,15 +1008,13 @@ __device__ void resolve_neuron(ResolveLds& sh, ResolveStats& acc, int b, int n, 
     float* st = out_t + idx * (size_t)m.s_max;
     float* si = out_i ? out_i + idx * (size_t)m.s_max : nullptr;
     const int Sb = (nb + kSeg - 1) / kSeg;
+    const bool has_open = nb > 0 && m.t_end > (double)tt[nb - 1];
 
-    int ns = 0, walked = 0, fallback = 0;
-    bool capped = false, last_seen = false;
-    int last_seg = 0, last_cnt = 0;
-    uint32_t last_slot = kNoSlot;
-    double dref = 0.0, tref = 0.0;     // deficit right after the latest spike, its time
+    Chain ch{0, 0.0, 0.0, false};
+    int walked = 0, fallback = 0;
 
-    for (int seg0 = 0; seg0 < Sb && !capped; seg0 += kWave) {
-        // ---- compact this chunk's flagged sub-blocks into a time-ordered list
+    for (int seg0 = 0; seg0 < Sb && !ch.capped; seg0 += kWave) {
+        // ---- this chunk's flagged sub-blocks as a time-ordered list, with slots
         const int sj = seg0 + lane;
         const uint32_t mv = sj < Sb ? mask[((size_t)b * S + sj) * N + n] : 0u;
         const int pc = __popc(mv);
@@ -902,146 +1035,90 @@ __device__ void resolve_neuron(ResolveLds& sh, ResolveStats& acc, int b, int n, 
             }
         }
         __syncthreads();
-
-        for (int w0 = 0; w0 < tot && !capped; w0 += kWave) {
-            // ---- window: lane c holds candidate w0 + c
-            const int nwin = min(kWave, tot - w0);
-            WinLane w{0, 0, 0, kNoSlot};
-            bool last = false;
-            if (lane < nwin) {
-                uint32_t cw = sh.cand[w0 + lane];
-                w.seg = seg0 + (int)(cw >> 3);
-                int q = (int)(cw & 7u);
-                w.kq0 = w.seg * kSeg + q * kSub;
-                w.cnt = min(kSub, nb - w.kq0);
-                w.slot = slotmap[(((size_t)b * S + w.seg) * kSubPerSeg + q) * N + n];
-                last = w.kq0 + w.cnt == nb;
-            }
-            fallback += __popcll(__ballot(lane < nwin && w.slot == kNoSlot));
-            {
-                unsigned long long lm = __ballot(last);
-                if (lm) {
-                    const int ll = __ffsll((long long)lm) - 1;
-                    last_seen = true;
-                    last_seg = rl_int(w.seg, ll);
-                    last_cnt = rl_int(w.cnt, ll);
-                    last_slot = (uint32_t)rl_int((int)w.slot, ll);
+        // record slots of the candidates: independent loads, kWave at a time
+        for (int c0 = 0; c0 < tot; c0 += kWave) {
+            const int c = min(c0 + lane, tot - 1);
+            const uint32_t cw = sh.cand[c];
+            const uint32_t sl = slotmap[(((size_t)b * S + seg0 + (cw >> 3)) * kSubPerSeg + (cw & 7u)) * N + n];
+            if (c0 + lane < tot) sh.slot[c] = sl;
+        }
+        __syncthreads();
+        if (tot > 0) {
+            walked += tot;
+            int nfb = 0;
+            for (int c = lane; c < tot; c += kWave) nfb += sh.slot[c] == kNoSlot ? 1 : 0;
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) nfb += __shfl_xor(nfb, off, kWave);
+            fallback += nfb;
+            // the open interval is taken after the window holding the sample's
+            // last sub-block, when that sub-block is flagged (it is the last
+            // candidate of the last chunk)
+            const uint32_t cwl = sh.cand[tot - 1];
+            const bool open_here = has_open && (seg0 + (int)(cwl >> 3)) * kSeg + (int)(cwl & 7u) * kSub + kSub >= nb;
+            // ---- windows of kWinCand candidates: the next window's loads are
+            // in flight (registers) while the current one (LDS) is resolved
+            const int nwin = (tot + kWinCand - 1) / kWinCand;
+            StageIv nx[kIvPerLane];
+#pragma unroll
+            for (int h = 0; h < kIvPerLane; ++h) nx[h] = stage_load(sh, h * kStep + r, tot, seg0, nb, j, tt, pool);
+            for (int wi = 0; wi < nwin && !ch.capped; ++wi) {
+                const int c0 = wi * kWinCand;
+                // commit the staged window to LDS
+#pragma unroll
+                for (int h = 0; h < kIvPerLane; ++h) {
+                    const int c = c0 + h * kStep + r;
+                    const int i = h * kWave + lane;
+                    const uint32_t cw = sh.cand[min(c, tot - 1)];
+                    const int kq0 = (seg0 + (int)(cw >> 3)) * kSeg + (int)(cw & 7u) * kSub;
+                    const bool valid = c < tot && kq0 + j < nb;
+                    sh.crit[i] = valid ? nx[h].crit : -1.0;
+                    sh.hi[i] = nx[h].hi;
+                    sh.fhi[i] = nx[h].fhi;
+                    sh.s0[i] = nx[h].s0;
+                    sh.t0[i] = kq0 + j > 0 ? (double)nx[h].tp : 0.0;
                 }
-            }
-
-            IvRaw nx[kSlices];
-#pragma unroll
-            for (int i = 0; i < kSlices; ++i) nx[i] = load_slice(i * (kWave / kSub) + r, nwin, w, j, tt, d, pool);
-            for (int c0 = 0; c0 < nwin && !capped; c0 += kChunk) {
-                IvRaw raw[kSlices];
-#pragma unroll
-                for (int i = 0; i < kSlices; ++i) raw[i] = nx[i];
-                walked += min(kChunk, nwin - c0);
-                // ---- prefetch the next chunk
-                if (c0 + kChunk < nwin) {
-#pragma unroll
-                    for (int i = 0; i < kSlices; ++i)
-                        nx[i] = load_slice(c0 + kChunk + i * (kWave / kSub) + r, nwin, w, j, tt, d, pool);
-                }
-                Iv v[kSlices];
-#pragma unroll
-                for (int i = 0; i < kSlices; ++i) v[i] = finish_slice(m, raw[i], b, n, S, N, C_in, src, d, WT, ent);
-                // ---- slices in time order: screen in float32 with the current
-                // deficit, then the deficit and the maximum in float64 where
-                // an interval may cross, then rounds
-#pragma unroll
-                for (int i = 0; i < kSlices; ++i) {
-                    if (capped) break;
-                    const Iv& x = v[i];
-                    const Screen sc = screen32(m, x);
-                    bool pend = x.valid && x.L > 0.0 && may_cross(sc, deficit32(ns, dref, tref, x.t0, m));
-                    if (!__ballot(pend)) continue;
-                    double Dl = 0.0, lo = 0.0, Flo = 0.0;
-                    IntervalMax im{-1.0, 1.0, 0.0, 0.0};
-                    if (pend) {
-                        Dl = ns > 0 ? dref * exp(-(x.t0 - tref) * m.inv_tm) : 0.0;
-                        im = interval_max(m, x.V0, x.I0, x.V1, x.L, x.A, x.D);
-                        Flo = x.V0 - m.th - Dl;
+                const bool last_win = wi == nwin - 1;
+                if (last_win && open_here && lane == 0) {
+                    // the open interval, from the last candidate's record
+                    const uint32_t slot = sh.slot[tot - 1];
+                    const int kq0 = (seg0 + (int)(cwl >> 3)) * kSeg + (int)(cwl & 7u) * kSub;
+                    sh.crit[kOpenIv] = -1.0;
+                    if (slot != kNoSlot) {
+                        const Record* rec = pool + slot;
+                        sh.crit[kOpenIv] = rec->crit[kSub];
+                        sh.hi[kOpenIv] = rec->hi[kSub];
+                        sh.fhi[kOpenIv] = rec->fhi[kSub];
+                        sh.s0[kOpenIv] = rec->s[nb - kq0];
                     }
-                    // ---- rounds: the earliest crossing lane solves, the later
-                    // ones re-test
-                    for (;;) {
-                        const unsigned long long cm = __ballot(pend && Dl * im.a <= im.g);
-                        if (!cm) break;
-                        const int kl = __ffsll((long long)cm) - 1;
-                        double tsp = 0.0, dnew = 0.0;
-                        if (lane == kl) {
-                            double E1, E2;
-                            const double kI = m.kappa * x.I0;
-                            const double u = root_h(m, x.V0 - Dl + kI, kI, lo, Flo, im.hi, im.Fhi - Dl, &E1, &E2,
-                                                    nullptr);
-                            const double iE1 = rcp_refined(E1);
-                            tsp = x.t0 + u;
-                            st[ns] = (float)tsp;
-                            if (si) si[ns] = (float)(x.I0 * (E2 * iE1));
-                            dnew = Dl * iE1 + m.dth;
-                            // the same interval is tested again with the raised deficit
-                            Dl += m.dth * E1;
-                            lo = u;
-                            Flo = -m.dth * E1;
-                        }
-                        ++ns;
-                        dref = rl_double(dnew, kl);
-                        tref = rl_double(tsp, kl);
-                        if (ns >= m.s_max) { capped = true; break; }
-                        if (lane < kl) pend = false;
-                        if (pend && lane > kl) {
-                            pend = may_cross(sc, deficit32(ns, dref, tref, x.t0, m));
-                            if (__ballot(pend) && pend) {
-                                Dl = dref * exp(-(x.t0 - tref) * m.inv_tm);
-                                Flo = x.V0 - m.th - Dl;
-                            }
-                        }
-                    }
+                    sh.t0[kOpenIv] = (double)tt[nb - 1];
                 }
+                __syncthreads();
+                if (__ballot(sh.slot[min(c0 + lane / 2, tot - 1)] == kNoSlot))
+                    rebuild_window(sh, m, c0, tot, seg0, b, n, nb, S, N, C_in, tt, src, d, WT, ent);
+                __syncthreads();
+                const int c1 = c0 + kWinCand;
+                if (c1 < tot) {
+#pragma unroll
+                    for (int h = 0; h < kIvPerLane; ++h) nx[h] = stage_load(sh, c1 + h * kStep + r, tot, seg0, nb, j, tt, pool);
+                    // keep the loads here, ahead of the window's steps (not sunk to the commit)
+                    asm volatile("" ::: "memory");
+                }
+                // the window's steps, then (last window) the open interval as one more
+                const int steps = min(kWinSteps, (tot - c0 + kStep - 1) / kStep);
+                const int nsteps = steps + (last_win && open_here ? 1 : 0);
+                for (int g = 0; g < nsteps && !ch.capped; ++g)
+                    resolve_step(sh, m, g < steps ? g * kWave : kOpenIv, g < steps ? kWave : 1, ch, st, si);
+                __syncthreads();                      // the window is rewritten next
             }
         }
         __syncthreads();                              // the list is rewritten by the next chunk
     }
-
-    // ---- the open interval (t_last, t_end] after the last event, lane 0
-    const double t_last = nb > 0 ? (double)tt[nb - 1] : 0.0;
-    if (!capped && last_seen && m.t_end > t_last && lane == 0) {
-        double2 s0 = last_slot != kNoSlot
-                         ? pool[last_slot].s[last_cnt]
-                         : entering_state(m, carry, ((size_t)b * S + last_seg) * N, n, last_seg * kSeg, nb, src, d, WT,
-                                          C_in, N);
-        const double V0 = s0.x, I0 = s0.y, L = m.t_end - t_last;
-        double A = 0.0, Dd = 0.0, V1 = 0.0;
-        if (!isinf(L)) {
-            A = exp(-L * m.inv_tm);
-            Dd = exp(-L * m.inv_ts);
-            V1 = V0 * A + unit_kernel(m, L, A) * I0;
-        }
-        const IntervalMax im = interval_max(m, V0, I0, V1, L, A, Dd);
-        double Dk = ns > 0 ? dref * exp(-(t_last - tref) * m.inv_tm) : 0.0;
-        double lo = 0.0, Flo = V0 - m.th - Dk;
-        const double kI = m.kappa * I0;
-        while (Dk * im.a <= im.g) {
-            double E1, E2;
-            double u = root_h(m, V0 - Dk + kI, kI, lo, Flo, im.hi, im.Fhi - Dk, &E1, &E2, nullptr);
-            st[ns] = (float)(t_last + u);
-            if (si) si[ns] = (float)(I0 * (E2 * rcp_refined(E1)));
-            ++ns;
-            Dk += m.dth * E1;
-            lo = u;
-            Flo = -m.dth * E1;
-            if (ns >= m.s_max) { capped = true; break; }
-        }
-    }
-    ns = rl_int(ns, 0);
-    capped = rl_int((int)capped, 0) != 0;
-
-    if (lane == 0) out_n[idx] = ns;
+    flush_spikes(sh, ch.ns - ch.ns % kWave, ch.ns, st, si);
+    if (lane == 0) out_n[idx] = ch.ns;
     acc.walked += walked;
     acc.fallback += fallback;
-    acc.capped += capped ? 1 : 0;
-    acc.spikes += ns;
+    acc.capped += ch.capped ? 1 : 0;
+    acc.spikes += ch.ns;
 }
 
 // Work-list driven: the per-sample lists of neurons built by k_check are
@@ -1052,7 +1129,6 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
                                                    const int32_t* __restrict__ ev_n, int B, int E_max,
                                                    const float* __restrict__ WT, int C_in, int N, int E_pad, int S,
                                                    Model m, const Decay* __restrict__ dec,
-                                                   const double2* __restrict__ carry,
                                                    const double2* __restrict__ ent,
                                                    const uint32_t* __restrict__ mask,
                                                    const uint32_t* __restrict__ slotmap,
@@ -1095,7 +1171,7 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
         const uint32_t before = l > 0 ? (uint32_t)__shfl((int)incl, l - 1, kWave) : base;
         const uint32_t bn = work[(size_t)b * N + (w - before)];
         resolve_neuron(sh, acc, (int)(bn / (uint32_t)N), (int)(bn % (uint32_t)N), ev_t, ev_src, ev_n, E_max, WT,
-                       C_in, N, E_pad, S, m, dec, carry, ent, mask, slotmap, pool, out_t, out_n, out_i);
+                       C_in, N, E_pad, S, m, dec, ent, mask, slotmap, pool, out_t, out_n, out_i);
     }
     if (threadIdx.x == 0) {
         if (acc.walked) {
@@ -1343,11 +1419,19 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     case 2: launch_walks<2>(L, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, status, stream); break;
     default: launch_walks<1>(L, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, status, stream); break;
     }
+    {
+        // blocks per sample: enough for the pool slice at 16 records per block, at most 64
+        const size_t per = (L.pool_cap + 15) / 16;
+        const unsigned bx = (unsigned)(per < 1 ? 1 : (per > 64 ? 64 : per));
+        if (B > 0)
+            TIMED_LAUNCH("intervals", k_intervals, dim3(bx, (unsigned)B), dim3(256), 0, stream,
+                         ev_t, ev_n, E_max, L.E_pad, m, P.dec, P.pool, P.pool_count, (uint32_t)L.pool_cap);
+    }
     // Single-wave workgroups over the concatenated per-sample lists.
     const unsigned rgrid = (unsigned)(nn < 4096 ? nn : 4096);
     TIMED_LAUNCH("resolve", k_resolve, dim3(rgrid), dim3(kWave), 0, stream,
-                 ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, L.E_pad, L.S, m, P.dec, P.carry, P.ent, P.mask,
-                 P.slotmap, P.pool, P.work, P.nwork, out_t, out_n, out_i, status);
+                 ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, L.E_pad, L.S, m, P.dec, P.ent, P.mask, P.slotmap,
+                 P.pool, P.work, P.nwork, out_t, out_n, out_i, status);
     return check_launch();
 }
 
