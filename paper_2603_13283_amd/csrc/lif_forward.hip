@@ -566,7 +566,6 @@ __device__ __forceinline__ void screen_grp(const Model& m, const double2* __rest
 // appends it to the sample's work list.  When the pool is full, the
 // sub-block's entering state (U, J) goes to ent instead (the resolve pass
 // then rebuilds its states from it).
-template <int NPL>
 __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
     const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
     int E_pad, const float* __restrict__ WT, int C_in, int N, int tiles, int S, int items, Model m,
@@ -577,6 +576,7 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
 // work: per-sample lists of the neurons with flagged sub-blocks (capacity N
 // each); nwork: per-sample list lengths.
 {
+    constexpr int NPL = 1;                  // one neuron per lane (occupancy)
     __shared__ double2 s_ad[kWalkWaves][kSeg];
     __shared__ double s_lk[kWalkWaves][kSeg];
     __shared__ double s_gk[kWalkWaves][kGrpPerSeg];
@@ -1359,8 +1359,14 @@ static void launch_walks(const FwdLayout& L, const FwdPtrs& P, const float* ev_t
     const int ctiles = (N + kWave - 1) / kWave;
     TIMED_LAUNCH("carry", k_carry, dim3((unsigned)((size_t)B * ctiles)), dim3(kWave * kCarryWaves), 0, stream,
                  ev_n, B, E_max, N, ctiles, L.S, P.segm, P.agg, P.carry, status);
-    TIMED_LAUNCH("check", k_check<NPL>, dim3(blocks), dim3(kWave * kWalkWaves), 0, stream,
-                 ev_t, ev_src, ev_n, E_max, L.E_pad, WT, C_in, N, tiles, L.S, (int)items, m, P.dec, P.carry, P.ent,
+    // The check pass takes one neuron per lane whatever NPL the aggregate
+    // uses: its screen and record state make wider lanes cost occupancy
+    // (about 200 VGPRs at four neurons per lane against under 80 at one).
+    const int ctl = (N + kWave - 1) / kWave;
+    const size_t citems = (size_t)B * L.S * ctl;
+    const unsigned cblocks = (unsigned)((citems + kWalkWaves - 1) / kWalkWaves);
+    TIMED_LAUNCH("check", k_check, dim3(cblocks), dim3(kWave * kWalkWaves), 0, stream,
+                 ev_t, ev_src, ev_n, E_max, L.E_pad, WT, C_in, N, ctl, L.S, (int)citems, m, P.dec, P.carry, P.ent,
                  P.mask, P.slotmap, P.pool, P.pool_count, (uint32_t)L.pool_cap, P.listed, P.work, P.nwork);
 }
 
