@@ -22,8 +22,11 @@
 //                with a no-crossing screen per inter-event interval
 //                (screen_value).  Resets only lower V, so a sub-block of kSub
 //                events whose no-reset trajectory passes every screen holds
-//                no spike whatever happened before it; flagged sub-blocks
-//                get a record of their no-reset states for the resolve pass.
+//                no spike whatever happened before it; a flagged
+//                sub-block stores its entering state and reserves a record.
+//   k_records    per reserved record (lanes are the sub-block's intervals):
+//                the no-reset states at every interval boundary of the
+//                sub-block and each interval's crossing data.
 //   k_resolve    per (sample, neuron) with flagged sub-blocks: walks only
 //                those, in time order.  Spikes found so far lower V by a
 //                known decaying amount (the reset deficit), which corrects
@@ -38,23 +41,25 @@
 
 namespace lif {
 
-// Record of one flagged sub-block of one neuron: the no-reset state (V, I)
-// entering it and right after each of its kSub events, written by the check
-// pass; and, per interval, its crossing data written by k_intervals.  With
-// the reset deficit of the spikes found so far these give the true state at
-// every interval boundary of the sub-block in O(1), so the resolve pass can
-// test all of its intervals at once.  Records live in per-sample pools; each
-// wave allocates the records of one sub-block with one atomic.
+// Record of one flagged sub-block of one neuron, in per-sample pools.  The
+// check pass reserves it (one atomic per wave) and writes its header; the
+// record pass k_records fills in, per interval j of the sub-block, the
+// no-reset state (V, I) at the interval start and the interval's crossing
+// data.  With the reset deficit of the spikes found so far these give the
+// true state at every interval boundary in O(1), so the resolve pass can test
+// all intervals of the sub-block at once.
 struct alignas(16) Record {
-    double2 s[kSub + 1];    // s[0]: entering state; s[j + 1]: after event j
+    double2 s[kSub + 1];    // s[j]: state at the start of interval j (after event j - 1); in the
+                            // sub-block holding the sample's last event, s[cnt]: the state after it
     double crit[kSub + 1];  // interval j crosses iff the deficit at its start is <= crit[j] (< 0: never);
                             // entry kSub: the open interval after the sample's last event (in the
                             // record of the sub-block that holds it)
     double hi[kSub + 1];    // right end of interval j's root bracket (u* or its length)
     double fhi[kSub + 1];   // h(hi) of interval j (F(hi) = fhi - deficit)
-    int32_t kq0, cnt;       // first event of the sub-block (index in the sample), events in it
+    int32_t kq0, cnt, n;    // first event of the sub-block (index in the sample), events in it, neuron
+    int32_t pad_[3];
 };
-static_assert(sizeof(Record) == 16 * (kSub + 1) + 24 * (kSub + 1) + 8, "record layout");
+static_assert(sizeof(Record) % 16 == 0, "record layout");
 constexpr uint32_t kNoSlot = 0xffffffffu;
 
 // Workgroup index -> work index such that each of the 8 XCDs (which receive
@@ -430,78 +435,6 @@ __global__ __launch_bounds__(kWave * kCarryWaves) void k_carry(
     }
 }
 
-// Records of a flagged sub-block: one pool allocation for the wave, then a
-// second walk of the sub-block (its weights loaded again) storing the
-// no-reset states (V, I) of the flagged neurons.
-template <int NPL>
-__device__ __forceinline__ void record_subblock(const WalkCoords& c, const Model& m, int q, int S, int N,
-                                                const Stage& st, const double2* __restrict__ lad, double (&U0)[NPL],
-                                                double (&J0)[NPL], const bool (&f)[NPL],
-                                                const unsigned long long (&fm)[NPL], double2* __restrict__ ent,
-                                                uint32_t* __restrict__ slotmap, Record* __restrict__ pool,
-                                                uint32_t* __restrict__ pool_count, uint32_t pool_cap,
-                                                uint32_t (&msk)[NPL])
-{
-    const int lane = c.lane;
-    const unsigned long long below = (1ull << lane) - 1ull;
-    uint32_t total = 0;
-#pragma unroll
-    for (int i = 0; i < NPL; ++i) total += (uint32_t)__popcll(fm[i]);
-    uint32_t base = 0;
-    if (lane == 0) base = atomicAdd(&pool_count[c.b], total);
-    base = (uint32_t)__shfl((int)base, 0, kWave);
-    const bool ok = (unsigned long long)base + total <= (unsigned long long)pool_cap;
-    uint32_t slot[NPL];
-    uint32_t before = 0;
-#pragma unroll
-    for (int i = 0; i < NPL; ++i) {
-        slot[i] = ok ? (uint32_t)c.b * pool_cap + base + before + (uint32_t)__popcll(fm[i] & below) : kNoSlot;
-        before += (uint32_t)__popcll(fm[i]);
-    }
-    const size_t srow = (((size_t)c.b * S + c.seg) * kSubPerSeg + q) * N + c.n0;
-#pragma unroll
-    for (int i = 0; i < NPL; ++i) {
-        if (f[i]) {
-            slotmap[srow + i] = slot[i];
-            if (!ok) ent[srow + i] = make_double2(U0[i], J0[i]);
-            msk[i] |= 1u << q;
-        }
-    }
-    if (!ok) {
-        // Slots of this allocation that still lie inside the pool are marked
-        // empty, so that k_intervals (which takes every slot below the pool
-        // counter) sees only records written by this call.
-        const uint32_t hi = min(base + total, pool_cap);
-        for (uint32_t t = base + (uint32_t)lane; t < hi; t += kWave) pool[(size_t)c.b * pool_cap + t].cnt = 0;
-        return;
-    }
-    const int kq0 = c.k0 + q * kSub;
-#pragma unroll
-    for (int i = 0; i < NPL; ++i)
-        if (f[i]) {
-            Record* r = pool + slot[i];
-            r->s[0] = make_double2(v_of(m, U0[i], J0[i]), J0[i]);
-            r->kq0 = kq0;
-            r->cnt = min(kSub, c.nb - kq0);
-        }
-#pragma unroll
-    for (int g = 0; g < kSub / kGrp; ++g) {
-        const int e0 = q * kSub + g * kGrp;
-        float w[kGrp][NPL];
-        load_grp<NPL>(st, e0, w);
-#pragma unroll
-        for (int j = 0; j < kGrp; ++j) {
-            if (e0 + j < c.cnt) {
-                const double2 ad = lad[e0 + j];
-                step<NPL>(ad.x, ad.y, w[j], U0, J0);
-            }
-#pragma unroll
-            for (int i = 0; i < NPL; ++i)
-                if (f[i]) pool[slot[i]].s[g * kGrp + j + 1] = make_double2(v_of(m, U0[i], J0[i]), J0[i]);
-        }
-    }
-}
-
 // Screen of one group of intervals.  The coarse test bounds every interval
 // of the group at once: with X = U - J at each interval start, the largest X
 // and J over the group and the group's largest slope glk,
@@ -560,12 +493,13 @@ __device__ __forceinline__ void screen_grp(const Model& m, const double2* __rest
 // Re-walk from the carried no-reset state with the no-crossing screen on
 // every interval: the interval before each event of the sub-block and, in
 // the sub-block holding the sample's last event, the open interval after it
-// (up to t_end).  A flagged (sub-block, neuron) gets a record of its no-reset
-// states (V, I) in the sample's pool, its slot in slotmap and a bit in the
-// neuron's sub-block mask of the segment; the first segment to flag a neuron
-// appends it to the sample's work list.  When the pool is full, the
-// sub-block's entering state (U, J) goes to ent instead (the resolve pass
-// then rebuilds its states from it).
+// (up to t_end).  A flagged (sub-block, neuron) stores its entering state
+// (U, J) in ent and sets a bit in the neuron's sub-block mask of the segment.
+// At the end of the item the wave reserves records for all its flagged
+// sub-blocks with one atomic on the sample's pool counter and writes their
+// headers and slots (kNoSlot past the pool capacity: the resolve pass then
+// rebuilds that sub-block's states from ent itself); the first segment to
+// flag a neuron appends it to the sample's work list.
 __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
     const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
     int E_pad, const float* __restrict__ WT, int C_in, int N, int tiles, int S, int items, Model m,
@@ -629,21 +563,55 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
             for (int i = 0; i < NPL; ++i)
                 z[i] = fmax(z[i], J[i] > m.th ? fma(J[i] - m.th, open_lk, U[i] - J[i]) : U[i] - J[i]);
         }
-        bool f[NPL];
-        unsigned long long fm[NPL];
-        unsigned long long any = 0ull;
+        const size_t srow = (((size_t)c.b * S + c.seg) * kSubPerSeg + q) * N + c.n0;
 #pragma unroll
-        for (int i = 0; i < NPL; ++i) {
-            f[i] = c.live && z[i] >= m.thk_lo;
-            fm[i] = __ballot(f[i]);
-            any |= fm[i];
-        }
-        if (any) record_subblock<NPL>(c, m, q, S, N, st, lad, U0, J0, f, fm, ent, slotmap, pool, pool_count,
-                                      pool_cap, msk);
+        for (int i = 0; i < NPL; ++i)
+            if (c.live && z[i] >= m.thk_lo) {
+                ent[srow + i] = make_double2(U0[i], J0[i]);
+                msk[i] |= 1u << q;
+            }
     }
     if (c.live) {
 #pragma unroll
         for (int i = 0; i < NPL; ++i) mask[row + i] = msk[i];
+    }
+    // Records of the wave's flagged sub-blocks: one reservation, slots in
+    // lane order (exclusive prefix sum of the per-lane counts).
+    {
+        uint32_t mine = 0;
+#pragma unroll
+        for (int i = 0; i < NPL; ++i) mine += (uint32_t)__popc(msk[i]);
+        uint32_t ex = mine;
+#pragma unroll
+        for (int off = 1; off < kWave; off <<= 1) {
+            const uint32_t v = (uint32_t)__shfl_up((int)ex, off, kWave);
+            if (lane >= off) ex += v;
+        }
+        const uint32_t total = (uint32_t)__shfl((int)ex, kWave - 1, kWave);
+        ex -= mine;
+        if (total) {
+            uint32_t base = 0;
+            if (lane == 0) base = atomicAdd(&pool_count[c.b], total);
+            base = (uint32_t)__shfl((int)base, 0, kWave) + ex;
+#pragma unroll
+            for (int i = 0; i < NPL; ++i) {
+                for (uint32_t mm = msk[i]; mm; mm &= mm - 1u) {
+                    const int q = __builtin_ctz(mm);
+                    const size_t srow = (((size_t)c.b * S + c.seg) * kSubPerSeg + q) * N + c.n0 + i;
+                    uint32_t slot = kNoSlot;
+                    if (base < pool_cap) {
+                        slot = (uint32_t)c.b * pool_cap + base;
+                        Record* r = pool + slot;
+                        const int kq0 = c.k0 + q * kSub;
+                        r->kq0 = kq0;
+                        r->cnt = min(kSub, c.nb - kq0);
+                        r->n = c.n0 + i;
+                    }
+                    slotmap[srow] = slot;
+                    ++base;
+                }
+            }
+        }
     }
     // Work list of the sample: the first segment to flag a neuron appends it
     // (one OR per flagged neuron, one counter update per wave).
@@ -690,7 +658,7 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
 //     window are in flight (registers) while the current one is resolved.
 //   * Steps of kWave / kSub = 4 candidates: lane l takes interval l % kSub of
 //     candidate l / kSub, so time order is lane order.  Each interval
-//     carries its crossing data (k_intervals): it crosses iff the reset
+//     carries its crossing data (k_records): it crosses iff the reset
 //     deficit at its start is <= crit.  A round takes the earliest crossing
 //     interval (ballot), solves its spike time (root_h) on its lane, emits
 //     the spike and raises that interval's own deficit (so it is tested again
@@ -730,7 +698,7 @@ struct ResolveLds {
 // the threshold iff the reset deficit at its start is <= crit (crit < 0:
 // never), by interval_max's test D a <= g; the spike then lies in
 // (lo, hi] with F(hi) = fhi - deficit.  Zero-length intervals never cross.
-// k_intervals (records) and the resolve pass (sub-blocks without a record)
+// k_records and the resolve pass (sub-blocks without a record)
 // both evaluate it; with floating-point contraction off here and in
 // interval_max, every inlined copy performs the same IEEE operations, so
 // both give the same bits whichever path a sub-block takes.
@@ -762,16 +730,83 @@ __device__ __forceinline__ void open_interval_data(const Model& m, double V, dou
     crossing_data(m, V, I, V1, L, A, D, crit, hi, fhi);
 }
 
-// k_intervals: crossing data of every interval of every record, in
+// States of interval j of a sub-block (events kq0 .. kq0 + cnt - 1 of the
+// sample) from the sub-block's entering no-reset state (U, J): the lane walks
+// events 0 .. j, taking the state at the interval start (after event j - 1)
+// and, after event j, V at the interval end and J.  The record pass and the
+// resolve pass's rebuild of sub-blocks without a record both call it, so the
+// two give the same bits.
+struct IvStates {
+    double V0, I0, V1, J1;
+};
+
+template <bool kHoist>
+__device__ __forceinline__ IvStates subblock_walk(const Model& m, double U, double J, int kq0, int cnt, int j, int n,
+                                                  int N, int C_in, const int32_t* __restrict__ src,
+                                                  const Decay* __restrict__ d, const float* __restrict__ WT)
+{
+    IvStates r{0.0, 0.0, 0.0, 0.0};
+    const int last = max(cnt - 1, 0);
+    if constexpr (kHoist) {
+        // every load first (independent, clamped to the sub-block), then the walk
+        int sc[kSub];
+#pragma unroll
+        for (int e = 0; e < kSub; ++e) sc[e] = clamp_src(src[kq0 + min(e, last)], C_in);
+        float wv[kSub];
+        double2 ad[kSub];
+#pragma unroll
+        for (int e = 0; e < kSub; ++e) {
+            wv[e] = WT[(size_t)sc[e] * (size_t)N + n];
+            const Decay dk = d[kq0 + min(e, last)];
+            ad[e] = make_double2(dk.A, dk.D);
+        }
+#pragma unroll
+        for (int e = 0; e < kSub; ++e) {
+            if (e == j) {
+                r.V0 = v_of(m, U, J);
+                r.I0 = J;
+            }
+            if (e <= j && e < cnt) {
+                const double w = (double)wv[e];
+                U = fma(ad[e].x, U, w);
+                J = fma(ad[e].y, J, w);
+            }
+        }
+    } else {
+        // the same operations, one event at a time (few registers)
+        for (int e = 0; e < kSub; ++e) {
+            if (e == j) {
+                r.V0 = v_of(m, U, J);
+                r.I0 = J;
+            }
+            const int k = kq0 + min(e, last);
+            const bool step_in = e <= j && e < cnt;
+            const double w = step_in ? (double)WT[(size_t)clamp_src(src[k], C_in) * (size_t)N + n] : 0.0;
+            const Decay dk = d[k];
+            if (step_in) {
+                U = fma(dk.A, U, w);
+                J = fma(dk.D, J, w);
+            }
+        }
+    }
+    r.V1 = v_of(m, U, J);
+    r.J1 = J;
+    return r;
+}
+
+// k_records: the states and crossing data of every reserved record, in
 // parallel (lanes are intervals, 4 records per wave), and of the open
-// interval in the record of each sample's last sub-block.  This takes the
-// closed-form maximum of each interval (a log and an exp) off the resolve
-// pass's per-neuron serial chain.  Grid: (blocks per sample, B); the records
-// of sample blockIdx.y are spread over that sample's blocks.
-__global__ __launch_bounds__(256) void k_intervals(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_n,
-                                                   int E_max, int E_pad, Model m, const Decay* __restrict__ dec,
-                                                   Record* __restrict__ pool, const uint32_t* __restrict__ pool_count,
-                                                   uint32_t pool_cap)
+// interval in the record of each sample's last sub-block.  This keeps the
+// sub-block walks and the closed-form maximum of each interval (a log and an
+// exp) off the resolve pass's per-neuron serial chain.  Grid: (blocks per
+// sample, B); the records of sample blockIdx.y are spread over that sample's
+// blocks.
+__global__ __launch_bounds__(256) void k_records(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src,
+                                                 const int32_t* __restrict__ ev_n, int E_max, int E_pad, int S,
+                                                 const float* __restrict__ WT, int C_in, int N, Model m,
+                                                 const Decay* __restrict__ dec, const double2* __restrict__ ent,
+                                                 Record* __restrict__ pool, const uint32_t* __restrict__ pool_count,
+                                                 uint32_t pool_cap)
 {
     const int lane = (int)threadIdx.x % kWave;
     const int j = lane % kSub;
@@ -782,25 +817,29 @@ __global__ __launch_bounds__(256) void k_intervals(const float* __restrict__ ev_
     const int nb = clamp_count(ev_n[b], E_max);
     const uint32_t used = min(pool_count[b], pool_cap);
     const float* tt = ev_t + (size_t)b * E_max;
+    const int32_t* src = ev_src + (size_t)b * E_max;
     const Decay* d = dec + (size_t)b * E_pad;
     for (uint32_t r0 = gw * kRecPerWave; r0 < used; r0 += nw * kRecPerWave) {
         const uint32_t r = r0 + (uint32_t)(lane / kSub);
         if (r >= used) continue;
         Record* rec = pool + (size_t)b * pool_cap + r;
-        const int kq0 = rec->kq0, cnt = rec->cnt;
-        if (j >= cnt || kq0 < 0 || kq0 + j >= nb) continue;
+        const int kq0 = rec->kq0, cnt = rec->cnt, n = rec->n;
+        if (j >= cnt || kq0 < 0 || kq0 + j >= nb || n < 0 || n >= N) continue;
+        const int seg = kq0 / kSeg, q = (kq0 % kSeg) / kSub;
+        const double2 e0 = ent[(((size_t)b * S + seg) * kSubPerSeg + q) * N + n];
+        const IvStates v = subblock_walk<true>(m, e0.x, e0.y, kq0, cnt, j, n, N, C_in, src, d, WT);
         const int k = kq0 + j;
         const double t0 = k > 0 ? (double)tt[k - 1] : 0.0;
-        const double2 s0 = rec->s[j];
         double crit, hi, fhi;
-        crossing_data(m, s0.x, s0.y, rec->s[j + 1].x, (double)tt[k] - t0, d[k].A, d[k].D, crit, hi, fhi);
+        crossing_data(m, v.V0, v.I0, v.V1, (double)tt[k] - t0, d[k].A, d[k].D, crit, hi, fhi);
+        rec->s[j] = make_double2(v.V0, v.I0);
         rec->crit[j] = crit;
         rec->hi[j] = hi;
         rec->fhi[j] = fhi;
-        if (j == cnt - 1 && k == nb - 1) {
+        if (k == nb - 1) {
             // the open interval after the sample's last event
-            const double2 s1 = rec->s[cnt];
-            open_interval_data(m, s1.x, s1.y, m.t_end - (double)tt[k], crit, hi, fhi);
+            open_interval_data(m, v.V1, v.J1, m.t_end - (double)tt[k], crit, hi, fhi);
+            rec->s[j + 1] = make_double2(v.V1, v.J1);
             rec->crit[kSub] = crit;
             rec->hi[kSub] = hi;
             rec->fhi[kSub] = fhi;
@@ -846,12 +885,9 @@ __device__ __forceinline__ StageIv stage_load(const ResolveLds& sh, int c, int t
 }
 
 // Sub-blocks without a record (the pool was full): rebuild the window's
-// interval i from the sub-block's entering state (U, J).  Lane j walks
-// events 0 .. j of its sub-block with the same float64 operations, in the
-// same order, as the check pass's record walk, so the rebuilt states equal
-// the recorded ones bit for bit; then the crossing data as k_intervals
-// computes it (and the open interval's, on the lane of the sample's last
-// event).
+// intervals from the sub-blocks' entering states (U, J) with subblock_walk,
+// as the record pass does, then the crossing data (and the open interval's,
+// on the lane of the sample's last event).
 __device__ __forceinline__ void rebuild_window(ResolveLds& sh, const Model& m, int c0, int tot, int seg0, int b, int n,
                                             int nb, int S, int N, int C_in, const float* __restrict__ tt,
                                             const int32_t* __restrict__ src, const Decay* __restrict__ d,
@@ -869,30 +905,18 @@ __device__ __forceinline__ void rebuild_window(ResolveLds& sh, const Model& m, i
         const int seg = seg0 + (int)(cw >> 3), q = (int)(cw & 7u);
         const int kq0 = seg * kSeg + q * kSub, cnt = min(kSub, nb - kq0);
         const double2 e0 = fb ? ent[(((size_t)b * S + seg) * kSubPerSeg + q) * N + n] : make_double2(0.0, 0.0);
-        double U = e0.x, J = e0.y, V0 = 0.0, I0 = 0.0;
-        for (int e = 0; e < kSub; ++e) {
-            if (e == j) { V0 = v_of(m, U, J); I0 = J; }
-            const int k = kq0 + min(e, max(cnt - 1, 0));
-            const bool step_in = e <= j && e < cnt;
-            const double w = step_in ? (double)WT[(size_t)clamp_src(src[k], C_in) * (size_t)N + n] : 0.0;
-            const Decay dk = d[k];
-            if (step_in) {
-                U = fma(dk.A, U, w);
-                J = fma(dk.D, J, w);
-            }
-        }
+        const IvStates v = subblock_walk<false>(m, e0.x, e0.y, kq0, cnt, j, n, N, C_in, src, d, WT);
         if (fb && j < cnt) {
             const int i = h * kWave + lane;
             const int k = kq0 + j;
             const double t0 = k > 0 ? (double)tt[k - 1] : 0.0;
             const Decay dk = d[k];
-            crossing_data(m, V0, I0, v_of(m, U, J), (double)tt[k] - t0, dk.A, dk.D, sh.crit[i], sh.hi[i],
-                          sh.fhi[i]);
-            sh.s0[i] = make_double2(V0, I0);
+            crossing_data(m, v.V0, v.I0, v.V1, (double)tt[k] - t0, dk.A, dk.D, sh.crit[i], sh.hi[i], sh.fhi[i]);
+            sh.s0[i] = make_double2(v.V0, v.I0);
             if (k == nb - 1) {
-                open_interval_data(m, v_of(m, U, J), J, m.t_end - (double)tt[k], sh.crit[kOpenIv], sh.hi[kOpenIv],
+                open_interval_data(m, v.V1, v.J1, m.t_end - (double)tt[k], sh.crit[kOpenIv], sh.hi[kOpenIv],
                                    sh.fhi[kOpenIv]);
-                sh.s0[kOpenIv] = make_double2(v_of(m, U, J), J);
+                sh.s0[kOpenIv] = make_double2(v.V1, v.J1);
             }
         }
     }
@@ -1426,12 +1450,14 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     default: launch_walks<1>(L, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, status, stream); break;
     }
     {
-        // blocks per sample: enough for the pool slice at 16 records per block, at most 64
+        // 16 blocks of 4 waves per sample (256 records per round), fewer
+        // when the pool slice is smaller; the blocks loop over the records
         const size_t per = (L.pool_cap + 15) / 16;
-        const unsigned bx = (unsigned)(per < 1 ? 1 : (per > 64 ? 64 : per));
+        const unsigned bx = (unsigned)(per < 1 ? 1 : (per > 16 ? 16 : per));
         if (B > 0)
-            TIMED_LAUNCH("intervals", k_intervals, dim3(bx, (unsigned)B), dim3(256), 0, stream,
-                         ev_t, ev_n, E_max, L.E_pad, m, P.dec, P.pool, P.pool_count, (uint32_t)L.pool_cap);
+            TIMED_LAUNCH("records", k_records, dim3(bx, (unsigned)B), dim3(256), 0, stream,
+                         ev_t, ev_src, ev_n, E_max, L.E_pad, L.S, WT, C_in, N, m, P.dec, P.ent, P.pool, P.pool_count,
+                         (uint32_t)L.pool_cap);
     }
     // Single-wave workgroups over the concatenated per-sample lists.
     const unsigned rgrid = (unsigned)(nn < 4096 ? nn : 4096);
