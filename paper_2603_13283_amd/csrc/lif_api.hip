@@ -46,6 +46,12 @@ Model make_model(const lif_params& p)
     m.f_th = (float)m.th;
     m.f_inv_tm = (float)m.inv_tm;
     m.reg = p.solver_reg;
+    // tau_m / tau_s = p + 1 exactly for an integer 1 <= p <= 4: the
+    // spike-time solve works on a polynomial (root_poly)
+    m.p_int = 0;
+    for (int q = 1; q <= 4; ++q)
+        if (p.tau_mem / p.tau_syn == (double)(q + 1)) m.p_int = q;
+    if (const char* env = getenv("LIF_ROOT_GENERAL")) if (atoi(env)) m.p_int = 0;
     m.s_max = p.s_max;
     m.flags = p.flags;
     return m;

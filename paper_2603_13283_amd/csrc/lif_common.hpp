@@ -38,6 +38,7 @@ struct Model {
     double dth;        // th - vr: the drop of V at a reset
     double reg;        // backward floor on dV/dt
     float f_th, f_inv_tm;   // float32 copies for screening
+    int p_int;         // p when tau_m / tau_s = p + 1 exactly for an integer 1 <= p <= 4, else 0
     int s_max;
     uint32_t flags;
 };
@@ -231,6 +232,94 @@ __device__ __forceinline__ double root_h(const Model& m, double c0, double kI, d
     *E2o = E2;
     if (iters) *iters += it;
     return u;
+}
+
+// Spike time when tau_m / tau_s = p + 1 for an integer 1 <= p <= 4 (the
+// paper's 20 ms / 5 ms gives p = 3).  With y = e^{-u/tm} the two
+// exponentials of F become powers of y: e^{u/tm} = 1/y and e^{-u r} = y^p, so
+//   P(y) = -y F(u) = kI y^{p+1} - c0 y + th
+// is a polynomial.  A crossing interval has kI > 0, where P is convex in
+// y > 0; its first root in u is the largest root in y, and P(ylo) =
+// -ylo F(lo) > 0 at the bracket end ylo = e^{-lo/tm}, so Newton steps from
+// ylo decrease monotonically onto that root.  Four float32 steps (hardware
+// reciprocal) bring y near float32 resolution, float64 steps finish; no
+// exponential or logarithm is evaluated.  Returns false when an iteration
+// leaves this pattern (non-increasing P, no convergence), which exact
+// arithmetic excludes; the caller then takes root_h.
+template <int P, typename T>
+__device__ __forceinline__ T ipow(T y)
+{
+    T r = y;
+#pragma unroll
+    for (int i = 1; i < P; ++i) r *= y;
+    return r;
+}
+
+template <int P>
+__device__ __forceinline__ bool root_poly(const Model& m, double c0, double kI, double ylo, double& y_out)
+{
+    {
+        const float c0f = (float)c0, kIf = (float)kI, thf = (float)m.th, kp1f = (float)(P + 1) * kIf;
+        float y = (float)ylo;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float yp = ipow<P>(y);
+            const float Pv = fmaf(kIf * yp, y, fmaf(-c0f, y, thf));
+            const float dP = fmaf(kp1f, yp, -c0f);
+            const float yn = y - Pv * __builtin_amdgcn_rcpf(dP);
+            y = (dP > 0.0f && yn > 0.0f && yn < y) ? yn : y;
+        }
+        // the float32 iterate may sit a rounding step left of the root;
+        // the float64 steps below converge from either side
+        y_out = (double)y;
+    }
+    const double kp1 = (double)(P + 1) * kI;
+    double y = y_out;
+#pragma unroll 1
+    for (int it = 0; it < 64; ++it) {
+        const double yp = ipow<P>(y);
+        const double Pv = fma(kI * yp, y, fma(-c0, y, m.th));
+        const double dP = fma(kp1, yp, -c0);
+        if (!(dP > 0.0)) return false;
+        const double step = Pv * rcp_refined(dP);
+        y -= step;
+        if (!(y > 0.0 && y <= ylo)) return false;
+        if (fabs(step) <= 0x1p-48 * y) {     // quadratic convergence: the next step is below resolution
+            y_out = y;
+            return true;
+        }
+    }
+    return false;
+}
+
+// Spike inside a crossing interval (F(lo) = Flo < 0 <= F(hi) = Fhi, ylo =
+// e^{-lo/tm}): y = e^{-u/tm} at the spike time u, E1 = e^{u/tm},
+// E2 = e^{-u r}.  The spike time itself is u = -tm ln y.
+struct SpikeY {
+    double y, E1, E2;
+};
+
+__device__ __forceinline__ SpikeY solve_spike_y(const Model& m, double c0, double kI, double lo, double ylo, double Flo,
+                                                double hi, double Fhi)
+{
+    SpikeY r;
+    double y = 0.0;
+    bool ok = false;
+    switch (m.p_int) {
+    case 1: ok = root_poly<1>(m, c0, kI, ylo, y); if (ok) r.E2 = y; break;
+    case 2: ok = root_poly<2>(m, c0, kI, ylo, y); if (ok) r.E2 = ipow<2>(y); break;
+    case 3: ok = root_poly<3>(m, c0, kI, ylo, y); if (ok) r.E2 = ipow<3>(y); break;
+    case 4: ok = root_poly<4>(m, c0, kI, ylo, y); if (ok) r.E2 = ipow<4>(y); break;
+    default: break;
+    }
+    if (ok) {
+        r.y = y;
+        r.E1 = rcp_refined(y);
+    } else {
+        root_h(m, c0, kI, lo, Flo, hi, Fhi, &r.E1, &r.E2, nullptr);
+        r.y = rcp_refined(r.E1);
+    }
+    return r;
 }
 
 }  // namespace lif

@@ -690,7 +690,8 @@ struct ResolveLds {
     double crit[kWinIv + 1], hi[kWinIv + 1], fhi[kWinIv + 1];
     double2 s0[kWinIv + 1];                      // (V0, I0)
     double t0[kWinIv + 1];                       // interval start
-    float st[kWave], si[kWave];                  // spike buffer
+    double sp_t0[kWave], sp_y[kWave];            // spike buffer: interval start, e^{-u/tm}
+    float si[kWave];
 };
 
 // Crossing data of one interval of length L that starts in the no-reset
@@ -922,32 +923,25 @@ __device__ __forceinline__ void rebuild_window(ResolveLds& sh, const Model& m, i
     }
 }
 
-// Float32 screen of the deficit test D <= crit at an interval start t0 with
-// the deficit dref e^{-(t0 - tref)/tm} of the spikes so far: the hardware
-// exponential and the float32 products err by a few 1e-7 relative, far
-// inside the 1e-4 margin, so an interval that fails the screen cannot cross.
-__device__ __forceinline__ bool deficit_may_cross(int ns, double dref, double tref, double t0, double crit,
-                                                  const Model& m)
-{
-    if (ns == 0) return true;
-    const float D = (float)dref * __expf((float)(-(t0 - tref) * m.inv_tm));
-    return D <= (float)crit * 1.0001f;
-}
-
 // Status counts of one wave, added to the status words once per wave.
 struct ResolveStats {
     int walked, fallback, capped, spikes;
 };
 
-// Wave-uniform resolve state of one neuron.
+// Wave-uniform resolve state of one neuron: the reset deficit of the spikes
+// so far is D(t) = dref e^{-(t - tref)/tm} for t after the latest spike,
+// with tref the start of the interval that spike lies in (the deficit is
+// carried in that interval's frame, so no spike time is needed on the chain).
 struct Chain {
     int ns;              // spikes so far
-    double dref, tref;   // deficit right after the latest spike, its time
+    double dref, tref;
     bool capped;
 };
 
-// Spikes [from, to) from the LDS buffer to the outputs (coalesced).
-__device__ __forceinline__ void flush_spikes(ResolveLds& sh, int from, int to, float* __restrict__ st,
+// Spikes [from, to) from the LDS buffer to the outputs (coalesced); the
+// spike times t0 - tm ln y are taken here, 64 at a time, off the per-spike
+// chain.
+__device__ __forceinline__ void flush_spikes(ResolveLds& sh, const Model& m, int from, int to, float* __restrict__ st,
                                              float* __restrict__ si)
 {
     const int lane = (int)threadIdx.x;
@@ -955,14 +949,18 @@ __device__ __forceinline__ void flush_spikes(ResolveLds& sh, int from, int to, f
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     if (from + lane < to) {
-        st[from + lane] = sh.st[(from + lane) % kWave];
-        if (si) si[from + lane] = sh.si[(from + lane) % kWave];
+        const int q = (from + lane) % kWave;
+        st[from + lane] = (float)(sh.sp_t0[q] - m.tm * log(sh.sp_y[q]));
+        if (si) si[from + lane] = sh.si[q];
     }
     __builtin_amdgcn_wave_barrier();
 }
 
 // Rounds over one step (see the section comment): lane l takes window
-// interval i0 + l if l < nlanes.
+// interval i0 + l if l < nlanes.  Each lane holds the deficit Dl at its
+// interval's start; an interval crosses iff Dl <= crit.  The spike-time
+// solve of a round runs wave-uniform on the crossing interval's data
+// (broadcast from its lane), so its iterations branch on scalars.
 __device__ __forceinline__ void resolve_step(ResolveLds& sh, const Model& m, int i0, int nlanes, Chain& ch,
                                           float* __restrict__ st, float* __restrict__ si)
 {
@@ -970,47 +968,43 @@ __device__ __forceinline__ void resolve_step(ResolveLds& sh, const Model& m, int
     const int i = lane < nlanes ? i0 + lane : i0;
     const double crit = sh.crit[i];
     const double t0 = sh.t0[i];
-    bool pend = lane < nlanes && crit >= 0.0 && deficit_may_cross(ch.ns, ch.dref, ch.tref, t0, crit, m);
-    if (!__ballot(pend)) return;
+    double Dl = ch.ns > 0 ? ch.dref * exp(-(t0 - ch.tref) * m.inv_tm) : 0.0;
+    bool pend = lane < nlanes && crit >= 0.0 && Dl <= crit;
+    unsigned long long cm = __ballot(pend);
+    if (!cm) return;
     const double2 s0 = sh.s0[i];
     const double hi = sh.hi[i], fhi = sh.fhi[i];
-    double Dl = 0.0, lo = 0.0, Flo = 0.0;
-    if (pend) {
-        Dl = ch.ns > 0 ? ch.dref * exp(-(t0 - ch.tref) * m.inv_tm) : 0.0;
-        Flo = s0.x - m.th - Dl;
-    }
+    double ylo = 1.0;
     for (;;) {
-        const unsigned long long cm = __ballot(pend && Dl <= crit);
-        if (!cm) return;
         const int kl = __ffsll((long long)cm) - 1;
-        double tsp = 0.0, dnew = 0.0;
-        if (lane == kl) {
-            double E1, E2;
-            const double kI = m.kappa * s0.y;
-            const double u = root_h(m, s0.x - Dl + kI, kI, lo, Flo, hi, fhi - Dl, &E1, &E2, nullptr);
-            const double iE1 = rcp_refined(E1);
-            tsp = t0 + u;
-            sh.st[ch.ns % kWave] = (float)tsp;
-            sh.si[ch.ns % kWave] = (float)(s0.y * (E2 * iE1));
-            dnew = Dl * iE1 + m.dth;
-            // the same interval is tested again with the raised deficit
-            Dl += m.dth * E1;
-            lo = u;
-            Flo = -m.dth * E1;
+        const double V0k = rl_double(s0.x, kl), I0k = rl_double(s0.y, kl), Dk = rl_double(Dl, kl);
+        const double t0k = rl_double(t0, kl), hik = rl_double(hi, kl), fhik = rl_double(fhi, kl);
+        const double ylok = rl_double(ylo, kl);
+        const double kI = m.kappa * I0k;
+        // after a spike inside the interval the raised deficit keeps F < 0
+        // on all of [0, u], so the general solver may bracket from the
+        // interval start; the polynomial solver starts from the spike (ylo)
+        const SpikeY sp = solve_spike_y(m, V0k - Dk + kI, kI, 0.0, ylok, V0k - m.th - Dk, hik, fhik - Dk);
+        if (lane == 0) {
+            sh.sp_t0[ch.ns % kWave] = t0k;
+            sh.sp_y[ch.ns % kWave] = sp.y;
+            sh.si[ch.ns % kWave] = (float)(I0k * (sp.E2 * sp.y));
         }
+        // the deficit in interval kl's frame
+        const double Dnew = Dk + m.dth * sp.E1;
         ++ch.ns;
-        ch.dref = rl_double(dnew, kl);
-        ch.tref = rl_double(tsp, kl);
-        if (ch.ns % kWave == 0) flush_spikes(sh, ch.ns - kWave, ch.ns, st, si);
+        ch.dref = Dnew;
+        ch.tref = t0k;
+        if (ch.ns % kWave == 0) flush_spikes(sh, m, ch.ns - kWave, ch.ns, st, si);
         if (ch.ns >= m.s_max) { ch.capped = true; return; }
-        if (lane < kl) pend = false;
-        if (pend && lane > kl) {
-            pend = deficit_may_cross(ch.ns, ch.dref, ch.tref, t0, crit, m);
-            if (__ballot(pend) && pend) {
-                Dl = ch.dref * exp(-(t0 - ch.tref) * m.inv_tm);
-                Flo = s0.x - m.th - Dl;
-            }
-        }
+        // interval kl is tested again with the raised deficit (a second spike
+        // in it); later intervals take the new deficit; earlier ones are done
+        const double Dlater = Dnew * exp(-(t0 - t0k) * m.inv_tm);
+        Dl = lane == kl ? Dnew : Dlater;
+        ylo = lane == kl ? sp.y : ylo;
+        pend = pend && lane >= kl && Dl <= crit;
+        cm = __ballot(pend);
+        if (!cm) return;
     }
 }
 
@@ -1024,7 +1018,7 @@ __device__ void resolve_neuron(ResolveLds& sh, ResolveStats& acc, int b, int n, 
 {
     const int lane = (int)threadIdx.x;
     const int j = lane % kSub, r = lane / kSub;
-    const int nb = clamp_count(ev_n[b], E_max);
+    const int nb = __builtin_amdgcn_readfirstlane(clamp_count(ev_n[b], E_max));
     const float* tt = ev_t + (size_t)b * E_max;
     const int32_t* src = ev_src + (size_t)b * E_max;
     const Decay* d = dec + (size_t)b * E_pad;
@@ -1032,7 +1026,7 @@ __device__ void resolve_neuron(ResolveLds& sh, ResolveStats& acc, int b, int n, 
     float* st = out_t + idx * (size_t)m.s_max;
     float* si = out_i ? out_i + idx * (size_t)m.s_max : nullptr;
     const int Sb = (nb + kSeg - 1) / kSeg;
-    const bool has_open = nb > 0 && m.t_end > (double)tt[nb - 1];
+    const bool has_open = __builtin_amdgcn_readfirstlane(nb > 0 && m.t_end > (double)tt[max(nb - 1, 0)] ? 1 : 0) != 0;
 
     Chain ch{0, 0.0, 0.0, false};
     int walked = 0, fallback = 0;
@@ -1077,8 +1071,25 @@ __device__ void resolve_neuron(ResolveLds& sh, ResolveStats& acc, int b, int n, 
             // the open interval is taken after the window holding the sample's
             // last sub-block, when that sub-block is flagged (it is the last
             // candidate of the last chunk)
-            const uint32_t cwl = sh.cand[tot - 1];
+            const uint32_t cwl = (uint32_t)__builtin_amdgcn_readfirstlane((int)sh.cand[tot - 1]);
             const bool open_here = has_open && (seg0 + (int)(cwl >> 3)) * kSeg + (int)(cwl & 7u) * kSub + kSub >= nb;
+            if (open_here) {
+                // the open interval's data, from the last candidate's record
+                // (slot kOpenIv, which the windows do not overwrite)
+                const uint32_t slot = (uint32_t)__builtin_amdgcn_readfirstlane((int)sh.slot[tot - 1]);
+                const int kq0 = (seg0 + (int)(cwl >> 3)) * kSeg + (int)(cwl & 7u) * kSub;
+                const Record* rec = pool + (slot != kNoSlot ? slot : 0u);
+                const double oc = rec->crit[kSub], oh = rec->hi[kSub], of = rec->fhi[kSub];
+                const double2 os = rec->s[min(nb - kq0, kSub)];
+                const double ot = (double)tt[nb - 1];
+                if (lane == 0) {
+                    sh.crit[kOpenIv] = slot != kNoSlot ? oc : -1.0;
+                    sh.hi[kOpenIv] = oh;
+                    sh.fhi[kOpenIv] = of;
+                    sh.s0[kOpenIv] = os;
+                    sh.t0[kOpenIv] = ot;
+                }
+            }
             // ---- windows of kWinCand candidates: the next window's loads are
             // in flight (registers) while the current one (LDS) is resolved
             const int nwin = (tot + kWinCand - 1) / kWinCand;
@@ -1102,20 +1113,6 @@ __device__ void resolve_neuron(ResolveLds& sh, ResolveStats& acc, int b, int n, 
                     sh.t0[i] = kq0 + j > 0 ? (double)nx[h].tp : 0.0;
                 }
                 const bool last_win = wi == nwin - 1;
-                if (last_win && open_here && lane == 0) {
-                    // the open interval, from the last candidate's record
-                    const uint32_t slot = sh.slot[tot - 1];
-                    const int kq0 = (seg0 + (int)(cwl >> 3)) * kSeg + (int)(cwl & 7u) * kSub;
-                    sh.crit[kOpenIv] = -1.0;
-                    if (slot != kNoSlot) {
-                        const Record* rec = pool + slot;
-                        sh.crit[kOpenIv] = rec->crit[kSub];
-                        sh.hi[kOpenIv] = rec->hi[kSub];
-                        sh.fhi[kOpenIv] = rec->fhi[kSub];
-                        sh.s0[kOpenIv] = rec->s[nb - kq0];
-                    }
-                    sh.t0[kOpenIv] = (double)tt[nb - 1];
-                }
                 __syncthreads();
                 if (__ballot(sh.slot[min(c0 + lane / 2, tot - 1)] == kNoSlot))
                     rebuild_window(sh, m, c0, tot, seg0, b, n, nb, S, N, C_in, tt, src, d, WT, ent);
@@ -1137,7 +1134,7 @@ __device__ void resolve_neuron(ResolveLds& sh, ResolveStats& acc, int b, int n, 
         }
         __syncthreads();                              // the list is rewritten by the next chunk
     }
-    flush_spikes(sh, ch.ns - ch.ns % kWave, ch.ns, st, si);
+    flush_spikes(sh, m, ch.ns - ch.ns % kWave, ch.ns, st, si);
     if (lane == 0) out_n[idx] = ch.ns;
     acc.walked += walked;
     acc.fallback += fallback;
@@ -1193,7 +1190,9 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
         const int b = b0 + l;
         if (b0 >= B || l >= kWave || b >= B) break;
         const uint32_t before = l > 0 ? (uint32_t)__shfl((int)incl, l - 1, kWave) : base;
-        const uint32_t bn = work[(size_t)b * N + (w - before)];
+        // wave-uniform by construction; readfirstlane lets the compiler
+        // treat everything derived from it as uniform (scalar branches)
+        const uint32_t bn = (uint32_t)__builtin_amdgcn_readfirstlane((int)work[(size_t)b * N + (w - before)]);
         resolve_neuron(sh, acc, (int)(bn / (uint32_t)N), (int)(bn % (uint32_t)N), ev_t, ev_src, ev_n, E_max, WT,
                        C_in, N, E_pad, S, m, dec, ent, mask, slotmap, pool, out_t, out_n, out_i);
     }
@@ -1261,19 +1260,20 @@ __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_
         // no-crossing screen V0 + max(I0 - th, 0) L / tm >= th_lo (screen_value)
         if (L > 0.0 && V + (I > m.th ? (I - m.th) * (L * m.inv_tm) : 0.0) >= m.th_lo) {
             IntervalMax im = interval_max(m, V, I, V1, L, A, Dd);
-            double Dk = 0.0, lo = 0.0, Flo = V - m.th;
+            double Dk = 0.0, lo = 0.0, ylo = 1.0, Flo = V - m.th;
             const double kI = m.kappa * I;
             while (Dk * im.a <= im.g) {
-                double E1, E2;
-                double u = root_h(m, V - Dk + kI, kI, lo, Flo, im.hi, im.Fhi - Dk, &E1, &E2, nullptr);
+                const SpikeY sp = solve_spike_y(m, V - Dk + kI, kI, lo, ylo, Flo, im.hi, im.Fhi - Dk);
+                const double u = -m.tm * log(sp.y);
                 if (live) {
                     st[ns] = (float)(t_prev + u);
-                    if (si) si[ns] = (float)(I * (E2 / E1));
+                    if (si) si[ns] = (float)(I * (sp.E2 * sp.y));
                 }
                 ++ns;
-                Dk += m.dth * E1;
+                Dk += m.dth * sp.E1;
                 lo = u;
-                Flo = -m.dth * E1;
+                ylo = sp.y;
+                Flo = -m.dth * sp.E1;
                 if (ns >= m.s_max) { capped = true; break; }
             }
             V1 -= Dk * A;                               // true V at the end of the interval

@@ -229,3 +229,24 @@ def test_odd_neuron_count(env):
     cfg = W.random_small(32, B=2, C=40, N=77, n_events=500, T=0.3, gain=12.0)
     s = check(env, cfg.events, cfg.layers[0].WT, "odd-N", both=False)
     assert s["par"]["spikes"] > 0
+
+
+@pytest.mark.parametrize("general", [False, True])
+def test_spike_solver_paths(env, monkeypatch, general):
+    """tau_m / tau_s = 4 takes the polynomial spike-time solve; LIF_ROOT_GENERAL
+    forces the exponential Newton solve on the same bursting input (several
+    spikes per interval).  Both match the oracle."""
+    if general:
+        monkeypatch.setenv("LIF_ROOT_GENERAL", "1")
+    cfg = W.random_small(33, B=2, C=30, N=96, n_events=600, T=0.3, gain=20.0)
+    s = check(env, cfg.events, cfg.layers[0].WT, f"solver-{'general' if general else 'poly'}")
+    assert s["par"]["spikes"] > 50
+
+
+@pytest.mark.parametrize("ratio", [2.0, 3.0, 3.7, 5.0])
+def test_tau_ratios(env, ratio):
+    """tau_m / tau_s = 2, 3 and 5 take the polynomial solve with p = 1, 2, 4;
+    3.7 takes the exponential solve."""
+    cfg = W.random_small(34, B=2, C=30, N=70, n_events=500, T=0.3, gain=16.0)
+    s = check(env, cfg.events, cfg.layers[0].WT, f"ratio{ratio}", both=False, tau_mem=0.02, tau_syn=0.02 / ratio)
+    assert s["par"]["spikes"] > 0
