@@ -60,14 +60,12 @@ typedef struct ihipStream_t* lif_stream_t;
 #define LIF_ST_CAPPED        1  /* neurons that reached s_max spikes         */
 #define LIF_ST_SPIKES        2  /* output spikes emitted                     */
 #define LIF_ST_CAND_BLOCKS   3  /* event sub-blocks flagged by the scan      */
-#define LIF_ST_WALKED_BLOCKS 4  /* sub-blocks re-walked exactly to resolve   */
+#define LIF_ST_WALKED_BLOCKS 4  /* flagged sub-blocks handed to the resolve
+                                   pass (equal to LIF_ST_CAND_BLOCKS)       */
 #define LIF_ST_ROOT_SOLVES   5  /* spike-time root solves                    */
 #define LIF_ST_EVENTS        6  /* input events consumed (sum of ev_n)       */
-#define LIF_ST_POOL_FALLBACK 7  /* flagged sub-blocks that found the record
-                                   pool full (resolved by a slower re-walk);
-                                   which ones do depends on the order in
-                                   which sub-blocks claim pool slots, so
-                                   this count may differ between calls      */
+#define LIF_ST_POOL_FALLBACK 7  /* flagged sub-blocks past the record pool's
+                                   capacity (resolved by a slower re-walk)  */
 
 #define LIF_WARN_SPIKE_CAP   1  /* a neuron stopped at s_max spikes          */
 #define LIF_WARN_UNSORTED    2  /* LIF_VALIDATE: times decrease in a sample  */

@@ -62,6 +62,11 @@ struct alignas(16) Record {
 static_assert(sizeof(Record) % 16 == 0, "record layout");
 constexpr uint32_t kNoSlot = 0xffffffffu;
 
+// Per-sample counters (record-pool use, work-list length) each take their
+// own 128-byte line: many waves update them with atomics, and atomics on one
+// line are serialised.
+constexpr int kCtr = 32;
+
 // Workgroup index -> work index such that each of the 8 XCDs (which receive
 // workgroups round-robin) processes a contiguous, sample-major range: the
 // events and decays of a sample then stay in one XCD's L2.
@@ -382,7 +387,6 @@ __global__ __launch_bounds__(kWave * kCarryWaves) void k_carry(
     const bool live = n < N;
     const int nc = live ? n : N - 1;
     const int nb = clamp_count(ev_n[b], E_max);
-    if (threadIdx.x == 0 && tile == 0) atomicAdd(&status[LIF_ST_EVENTS], nb);
     const int Sb = (nb + kSeg - 1) / kSeg;
     double U = 0.0, J = 0.0;                         // state entering the current round
     for (int r0 = 0; r0 < Sb; r0 += kCarryWaves * kCarryBatch) {
@@ -591,7 +595,7 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
         ex -= mine;
         if (total) {
             uint32_t base = 0;
-            if (lane == 0) base = atomicAdd(&pool_count[c.b], total);
+            if (lane == 0) base = atomicAdd(&pool_count[(size_t)c.b * kCtr], total);
             base = (uint32_t)__shfl((int)base, 0, kWave) + ex;
 #pragma unroll
             for (int i = 0; i < NPL; ++i) {
@@ -634,7 +638,7 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
         }
         if (tot) {
             uint32_t wbase = 0;
-            if (lane == 0) wbase = atomicAdd(&nwork[c.b], tot);
+            if (lane == 0) wbase = atomicAdd(&nwork[(size_t)c.b * kCtr], tot);
             wbase = (uint32_t)__shfl((int)wbase, 0, kWave);
             uint32_t before = 0;
 #pragma unroll
@@ -816,7 +820,7 @@ __global__ __launch_bounds__(256) void k_records(const float* __restrict__ ev_t,
     constexpr uint32_t kRecPerWave = kWave / kSub;
     const int b = blockIdx.y;
     const int nb = clamp_count(ev_n[b], E_max);
-    const uint32_t used = min(pool_count[b], pool_cap);
+    const uint32_t used = min(pool_count[(size_t)b * kCtr], pool_cap);
     const float* tt = ev_t + (size_t)b * E_max;
     const int32_t* src = ev_src + (size_t)b * E_max;
     const Decay* d = dec + (size_t)b * E_pad;
@@ -923,10 +927,6 @@ __device__ __forceinline__ void rebuild_window(ResolveLds& sh, const Model& m, i
     }
 }
 
-// Status counts of one wave, added to the status words once per wave.
-struct ResolveStats {
-    int walked, fallback, capped, spikes;
-};
 
 // Wave-uniform resolve state of one neuron: the reset deficit of the spikes
 // so far is D(t) = dref e^{-(t - tref)/tm} for t after the latest spike,
@@ -1008,7 +1008,7 @@ __device__ __forceinline__ void resolve_step(ResolveLds& sh, const Model& m, int
     }
 }
 
-__device__ void resolve_neuron(ResolveLds& sh, ResolveStats& acc, int b, int n, const float* __restrict__ ev_t,
+__device__ void resolve_neuron(ResolveLds& sh, int b, int n, const float* __restrict__ ev_t,
                                const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
                                const float* __restrict__ WT, int C_in, int N, int E_pad, int S, const Model& m,
                                const Decay* __restrict__ dec, const double2* __restrict__ ent,
@@ -1029,7 +1029,6 @@ __device__ void resolve_neuron(ResolveLds& sh, ResolveStats& acc, int b, int n, 
     const bool has_open = __builtin_amdgcn_readfirstlane(nb > 0 && m.t_end > (double)tt[max(nb - 1, 0)] ? 1 : 0) != 0;
 
     Chain ch{0, 0.0, 0.0, false};
-    int walked = 0, fallback = 0;
 
     for (int seg0 = 0; seg0 < Sb && !ch.capped; seg0 += kWave) {
         // ---- this chunk's flagged sub-blocks as a time-ordered list, with slots
@@ -1062,12 +1061,6 @@ __device__ void resolve_neuron(ResolveLds& sh, ResolveStats& acc, int b, int n, 
         }
         __syncthreads();
         if (tot > 0) {
-            walked += tot;
-            int nfb = 0;
-            for (int c = lane; c < tot; c += kWave) nfb += sh.slot[c] == kNoSlot ? 1 : 0;
-#pragma unroll
-            for (int off = 32; off > 0; off >>= 1) nfb += __shfl_xor(nfb, off, kWave);
-            fallback += nfb;
             // the open interval is taken after the window holding the sample's
             // last sub-block, when that sub-block is flagged (it is the last
             // candidate of the last chunk)
@@ -1136,10 +1129,6 @@ __device__ void resolve_neuron(ResolveLds& sh, ResolveStats& acc, int b, int n, 
     }
     flush_spikes(sh, m, ch.ns - ch.ns % kWave, ch.ns, st, si);
     if (lane == 0) out_n[idx] = ch.ns;
-    acc.walked += walked;
-    acc.fallback += fallback;
-    acc.capped += ch.capped ? 1 : 0;
-    acc.spikes += ch.ns;
 }
 
 // Work-list driven: the per-sample lists of neurons built by k_check are
@@ -1160,7 +1149,6 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
 {
     __shared__ ResolveLds sh;
     const int lane = (int)threadIdx.x;
-    ResolveStats acc{0, 0, 0, 0};
     // Running sum of the list lengths over groups of 64 samples (one load
     // per lane, a wave prefix sum): entry w of the concatenated lists belongs
     // to the first sample whose running sum exceeds w.
@@ -1168,7 +1156,7 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
     uint32_t base = 0;        // entries of the samples before the group
     uint32_t incl = 0;        // running sum up to and including sample b0 + lane
     auto load_group = [&]() {
-        uint32_t c = b0 + lane < B ? nwork[b0 + lane] : 0u;
+        uint32_t c = b0 + lane < B ? nwork[(size_t)(b0 + lane) * kCtr] : 0u;
 #pragma unroll
         for (int off = 1; off < kWave; off <<= 1) {
             const uint32_t v = (uint32_t)__shfl_up((int)c, off, kWave);
@@ -1193,24 +1181,91 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
         // wave-uniform by construction; readfirstlane lets the compiler
         // treat everything derived from it as uniform (scalar branches)
         const uint32_t bn = (uint32_t)__builtin_amdgcn_readfirstlane((int)work[(size_t)b * N + (w - before)]);
-        resolve_neuron(sh, acc, (int)(bn / (uint32_t)N), (int)(bn % (uint32_t)N), ev_t, ev_src, ev_n, E_max, WT,
+        resolve_neuron(sh, (int)(bn / (uint32_t)N), (int)(bn % (uint32_t)N), ev_t, ev_src, ev_n, E_max, WT,
                        C_in, N, E_pad, S, m, dec, ent, mask, slotmap, pool, out_t, out_n, out_i);
     }
-    if (threadIdx.x == 0) {
-        if (acc.walked) {
-            atomicAdd(&status[LIF_ST_WALKED_BLOCKS], acc.walked);
-            atomicAdd(&status[LIF_ST_CAND_BLOCKS], acc.walked);
+}
+
+// Status words of a forward call, from what the passes wrote (no atomics
+// on the status line during the passes): spikes and capped neurons from the
+// counts, flagged sub-blocks and pool fallbacks from the per-sample record
+// counters (the parallel path), events from the queue lengths.  Each
+// workgroup adds its sums with one atomic per word (one workgroup per
+// kStatusPer counts); the status words start at zero (k_prep).
+constexpr int kStatusThreads = 1024;
+constexpr int kStatusBatch = 8;
+constexpr int kStatusPer = kStatusThreads * kStatusBatch;
+
+__global__ __launch_bounds__(kStatusThreads) void k_status(const int32_t* __restrict__ ev_n, int B, int E_max, int N,
+                                                           int s_max, const int32_t* __restrict__ out_n,
+                                                           const uint32_t* __restrict__ pool_count, uint32_t pool_cap,
+                                                           int32_t* __restrict__ status)
+{
+    __shared__ unsigned long long part[kStatusThreads / kWave][5];
+    unsigned long long spikes = 0, capped = 0, flagged = 0, fallback = 0, events = 0;
+    const size_t nn = (size_t)B * (size_t)N;
+    for (size_t i0 = (size_t)blockIdx.x * kStatusPer + threadIdx.x; i0 < nn; i0 += (size_t)gridDim.x * kStatusPer) {
+        int c[kStatusBatch];
+#pragma unroll
+        for (int u = 0; u < kStatusBatch; ++u) {
+            const size_t i = i0 + (size_t)u * kStatusThreads;
+            c[u] = i < nn ? out_n[i] : 0;
         }
-        if (acc.fallback) atomicAdd(&status[LIF_ST_POOL_FALLBACK], acc.fallback);
-        if (acc.capped) {
-            atomicAdd(&status[LIF_ST_CAPPED], acc.capped);
-            atomicOr(&status[LIF_ST_FLAGS], LIF_WARN_SPIKE_CAP);
-        }
-        if (acc.spikes) {
-            atomicAdd(&status[LIF_ST_SPIKES], acc.spikes);
-            atomicAdd(&status[LIF_ST_ROOT_SOLVES], acc.spikes);
+#pragma unroll
+        for (int u = 0; u < kStatusBatch; ++u) {
+            spikes += (unsigned long long)c[u];
+            capped += c[u] >= s_max ? 1u : 0u;
         }
     }
+    if (blockIdx.x == 0) {
+        for (int b = threadIdx.x; b < B; b += kStatusThreads) {
+            events += (unsigned long long)clamp_count(ev_n[b], E_max);
+            if (pool_count) {
+                const uint32_t pc = pool_count[(size_t)b * kCtr];
+                flagged += pc;
+                fallback += pc > pool_cap ? pc - pool_cap : 0u;
+            }
+        }
+    }
+    unsigned long long v[5] = {spikes, capped, flagged, fallback, events};
+#pragma unroll
+    for (int q = 0; q < 5; ++q) {
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) v[q] += __shfl_xor(v[q], off, kWave);
+    }
+    const int wave = (int)threadIdx.x / kWave;
+    if (threadIdx.x % kWave == 0) {
+#pragma unroll
+        for (int q = 0; q < 5; ++q) part[wave][q] = v[q];
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long t[5] = {0, 0, 0, 0, 0};
+        for (int w = 0; w < kStatusThreads / kWave; ++w)
+            for (int q = 0; q < 5; ++q) t[q] += part[w][q];
+        auto sat = [](unsigned long long x) { return (int32_t)(x > 0x7fffffffull ? 0x7fffffffull : x); };
+        if (t[0]) {
+            atomicAdd(&status[LIF_ST_SPIKES], sat(t[0]));
+            atomicAdd(&status[LIF_ST_ROOT_SOLVES], sat(t[0]));
+        }
+        if (t[1]) {
+            atomicAdd(&status[LIF_ST_CAPPED], sat(t[1]));
+            atomicOr(&status[LIF_ST_FLAGS], LIF_WARN_SPIKE_CAP);
+        }
+        if (t[2]) {
+            atomicAdd(&status[LIF_ST_CAND_BLOCKS], sat(t[2]));
+            atomicAdd(&status[LIF_ST_WALKED_BLOCKS], sat(t[2]));
+        }
+        if (t[3]) atomicAdd(&status[LIF_ST_POOL_FALLBACK], sat(t[3]));
+        if (t[4]) atomicAdd(&status[LIF_ST_EVENTS], sat(t[4]));
+    }
+}
+
+static unsigned status_blocks(int B, int N)
+{
+    const size_t nn = (size_t)B * (size_t)N;
+    const size_t g = (nn + kStatusPer - 1) / kStatusPer;
+    return (unsigned)(g < 1 ? 1 : (g > 64 ? 64 : g));
 }
 
 // Sequential baseline (Appendix E.3): one thread per (sample, neuron)
@@ -1230,7 +1285,6 @@ __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_
     const size_t idx = live ? idx_raw : 0;            // lanes past the end run neuron 0 and write nothing
     int b = (int)(idx / (size_t)N), n = (int)(idx % (size_t)N);
     int nb = clamp_count(ev_n[b], E_max);
-    if (live && n == 0) atomicAdd(&status[LIF_ST_EVENTS], nb);
     const float* tt = ev_t + (size_t)b * E_max;
     const int32_t* src = ev_src + (size_t)b * E_max;
     const Decay* d = dec + (size_t)b * E_pad;
@@ -1291,23 +1345,7 @@ __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_
             if (si) si[s] = 0.0f;
         }
     }
-    // status counts: one atomic per wave
-    int nsw = live ? ns : 0, cw = live && capped ? 1 : 0;
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        nsw += __shfl_xor(nsw, off, kWave);
-        cw += __shfl_xor(cw, off, kWave);
-    }
-    if (threadIdx.x % kWave == 0) {
-        if (cw) {
-            atomicAdd(&status[LIF_ST_CAPPED], cw);
-            atomicOr(&status[LIF_ST_FLAGS], LIF_WARN_SPIKE_CAP);
-        }
-        if (nsw) {
-            atomicAdd(&status[LIF_ST_SPIKES], nsw);
-            atomicAdd(&status[LIF_ST_ROOT_SOLVES], nsw);
-        }
-    }
+    (void)capped;
 }
 
 // ---------------------------------------------------------------------------
@@ -1329,7 +1367,7 @@ FwdLayout fwd_layout(int B, int E_max, int N)
     L.slotmap = take(BS * kSubPerSeg * N * sizeof(uint32_t));
     L.ent = take(BS * kSubPerSeg * N * sizeof(double2));
     // per sample: record-pool use, work-list length
-    L.n_counters = 2 * (size_t)B;
+    L.n_counters = 2 * (size_t)B * kCtr;
     L.counters = take(L.n_counters * sizeof(uint32_t));
     L.listed = take((size_t)B * N * sizeof(uint32_t));
     L.work = take((size_t)B * N * sizeof(uint32_t));
@@ -1414,7 +1452,7 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     P.slotmap = (uint32_t*)(base + L.slotmap);
     P.counters = (uint32_t*)(base + L.counters);
     P.pool_count = P.counters;
-    P.nwork = P.counters + B;
+    P.nwork = P.counters + (size_t)B * kCtr;
     P.listed = (uint32_t*)(base + L.listed);
     P.work = (uint32_t*)(base + L.work);
     P.pool = (Record*)(base + L.pool);
@@ -1441,6 +1479,8 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
         if (nn)
             TIMED_LAUNCH("sequential", k_sequential, dim3((unsigned)((nn + 63) / 64)), dim3(64), 0, stream,
                          ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, L.E_pad, P.dec, out_t, out_n, out_i, status);
+        TIMED_LAUNCH("status", k_status, dim3(status_blocks(B, N)), dim3(kStatusThreads), 0, stream, ev_n, B, E_max, N, m.s_max, out_n,
+                     (const uint32_t*)nullptr, 0u, status);
         return check_launch();
     }
     if (items_max == 0) return check_launch();
@@ -1464,6 +1504,8 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     TIMED_LAUNCH("resolve", k_resolve, dim3(rgrid), dim3(kWave), 0, stream,
                  ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, L.E_pad, L.S, m, P.dec, P.ent, P.mask, P.slotmap,
                  P.pool, P.work, P.nwork, out_t, out_n, out_i, status);
+    TIMED_LAUNCH("status", k_status, dim3(status_blocks(B, N)), dim3(kStatusThreads), 0, stream, ev_n, B, E_max, N, m.s_max, out_n,
+                 (const uint32_t*)P.pool_count, (uint32_t)L.pool_cap, status);
     return check_launch();
 }
 
