@@ -274,7 +274,7 @@ __device__ __forceinline__ bool root_poly(const Model& m, double c0, double kI, 
         y_out = (double)y;
     }
     const double kp1 = (double)(P + 1) * kI;
-    double y = y_out;
+    double y = y_out, prev = INFINITY;
 #pragma unroll 1
     for (int it = 0; it < 64; ++it) {
         const double yp = ipow<P>(y);
@@ -284,10 +284,15 @@ __device__ __forceinline__ bool root_poly(const Model& m, double c0, double kI, 
         const double step = Pv * rcp_refined(dP);
         y -= step;
         if (!(y > 0.0 && y <= ylo)) return false;
-        if (fabs(step) <= 0x1p-48 * y) {     // quadratic convergence: the next step is below resolution
+        // converged: a step below resolution, or a small step that is a tiny
+        // fraction of the one before it (quadratic convergence: the error
+        // left is about the square of that fraction)
+        const double as = fabs(step);
+        if (as <= 0x1p-48 * y || (as <= 0x1p-30 * y && as <= 0x1p-10 * prev)) {
             y_out = y;
             return true;
         }
+        prev = as;
     }
     return false;
 }
