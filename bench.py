@@ -34,7 +34,7 @@ def log(*a):
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_forward_700x256_b32.txt")
-KERNEL_SOURCES = ("lif_forward.hip", "lif_common.hpp", "lif_host.hpp")
+KERNEL_SOURCES = ("lif_forward.hip", "lif_common.hpp", "lif_host.hpp", "lif_walk.hpp")
 
 
 def kernel_sources_sha256() -> str:

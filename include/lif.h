@@ -50,6 +50,8 @@ typedef struct ihipStream_t* lif_stream_t;
 #define LIF_ERR_WORKSPACE  -4  /* ws_bytes below the *_workspace_size value  */
 #define LIF_ERR_HIP        -5  /* a kernel launch failed                     */
 #define LIF_ERR_SIZE       -6  /* a size exceeds a documented limit          */
+/* Size limits: C_in * N_out < 2^29 (W^T is addressed with 32-bit byte
+   offsets); B * E_max < 2^40. */
 
 /* lif_params.flags */
 #define LIF_VALIDATE  1u  /* check sorted times, finite values, source range */

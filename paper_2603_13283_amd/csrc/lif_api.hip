@@ -68,7 +68,8 @@ int validate_forward_args(const float* ev_t, const int32_t* ev_src, const int32_
     if (B > 0 && !ev_n) return LIF_ERR_ARG;
     if ((size_t)B * (size_t)E_max > 0 && (!ev_t || !ev_src)) return LIF_ERR_ARG;
     if ((size_t)B * (size_t)E_max >= ((size_t)1 << 40)) return LIF_ERR_SIZE;
-    if ((size_t)C_in * (size_t)N >= ((size_t)1 << 40)) return LIF_ERR_SIZE;
+    // the walks address W^T through a buffer descriptor with a 32-bit byte range
+    if ((size_t)C_in * (size_t)N >= ((size_t)1 << 29)) return LIF_ERR_SIZE;
     return LIF_OK;
 }
 

@@ -20,14 +20,17 @@
 // forward scan, P_{k-1} = M P_k + (spike injections in (t_{k-1}, t_k]),
 // which k_event_adjoint walks backwards per (sample, 64-neuron tile,
 // segment); each segment starts from the closed-form sums over the
-// (few) spikes that follow it, so segments are independent.
+// (few) spikes that follow it, so segments are independent.  The walk is
+// staged like the forward walks (decays and times in LDS, weights of the
+// next group of events in flight).
 #include "lif_common.hpp"
 #include "lif_host.hpp"
+#include "lif_walk.hpp"
 
 namespace lif {
 
 struct BwdLayout {
-    int S;
+    int S, E_pad;
     size_t dec, mu, last, gw, gt, total;
 };
 
@@ -35,9 +38,10 @@ static BwdLayout bwd_layout(int B, int E_max, int C_in, int N, int s_max)
 {
     BwdLayout L{};
     L.S = (E_max + kSeg - 1) / kSeg;
+    L.E_pad = L.S * kSeg;
     size_t off = 0;
     auto take = [&](size_t bytes) { size_t o = off; off += (bytes + 255) & ~(size_t)255; return o; };
-    L.dec = take((size_t)B * E_max * sizeof(Decay));
+    L.dec = take((size_t)B * L.E_pad * sizeof(Decay));
     L.mu = take((size_t)B * N * s_max * sizeof(double));
     L.last = take((size_t)B * N * sizeof(float));
     L.gw = take((size_t)C_in * N * sizeof(double));
@@ -46,20 +50,21 @@ static BwdLayout bwd_layout(int B, int E_max, int C_in, int N, int s_max)
     return L;
 }
 
+// Decays (A, D) per event, dec[B][E_pad]; identity past each sample's last
+// event, so that the walks stage whole segments.
 __global__ __launch_bounds__(256) void k_bwd_decay(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_n,
-                                                   int B, int E_max, Model m, Decay* __restrict__ dec)
+                                                   int B, int E_max, int E_pad, Model m, Decay* __restrict__ dec)
 {
     size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= (size_t)B * (size_t)E_max) return;
-    int b = (int)(idx / (size_t)E_max), k = (int)(idx % (size_t)E_max);
-    if (k >= clamp_count(ev_n[b], E_max)) return;
-    const float* t = ev_t + (size_t)b * E_max;
-    double dt = (double)t[k] - (k > 0 ? (double)t[k - 1] : 0.0);
-    Decay d;
-    d.A = exp(-dt * m.inv_tm);
-    d.D = exp(-dt * m.inv_ts);
-    d.C = 0.0;
-    d.lk = 0.0;
+    if (idx >= (size_t)B * (size_t)E_pad) return;
+    int b = (int)(idx / (size_t)E_pad), k = (int)(idx % (size_t)E_pad);
+    Decay d{1.0, 1.0, 0.0, 0.0};
+    if (k < clamp_count(ev_n[b], E_max)) {
+        const float* t = ev_t + (size_t)b * E_max;
+        double dt = (double)t[k] - (k > 0 ? (double)t[k - 1] : 0.0);
+        d.A = exp(-dt * m.inv_tm);
+        d.D = exp(-dt * m.inv_ts);
+    }
     dec[idx] = d;
 }
 
@@ -105,84 +110,128 @@ __global__ __launch_bounds__(256) void k_spike_adjoint(int B, int N, Model m, co
     last[idx] = ns > 0 ? ts[ns - 1] : -INFINITY;
 }
 
-__device__ __forceinline__ double wave_sum(double v)
+// Sums over the 64 lanes of 8 values per lane (one per event of a group):
+// a butterfly that halves the values each lane carries at the first three
+// steps (10 shuffles instead of 48).  Lane l ends with the sum for value
+// 4 [l & 32] + 2 [l & 16] + [l & 8] (complete on every lane).
+__device__ __forceinline__ double group_sum8(const double (&v)[kGrp], int lane)
 {
+    const bool u32 = (lane & 32) != 0, u16 = (lane & 16) != 0, u8 = (lane & 8) != 0;
+    double r4[4];
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
-    return v;
+    for (int q = 0; q < 4; ++q) {
+        const double keep = u32 ? v[q + 4] : v[q], send = u32 ? v[q] : v[q + 4];
+        r4[q] = keep + __shfl_xor(send, 32, kWave);
+    }
+    double r2[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const double keep = u16 ? r4[q + 2] : r4[q], send = u16 ? r4[q] : r4[q + 2];
+        r2[q] = keep + __shfl_xor(send, 16, kWave);
+    }
+    double r = (u8 ? r2[1] : r2[0]) + __shfl_xor(u8 ? r2[0] : r2[1], 8, kWave);
+    r += __shfl_xor(r, 4, kWave);
+    r += __shfl_xor(r, 2, kWave);
+    r += __shfl_xor(r, 1, kWave);
+    return r;
 }
 
-__global__ __launch_bounds__(64) void k_event_adjoint(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src,
-                                                      const int32_t* __restrict__ ev_n, int E_max,
-                                                      const float* __restrict__ WT, int C_in, int N, int tiles, int S,
-                                                      Model m, const Decay* __restrict__ dec,
-                                                      const float* __restrict__ out_t,
-                                                      const int32_t* __restrict__ out_n,
-                                                      const double* __restrict__ mu,
-                                                      const float* __restrict__ last, double* __restrict__ gWT,
-                                                      double* __restrict__ gT)
+// One wave per (sample, segment, 64-neuron tile), walking the segment's
+// events backwards: at event k, dL/dw += kappa (P^m - P^s) (one atomic per
+// live lane) and dL/dt_k += sum over lanes of w kappa (P^m/tm - P^s/ts)
+// (one atomic per event); then P decays to event k-1 and takes the spikes
+// in (t_{k-1}, t_k].  A lane is live while its neuron has a spike after
+// the event.
+__global__ __launch_bounds__(kWave * kWalkWaves) void k_event_adjoint(
+    const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
+    int E_pad, const float* __restrict__ WT, int C_in, int N, int tiles, int S, int items, Model m,
+    const Decay* __restrict__ dec, const float* __restrict__ out_t, const int32_t* __restrict__ out_n,
+    const double* __restrict__ mu, const float* __restrict__ last, double* __restrict__ gWT, double* __restrict__ gT)
 {
-    int lin = blockIdx.x;
-    int tile = lin % tiles;
-    int rest = lin / tiles;
-    int seg = rest % S;
-    int b = rest / S;
-    int nb = clamp_count(ev_n[b], E_max);
-    int k0 = seg * kSeg;
-    if (k0 >= nb) return;
-    int k1 = min(k0 + kSeg, nb);
-    int n = tile * kWave + (int)threadIdx.x;
-    bool act = n < N;
-    int nc = min(n, N - 1);
-    const float* tt = ev_t + (size_t)b * E_max;
-    // Only spikes after the segment's first event matter; skip the wave when
-    // no lane has one.
-    float tlast = act ? last[(size_t)b * N + nc] : -INFINITY;
-    bool live = tlast > tt[k0];
-    if (__ballot(live) == 0) return;
-    size_t base = ((size_t)b * N + nc) * (size_t)m.s_max;
+    __shared__ double2 s_ad[kWalkWaves][kSeg];
+    __shared__ float s_t[kWalkWaves][kSeg];
+    WalkCoords c;
+    if (!walk_coords<1>(items, tiles, S, ev_n, E_max, N, c)) return;
+    const int lane = c.lane;
+    const int wv = (int)threadIdx.x / kWave;
+    const int n = c.tile * kWave + lane;
+    const float* tt = ev_t + (size_t)c.b * E_max;
+    // only neurons with a spike after the segment's first event take part
+    const float tlast = c.live ? last[(size_t)c.b * N + n] : -INFINITY;
+    const bool liv = tlast > tt[c.k0];
+    if (__ballot(liv) == 0ull) return;
+    double2* lad = s_ad[wv];
+    float* lt = s_t[wv];
+    const Stage st = stage_segment(c, ev_src + (size_t)c.b * E_max + c.k0, dec + (size_t)c.b * E_pad + c.k0, WT,
+                                   C_in, N, lad, nullptr, nullptr);
+#pragma unroll
+    for (int h = 0; h < kSrcRegs; ++h) {
+        const int e = h * kWave + lane;
+        if (e < c.cnt) lt[e] = tt[c.k0 + e];
+    }
+    wave_lds_sync();
+    // closed-form P at the segment's last event: the spikes strictly later
+    const size_t base = ((size_t)c.b * N + c.n0) * (size_t)m.s_max;
     const float* ts = out_t + base;
     const double* mo = mu + base;
-    int ns = act ? min(out_n[(size_t)b * N + nc], m.s_max) : 0;
-    // Closed-form P at the last event of the segment: spikes strictly later.
-    double tk = (double)tt[k1 - 1];
+    const int ns = liv ? min(out_n[(size_t)c.b * N + c.n0], m.s_max) : 0;
+    const double tk = (double)lt[c.cnt - 1];
     double Pm = 0.0, Ps = 0.0;
-    int sp = ns;                 // spikes with index >= sp are later than the current event
-    if (live) {
-        while (sp > 0 && (double)ts[sp - 1] > tk) --sp;
-        for (int s = sp; s < ns; ++s) {
-            double u = (double)ts[s] - tk;
-            Pm += mo[s] * exp(-u * m.inv_tm);
-            Ps += mo[s] * exp(-u * m.inv_ts);
-        }
+    int sp = ns;                                 // spikes sp .. ns-1 are already in P
+    while (sp > 0 && (double)ts[sp - 1] > tk) --sp;
+    for (int q = sp; q < ns; ++q) {
+        const double u = (double)ts[q] - tk;
+        Pm += mo[q] * exp(-u * m.inv_tm);
+        Ps += mo[q] * exp(-u * m.inv_ts);
     }
-    const int32_t* src = ev_src + (size_t)b * E_max;
-    const Decay* d = dec + (size_t)b * E_max;
-    for (int k = k1 - 1; k >= k0; --k) {
-        int c = clamp_src(src[k], C_in);
-        float w = WT[(size_t)c * N + nc];
-        double a = m.kappa * (Pm - Ps);
-        if (live && a != 0.0) atomicAdd(&gWT[(size_t)c * N + n], a);
-        if (gT) {
-            double contrib = live ? (double)w * m.kappa * (Pm * m.inv_tm - Ps * m.inv_ts) : 0.0;
-            double tot = wave_sum(contrib);
-            if (threadIdx.x == 0 && tot != 0.0) atomicAdd(&gT[(size_t)b * E_max + k], tot);
-        }
-        if (k == k0) break;
-        // Step to event k-1: decay over the gap t_k - t_{k-1} and inject the
-        // spikes in (t_{k-1}, t_k].
-        Decay e = d[k];
-        Pm *= e.A;
-        Ps *= e.D;
-        if (live) {
-            double tp = (double)tt[k - 1];
-            while (sp > 0 && (double)ts[sp - 1] > tp) {
-                --sp;
-                double u = (double)ts[sp] - tp;
-                Pm += mo[sp] * exp(-u * m.inv_tm);
-                Ps += mo[sp] * exp(-u * m.inv_ts);
+    double tnext = sp > 0 ? (double)ts[sp - 1] : -INFINITY;   // the next spike to take, walking back
+    double mnext = sp > 0 ? mo[sp - 1] : 0.0;
+    const double kap = m.kappa;
+    double* gt = gT ? gT + (size_t)c.b * E_max + c.k0 : nullptr;
+    auto group = [&](int g, const float (&w)[kGrp][1]) {
+        double ca[kGrp];
+        const int oreg = g * kGrp < kWave ? st.off[0] : st.off[kSrcRegs - 1];
+#pragma unroll
+        for (int jj = kGrp - 1; jj >= 0; --jj) {
+            const int e = g * kGrp + jj;
+            ca[jj] = 0.0;
+            if (e >= c.cnt) continue;
+            const int roff = __builtin_amdgcn_readlane(oreg, e & (kWave - 1));
+            const double a = kap * (Pm - Ps);
+            if (liv && a != 0.0) atomicAdd(&gWT[(size_t)(roff >> 2) + (size_t)n], a);
+            if (gt && liv) ca[jj] = (double)w[jj][0] * kap * (Pm * m.inv_tm - Ps * m.inv_ts);
+            if (e > 0) {
+                const double2 ad = lad[e];
+                Pm *= ad.x;
+                Ps *= ad.y;
+                const double tp = (double)lt[e - 1];
+                while (tnext > tp) {
+                    const double u = tnext - tp;
+                    Pm += mnext * exp(-u * m.inv_tm);
+                    Ps += mnext * exp(-u * m.inv_ts);
+                    --sp;
+                    tnext = sp > 0 ? (double)ts[sp - 1] : -INFINITY;
+                    mnext = sp > 0 ? mo[sp - 1] : 0.0;
+                }
             }
         }
+        if (gt) {
+            const double r = group_sum8(ca, lane);
+            const int j = ((lane >> 5) & 1) * 4 + ((lane >> 4) & 1) * 2 + ((lane >> 3) & 1);
+            const int e = g * kGrp + j;
+            if ((lane & 7) == 0 && e < c.cnt && r != 0.0) atomicAdd(&gt[e], r);
+        }
+    };
+    // groups from the last backwards, the weights of the next one in flight
+    const int ng = (c.cnt + kGrp - 1) / kGrp;
+    float wa[kGrp][1], wb[kGrp][1];
+    load_grp<1>(st, (ng - 1) * kGrp, wa);
+    for (int g = ng - 1; g >= 0; g -= 2) {
+        if (g >= 1) load_grp<1>(st, (g - 1) * kGrp, wb);
+        group(g, wa);
+        if (g < 1) break;
+        if (g >= 2) load_grp<1>(st, (g - 2) * kGrp, wa);
+        group(g - 1, wb);
     }
 }
 
@@ -197,6 +246,7 @@ int backward_impl(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n,
     if (!WT || !out_t || !out_n || !out_i || !grad_out_t || !grad_WT || !ws) return LIF_ERR_ARG;
     if (B > 0 && !ev_n) return LIF_ERR_ARG;
     if ((size_t)B * (size_t)E_max > 0 && (!ev_t || !ev_src)) return LIF_ERR_ARG;
+    if ((size_t)C_in * (size_t)N >= ((size_t)1 << 29)) return LIF_ERR_SIZE;   // 32-bit W^T byte offsets
     BwdLayout L = bwd_layout(B, E_max, C_in, N, p->s_max);
     if (ws_bytes < L.total) return LIF_ERR_WORKSPACE;
     Model m = make_model(*p);
@@ -209,16 +259,18 @@ int backward_impl(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n,
     size_t nW = (size_t)C_in * N, nT = (size_t)B * E_max, nn = (size_t)B * N;
     TIMED_LAUNCH("bwd_zero", k_fill_zero, dim3(1024), dim3(256), 0, stream, gw, nW);
     if (gt && nT) TIMED_LAUNCH("bwd_zero", k_fill_zero, dim3(256), dim3(256), 0, stream, gt, nT);
-    if (nT) TIMED_LAUNCH("bwd_decay", k_bwd_decay, dim3((unsigned)((nT + 255) / 256)), dim3(256), 0, stream,
-                         ev_t, ev_n, B, E_max, m, dec);
+    const size_t nD = (size_t)B * L.E_pad;
+    if (nD) TIMED_LAUNCH("bwd_decay", k_bwd_decay, dim3((unsigned)((nD + 255) / 256)), dim3(256), 0, stream,
+                         ev_t, ev_n, B, E_max, L.E_pad, m, dec);
     if (nn) TIMED_LAUNCH("spike_adjoint", k_spike_adjoint, dim3((unsigned)((nn + 255) / 256)), dim3(256), 0,
                          stream, B, N, m, out_t, out_n, out_i, grad_out_t, mu, last);
-    int tiles = (N + kWave - 1) / kWave;
-    size_t total = (size_t)B * L.S * tiles;
-    if (total > 0x7fffffff) return LIF_ERR_SIZE;
-    if (total) TIMED_LAUNCH("event_adjoint", k_event_adjoint, dim3((unsigned)total), dim3(kWave), 0, stream,
-                            ev_t, ev_src, ev_n, E_max, WT, C_in, N, tiles, L.S, m, dec, out_t, out_n, mu, last, gw,
-                            gt);
+    const int tiles = (N + kWave - 1) / kWave;
+    const size_t items = (size_t)B * L.S * tiles;
+    if (items > 0x7fffffff) return LIF_ERR_SIZE;
+    const unsigned blocks = (unsigned)((items + kWalkWaves - 1) / kWalkWaves);
+    if (items) TIMED_LAUNCH("event_adjoint", k_event_adjoint, dim3(blocks), dim3(kWave * kWalkWaves), 0, stream,
+                            ev_t, ev_src, ev_n, E_max, L.E_pad, WT, C_in, N, tiles, L.S, (int)items, m, dec, out_t,
+                            out_n, mu, last, gw, gt);
     TIMED_LAUNCH("bwd_convert", k_to_float, dim3(1024), dim3(256), 0, stream, gw, grad_WT, nW);
     if (gt && nT) TIMED_LAUNCH("bwd_convert", k_to_float, dim3(256), dim3(256), 0, stream, gt, grad_ev_t, nT);
     return check_launch();

@@ -102,3 +102,14 @@ def test_library_missing_fails_loudly(tmp_path):
             mod.load(str(tmp_path / "nope.so"))
     finally:
         mod._lib = saved
+
+
+@pytest.mark.parametrize("fn", [L.lif_layer_forward, L.lif_layer_forward_sequential])
+def test_weight_matrix_size_limit(lib, fn):
+    """W^T is addressed with 32-bit byte offsets: C_in * N_out must stay below
+    2^29 (rejected on the host, forward and backward)."""
+    p = L.Params().c()
+    assert _fwd(fn, p, C=1 << 15, N=1 << 14) == L.LIF_ERR_SIZE
+    assert _fwd(fn, p, C=1 << 15, N=(1 << 14) - 1, ws_bytes=0) == L.LIF_ERR_WORKSPACE
+    bargs = [F, F, F, 2, 10, F, 1 << 15, 1 << 14, ctypes.byref(p), F, F, F, F, F, F, F, 10 ** 9, None]
+    assert L.lif_layer_backward(*bargs) == L.LIF_ERR_SIZE
