@@ -2,13 +2,12 @@
 //
 // Pipeline for one call (a sample is one sorted event queue, shared by the
 // N neurons of the layer):
-//   k_prep       per (sample, event): the affine map M(dt) of Eq. affine
-//                depends only on the gap to the previous event, so its
-//                entries are computed once per sample and shared by every
-//                neuron; per segment of kSeg events also the composed map
-//                (the maps form a semigroup, M(a) M(b) = M(a + b)).  Also
-//                resets the outputs, status words and counters.
-//   k_aggregate  per (sample, segment, tile of 64 NPL neurons): one wave walks
+//   k_aggregate  per (sample, segment, tile of 64 NPL neurons): the affine
+//                map M(dt) of Eq. affine depends only on the gap to the
+//                previous event, so the segment's maps are computed once per
+//                sample (the first tile's wave stores them, and the composed
+//                map of the segment: the maps form a semigroup,
+//                M(a) M(b) = M(a + b)) and shared by every neuron.  One wave walks
 //                the segment from the zero state in the eigen-coordinates
 //                (U, J) of the maps (two FMAs per neuron-event, the decays as
 //                scalar operands).  Lane l holds NPL adjacent neurons and
@@ -26,7 +25,8 @@
 //                sub-block stores its entering state and reserves a record.
 //   k_records    per reserved record (lanes are the sub-block's intervals):
 //                the no-reset states at every interval boundary of the
-//                sub-block and each interval's crossing data.
+//                sub-block and each interval's crossing data; also resets the
+//                outputs ahead of the resolve pass.
 //   k_resolve    per (sample, neuron) with flagged sub-blocks: walks only
 //                those, in time order.  Spikes found so far lower V by a
 //                known decaying amount (the reset deficit), which corrects
@@ -186,16 +186,44 @@ __device__ __forceinline__ void walk_grp(const double2* __restrict__ lad, int e0
 
 template <int NPL>
 __global__ __launch_bounds__(kWave * kWalkWaves) void k_aggregate(
-    const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max, int E_pad,
-    const float* __restrict__ WT, int C_in, int N, int tiles, int S, int items, const Decay* __restrict__ dec,
-    double2* __restrict__ agg)
+    const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
+    int E_pad, const float* __restrict__ WT, int C_in, int N, int tiles, int S, int items, Model m,
+    Decay* __restrict__ dec, double2* __restrict__ segm, double2* __restrict__ agg, int32_t* __restrict__ status,
+    uint32_t* __restrict__ counters, size_t n_counters, uint32_t* __restrict__ listed, size_t nn)
 {
+    {
+        // resets for the later passes: status words, per-sample counters,
+        // listed flags (grid-stride over every thread)
+        const size_t gt = (size_t)blockIdx.x * blockDim.x + threadIdx.x, gs = (size_t)gridDim.x * blockDim.x;
+        if (gt < LIF_STATUS_WORDS) status[gt] = 0;
+        for (size_t i = gt; i < n_counters; i += gs) counters[i] = 0u;
+        for (size_t i = gt; i < nn; i += gs) listed[i] = 0u;
+    }
     __shared__ double2 s_ad[kWalkWaves][kSeg];
     WalkCoords c;
     if (!walk_coords<NPL>(items, tiles, S, ev_n, E_max, N, c)) return;
     double2* lad = s_ad[threadIdx.x / kWave];
-    const Stage st = stage_segment(c, ev_src + (size_t)c.b * E_max + c.k0, dec + (size_t)c.b * E_pad + c.k0, WT,
-                                   C_in, N, lad, nullptr, nullptr);
+    // the decays of the segment's events (identity past the sample's last
+    // event); the first tile's wave stores them, and the segment's composed
+    // map, for the later passes
+    {
+        const float* tt = ev_t + (size_t)c.b * E_max;
+        Decay* dd = dec + (size_t)c.b * E_pad + c.k0;
+#pragma unroll
+        for (int h = 0; h < kSrcRegs; ++h) {
+            const int e = h * kWave + c.lane;
+            Decay dk{1.0, 1.0, 0.0, 0.0};
+            if (c.k0 + e < c.nb) dk = make_decay(m, tt, c.k0 + e);
+            lad[e] = make_double2(dk.A, dk.D);
+            if (c.tile == 0) dd[e] = dk;
+        }
+        if (c.tile == 0 && c.lane == 0) {
+            const double T = (double)tt[c.k0 + c.cnt - 1] - (c.k0 > 0 ? (double)tt[c.k0 - 1] : 0.0);
+            segm[(size_t)c.b * S + c.seg] = make_double2(exp(-T * m.inv_tm), exp(-T * m.inv_ts));
+        }
+    }
+    const Stage st = stage_segment(c, ev_src + (size_t)c.b * E_max + c.k0, nullptr, WT, C_in, N, lad, nullptr,
+                                   nullptr);
     double U[NPL], J[NPL];
 #pragma unroll
     for (int i = 0; i < NPL; ++i) U[i] = J[i] = 0.0;
@@ -664,8 +692,20 @@ __global__ __launch_bounds__(256) void k_records(const float* __restrict__ ev_t,
                                                  const float* __restrict__ WT, int C_in, int N, Model m,
                                                  const Decay* __restrict__ dec, const double2* __restrict__ ent,
                                                  Record* __restrict__ pool, const uint32_t* __restrict__ pool_count,
-                                                 uint32_t pool_cap)
+                                                 uint32_t pool_cap, int32_t* __restrict__ out_n, size_t nn,
+                                                 float* __restrict__ out_t, float* __restrict__ out_i, size_t n_out)
 {
+    {
+        // outputs reset ahead of the resolve pass (it writes only the
+        // neurons that fire): counts 0, times +inf, currents 0
+        const size_t gs = (size_t)gridDim.x * gridDim.y * blockDim.x;
+        const size_t gt = ((size_t)blockIdx.y * gridDim.x + blockIdx.x) * blockDim.x + threadIdx.x;
+        for (size_t i = gt; i < nn; i += gs) out_n[i] = 0;
+        for (size_t i = gt; i < n_out; i += gs) {
+            out_t[i] = INFINITY;
+            if (out_i) out_i[i] = 0.0f;
+        }
+    }
     const int lane = (int)threadIdx.x % kWave;
     const int j = lane % kSub;
     const uint32_t gw = (blockIdx.x * blockDim.x + threadIdx.x) / kWave;
@@ -1264,13 +1304,19 @@ struct FwdPtrs {
 template <int NPL>
 static void launch_walks(const FwdLayout& L, const FwdPtrs& P, const float* ev_t, const int32_t* ev_src,
                          const int32_t* ev_n, int B, int E_max, const float* WT, int C_in, int N, const Model& m,
-                         int32_t* status, hipStream_t stream)
+                         int32_t* status, bool validate, hipStream_t stream)
 {
     const int tiles = (N + kWave * NPL - 1) / (kWave * NPL);
     const size_t items = (size_t)B * L.S * tiles;
     const unsigned blocks = (unsigned)((items + kWalkWaves - 1) / kWalkWaves);
+    // the aggregate pass also computes the decays and resets the counters and
+    // status words (validation flags are ORed in after it)
     TIMED_LAUNCH("aggregate", k_aggregate<NPL>, dim3(blocks), dim3(kWave * kWalkWaves), 0, stream,
-                 ev_src, ev_n, E_max, L.E_pad, WT, C_in, N, tiles, L.S, (int)items, P.dec, P.agg);
+                 ev_t, ev_src, ev_n, E_max, L.E_pad, WT, C_in, N, tiles, L.S, (int)items, m, P.dec, P.segm, P.agg,
+                 status, P.counters, L.n_counters, P.listed, (size_t)B * N);
+    if (validate)
+        TIMED_LAUNCH("validate", k_validate, dim3((unsigned)(((size_t)B * E_max + 255) / 256)), dim3(256), 0,
+                     stream, ev_t, ev_src, ev_n, B, E_max, C_in, status);
     const int ctiles = (N + kWave - 1) / kWave;
     TIMED_LAUNCH("carry", k_carry, dim3((unsigned)((size_t)B * ctiles)), dim3(kWave * kCarryWaves), 0, stream,
                  ev_n, B, E_max, N, ctiles, L.S, P.segm, P.agg, P.carry, status);
@@ -1314,8 +1360,11 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     const size_t nn = (size_t)B * N;
     const size_t items_max = (size_t)B * L.S * ((N + kWave - 1) / kWave);
     if (items_max > 0x7fffffff || nn > 0xffffffffull) return LIF_ERR_SIZE;
-    {
-        const size_t n_out = nn * (size_t)p->s_max;
+    const size_t n_out = nn * (size_t)p->s_max;
+    const bool validate = (p->flags & LIF_VALIDATE) && (size_t)B * E_max;
+    if (sequential || items_max == 0) {
+        // decays and resets in their own pass (the parallel path folds them
+        // into the aggregate and record passes)
         size_t work_items = nev > n_out ? nev : n_out;
         size_t blocks = (work_items + 255) / 256;
         if (blocks > 2048) blocks = 2048;
@@ -1324,10 +1373,10 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
                      ev_t, ev_n, B, E_max, L.E_pad, L.S, m, P.dec, sequential ? nullptr : P.segm, status, P.counters,
                      L.n_counters, out_n, sequential ? nullptr : P.listed, nn, sequential ? nullptr : out_t, out_i,
                      n_out);
+        if (validate)
+            TIMED_LAUNCH("validate", k_validate, dim3((unsigned)(((size_t)B * E_max + 255) / 256)), dim3(256), 0,
+                         stream, ev_t, ev_src, ev_n, B, E_max, C_in, status);
     }
-    if ((p->flags & LIF_VALIDATE) && (size_t)B * E_max)
-        TIMED_LAUNCH("validate", k_validate, dim3((unsigned)(((size_t)B * E_max + 255) / 256)), dim3(256), 0,
-                     stream, ev_t, ev_src, ev_n, B, E_max, C_in, status);
     if (sequential) {
         if (nn)
             TIMED_LAUNCH("sequential", k_sequential, dim3((unsigned)((nn + 63) / 64)), dim3(64), 0, stream,
@@ -1338,9 +1387,9 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     }
     if (items_max == 0) return check_launch();
     switch (pick_npl(WT, N)) {
-    case 4: launch_walks<4>(L, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, status, stream); break;
-    case 2: launch_walks<2>(L, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, status, stream); break;
-    default: launch_walks<1>(L, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, status, stream); break;
+    case 4: launch_walks<4>(L, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, status, validate, stream); break;
+    case 2: launch_walks<2>(L, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, status, validate, stream); break;
+    default: launch_walks<1>(L, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, status, validate, stream); break;
     }
     {
         // 16 blocks of 4 waves per sample (256 records per round), fewer
@@ -1350,7 +1399,7 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
         if (B > 0)
             TIMED_LAUNCH("records", k_records, dim3(bx, (unsigned)B), dim3(256), 0, stream,
                          ev_t, ev_src, ev_n, E_max, L.E_pad, L.S, WT, C_in, N, m, P.dec, P.ent, P.pool, P.pool_count,
-                         (uint32_t)L.pool_cap);
+                         (uint32_t)L.pool_cap, out_n, nn, out_t, out_i, n_out);
     }
     // Single-wave workgroups over the concatenated per-sample lists.
     const unsigned rgrid = (unsigned)(nn < 4096 ? nn : 4096);

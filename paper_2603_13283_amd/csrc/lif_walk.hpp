@@ -115,9 +115,11 @@ __device__ __forceinline__ Stage stage_segment(const WalkCoords& c, const int32_
     for (int h = 0; h < kSrcRegs; ++h) {
         const int e = h * kWave + c.lane;
         st.off[h] = clamp_src(ss[min(e, c.cnt - 1)], C_in) * N * 4;
-        const Decay d = sd[e];
-        lad[e] = make_double2(d.A, d.D);
-        if (llk) llk[e] = d.lk;
+        if (sd) {                       // else the caller has filled lad
+            const Decay d = sd[e];
+            lad[e] = make_double2(d.A, d.D);
+            if (llk) llk[e] = d.lk;
+        }
     }
     wave_lds_sync();
     if (lgk) {
