@@ -50,70 +50,73 @@ static BwdLayout bwd_layout(int B, int E_max, int C_in, int N, int s_max)
     return L;
 }
 
-// Decays (A, D) per event, dec[B][E_pad]; identity past each sample's last
-// event, so that the walks stage whole segments.
-__global__ __launch_bounds__(256) void k_bwd_decay(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_n,
-                                                   int B, int E_max, int E_pad, Model m, Decay* __restrict__ dec)
+// Backward setup in one pass (grid-stride over every thread): the float64
+// accumulators of dL/dW and dL/dt set to zero; the decays (A, D) per event,
+// dec[B][E_pad], identity past each sample's last event (so that the walks
+// stage whole segments); and per (sample, neuron) the reverse recurrence
+// over its spikes:
+//   lambda_s = g_s - ((V_th - V_reset)/tm) sum_{s'' > s} mu_s'' e^{-(t_s'' - t_s)/tm}
+//   mu_s     = -lambda_s / max(dV/dt(t_s), reg)
+// with the time of its last spike (-inf when silent).
+__global__ __launch_bounds__(256) void k_bwd_setup(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_n,
+                                                   int B, int E_max, int E_pad, int N, Model m,
+                                                   Decay* __restrict__ dec, double* __restrict__ gw, size_t nW,
+                                                   double* __restrict__ gt, size_t nT,
+                                                   const float* __restrict__ out_t, const int32_t* __restrict__ out_n,
+                                                   const float* __restrict__ out_i,
+                                                   const float* __restrict__ grad_out_t, double* __restrict__ mu,
+                                                   float* __restrict__ last)
 {
-    size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= (size_t)B * (size_t)E_pad) return;
-    int b = (int)(idx / (size_t)E_pad), k = (int)(idx % (size_t)E_pad);
-    Decay d{1.0, 1.0, 0.0, 0.0};
-    if (k < clamp_count(ev_n[b], E_max)) {
-        const float* t = ev_t + (size_t)b * E_max;
-        double dt = (double)t[k] - (k > 0 ? (double)t[k - 1] : 0.0);
-        d.A = exp(-dt * m.inv_tm);
-        d.D = exp(-dt * m.inv_ts);
+    const size_t gtid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const size_t gs = (size_t)gridDim.x * blockDim.x;
+    for (size_t i = gtid; i < nW; i += gs) gw[i] = 0.0;
+    if (gt)
+        for (size_t i = gtid; i < nT; i += gs) gt[i] = 0.0;
+    const size_t nD = (size_t)B * (size_t)E_pad;
+    for (size_t idx = gtid; idx < nD; idx += gs) {
+        const int b = (int)(idx / (size_t)E_pad), k = (int)(idx % (size_t)E_pad);
+        Decay d{1.0, 1.0, 0.0, 0.0};
+        if (k < clamp_count(ev_n[b], E_max)) {
+            const float* t = ev_t + (size_t)b * E_max;
+            const double dt = (double)t[k] - (k > 0 ? (double)t[k - 1] : 0.0);
+            d.A = exp(-dt * m.inv_tm);
+            d.D = exp(-dt * m.inv_ts);
+        }
+        dec[idx] = d;
     }
-    dec[idx] = d;
-}
-
-__global__ __launch_bounds__(256) void k_fill_zero(double* __restrict__ a, size_t n)
-{
-    size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    size_t stride = (size_t)gridDim.x * blockDim.x;
-    for (; i < n; i += stride) a[i] = 0.0;
-}
-
-// float64 accumulators -> float32 outputs.
-__global__ __launch_bounds__(256) void k_to_float(const double* __restrict__ a, float* __restrict__ out, size_t n)
-{
-    size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    size_t stride = (size_t)gridDim.x * blockDim.x;
-    for (; i < n; i += stride) out[i] = (float)a[i];
-}
-
-// Per (sample, neuron): reverse recurrence over its spikes.
-__global__ __launch_bounds__(256) void k_spike_adjoint(int B, int N, Model m, const float* __restrict__ out_t,
-                                                       const int32_t* __restrict__ out_n,
-                                                       const float* __restrict__ out_i,
-                                                       const float* __restrict__ grad_out_t,
-                                                       double* __restrict__ mu, float* __restrict__ last)
-{
-    size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= (size_t)B * (size_t)N) return;
-    int ns = min(out_n[idx], m.s_max);
-    const float* ts = out_t + idx * (size_t)m.s_max;
-    const float* is = out_i + idx * (size_t)m.s_max;
-    const float* g = grad_out_t + idx * (size_t)m.s_max;
-    double* mo = mu + idx * (size_t)m.s_max;
-    double Q = 0.0, mu_next = 0.0;
-    double jump = (m.th - m.vr) * m.inv_tm;
-    for (int s = ns - 1; s >= 0; --s) {
-        if (s + 1 < ns) Q = (Q + mu_next) * exp(-((double)ts[s + 1] - (double)ts[s]) * m.inv_tm);
-        double lam = (double)g[s] - jump * Q;
-        double vp = fmax(((double)is[s] - m.th) * m.inv_tm, m.reg);
-        double mu_s = vp > 0.0 ? -lam / vp : 0.0;
-        mo[s] = mu_s;
-        mu_next = mu_s;
+    const size_t nn = (size_t)B * (size_t)N;
+    const double jump = (m.th - m.vr) * m.inv_tm;
+    for (size_t idx = gtid; idx < nn; idx += gs) {
+        const int ns = min(out_n[idx], m.s_max);
+        const float* ts = out_t + idx * (size_t)m.s_max;
+        const float* is = out_i + idx * (size_t)m.s_max;
+        const float* g = grad_out_t + idx * (size_t)m.s_max;
+        double* mo = mu + idx * (size_t)m.s_max;
+        double Q = 0.0, mu_next = 0.0;
+        for (int s = ns - 1; s >= 0; --s) {
+            if (s + 1 < ns) Q = (Q + mu_next) * exp(-((double)ts[s + 1] - (double)ts[s]) * m.inv_tm);
+            const double lam = (double)g[s] - jump * Q;
+            const double vp = fmax(((double)is[s] - m.th) * m.inv_tm, m.reg);
+            const double mu_s = vp > 0.0 ? -lam / vp : 0.0;
+            mo[s] = mu_s;
+            mu_next = mu_s;
+        }
+        last[idx] = ns > 0 ? ts[ns - 1] : -INFINITY;
     }
-    last[idx] = ns > 0 ? ts[ns - 1] : -INFINITY;
 }
 
-// Sums over the 64 lanes of 8 values per lane (one per event of a group):
-// a butterfly that halves the values each lane carries at the first three
-// steps (10 shuffles instead of 48).  Lane l ends with the sum for value
-// 4 [l & 32] + 2 [l & 16] + [l & 8] (complete on every lane).
+// float64 accumulators -> float32 outputs (both gradients in one pass).
+__global__ __launch_bounds__(256) void k_bwd_convert(const double* __restrict__ gw, float* __restrict__ grad_WT,
+                                                     size_t nW, const double* __restrict__ gt,
+                                                     float* __restrict__ grad_ev_t, size_t nT)
+{
+    const size_t gtid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const size_t gs = (size_t)gridDim.x * blockDim.x;
+    for (size_t i = gtid; i < nW; i += gs) grad_WT[i] = (float)gw[i];
+    if (gt)
+        for (size_t i = gtid; i < nT; i += gs) grad_ev_t[i] = (float)gt[i];
+}
+
 __device__ __forceinline__ double group_sum8(const double (&v)[kGrp], int lane)
 {
     const bool u32 = (lane & 32) != 0, u16 = (lane & 16) != 0, u8 = (lane & 8) != 0;
@@ -257,13 +260,18 @@ int backward_impl(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n,
     double* gw = (double*)(base + L.gw);
     double* gt = grad_ev_t ? (double*)(base + L.gt) : nullptr;
     size_t nW = (size_t)C_in * N, nT = (size_t)B * E_max, nn = (size_t)B * N;
-    TIMED_LAUNCH("bwd_zero", k_fill_zero, dim3(1024), dim3(256), 0, stream, gw, nW);
-    if (gt && nT) TIMED_LAUNCH("bwd_zero", k_fill_zero, dim3(256), dim3(256), 0, stream, gt, nT);
     const size_t nD = (size_t)B * L.E_pad;
-    if (nD) TIMED_LAUNCH("bwd_decay", k_bwd_decay, dim3((unsigned)((nD + 255) / 256)), dim3(256), 0, stream,
-                         ev_t, ev_n, B, E_max, L.E_pad, m, dec);
-    if (nn) TIMED_LAUNCH("spike_adjoint", k_spike_adjoint, dim3((unsigned)((nn + 255) / 256)), dim3(256), 0,
-                         stream, B, N, m, out_t, out_n, out_i, grad_out_t, mu, last);
+    {
+        size_t work = nW;
+        if (gt && nT > work) work = nT;
+        if (nD > work) work = nD;
+        if (nn > work) work = nn;
+        size_t blocks = (work + 255) / 256;
+        if (blocks > 2048) blocks = 2048;
+        if (blocks < 1) blocks = 1;
+        TIMED_LAUNCH("bwd_setup", k_bwd_setup, dim3((unsigned)blocks), dim3(256), 0, stream, ev_t, ev_n, B, E_max,
+                     L.E_pad, N, m, dec, gw, nW, gt, nT, out_t, out_n, out_i, grad_out_t, mu, last);
+    }
     const int tiles = (N + kWave - 1) / kWave;
     const size_t items = (size_t)B * L.S * tiles;
     if (items > 0x7fffffff) return LIF_ERR_SIZE;
@@ -271,8 +279,7 @@ int backward_impl(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n,
     if (items) TIMED_LAUNCH("event_adjoint", k_event_adjoint, dim3(blocks), dim3(kWave * kWalkWaves), 0, stream,
                             ev_t, ev_src, ev_n, E_max, L.E_pad, WT, C_in, N, tiles, L.S, (int)items, m, dec, out_t,
                             out_n, mu, last, gw, gt);
-    TIMED_LAUNCH("bwd_convert", k_to_float, dim3(1024), dim3(256), 0, stream, gw, grad_WT, nW);
-    if (gt && nT) TIMED_LAUNCH("bwd_convert", k_to_float, dim3(256), dim3(256), 0, stream, gt, grad_ev_t, nT);
+    TIMED_LAUNCH("bwd_convert", k_bwd_convert, dim3(1024), dim3(256), 0, stream, gw, grad_WT, nW, gt, grad_ev_t, nT);
     return check_launch();
 }
 
