@@ -258,7 +258,7 @@ constexpr int kCarryBatch = 16;
 
 __global__ __launch_bounds__(kWave * kCarryWaves) void k_carry(
     const int32_t* __restrict__ ev_n, int B, int E_max, int N, int tiles, int S, const double2* __restrict__ segm,
-    const double2* __restrict__ agg, double2* __restrict__ carry, int32_t* __restrict__ status)
+    const double2* __restrict__ agg, double2* __restrict__ carry)
 {
     __shared__ double2 tot[kCarryWaves][kWave];      // range map b-part
     __shared__ double2 dec_tot[kCarryWaves];         // range map diagonal
@@ -1038,7 +1038,7 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
                                                    const Record* __restrict__ pool,
                                                    const uint32_t* __restrict__ work, const uint32_t* __restrict__ nwork,
                                                    float* __restrict__ out_t, int32_t* __restrict__ out_n,
-                                                   float* __restrict__ out_i, int32_t* __restrict__ status)
+                                                   float* __restrict__ out_i)
 {
     __shared__ ResolveLds sh;
     const int lane = (int)threadIdx.x;
@@ -1084,7 +1084,8 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
 // counts, flagged sub-blocks and pool fallbacks from the per-sample record
 // counters (the parallel path), events from the queue lengths.  Each
 // workgroup adds its sums with one atomic per word (one workgroup per
-// kStatusPer counts); the status words start at zero (k_prep).
+// kStatusPer counts); the status words start at zero (reset by the
+// aggregate pass, or by k_prep on the sequential path).
 constexpr int kStatusThreads = 1024;
 constexpr int kStatusBatch = 8;
 constexpr int kStatusPer = kStatusThreads * kStatusBatch;
@@ -1170,8 +1171,7 @@ __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_
                                                    const int32_t* __restrict__ ev_n, int B, int E_max,
                                                    const float* __restrict__ WT, int C_in, int N, Model m,
                                                    int E_pad, const Decay* __restrict__ dec, float* __restrict__ out_t,
-                                                   int32_t* __restrict__ out_n, float* __restrict__ out_i,
-                                                   int32_t* __restrict__ status)
+                                                   int32_t* __restrict__ out_n, float* __restrict__ out_i)
 {
     const size_t idx_raw = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     const bool live = idx_raw < (size_t)B * (size_t)N;
@@ -1238,7 +1238,6 @@ __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_
             if (si) si[s] = 0.0f;
         }
     }
-    (void)capped;
 }
 
 // ---------------------------------------------------------------------------
@@ -1319,7 +1318,7 @@ static void launch_walks(const FwdLayout& L, const FwdPtrs& P, const float* ev_t
                      stream, ev_t, ev_src, ev_n, B, E_max, C_in, status);
     const int ctiles = (N + kWave - 1) / kWave;
     TIMED_LAUNCH("carry", k_carry, dim3((unsigned)((size_t)B * ctiles)), dim3(kWave * kCarryWaves), 0, stream,
-                 ev_n, B, E_max, N, ctiles, L.S, P.segm, P.agg, P.carry, status);
+                 ev_n, B, E_max, N, ctiles, L.S, P.segm, P.agg, P.carry);
     // The check pass takes one neuron per lane whatever NPL the aggregate
     // uses: its screen and record state make wider lanes cost occupancy
     // (about 200 VGPRs at four neurons per lane against under 80 at one).
@@ -1380,7 +1379,7 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     if (sequential) {
         if (nn)
             TIMED_LAUNCH("sequential", k_sequential, dim3((unsigned)((nn + 63) / 64)), dim3(64), 0, stream,
-                         ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, L.E_pad, P.dec, out_t, out_n, out_i, status);
+                         ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, L.E_pad, P.dec, out_t, out_n, out_i);
         TIMED_LAUNCH("status", k_status, dim3(status_blocks(B, N)), dim3(kStatusThreads), 0, stream, ev_n, B, E_max, N, m.s_max, out_n,
                      (const uint32_t*)nullptr, 0u, status);
         return check_launch();
@@ -1405,7 +1404,7 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     const unsigned rgrid = (unsigned)(nn < 4096 ? nn : 4096);
     TIMED_LAUNCH("resolve", k_resolve, dim3(rgrid), dim3(kWave), 0, stream,
                  ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, L.E_pad, L.S, m, P.dec, P.ent, P.mask, P.slotmap,
-                 P.pool, P.work, P.nwork, out_t, out_n, out_i, status);
+                 P.pool, P.work, P.nwork, out_t, out_n, out_i);
     TIMED_LAUNCH("status", k_status, dim3(status_blocks(B, N)), dim3(kStatusThreads), 0, stream, ev_n, B, E_max, N, m.s_max, out_n,
                  (const uint32_t*)P.pool_count, (uint32_t)L.pool_cap, status);
     return check_launch();
