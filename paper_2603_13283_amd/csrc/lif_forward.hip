@@ -693,8 +693,35 @@ __global__ __launch_bounds__(256) void k_records(const float* __restrict__ ev_t,
                                                  const Decay* __restrict__ dec, const double2* __restrict__ ent,
                                                  Record* __restrict__ pool, const uint32_t* __restrict__ pool_count,
                                                  uint32_t pool_cap, int32_t* __restrict__ out_n, size_t nn,
-                                                 float* __restrict__ out_t, float* __restrict__ out_i, size_t n_out)
+                                                 float* __restrict__ out_t, float* __restrict__ out_i, size_t n_out,
+                                                 int B, int32_t* __restrict__ status)
 {
+    if (blockIdx.x == gridDim.x - 1 && blockIdx.y == gridDim.y - 1 && threadIdx.x >= blockDim.x - kWave) {
+        // status words fixed once the check pass has run (the only writer of
+        // these words in the call): events consumed, flagged sub-blocks,
+        // sub-blocks past the pool's capacity
+        const int l = (int)threadIdx.x % kWave;
+        unsigned long long ev = 0, fl = 0, fb = 0;
+        for (int bb = l; bb < B; bb += kWave) {
+            ev += (unsigned long long)clamp_count(ev_n[bb], E_max);
+            const uint32_t pc = pool_count[(size_t)bb * kCtr];
+            fl += pc;
+            fb += pc > pool_cap ? pc - pool_cap : 0u;
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+            ev += __shfl_xor(ev, off, kWave);
+            fl += __shfl_xor(fl, off, kWave);
+            fb += __shfl_xor(fb, off, kWave);
+        }
+        if (l == 0) {
+            auto sat = [](unsigned long long x) { return (int32_t)(x > 0x7fffffffull ? 0x7fffffffull : x); };
+            status[LIF_ST_EVENTS] = sat(ev);
+            status[LIF_ST_CAND_BLOCKS] = sat(fl);
+            status[LIF_ST_WALKED_BLOCKS] = sat(fl);
+            status[LIF_ST_POOL_FALLBACK] = sat(fb);
+        }
+    }
     {
         // outputs reset ahead of the resolve pass (it writes only the
         // neurons that fire): counts 0, times +inf, currents 0
@@ -901,7 +928,7 @@ __device__ __forceinline__ void resolve_step(ResolveLds& sh, const Model& m, int
     }
 }
 
-__device__ void resolve_neuron(ResolveLds& sh, int b, int n, const float* __restrict__ ev_t,
+__device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restrict__ ev_t,
                                const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
                                const float* __restrict__ WT, int C_in, int N, int E_pad, int S, const Model& m,
                                const Decay* __restrict__ dec, const double2* __restrict__ ent,
@@ -1022,6 +1049,7 @@ __device__ void resolve_neuron(ResolveLds& sh, int b, int n, const float* __rest
     }
     flush_spikes(sh, m, ch.ns - ch.ns % kWave, ch.ns, st, si);
     if (lane == 0) out_n[idx] = ch.ns;
+    return ch.ns;
 }
 
 // Work-list driven: the per-sample lists of neurons built by k_check are
@@ -1038,9 +1066,14 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
                                                    const Record* __restrict__ pool,
                                                    const uint32_t* __restrict__ work, const uint32_t* __restrict__ nwork,
                                                    float* __restrict__ out_t, int32_t* __restrict__ out_n,
-                                                   float* __restrict__ out_i)
+                                                   float* __restrict__ out_i, int32_t* __restrict__ status)
 {
     __shared__ ResolveLds sh;
+    // spikes and capped neurons of this workgroup's neurons, added to the
+    // status words once at its end (no-return atomics: the wave does not
+    // wait for them)
+    unsigned long long spikes = 0;
+    uint32_t capped = 0;
     const int lane = (int)threadIdx.x;
     // Running sum of the list lengths over groups of 64 samples (one load
     // per lane, a wave prefix sum): entry w of the concatenated lists belongs
@@ -1074,29 +1107,40 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
         // wave-uniform by construction; readfirstlane lets the compiler
         // treat everything derived from it as uniform (scalar branches)
         const uint32_t bn = (uint32_t)__builtin_amdgcn_readfirstlane((int)work[(size_t)b * N + (w - before)]);
-        resolve_neuron(sh, (int)(bn / (uint32_t)N), (int)(bn % (uint32_t)N), ev_t, ev_src, ev_n, E_max, WT,
-                       C_in, N, E_pad, S, m, dec, ent, mask, slotmap, pool, out_t, out_n, out_i);
+        const int ns = resolve_neuron(sh, (int)(bn / (uint32_t)N), (int)(bn % (uint32_t)N), ev_t, ev_src, ev_n,
+                                      E_max, WT, C_in, N, E_pad, S, m, dec, ent, mask, slotmap, pool, out_t, out_n,
+                                      out_i);
+        spikes += (unsigned long long)ns;
+        capped += ns >= m.s_max ? 1u : 0u;
+    }
+    if (lane == 0) {
+        const int32_t sp = (int32_t)(spikes > 0x7fffffffull ? 0x7fffffffull : spikes);
+        if (sp) {
+            atomicAdd(&status[LIF_ST_SPIKES], sp);
+            atomicAdd(&status[LIF_ST_ROOT_SOLVES], sp);
+        }
+        if (capped) {
+            atomicAdd(&status[LIF_ST_CAPPED], (int32_t)capped);
+            atomicOr(&status[LIF_ST_FLAGS], LIF_WARN_SPIKE_CAP);
+        }
     }
 }
 
-// Status words of a forward call, from what the passes wrote (no atomics
-// on the status line during the passes): spikes and capped neurons from the
-// counts, flagged sub-blocks and pool fallbacks from the per-sample record
-// counters (the parallel path), events from the queue lengths.  Each
-// workgroup adds its sums with one atomic per word (one workgroup per
-// kStatusPer counts); the status words start at zero (reset by the
-// aggregate pass, or by k_prep on the sequential path).
+// Status words of a sequential forward call, from what the pass wrote:
+// spikes and capped neurons from the counts, events from the queue lengths.
+// Each workgroup adds its sums with one atomic per word (one workgroup per
+// kStatusPer counts); the status words start at zero (reset by k_prep).  The
+// parallel path fills the same words inside its record and resolve passes.
 constexpr int kStatusThreads = 1024;
 constexpr int kStatusBatch = 8;
 constexpr int kStatusPer = kStatusThreads * kStatusBatch;
 
 __global__ __launch_bounds__(kStatusThreads) void k_status(const int32_t* __restrict__ ev_n, int B, int E_max, int N,
                                                            int s_max, const int32_t* __restrict__ out_n,
-                                                           const uint32_t* __restrict__ pool_count, uint32_t pool_cap,
                                                            int32_t* __restrict__ status)
 {
-    __shared__ unsigned long long part[kStatusThreads / kWave][5];
-    unsigned long long spikes = 0, capped = 0, flagged = 0, fallback = 0, events = 0;
+    __shared__ unsigned long long part[kStatusThreads / kWave][3];
+    unsigned long long spikes = 0, capped = 0, events = 0;
     const size_t nn = (size_t)B * (size_t)N;
     for (size_t i0 = (size_t)blockIdx.x * kStatusPer + threadIdx.x; i0 < nn; i0 += (size_t)gridDim.x * kStatusPer) {
         int c[kStatusBatch];
@@ -1112,31 +1156,25 @@ __global__ __launch_bounds__(kStatusThreads) void k_status(const int32_t* __rest
         }
     }
     if (blockIdx.x == 0) {
-        for (int b = threadIdx.x; b < B; b += kStatusThreads) {
+        for (int b = threadIdx.x; b < B; b += kStatusThreads)
             events += (unsigned long long)clamp_count(ev_n[b], E_max);
-            if (pool_count) {
-                const uint32_t pc = pool_count[(size_t)b * kCtr];
-                flagged += pc;
-                fallback += pc > pool_cap ? pc - pool_cap : 0u;
-            }
-        }
     }
-    unsigned long long v[5] = {spikes, capped, flagged, fallback, events};
+    unsigned long long v[3] = {spikes, capped, events};
 #pragma unroll
-    for (int q = 0; q < 5; ++q) {
+    for (int q = 0; q < 3; ++q) {
 #pragma unroll
         for (int off = 32; off > 0; off >>= 1) v[q] += __shfl_xor(v[q], off, kWave);
     }
     const int wave = (int)threadIdx.x / kWave;
     if (threadIdx.x % kWave == 0) {
 #pragma unroll
-        for (int q = 0; q < 5; ++q) part[wave][q] = v[q];
+        for (int q = 0; q < 3; ++q) part[wave][q] = v[q];
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        unsigned long long t[5] = {0, 0, 0, 0, 0};
+        unsigned long long t[3] = {0, 0, 0};
         for (int w = 0; w < kStatusThreads / kWave; ++w)
-            for (int q = 0; q < 5; ++q) t[q] += part[w][q];
+            for (int q = 0; q < 3; ++q) t[q] += part[w][q];
         auto sat = [](unsigned long long x) { return (int32_t)(x > 0x7fffffffull ? 0x7fffffffull : x); };
         if (t[0]) {
             atomicAdd(&status[LIF_ST_SPIKES], sat(t[0]));
@@ -1146,12 +1184,7 @@ __global__ __launch_bounds__(kStatusThreads) void k_status(const int32_t* __rest
             atomicAdd(&status[LIF_ST_CAPPED], sat(t[1]));
             atomicOr(&status[LIF_ST_FLAGS], LIF_WARN_SPIKE_CAP);
         }
-        if (t[2]) {
-            atomicAdd(&status[LIF_ST_CAND_BLOCKS], sat(t[2]));
-            atomicAdd(&status[LIF_ST_WALKED_BLOCKS], sat(t[2]));
-        }
-        if (t[3]) atomicAdd(&status[LIF_ST_POOL_FALLBACK], sat(t[3]));
-        if (t[4]) atomicAdd(&status[LIF_ST_EVENTS], sat(t[4]));
+        if (t[2]) atomicAdd(&status[LIF_ST_EVENTS], sat(t[2]));
     }
 }
 
@@ -1381,7 +1414,7 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
             TIMED_LAUNCH("sequential", k_sequential, dim3((unsigned)((nn + 63) / 64)), dim3(64), 0, stream,
                          ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, L.E_pad, P.dec, out_t, out_n, out_i);
         TIMED_LAUNCH("status", k_status, dim3(status_blocks(B, N)), dim3(kStatusThreads), 0, stream, ev_n, B, E_max, N, m.s_max, out_n,
-                     (const uint32_t*)nullptr, 0u, status);
+                     status);
         return check_launch();
     }
     if (items_max == 0) return check_launch();
@@ -1398,15 +1431,13 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
         if (B > 0)
             TIMED_LAUNCH("records", k_records, dim3(bx, (unsigned)B), dim3(256), 0, stream,
                          ev_t, ev_src, ev_n, E_max, L.E_pad, L.S, WT, C_in, N, m, P.dec, P.ent, P.pool, P.pool_count,
-                         (uint32_t)L.pool_cap, out_n, nn, out_t, out_i, n_out);
+                         (uint32_t)L.pool_cap, out_n, nn, out_t, out_i, n_out, B, status);
     }
     // Single-wave workgroups over the concatenated per-sample lists.
     const unsigned rgrid = (unsigned)(nn < 4096 ? nn : 4096);
     TIMED_LAUNCH("resolve", k_resolve, dim3(rgrid), dim3(kWave), 0, stream,
                  ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, L.E_pad, L.S, m, P.dec, P.ent, P.mask, P.slotmap,
-                 P.pool, P.work, P.nwork, out_t, out_n, out_i);
-    TIMED_LAUNCH("status", k_status, dim3(status_blocks(B, N)), dim3(kStatusThreads), 0, stream, ev_n, B, E_max, N, m.s_max, out_n,
-                 (const uint32_t*)P.pool_count, (uint32_t)L.pool_cap, status);
+                 P.pool, P.work, P.nwork, out_t, out_n, out_i, status);
     return check_launch();
 }
 
