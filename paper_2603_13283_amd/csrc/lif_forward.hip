@@ -381,15 +381,19 @@ __device__ __forceinline__ void screen_grp(const Model& m, const double2* __rest
 // (up to t_end).  A flagged (sub-block, neuron) stores its entering state
 // (U, J) in ent and sets a bit in the neuron's sub-block mask of the segment.
 // At the end of the item the wave reserves records for all its flagged
-// sub-blocks with one atomic on the sample's pool counter and writes their
-// headers and slots (kNoSlot past the pool capacity: the resolve pass then
-// rebuilds that sub-block's states from ent itself); the first segment to
-// flag a neuron appends it to the sample's work list.
+// sub-blocks with one atomic on the sample's pool counter, in lane order, so
+// that the records of one (segment, neuron) are consecutive: the mask word
+// of the pair holds the sub-block bits and the pool offset of its first
+// record, and the record of a flagged sub-block is that offset plus the
+// number of flagged sub-blocks before it (none past the pool capacity: the
+// resolve pass then rebuilds that sub-block's states from ent itself).  The
+// wave writes the records' headers; the first segment to flag a neuron
+// appends it to the sample's work list.
 __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
     const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
     int E_pad, const float* __restrict__ WT, int C_in, int N, int tiles, int S, int items, Model m,
     const Decay* __restrict__ dec, const double2* __restrict__ carry, double2* __restrict__ ent,
-    uint32_t* __restrict__ mask, uint32_t* __restrict__ slotmap, Record* __restrict__ pool,
+    uint2* __restrict__ mask, Record* __restrict__ pool,
     uint32_t* __restrict__ pool_count, uint32_t pool_cap, uint32_t* __restrict__ listed,
     uint32_t* __restrict__ work, uint32_t* __restrict__ nwork)
 // work: per-sample lists of the neurons with flagged sub-blocks (capacity N
@@ -456,10 +460,6 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
                 msk[i] |= 1u << q;
             }
     }
-    if (c.live) {
-#pragma unroll
-        for (int i = 0; i < NPL; ++i) mask[row + i] = msk[i];
-    }
     // Records of the wave's flagged sub-blocks: one reservation, slots in
     // lane order (exclusive prefix sum of the per-lane counts).
     {
@@ -474,27 +474,23 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
         }
         const uint32_t total = (uint32_t)__shfl((int)ex, kWave - 1, kWave);
         ex -= mine;
+        uint32_t base = 0;
         if (total) {
-            uint32_t base = 0;
             if (lane == 0) base = atomicAdd(&pool_count[(size_t)c.b * kCtr], total);
             base = (uint32_t)__shfl((int)base, 0, kWave) + ex;
+        }
 #pragma unroll
-            for (int i = 0; i < NPL; ++i) {
-                for (uint32_t mm = msk[i]; mm; mm &= mm - 1u) {
-                    const int q = __builtin_ctz(mm);
-                    const size_t srow = (((size_t)c.b * S + c.seg) * kSubPerSeg + q) * N + c.n0 + i;
-                    uint32_t slot = kNoSlot;
-                    if (base < pool_cap) {
-                        slot = (uint32_t)c.b * pool_cap + base;
-                        Record* r = pool + slot;
-                        const int kq0 = c.k0 + q * kSub;
-                        r->kq0 = kq0;
-                        r->cnt = min(kSub, c.nb - kq0);
-                        r->n = c.n0 + i;
-                    }
-                    slotmap[srow] = slot;
-                    ++base;
+        for (int i = 0; i < NPL; ++i) {
+            if (c.live) mask[row + i] = make_uint2(msk[i], base);
+            for (uint32_t mm = msk[i]; mm; mm &= mm - 1u) {
+                if (base < pool_cap) {
+                    Record* r = pool + ((size_t)c.b * pool_cap + base);
+                    const int kq0 = c.k0 + __builtin_ctz(mm) * kSub;
+                    r->kq0 = kq0;
+                    r->cnt = min(kSub, c.nb - kq0);
+                    r->n = c.n0 + i;
                 }
+                ++base;
             }
         }
     }
@@ -932,12 +928,15 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
                                const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
                                const float* __restrict__ WT, int C_in, int N, int E_pad, int S, const Model& m,
                                const Decay* __restrict__ dec, const double2* __restrict__ ent,
-                               const uint32_t* __restrict__ mask, const uint32_t* __restrict__ slotmap,
+                               const uint2* __restrict__ mask, uint32_t pool_cap,
                                const Record* __restrict__ pool, float* __restrict__ out_t, int32_t* __restrict__ out_n,
                                float* __restrict__ out_i)
 {
     const int lane = (int)threadIdx.x;
     const int j = lane % kSub, r = lane / kSub;
+    // the first chunk's mask words are loaded together with the event count
+    // (words past the sample's segments are dropped below)
+    uint2 mw = lane < S ? mask[((size_t)b * S + lane) * N + n] : make_uint2(0u, 0u);
     const int nb = __builtin_amdgcn_readfirstlane(clamp_count(ev_n[b], E_max));
     const float* tt = ev_t + (size_t)b * E_max;
     const int32_t* src = ev_src + (size_t)b * E_max;
@@ -953,7 +952,8 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
     for (int seg0 = 0; seg0 < Sb && !ch.capped; seg0 += kWave) {
         // ---- this chunk's flagged sub-blocks as a time-ordered list, with slots
         const int sj = seg0 + lane;
-        const uint32_t mv = sj < Sb ? mask[((size_t)b * S + sj) * N + n] : 0u;
+        if (seg0 > 0) mw = sj < Sb ? mask[((size_t)b * S + sj) * N + n] : make_uint2(0u, 0u);
+        const uint32_t mv = sj < Sb ? mw.x : 0u;
         const int pc = __popc(mv);
         int ex = pc;
 #pragma unroll
@@ -964,20 +964,16 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
         const int tot = rl_int(ex, kWave - 1);
         ex -= pc;
         {
-            uint32_t mm = mv;
+            // candidates and their record slots (consecutive per segment)
+            uint32_t mm = mv, rel = mw.y;
             int o = ex;
             while (mm) {
-                sh.cand[o++] = ((uint32_t)lane << 3) | (uint32_t)__builtin_ctz(mm);
+                sh.cand[o] = ((uint32_t)lane << 3) | (uint32_t)__builtin_ctz(mm);
+                sh.slot[o] = rel < pool_cap ? (uint32_t)b * pool_cap + rel : kNoSlot;
+                ++o;
+                ++rel;
                 mm &= mm - 1u;
             }
-        }
-        __syncthreads();
-        // record slots of the candidates: independent loads, kWave at a time
-        for (int c0 = 0; c0 < tot; c0 += kWave) {
-            const int c = min(c0 + lane, tot - 1);
-            const uint32_t cw = sh.cand[c];
-            const uint32_t sl = slotmap[(((size_t)b * S + seg0 + (cw >> 3)) * kSubPerSeg + (cw & 7u)) * N + n];
-            if (c0 + lane < tot) sh.slot[c] = sl;
         }
         __syncthreads();
         if (tot > 0) {
@@ -1061,8 +1057,7 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
                                                    const float* __restrict__ WT, int C_in, int N, int E_pad, int S,
                                                    Model m, const Decay* __restrict__ dec,
                                                    const double2* __restrict__ ent,
-                                                   const uint32_t* __restrict__ mask,
-                                                   const uint32_t* __restrict__ slotmap,
+                                                   const uint2* __restrict__ mask, uint32_t pool_cap,
                                                    const Record* __restrict__ pool,
                                                    const uint32_t* __restrict__ work, const uint32_t* __restrict__ nwork,
                                                    float* __restrict__ out_t, int32_t* __restrict__ out_n,
@@ -1108,7 +1103,7 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
         // treat everything derived from it as uniform (scalar branches)
         const uint32_t bn = (uint32_t)__builtin_amdgcn_readfirstlane((int)work[(size_t)b * N + (w - before)]);
         const int ns = resolve_neuron(sh, (int)(bn / (uint32_t)N), (int)(bn % (uint32_t)N), ev_t, ev_src, ev_n,
-                                      E_max, WT, C_in, N, E_pad, S, m, dec, ent, mask, slotmap, pool, out_t, out_n,
+                                      E_max, WT, C_in, N, E_pad, S, m, dec, ent, mask, pool_cap, pool, out_t, out_n,
                                       out_i);
         spikes += (unsigned long long)ns;
         capped += ns >= m.s_max ? 1u : 0u;
@@ -1288,8 +1283,7 @@ FwdLayout fwd_layout(int B, int E_max, int N)
     L.segm = take(BS * sizeof(double2));
     L.agg = take(BS * N * sizeof(double2));
     L.carry = take(BS * N * sizeof(double2));
-    L.mask = take(BS * N * sizeof(uint32_t));
-    L.slotmap = take(BS * kSubPerSeg * N * sizeof(uint32_t));
+    L.mask = take(BS * N * sizeof(uint2));
     L.ent = take(BS * kSubPerSeg * N * sizeof(double2));
     // per sample: record-pool use, work-list length
     L.n_counters = 2 * (size_t)B * kCtr;
@@ -1329,7 +1323,8 @@ static int pick_npl(const float* WT, int N)
 struct FwdPtrs {
     Decay* dec;
     double2 *segm, *agg, *carry, *ent;
-    uint32_t *mask, *slotmap, *counters, *pool_count, *nwork, *listed, *work;
+    uint2* mask;
+    uint32_t *counters, *pool_count, *nwork, *listed, *work;
     Record* pool;
 };
 
@@ -1360,7 +1355,7 @@ static void launch_walks(const FwdLayout& L, const FwdPtrs& P, const float* ev_t
     const unsigned cblocks = (unsigned)((citems + kWalkWaves - 1) / kWalkWaves);
     TIMED_LAUNCH("check", k_check, dim3(cblocks), dim3(kWave * kWalkWaves), 0, stream,
                  ev_t, ev_src, ev_n, E_max, L.E_pad, WT, C_in, N, ctl, L.S, (int)citems, m, P.dec, P.carry, P.ent,
-                 P.mask, P.slotmap, P.pool, P.pool_count, (uint32_t)L.pool_cap, P.listed, P.work, P.nwork);
+                 P.mask, P.pool, P.pool_count, (uint32_t)L.pool_cap, P.listed, P.work, P.nwork);
 }
 
 int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
@@ -1379,8 +1374,7 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     P.agg = (double2*)(base + L.agg);
     P.carry = (double2*)(base + L.carry);
     P.ent = (double2*)(base + L.ent);
-    P.mask = (uint32_t*)(base + L.mask);
-    P.slotmap = (uint32_t*)(base + L.slotmap);
+    P.mask = (uint2*)(base + L.mask);
     P.counters = (uint32_t*)(base + L.counters);
     P.pool_count = P.counters;
     P.nwork = P.counters + (size_t)B * kCtr;
@@ -1436,7 +1430,7 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     // Single-wave workgroups over the concatenated per-sample lists.
     const unsigned rgrid = (unsigned)(nn < 4096 ? nn : 4096);
     TIMED_LAUNCH("resolve", k_resolve, dim3(rgrid), dim3(kWave), 0, stream,
-                 ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, L.E_pad, L.S, m, P.dec, P.ent, P.mask, P.slotmap,
+                 ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, L.E_pad, L.S, m, P.dec, P.ent, P.mask, (uint32_t)L.pool_cap,
                  P.pool, P.work, P.nwork, out_t, out_n, out_i, status);
     return check_launch();
 }
