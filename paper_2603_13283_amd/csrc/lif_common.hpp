@@ -249,10 +249,14 @@ __device__ __forceinline__ double root_h(const Model& m, double c0, double kI, d
 template <int P, typename T>
 __device__ __forceinline__ T ipow(T y)
 {
-    T r = y;
+    if constexpr (P == 0) {
+        return T(1);
+    } else {
+        T r = y;
 #pragma unroll
-    for (int i = 1; i < P; ++i) r *= y;
-    return r;
+        for (int i = 1; i < P; ++i) r *= y;
+        return r;
+    }
 }
 
 template <int P>
@@ -274,25 +278,28 @@ __device__ __forceinline__ bool root_poly(const Model& m, double c0, double kI, 
         y_out = (double)y;
     }
     const double kp1 = (double)(P + 1) * kI;
-    double y = y_out, prev = INFINITY;
+    const double half_d2 = 0.5 * (double)(P * (P + 1)) * kI;   // P''(y) / 2 = half_d2 y^(P-1)
+    double y = y_out;
 #pragma unroll 1
     for (int it = 0; it < 64; ++it) {
-        const double yp = ipow<P>(y);
+        const double ym = ipow<P - 1>(y);
+        const double yp = ym * y;
         const double Pv = fma(kI * yp, y, fma(-c0, y, m.th));
         const double dP = fma(kp1, yp, -c0);
         if (!(dP > 0.0)) return false;
-        const double step = Pv * rcp_refined(dP);
+        const double rdP = rcp_refined(dP);
+        const double step = Pv * rdP;
         y -= step;
         if (!(y > 0.0 && y <= ylo)) return false;
-        // converged: a step below resolution, or a small step that is a tiny
-        // fraction of the one before it (quadratic convergence: the error
-        // left is about the square of that fraction)
+        // converged: the error left after a Newton step of size s is about
+        // P'' s^2 / (2 P') (Taylor's theorem), trusted once the step is
+        // small; it must lie below 2^-40 y (spike times and reset deficits
+        // then carry errors far below the float32 outputs' resolution)
         const double as = fabs(step);
-        if (as <= 0x1p-48 * y || (as <= 0x1p-30 * y && as <= 0x1p-10 * prev)) {
+        if (as <= 0x1p-48 * y || (as <= 0x1p-20 * y && half_d2 * ym * (as * as) * rdP <= 0x1p-40 * y)) {
             y_out = y;
             return true;
         }
-        prev = as;
     }
     return false;
 }
