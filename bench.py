@@ -178,8 +178,9 @@ def main():
     #   records: per record its entering state (16 B), the 16 weights, event
     #     times and decay records of its sub-block (4 + 4 + 32 B each) and the
     #     record written (17 x 40 B);
-    #   resolve: per walked sub-block its record (17 float64 pairs), the 17
-    #     event times and 16 decay pairs, plus 8 B per spike and 4 B per count.
+    #   resolve: per walked sub-block, for each of its 16 intervals, the
+    #     record's state and crossing data (16 + 24 B) and the interval's
+    #     start time (4 B); plus 8 B per spike and 4 B per count.
     S = (E + 127) // 128
     walked = status[4]
     alg = {"prep": B * S * 128 * 32 + total_ev * 4 + B * N * P.s_max * 8,
@@ -187,7 +188,7 @@ def main():
            "check": total_ev * (8 + 4 * N),
            "carry": B * S * N * 32,
            "records": walked * (16 + 16 * 40 + 17 * 40),
-           "resolve": walked * (17 * 16 + 17 * 4 + 16 * 16) + n_spikes * 8 + B * N * 4}
+           "resolve": walked * 16 * (16 + 24 + 4) + n_spikes * 8 + B * N * 4}
     kern_us = {k: v[0] / v[1] * 1e3 for k, v in kern.items()}
     dom_name = max(kern_us, key=kern_us.get)
     dom_us = kern_us[dom_name]
