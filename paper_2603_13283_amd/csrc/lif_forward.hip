@@ -529,14 +529,17 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
     }
 }
 // ---------------------------------------------------------------------------
-// Resolve pass: one wave per neuron that has flagged sub-blocks (a work list
-// built by the check pass).  Intervals outside flagged sub-blocks provably
-// hold no spike.  The flagged sub-blocks are taken in time order:
+// Resolve pass: one workgroup of two waves per neuron that has flagged
+// sub-blocks (a work list built by the check pass).  Intervals outside
+// flagged sub-blocks provably hold no spike.  The flagged sub-blocks are
+// taken in time order:
 //   * Candidate list: per 64 segments, the sub-block masks are compacted into
-//     a time-ordered list in LDS with one wave prefix sum, and the record
-//     slot of every candidate is looked up once.
-//   * Windows of kWinCand candidates are staged in LDS: the loads of the next
-//     window are in flight (registers) while the current one is resolved.
+//     a time-ordered list in LDS with one wave prefix sum, with the record
+//     slot of every candidate.
+//   * Windows of kWinCand candidates in two LDS buffers: the staging wave
+//     (wave 1) loads and commits window w + 1 into one buffer while the chain
+//     wave (wave 0) resolves window w from the other, so the loads and LDS
+//     writes of a window stay off the serial chain.  One barrier per window.
 //   * Steps of kWave / kSub = 4 candidates: lane l takes interval l % kSub of
 //     candidate l / kSub, so time order is lane order.  Each interval
 //     carries its crossing data (k_records): it crosses iff the reset
@@ -557,23 +560,30 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
 // ---------------------------------------------------------------------------
 constexpr int kCandCap = kWave * kSubPerSeg;     // candidates of 64 segments
 constexpr int kStep = kWave / kSub;              // candidates per step
-constexpr int kWinCand = 32;                     // candidates per window
+constexpr int kWinCand = 16;                     // candidates per window
 constexpr int kWinIv = kWinCand * kSub;          // intervals per window
 constexpr int kIvPerLane = kWinIv / kWave;       // window intervals staged by each lane
 constexpr int kWinSteps = kWinCand / kStep;
 constexpr int kOpenIv = kWinIv;                  // window slot of the open interval
 
-struct ResolveLds {
-    uint32_t cand[kCandCap];                     // (segment in chunk << 3) | sub-block
-    uint32_t slot[kCandCap];                     // record slot of each candidate (kNoSlot: none)
-    // the current window, interval i = candidate * kSub + j; slot kOpenIv:
-    // the open interval
+// One window, interval i = candidate * kSub + j; slot kOpenIv: the open
+// interval.
+struct WinBuf {
     double crit[kWinIv + 1], hi[kWinIv + 1], fhi[kWinIv + 1];
     double2 s0[kWinIv + 1];                      // (V0, I0)
     double t0[kWinIv + 1];                       // interval start
+};
+
+struct ResolveLds {
+    uint32_t cand[kCandCap];                     // (segment in chunk << 3) | sub-block
+    uint32_t slot[kCandCap];                     // record slot of each candidate (kNoSlot: none)
+    WinBuf win[2];
     double sp_t0[kWave], sp_y[kWave];            // spike buffer: interval start, e^{-u/tm}
     float si[kWave];
+    int ntot;                                    // candidates of the chunk (chain wave -> both)
+    int stop[2];                                 // capped after window w (slot w % 2)
 };
+constexpr int kResolveWaves = 2;
 
 // Crossing data of one interval of length L that starts in the no-reset
 // state (V0, I0) and ends with V1 (A, D: its decays): the interval reaches
@@ -809,12 +819,13 @@ __device__ __forceinline__ StageIv stage_load(const ResolveLds& sh, int c, int t
 // intervals from the sub-blocks' entering states (U, J) with subblock_walk,
 // as the record pass does, then the crossing data (and the open interval's,
 // on the lane of the sample's last event).
-__device__ __forceinline__ void rebuild_window(ResolveLds& sh, const Model& m, int c0, int tot, int seg0, int b, int n,
-                                            int nb, int S, int N, int C_in, const float* __restrict__ tt,
-                                            const int32_t* __restrict__ src, const Decay* __restrict__ d,
-                                            const float* __restrict__ WT, const double2* __restrict__ ent)
+__device__ __forceinline__ void rebuild_window(const ResolveLds& sh, WinBuf& w, const Model& m, int c0, int tot,
+                                               int seg0, int b, int n, int nb, int S, int N, int C_in,
+                                               const float* __restrict__ tt, const int32_t* __restrict__ src,
+                                               const Decay* __restrict__ d, const float* __restrict__ WT,
+                                               const double2* __restrict__ ent)
 {
-    const int lane = (int)threadIdx.x;
+    const int lane = (int)threadIdx.x % kWave;
     const int j = lane % kSub;
     for (int h = 0; h < kIvPerLane; ++h) {
         const int c = c0 + h * kStep + lane / kSub;
@@ -832,12 +843,12 @@ __device__ __forceinline__ void rebuild_window(ResolveLds& sh, const Model& m, i
             const int k = kq0 + j;
             const double t0 = k > 0 ? (double)tt[k - 1] : 0.0;
             const Decay dk = d[k];
-            crossing_data(m, v.V0, v.I0, v.V1, (double)tt[k] - t0, dk.A, dk.D, sh.crit[i], sh.hi[i], sh.fhi[i]);
-            sh.s0[i] = make_double2(v.V0, v.I0);
+            crossing_data(m, v.V0, v.I0, v.V1, (double)tt[k] - t0, dk.A, dk.D, w.crit[i], w.hi[i], w.fhi[i]);
+            w.s0[i] = make_double2(v.V0, v.I0);
             if (k == nb - 1) {
-                open_interval_data(m, v.V1, v.J1, m.t_end - (double)tt[k], sh.crit[kOpenIv], sh.hi[kOpenIv],
-                                   sh.fhi[kOpenIv]);
-                sh.s0[kOpenIv] = make_double2(v.V1, v.J1);
+                open_interval_data(m, v.V1, v.J1, m.t_end - (double)tt[k], w.crit[kOpenIv], w.hi[kOpenIv],
+                                   w.fhi[kOpenIv]);
+                w.s0[kOpenIv] = make_double2(v.V1, v.J1);
             }
         }
     }
@@ -877,19 +888,19 @@ __device__ __forceinline__ void flush_spikes(ResolveLds& sh, const Model& m, int
 // interval's start; an interval crosses iff Dl <= crit.  The spike-time
 // solve of a round runs wave-uniform on the crossing interval's data
 // (broadcast from its lane), so its iterations branch on scalars.
-__device__ __forceinline__ void resolve_step(ResolveLds& sh, const Model& m, int i0, int nlanes, Chain& ch,
-                                          float* __restrict__ st, float* __restrict__ si)
+__device__ __forceinline__ void resolve_step(ResolveLds& sh, const WinBuf& w, const Model& m, int i0, int nlanes,
+                                             Chain& ch, float* __restrict__ st, float* __restrict__ si)
 {
     const int lane = (int)threadIdx.x;
     const int i = lane < nlanes ? i0 + lane : i0;
-    const double crit = sh.crit[i];
-    const double t0 = sh.t0[i];
+    const double crit = w.crit[i];
+    const double t0 = w.t0[i];
     double Dl = ch.ns > 0 ? ch.dref * exp(-(t0 - ch.tref) * m.inv_tm) : 0.0;
     bool pend = lane < nlanes && crit >= 0.0 && Dl <= crit;
     unsigned long long cm = __ballot(pend);
     if (!cm) return;
-    const double2 s0 = sh.s0[i];
-    const double hi = sh.hi[i], fhi = sh.fhi[i];
+    const double2 s0 = w.s0[i];
+    const double hi = w.hi[i], fhi = w.fhi[i];
     double ylo = 1.0;
     for (;;) {
         const int kl = __ffsll((long long)cm) - 1;
@@ -924,19 +935,54 @@ __device__ __forceinline__ void resolve_step(ResolveLds& sh, const Model& m, int
     }
 }
 
-__device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restrict__ ev_t,
-                               const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
-                               const float* __restrict__ WT, int C_in, int N, int E_pad, int S, const Model& m,
-                               const Decay* __restrict__ dec, const double2* __restrict__ ent,
-                               const uint2* __restrict__ mask, uint32_t pool_cap,
-                               const Record* __restrict__ pool, float* __restrict__ out_t, int32_t* __restrict__ out_n,
-                               float* __restrict__ out_i)
+// The staging wave's part of window c0 / kWinCand: its intervals' loads,
+// committed to buffer w, then the rebuild of its sub-blocks without a record.
+__device__ __forceinline__ void stage_window(const ResolveLds& sh, WinBuf& w, const Model& m, int c0, int tot,
+                                             int seg0, int b, int n, int nb, int S, int N, int C_in,
+                                             const float* __restrict__ tt, const int32_t* __restrict__ src,
+                                             const Decay* __restrict__ d, const float* __restrict__ WT,
+                                             const double2* __restrict__ ent, const Record* __restrict__ pool)
 {
-    const int lane = (int)threadIdx.x;
+    const int lane = (int)threadIdx.x % kWave;
     const int j = lane % kSub, r = lane / kSub;
+    StageIv nx[kIvPerLane];
+#pragma unroll
+    for (int h = 0; h < kIvPerLane; ++h) nx[h] = stage_load(sh, c0 + h * kStep + r, tot, seg0, nb, j, tt, pool);
+#pragma unroll
+    for (int h = 0; h < kIvPerLane; ++h) {
+        const int c = c0 + h * kStep + r;
+        const int i = h * kWave + lane;
+        const uint32_t cw = sh.cand[min(c, tot - 1)];
+        const int kq0 = (seg0 + (int)(cw >> 3)) * kSeg + (int)(cw & 7u) * kSub;
+        const bool valid = c < tot && kq0 + j < nb;
+        w.crit[i] = valid ? nx[h].crit : -1.0;
+        w.hi[i] = nx[h].hi;
+        w.fhi[i] = nx[h].fhi;
+        w.s0[i] = nx[h].s0;
+        w.t0[i] = kq0 + j > 0 ? (double)nx[h].tp : 0.0;
+    }
+    static_assert(kWinCand <= kWave, "one lane per candidate of the window");
+    if (__ballot(sh.slot[min(c0 + lane % kWinCand, tot - 1)] == kNoSlot))
+        rebuild_window(sh, w, m, c0, tot, seg0, b, n, nb, S, N, C_in, tt, src, d, WT, ent);
+}
+
+// Both waves of the workgroup call this for the same neuron and pass the
+// same barriers (every loop bound is workgroup-uniform: candidate counts and
+// the capped flag are exchanged through LDS).  Returns the spike count on the
+// chain wave, 0 on the staging wave.
+__device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restrict__ ev_t,
+                              const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
+                              const float* __restrict__ WT, int C_in, int N, int E_pad, int S, const Model& m,
+                              const Decay* __restrict__ dec, const double2* __restrict__ ent,
+                              const uint2* __restrict__ mask, uint32_t pool_cap,
+                              const Record* __restrict__ pool, float* __restrict__ out_t, int32_t* __restrict__ out_n,
+                              float* __restrict__ out_i)
+{
+    const int lane = (int)threadIdx.x % kWave;
+    const bool chain = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)) == 0;   // wave-uniform
     // the first chunk's mask words are loaded together with the event count
     // (words past the sample's segments are dropped below)
-    uint2 mw = lane < S ? mask[((size_t)b * S + lane) * N + n] : make_uint2(0u, 0u);
+    uint2 mw = chain && lane < S ? mask[((size_t)b * S + lane) * N + n] : make_uint2(0u, 0u);
     const int nb = __builtin_amdgcn_readfirstlane(clamp_count(ev_n[b], E_max));
     const float* tt = ev_t + (size_t)b * E_max;
     const int32_t* src = ev_src + (size_t)b * E_max;
@@ -948,22 +994,23 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
     const bool has_open = __builtin_amdgcn_readfirstlane(nb > 0 && m.t_end > (double)tt[max(nb - 1, 0)] ? 1 : 0) != 0;
 
     Chain ch{0, 0.0, 0.0, false};
+    bool stop = false;
 
-    for (int seg0 = 0; seg0 < Sb && !ch.capped; seg0 += kWave) {
+    for (int seg0 = 0; seg0 < Sb && !stop; seg0 += kWave) {
         // ---- this chunk's flagged sub-blocks as a time-ordered list, with slots
-        const int sj = seg0 + lane;
-        if (seg0 > 0) mw = sj < Sb ? mask[((size_t)b * S + sj) * N + n] : make_uint2(0u, 0u);
-        const uint32_t mv = sj < Sb ? mw.x : 0u;
-        const int pc = __popc(mv);
-        int ex = pc;
+        if (chain) {
+            const int sj = seg0 + lane;
+            if (seg0 > 0) mw = sj < Sb ? mask[((size_t)b * S + sj) * N + n] : make_uint2(0u, 0u);
+            const uint32_t mv = sj < Sb ? mw.x : 0u;
+            const int pc = __popc(mv);
+            int ex = pc;
 #pragma unroll
-        for (int off = 1; off < kWave; off <<= 1) {
-            int v = __shfl_up(ex, off, kWave);
-            if (lane >= off) ex += v;
-        }
-        const int tot = rl_int(ex, kWave - 1);
-        ex -= pc;
-        {
+            for (int off = 1; off < kWave; off <<= 1) {
+                int v = __shfl_up(ex, off, kWave);
+                if (lane >= off) ex += v;
+            }
+            const int ctot = rl_int(ex, kWave - 1);
+            ex -= pc;
             // candidates and their record slots (consecutive per segment)
             uint32_t mm = mv, rel = mw.y;
             int o = ex;
@@ -974,75 +1021,63 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
                 ++rel;
                 mm &= mm - 1u;
             }
+            if (lane == 0) sh.ntot = ctot;
         }
         __syncthreads();
+        const int tot = __builtin_amdgcn_readfirstlane(sh.ntot);
         if (tot > 0) {
             // the open interval is taken after the window holding the sample's
             // last sub-block, when that sub-block is flagged (it is the last
             // candidate of the last chunk)
             const uint32_t cwl = (uint32_t)__builtin_amdgcn_readfirstlane((int)sh.cand[tot - 1]);
             const bool open_here = has_open && (seg0 + (int)(cwl >> 3)) * kSeg + (int)(cwl & 7u) * kSub + kSub >= nb;
-            if (open_here) {
-                // the open interval's data, from the last candidate's record
-                // (slot kOpenIv, which the windows do not overwrite)
-                const uint32_t slot = (uint32_t)__builtin_amdgcn_readfirstlane((int)sh.slot[tot - 1]);
-                const int kq0 = (seg0 + (int)(cwl >> 3)) * kSeg + (int)(cwl & 7u) * kSub;
-                const Record* rec = pool + (slot != kNoSlot ? slot : 0u);
-                const double oc = rec->crit[kSub], oh = rec->hi[kSub], of = rec->fhi[kSub];
-                const double2 os = rec->s[min(nb - kq0, kSub)];
-                const double ot = (double)tt[nb - 1];
-                if (lane == 0) {
-                    sh.crit[kOpenIv] = slot != kNoSlot ? oc : -1.0;
-                    sh.hi[kOpenIv] = oh;
-                    sh.fhi[kOpenIv] = of;
-                    sh.s0[kOpenIv] = os;
-                    sh.t0[kOpenIv] = ot;
-                }
-            }
-            // ---- windows of kWinCand candidates: the next window's loads are
-            // in flight (registers) while the current one (LDS) is resolved
             const int nwin = (tot + kWinCand - 1) / kWinCand;
-            StageIv nx[kIvPerLane];
-#pragma unroll
-            for (int h = 0; h < kIvPerLane; ++h) nx[h] = stage_load(sh, h * kStep + r, tot, seg0, nb, j, tt, pool);
-            for (int wi = 0; wi < nwin && !ch.capped; ++wi) {
-                const int c0 = wi * kWinCand;
-                // commit the staged window to LDS
-#pragma unroll
-                for (int h = 0; h < kIvPerLane; ++h) {
-                    const int c = c0 + h * kStep + r;
-                    const int i = h * kWave + lane;
-                    const uint32_t cw = sh.cand[min(c, tot - 1)];
-                    const int kq0 = (seg0 + (int)(cw >> 3)) * kSeg + (int)(cw & 7u) * kSub;
-                    const bool valid = c < tot && kq0 + j < nb;
-                    sh.crit[i] = valid ? nx[h].crit : -1.0;
-                    sh.hi[i] = nx[h].hi;
-                    sh.fhi[i] = nx[h].fhi;
-                    sh.s0[i] = nx[h].s0;
-                    sh.t0[i] = kq0 + j > 0 ? (double)nx[h].tp : 0.0;
+            if (!chain) {
+                if (open_here) {
+                    // the open interval's data, from the last candidate's
+                    // record, in slot kOpenIv of both buffers (the windows do
+                    // not overwrite it; a rebuild of the last sub-block does)
+                    const uint32_t slot = (uint32_t)__builtin_amdgcn_readfirstlane((int)sh.slot[tot - 1]);
+                    const int kq0 = (seg0 + (int)(cwl >> 3)) * kSeg + (int)(cwl & 7u) * kSub;
+                    const Record* rec = pool + (slot != kNoSlot ? slot : 0u);
+                    const double oc = rec->crit[kSub], oh = rec->hi[kSub], of = rec->fhi[kSub];
+                    const double2 os = rec->s[min(nb - kq0, kSub)];
+                    const double ot = (double)tt[nb - 1];
+                    if (lane < 2) {
+                        WinBuf& w = sh.win[lane];
+                        w.crit[kOpenIv] = slot != kNoSlot ? oc : -1.0;
+                        w.hi[kOpenIv] = oh;
+                        w.fhi[kOpenIv] = of;
+                        w.s0[kOpenIv] = os;
+                        w.t0[kOpenIv] = ot;
+                    }
                 }
-                const bool last_win = wi == nwin - 1;
-                __syncthreads();
-                if (__ballot(sh.slot[min(c0 + lane / 2, tot - 1)] == kNoSlot))
-                    rebuild_window(sh, m, c0, tot, seg0, b, n, nb, S, N, C_in, tt, src, d, WT, ent);
-                __syncthreads();
-                const int c1 = c0 + kWinCand;
-                if (c1 < tot) {
-#pragma unroll
-                    for (int h = 0; h < kIvPerLane; ++h) nx[h] = stage_load(sh, c1 + h * kStep + r, tot, seg0, nb, j, tt, pool);
-                    // keep the loads here, ahead of the window's steps (not sunk to the commit)
-                    asm volatile("" ::: "memory");
+                stage_window(sh, sh.win[0], m, 0, tot, seg0, b, n, nb, S, N, C_in, tt, src, d, WT, ent, pool);
+            }
+            __syncthreads();
+            for (int wi = 0; wi < nwin; ++wi) {
+                if (!chain) {
+                    if (wi + 1 < nwin)
+                        stage_window(sh, sh.win[(wi + 1) & 1], m, (wi + 1) * kWinCand, tot, seg0, b, n, nb, S, N,
+                                     C_in, tt, src, d, WT, ent, pool);
+                } else {
+                    // the window's steps, then (last window) the open interval as one more
+                    const WinBuf& w = sh.win[wi & 1];
+                    const int c0 = wi * kWinCand;
+                    const int steps = min(kWinSteps, (tot - c0 + kStep - 1) / kStep);
+                    const int nsteps = steps + (wi == nwin - 1 && open_here ? 1 : 0);
+                    for (int g = 0; g < nsteps && !ch.capped; ++g)
+                        resolve_step(sh, w, m, g < steps ? g * kWave : kOpenIv, g < steps ? kWave : 1, ch, st, si);
+                    if (lane == 0) sh.stop[wi & 1] = ch.capped ? 1 : 0;
                 }
-                // the window's steps, then (last window) the open interval as one more
-                const int steps = min(kWinSteps, (tot - c0 + kStep - 1) / kStep);
-                const int nsteps = steps + (last_win && open_here ? 1 : 0);
-                for (int g = 0; g < nsteps && !ch.capped; ++g)
-                    resolve_step(sh, m, g < steps ? g * kWave : kOpenIv, g < steps ? kWave : 1, ch, st, si);
-                __syncthreads();                      // the window is rewritten next
+                __syncthreads();              // window wi + 1 staged, window wi free
+                stop = __builtin_amdgcn_readfirstlane(sh.stop[wi & 1]) != 0;
+                if (stop) break;
             }
         }
-        __syncthreads();                              // the list is rewritten by the next chunk
+        __syncthreads();                      // the list is rewritten by the next chunk
     }
+    if (!chain) return 0;
     flush_spikes(sh, m, ch.ns - ch.ns % kWave, ch.ns, st, si);
     if (lane == 0) out_n[idx] = ch.ns;
     return ch.ns;
@@ -1052,7 +1087,7 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
 // taken as one concatenated list, entry w by workgroup w mod gridDim.x, so
 // that samples with many listed neurons spread over the whole grid.  Status
 // counts are added once per workgroup.
-__global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src,
+__global__ __launch_bounds__(kWave * kResolveWaves) void k_resolve(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src,
                                                    const int32_t* __restrict__ ev_n, int B, int E_max,
                                                    const float* __restrict__ WT, int C_in, int N, int E_pad, int S,
                                                    Model m, const Decay* __restrict__ dec,
@@ -1069,8 +1104,8 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
     // wait for them)
     unsigned long long spikes = 0;
     uint32_t capped = 0;
-    const int lane = (int)threadIdx.x;
-    // Running sum of the list lengths over groups of 64 samples (one load
+    const int lane = (int)threadIdx.x % kWave;
+    // Both waves walk the list the same way.  Running sum of the list lengths over groups of 64 samples (one load
     // per lane, a wave prefix sum): entry w of the concatenated lists belongs
     // to the first sample whose running sum exceeds w.
     int b0 = 0;               // first sample of the current group
@@ -1108,7 +1143,7 @@ __global__ __launch_bounds__(kWave) void k_resolve(const float* __restrict__ ev_
         spikes += (unsigned long long)ns;
         capped += ns >= m.s_max ? 1u : 0u;
     }
-    if (lane == 0) {
+    if (threadIdx.x == 0) {
         const int32_t sp = (int32_t)(spikes > 0x7fffffffull ? 0x7fffffffull : spikes);
         if (sp) {
             atomicAdd(&status[LIF_ST_SPIKES], sp);
@@ -1427,9 +1462,10 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
                          ev_t, ev_src, ev_n, E_max, L.E_pad, L.S, WT, C_in, N, m, P.dec, P.ent, P.pool, P.pool_count,
                          (uint32_t)L.pool_cap, out_n, nn, out_t, out_i, n_out, B, status);
     }
-    // Single-wave workgroups over the concatenated per-sample lists.
+    // Two-wave workgroups (chain and staging waves) over the concatenated
+    // per-sample lists.
     const unsigned rgrid = (unsigned)(nn < 4096 ? nn : 4096);
-    TIMED_LAUNCH("resolve", k_resolve, dim3(rgrid), dim3(kWave), 0, stream,
+    TIMED_LAUNCH("resolve", k_resolve, dim3(rgrid), dim3(kWave * kResolveWaves), 0, stream,
                  ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, L.E_pad, L.S, m, P.dec, P.ent, P.mask, (uint32_t)L.pool_cap,
                  P.pool, P.work, P.nwork, out_t, out_n, out_i, status);
     return check_launch();
