@@ -16,7 +16,7 @@
 namespace lif {
 
 constexpr int kWave = 64;       // CDNA wavefront width
-constexpr int kSeg = 128;       // events per scan segment (one wave walks it)
+constexpr int kSeg = 64;        // events per scan segment (one wave walks it)
 constexpr int kSub = 16;        // events per sub-block (candidate granularity)
 constexpr int kSubPerSeg = kSeg / kSub;
 static_assert(kSeg % kSub == 0 && kSubPerSeg <= 32, "sub-block mask is 32 bits");

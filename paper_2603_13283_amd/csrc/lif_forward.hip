@@ -253,7 +253,7 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_aggregate(
 // from the zero state (its aggregates loaded at once and kept), the range
 // totals are combined across waves in LDS, and each wave walks its range
 // again from its incoming state, writing the carries.
-constexpr int kCarryWaves = 4;
+constexpr int kCarryWaves = 8;
 constexpr int kCarryBatch = 16;
 
 __global__ __launch_bounds__(kWave * kCarryWaves) void k_carry(
@@ -533,7 +533,8 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
 // sub-blocks (a work list built by the check pass).  Intervals outside
 // flagged sub-blocks provably hold no spike.  The flagged sub-blocks are
 // taken in time order:
-//   * Candidate list: per 64 segments, the sub-block masks are compacted into
+//   * Candidate list: per chunk of kChunkEv events, the sub-block masks (one
+//     to two segments per lane) are compacted into
 //     a time-ordered list in LDS with one wave prefix sum, with the record
 //     slot of every candidate.
 //   * Windows of kWinCand candidates in two LDS buffers: the staging wave
@@ -558,7 +559,11 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
 // Wave-uniform state: spike count, reset deficit dref right after the
 // latest spike, at time tref.
 // ---------------------------------------------------------------------------
-constexpr int kCandCap = kWave * kSubPerSeg;     // candidates of 64 segments
+constexpr int kChunkEv = 8192;                   // events per chunk of the candidate list
+constexpr int kChunkSeg = kChunkEv / kSeg;       // segments per chunk
+constexpr int kSegPerLane = kChunkSeg / kWave;   // mask words per lane
+static_assert(kChunkSeg % kWave == 0 && kSubPerSeg <= 8, "chunk layout; 3-bit sub-block field of a candidate");
+constexpr int kCandCap = kChunkSeg * kSubPerSeg; // candidates of one chunk
 constexpr int kStep = kWave / kSub;              // candidates per step
 constexpr int kWinCand = 16;                     // candidates per window
 constexpr int kWinIv = kWinCand * kSub;          // intervals per window
@@ -982,7 +987,12 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
     const bool chain = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)) == 0;   // wave-uniform
     // the first chunk's mask words are loaded together with the event count
     // (words past the sample's segments are dropped below)
-    uint2 mw = chain && lane < S ? mask[((size_t)b * S + lane) * N + n] : make_uint2(0u, 0u);
+    uint2 mw[kSegPerLane];
+#pragma unroll
+    for (int h = 0; h < kSegPerLane; ++h) {
+        const int sj = lane * kSegPerLane + h;
+        mw[h] = chain && sj < S ? mask[((size_t)b * S + sj) * N + n] : make_uint2(0u, 0u);
+    }
     const int nb = __builtin_amdgcn_readfirstlane(clamp_count(ev_n[b], E_max));
     const float* tt = ev_t + (size_t)b * E_max;
     const int32_t* src = ev_src + (size_t)b * E_max;
@@ -996,13 +1006,19 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
     Chain ch{0, 0.0, 0.0, false};
     bool stop = false;
 
-    for (int seg0 = 0; seg0 < Sb && !stop; seg0 += kWave) {
-        // ---- this chunk's flagged sub-blocks as a time-ordered list, with slots
+    for (int seg0 = 0; seg0 < Sb && !stop; seg0 += kChunkSeg) {
+        // ---- this chunk's flagged sub-blocks as a time-ordered list, with
+        // slots; lane l takes segments seg0 + kSegPerLane l + h
         if (chain) {
-            const int sj = seg0 + lane;
-            if (seg0 > 0) mw = sj < Sb ? mask[((size_t)b * S + sj) * N + n] : make_uint2(0u, 0u);
-            const uint32_t mv = sj < Sb ? mw.x : 0u;
-            const int pc = __popc(mv);
+            uint32_t mv[kSegPerLane];
+            int pc = 0;
+#pragma unroll
+            for (int h = 0; h < kSegPerLane; ++h) {
+                const int sj = seg0 + lane * kSegPerLane + h;
+                if (seg0 > 0) mw[h] = sj < Sb ? mask[((size_t)b * S + sj) * N + n] : make_uint2(0u, 0u);
+                mv[h] = sj < Sb ? mw[h].x : 0u;
+                pc += __popc(mv[h]);
+            }
             int ex = pc;
 #pragma unroll
             for (int off = 1; off < kWave; off <<= 1) {
@@ -1012,14 +1028,17 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
             const int ctot = rl_int(ex, kWave - 1);
             ex -= pc;
             // candidates and their record slots (consecutive per segment)
-            uint32_t mm = mv, rel = mw.y;
             int o = ex;
-            while (mm) {
-                sh.cand[o] = ((uint32_t)lane << 3) | (uint32_t)__builtin_ctz(mm);
-                sh.slot[o] = rel < pool_cap ? (uint32_t)b * pool_cap + rel : kNoSlot;
-                ++o;
-                ++rel;
-                mm &= mm - 1u;
+#pragma unroll
+            for (int h = 0; h < kSegPerLane; ++h) {
+                uint32_t mm = mv[h], rel = mw[h].y;
+                while (mm) {
+                    sh.cand[o] = ((uint32_t)(lane * kSegPerLane + h) << 3) | (uint32_t)__builtin_ctz(mm);
+                    sh.slot[o] = rel < pool_cap ? (uint32_t)b * pool_cap + rel : kNoSlot;
+                    ++o;
+                    ++rel;
+                    mm &= mm - 1u;
+                }
             }
             if (lane == 0) sh.ntot = ctot;
         }
