@@ -181,9 +181,9 @@ def main():
     #   resolve: per walked sub-block, for each of its 16 intervals, the
     #     record's state and crossing data (16 + 24 B) and the interval's
     #     start time (4 B); plus 8 B per spike and 4 B per count.
-    S = (E + 127) // 128
+    S = (E + 63) // 64                       # 64-event scan segments
     walked = status[4]
-    alg = {"prep": B * S * 128 * 32 + total_ev * 4 + B * N * P.s_max * 8,
+    alg = {"prep": B * S * 64 * 32 + total_ev * 4 + B * N * P.s_max * 8,
            "aggregate": total_ev * (8 + 4 * N),
            "check": total_ev * (8 + 4 * N),
            "carry": B * S * N * 32,
