@@ -106,6 +106,22 @@ def test_spike_cap(env):
     check(env, cfg.events, cfg.layers[0].WT, "cap3", s_max=3)
 
 
+def test_long_stream_chunks_and_cap(env):
+    """Streams of 20 000 events per sample: the resolve pass takes the
+    flagged sub-blocks in chunks of 8192 events, so spike chains (up to about
+    600 spikes per neuron, flushed 64 at a time) run across window and chunk
+    boundaries; with a small cap, neurons stop in an early chunk while later
+    chunks of the same sample follow, and with a cap of 100 they stop in a
+    later one."""
+    cfg = W.random_small(35, B=2, C=40, N=96, n_events=20000, T=4.0, gain=3.0, ragged=False)
+    s = check(env, cfg.events, cfg.layers[0].WT, "long", s_max=640, both=False)
+    assert s["par"]["spikes"] > 10000 and s["par"]["status"][1] == 0
+    s = check(env, cfg.events, cfg.layers[0].WT, "long_cap2", s_max=2, both=False)
+    assert s["par"]["status"][1] > 0
+    s = check(env, cfg.events, cfg.layers[0].WT, "long_cap100", s_max=100, both=False)
+    assert s["par"]["status"][1] > 0
+
+
 def test_config2_full(env):
     cfg = W.config2()
     s = check(env, cfg.events, cfg.layers[0].WT, "c2")
