@@ -842,7 +842,7 @@ __device__ __forceinline__ void rebuild_window(const ResolveLds& sh, WinBuf& w, 
         const int seg = seg0 + (int)(cw >> 3), q = (int)(cw & 7u);
         const int kq0 = seg * kSeg + q * kSub, cnt = min(kSub, nb - kq0);
         const double2 e0 = fb ? ent[(((size_t)b * S + seg) * kSubPerSeg + q) * N + n] : make_double2(0.0, 0.0);
-        const IvStates v = subblock_walk<false>(m, e0.x, e0.y, kq0, cnt, j, n, N, C_in, src, d, WT);
+        const IvStates v = subblock_walk<true>(m, e0.x, e0.y, kq0, cnt, j, n, N, C_in, src, d, WT);
         if (fb && j < cnt) {
             const int i = h * kWave + lane;
             const int k = kq0 + j;
