@@ -24,7 +24,16 @@ def _dev(torch, a):
     return torch.from_numpy(np.ascontiguousarray(a)).to("cuda:0")
 
 
-def _fwd_bwd(env, ev, WT, seed, s_max=64, reg=0.01, **kw):
+def _rel(a, b):
+    n = np.linalg.norm(b)
+    return float(np.linalg.norm(np.asarray(a, np.float64) - b) / n) if n > 0 else float(np.linalg.norm(a))
+
+
+def _fwd_bwd(env, ev, WT, seed, s_max=64, reg=0.01, e2e=True, **kw):
+    """e2e=False: the end-to-end errors are printed, not asserted (for spike
+    trains long enough that the float32 rounding of the spike times handed
+    to the backward pass is amplified by the adjoint recurrence); the
+    backward kernels are still checked on identical inputs."""
     torch, lif = env
     P = lif.Params(s_max=s_max, solver_reg=reg, **kw)
     OP = oracle.LifParams(s_max=s_max, solver_reg=reg, **kw)
@@ -42,8 +51,12 @@ def _fwd_bwd(env, ev, WT, seed, s_max=64, reg=0.01, **kw):
     # neurons with a flagged near-tie are excluded from the comparison
     okN = ~np.isfinite(ref.tie_t).any(axis=0)
     okB = ~np.isfinite(ref.tie_t).any(axis=1)
-    rW = compare_grad(gW.cpu().numpy()[:, okN], oW[:, okN], label="grad_WT", elem_rtol=E2E_ELEM_RTOL)
-    rT = compare_grad(gT.cpu().numpy()[okB], oT[okB], label="grad_ev_t", elem_rtol=E2E_ELEM_RTOL)
+    if e2e:
+        rW = compare_grad(gW.cpu().numpy()[:, okN], oW[:, okN], label="grad_WT", elem_rtol=E2E_ELEM_RTOL)
+        rT = compare_grad(gT.cpu().numpy()[okB], oT[okB], label="grad_ev_t", elem_rtol=E2E_ELEM_RTOL)
+    else:
+        rW = _rel(gW.cpu().numpy()[:, okN], oW[:, okN])
+        rT = _rel(gT.cpu().numpy()[okB], oT[okB])
     # The backward kernels alone, on identical inputs: the oracle's spikes
     # rounded to float32 go to both sides.
     r32 = copy.deepcopy(ref)
@@ -75,6 +88,20 @@ def test_backward_no_regularisation_and_reset(env):
 def test_backward_config2_driven(env):
     cfg = W.config2(B=4)
     _fwd_bwd(env, cfg.events, cfg.layers[0].WT, 25, v_th=0.5)
+
+
+def test_backward_long_spike_trains(env):
+    """20 000-event streams, up to about 600 spikes per neuron: long
+    spike-adjoint recurrences in the setup pass and spikes spread over
+    hundreds of segments in the adjoint walk.  The kernels are checked on
+    identical inputs.  End to end, dL/dt_in is not asserted.  Over 4 s the
+    float32 spike times are resolved to about 240 ns, so input events that
+    close to a spike can fall on either side of it between the float32 and
+    float64 spike trains.  An event counts only for spikes strictly after it,
+    so its gradient term switches on or off (about 1e-3 relative in norm
+    here, against 3e-8 on identical inputs)."""
+    cfg = W.random_small(35, B=2, C=40, N=96, n_events=20000, T=4.0, gain=3.0, ragged=False)
+    _fwd_bwd(env, cfg.events, cfg.layers[0].WT, 35, s_max=640, e2e=False)
 
 
 def test_backward_silent_layer_is_zero(env):
