@@ -94,12 +94,12 @@ def test_backward_long_spike_trains(env):
     """20 000-event streams, up to about 600 spikes per neuron: long
     spike-adjoint recurrences in the setup pass and spikes spread over
     hundreds of segments in the adjoint walk.  The kernels are checked on
-    identical inputs.  End to end, dL/dt_in is not asserted.  Over 4 s the
-    float32 spike times are resolved to about 240 ns, so input events that
-    close to a spike can fall on either side of it between the float32 and
-    float64 spike trains.  An event counts only for spikes strictly after it,
-    so its gradient term switches on or off (about 1e-3 relative in norm
-    here, against 3e-8 on identical inputs)."""
+    identical inputs.  End to end, dL/dt_in is not asserted.  Rounded to
+    float32, 18 of the spike times here equal an input event's time, and 26
+    more lie within one float32 step (240 ns at 4 s) of one.  In float64
+    those events are strictly before the spike; at a tie an event counts as
+    after it, so its term drops out (about 1e-3 relative in norm here, against
+    3e-8 on identical inputs)."""
     cfg = W.random_small(35, B=2, C=40, N=96, n_events=20000, T=4.0, gain=3.0, ragged=False)
     _fwd_bwd(env, cfg.events, cfg.layers[0].WT, 35, s_max=640, e2e=False)
 
