@@ -85,6 +85,15 @@ def test_backward_no_regularisation_and_reset(env):
     _fwd_bwd(env, cfg.events, cfg.layers[0].WT, 24, reg=0.0, v_reset=-0.2)
 
 
+@pytest.mark.parametrize("ratio", [2.0, 3.7])
+def test_backward_tau_ratios(env, ratio):
+    """tau_m / tau_s other than the configs' 4: the adjoint decays and the
+    kernel derivative use both time constants; 3.7 also takes the
+    exponential spike-time solve in the forward pass."""
+    cfg = W.random_small(36, B=3, C=25, N=70, n_events=500, T=0.3, gain=16.0)
+    _fwd_bwd(env, cfg.events, cfg.layers[0].WT, 36, tau_mem=0.02, tau_syn=0.02 / ratio)
+
+
 def test_backward_config2_driven(env):
     cfg = W.config2(B=4)
     _fwd_bwd(env, cfg.events, cfg.layers[0].WT, 25, v_th=0.5)
