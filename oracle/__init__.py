@@ -60,10 +60,10 @@ def _load():
         _lib = ctypes.CDLL(_LIB_PATH)
         P = ctypes.c_void_p
         _lib.or_forward.argtypes = [P, P, P, ctypes.c_int, ctypes.c_int, P, ctypes.c_int, ctypes.c_int,
-                                    ctypes.POINTER(_Params), ctypes.c_int, P, P, P, P, P, P]
+                                    ctypes.POINTER(_Params), ctypes.c_int, P, P, P, P, P, P, P]
         _lib.or_forward.restype = ctypes.c_int
         _lib.or_backward.argtypes = [P, P, P, ctypes.c_int, ctypes.c_int, P, ctypes.c_int, ctypes.c_int,
-                                     ctypes.POINTER(_Params), ctypes.c_int, P, P, P, P, P, P]
+                                     ctypes.POINTER(_Params), ctypes.c_int, P, P, P, P, P, P, P]
         _lib.or_backward.restype = ctypes.c_int
         _lib.or_trace.argtypes = [P, P, ctypes.c_int, P, ctypes.c_int, ctypes.c_int,
                                   ctypes.POINTER(_Params), P, P]
@@ -102,6 +102,19 @@ class ForwardResult:
     capped: np.ndarray   # int32 [B, N]
     tie_t: np.ndarray    # float64 [B, N]: start of first near-tie interval, +inf if none
     min_gap: np.ndarray  # float64 [B, N]: smallest |V_max - V_th| over checked intervals
+    out_k: np.ndarray    # int32 [B, N, s_max]: input events consumed before each spike, 0 padding
+
+    def rounded(self) -> "ForwardResult":
+        """The same result with spike times and currents rounded to float32
+        (what a float32 forward hands to a backward pass), widened again."""
+        return ForwardResult(self.out_t.astype(np.float32).astype(np.float64),
+                             self.out_i.astype(np.float32).astype(np.float64), self.out_n, self.capped,
+                             self.tie_t, self.min_gap, self.out_k)
+
+    def select(self, keep) -> "ForwardResult":
+        """The samples selected by a boolean mask over the batch."""
+        return ForwardResult(self.out_t[keep], self.out_i[keep], self.out_n[keep], self.capped[keep],
+                             self.tie_t[keep], self.min_gap[keep], self.out_k[keep])
 
 
 def _ptr(a: np.ndarray):
@@ -126,23 +139,25 @@ def forward(ev_t, ev_src, ev_n, WT, params: LifParams = LifParams(), nthreads: O
     S = int(params.s_max)
     out_t = np.empty((B, N, S), np.float64)
     out_i = np.empty((B, N, S), np.float64)
+    out_k = np.empty((B, N, S), np.int32)
     out_n = np.empty((B, N), np.int32)
     capped = np.empty((B, N), np.int32)
     tie_t = np.empty((B, N), np.float64)
     min_gap = np.empty((B, N), np.float64)
     p = params.c()
     rc = lib.or_forward(_ptr(ev_t), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(WT), C, N, ctypes.byref(p),
-                        _nthreads(nthreads), _ptr(out_t), _ptr(out_i), _ptr(out_n), _ptr(capped),
+                        _nthreads(nthreads), _ptr(out_t), _ptr(out_i), _ptr(out_k), _ptr(out_n), _ptr(capped),
                         _ptr(tie_t), _ptr(min_gap))
     if rc != 0:
         raise ValueError(f"oracle forward rejected its arguments (rc={rc})")
-    return ForwardResult(out_t, out_i, out_n, capped, tie_t, min_gap)
+    return ForwardResult(out_t, out_i, out_n, capped, tie_t, min_gap, out_k)
 
 
 def backward(ev_t, ev_src, ev_n, WT, fwd: ForwardResult, grad_out_t, params: LifParams = LifParams(),
              nthreads: Optional[int] = None):
     """float64 gradients (grad_WT [C_in, N], grad_ev_t [B, E_max]) of
-    L = sum grad_out_t * out_t through the oracle's own forward result."""
+    L = sum grad_out_t * out_t, through a forward result for the same inputs
+    (spike times, currents at the spikes and the consumed-event counts)."""
     lib = _load()
     ev_t = np.ascontiguousarray(ev_t, dtype=np.float32)
     ev_src = np.ascontiguousarray(ev_src, dtype=np.int32)
@@ -155,8 +170,10 @@ def backward(ev_t, ev_src, ev_n, WT, fwd: ForwardResult, grad_out_t, params: Lif
     gT = np.empty((B, E), np.float64)
     p = params.c()
     rc = lib.or_backward(_ptr(ev_t), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(WT), C, N, ctypes.byref(p),
-                         _nthreads(nthreads), _ptr(np.ascontiguousarray(fwd.out_t)),
-                         _ptr(np.ascontiguousarray(fwd.out_i)), _ptr(np.ascontiguousarray(fwd.out_n)),
+                         _nthreads(nthreads), _ptr(np.ascontiguousarray(fwd.out_t, dtype=np.float64)),
+                         _ptr(np.ascontiguousarray(fwd.out_i, dtype=np.float64)),
+                         _ptr(np.ascontiguousarray(fwd.out_k, dtype=np.int32)),
+                         _ptr(np.ascontiguousarray(fwd.out_n, dtype=np.int32)),
                          _ptr(g), _ptr(gW), _ptr(gT))
     if rc != 0:
         raise RuntimeError(f"oracle backward failed (rc={rc})")

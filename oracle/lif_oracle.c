@@ -155,7 +155,7 @@ typedef struct {
 
 static or_neuron_result simulate_neuron(const or_params* p, const float* ev_t, const int32_t* ev_src,
                                         int n, const float* WT, int N, int i,
-                                        double* st, double* si)
+                                        double* st, double* si, int32_t* sk)
 {
     or_neuron_result res = {0, 0, INFINITY, INFINITY};
     double t_cur = 0.0, V = 0.0, I = 0.0;
@@ -173,6 +173,7 @@ static or_neuron_result simulate_neuron(const or_params* p, const float* ev_t, c
                 double Istar = i_at(p, I, tau);
                 st[res.n_spikes] = t_cur + tau;
                 si[res.n_spikes] = Istar;
+                sk[res.n_spikes] = k;          /* events 0 .. k-1 came before this spike */
                 res.n_spikes++;
                 if (res.n_spikes >= p->s_max) { res.capped = 1; return res; }
                 /* Hard reset of V only; the interval is tested again from t*. */
@@ -201,7 +202,8 @@ typedef struct {
     const or_params* p;
     const float* ev_t; const int32_t* ev_src; const int32_t* ev_n;
     int B, E_max; const float* WT; int C_in, N;
-    double* out_t; double* out_i; int32_t* out_n; int32_t* capped; double* tie_t; double* min_gap;
+    double* out_t; double* out_i; int32_t* out_k; int32_t* out_n; int32_t* capped; double* tie_t;
+    double* min_gap;
     int tid, nthreads;
 } fwd_job;
 
@@ -212,10 +214,14 @@ static void* fwd_worker(void* arg)
     for (size_t item = (size_t)j->tid; item < total; item += (size_t)j->nthreads) {
         int b = (int)(item / (size_t)j->N), i = (int)(item % (size_t)j->N);
         size_t o = item * (size_t)j->p->s_max;
-        for (int s = 0; s < j->p->s_max; ++s) { j->out_t[o + s] = INFINITY; j->out_i[o + s] = 0.0; }
+        for (int s = 0; s < j->p->s_max; ++s) {
+            j->out_t[o + s] = INFINITY;
+            j->out_i[o + s] = 0.0;
+            j->out_k[o + s] = 0;
+        }
         or_neuron_result r = simulate_neuron(j->p, j->ev_t + (size_t)b * j->E_max,
                                              j->ev_src + (size_t)b * j->E_max, j->ev_n[b],
-                                             j->WT, j->N, i, j->out_t + o, j->out_i + o);
+                                             j->WT, j->N, i, j->out_t + o, j->out_i + o, j->out_k + o);
         j->out_n[item] = r.n_spikes;
         j->capped[item] = r.capped;
         j->tie_t[item] = r.tie_t;
@@ -235,12 +241,13 @@ static int run_threads(void* (*fn)(void*), void* jobs, size_t job_size, int nthr
     return 0;
 }
 
-/* Forward over a batch.  Outputs are [B][N][s_max] (times, I at spike; +inf
- * and 0 padding), [B][N] counts, capped flags, first near-tie interval start
- * and the smallest |V_max - V_th| seen. */
+/* Forward over a batch.  Outputs are [B][N][s_max] (times, I at spike, and
+ * the number of input events consumed before each spike; +inf, 0 and 0
+ * padding), [B][N] counts, capped flags, first near-tie interval start and
+ * the smallest |V_max - V_th| seen. */
 int or_forward(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
                const float* WT, int C_in, int N, const or_params* p, int nthreads,
-               double* out_t, double* out_i, int32_t* out_n, int32_t* capped,
+               double* out_t, double* out_i, int32_t* out_k, int32_t* out_n, int32_t* capped,
                double* tie_t, double* min_gap)
 {
     if (!(p->tau_mem > p->tau_syn && p->tau_syn > 0.0) || !(p->v_reset < p->v_th) || p->s_max < 1)
@@ -250,7 +257,7 @@ int or_forward(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, in
     if (!jobs) return -2;
     for (int t = 0; t < nthreads; ++t) {
         fwd_job j = {p, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N,
-                     out_t, out_i, out_n, capped, tie_t, min_gap, t, nthreads};
+                     out_t, out_i, out_k, out_n, capped, tie_t, min_gap, t, nthreads};
         jobs[t] = j;
     }
     int rc = run_threads(fwd_worker, jobs, sizeof(fwd_job), nthreads);
@@ -309,13 +316,23 @@ int or_trace(const float* ev_t, const int32_t* ev_src, int n, const float* WT, i
 /* floored by the solver regularisation.  The adjoints are taken by a       */
 /* reverse pass over the spikes of each neuron, then every input event      */
 /* collects its weight and time gradients directly from the sums.           */
+/*                                                                          */
+/* Which events a spike depends on is the forward pass's own decision: the  */
+/* spike solved in the interval before event k depends on events 0 .. k-1   */
+/* (out_k holds k).  An event at exactly the spike time comes after it (the */
+/* interval is tested before its closing event is consumed).  Deciding this */
+/* from the index instead of comparing times keeps the decision when the    */
+/* spike times handed over have been rounded (to float32, a spike can round */
+/* onto the time of the event just before it); the offset t_s - t_k is then */
+/* at least 0.                                                              */
 /* ---------------------------------------------------------------------- */
 
 typedef struct {
     const or_params* p;
     const float* ev_t; const int32_t* ev_src; const int32_t* ev_n;
     int B, E_max; const float* WT; int C_in, N;
-    const double* out_t; const double* out_i; const int32_t* out_n; const double* grad_out_t;
+    const double* out_t; const double* out_i; const int32_t* out_k; const int32_t* out_n;
+    const double* grad_out_t;
     double* gW_part;   /* [nthreads][C_in][N] partial weight gradients       */
     double* gT_part;   /* [nthreads][B][E_max] partial time gradients        */
     int tid, nthreads;
@@ -337,6 +354,7 @@ static void* bwd_worker(void* arg)
         if (ns <= 0) continue;
         const double* ts_ = j->out_t + item * (size_t)smax;
         const double* is_ = j->out_i + item * (size_t)smax;
+        const int32_t* ks_ = j->out_k + item * (size_t)smax;
         const double* g = j->grad_out_t + item * (size_t)smax;
         /* Reverse pass over the spikes: lambda_s = dL/dt_s (total),
          * mu_s = -lambda_s / V'_s is the multiplier of constraint F_s. */
@@ -354,12 +372,13 @@ static void* bwd_worker(void* arg)
         const int32_t* es = j->ev_src + (size_t)b * j->E_max;
         int n = j->ev_n[b];
         for (int k = 0; k < n; ++k) {
+            if (k >= ks_[ns - 1]) break;          /* no spike depends on event k */
             double tk = (double)et[k];
-            if (!(tk < ts_[ns - 1])) break;
             double a = 0.0, ad = 0.0;
             for (int s = 0; s < ns; ++s) {
+                if (k >= ks_[s]) continue;        /* spike s came before event k */
                 double u = ts_[s] - tk;
-                if (!(u > 0.0)) continue;
+                if (u < 0.0) u = 0.0;
                 double em = exp(-u / tm), es2 = exp(-u / ts);
                 a += mu[s] * ka * (em - es2);
                 ad += mu[s] * ka * (-em / tm + es2 / ts);
@@ -374,10 +393,11 @@ static void* bwd_worker(void* arg)
 }
 
 /* Backward over a batch: grad_WT [C_in][N] and grad_ev_t [B][E_max] are
- * overwritten.  out_t/out_i/out_n are the oracle's own forward outputs. */
+ * overwritten.  out_t/out_i/out_k/out_n are forward outputs for the same
+ * inputs (the oracle's own, possibly rounded). */
 int or_backward(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
                 const float* WT, int C_in, int N, const or_params* p, int nthreads,
-                const double* out_t, const double* out_i, const int32_t* out_n,
+                const double* out_t, const double* out_i, const int32_t* out_k, const int32_t* out_n,
                 const double* grad_out_t, double* grad_WT, double* grad_ev_t)
 {
     if (nthreads < 1) nthreads = 1;
@@ -387,7 +407,7 @@ int or_backward(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, i
     bwd_job* jobs = (bwd_job*)calloc((size_t)nthreads, sizeof(bwd_job));
     if (!gW_part || !gT_part || !jobs) { free(gW_part); free(gT_part); free(jobs); return -2; }
     for (int t = 0; t < nthreads; ++t) {
-        bwd_job j = {p, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, out_t, out_i, out_n, grad_out_t,
+        bwd_job j = {p, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, out_t, out_i, out_k, out_n, grad_out_t,
                      gW_part, gT_part, t, nthreads};
         jobs[t] = j;
     }

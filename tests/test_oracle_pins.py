@@ -111,6 +111,38 @@ def test_unbounded_last_interval():
     assert not c
 
 
+def test_finite_t_end_against_rk4():
+    """A finite t_end: the interval after the last event ends there (reading
+    of the last interval under the Sec. 3.2.2 rule).  Events at 10 ms (w =
+    10) and 20 ms (w = 10): the neuron fires once between them and twice in
+    the open interval after 20 ms (several times).  RK4 stepping with threshold detection
+    and reset (no closed forms) gives the spikes up to a horizon T, which
+    must match the oracle run with t_end = T; with t_end before the last
+    event, the events are still consumed (the spike between them stays) and
+    only the open interval is empty."""
+    times = np.array([0.010, 0.020])
+    wts = np.array([[10.0], [10.0]])
+    ev = W.pack_events([times], [np.array([0, 1])])
+    WT = wts.astype(np.float32)
+    full = _bruteforce(times, wts, 2e-6, P.tau_mem, P.tau_syn, P.v_th, P.v_reset, 0.08)[0]
+    assert len(full) >= 3 and full[0] < 0.020 < full[1], full
+    horizons = [np.inf, 0.5 * (full[1] + full[2]), 0.5 * (0.020 + full[1])]
+    for T in horizons:
+        r = oracle.forward(ev.ev_t, ev.ev_src, ev.ev_n, WT, oracle.LifParams(t_end=T))
+        bf = full if np.isinf(T) else _bruteforce(times, wts, 2e-6, P.tau_mem, P.tau_syn, P.v_th, P.v_reset, T)[0]
+        n = int(r.out_n[0, 0])
+        assert n == len(bf), (T, r.out_t[0, 0, :n], bf)
+        assert np.all(np.abs(r.out_t[0, 0, :n] - np.array(bf)) < 1e-9), T
+    # t_end = 12 ms lies before the first spike and before the last event:
+    # the spike at ~12.9 ms is in the interval closed by the event at 20 ms,
+    # which is still consumed; the open interval after 20 ms is empty.
+    assert full[0] > 0.012
+    r = oracle.forward(ev.ev_t, ev.ev_src, ev.ev_n, WT, oracle.LifParams(t_end=0.012))
+    bf = _bruteforce(times[:1], wts[:1], 2e-6, P.tau_mem, P.tau_syn, P.v_th, P.v_reset, 0.020)[0]
+    assert int(r.out_n[0, 0]) == len(bf) == 1
+    assert abs(r.out_t[0, 0, 0] - bf[0]) < 1e-9
+
+
 # --------------------------------------------------------------------------
 # Spike-time pins
 # --------------------------------------------------------------------------
@@ -186,6 +218,30 @@ def test_single_event_critical_weight_and_monotone_time():
         for s in range(n[j] - 1):
             assert r.out_i[0, j, s] >= 6.3496
         assert r.out_i[0, j, n[j] - 1] < 6.3497
+
+
+def test_near_tie_flag_on_grazing_input():
+    """The near-tie flag (|V_max - V_th| < 1e-6 in some checked interval)
+    on a single event from rest, whose interval maximum is w K(t_peak): the
+    critical weight 1 / K(t_peak) is taken in closed form (t_peak from
+    Eq. t_vmax with V0 = 0), not from the oracle.  Weights within 1e-7 of it
+    (relative) must be flagged, at the event's time; weights 1e-4 away must
+    not, and the smallest gap reported must be |w K(t_peak) - 1|."""
+    tm, ts = P.tau_mem, P.tau_syn
+    k = ts / (tm - ts)
+    tp = tm * ts / (tm - ts) * math.log(tm / ts)
+    kpeak = k * (math.exp(-tp / tm) - math.exp(-tp / ts))
+    w_crit = P.v_th / kpeak
+    ws = np.array([w_crit * (1 + 1e-7), w_crit * (1 - 1e-7), w_crit * (1 + 1e-4), w_crit * (1 - 1e-4)],
+                  np.float32)
+    ev = W.pack_events([np.array([0.25])], [np.array([0])])
+    r = oracle.forward(ev.ev_t, ev.ev_src, ev.ev_n, ws.reshape(1, -1), P)
+    flagged = np.isfinite(r.tie_t[0])
+    assert flagged.tolist() == [True, True, False, False]
+    assert np.all(r.tie_t[0, :2] == 0.25)
+    gap = np.abs(ws.astype(np.float64) * kpeak - P.v_th)
+    assert np.all(np.abs(r.min_gap[0] - gap) < 1e-12)
+    assert r.out_n[0].tolist() == [1, 0, 1, 0]
 
 
 def test_python_bisection_reference_matches_c_newton():
@@ -378,8 +434,8 @@ def test_invariant_neuron_permutation_and_silent_channels():
 # Gradients
 # --------------------------------------------------------------------------
 
-def _ref_loss(times, src, W64, g, i, n_max):
-    sp = ref.simulate(times, [W64[c, i] for c in src])
+def _ref_loss(times, src, W64, g, i, n_max, vr=0.0):
+    sp = ref.simulate(times, [W64[c, i] for c in src], vr=vr)
     return sum(g[s] * t for s, (t, _) in enumerate(sp[:n_max])), len(sp)
 
 
@@ -423,6 +479,49 @@ def test_backward_matches_finite_differences():
             tot_m += _ref_loss(Tm, src, W64, g[0, i], i, int(r.out_n[0, i]))[0]
         fd = (tot_p - tot_m) / (2 * h)
         assert abs(fd - gT[0, k]) <= 1e-5 * max(1.0, abs(fd))
+
+
+def test_backward_matches_finite_differences_nonzero_reset():
+    """The same finite-difference pin with V_reset = -0.3: each reset then
+    lowers V by V_th - V_reset = 1.3, which enters the spike-to-spike adjoint
+    recurrence (App. D.3, Eq. ift_vjp through Sec. 3.1's reset).  A neuron
+    with three or more spikes makes that term matter."""
+    rng = np.random.default_rng(19)
+    C, N, n = 5, 3, 60
+    t = np.sort(rng.random(n) * 0.15).astype(np.float32)
+    src = rng.integers(0, C, n).astype(np.int32)
+    WT = (rng.uniform(-0.5, 6.0, (C, N))).astype(np.float32)
+    ev = W.pack_events([t], [src])
+    p0 = oracle.LifParams(solver_reg=0.0, v_reset=-0.3)
+    r = oracle.forward(ev.ev_t, ev.ev_src, ev.ev_n, WT, p0)
+    assert r.out_n.max() >= 3
+    g = rng.standard_normal(r.out_t.shape) * np.isfinite(r.out_t)
+    gW, gT = oracle.backward(ev.ev_t, ev.ev_src, ev.ev_n, WT, r, g, p0)
+    W64 = WT.astype(np.float64)
+    T64 = t.astype(np.float64)
+    for i in range(N):
+        base_n = int(r.out_n[0, i])
+        for c in range(C):
+            h = 1e-6
+            Wp, Wm = W64.copy(), W64.copy()
+            Wp[c, i] += h
+            Wm[c, i] -= h
+            lp, np_ = _ref_loss(T64, src, Wp, g[0, i], i, base_n, vr=-0.3)
+            lm, nm = _ref_loss(T64, src, Wm, g[0, i], i, base_n, vr=-0.3)
+            assert np_ == nm == base_n
+            fd = (lp - lm) / (2 * h)
+            assert abs(fd - gW[c, i]) <= 1e-6 * max(1.0, abs(fd)), (c, i, fd, gW[c, i])
+    for k in range(0, n, 4):
+        h = 1e-9
+        tot_p = tot_m = 0.0
+        for i in range(N):
+            Tp, Tm = T64.copy(), T64.copy()
+            Tp[k] += h
+            Tm[k] -= h
+            tot_p += _ref_loss(Tp, src, W64, g[0, i], i, int(r.out_n[0, i]), vr=-0.3)[0]
+            tot_m += _ref_loss(Tm, src, W64, g[0, i], i, int(r.out_n[0, i]), vr=-0.3)[0]
+        fd = (tot_p - tot_m) / (2 * h)
+        assert abs(fd - gT[0, k]) <= 1e-5 * max(1.0, abs(fd)), (k, fd, gT[0, k])
 
 
 def test_backward_closed_form_tm_2ts():
