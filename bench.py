@@ -8,15 +8,19 @@ reset to 0 (synthetic, seeded).  A step is one forward pass of the layer
 outputs) over the batch, with all inputs resident in HBM.
 
 Prints one JSON line: throughput in neuron-events/s (N_out * sum of events
-per sample, per second), the roofline of the dominant kernel, the speedup
-over the sequential one-thread-per-neuron GPU event loop, the backward time,
-and the float64 CPU oracle timed on the host cores.
+per sample, per second); the roofline of the forward pass (its algorithmic
+bytes over its duration, timed with HIP events on the launch stream, against
+the HBM peak); the speedup over the sequential one-thread-per-neuron GPU
+event loop; the backward time; the same figures for the other workloads
+(two-layer, event-camera and large shapes) as extra keys; and the float64
+CPU oracle timed on the host cores on a bounded sample.
 """
 from __future__ import annotations
 
 import argparse
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -27,6 +31,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0     # MI355X HBM3E, GB/s
+FORWARD_KERNELS = ("aggregate", "carry", "check", "records", "resolve")
 
 
 def log(*a):
@@ -34,6 +39,7 @@ def log(*a):
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_forward_700x256_b32.txt")
+L2_FILE = os.path.join(ROOT, "profiles", "l2_forward_700x256_b32.txt")
 KERNEL_SOURCES = ("lif_forward.hip", "lif_common.hpp", "lif_host.hpp", "lif_walk.hpp")
 
 
@@ -46,25 +52,141 @@ def kernel_sources_sha256() -> str:
     return h.hexdigest()
 
 
-def measured_traffic(kernel: str):
-    """HBM bytes per launch of `kernel` from the rocprofv3 FETCH_SIZE and
-    WRITE_SIZE runs summarised in profiles/ (already scaled by the copy-probe
-    factors), or None when they are missing or were taken on other kernel
-    sources than the ones built now."""
+def _profile_table(path):
+    """Rows `kernel a b` of a profile summary in profiles/, or None when it
+    is missing or was taken on other kernel sources than the ones built now."""
     try:
-        lines = open(TRAFFIC_FILE).read().splitlines()
+        lines = open(path).read().splitlines()
     except OSError:
         return None
-    sha = None
+    sha, rows = None, {}
     for ln in lines:
         if ln.startswith("sources_sha256:"):
             sha = ln.split(":", 1)[1].strip()
+            continue
         parts = ln.split()
-        if sha and len(parts) == 3 and parts[0] == kernel:
-            if sha != kernel_sources_sha256():
-                return None
-            return int(parts[1]) + int(parts[2])
-    return None
+        if not ln.startswith("#") and len(parts) == 3:
+            rows[parts[0]] = (float(parts[1]), float(parts[2]))
+    if sha != kernel_sources_sha256():
+        return None
+    return rows
+
+
+def measured_traffic():
+    """HBM bytes of one forward pass (all its kernels) from the rocprofv3
+    FETCH_SIZE and WRITE_SIZE runs summarised in profiles/ (already scaled by
+    the copy-probe factors), with the per-kernel split, or (None, None)."""
+    rows = _profile_table(TRAFFIC_FILE)
+    if not rows or not all(k in rows for k in FORWARD_KERNELS):
+        return None, None
+    per = {k: int(rows[k][0] + rows[k][1]) for k in FORWARD_KERNELS}
+    return sum(per.values()), per
+
+
+def measured_l2():
+    """L2 (TCC) hit rate per forward kernel from profiles/, or None."""
+    rows = _profile_table(L2_FILE)
+    if not rows:
+        return None
+    return {k: (h / (h + m) if h + m > 0 else None) for k, (h, m) in rows.items()}
+
+
+def fwd_alg_bytes(total_ev, N, B, spikes):
+    """Algorithmic bytes of one forward pass: per event its time and source
+    (8 B) and one float32 weight per neuron (4 B per neuron-event); the spike
+    counts (4 B per neuron); the spike time and I at each spike (8 B)."""
+    return total_ev * (8 + 4 * N) + B * N * 4 + spikes * 8
+
+
+class Dev:
+    def __init__(self, torch, dev):
+        self.torch, self.dev = torch, dev
+
+    def __call__(self, a):
+        return self.torch.from_numpy(np.ascontiguousarray(a)).to(self.dev)
+
+
+def time_steps(torch, fn, steps, warmup):
+    """Warm up, then time `steps` calls: wall clock over the whole loop
+    (bracketed by device synchronisations) and HIP events around every call
+    on the current stream (the library launches on it).  Returns (ms per
+    step by wall clock, per-step event durations in ms)."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    t0 = time.perf_counter()
+    for a, b in ev:
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps * 1e3
+    return wall, [a.elapsed_time(b) for a, b in ev]
+
+
+def stats_ms(xs):
+    return {"mean": statistics.fmean(xs), "median": statistics.median(xs),
+            "stdev": statistics.stdev(xs) if len(xs) > 1 else 0.0, "min": min(xs), "max": max(xs)}
+
+
+def run_workload(torch, lif, d, name, ev, WT, P, steps, warmup, seq_steps, backward=False):
+    """Forward (and optionally backward) timing of one workload, with the
+    sequential GPU loop on the same inputs."""
+    B, E = ev.ev_t.shape
+    C, N = WT.shape
+    total_ev = int(ev.ev_n.sum())
+    dt, ds, dn, dW = d(ev.ev_t), d(ev.ev_src), d(ev.ev_n), d(WT)
+    pc = P.c()
+    ws = torch.empty(lif.lif_layer_forward_workspace_size(B, E, C, N, pc), dtype=torch.uint8, device=d.dev)
+    out = lif.forward(dt, ds, dn, dW, P, ws=ws)
+    wall, evs = time_steps(torch, lambda: lif.forward(dt, ds, dn, dW, P, ws=ws, out=out), steps, warmup)
+    spikes = int(out.out_n.sum().item())
+    status = out.status.cpu().numpy().tolist()
+    seq = lif.forward(dt, ds, dn, dW, P, sequential=True, ws=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(seq.out_n, out.out_n), f"{name}: sequential and parallel spike counts differ"
+    seq_wall, _ = time_steps(torch, lambda: lif.forward(dt, ds, dn, dW, P, sequential=True, ws=ws, out=seq),
+                             seq_steps, 0)
+    r = {"workload": name, "batch": B, "c_in": C, "n_out": N, "events": total_ev, "e_max": E,
+         "neuron_events": N * total_ev, "spikes": spikes, "forward_ms": wall,
+         "forward_event_ms": stats_ms(evs), "neuron_events_per_s": N * total_ev / (wall * 1e-3),
+         "hbm_frac": fwd_alg_bytes(total_ev, N, B, spikes) / (wall * 1e-3) / 1e9 / HBM_PEAK_GBS,
+         "sequential_ms": seq_wall, "speedup_vs_sequential": seq_wall / wall, "status": status,
+         "workspace_bytes": int(ws.numel())}
+    if backward:
+        rng = np.random.default_rng(1)
+        valid = np.isfinite(out.out_t.cpu().numpy())
+        g = d((rng.standard_normal(valid.shape) * valid).astype(np.float32))
+        bws = torch.empty(lif.lif_layer_backward_workspace_size(B, E, C, N, pc), dtype=torch.uint8, device=d.dev)
+        bwall, bevs = time_steps(torch, lambda: lif.backward(dt, ds, dn, dW, out, g, P, ws=bws),
+                                 max(3, steps // 2), 2)
+        r["backward_ms"] = bwall
+        r["backward_event_ms"] = stats_ms(bevs)
+    log(f"[bench] {name}: forward {wall * 1e3:.1f} us ({r['neuron_events_per_s']:.3e} neuron-events/s, "
+        f"{r['hbm_frac']:.1%} of HBM peak), sequential {seq_wall:.3f} ms ({r['speedup_vs_sequential']:.1f}x)"
+        + (f", backward {r['backward_ms'] * 1e3:.1f} us" if backward else "") + f", {spikes} spikes")
+    del ws
+    return r
+
+
+def cpu_oracle(ev, WT, nthreads, seconds, n_samples, n_neurons):
+    """The float64 oracle on a bounded sample of a workload (the first
+    n_samples samples and n_neurons neurons), repeated for about `seconds`;
+    returns (neuron-events per second, seconds per call, repetitions)."""
+    import oracle
+    OP = oracle.LifParams(s_max=64)
+    sub = np.ascontiguousarray(WT[:, :n_neurons])
+    args = (ev.ev_t[:n_samples], ev.ev_src[:n_samples], ev.ev_n[:n_samples], sub, OP)
+    oracle.forward(*args, nthreads=nthreads)
+    reps = 0
+    c0 = time.perf_counter()
+    while reps < 2 or time.perf_counter() - c0 < seconds:
+        oracle.forward(*args, nthreads=nthreads)
+        reps += 1
+    per = (time.perf_counter() - c0) / reps
+    ne = int(ev.ev_n[:n_samples].sum()) * sub.shape[1]
+    return ne / per, per, reps
 
 
 def main():
@@ -74,8 +196,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--seq-steps", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true", help="time the headline workload only")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
-                    help="CPU oracle baseline: repeat the full-batch forward until this much time has passed")
+                    help="CPU oracle baseline: repeat the bounded sample until this much time has passed")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run one plain device-to-device copy of BYTES bytes (calibrates the HBM byte "
                          "counters of a profiler against a kernel of known traffic) and exit")
@@ -100,6 +223,7 @@ def main():
         torch.cuda.synchronize()
         log(f"[bench] copy probe: {n * 4} bytes read, {n * 4} bytes written")
         return
+    d = Dev(torch, dev)
     cfg = W.config2()
     ev, WT = cfg.events, cfg.layers[0].WT
     B, E = ev.ev_t.shape
@@ -107,141 +231,114 @@ def main():
     total_ev = int(ev.ev_n.sum())
     neuron_events = N * total_ev
     P = lif.Params(s_max=64)
-    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
-    d_t, d_s, d_n, d_W = t(ev.ev_t), t(ev.ev_src), t(ev.ev_n), t(WT)
+    d_t, d_s, d_n, d_W = d(ev.ev_t), d(ev.ev_src), d(ev.ev_n), d(WT)
     pc = P.c()
     ws = torch.empty(lif.lif_layer_forward_workspace_size(B, E, C, N, pc), dtype=torch.uint8, device=dev)
     out = lif.forward(d_t, d_s, d_n, d_W, P, ws=ws)
     torch.cuda.synchronize()
     log(f"[bench] {cfg.name}: B={B} E_max={E} events={total_ev} N={N} neuron-events={neuron_events} "
         f"lib={lif.lif_version()}")
+    fwd = lambda: lif.forward(d_t, d_s, d_n, d_W, P, ws=ws, out=out)
 
-    # ---- per-kernel durations: eager launches bracketed by HIP events on the
-    # launch stream (the library's kernel timer)
+    # ---- per-kernel durations: every launch bracketed by HIP events that
+    # its own dispatch records (the library's kernel timer)
     lif.lif_timer_enable(True)
     for _ in range(args.warmup):
-        lif.forward(d_t, d_s, d_n, d_W, P, ws=ws, out=out)
+        fwd()
     torch.cuda.synchronize()
     lif.lif_timer_enable(True)
     for _ in range(args.steps):
-        lif.forward(d_t, d_s, d_n, d_W, P, ws=ws, out=out)
+        fwd()
     torch.cuda.synchronize()
     kern = lif.lif_timer_read()
     lif.lif_timer_enable(False)
-    log(f"[bench] kernels: " + ", ".join(f"{k}={v[0] / v[1] * 1e3:.1f}us" for k, v in kern.items()))
+    kern_us = {k: v[0] / v[1] * 1e3 for k, v in kern.items()}
+    log("[bench] kernels: " + ", ".join(f"{k}={v:.1f}us" for k, v in kern_us.items()))
 
-    # ---- eager forward steps (no timer)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        lif.forward(d_t, d_s, d_n, d_W, P, ws=ws, out=out)
-    torch.cuda.synchronize()
-    eager_ms = (time.perf_counter() - t0) / args.steps * 1e3
+    # ---- the timed steps: eager forward calls
+    ms_step, ev_ms = time_steps(torch, fwd, args.steps, args.warmup)
+    fst = stats_ms(ev_ms)
     ref_t, ref_n, ref_st = out.out_t.clone(), out.out_n.clone(), out.status.clone()
+    value = neuron_events / (ms_step * 1e-3)
+    status = out.status.cpu().numpy().tolist()
+    n_spikes = int(out.out_n.sum().item())
 
-    # ---- timed steps: the forward call captured once in a HIP graph and
-    # replayed (the call allocates nothing and issues only kernel launches)
+    # ---- the same call captured once in a HIP graph and replayed
     gstream = torch.cuda.Stream()
     gstream.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(gstream):
-        lif.forward(d_t, d_s, d_n, d_W, P, ws=ws, out=out)
+        fwd()
     torch.cuda.current_stream().wait_stream(gstream)
     torch.cuda.synchronize()
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
-        lif.forward(d_t, d_s, d_n, d_W, P, ws=ws, out=out)
-    for _ in range(args.warmup):
-        graph.replay()
-    torch.cuda.synchronize()
+        fwd()
+    graph_ms, _ = time_steps(torch, graph.replay, args.steps, args.warmup)
     assert torch.equal(out.out_t, ref_t) and torch.equal(out.out_n, ref_n) and torch.equal(out.status, ref_st), \
         "graph replay differs from the eager forward"
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        graph.replay()
-    torch.cuda.synchronize()
-    graph_ms = (time.perf_counter() - t0) / args.steps * 1e3
-    # The reported step is the plain (eager) library call.
-    ms_step = eager_ms
-    value = neuron_events / (ms_step * 1e-3)
-    status = out.status.cpu().numpy().tolist()
-    n_spikes = int(out.out_n.sum().item())
-    log(f"[bench] forward {ms_step * 1e3:.1f} us/step eager, {graph_ms * 1e3:.1f} us/step graph replay, "
+    log(f"[bench] forward {ms_step * 1e3:.1f} us/step eager (events: median {fst['median'] * 1e3:.1f}, "
+        f"stdev {fst['stdev'] * 1e3:.1f} us), {graph_ms * 1e3:.1f} us/step graph replay, "
         f"{value:.3e} neuron-events/s, status {status}")
 
-    # ---- roofline of the dominant kernel.  Algorithmic bytes per launch:
-    #   aggregate, check: every event record (time + source, 8 B) and one
-    #     float32 weight per neuron-event (4 B) -- both passes gather the
-    #     whole W^T row slice of every event;
-    #   carry: one float64 (V, I) aggregate read and one carry written per
-    #     (sample, segment, neuron);
-    #   records: per record its entering state (16 B), the 16 weights, event
-    #     times and decay records of its sub-block (4 + 4 + 32 B each) and the
-    #     record written (17 x 40 B);
-    #   resolve: per walked sub-block, for each of its 16 intervals, the
-    #     record's state and crossing data (16 + 24 B) and the interval's
-    #     start time (4 B); plus 8 B per spike and 4 B per count.
-    S = (E + 63) // 64                       # 64-event scan segments
-    walked = status[4]
-    alg = {"prep": B * S * 64 * 32 + total_ev * 4 + B * N * P.s_max * 8,
-           "aggregate": total_ev * (8 + 4 * N),
-           "check": total_ev * (8 + 4 * N),
-           "carry": B * S * N * 32,
-           "records": walked * (16 + 16 * 40 + 17 * 40),
-           "resolve": walked * 16 * (16 + 24 + 4) + n_spikes * 8 + B * N * 4}
-    kern_us = {k: v[0] / v[1] * 1e3 for k, v in kern.items()}
-    dom_name = max(kern_us, key=kern_us.get)
-    dom_us = kern_us[dom_name]
-    alg_bytes = alg.get(dom_name, 0)
-    achieved = alg_bytes / (dom_us * 1e-6) / 1e9
-    fwd_alg_bytes = total_ev * (8 + 4 * N) + B * N * 4 + n_spikes * 8
-    traffic = measured_traffic(dom_name)
+    # ---- roofline of the forward pass: its algorithmic bytes over its
+    # duration (HIP events on the launch stream, mean over the timed steps)
+    alg_bytes = fwd_alg_bytes(total_ev, N, B, n_spikes)
+    achieved = alg_bytes / (fst["mean"] * 1e-3) / 1e9
+    traffic, traffic_per_kernel = measured_traffic()
+    l2 = measured_l2()
 
     # ---- sequential GPU baseline (same ABI, same inputs)
     seq = lif.forward(d_t, d_s, d_n, d_W, P, sequential=True, ws=ws)
     torch.cuda.synchronize()
     assert torch.equal(seq.out_n, out.out_n), "sequential and parallel spike counts differ"
-    ts0 = time.perf_counter()
-    for _ in range(args.seq_steps):
-        lif.forward(d_t, d_s, d_n, d_W, P, sequential=True, ws=ws, out=seq)
-    torch.cuda.synchronize()
-    seq_ms = (time.perf_counter() - ts0) / args.seq_steps * 1e3
+    seq_ms, _ = time_steps(torch, lambda: lif.forward(d_t, d_s, d_n, d_W, P, sequential=True, ws=ws, out=seq),
+                           args.seq_steps, 0)
     log(f"[bench] sequential {seq_ms:.3f} ms/step, speedup {seq_ms / ms_step:.1f}x")
 
     # ---- backward pass on the same batch (dL/dt ~ N(0,1) on every spike)
     rng = np.random.default_rng(1)
     valid = np.isfinite(out.out_t.cpu().numpy())
-    g = t((rng.standard_normal(valid.shape) * valid).astype(np.float32))
+    g = d((rng.standard_normal(valid.shape) * valid).astype(np.float32))
     bws = torch.empty(lif.lif_layer_backward_workspace_size(B, E, C, N, pc), dtype=torch.uint8, device=dev)
-    for _ in range(3):
-        lif.backward(d_t, d_s, d_n, d_W, out, g, P, ws=bws)
-    torch.cuda.synchronize()
-    tb0 = time.perf_counter()
-    nb = max(5, args.steps // 5)
-    for _ in range(nb):
-        lif.backward(d_t, d_s, d_n, d_W, out, g, P, ws=bws)
-    torch.cuda.synchronize()
-    bwd_ms = (time.perf_counter() - tb0) / nb * 1e3
+    bwd_ms, bev = time_steps(torch, lambda: lif.backward(d_t, d_s, d_n, d_W, out, g, P, ws=bws),
+                             max(5, args.steps // 5), 3)
     log(f"[bench] backward {bwd_ms * 1e3:.1f} us/step")
+    del ws, bws
 
-    # ---- float64 CPU oracle on the host cores (full batch, repeated)
+    # ---- the other workloads (extra keys; the headline stays the one above)
+    extras = {}
+    if not args.no_extras:
+        st, wu = max(3, args.steps // 10), 2
+        c3 = W.config3()
+        extras["c3_layer1"] = run_workload(torch, lif, d, "700->512 layer 1 of 700->512->512, B=128, ~10k events",
+                                           c3.events, c3.layers[0].WT, lif.Params(s_max=128), st, wu, 1)
+        c4 = W.config4()
+        extras["c4"] = run_workload(torch, lif, d, "2312->1024, B=64, ~20k events in 3 bursts", c4.events,
+                                    c4.layers[0].WT, lif.Params(s_max=64), st, wu, 1)
+        c5 = W.config5()
+        extras["c5_hidden"] = run_workload(torch, lif, d, "32768->2048, B=16, ~100k events (stated gain 4)",
+                                           c5.events, c5.layers[0].WT, lif.Params(s_max=64), st, wu, 1,
+                                           backward=True)
+        W1d = (c5.layers[0].WT * 4.0).astype(np.float32)    # gain 16: the driven variant of the parity tests
+        extras["c5_hidden_driven"] = run_workload(torch, lif, d, "32768->2048, B=16, ~100k events, gain 16",
+                                                  c5.events, W1d, lif.Params(s_max=64), st, wu, 1, backward=True)
+        del c3, c4, c5, W1d
+
+    # ---- float64 CPU oracle on the host cores (bounded samples)
     cpu = None
+    cpu1 = None
     if not args.no_cpu_baseline:
-        import oracle
         ncores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
         ncores = max(1, min(int(ncores), 16))
-        OP = oracle.LifParams(s_max=64)
-        oracle.forward(ev.ev_t[:1], ev.ev_src[:1], ev.ev_n[:1], WT, OP, nthreads=ncores)
-        reps = 0
-        c0 = time.perf_counter()
-        while reps < 3 or time.perf_counter() - c0 < args.cpu_seconds:
-            oracle.forward(ev.ev_t, ev.ev_src, ev.ev_n, WT, OP, nthreads=ncores)
-            reps += 1
-        cpu_s = (time.perf_counter() - c0) / reps
-        cpu = {"value": neuron_events / cpu_s, "unit": "neuron-events/s", "cores": ncores, "kind": "oracle",
-               "sample": f"the full workload (32 samples x 256 neurons, {total_ev} events) repeated {reps} times, "
-                         f"{cpu_s:.3f} s each, float64, one thread per core over (sample, neuron)"}
-        log(f"[bench] cpu oracle {cpu_s:.3f} s/forward on {ncores} threads")
+        rate, per, reps = cpu_oracle(ev, WT, ncores, args.cpu_seconds, B, N)
+        cpu = {"value": rate, "unit": "neuron-events/s", "cores": ncores, "kind": "oracle",
+               "sample": f"the full workload (32 samples x 256 neurons, {total_ev} events), repeated {reps} "
+                         f"times, {per:.3f} s each; float64, one thread per core over (sample, neuron)"}
+        rate1, per1, reps1 = cpu_oracle(ev, WT, 1, args.cpu_seconds / 2, 4, N)
+        cpu1 = {"value": rate1, "unit": "neuron-events/s", "cores": 1, "kind": "oracle",
+                "sample": f"4 samples x 256 neurons ({int(ev.ev_n[:4].sum())} events), repeated {reps1} times, "
+                          f"{per1:.3f} s each; float64, one thread"}
+        log(f"[bench] cpu oracle {per:.3f} s/forward on {ncores} threads; {rate1:.3e} neuron-events/s on one")
 
     line = {
         "metric": "neuron-events/s fwd (700->256, B=32)",
@@ -251,6 +348,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_step,
+        "step_event_ms": fst,
         "ms_per_step_graph_replay": graph_ms,
         "higher_is_better": True,
         "scaling": "weak",
@@ -262,16 +360,20 @@ def main():
                                "tau_m 20 ms, tau_s 5 ms, threshold 1, reset 0",
                    "batch": B, "c_in": C, "n_out": N, "events": total_ev, "e_max": E,
                    "neuron_events": neuron_events, "spikes": n_spikes, "s_max": P.s_max},
-        "roofline": {"bound": "hbm", "kernel": dom_name, "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "alg_bytes_per_launch": alg_bytes, "kernel_us": dom_us},
-        "hbm_frac_forward": fwd_alg_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "roofline": {"bound": "hbm", "kernel": "forward pass (" + " + ".join(FORWARD_KERNELS) + ")",
+                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic, "alg_bytes_per_launch": alg_bytes, "launch_us": fst["mean"] * 1e3,
+                     "traffic_per_kernel": traffic_per_kernel, "l2_hit_rate": l2},
+        "hbm_frac_forward": alg_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "kernels_us": kern_us,
         "sequential_ms": seq_ms,
         "speedup_vs_sequential": seq_ms / ms_step,
         "backward_ms": bwd_ms,
+        "backward_event_ms": stats_ms(bev),
         "status": status,
+        "other_workloads": extras,
         "cpu_baseline": cpu,
+        "cpu_baseline_1thread": cpu1,
     }
     print(json.dumps(line), flush=True)
 

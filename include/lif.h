@@ -8,7 +8,8 @@
  *     allocates and owns every buffer (outputs and workspace included).  The
  *     library never allocates device memory, never synchronises the stream
  *     and keeps no state between calls (except the optional kernel timer,
- *     see lif_timer_*).
+ *     see lif_timer_*).  Every behaviour is set by the arguments (no
+ *     environment variables are read).
  *   - Work is enqueued on `stream` (a hipStream_t; NULL is the null stream)
  *     and the call returns at once.  Calls on different streams with
  *     distinct buffers may run concurrently.
@@ -54,7 +55,12 @@ typedef struct ihipStream_t* lif_stream_t;
    offsets); B * E_max < 2^40. */
 
 /* lif_params.flags */
-#define LIF_VALIDATE  1u  /* check sorted times, finite values, source range */
+#define LIF_VALIDATE      1u  /* check sorted times, finite values, source range */
+#define LIF_ROOT_GENERAL  2u  /* solve spike times with the exponential Newton
+                                 iteration even when tau_m / tau_s is an integer
+                                 plus one (where a polynomial solve is used by
+                                 default); both give the same spike times to
+                                 float64 rounding.  For tests of that path.    */
 
 /* Device status words written by every forward call (int32 each). */
 #define LIF_STATUS_WORDS     8
@@ -85,9 +91,16 @@ typedef struct lif_params {
                             (events later than t_end are still consumed; the
                             open interval is then empty)                        */
     int32_t  s_max;      /* output spike capacity per neuron, >= 1 (App. E.2)   */
-    uint32_t flags;      /* LIF_VALIDATE                                        */
+    uint32_t flags;      /* LIF_VALIDATE, LIF_ROOT_GENERAL                      */
     double   solver_reg; /* backward floor on dV/dt at a spike (paper 0.01,
-                            Table 4 "Solver Regularization"); 0 disables it     */
+                            App. E hyperparameter table, "Solver
+                            Regularization"); 0 disables it                     */
+    int32_t  pool_cap;   /* forward: record slots per sample for flagged
+                            event blocks; < 0 selects the library's default.
+                            Blocks past the slots are rebuilt by a slower path
+                            with identical results (0: every block is; for
+                            tests of that path).  Enters the workspace size.  */
+    int32_t  reserved;   /* must be 0                                           */
 } lif_params;
 
 /* Library version string (static storage). */
@@ -109,6 +122,12 @@ const char* lif_version(void);
 /*   out_i  float [B][N_out][s_max] synaptic current I at each spike (the  */
 /*                             backward pass needs it); 0 padding; may be  */
 /*                             NULL                                        */
+/*   out_k  int32 [B][N_out][s_max] input events consumed before each      */
+/*                             spike: the spike lies in the interval that  */
+/*                             event out_k closes (or after the last event */
+/*                             when out_k = ev_n[b]), and depends on       */
+/*                             events 0 .. out_k - 1 only; 0 padding; the  */
+/*                             backward pass needs it; may be NULL         */
 /*   status int32 [LIF_STATUS_WORDS]                                       */
 /*   ws     device workspace of ws_bytes >= lif_layer_forward_workspace_size */
 /* The spike times are exact up to float64 rounding of the closed-form     */
@@ -118,7 +137,7 @@ size_t lif_layer_forward_workspace_size(int B, int E_max, int C_in, int N_out, c
 
 int lif_layer_forward(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
                       const float* WT, int C_in, int N_out, const lif_params* p,
-                      float* out_t, int32_t* out_n, float* out_i, int32_t* status,
+                      float* out_t, int32_t* out_n, float* out_i, int32_t* out_k, int32_t* status,
                       void* ws, size_t ws_bytes, lif_stream_t stream);
 
 /* The sequential baseline (paper Appendix E.3): one GPU thread per
@@ -127,28 +146,31 @@ int lif_layer_forward(const float* ev_t, const int32_t* ev_src, const int32_t* e
  * its workspace size is lif_layer_forward_workspace_size as well. */
 int lif_layer_forward_sequential(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B,
                                  int E_max, const float* WT, int C_in, int N_out, const lif_params* p,
-                                 float* out_t, int32_t* out_n, float* out_i, int32_t* status,
-                                 void* ws, size_t ws_bytes, lif_stream_t stream);
+                                 float* out_t, int32_t* out_n, float* out_i, int32_t* out_k,
+                                 int32_t* status, void* ws, size_t ws_bytes, lif_stream_t stream);
 
 /* --------------------------------------------------------------------- */
 /* Backward pass (paper Appendix D.3, Eq. ift_vjp, chained through the     */
 /* hard resets): given dL/dt for every output spike, returns dL/dW and     */
 /* dL/d(event time).                                                       */
 /*                                                                         */
-/*   out_t, out_n, out_i  the forward results for the same inputs          */
-/*                        (out_i is required here)                         */
+/*   out_t, out_n, out_i, out_k  the forward results for the same inputs */
+/*                        (out_i and out_k are required here)              */
 /*   grad_out_t float [B][N_out][s_max]  dL/dt_s; padding entries ignored  */
 /*   grad_WT    float [C_in][N_out]      overwritten with dL/dWT           */
 /*   grad_ev_t  float [B][E_max]         overwritten with dL/dev_t (0 on   */
 /*                                       padding); may be NULL             */
-/* dV/dt at each spike is floored at p->solver_reg.  grad_WT sums over     */
-/* samples with float atomics, so its last bits depend on timing.          */
+/* dV/dt at each spike is floored at p->solver_reg.  Which input events a  */
+/* spike depends on is read from out_k, not from comparing the (float32)   */
+/* times, so an event that the rounding of a spike time puts at the same   */
+/* time still counts as before it.  grad_WT sums over samples with float64 */
+/* atomics, so its last bits can depend on timing.                         */
 /* --------------------------------------------------------------------- */
 size_t lif_layer_backward_workspace_size(int B, int E_max, int C_in, int N_out, const lif_params* p);
 
 int lif_layer_backward(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
                        const float* WT, int C_in, int N_out, const lif_params* p,
-                       const float* out_t, const int32_t* out_n, const float* out_i,
+                       const float* out_t, const int32_t* out_n, const float* out_i, const int32_t* out_k,
                        const float* grad_out_t, float* grad_WT, float* grad_ev_t,
                        void* ws, size_t ws_bytes, lif_stream_t stream);
 
@@ -159,7 +181,9 @@ int lif_layer_backward(const float* ev_t, const int32_t* ev_src, const int32_t* 
 /*   out_t, out_n   a forward result, [B][N][s_max] and [B][N]             */
 /*   ev_t2   float [B][E2_max]  merged times (+INFINITY padding)           */
 /*   ev_src2 int32 [B][E2_max]  source = emitting neuron index             */
-/*   ev_n2   int32 [B]          merged counts (clipped at E2_max)          */
+/*   ev_n2   int32 [B]          merged counts (clipped at E2_max: a sample */
+/*                              with more spikes keeps its E2_max earliest  */
+/*                              in (time, neuron) order)                    */
 /*   perm    int32 [B][E2_max]  i*s_max + s of each merged spike, -1 on    */
 /*                              padding; may be NULL                       */
 /*   status  int32 [LIF_STATUS_WORDS] (LIF_WARN_MERGE_FULL on overflow)    */

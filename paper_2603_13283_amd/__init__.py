@@ -35,6 +35,7 @@ ERR_NAMES = {LIF_ERR_ARG: "LIF_ERR_ARG", LIF_ERR_TAU: "LIF_ERR_TAU", LIF_ERR_THR
              LIF_ERR_WORKSPACE: "LIF_ERR_WORKSPACE", LIF_ERR_HIP: "LIF_ERR_HIP", LIF_ERR_SIZE: "LIF_ERR_SIZE"}
 
 LIF_VALIDATE = 1
+LIF_ROOT_GENERAL = 2
 LIF_STATUS_WORDS = 8
 ST_FLAGS, ST_CAPPED, ST_SPIKES, ST_CAND_BLOCKS, ST_WALKED_BLOCKS, ST_ROOT_SOLVES, ST_EVENTS, ST_POOL_FALLBACK = range(8)
 WARN_SPIKE_CAP, WARN_UNSORTED, WARN_BAD_SOURCE, WARN_NONFINITE, WARN_MERGE_FULL, WARN_BAD_COUNT = 1, 2, 4, 8, 16, 32
@@ -59,12 +60,14 @@ class LifError(RuntimeError):
 class lif_params(ctypes.Structure):
     _fields_ = [("tau_mem", ctypes.c_double), ("tau_syn", ctypes.c_double), ("v_th", ctypes.c_double),
                 ("v_reset", ctypes.c_double), ("t_end", ctypes.c_double), ("s_max", ctypes.c_int32),
-                ("flags", ctypes.c_uint32), ("solver_reg", ctypes.c_double)]
+                ("flags", ctypes.c_uint32), ("solver_reg", ctypes.c_double), ("pool_cap", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 @dataclass
 class Params:
-    """Layer constants (defaults: paper Table 4, SHD/SSC columns)."""
+    """Layer constants (defaults: the paper's hyperparameter table in App. E,
+    SHD/SSC columns) and the per-call options of lif_params."""
     tau_mem: float = 0.02
     tau_syn: float = 0.005
     v_th: float = 1.0
@@ -73,10 +76,13 @@ class Params:
     s_max: int = 64
     solver_reg: float = 0.01
     validate: bool = False
+    root_general: bool = False
+    pool_cap: int = -1
 
     def c(self) -> lif_params:
+        flags = (LIF_VALIDATE if self.validate else 0) | (LIF_ROOT_GENERAL if self.root_general else 0)
         return lif_params(self.tau_mem, self.tau_syn, self.v_th, self.v_reset, self.t_end, int(self.s_max),
-                          LIF_VALIDATE if self.validate else 0, self.solver_reg)
+                          flags, self.solver_reg, int(self.pool_cap), 0)
 
 
 _lib = None
@@ -101,13 +107,14 @@ def load(path: Optional[str] = None):
         f = getattr(lib, name)
         f.restype = _SZ
         f.argtypes = [_I, _I, _I, _I, _PP]
-    fwd_args = [_P, _P, _P, _I, _I, _P, _I, _I, _PP, _P, _P, _P, _P, _P, _SZ, _P]
+    fwd_args = [_P, _P, _P, _I, _I, _P, _I, _I, _PP, _P, _P, _P, _P, _P, _P, _SZ, _P]
     for name in ("lif_layer_forward", "lif_layer_forward_sequential"):
         f = getattr(lib, name)
         f.restype = _I
         f.argtypes = fwd_args
     lib.lif_layer_backward.restype = _I
-    lib.lif_layer_backward.argtypes = [_P, _P, _P, _I, _I, _P, _I, _I, _PP, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]
+    lib.lif_layer_backward.argtypes = [_P, _P, _P, _I, _I, _P, _I, _I, _PP, _P, _P, _P, _P, _P, _P, _P, _P, _SZ,
+                                       _P]
     lib.lif_merge_workspace_size.restype = _SZ
     lib.lif_merge_workspace_size.argtypes = [_I, _I, _I, _I]
     lib.lif_merge_spikes.restype = _I
@@ -218,6 +225,7 @@ class ForwardOut:
     out_n: "object"     # int32 [B, N]
     out_i: "object"     # float32 [B, N, s_max]
     status: "object"    # int32 [LIF_STATUS_WORDS]
+    out_k: "object" = None   # int32 [B, N, s_max]: input events consumed before each spike
 
 
 def forward(ev_t, ev_src, ev_n, WT, params: Params = Params(), sequential: bool = False, stream=None,
@@ -231,13 +239,15 @@ def forward(ev_t, ev_src, ev_n, WT, params: Params = Params(), sequential: bool 
         out = ForwardOut(torch.empty((B, N, params.s_max), dtype=torch.float32, device=dev),
                          torch.empty((B, N), dtype=torch.int32, device=dev),
                          torch.empty((B, N, params.s_max), dtype=torch.float32, device=dev),
-                         torch.empty(LIF_STATUS_WORDS, dtype=torch.int32, device=dev))
+                         torch.empty(LIF_STATUS_WORDS, dtype=torch.int32, device=dev),
+                         torch.empty((B, N, params.s_max), dtype=torch.int32, device=dev))
     need = lif_layer_forward_workspace_size(B, E, C, N, p)
     if ws is None or ws.numel() < need:
         ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     fn = lif_layer_forward_sequential if sequential else lif_layer_forward
     rc = fn(_ptr(ev_t), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(WT), C, N, ctypes.byref(p), _ptr(out.out_t),
-            _ptr(out.out_n), _ptr(out.out_i), _ptr(out.status), _ptr(ws), ws.numel(), _stream(stream))
+            _ptr(out.out_n), _ptr(out.out_i), _ptr(out.out_k), _ptr(out.status), _ptr(ws), ws.numel(),
+            _stream(stream))
     _check(fn.__name__, rc)
     return out
 
@@ -256,8 +266,8 @@ def backward(ev_t, ev_src, ev_n, WT, fwd: ForwardOut, grad_out_t, params: Params
         ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     g = grad_out_t.contiguous().to(torch.float32)
     rc = lif_layer_backward(_ptr(ev_t), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(WT), C, N, ctypes.byref(p),
-                            _ptr(fwd.out_t), _ptr(fwd.out_n), _ptr(fwd.out_i), _ptr(g), _ptr(gW), _ptr(gT),
-                            _ptr(ws), ws.numel(), _stream(stream))
+                            _ptr(fwd.out_t), _ptr(fwd.out_n), _ptr(fwd.out_i), _ptr(fwd.out_k), _ptr(g), _ptr(gW),
+                            _ptr(gT), _ptr(ws), ws.numel(), _stream(stream))
     _check("lif_layer_backward", rc)
     return gW, gT
 

@@ -17,6 +17,7 @@ int check_params(const lif_params* p)
         return LIF_ERR_THRESHOLD;
     if (p->s_max < 1) return LIF_ERR_ARG;
     if (isnan(p->t_end) || !(p->solver_reg >= 0.0)) return LIF_ERR_ARG;
+    if (p->reserved != 0 || (p->flags & ~(LIF_VALIDATE | LIF_ROOT_GENERAL))) return LIF_ERR_ARG;
     return LIF_OK;
 }
 
@@ -51,7 +52,7 @@ Model make_model(const lif_params& p)
     m.p_int = 0;
     for (int q = 1; q <= 4; ++q)
         if (p.tau_mem / p.tau_syn == (double)(q + 1)) m.p_int = q;
-    if (const char* env = getenv("LIF_ROOT_GENERAL")) if (atoi(env)) m.p_int = 0;
+    if (p.flags & LIF_ROOT_GENERAL) m.p_int = 0;
     m.s_max = p.s_max;
     m.flags = p.flags;
     return m;

@@ -12,12 +12,17 @@
 // With mu_s the adjoint of constraint F_s,
 //   lambda_s = g_s - ((V_th - V_reset)/tm) sum_{s'' > s} mu_s'' e^{-(t_s'' - t_s)/tm}
 //   mu_s     = -lambda_s / max(dV/dt(t_s), reg)                  (k_spike_adjoint)
-// and every input event k collects, with P^m_k = sum_{t_s > t_k} mu_s
-// e^{-(t_s - t_k)/tm} and P^s_k the same with ts,
+// and every input event k collects, with P^m_k = sum over the spikes s
+// that come after event k of mu_s e^{-(t_s - t_k)/tm} and P^s_k the same
+// with ts,
 //   dL/dw_{i, src_k} += kappa (P^m_k - P^s_k)
 //   dL/dt_k          += w_{i, src_k} kappa (P^m_k / tm - P^s_k / ts).
+// Spike s comes after event k iff k < out_k[s], the forward pass's own count
+// of the events consumed before the spike (not a comparison of float32
+// times, which can round a spike onto the time of the event before it; the
+// offset t_s - t_k is then taken as 0).
 // P^m, P^s obey a reverse recurrence with the same per-event decays as the
-// forward scan, P_{k-1} = M P_k + (spike injections in (t_{k-1}, t_k]),
+// forward scan, P_{k-1} = M P_k + (the spikes with out_k = k),
 // which k_event_adjoint walks backwards per (sample, 64-neuron tile,
 // segment); each segment starts from the closed-form sums over the
 // (few) spikes that follow it, so segments are independent.  The walk is
@@ -31,7 +36,7 @@ namespace lif {
 
 struct BwdLayout {
     int S, E_pad;
-    size_t dec, mu, last, gw, gt, total;
+    size_t dec, mu, klast, gw, gt, total;
 };
 
 static BwdLayout bwd_layout(int B, int E_max, int C_in, int N, int s_max)
@@ -43,7 +48,7 @@ static BwdLayout bwd_layout(int B, int E_max, int C_in, int N, int s_max)
     auto take = [&](size_t bytes) { size_t o = off; off += (bytes + 255) & ~(size_t)255; return o; };
     L.dec = take((size_t)B * L.E_pad * sizeof(Decay));
     L.mu = take((size_t)B * N * s_max * sizeof(double));
-    L.last = take((size_t)B * N * sizeof(float));
+    L.klast = take((size_t)B * N * sizeof(int32_t));
     L.gw = take((size_t)C_in * N * sizeof(double));
     L.gt = take((size_t)B * E_max * sizeof(double));
     L.total = off + 256;
@@ -57,15 +62,16 @@ static BwdLayout bwd_layout(int B, int E_max, int C_in, int N, int s_max)
 // over its spikes:
 //   lambda_s = g_s - ((V_th - V_reset)/tm) sum_{s'' > s} mu_s'' e^{-(t_s'' - t_s)/tm}
 //   mu_s     = -lambda_s / max(dV/dt(t_s), reg)
-// with the time of its last spike (-inf when silent).
+// with the consumed-event count of its last spike (0 when silent): events
+// from there on feed no spike.
 __global__ __launch_bounds__(256) void k_bwd_setup(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_n,
                                                    int B, int E_max, int E_pad, int N, Model m,
                                                    Decay* __restrict__ dec, double* __restrict__ gw, size_t nW,
                                                    double* __restrict__ gt, size_t nT,
                                                    const float* __restrict__ out_t, const int32_t* __restrict__ out_n,
-                                                   const float* __restrict__ out_i,
+                                                   const float* __restrict__ out_i, const int32_t* __restrict__ out_k,
                                                    const float* __restrict__ grad_out_t, double* __restrict__ mu,
-                                                   float* __restrict__ last)
+                                                   int32_t* __restrict__ klast)
 {
     const size_t gtid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     const size_t gs = (size_t)gridDim.x * blockDim.x;
@@ -101,7 +107,7 @@ __global__ __launch_bounds__(256) void k_bwd_setup(const float* __restrict__ ev_
             mo[s] = mu_s;
             mu_next = mu_s;
         }
-        last[idx] = ns > 0 ? ts[ns - 1] : -INFINITY;
+        klast[idx] = ns > 0 ? out_k[idx * (size_t)m.s_max + ns - 1] : 0;
     }
 }
 
@@ -143,13 +149,14 @@ __device__ __forceinline__ double group_sum8(const double (&v)[kGrp], int lane)
 // events backwards: at event k, dL/dw += kappa (P^m - P^s) (one atomic per
 // live lane) and dL/dt_k += sum over lanes of w kappa (P^m/tm - P^s/ts)
 // (one atomic per event); then P decays to event k-1 and takes the spikes
-// in (t_{k-1}, t_k].  A lane is live while its neuron has a spike after
-// the event.
+// with out_k = k (those between events k-1 and k).  A lane is live while its
+// neuron has a spike after the event.
 __global__ __launch_bounds__(kWave * kWalkWaves) void k_event_adjoint(
     const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
     int E_pad, const float* __restrict__ WT, int C_in, int N, int tiles, int S, int items, Model m,
     const Decay* __restrict__ dec, const float* __restrict__ out_t, const int32_t* __restrict__ out_n,
-    const double* __restrict__ mu, const float* __restrict__ last, double* __restrict__ gWT, double* __restrict__ gT)
+    const int32_t* __restrict__ out_k, const double* __restrict__ mu, const int32_t* __restrict__ klast,
+    double* __restrict__ gWT, double* __restrict__ gT)
 {
     __shared__ double2 s_ad[kWalkWaves][kSeg];
     __shared__ float s_t[kWalkWaves][kSeg];
@@ -160,8 +167,8 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_event_adjoint(
     const int n = c.tile * kWave + lane;
     const float* tt = ev_t + (size_t)c.b * E_max;
     // only neurons with a spike after the segment's first event take part
-    const float tlast = c.live ? last[(size_t)c.b * N + n] : -INFINITY;
-    const bool liv = tlast > tt[c.k0];
+    const int kl = c.live ? klast[(size_t)c.b * N + n] : 0;
+    const bool liv = kl > c.k0;
     if (__ballot(liv) == 0ull) return;
     double2* lad = s_ad[wv];
     float* lt = s_t[wv];
@@ -173,21 +180,25 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_event_adjoint(
         if (e < c.cnt) lt[e] = tt[c.k0 + e];
     }
     wave_lds_sync();
-    // closed-form P at the segment's last event: the spikes strictly later
+    // closed-form P at the segment's last event: the spikes after it
     const size_t base = ((size_t)c.b * N + c.n0) * (size_t)m.s_max;
     const float* ts = out_t + base;
+    const int32_t* ks = out_k + base;
     const double* mo = mu + base;
     const int ns = liv ? min(out_n[(size_t)c.b * N + c.n0], m.s_max) : 0;
+    const int elast = c.k0 + c.cnt - 1;
     const double tk = (double)lt[c.cnt - 1];
     double Pm = 0.0, Ps = 0.0;
     int sp = ns;                                 // spikes sp .. ns-1 are already in P
-    while (sp > 0 && (double)ts[sp - 1] > tk) --sp;
+    while (sp > 0 && ks[sp - 1] > elast) --sp;
     for (int q = sp; q < ns; ++q) {
-        const double u = (double)ts[q] - tk;
+        const double u = fmax((double)ts[q] - tk, 0.0);
         Pm += mo[q] * exp(-u * m.inv_tm);
         Ps += mo[q] * exp(-u * m.inv_ts);
     }
-    double tnext = sp > 0 ? (double)ts[sp - 1] : -INFINITY;   // the next spike to take, walking back
+    // the next spike to take, walking back: its event count, time, adjoint
+    int knext = sp > 0 ? ks[sp - 1] : -1;
+    double tnext = sp > 0 ? (double)ts[sp - 1] : 0.0;
     double mnext = sp > 0 ? mo[sp - 1] : 0.0;
     const double kap = m.kappa;
     double* gt = gT ? gT + (size_t)c.b * E_max + c.k0 : nullptr;
@@ -208,12 +219,14 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_event_adjoint(
                 Pm *= ad.x;
                 Ps *= ad.y;
                 const double tp = (double)lt[e - 1];
-                while (tnext > tp) {
-                    const double u = tnext - tp;
+                // spikes between events e - 1 and e (out_k = e)
+                while (knext >= c.k0 + e) {
+                    const double u = fmax(tnext - tp, 0.0);
                     Pm += mnext * exp(-u * m.inv_tm);
                     Ps += mnext * exp(-u * m.inv_ts);
                     --sp;
-                    tnext = sp > 0 ? (double)ts[sp - 1] : -INFINITY;
+                    knext = sp > 0 ? ks[sp - 1] : -1;
+                    tnext = sp > 0 ? (double)ts[sp - 1] : 0.0;
                     mnext = sp > 0 ? mo[sp - 1] : 0.0;
                 }
             }
@@ -240,13 +253,13 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_event_adjoint(
 
 int backward_impl(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max, const float* WT,
                   int C_in, int N, const lif_params* p, const float* out_t, const int32_t* out_n,
-                  const float* out_i, const float* grad_out_t, float* grad_WT, float* grad_ev_t, void* ws,
-                  size_t ws_bytes, hipStream_t stream)
+                  const float* out_i, const int32_t* out_k, const float* grad_out_t, float* grad_WT,
+                  float* grad_ev_t, void* ws, size_t ws_bytes, hipStream_t stream)
 {
     int rc = check_params(p);
     if (rc) return rc;
     if (B < 0 || E_max < 0 || C_in < 1 || N < 1) return LIF_ERR_ARG;
-    if (!WT || !out_t || !out_n || !out_i || !grad_out_t || !grad_WT || !ws) return LIF_ERR_ARG;
+    if (!WT || !out_t || !out_n || !out_i || !out_k || !grad_out_t || !grad_WT || !ws) return LIF_ERR_ARG;
     if (B > 0 && !ev_n) return LIF_ERR_ARG;
     if ((size_t)B * (size_t)E_max > 0 && (!ev_t || !ev_src)) return LIF_ERR_ARG;
     if ((size_t)C_in * (size_t)N >= ((size_t)1 << 29)) return LIF_ERR_SIZE;   // 32-bit W^T byte offsets
@@ -256,7 +269,7 @@ int backward_impl(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n,
     char* base = (char*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
     Decay* dec = (Decay*)(base + L.dec);
     double* mu = (double*)(base + L.mu);
-    float* last = (float*)(base + L.last);
+    int32_t* klast = (int32_t*)(base + L.klast);
     double* gw = (double*)(base + L.gw);
     double* gt = grad_ev_t ? (double*)(base + L.gt) : nullptr;
     size_t nW = (size_t)C_in * N, nT = (size_t)B * E_max, nn = (size_t)B * N;
@@ -270,7 +283,7 @@ int backward_impl(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n,
         if (blocks > 2048) blocks = 2048;
         if (blocks < 1) blocks = 1;
         TIMED_LAUNCH("bwd_setup", k_bwd_setup, dim3((unsigned)blocks), dim3(256), 0, stream, ev_t, ev_n, B, E_max,
-                     L.E_pad, N, m, dec, gw, nW, gt, nT, out_t, out_n, out_i, grad_out_t, mu, last);
+                     L.E_pad, N, m, dec, gw, nW, gt, nT, out_t, out_n, out_i, out_k, grad_out_t, mu, klast);
     }
     const int tiles = (N + kWave - 1) / kWave;
     const size_t items = (size_t)B * L.S * tiles;
@@ -278,7 +291,7 @@ int backward_impl(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n,
     const unsigned blocks = (unsigned)((items + kWalkWaves - 1) / kWalkWaves);
     if (items) TIMED_LAUNCH("event_adjoint", k_event_adjoint, dim3(blocks), dim3(kWave * kWalkWaves), 0, stream,
                             ev_t, ev_src, ev_n, E_max, L.E_pad, WT, C_in, N, tiles, L.S, (int)items, m, dec, out_t,
-                            out_n, mu, last, gw, gt);
+                            out_n, out_k, mu, klast, gw, gt);
     TIMED_LAUNCH("bwd_convert", k_bwd_convert, dim3(1024), dim3(256), 0, stream, gw, grad_WT, nW, gt, grad_ev_t, nT);
     return check_launch();
 }
@@ -293,9 +306,10 @@ extern "C" size_t lif_layer_backward_workspace_size(int B, int E_max, int C_in, 
 
 extern "C" int lif_layer_backward(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
                                   const float* WT, int C_in, int N_out, const lif_params* p, const float* out_t,
-                                  const int32_t* out_n, const float* out_i, const float* grad_out_t, float* grad_WT,
-                                  float* grad_ev_t, void* ws, size_t ws_bytes, lif_stream_t stream)
+                                  const int32_t* out_n, const float* out_i, const int32_t* out_k,
+                                  const float* grad_out_t, float* grad_WT, float* grad_ev_t, void* ws,
+                                  size_t ws_bytes, lif_stream_t stream)
 {
-    return lif::backward_impl(ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, p, out_t, out_n, out_i, grad_out_t,
-                              grad_WT, grad_ev_t, ws, ws_bytes, (hipStream_t)stream);
+    return lif::backward_impl(ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, p, out_t, out_n, out_i, out_k,
+                              grad_out_t, grad_WT, grad_ev_t, ws, ws_bytes, (hipStream_t)stream);
 }

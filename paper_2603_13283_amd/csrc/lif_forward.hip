@@ -93,7 +93,8 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ ev_t, co
                                               double2* __restrict__ segm, int32_t* __restrict__ status,
                                               uint32_t* __restrict__ counters, size_t n_counters,
                                               int32_t* __restrict__ out_n, uint32_t* __restrict__ listed, size_t nn,
-                                              float* __restrict__ out_t, float* __restrict__ out_i, size_t n_out)
+                                              float* __restrict__ out_t, float* __restrict__ out_i,
+                                              int32_t* __restrict__ out_k, size_t n_out)
 {
     const size_t tid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     const size_t stride = (size_t)gridDim.x * blockDim.x;
@@ -107,6 +108,7 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ ev_t, co
         for (size_t i = tid; i < n_out; i += stride) {
             out_t[i] = INFINITY;
             if (out_i) out_i[i] = 0.0f;
+            if (out_k) out_k[i] = 0;
         }
     }
     const size_t nev = (size_t)B * (size_t)E_pad;
@@ -577,14 +579,16 @@ struct WinBuf {
     double crit[kWinIv + 1], hi[kWinIv + 1], fhi[kWinIv + 1];
     double2 s0[kWinIv + 1];                      // (V0, I0)
     double t0[kWinIv + 1];                       // interval start
+    int32_t kev[kWinIv + 1];                     // index of the event that closes the interval (ev_n[b]: open)
 };
 
 struct ResolveLds {
     uint32_t cand[kCandCap];                     // (segment in chunk << 3) | sub-block
     uint32_t slot[kCandCap];                     // record slot of each candidate (kNoSlot: none)
     WinBuf win[2];
-    double sp_t0[kWave], sp_y[kWave];            // spike buffer: interval start, e^{-u/tm}
-    float si[kWave];
+    double sp_t0[kWave], sp_y[kWave];            // spike buffer: interval start, e^{-u/tm},
+    float si[kWave];                             // I at the spike,
+    int32_t sk[kWave];                           // events consumed before the spike
     int ntot;                                    // candidates of the chunk (chain wave -> both)
     int stop[2];                                 // capped after window w (slot w % 2)
 };
@@ -704,8 +708,9 @@ __global__ __launch_bounds__(256) void k_records(const float* __restrict__ ev_t,
                                                  const Decay* __restrict__ dec, const double2* __restrict__ ent,
                                                  Record* __restrict__ pool, const uint32_t* __restrict__ pool_count,
                                                  uint32_t pool_cap, int32_t* __restrict__ out_n, size_t nn,
-                                                 float* __restrict__ out_t, float* __restrict__ out_i, size_t n_out,
-                                                 int B, int32_t* __restrict__ status)
+                                                 float* __restrict__ out_t, float* __restrict__ out_i,
+                                                 int32_t* __restrict__ out_k, size_t n_out, int B,
+                                                 int32_t* __restrict__ status)
 {
     if (blockIdx.x == gridDim.x - 1 && blockIdx.y == gridDim.y - 1 && threadIdx.x >= blockDim.x - kWave) {
         // status words fixed once the check pass has run (the only writer of
@@ -735,13 +740,15 @@ __global__ __launch_bounds__(256) void k_records(const float* __restrict__ ev_t,
     }
     {
         // outputs reset ahead of the resolve pass (it writes only the
-        // neurons that fire): counts 0, times +inf, currents 0
+        // neurons that fire): counts 0, times +inf, currents and event
+        // counts 0
         const size_t gs = (size_t)gridDim.x * gridDim.y * blockDim.x;
         const size_t gt = ((size_t)blockIdx.y * gridDim.x + blockIdx.x) * blockDim.x + threadIdx.x;
         for (size_t i = gt; i < nn; i += gs) out_n[i] = 0;
         for (size_t i = gt; i < n_out; i += gs) {
             out_t[i] = INFINITY;
             if (out_i) out_i[i] = 0.0f;
+            if (out_k) out_k[i] = 0;
         }
     }
     const int lane = (int)threadIdx.x % kWave;
@@ -874,7 +881,7 @@ struct Chain {
 // spike times t0 - tm ln y are taken here, 64 at a time, off the per-spike
 // chain.
 __device__ __forceinline__ void flush_spikes(ResolveLds& sh, const Model& m, int from, int to, float* __restrict__ st,
-                                             float* __restrict__ si)
+                                             float* __restrict__ si, int32_t* __restrict__ sk)
 {
     const int lane = (int)threadIdx.x;
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -884,6 +891,7 @@ __device__ __forceinline__ void flush_spikes(ResolveLds& sh, const Model& m, int
         const int q = (from + lane) % kWave;
         st[from + lane] = (float)(sh.sp_t0[q] - m.tm * log(sh.sp_y[q]));
         if (si) si[from + lane] = sh.si[q];
+        if (sk) sk[from + lane] = sh.sk[q];
     }
     __builtin_amdgcn_wave_barrier();
 }
@@ -894,7 +902,8 @@ __device__ __forceinline__ void flush_spikes(ResolveLds& sh, const Model& m, int
 // solve of a round runs wave-uniform on the crossing interval's data
 // (broadcast from its lane), so its iterations branch on scalars.
 __device__ __forceinline__ void resolve_step(ResolveLds& sh, const WinBuf& w, const Model& m, int i0, int nlanes,
-                                             Chain& ch, float* __restrict__ st, float* __restrict__ si)
+                                             Chain& ch, float* __restrict__ st, float* __restrict__ si,
+                                             int32_t* __restrict__ sk)
 {
     const int lane = (int)threadIdx.x;
     const int i = lane < nlanes ? i0 + lane : i0;
@@ -921,13 +930,14 @@ __device__ __forceinline__ void resolve_step(ResolveLds& sh, const WinBuf& w, co
             sh.sp_t0[ch.ns % kWave] = t0k;
             sh.sp_y[ch.ns % kWave] = sp.y;
             sh.si[ch.ns % kWave] = (float)(I0k * (sp.E2 * sp.y));
+            sh.sk[ch.ns % kWave] = w.kev[i0 + kl];
         }
         // the deficit in interval kl's frame
         const double Dnew = Dk + m.dth * sp.E1;
         ++ch.ns;
         ch.dref = Dnew;
         ch.tref = t0k;
-        if (ch.ns % kWave == 0) flush_spikes(sh, m, ch.ns - kWave, ch.ns, st, si);
+        if (ch.ns % kWave == 0) flush_spikes(sh, m, ch.ns - kWave, ch.ns, st, si, sk);
         if (ch.ns >= m.s_max) { ch.capped = true; return; }
         // interval kl is tested again with the raised deficit (a second spike
         // in it); later intervals take the new deficit; earlier ones are done
@@ -965,6 +975,7 @@ __device__ __forceinline__ void stage_window(const ResolveLds& sh, WinBuf& w, co
         w.fhi[i] = nx[h].fhi;
         w.s0[i] = nx[h].s0;
         w.t0[i] = kq0 + j > 0 ? (double)nx[h].tp : 0.0;
+        w.kev[i] = kq0 + j;
     }
     static_assert(kWinCand <= kWave, "one lane per candidate of the window");
     if (__ballot(sh.slot[min(c0 + lane % kWinCand, tot - 1)] == kNoSlot))
@@ -981,7 +992,7 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
                               const Decay* __restrict__ dec, const double2* __restrict__ ent,
                               const uint2* __restrict__ mask, uint32_t pool_cap,
                               const Record* __restrict__ pool, float* __restrict__ out_t, int32_t* __restrict__ out_n,
-                              float* __restrict__ out_i)
+                              float* __restrict__ out_i, int32_t* __restrict__ out_k)
 {
     const int lane = (int)threadIdx.x % kWave;
     const bool chain = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)) == 0;   // wave-uniform
@@ -1000,6 +1011,7 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
     const size_t idx = (size_t)b * N + n;
     float* st = out_t + idx * (size_t)m.s_max;
     float* si = out_i ? out_i + idx * (size_t)m.s_max : nullptr;
+    int32_t* sk = out_k ? out_k + idx * (size_t)m.s_max : nullptr;
     const int Sb = (nb + kSeg - 1) / kSeg;
     const bool has_open = __builtin_amdgcn_readfirstlane(nb > 0 && m.t_end > (double)tt[max(nb - 1, 0)] ? 1 : 0) != 0;
 
@@ -1069,6 +1081,7 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
                         w.fhi[kOpenIv] = of;
                         w.s0[kOpenIv] = os;
                         w.t0[kOpenIv] = ot;
+                        w.kev[kOpenIv] = nb;
                     }
                 }
                 stage_window(sh, sh.win[0], m, 0, tot, seg0, b, n, nb, S, N, C_in, tt, src, d, WT, ent, pool);
@@ -1086,7 +1099,7 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
                     const int steps = min(kWinSteps, (tot - c0 + kStep - 1) / kStep);
                     const int nsteps = steps + (wi == nwin - 1 && open_here ? 1 : 0);
                     for (int g = 0; g < nsteps && !ch.capped; ++g)
-                        resolve_step(sh, w, m, g < steps ? g * kWave : kOpenIv, g < steps ? kWave : 1, ch, st, si);
+                        resolve_step(sh, w, m, g < steps ? g * kWave : kOpenIv, g < steps ? kWave : 1, ch, st, si, sk);
                     if (lane == 0) sh.stop[wi & 1] = ch.capped ? 1 : 0;
                 }
                 __syncthreads();              // window wi + 1 staged, window wi free
@@ -1097,7 +1110,7 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
         __syncthreads();                      // the list is rewritten by the next chunk
     }
     if (!chain) return 0;
-    flush_spikes(sh, m, ch.ns - ch.ns % kWave, ch.ns, st, si);
+    flush_spikes(sh, m, ch.ns - ch.ns % kWave, ch.ns, st, si, sk);
     if (lane == 0) out_n[idx] = ch.ns;
     return ch.ns;
 }
@@ -1115,7 +1128,8 @@ __global__ __launch_bounds__(kWave * kResolveWaves) void k_resolve(const float* 
                                                    const Record* __restrict__ pool,
                                                    const uint32_t* __restrict__ work, const uint32_t* __restrict__ nwork,
                                                    float* __restrict__ out_t, int32_t* __restrict__ out_n,
-                                                   float* __restrict__ out_i, int32_t* __restrict__ status)
+                                                   float* __restrict__ out_i, int32_t* __restrict__ out_k,
+                                                   int32_t* __restrict__ status)
 {
     __shared__ ResolveLds sh;
     // spikes and capped neurons of this workgroup's neurons, added to the
@@ -1158,7 +1172,7 @@ __global__ __launch_bounds__(kWave * kResolveWaves) void k_resolve(const float* 
         const uint32_t bn = (uint32_t)__builtin_amdgcn_readfirstlane((int)work[(size_t)b * N + (w - before)]);
         const int ns = resolve_neuron(sh, (int)(bn / (uint32_t)N), (int)(bn % (uint32_t)N), ev_t, ev_src, ev_n,
                                       E_max, WT, C_in, N, E_pad, S, m, dec, ent, mask, pool_cap, pool, out_t, out_n,
-                                      out_i);
+                                      out_i, out_k);
         spikes += (unsigned long long)ns;
         capped += ns >= m.s_max ? 1u : 0u;
     }
@@ -1253,7 +1267,8 @@ __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_
                                                    const int32_t* __restrict__ ev_n, int B, int E_max,
                                                    const float* __restrict__ WT, int C_in, int N, Model m,
                                                    int E_pad, const Decay* __restrict__ dec, float* __restrict__ out_t,
-                                                   int32_t* __restrict__ out_n, float* __restrict__ out_i)
+                                                   int32_t* __restrict__ out_n, float* __restrict__ out_i,
+                                                   int32_t* __restrict__ out_k)
 {
     const size_t idx_raw = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     const bool live = idx_raw < (size_t)B * (size_t)N;
@@ -1265,6 +1280,7 @@ __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_
     const Decay* d = dec + (size_t)b * E_pad;
     float* st = out_t + idx * (size_t)m.s_max;
     float* si = out_i ? out_i + idx * (size_t)m.s_max : nullptr;
+    int32_t* sk = out_k ? out_k + idx * (size_t)m.s_max : nullptr;
     int ns = 0;
     bool capped = false;
     double V = 0.0, I = 0.0, t_prev = 0.0;
@@ -1297,6 +1313,7 @@ __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_
                 if (live) {
                     st[ns] = (float)(t_prev + u);
                     if (si) si[ns] = (float)(I * (sp.E2 * sp.y));
+                    if (sk) sk[ns] = k;
                 }
                 ++ns;
                 Dk += m.dth * sp.E1;
@@ -1318,6 +1335,7 @@ __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_
         for (int s = ns; s < m.s_max; ++s) {
             st[s] = INFINITY;
             if (si) si[s] = 0.0f;
+            if (sk) sk[s] = 0;
         }
     }
 }
@@ -1325,7 +1343,7 @@ __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_
 // ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
-FwdLayout fwd_layout(int B, int E_max, int N)
+FwdLayout fwd_layout(int B, int E_max, int N, int pool_cap)
 {
     FwdLayout L{};
     L.S = (E_max + kSeg - 1) / kSeg;
@@ -1348,11 +1366,11 @@ FwdLayout fwd_layout(int B, int E_max, int N)
     // slices sized at a 16th of the dense bound (every sub-block of every
     // neuron flagged), at least 4096 records (or the dense bound when
     // smaller).  A full slice only sends the excess sub-blocks through a
-    // slower re-walk.  LIF_POOL_CAP overrides the slice size (tests of the
-    // re-walk path).
+    // slower re-walk.  lif_params.pool_cap >= 0 sets the slice size (tests
+    // of the re-walk path).
     const size_t dense = (size_t)L.S * kSubPerSeg * N;
     size_t cap = dense / 16 > 4096 ? dense / 16 : (dense < 4096 ? dense : 4096);
-    if (const char* env = getenv("LIF_POOL_CAP")) cap = (size_t)strtoull(env, nullptr, 10);
+    if (pool_cap >= 0) cap = (size_t)pool_cap;
     if (B > 0 && (size_t)B * cap > 0xfffffff0ull) cap = 0xfffffff0ull / (size_t)B;   // slot indices are 32-bit
     L.pool_cap = cap;
     const size_t recs = (size_t)B * cap;
@@ -1362,15 +1380,12 @@ FwdLayout fwd_layout(int B, int E_max, int N)
 }
 
 // Neurons per lane of the segment walks: NPL-wide weight loads need W^T rows
-// of a multiple of NPL floats and an aligned base.  LIF_NPL (1, 2 or 4)
-// restricts the choice.
+// of a multiple of NPL floats and an aligned base.
 static int pick_npl(const float* WT, int N)
 {
-    int lim = 4;
-    if (const char* env = getenv("LIF_NPL")) lim = atoi(env);
     const uintptr_t a = (uintptr_t)WT;
-    if (lim >= 4 && N % 4 == 0 && a % 16 == 0) return 4;
-    if (lim >= 2 && N % 2 == 0 && a % 8 == 0) return 2;
+    if (N % 4 == 0 && a % 16 == 0) return 4;
+    if (N % 2 == 0 && a % 8 == 0) return 2;
     return 1;
 }
 
@@ -1414,11 +1429,11 @@ static void launch_walks(const FwdLayout& L, const FwdPtrs& P, const float* ev_t
 
 int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
                  const float* WT, int C_in, int N, const lif_params* p, float* out_t, int32_t* out_n,
-                 float* out_i, int32_t* status, void* ws, size_t ws_bytes, hipStream_t stream)
+                 float* out_i, int32_t* out_k, int32_t* status, void* ws, size_t ws_bytes, hipStream_t stream)
 {
     int rc = validate_forward_args(ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, p, out_t, out_n, status, ws);
     if (rc) return rc;
-    FwdLayout L = fwd_layout(B, E_max, N);
+    FwdLayout L = fwd_layout(B, E_max, N, p->pool_cap);
     if (ws_bytes < L.total) return LIF_ERR_WORKSPACE;
     Model m = make_model(*p);
     char* base = (char*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
@@ -1452,7 +1467,7 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
         TIMED_LAUNCH("prep", k_prep, dim3((unsigned)blocks), dim3(256), 0, stream,
                      ev_t, ev_n, B, E_max, L.E_pad, L.S, m, P.dec, sequential ? nullptr : P.segm, status, P.counters,
                      L.n_counters, out_n, sequential ? nullptr : P.listed, nn, sequential ? nullptr : out_t, out_i,
-                     n_out);
+                     out_k, n_out);
         if (validate)
             TIMED_LAUNCH("validate", k_validate, dim3((unsigned)(((size_t)B * E_max + 255) / 256)), dim3(256), 0,
                          stream, ev_t, ev_src, ev_n, B, E_max, C_in, status);
@@ -1460,7 +1475,7 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     if (sequential) {
         if (nn)
             TIMED_LAUNCH("sequential", k_sequential, dim3((unsigned)((nn + 63) / 64)), dim3(64), 0, stream,
-                         ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, L.E_pad, P.dec, out_t, out_n, out_i);
+                         ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, L.E_pad, P.dec, out_t, out_n, out_i, out_k);
         TIMED_LAUNCH("status", k_status, dim3(status_blocks(B, N)), dim3(kStatusThreads), 0, stream, ev_n, B, E_max, N, m.s_max, out_n,
                      status);
         return check_launch();
@@ -1479,14 +1494,14 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
         if (B > 0)
             TIMED_LAUNCH("records", k_records, dim3(bx, (unsigned)B), dim3(256), 0, stream,
                          ev_t, ev_src, ev_n, E_max, L.E_pad, L.S, WT, C_in, N, m, P.dec, P.ent, P.pool, P.pool_count,
-                         (uint32_t)L.pool_cap, out_n, nn, out_t, out_i, n_out, B, status);
+                         (uint32_t)L.pool_cap, out_n, nn, out_t, out_i, out_k, n_out, B, status);
     }
     // Two-wave workgroups (chain and staging waves) over the concatenated
     // per-sample lists.
     const unsigned rgrid = (unsigned)(nn < 4096 ? nn : 4096);
     TIMED_LAUNCH("resolve", k_resolve, dim3(rgrid), dim3(kWave * kResolveWaves), 0, stream,
                  ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, L.E_pad, L.S, m, P.dec, P.ent, P.mask, (uint32_t)L.pool_cap,
-                 P.pool, P.work, P.nwork, out_t, out_n, out_i, status);
+                 P.pool, P.work, P.nwork, out_t, out_n, out_i, out_k, status);
     return check_launch();
 }
 
@@ -1494,25 +1509,25 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
 
 extern "C" size_t lif_layer_forward_workspace_size(int B, int E_max, int C_in, int N_out, const lif_params* p)
 {
-    (void)C_in; (void)p;
-    if (B < 0 || E_max < 0 || N_out < 1) return 0;
-    return lif::fwd_layout(B, E_max, N_out).total;
+    (void)C_in;
+    if (B < 0 || E_max < 0 || N_out < 1 || !p) return 0;
+    return lif::fwd_layout(B, E_max, N_out, p->pool_cap).total;
 }
 
 extern "C" int lif_layer_forward(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
                                  const float* WT, int C_in, int N_out, const lif_params* p, float* out_t,
-                                 int32_t* out_n, float* out_i, int32_t* status, void* ws, size_t ws_bytes,
-                                 lif_stream_t stream)
+                                 int32_t* out_n, float* out_i, int32_t* out_k, int32_t* status, void* ws,
+                                 size_t ws_bytes, lif_stream_t stream)
 {
-    return lif::forward_impl(false, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, p, out_t, out_n, out_i, status,
-                             ws, ws_bytes, (hipStream_t)stream);
+    return lif::forward_impl(false, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, p, out_t, out_n, out_i, out_k,
+                             status, ws, ws_bytes, (hipStream_t)stream);
 }
 
 extern "C" int lif_layer_forward_sequential(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B,
                                             int E_max, const float* WT, int C_in, int N_out, const lif_params* p,
-                                            float* out_t, int32_t* out_n, float* out_i, int32_t* status, void* ws,
-                                            size_t ws_bytes, lif_stream_t stream)
+                                            float* out_t, int32_t* out_n, float* out_i, int32_t* out_k,
+                                            int32_t* status, void* ws, size_t ws_bytes, lif_stream_t stream)
 {
-    return lif::forward_impl(true, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, p, out_t, out_n, out_i, status,
-                             ws, ws_bytes, (hipStream_t)stream);
+    return lif::forward_impl(true, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, p, out_t, out_n, out_i, out_k,
+                             status, ws, ws_bytes, (hipStream_t)stream);
 }

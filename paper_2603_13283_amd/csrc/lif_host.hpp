@@ -20,7 +20,7 @@ struct FwdLayout {
     size_t n_counters;                       // uint32 counters reset by every call
     size_t pool_cap;                         // record slots per sample
 };
-FwdLayout fwd_layout(int B, int E_max, int N);
+FwdLayout fwd_layout(int B, int E_max, int N, int pool_cap);
 
 int check_params(const lif_params* p);
 Model make_model(const lif_params& p);

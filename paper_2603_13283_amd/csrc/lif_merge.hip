@@ -4,16 +4,50 @@
 // softmax cross-entropy readout used to drive a backward pass.
 //
 // Merge: one workgroup per sample.  Each neuron's spikes are already in
-// time order; the workgroup gathers all of them into LDS as 64-bit keys
-// (float bits of the time, which order like the times since spike times are
-// positive, then i * s_max + s, which orders equal times by neuron) and
-// sorts them with a bitonic network in LDS.
+// time order; the workgroup gathers them into LDS as 64-bit keys (float bits
+// of the time, which order like the times since spike times are positive,
+// then i * s_max + s, which orders equal times by neuron) and sorts them
+// with a bitonic network in LDS.  When a sample has more spikes than the
+// sort holds, the K = min(total, E2_max) earliest are found first: the
+// K-th smallest time t_K by bisection on its float bits (each neuron's
+// spikes are sorted, so counting the spikes at or before a time is a binary
+// search per neuron), then every spike before t_K and, in neuron order, as
+// many spikes at exactly t_K as K allows.
 #include "lif_common.hpp"
 #include "lif_host.hpp"
 
 namespace lif {
 
 constexpr int kMergeThreads = 1024;
+
+// Exclusive prefix sum over the workgroup of one value per thread; also
+// returns the total.
+__device__ __forceinline__ int block_exclusive_scan(int v, int* s_scan, int& total)
+{
+    const int tid = threadIdx.x;
+    __syncthreads();
+    s_scan[tid] = v;
+    __syncthreads();
+    for (int off = 1; off < kMergeThreads; off <<= 1) {
+        const int x = tid >= off ? s_scan[tid - off] : 0;
+        __syncthreads();
+        s_scan[tid] += x;
+        __syncthreads();
+    }
+    total = s_scan[kMergeThreads - 1];
+    return s_scan[tid] - v;
+}
+
+// Spikes of one neuron (sorted times ts[0 .. c)) whose float bits are <= x.
+__device__ __forceinline__ int count_le(const float* __restrict__ ts, int c, uint32_t x)
+{
+    int lo = 0, hi = c;                    // first index with bits > x
+    while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (__float_as_uint(ts[mid]) <= x) lo = mid + 1; else hi = mid;
+    }
+    return lo;
+}
 
 __global__ __launch_bounds__(kMergeThreads) void k_merge(const float* __restrict__ out_t,
                                                          const int32_t* __restrict__ out_n, int N, int s_max,
@@ -23,36 +57,68 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(const float* __restrict
 {
     extern __shared__ unsigned long long keys[];   // cap entries (power of two)
     __shared__ int s_scan[kMergeThreads];
-    __shared__ int s_total;
     const int b = blockIdx.x;
     const int tid = threadIdx.x;
     const int32_t* cnt = out_n + (size_t)b * N;
-    // Exclusive prefix of the spike counts over neurons: each thread owns a
-    // contiguous run of neurons.
-    int per = (N + kMergeThreads - 1) / kMergeThreads;
-    int i0 = min(tid * per, N), i1 = min(i0 + per, N);
+    const float* tb = out_t + (size_t)b * N * s_max;
+    // each thread owns a contiguous run of neurons
+    const int per = (N + kMergeThreads - 1) / kMergeThreads;
+    const int i0 = min(tid * per, N), i1 = min(i0 + per, N);
     int local = 0;
     for (int i = i0; i < i1; ++i) local += min(max(cnt[i], 0), s_max);
-    s_scan[tid] = local;
-    __syncthreads();
-    for (int off = 1; off < kMergeThreads; off <<= 1) {
-        int v = tid >= off ? s_scan[tid - off] : 0;
-        __syncthreads();
-        s_scan[tid] += v;
-        __syncthreads();
-    }
-    if (tid == kMergeThreads - 1) s_total = s_scan[tid];
-    int pos = s_scan[tid] - local;
+    int total = 0;
+    int pos = block_exclusive_scan(local, s_scan, total);
+    const int kept = min(total, E2_max);
     for (int e = tid; e < cap; e += kMergeThreads) keys[e] = ~0ull;
     __syncthreads();
-    int total = s_total;
-    for (int i = i0; i < i1; ++i) {
-        int c = min(max(cnt[i], 0), s_max);
-        const float* ts = out_t + ((size_t)b * N + i) * s_max;
-        for (int s = 0; s < c; ++s, ++pos) {
-            if (pos < cap) {
-                unsigned int tb = __float_as_uint(ts[s]);
-                keys[pos] = ((unsigned long long)tb << 32) | (unsigned int)(i * s_max + s);
+    if (total <= cap) {
+        // every spike fits: gather all of them
+        for (int i = i0; i < i1; ++i) {
+            const int c = min(max(cnt[i], 0), s_max);
+            const float* ts = tb + (size_t)i * s_max;
+            for (int s = 0; s < c; ++s, ++pos)
+                keys[pos] = ((unsigned long long)__float_as_uint(ts[s]) << 32) | (unsigned int)(i * s_max + s);
+        }
+    } else {
+        // the smallest float bits x with at least `kept` spikes at or before x
+        uint32_t lo = 0u, hi = 0x7f800000u;             // +inf bits: every spike
+        while (lo < hi) {
+            const uint32_t mid = lo + ((hi - lo) >> 1);
+            int le = 0;
+            for (int i = i0; i < i1; ++i) le += count_le(tb + (size_t)i * s_max, min(max(cnt[i], 0), s_max), mid);
+            int all = 0;
+            (void)block_exclusive_scan(le, s_scan, all);
+            if (all >= kept) hi = mid; else lo = mid + 1;
+        }
+        const uint32_t xk = lo;
+        // spikes before xk, then the ones at xk in neuron order, up to kept
+        int nlt = 0, neq = 0;
+        for (int i = i0; i < i1; ++i) {
+            const float* ts = tb + (size_t)i * s_max;
+            const int c = min(max(cnt[i], 0), s_max);
+            const int lt = xk > 0u ? count_le(ts, c, xk - 1u) : 0;
+            nlt += lt;
+            neq += count_le(ts, c, xk) - lt;
+        }
+        int tot_lt = 0, tot_eq = 0;
+        int plt = block_exclusive_scan(nlt, s_scan, tot_lt);
+        int peq = tot_lt + block_exclusive_scan(neq, s_scan, tot_eq);
+        for (int i = i0; i < i1; ++i) {
+            const float* ts = tb + (size_t)i * s_max;
+            const int c = min(max(cnt[i], 0), s_max);
+            for (int s = 0; s < c; ++s) {
+                const uint32_t tbits = __float_as_uint(ts[s]);
+                const unsigned long long key = ((unsigned long long)tbits << 32) | (unsigned int)(i * s_max + s);
+                // (the bounds keep malformed, unsorted lists inside the sort)
+                if (tbits < xk) {
+                    if (plt < kept) keys[plt] = key;
+                    ++plt;
+                } else if (tbits == xk) {
+                    if (peq < kept) keys[peq] = key;
+                    ++peq;
+                } else {
+                    break;
+                }
             }
         }
     }
@@ -71,10 +137,9 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(const float* __restrict
             __syncthreads();
         }
     }
-    int kept = min(total, E2_max);
     for (int e = tid; e < E2_max; e += kMergeThreads) {
         size_t o = (size_t)b * E2_max + e;
-        if (e < kept && e < cap) {
+        if (e < kept) {
             unsigned long long k = keys[e];
             unsigned int lo = (unsigned int)(k & 0xffffffffull);
             ev_t2[o] = __uint_as_float((unsigned int)(k >> 32));
@@ -87,8 +152,8 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(const float* __restrict
         }
     }
     if (tid == 0) {
-        ev_n2[b] = min(kept, cap);
-        if (total > E2_max || total > cap) atomicOr(&status[LIF_ST_FLAGS], LIF_WARN_MERGE_FULL);
+        ev_n2[b] = kept;
+        if (total > E2_max) atomicOr(&status[LIF_ST_FLAGS], LIF_WARN_MERGE_FULL);
     }
 }
 
@@ -170,12 +235,11 @@ extern "C" int lif_merge_spikes(const float* out_t, const int32_t* out_n, int B,
     TIMED_LAUNCH("merge_status", lif::k_zero_status, dim3(1), dim3(64), 0, stream, status);
     if (B == 0) return lif::check_launch();
     size_t shmem = (size_t)cap * sizeof(unsigned long long);
-    static bool attr_set = false;
-    if (!attr_set) {
-        (void)hipFuncSetAttribute((const void*)lif::k_merge, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                  (int)(LIF_MERGE_MAX * sizeof(unsigned long long)));
-        attr_set = true;
-    }
+    // the sort's LDS exceeds the default dynamic-LDS limit; the attribute is
+    // set on every call (for the current device; no state kept here)
+    if (hipFuncSetAttribute((const void*)lif::k_merge, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)(LIF_MERGE_MAX * sizeof(unsigned long long))) != hipSuccess)
+        return LIF_ERR_HIP;
     TIMED_LAUNCH("merge", lif::k_merge, dim3(B), dim3(lif::kMergeThreads), shmem, stream, out_t, out_n, N, s_max,
                  ev_t2, ev_src2, ev_n2, perm, E2_max, cap, status);
     return lif::check_launch();

@@ -40,12 +40,17 @@ def test_version_and_workspace_sizes(lib):
     big = L.lif_layer_forward_workspace_size(32, 5200, 700, 256, p)
     assert 0 < small < big < 2 ** 31
     assert L.lif_layer_forward_workspace_size(-1, 10, 4, 8, p) == 0
+    # the record pool's slots per sample enter the workspace size
+    p0, p9 = L.Params(pool_cap=0).c(), L.Params(pool_cap=9000).c()
+    assert (L.lif_layer_forward_workspace_size(32, 5200, 700, 256, p0)
+            < L.lif_layer_forward_workspace_size(32, 5200, 700, 256, p9))
     assert L.lif_layer_backward_workspace_size(4, 100, 10, 20, p) > 0
     assert L.lif_merge_workspace_size(4, 20, 8, 100) > 0
 
 
 def _fwd(fn, p, B=2, E=10, C=4, N=8, ws_bytes=10 ** 9, null=None):
-    args = [F, F, F, B, E, F, C, N, ctypes.byref(p), F, F, F, F, F, ws_bytes, None]
+    # ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, p, out_t, out_n, out_i, out_k, status, ws, ws_bytes, stream
+    args = [F, F, F, B, E, F, C, N, ctypes.byref(p), F, F, F, F, F, F, ws_bytes, None]
     if null is not None:
         args[null] = None
     return fn(*args)
@@ -62,24 +67,33 @@ def test_forward_argument_errors(lib, fn):
     assert _fwd(fn, L.Params(s_max=0).c()) == L.LIF_ERR_ARG
     assert _fwd(fn, L.Params(t_end=math.nan).c()) == L.LIF_ERR_ARG
     assert _fwd(fn, L.Params(solver_reg=-1.0).c()) == L.LIF_ERR_ARG
+    bad = L.Params().c()
+    bad.reserved = 1
+    assert _fwd(fn, bad) == L.LIF_ERR_ARG
+    bad = L.Params().c()
+    bad.flags = 8                                   # no such flag
+    assert _fwd(fn, bad) == L.LIF_ERR_ARG
     p = L.Params().c()
     assert _fwd(fn, p, B=-1) == L.LIF_ERR_ARG
     assert _fwd(fn, p, N=0) == L.LIF_ERR_ARG
     assert _fwd(fn, p, C=0) == L.LIF_ERR_ARG
-    for null in (0, 1, 2, 5, 9, 10, 12, 13):       # ev_t, ev_src, ev_n, WT, out_t, out_n, status, ws
+    for null in (0, 1, 2, 5, 9, 10, 13, 14):       # ev_t, ev_src, ev_n, WT, out_t, out_n, status, ws
         assert _fwd(fn, p, null=null) == L.LIF_ERR_ARG, null
     assert _fwd(fn, p, ws_bytes=10) == L.LIF_ERR_WORKSPACE
-    assert fn(F, F, F, 2, 10, F, 4, 8, None, F, F, F, F, F, 10 ** 9, None) == L.LIF_ERR_ARG
+    assert fn(F, F, F, 2, 10, F, 4, 8, None, F, F, F, F, F, F, 10 ** 9, None) == L.LIF_ERR_ARG
 
 
 def test_backward_and_merge_argument_errors(lib):
     p = L.Params().c()
-    base = [F, F, F, 2, 10, F, 4, 8, ctypes.byref(p), F, F, F, F, F, F, F, 10 ** 9, None]
+    # ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, p, out_t, out_n, out_i, out_k, grad_out_t, grad_WT,
+    # grad_ev_t, ws, ws_bytes, stream
+    base = [F, F, F, 2, 10, F, 4, 8, ctypes.byref(p), F, F, F, F, F, F, F, F, 10 ** 9, None]
     assert L.lif_layer_backward(*base[:11], None, *base[12:]) == L.LIF_ERR_ARG      # out_i required
+    assert L.lif_layer_backward(*base[:12], None, *base[13:]) == L.LIF_ERR_ARG      # out_k required
     bad = L.Params(tau_mem=0.001).c()
     assert L.lif_layer_backward(*base[:8], ctypes.byref(bad), *base[9:]) == L.LIF_ERR_TAU
     small = list(base)
-    small[16] = 10
+    small[17] = 10
     assert L.lif_layer_backward(*small) == L.LIF_ERR_WORKSPACE
     margs = [F, F, 2, 8, 4, F, F, F, F, 100, F, F, 10 ** 6, None]
     m2 = list(margs)
@@ -111,5 +125,5 @@ def test_weight_matrix_size_limit(lib, fn):
     p = L.Params().c()
     assert _fwd(fn, p, C=1 << 15, N=1 << 14) == L.LIF_ERR_SIZE
     assert _fwd(fn, p, C=1 << 15, N=(1 << 14) - 1, ws_bytes=0) == L.LIF_ERR_WORKSPACE
-    bargs = [F, F, F, 2, 10, F, 1 << 15, 1 << 14, ctypes.byref(p), F, F, F, F, F, F, F, 10 ** 9, None]
+    bargs = [F, F, F, 2, 10, F, 1 << 15, 1 << 14, ctypes.byref(p), F, F, F, F, F, F, F, F, 10 ** 9, None]
     assert L.lif_layer_backward(*bargs) == L.LIF_ERR_SIZE

@@ -4,9 +4,8 @@ import pytest
 
 import oracle
 import workloads as W
-import copy
 
-from tests.parity import E2E_ELEM_RTOL, compare_grad, compare_spikes
+from tests.parity import compare_grad, compare_grad_e2e, compare_spikes
 
 pytestmark = pytest.mark.gpu
 
@@ -29,11 +28,21 @@ def _rel(a, b):
     return float(np.linalg.norm(np.asarray(a, np.float64) - b) / n) if n > 0 else float(np.linalg.norm(a))
 
 
-def _fwd_bwd(env, ev, WT, seed, s_max=64, reg=0.01, e2e=True, **kw):
-    """e2e=False: the end-to-end errors are printed, not asserted (for spike
-    trains long enough that the float32 rounding of the spike times handed
-    to the backward pass is amplified by the adjoint recurrence); the
-    backward kernels are still checked on identical inputs."""
+def _dev_fwd(torch, lif, r):
+    """A forward result on the device from an oracle result (float32 times
+    and currents, the oracle's consumed-event counts)."""
+    return lif.ForwardOut(_dev(torch, r.out_t.astype(np.float32)), _dev(torch, r.out_n),
+                          _dev(torch, r.out_i.astype(np.float32)), None, _dev(torch, r.out_k))
+
+
+def _fwd_bwd(env, ev, WT, seed, s_max=64, reg=0.01, label="", **kw):
+    """GPU forward + backward against the oracle's.  End to end: norms
+    within 1e-4 of the exact gradients, entries within 1e-4 of them or, where
+    the float32 hand-over itself moves them (compare_grad_e2e), of the
+    oracle's gradients of its own float32-rounded spike train.  The backward
+    kernels alone: both sides fed the oracle's spike train rounded to
+    float32, within 1e-4 everywhere.  Neurons excused after a near-tie are
+    left out."""
     torch, lif = env
     P = lif.Params(s_max=s_max, solver_reg=reg, **kw)
     OP = oracle.LifParams(s_max=s_max, solver_reg=reg, **kw)
@@ -41,35 +50,29 @@ def _fwd_bwd(env, ev, WT, seed, s_max=64, reg=0.01, e2e=True, **kw):
     out = lif.forward(*d, P)
     ref = oracle.forward(ev.ev_t, ev.ev_src, ev.ev_n, WT, OP)
     torch.cuda.synchronize()
-    compare_spikes(out.out_t.cpu().numpy(), out.out_n.cpu().numpy(), ref)
+    st = compare_spikes(out.out_t.cpu().numpy(), out.out_n.cpu().numpy(), ref, out.out_i.cpu().numpy(),
+                        label=label, out_k_gpu=out.out_k.cpu().numpy())
     rng = np.random.default_rng(seed)
     valid = np.isfinite(ref.out_t)
     g = (rng.standard_normal(ref.out_t.shape) * valid).astype(np.float32)
+    g64 = g.astype(np.float64)
     gW, gT = lif.backward(*d, out, _dev(torch, g), P)
     torch.cuda.synchronize()
-    oW, oT = oracle.backward(ev.ev_t, ev.ev_src, ev.ev_n, WT, ref, g.astype(np.float64), OP)
-    # neurons with a flagged near-tie are excluded from the comparison
-    okN = ~np.isfinite(ref.tie_t).any(axis=0)
-    okB = ~np.isfinite(ref.tie_t).any(axis=1)
-    if e2e:
-        rW = compare_grad(gW.cpu().numpy()[:, okN], oW[:, okN], label="grad_WT", elem_rtol=E2E_ELEM_RTOL)
-        rT = compare_grad(gT.cpu().numpy()[okB], oT[okB], label="grad_ev_t", elem_rtol=E2E_ELEM_RTOL)
-    else:
-        rW = _rel(gW.cpu().numpy()[:, okN], oW[:, okN])
-        rT = _rel(gT.cpu().numpy()[okB], oT[okB])
-    # The backward kernels alone, on identical inputs: the oracle's spikes
-    # rounded to float32 go to both sides.
-    r32 = copy.deepcopy(ref)
-    r32.out_t = ref.out_t.astype(np.float32).astype(np.float64)
-    r32.out_i = ref.out_i.astype(np.float32).astype(np.float64)
-    fwd32 = lif.ForwardOut(_dev(torch, ref.out_t.astype(np.float32)), _dev(torch, ref.out_n),
-                           _dev(torch, ref.out_i.astype(np.float32)), None)
-    hW, hT = lif.backward(*d, fwd32, _dev(torch, g), P)
+    oW, oT = oracle.backward(ev.ev_t, ev.ev_src, ev.ev_n, WT, ref, g64, OP)
+    r32 = ref.rounded()
+    qW, qT = oracle.backward(ev.ev_t, ev.ev_src, ev.ev_n, WT, r32, g64, OP)
+    ex = np.zeros(ref.out_n.shape, bool)
+    for b, i in st["excused_pairs"]:
+        ex[b, i] = True
+    okN, okB = ~ex.any(axis=0), ~ex.any(axis=1)
+    rW, fW = compare_grad_e2e(gW.cpu().numpy()[:, okN], oW[:, okN], qW[:, okN], label=f"{label} grad_WT")
+    rT, fT = compare_grad_e2e(gT.cpu().numpy()[okB], oT[okB], qT[okB], label=f"{label} grad_ev_t")
+    hW, hT = lif.backward(*d, _dev_fwd(torch, lif, r32), _dev(torch, g), P)
     torch.cuda.synchronize()
-    qW, qT = oracle.backward(ev.ev_t, ev.ev_src, ev.ev_n, WT, r32, g.astype(np.float64), OP)
-    sW = compare_grad(hW.cpu().numpy(), qW, label="grad_WT (same inputs)")
-    sT = compare_grad(hT.cpu().numpy(), qT, label="grad_ev_t (same inputs)")
-    print(f"[case] spikes={int(ref.out_n.sum())} e2e rel(gW)={rW:.2e} rel(gT)={rT:.2e}; "
+    sW = compare_grad(hW.cpu().numpy(), qW, label=f"{label} grad_WT (same inputs)")
+    sT = compare_grad(hT.cpu().numpy(), qT, label=f"{label} grad_ev_t (same inputs)")
+    print(f"[case] {label} spikes={int(ref.out_n.sum())} flagged={st['flagged']} excused={st['excused']} "
+          f"e2e rel(gW)={rW:.2e} rel(gT)={rT:.2e} (ill-conditioned entries {fW:.2%} / {fT:.2%}); "
           f"same-input rel(gW)={sW:.2e} rel(gT)={sT:.2e}", flush=True)
     return gW, gT, oW, oT
 
@@ -77,12 +80,12 @@ def _fwd_bwd(env, ev, WT, seed, s_max=64, reg=0.01, e2e=True, **kw):
 @pytest.mark.parametrize("seed,N", [(21, 64), (22, 90), (23, 20)])
 def test_backward_small(env, seed, N):
     cfg = W.random_small(seed, B=4, C=25, N=N, n_events=600, T=0.4, gain=14.0)
-    _fwd_bwd(env, cfg.events, cfg.layers[0].WT, seed)
+    _fwd_bwd(env, cfg.events, cfg.layers[0].WT, seed, label=f"small{seed}")
 
 
 def test_backward_no_regularisation_and_reset(env):
     cfg = W.random_small(24, B=3, C=25, N=70, n_events=500, T=0.4, gain=14.0)
-    _fwd_bwd(env, cfg.events, cfg.layers[0].WT, 24, reg=0.0, v_reset=-0.2)
+    _fwd_bwd(env, cfg.events, cfg.layers[0].WT, 24, reg=0.0, v_reset=-0.2, label="vr-0.2 reg0")
 
 
 @pytest.mark.parametrize("ratio", [2.0, 3.7])
@@ -91,32 +94,29 @@ def test_backward_tau_ratios(env, ratio):
     kernel derivative use both time constants; 3.7 also takes the
     exponential spike-time solve in the forward pass."""
     cfg = W.random_small(36, B=3, C=25, N=70, n_events=500, T=0.3, gain=16.0)
-    _fwd_bwd(env, cfg.events, cfg.layers[0].WT, 36, tau_mem=0.02, tau_syn=0.02 / ratio)
+    _fwd_bwd(env, cfg.events, cfg.layers[0].WT, 36, tau_mem=0.02, tau_syn=0.02 / ratio, label=f"ratio{ratio}")
 
 
 def test_backward_config2_driven(env):
     cfg = W.config2(B=4)
-    _fwd_bwd(env, cfg.events, cfg.layers[0].WT, 25, v_th=0.5)
+    _fwd_bwd(env, cfg.events, cfg.layers[0].WT, 25, v_th=0.5, label="c2 B4 th0.5")
 
 
 def test_backward_long_spike_trains(env):
     """20 000-event streams, up to about 600 spikes per neuron: long
     spike-adjoint recurrences in the setup pass and spikes spread over
-    hundreds of segments in the adjoint walk.  The kernels are checked on
-    identical inputs.  End to end, dL/dt_in is not asserted.  Rounded to
-    float32, 18 of the spike times here equal an input event's time, and 26
-    more lie within one float32 step (240 ns at 4 s) of one.  In float64
-    those events are strictly before the spike; at a tie an event counts as
-    after it, so its term drops out (about 1e-3 relative in norm here, against
-    3e-8 on identical inputs)."""
+    hundreds of segments in the adjoint walk.  End to end as well: which
+    events a spike depends on comes from the forward's consumed-event
+    counts, so float32 spike times that round onto an input event's time
+    (18 of them here) no longer drop that event's term."""
     cfg = W.random_small(35, B=2, C=40, N=96, n_events=20000, T=4.0, gain=3.0, ragged=False)
-    _fwd_bwd(env, cfg.events, cfg.layers[0].WT, 35, s_max=640, e2e=False)
+    _fwd_bwd(env, cfg.events, cfg.layers[0].WT, 35, s_max=640, label="long")
 
 
 def test_backward_silent_layer_is_zero(env):
     torch, lif = env
     cfg = W.config1()
-    _, _, oW, oT = _fwd_bwd(env, cfg.events, cfg.layers[0].WT, 26)
+    _, _, oW, oT = _fwd_bwd(env, cfg.events, cfg.layers[0].WT, 26, label="silent")
     assert np.all(oW == 0) and np.all(oT == 0)
 
 
@@ -144,6 +144,35 @@ def test_merge_bit_exact(env):
     rt, rs, rn, rp, ovf = oracle.merge(t32, n, 3)
     assert ovf and st.cpu().numpy()[0] & lif.WARN_MERGE_FULL
     assert np.array_equal(t2.cpu().numpy(), rt) and np.array_equal(s2.cpu().numpy(), rs)
+
+
+def test_merge_overflow_keeps_earliest(env):
+    """More spikes in a sample than the merge's sort holds (16 384): the
+    earliest E2_max in (time, neuron) order are kept, bit-exact against the
+    oracle's k-way merge, with many equal times across neurons at the cut.
+    The second sample fits and takes the plain path in the same launch."""
+    torch, lif = env
+    rng = np.random.default_rng(29)
+    B, N, S = 2, 600, 48
+    n = np.zeros((B, N), np.int32)
+    n[0] = rng.integers(20, S + 1, N)
+    n[1] = rng.integers(0, 20, N)
+    t = np.full((B, N, S), np.inf, np.float32)
+    for b in range(B):
+        for i in range(N):
+            t[b, i, : n[b, i]] = (np.sort(rng.choice(4000, n[b, i], replace=False)) + 1) / 4096.0
+    assert n[0].sum() > lif.LIF_MERGE_MAX and n[1].sum() < lif.LIF_MERGE_MAX
+    fwd = lif.ForwardOut(_dev(torch, t), _dev(torch, n), None, None)
+    for E2 in (lif.LIF_MERGE_MAX, 10000):
+        print(f"[case] merge overflow E2_max={E2} totals={n.sum(1).tolist()}", flush=True)
+        t2, s2, n2, perm, st = lif.merge(fwd, E2)
+        torch.cuda.synchronize()
+        rt, rs, rn, rp, ovf = oracle.merge(t, n, E2)
+        assert ovf and st.cpu().numpy()[0] & lif.WARN_MERGE_FULL
+        assert np.array_equal(n2.cpu().numpy(), rn)
+        assert np.array_equal(t2.cpu().numpy(), rt)
+        assert np.array_equal(s2.cpu().numpy(), rs)
+        assert np.array_equal(perm.cpu().numpy(), rp)
 
 
 def test_first_spike_ce(env):

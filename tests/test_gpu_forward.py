@@ -25,10 +25,13 @@ def _dev(torch, a):
     return torch.from_numpy(np.ascontiguousarray(a)).to("cuda:0")
 
 
+GPU_ONLY = ("validate", "pool_cap", "root_general")     # options of the GPU path alone
+
+
 def run_both(env, ev, WT, s_max=64, sequential=False, **kw):
     torch, lif = env
     P = lif.Params(s_max=s_max, **kw)
-    OP = oracle.LifParams(s_max=s_max, **{k: v for k, v in kw.items() if k != "validate"})
+    OP = oracle.LifParams(s_max=s_max, **{k: v for k, v in kw.items() if k not in GPU_ONLY})
     out = lif.forward(_dev(torch, ev.ev_t), _dev(torch, ev.ev_src), _dev(torch, ev.ev_n), _dev(torch, WT), P,
                       sequential=sequential)
     torch.cuda.synchronize()
@@ -43,7 +46,7 @@ def check(env, ev, WT, label, s_max=64, both=True, **kw):
         out, ref = run_both(env, ev, WT, s_max=s_max, sequential=seq, **kw)
         st = out.status.cpu().numpy()
         s = compare_spikes(out.out_t.cpu().numpy(), out.out_n.cpu().numpy(), ref, out.out_i.cpu().numpy(),
-                           label=f"{label}{' seq' if seq else ''}")
+                           label=f"{label}{' seq' if seq else ''}", out_k_gpu=out.out_k.cpu().numpy())
         assert st[2] == out.out_n.cpu().numpy().sum()
         assert st[6] == int(ev.ev_n.sum())
         assert st[1] == int(ref.capped.sum())
@@ -160,6 +163,7 @@ def test_determinism(env):
     b = lif.forward(_dev(torch, ev.ev_t), _dev(torch, ev.ev_src), _dev(torch, ev.ev_n), _dev(torch, WT))
     torch.cuda.synchronize()
     assert torch.equal(a.out_t, b.out_t) and torch.equal(a.out_n, b.out_n) and torch.equal(a.out_i, b.out_i)
+    assert torch.equal(a.out_k, b.out_k)
 
 
 def test_graph_replay_matches_eager(env):
@@ -197,6 +201,7 @@ def test_graph_replay_matches_eager(env):
         assert torch.equal(out.out_t, ref.out_t), rep
         assert torch.equal(out.out_n, ref.out_n), rep
         assert torch.equal(out.out_i, ref.out_i), rep
+        assert torch.equal(out.out_k, ref.out_k), rep
         assert torch.equal(out.status, ref.status), rep
         lif.forward(*do, P)                  # eager work between replays
         torch.cuda.synchronize()
@@ -215,25 +220,23 @@ def test_validation_flags(env):
     assert st[0] & lif.WARN_UNSORTED and st[0] & lif.WARN_BAD_SOURCE
 
 
-def test_record_pool_fallback(env, monkeypatch):
-    """With a tiny record pool the overflowing sub-blocks are resolved by the
-    re-walk fallback; results are unchanged."""
+def test_record_pool_fallback(env):
+    """With a tiny record pool (lif_params.pool_cap) the overflowing
+    sub-blocks are resolved by the re-walk fallback; results are unchanged."""
     cfg = W.random_small(9, B=3, C=30, N=130, n_events=600, T=0.4, gain=14.0)
-    monkeypatch.setenv("LIF_POOL_CAP", "5")
-    s = check(env, cfg.events, cfg.layers[0].WT, "pool5", both=False)
+    s = check(env, cfg.events, cfg.layers[0].WT, "pool5", both=False, pool_cap=5)
     assert s["par"]["status"][7] > 0
-    monkeypatch.setenv("LIF_POOL_CAP", "0")
-    s = check(env, cfg.events, cfg.layers[0].WT, "pool0", both=False)
+    s = check(env, cfg.events, cfg.layers[0].WT, "pool0", both=False, pool_cap=0)
     assert s["par"]["status"][7] >= s["par"]["status"][4] > 0   # every walked block fell back
 
 
-@pytest.mark.parametrize("npl", [1, 2, 4])
-def test_neurons_per_lane_variants(env, monkeypatch, npl):
-    """The segment walks hold 1, 2 or 4 adjacent neurons per lane; every
-    variant matches the oracle (N = 264 is a multiple of 4 but not of 256, so
-    the last tile is partial in each)."""
-    monkeypatch.setenv("LIF_NPL", str(npl))
-    cfg = W.random_small(31, B=2, C=50, N=264, n_events=700, T=0.35, gain=12.0)
+@pytest.mark.parametrize("N", [264, 266, 265])
+def test_neurons_per_lane_variants(env, N):
+    """The segment walks hold 4, 2 or 1 adjacent neurons per lane, as the
+    W^T row length allows (N = 264, 266, 265); every variant matches the
+    oracle, and in each the last tile of neurons is partial."""
+    npl = 4 if N % 4 == 0 else (2 if N % 2 == 0 else 1)
+    cfg = W.random_small(31, B=2, C=50, N=N, n_events=700, T=0.35, gain=12.0)
     s = check(env, cfg.events, cfg.layers[0].WT, f"npl{npl}", both=False)
     assert s["par"]["spikes"] > 0
 
@@ -246,14 +249,12 @@ def test_odd_neuron_count(env):
 
 
 @pytest.mark.parametrize("general", [False, True])
-def test_spike_solver_paths(env, monkeypatch, general):
-    """tau_m / tau_s = 4 takes the polynomial spike-time solve; LIF_ROOT_GENERAL
-    forces the exponential Newton solve on the same bursting input (several
-    spikes per interval).  Both match the oracle."""
-    if general:
-        monkeypatch.setenv("LIF_ROOT_GENERAL", "1")
+def test_spike_solver_paths(env, general):
+    """tau_m / tau_s = 4 takes the polynomial spike-time solve; the
+    LIF_ROOT_GENERAL flag forces the exponential Newton solve on the same
+    bursting input (several spikes per interval).  Both match the oracle."""
     cfg = W.random_small(33, B=2, C=30, N=96, n_events=600, T=0.3, gain=20.0)
-    s = check(env, cfg.events, cfg.layers[0].WT, f"solver-{'general' if general else 'poly'}")
+    s = check(env, cfg.events, cfg.layers[0].WT, f"solver-{'general' if general else 'poly'}", root_general=general)
     assert s["par"]["spikes"] > 50
 
 

@@ -21,7 +21,8 @@ from typing import List, Optional
 
 import numpy as np
 
-# Constants shared by every workload (Table 4 of the paper: tau_m = 20 ms,
+# Constants shared by every workload (the paper's hyperparameter table in App. E,
+# "System hyperparameters across the 3 datasets used": tau_m = 20 ms,
 # tau_s = 5 ms, threshold 1, reset 0, solver regularisation 0.01).
 TAU_MEM = 0.02
 TAU_SYN = 0.005
