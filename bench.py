@@ -31,7 +31,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0     # MI355X HBM3E, GB/s
-FORWARD_KERNELS = ("aggregate", "carry", "check", "records", "resolve")
+FORWARD_KERNELS = ("aggregate", "carry", "check", "resolve")
 
 
 def log(*a):

@@ -72,8 +72,8 @@ typedef struct ihipStream_t* lif_stream_t;
                                    pass (equal to LIF_ST_CAND_BLOCKS)       */
 #define LIF_ST_ROOT_SOLVES   5  /* spike-time root solves                    */
 #define LIF_ST_EVENTS        6  /* input events consumed (sum of ev_n)       */
-#define LIF_ST_POOL_FALLBACK 7  /* flagged sub-blocks past the record pool's
-                                   capacity (resolved by a slower re-walk)  */
+#define LIF_ST_POOL_FALLBACK 7  /* flagged sub-blocks past the pool's
+                                   capacity (rebuilt by a slower re-walk)   */
 
 #define LIF_WARN_SPIKE_CAP   1  /* a neuron stopped at s_max spikes          */
 #define LIF_WARN_UNSORTED    2  /* LIF_VALIDATE: times decrease in a sample  */
@@ -81,6 +81,8 @@ typedef struct ihipStream_t* lif_stream_t;
 #define LIF_WARN_NONFINITE   8  /* LIF_VALIDATE: NaN/inf event time          */
 #define LIF_WARN_MERGE_FULL 16  /* merge: more spikes than E2_max            */
 #define LIF_WARN_BAD_COUNT  32  /* LIF_VALIDATE: ev_n[b] outside [0, E_max]  */
+#define LIF_WARN_INTERNAL   64  /* internal error: a cross-workgroup wait gave
+                                   up (results are not valid)                */
 
 typedef struct lif_params {
     double   tau_mem;    /* tau_m (s); must exceed tau_syn (paper: 0.02)        */
@@ -95,11 +97,12 @@ typedef struct lif_params {
     double   solver_reg; /* backward floor on dV/dt at a spike (paper 0.01,
                             App. E hyperparameter table, "Solver
                             Regularization"); 0 disables it                     */
-    int32_t  pool_cap;   /* forward: record slots per sample for flagged
-                            event blocks; < 0 selects the library's default.
-                            Blocks past the slots are rebuilt by a slower path
-                            with identical results (0: every block is; for
-                            tests of that path).  Enters the workspace size.  */
+    int32_t  pool_cap;   /* forward: pool entries per sample (16 bytes each,
+                            the entering state of a flagged event block);
+                            < 0 selects the library's default.  Blocks past
+                            the entries are rebuilt by a slower path with
+                            identical results (0: every block is; for tests
+                            of that path).  Enters the workspace size.        */
     int32_t  reserved;   /* must be 0                                           */
 } lif_params;
 

@@ -39,6 +39,7 @@ LIF_ROOT_GENERAL = 2
 LIF_STATUS_WORDS = 8
 ST_FLAGS, ST_CAPPED, ST_SPIKES, ST_CAND_BLOCKS, ST_WALKED_BLOCKS, ST_ROOT_SOLVES, ST_EVENTS, ST_POOL_FALLBACK = range(8)
 WARN_SPIKE_CAP, WARN_UNSORTED, WARN_BAD_SOURCE, WARN_NONFINITE, WARN_MERGE_FULL, WARN_BAD_COUNT = 1, 2, 4, 8, 16, 32
+WARN_INTERNAL = 64
 LIF_MERGE_MAX = 16384
 
 EXPORTED = ["lif_version", "lif_layer_forward_workspace_size", "lif_layer_forward",

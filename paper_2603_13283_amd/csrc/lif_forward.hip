@@ -16,24 +16,25 @@
 //                Combine of the segment's maps.
 //   k_carry      per (sample, 64 neurons): exclusive Combine scan over the
 //                segments (diagonal maps in (U, J)), giving the no-reset
-//                state entering every segment.
+//                state entering every segment; it overwrites the aggregates.
 //   k_check      per (sample, segment, tile): re-walk from the carried state
 //                with a no-crossing screen per inter-event interval
 //                (screen_value).  Resets only lower V, so a sub-block of kSub
 //                events whose no-reset trajectory passes every screen holds
-//                no spike whatever happened before it; a flagged
-//                sub-block stores its entering state and reserves a record.
-//   k_records    per reserved record (lanes are the sub-block's intervals):
-//                the no-reset states at every interval boundary of the
-//                sub-block and each interval's crossing data; also resets the
-//                outputs ahead of the resolve pass.
+//                no spike whatever happened before it; a flagged sub-block
+//                reserves a pool entry and stores its entering state there.
 //   k_resolve    per (sample, neuron) with flagged sub-blocks: walks only
-//                those, in time order.  Spikes found so far lower V by a
-//                known decaying amount (the reset deficit), which corrects
-//                the recorded states exactly.  Each interval is tested with
-//                the interval rule (Sec. 3.2.2), the spike time is solved by
-//                bracketed Newton (Appendix D.1), V is hard-reset and the
-//                same interval is tested again from the spike (Appendix E.2).
+//                those, in time order.  Staging waves walk each flagged
+//                sub-block from its entering state (the no-reset state at
+//                every interval start) and compute each interval's crossing
+//                key, filling a ring of LDS windows ahead of the chain wave.
+//                Spikes found so far lower V by a known decaying amount (the
+//                reset deficit), which corrects the no-reset states exactly;
+//                an interval crosses iff its key is at least the deficit's
+//                current key (the interval rule of Sec. 3.2.2, one compare
+//                per interval).  The spike time is solved by bracketed Newton
+//                (Appendix D.1), V is hard-reset and the same interval is
+//                tested again from the spike (Appendix E.2).
 // The sequential baseline k_sequential (Appendix E.3) runs the same interval
 // rule and root solve one event at a time per (sample, neuron).
 #include "lif_common.hpp"
@@ -42,28 +43,35 @@
 
 namespace lif {
 
-// Record of one flagged sub-block of one neuron, in per-sample pools.  The
-// check pass reserves it (one atomic per wave) and writes its header; the
-// record pass k_records fills in, per interval j of the sub-block, the
-// no-reset state (V, I) at the interval start and the interval's crossing
-// data.  With the reset deficit of the spikes found so far these give the
-// true state at every interval boundary in O(1), so the resolve pass can test
-// all intervals of the sub-block at once.
-struct alignas(16) Record {
-    double2 s[kSub + 1];    // s[j]: state at the start of interval j (after event j - 1); in the
-                            // sub-block holding the sample's last event, s[cnt]: the state after it
-    double crit[kSub + 1];  // interval j crosses iff the deficit at its start is <= crit[j] (< 0: never);
-                            // entry kSub: the open interval after the sample's last event (in the
-                            // record of the sub-block that holds it)
-    double hi[kSub + 1];    // right end of interval j's root bracket (u* or its length)
-    double fhi[kSub + 1];   // h(hi) of interval j (F(hi) = fhi - deficit)
-    int32_t kq0, cnt, n;    // first event of the sub-block (index in the sample), events in it, neuron
-    int32_t pad_[3];
-};
-static_assert(sizeof(Record) % 16 == 0, "record layout");
+// Pool of entering states: one entry (the no-reset (U, J) entering the
+// sub-block) per flagged (sub-block, neuron), in per-sample slices.  The
+// check pass reserves the entries (one atomic per wave) and writes them; the
+// resolve pass rebuilds the sub-block's interval states from them.
 constexpr uint32_t kNoSlot = 0xffffffffu;
 
-// Per-sample counters (record-pool use, work-list length) each take their
+// Mask word of a (sample, segment, neuron): the flagged sub-blocks in bits
+// 0..3, the pool offset of the pair's first entry in bits 4..31.
+constexpr int kMaskBits = 4;
+static_assert(kSubPerSeg <= kMaskBits, "mask word layout");
+
+// Search key of an interval whose crossing test is "reset deficit at its
+// start <= crit" (crossing_data).  The deficit of the spikes so far is
+// D(t) = dref e^{-(t - tref)/tm}, so at an interval that starts at t0 the
+// test reads ln(crit) + t0/tm >= ln(dref) + tref/tm.  crit < 0 (never
+// crosses) gives NaN, for which every comparison is false; crit = 0 gives
+// -inf, which only the deficit of no spike at all (ln 0) reaches.
+__device__ __forceinline__ double crossing_key(const Model& m, double crit, double t0)
+{
+    if (!(crit >= 0.0)) return __builtin_nan("");
+    if (crit == 0.0) return -INFINITY;
+    return log(crit) + t0 * m.inv_tm;
+}
+
+// A wait inside a workgroup that does not end within this many polls is an
+// internal error (reported in the status words instead of waiting for ever).
+constexpr int kSpinLimit = 1 << 22;
+
+// Per-sample counters (pool use, work-list length) each take their
 // own 128-byte line: many waves update them with atomics, and atomics on one
 // line are serialised.
 constexpr int kCtr = 32;
@@ -164,6 +172,14 @@ __device__ __forceinline__ void step(double A, double D, const float (&w)[NPL], 
     }
 }
 
+// One event in eigen-coordinates: decay over the gap, then the jump.
+__device__ __forceinline__ void step1(double2 ad, float w, double& U, double& J)
+{
+    const double x = (double)w;
+    U = fma(ad.x, U, x);
+    J = fma(ad.y, J, x);
+}
+
 // Walk the n events of a group starting at e0 (n = kGrp on every group but
 // a sample's last).
 template <int NPL>
@@ -191,15 +207,27 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_aggregate(
     const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
     int E_pad, const float* __restrict__ WT, int C_in, int N, int tiles, int S, int items, Model m,
     Decay* __restrict__ dec, double2* __restrict__ segm, double2* __restrict__ agg, int32_t* __restrict__ status,
-    uint32_t* __restrict__ counters, size_t n_counters, uint32_t* __restrict__ listed, size_t nn)
+    uint32_t* __restrict__ counters, size_t n_counters, uint32_t* __restrict__ listed, size_t nn,
+    int32_t* __restrict__ out_n, float* __restrict__ out_t, float* __restrict__ out_i, int32_t* __restrict__ out_k,
+    size_t n_out)
 {
     {
         // resets for the later passes: status words, per-sample counters,
-        // listed flags (grid-stride over every thread)
+        // listed flags, and the outputs (the resolve pass writes only the
+        // neurons that fire: counts 0, times +inf, currents and event
+        // counts 0), grid-stride over every thread
         const size_t gt = (size_t)blockIdx.x * blockDim.x + threadIdx.x, gs = (size_t)gridDim.x * blockDim.x;
         if (gt < LIF_STATUS_WORDS) status[gt] = 0;
         for (size_t i = gt; i < n_counters; i += gs) counters[i] = 0u;
-        for (size_t i = gt; i < nn; i += gs) listed[i] = 0u;
+        for (size_t i = gt; i < nn; i += gs) {
+            listed[i] = 0u;
+            out_n[i] = 0;
+        }
+        for (size_t i = gt; i < n_out; i += gs) {
+            out_t[i] = INFINITY;
+            if (out_i) out_i[i] = 0.0f;
+            if (out_k) out_k[i] = 0;
+        }
     }
     __shared__ double2 s_ad[kWalkWaves][kSeg];
     WalkCoords c;
@@ -254,13 +282,14 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_aggregate(
 // range of at most kCarryBatch segments per round.  Each wave folds its range
 // from the zero state (its aggregates loaded at once and kept), the range
 // totals are combined across waves in LDS, and each wave walks its range
-// again from its incoming state, writing the carries.
+// again from its incoming state, writing the carries over the aggregates
+// (each element is read before it is written, by the same wave).
 constexpr int kCarryWaves = 8;
 constexpr int kCarryBatch = 16;
 
 __global__ __launch_bounds__(kWave * kCarryWaves) void k_carry(
     const int32_t* __restrict__ ev_n, int B, int E_max, int N, int tiles, int S, const double2* __restrict__ segm,
-    const double2* __restrict__ agg, double2* __restrict__ carry)
+    const double2* agg, double2* carry)
 {
     __shared__ double2 tot[kCarryWaves][kWave];      // range map b-part
     __shared__ double2 dec_tot[kCarryWaves];         // range map diagonal
@@ -380,22 +409,23 @@ __device__ __forceinline__ void screen_grp(const Model& m, const double2* __rest
 // Re-walk from the carried no-reset state with the no-crossing screen on
 // every interval: the interval before each event of the sub-block and, in
 // the sub-block holding the sample's last event, the open interval after it
-// (up to t_end).  A flagged (sub-block, neuron) stores its entering state
-// (U, J) in ent and sets a bit in the neuron's sub-block mask of the segment.
-// At the end of the item the wave reserves records for all its flagged
-// sub-blocks with one atomic on the sample's pool counter, in lane order, so
-// that the records of one (segment, neuron) are consecutive: the mask word
-// of the pair holds the sub-block bits and the pool offset of its first
-// record, and the record of a flagged sub-block is that offset plus the
-// number of flagged sub-blocks before it (none past the pool capacity: the
-// resolve pass then rebuilds that sub-block's states from ent itself).  The
-// wave writes the records' headers; the first segment to flag a neuron
-// appends it to the sample's work list.
+// (up to t_end).  A flagged (sub-block, neuron) sets a bit in the neuron's
+// sub-block mask of the segment; the entering state (U, J) of every
+// sub-block is kept in LDS until the pool entries are reserved.  At the end
+// of the item the wave reserves entries for all its flagged sub-blocks with
+// one atomic on the sample's pool counter, in lane order, so that the
+// entries of one (segment, neuron) are consecutive: the mask word of the pair
+// holds the sub-block bits and the pool offset of its first entry, and the
+// entry of a flagged sub-block is that offset plus the number of flagged
+// sub-blocks before it (none past the pool capacity: the resolve pass then
+// rebuilds that sub-block's entering state from the segment's carried
+// state).  The wave writes the entering states; the first segment to flag a
+// neuron appends it to the sample's work list.
 __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
     const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
     int E_pad, const float* __restrict__ WT, int C_in, int N, int tiles, int S, int items, Model m,
-    const Decay* __restrict__ dec, const double2* __restrict__ carry, double2* __restrict__ ent,
-    uint2* __restrict__ mask, Record* __restrict__ pool,
+    const Decay* __restrict__ dec, const double2* __restrict__ carry, uint32_t* __restrict__ mask,
+    double2* __restrict__ pool,
     uint32_t* __restrict__ pool_count, uint32_t pool_cap, uint32_t* __restrict__ listed,
     uint32_t* __restrict__ work, uint32_t* __restrict__ nwork)
 // work: per-sample lists of the neurons with flagged sub-blocks (capacity N
@@ -405,6 +435,7 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
     __shared__ double2 s_ad[kWalkWaves][kSeg];
     __shared__ double s_lk[kWalkWaves][kSeg];
     __shared__ double s_gk[kWalkWaves][kGrpPerSeg];
+    __shared__ double2 s_ent[kWalkWaves][kSubPerSeg][kWave];   // entering state of each sub-block
     WalkCoords c;
     if (!walk_coords<NPL>(items, tiles, S, ev_n, E_max, N, c)) return;
     const int lane = c.lane;
@@ -454,16 +485,13 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
             for (int i = 0; i < NPL; ++i)
                 z[i] = fmax(z[i], J[i] > m.th ? fma(J[i] - m.th, open_lk, U[i] - J[i]) : U[i] - J[i]);
         }
-        const size_t srow = (((size_t)c.b * S + c.seg) * kSubPerSeg + q) * N + c.n0;
+        s_ent[wv][q][lane] = make_double2(U0[0], J0[0]);
 #pragma unroll
         for (int i = 0; i < NPL; ++i)
-            if (c.live && z[i] >= m.thk_lo) {
-                ent[srow + i] = make_double2(U0[i], J0[i]);
-                msk[i] |= 1u << q;
-            }
+            if (c.live && z[i] >= m.thk_lo) msk[i] |= 1u << q;
     }
-    // Records of the wave's flagged sub-blocks: one reservation, slots in
-    // lane order (exclusive prefix sum of the per-lane counts).
+    // Pool entries of the wave's flagged sub-blocks: one reservation, slots
+    // in lane order (exclusive prefix sum of the per-lane counts).
     {
         uint32_t mine = 0;
 #pragma unroll
@@ -483,15 +511,9 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
         }
 #pragma unroll
         for (int i = 0; i < NPL; ++i) {
-            if (c.live) mask[row + i] = make_uint2(msk[i], base);
+            if (c.live) mask[row + i] = msk[i] | (base << kMaskBits);
             for (uint32_t mm = msk[i]; mm; mm &= mm - 1u) {
-                if (base < pool_cap) {
-                    Record* r = pool + ((size_t)c.b * pool_cap + base);
-                    const int kq0 = c.k0 + __builtin_ctz(mm) * kSub;
-                    r->kq0 = kq0;
-                    r->cnt = min(kSub, c.nb - kq0);
-                    r->n = c.n0 + i;
-                }
+                if (base < pool_cap) pool[(size_t)c.b * pool_cap + base] = s_ent[wv][__builtin_ctz(mm)][lane];
                 ++base;
             }
         }
@@ -530,79 +552,13 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_check(
         }
     }
 }
-// ---------------------------------------------------------------------------
-// Resolve pass: one workgroup of two waves per neuron that has flagged
-// sub-blocks (a work list built by the check pass).  Intervals outside
-// flagged sub-blocks provably hold no spike.  The flagged sub-blocks are
-// taken in time order:
-//   * Candidate list: per chunk of kChunkEv events, the sub-block masks (one
-//     to two segments per lane) are compacted into
-//     a time-ordered list in LDS with one wave prefix sum, with the record
-//     slot of every candidate.
-//   * Windows of kWinCand candidates in two LDS buffers: the staging wave
-//     (wave 1) loads and commits window w + 1 into one buffer while the chain
-//     wave (wave 0) resolves window w from the other, so the loads and LDS
-//     writes of a window stay off the serial chain.  One barrier per window.
-//   * Steps of kWave / kSub = 4 candidates: lane l takes interval l % kSub of
-//     candidate l / kSub, so time order is lane order.  Each interval
-//     carries its crossing data (k_records): it crosses iff the reset
-//     deficit at its start is <= crit.  A round takes the earliest crossing
-//     interval (ballot), solves its spike time (root_h) on its lane, emits
-//     the spike and raises that interval's own deficit (so it is tested again
-//     for a second spike, Appendix E.2 restart); every later interval takes
-//     the new deficit with one exponential.  Rounds repeat until no interval
-//     of the step crosses.
-//   * The open interval after the sample's last event is one more step (one
-//     lane) after the last window.
-//   * Spikes are buffered in LDS and written out kWave at a time.
-// The resolve kernel runs few waves per compute unit, so nearly all of its
-// code is fetched cold: every path is written once (no unrolled copies of
-// the solver or of the rare rebuild of sub-blocks without a record).
-// Wave-uniform state: spike count, reset deficit dref right after the
-// latest spike, at time tref.
-// ---------------------------------------------------------------------------
-constexpr int kChunkEv = 8192;                   // events per chunk of the candidate list
-constexpr int kChunkSeg = kChunkEv / kSeg;       // segments per chunk
-constexpr int kSegPerLane = kChunkSeg / kWave;   // mask words per lane
-static_assert(kChunkSeg % kWave == 0 && kSubPerSeg <= 8, "chunk layout; 3-bit sub-block field of a candidate");
-constexpr int kCandCap = kChunkSeg * kSubPerSeg; // candidates of one chunk
-constexpr int kStep = kWave / kSub;              // candidates per step
-constexpr int kWinCand = 16;                     // candidates per window
-constexpr int kWinIv = kWinCand * kSub;          // intervals per window
-constexpr int kIvPerLane = kWinIv / kWave;       // window intervals staged by each lane
-constexpr int kWinSteps = kWinCand / kStep;
-constexpr int kOpenIv = kWinIv;                  // window slot of the open interval
-
-// One window, interval i = candidate * kSub + j; slot kOpenIv: the open
-// interval.
-struct WinBuf {
-    double crit[kWinIv + 1], hi[kWinIv + 1], fhi[kWinIv + 1];
-    double2 s0[kWinIv + 1];                      // (V0, I0)
-    double t0[kWinIv + 1];                       // interval start
-    int32_t kev[kWinIv + 1];                     // index of the event that closes the interval (ev_n[b]: open)
-};
-
-struct ResolveLds {
-    uint32_t cand[kCandCap];                     // (segment in chunk << 3) | sub-block
-    uint32_t slot[kCandCap];                     // record slot of each candidate (kNoSlot: none)
-    WinBuf win[2];
-    double sp_t0[kWave], sp_y[kWave];            // spike buffer: interval start, e^{-u/tm},
-    float si[kWave];                             // I at the spike,
-    int32_t sk[kWave];                           // events consumed before the spike
-    int ntot;                                    // candidates of the chunk (chain wave -> both)
-    int stop[2];                                 // capped after window w (slot w % 2)
-};
-constexpr int kResolveWaves = 2;
-
 // Crossing data of one interval of length L that starts in the no-reset
 // state (V0, I0) and ends with V1 (A, D: its decays): the interval reaches
 // the threshold iff the reset deficit at its start is <= crit (crit < 0:
 // never), by interval_max's test D a <= g; the spike then lies in
 // (lo, hi] with F(hi) = fhi - deficit.  Zero-length intervals never cross.
-// k_records and the resolve pass (sub-blocks without a record)
-// both evaluate it; with floating-point contraction off here and in
-// interval_max, every inlined copy performs the same IEEE operations, so
-// both give the same bits whichever path a sub-block takes.
+// Floating-point contraction is off here and in interval_max, so every
+// inlined copy performs the same IEEE operations.
 __device__ __forceinline__ void crossing_data(const Model& m, double V0, double I0, double V1, double L, double A,
                                               double D, double& crit, double& hi, double& fhi)
 {
@@ -631,165 +587,6 @@ __device__ __forceinline__ void open_interval_data(const Model& m, double V, dou
     crossing_data(m, V, I, V1, L, A, D, crit, hi, fhi);
 }
 
-// States of interval j of a sub-block (events kq0 .. kq0 + cnt - 1 of the
-// sample) from the sub-block's entering no-reset state (U, J): the lane walks
-// events 0 .. j, taking the state at the interval start (after event j - 1)
-// and, after event j, V at the interval end and J.  The record pass and the
-// resolve pass's rebuild of sub-blocks without a record both call it, so the
-// two give the same bits.
-struct IvStates {
-    double V0, I0, V1, J1;
-};
-
-template <bool kHoist>
-__device__ __forceinline__ IvStates subblock_walk(const Model& m, double U, double J, int kq0, int cnt, int j, int n,
-                                                  int N, int C_in, const int32_t* __restrict__ src,
-                                                  const Decay* __restrict__ d, const float* __restrict__ WT)
-{
-    IvStates r{0.0, 0.0, 0.0, 0.0};
-    const int last = max(cnt - 1, 0);
-    if constexpr (kHoist) {
-        // every load first (independent, clamped to the sub-block), then the walk
-        int sc[kSub];
-#pragma unroll
-        for (int e = 0; e < kSub; ++e) sc[e] = clamp_src(src[kq0 + min(e, last)], C_in);
-        float wv[kSub];
-        double2 ad[kSub];
-#pragma unroll
-        for (int e = 0; e < kSub; ++e) {
-            wv[e] = WT[(size_t)sc[e] * (size_t)N + n];
-            const Decay dk = d[kq0 + min(e, last)];
-            ad[e] = make_double2(dk.A, dk.D);
-        }
-#pragma unroll
-        for (int e = 0; e < kSub; ++e) {
-            if (e == j) {
-                r.V0 = v_of(m, U, J);
-                r.I0 = J;
-            }
-            if (e <= j && e < cnt) {
-                const double w = (double)wv[e];
-                U = fma(ad[e].x, U, w);
-                J = fma(ad[e].y, J, w);
-            }
-        }
-    } else {
-        // the same operations, one event at a time (few registers)
-        for (int e = 0; e < kSub; ++e) {
-            if (e == j) {
-                r.V0 = v_of(m, U, J);
-                r.I0 = J;
-            }
-            const int k = kq0 + min(e, last);
-            const bool step_in = e <= j && e < cnt;
-            const double w = step_in ? (double)WT[(size_t)clamp_src(src[k], C_in) * (size_t)N + n] : 0.0;
-            const Decay dk = d[k];
-            if (step_in) {
-                U = fma(dk.A, U, w);
-                J = fma(dk.D, J, w);
-            }
-        }
-    }
-    r.V1 = v_of(m, U, J);
-    r.J1 = J;
-    return r;
-}
-
-// k_records: the states and crossing data of every reserved record, in
-// parallel (lanes are intervals, 4 records per wave), and of the open
-// interval in the record of each sample's last sub-block.  This keeps the
-// sub-block walks and the closed-form maximum of each interval (a log and an
-// exp) off the resolve pass's per-neuron serial chain.  Grid: (blocks per
-// sample, B); the records of sample blockIdx.y are spread over that sample's
-// blocks.
-__global__ __launch_bounds__(256) void k_records(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src,
-                                                 const int32_t* __restrict__ ev_n, int E_max, int E_pad, int S,
-                                                 const float* __restrict__ WT, int C_in, int N, Model m,
-                                                 const Decay* __restrict__ dec, const double2* __restrict__ ent,
-                                                 Record* __restrict__ pool, const uint32_t* __restrict__ pool_count,
-                                                 uint32_t pool_cap, int32_t* __restrict__ out_n, size_t nn,
-                                                 float* __restrict__ out_t, float* __restrict__ out_i,
-                                                 int32_t* __restrict__ out_k, size_t n_out, int B,
-                                                 int32_t* __restrict__ status)
-{
-    if (blockIdx.x == gridDim.x - 1 && blockIdx.y == gridDim.y - 1 && threadIdx.x >= blockDim.x - kWave) {
-        // status words fixed once the check pass has run (the only writer of
-        // these words in the call): events consumed, flagged sub-blocks,
-        // sub-blocks past the pool's capacity
-        const int l = (int)threadIdx.x % kWave;
-        unsigned long long ev = 0, fl = 0, fb = 0;
-        for (int bb = l; bb < B; bb += kWave) {
-            ev += (unsigned long long)clamp_count(ev_n[bb], E_max);
-            const uint32_t pc = pool_count[(size_t)bb * kCtr];
-            fl += pc;
-            fb += pc > pool_cap ? pc - pool_cap : 0u;
-        }
-#pragma unroll
-        for (int off = 32; off > 0; off >>= 1) {
-            ev += __shfl_xor(ev, off, kWave);
-            fl += __shfl_xor(fl, off, kWave);
-            fb += __shfl_xor(fb, off, kWave);
-        }
-        if (l == 0) {
-            auto sat = [](unsigned long long x) { return (int32_t)(x > 0x7fffffffull ? 0x7fffffffull : x); };
-            status[LIF_ST_EVENTS] = sat(ev);
-            status[LIF_ST_CAND_BLOCKS] = sat(fl);
-            status[LIF_ST_WALKED_BLOCKS] = sat(fl);
-            status[LIF_ST_POOL_FALLBACK] = sat(fb);
-        }
-    }
-    {
-        // outputs reset ahead of the resolve pass (it writes only the
-        // neurons that fire): counts 0, times +inf, currents and event
-        // counts 0
-        const size_t gs = (size_t)gridDim.x * gridDim.y * blockDim.x;
-        const size_t gt = ((size_t)blockIdx.y * gridDim.x + blockIdx.x) * blockDim.x + threadIdx.x;
-        for (size_t i = gt; i < nn; i += gs) out_n[i] = 0;
-        for (size_t i = gt; i < n_out; i += gs) {
-            out_t[i] = INFINITY;
-            if (out_i) out_i[i] = 0.0f;
-            if (out_k) out_k[i] = 0;
-        }
-    }
-    const int lane = (int)threadIdx.x % kWave;
-    const int j = lane % kSub;
-    const uint32_t gw = (blockIdx.x * blockDim.x + threadIdx.x) / kWave;
-    const uint32_t nw = gridDim.x * blockDim.x / kWave;
-    constexpr uint32_t kRecPerWave = kWave / kSub;
-    const int b = blockIdx.y;
-    const int nb = clamp_count(ev_n[b], E_max);
-    const uint32_t used = min(pool_count[(size_t)b * kCtr], pool_cap);
-    const float* tt = ev_t + (size_t)b * E_max;
-    const int32_t* src = ev_src + (size_t)b * E_max;
-    const Decay* d = dec + (size_t)b * E_pad;
-    for (uint32_t r0 = gw * kRecPerWave; r0 < used; r0 += nw * kRecPerWave) {
-        const uint32_t r = r0 + (uint32_t)(lane / kSub);
-        if (r >= used) continue;
-        Record* rec = pool + (size_t)b * pool_cap + r;
-        const int kq0 = rec->kq0, cnt = rec->cnt, n = rec->n;
-        if (j >= cnt || kq0 < 0 || kq0 + j >= nb || n < 0 || n >= N) continue;
-        const int seg = kq0 / kSeg, q = (kq0 % kSeg) / kSub;
-        const double2 e0 = ent[(((size_t)b * S + seg) * kSubPerSeg + q) * N + n];
-        const IvStates v = subblock_walk<true>(m, e0.x, e0.y, kq0, cnt, j, n, N, C_in, src, d, WT);
-        const int k = kq0 + j;
-        const double t0 = k > 0 ? (double)tt[k - 1] : 0.0;
-        double crit, hi, fhi;
-        crossing_data(m, v.V0, v.I0, v.V1, (double)tt[k] - t0, d[k].A, d[k].D, crit, hi, fhi);
-        rec->s[j] = make_double2(v.V0, v.I0);
-        rec->crit[j] = crit;
-        rec->hi[j] = hi;
-        rec->fhi[j] = fhi;
-        if (k == nb - 1) {
-            // the open interval after the sample's last event
-            open_interval_data(m, v.V1, v.J1, m.t_end - (double)tt[k], crit, hi, fhi);
-            rec->s[j + 1] = make_double2(v.V1, v.J1);
-            rec->crit[kSub] = crit;
-            rec->hi[kSub] = hi;
-            rec->fhi[kSub] = fhi;
-        }
-    }
-}
-
 __device__ __forceinline__ int rl_int(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
 
 __device__ __forceinline__ double rl_double(double v, int l)
@@ -800,90 +597,220 @@ __device__ __forceinline__ double rl_double(double v, int l)
     return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
 
-// Loads of window interval h kWave + lane: candidate c = c0 + h kStep +
-// lane / kSub, interval j = lane % kSub (unconditional loads from clamped
-// addresses; nothing derived from the loaded values here).
-struct StageIv {
-    double crit, hi, fhi;
-    double2 s0;
-    float tp;
+// ---------------------------------------------------------------------------
+// Resolve pass: one workgroup of four waves per neuron that has flagged
+// sub-blocks (the work lists of the check pass).  Intervals outside flagged
+// sub-blocks provably hold no spike.  The flagged sub-blocks are taken in
+// time order:
+//   * Candidate list: per chunk of kChunkEv events, the sub-block masks (two
+//     segments per lane) are compacted into a time-ordered list in LDS with
+//     one wave prefix sum, with the pool slot of every candidate.
+//   * Windows of kWinCand candidates (kWinIv intervals) in a ring of kRing
+//     LDS buffers: the staging waves (waves 1..3, windows in turn) walk the
+//     window's sub-blocks and fill its buffer while the chain wave (wave 0)
+//     works on an earlier one; a ready word per buffer and a consumed count
+//     hand the buffers over (no barrier per window).
+//   * The chain searches a window 64 intervals at a time: interval i crosses
+//     iff key_i >= K, the key of the current reset deficit (crossing_key), so
+//     one ballot finds the earliest crossing.  Its spike time is solved
+//     wave-uniform, the deficit and K are raised, and the search resumes at
+//     the same interval (a second spike in it, App. E.2 restart).
+//   * The open interval after the sample's last event is one more slot of
+//     the window holding the sample's last sub-block.
+//   * Spikes are buffered in LDS and written out kWave at a time.
+// ---------------------------------------------------------------------------
+constexpr int kChunkEv = 8192;                   // events per chunk of the candidate list
+constexpr int kChunkSeg = kChunkEv / kSeg;       // segments per chunk
+constexpr int kSegPerLane = kChunkSeg / kWave;   // mask words per lane
+static_assert(kChunkSeg % kWave == 0 && kSubPerSeg <= 8, "chunk layout; 3-bit sub-block field of a candidate");
+constexpr int kCandCap = kChunkSeg * kSubPerSeg; // candidates of one chunk
+constexpr int kCandPerStep = kWave / kSub;       // candidates per 64 intervals
+constexpr int kWinCand = kCandPerStep;           // candidates per window (one interval per lane)
+constexpr int kWinIv = kWinCand * kSub;          // intervals per window
+static_assert(kWinIv == kWave, "one window interval per lane");
+constexpr int kOpenIv = kWinIv;                  // window slot of the open interval
+constexpr int kRing = 8;                         // window buffers
+constexpr int kResolveWaves = 4;                 // the chain wave and three staging waves
+
+struct WinBuf {
+    double key[kWinIv + 1];                      // crossing key (NaN: no interval)
+    double v0[kWinIv + 1], i0[kWinIv + 1];       // no-reset (V, I) at the interval start
+    float t0[kWinIv + 1];                        // interval start (time of the event before it; 0 for the first)
+    float t1[kWinIv + 1];                        // interval end (its closing event's time)
 };
 
-__device__ __forceinline__ StageIv stage_load(const ResolveLds& sh, int c, int tot, int seg0, int nb, int j,
-                                              const float* __restrict__ tt, const Record* __restrict__ pool)
+struct ResolveLds {
+    uint32_t cand[kCandCap];                     // (segment in chunk << 3) | sub-block
+    uint32_t slot[kCandCap];                     // pool slot of each candidate (kNoSlot: none)
+    WinBuf win[kRing];
+    double sp_t0[kWave], sp_y[kWave];            // spike buffer: interval start, e^{-u/tm},
+    float si[kWave];                             // I at the spike,
+    int32_t sk[kWave];                           // events consumed before the spike
+    double open_len;                             // length of the open interval (t_end - last event)
+    int ntot;                                    // candidates of the chunk (chain wave -> both)
+    int ready[kRing];                            // 1 + window index staged in each buffer
+    double kmax[kRing];                          // largest key of each buffer's window (NaN keys left out)
+    int consumed;                                // windows the chain has finished
+    int stop;                                    // the chain reached s_max
+};
+
+__device__ __forceinline__ int lds_load(const int* p)
 {
-    StageIv v;
-    const int cc = min(c, tot - 1);
-    const uint32_t cw = sh.cand[cc];
-    const uint32_t slot = sh.slot[cc];
-    const int kq0 = (seg0 + (int)(cw >> 3)) * kSeg + (int)(cw & 7u) * kSub;
-    const int k = min(kq0 + j, nb - 1);
-    v.tp = tt[max(k - 1, 0)];
-    const Record* rec = pool + (slot != kNoSlot ? slot : 0u);   // pool holds at least one record
-    v.s0 = rec->s[j];
-    v.crit = rec->crit[j];
-    v.hi = rec->hi[j];
-    v.fhi = rec->fhi[j];
-    return v;
+    return __hip_atomic_load(const_cast<int*>(p), __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
-// Sub-blocks without a record (the pool was full): rebuild the window's
-// intervals from the sub-blocks' entering states (U, J) with subblock_walk,
-// as the record pass does, then the crossing data (and the open interval's,
-// on the lane of the sample's last event).
-__device__ __forceinline__ void rebuild_window(const ResolveLds& sh, WinBuf& w, const Model& m, int c0, int tot,
-                                               int seg0, int b, int n, int nb, int S, int N, int C_in,
-                                               const float* __restrict__ tt, const int32_t* __restrict__ src,
-                                               const Decay* __restrict__ d, const float* __restrict__ WT,
-                                               const double2* __restrict__ ent)
+__device__ __forceinline__ void lds_store(int* p, int v)
+{
+    __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// Entering no-reset state of sub-block kq0 (of the segment whose first
+// event is k0) from the segment's carried state (U, J), for a sub-block past
+// the pool's capacity, by the whole wave: lane e loads event k0 + e's weight
+// and decays, and every lane follows the same serial walk over events k0 ..
+// kq0 - 1 with those values broadcast (the check pass's operations, so the
+// state has the bits a pool entry would hold).  Wave-uniform result.
+__device__ double2 rebuild_entry(double U, double J, int k0, int kq0, int n, int N, int C_in,
+                                 const int32_t* __restrict__ src, const Decay* __restrict__ d,
+                                 const float* __restrict__ WT)
 {
     const int lane = (int)threadIdx.x % kWave;
-    const int j = lane % kSub;
-    for (int h = 0; h < kIvPerLane; ++h) {
-        const int c = c0 + h * kStep + lane / kSub;
-        const bool in = c < tot;
-        const int cc = min(c, tot - 1);
-        const bool fb = in && sh.slot[cc] == kNoSlot;
-        if (!__ballot(fb)) continue;
-        const uint32_t cw = sh.cand[cc];
-        const int seg = seg0 + (int)(cw >> 3), q = (int)(cw & 7u);
-        const int kq0 = seg * kSeg + q * kSub, cnt = min(kSub, nb - kq0);
-        const double2 e0 = fb ? ent[(((size_t)b * S + seg) * kSubPerSeg + q) * N + n] : make_double2(0.0, 0.0);
-        const IvStates v = subblock_walk<true>(m, e0.x, e0.y, kq0, cnt, j, n, N, C_in, src, d, WT);
-        if (fb && j < cnt) {
-            const int i = h * kWave + lane;
-            const int k = kq0 + j;
-            const double t0 = k > 0 ? (double)tt[k - 1] : 0.0;
-            const Decay dk = d[k];
-            crossing_data(m, v.V0, v.I0, v.V1, (double)tt[k] - t0, dk.A, dk.D, w.crit[i], w.hi[i], w.fhi[i]);
-            w.s0[i] = make_double2(v.V0, v.I0);
-            if (k == nb - 1) {
-                open_interval_data(m, v.V1, v.J1, m.t_end - (double)tt[k], w.crit[kOpenIv], w.hi[kOpenIv],
-                                   w.fhi[kOpenIv]);
-                w.s0[kOpenIv] = make_double2(v.V1, v.J1);
-            }
-        }
+    const int ne = kq0 - k0;
+    float we = 0.0f;
+    double A = 1.0, D = 1.0;
+    if (lane < ne) {
+        we = WT[(size_t)clamp_src(src[k0 + lane], C_in) * (size_t)N + n];
+        const Decay dk = d[k0 + lane];
+        A = dk.A;
+        D = dk.D;
     }
+    for (int e = 0; e < ne; ++e) {
+        const float w = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, we), e));
+        step1(make_double2(rl_double(A, e), rl_double(D, e)), w, U, J);
+    }
+    return make_double2(U, J);
 }
 
+// Lane E's value of the calling lane's row of 16 lanes (DPP row broadcast).
+template <int E>
+__device__ __forceinline__ int row_bcast(int v)
+{
+    return __builtin_amdgcn_update_dpp(0, v, 0x150 + E, 0xf, 0xf, false);
+}
+
+template <int E>
+__device__ __forceinline__ double row_bcast(double v)
+{
+    const unsigned long long u = (unsigned long long)__double_as_longlong(v);
+    const unsigned lo = (unsigned)row_bcast<E>((int)(unsigned)u), hi = (unsigned)row_bcast<E>((int)(unsigned)(u >> 32));
+    return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+
+// Step E of a sub-block walk: lane j takes its interval's start state before
+// event E = j, and steps the state through event E while E <= j (event E's
+// weight and decays come from lane E of the row).
+template <int E>
+__device__ __forceinline__ void walk_from(const Model& m, int j, float wv, double2 ad, double& U, double& J,
+                                          double& V0, double& I0)
+{
+    const float w = __builtin_bit_cast(float, row_bcast<E>(__builtin_bit_cast(int, wv)));
+    const double A = row_bcast<E>(ad.x), D = row_bcast<E>(ad.y);
+    if (E == j) {
+        V0 = v_of(m, U, J);
+        I0 = J;
+    }
+    if (E <= j) step1(make_double2(A, D), w, U, J);
+    if constexpr (E + 1 < kSub) walk_from<E + 1>(m, j, wv, ad, U, J, V0, I0);
+}
+
+// A staging wave's window: candidates c0 .. c0 + kWinCand - 1 of the chunk,
+// lane l taking interval j = l % kSub of candidate c0 + l / kSub.  Every lane
+// loads its own interval's closing event (source, decays, times) and its
+// candidate's entering state, then its weight; the 16 lanes of a candidate
+// (one row) walk the sub-block together, lane j taking the no-reset state at
+// its interval's start (after event j - 1) and end, and the interval's
+// crossing key.  Candidates past the pool's capacity take their entering
+// state from rebuild_entry.  open_last: the window holds the sample's last
+// sub-block, and the open interval after its last event is staged too.
+__device__ __forceinline__ void stage_window(ResolveLds& sh, WinBuf& w, const Model& m, int c0, int tot, int seg0,
+                                             int b, int n, int nb, int S, int N, int C_in,
+                                             const float* __restrict__ tt, const int32_t* __restrict__ src,
+                                             const Decay* __restrict__ d, const float* __restrict__ WT,
+                                             const double2* __restrict__ carry, const double2* __restrict__ pool,
+                                             bool open_last, double& kmax)
+{
+    const int lane = (int)threadIdx.x % kWave;
+    const int j = lane % kSub, r = lane / kSub;
+    const int c = c0 + r;
+    const int cc = min(c, tot - 1);
+    const uint32_t cw = sh.cand[cc], slot = sh.slot[cc];
+    const int kq = (seg0 + (int)(cw >> 3)) * kSeg + (int)(cw & 7u) * kSub;
+    const bool ok = c < tot && kq + j < nb;
+    const int k = min(kq + j, nb - 1);
+    const int sc = src[k];
+    const Decay dk = d[k];
+    const double2 ad = make_double2(dk.A, dk.D);
+    const float ta = tt[max(k - 1, 0)], tb = tt[k];
+    double2 u0 = pool[slot != kNoSlot ? slot : 0u];    // the pool holds at least one entry
+    const float wv = WT[(size_t)clamp_src(sc, C_in) * (size_t)N + n];
+    if (__ballot(c < tot && slot == kNoSlot)) {
+        const int nc = min(kWinCand, tot - c0);
+        for (int x = 0; x < nc; ++x) {
+            if (sh.slot[c0 + x] != kNoSlot) continue;
+            const uint32_t cx = sh.cand[c0 + x];
+            const int seg = seg0 + (int)(cx >> 3);
+            const double2 cs = carry[((size_t)b * S + seg) * N + n];
+            const double2 e = rebuild_entry(cs.x, cs.y, seg * kSeg, seg * kSeg + (int)(cx & 7u) * kSub, n, N, C_in,
+                                            src, d, WT);
+            if (x == r) u0 = e;
+        }
+    }
+    double U = u0.x, J = u0.y, V0 = 0.0, I0 = 0.0;
+    walk_from<0>(m, j, wv, ad, U, J, V0, I0);
+    const double V1 = v_of(m, U, J);
+    const double t0 = k > 0 ? (double)ta : 0.0, t1 = (double)tb;
+    double crit, hi, fhi;
+    crossing_data(m, V0, I0, V1, t1 - t0, ad.x, ad.y, crit, hi, fhi);
+    const double key = ok ? crossing_key(m, crit, t0) : __builtin_nan("");
+    w.key[lane] = key;
+    double km = key;
+    w.v0[lane] = V0;
+    w.i0[lane] = I0;
+    w.t0[lane] = k > 0 ? ta : 0.0f;
+    w.t1[lane] = tb;
+    if (open_last && ok && k == nb - 1) {
+        // the open interval after the sample's last event
+        open_interval_data(m, V1, J, m.t_end - t1, crit, hi, fhi);
+        w.key[kOpenIv] = crossing_key(m, crit, t1);
+        w.v0[kOpenIv] = V1;
+        w.i0[kOpenIv] = J;
+        w.t0[kOpenIv] = tb;
+        sh.open_len = m.t_end - t1;
+        km = fmax(km, w.key[kOpenIv]);
+    }
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) km = fmax(km, __shfl_xor(km, off, kWave));
+    if (lane == 0) kmax = km;
+}
 
 // Wave-uniform resolve state of one neuron: the reset deficit of the spikes
 // so far is D(t) = dref e^{-(t - tref)/tm} for t after the latest spike,
 // with tref the start of the interval that spike lies in (the deficit is
-// carried in that interval's frame, so no spike time is needed on the chain).
+// carried in that interval's frame), and K = ln(dref) + tref/tm its key.
 struct Chain {
     int ns;              // spikes so far
-    double dref, tref;
+    double dref, tref, K;
+    double ylast;        // e^{-u/tm} of the latest spike (its offset u in its interval)
+    int lastw, lasti;    // window and interval of the latest spike
     bool capped;
 };
 
 // Spikes [from, to) from the LDS buffer to the outputs (coalesced); the
-// spike times t0 - tm ln y are taken here, 64 at a time, off the per-spike
-// chain.
+// spike times t0 - tm ln y are taken here, 64 at a time, off the chain.
 __device__ __forceinline__ void flush_spikes(ResolveLds& sh, const Model& m, int from, int to, float* __restrict__ st,
                                              float* __restrict__ si, int32_t* __restrict__ sk)
 {
-    const int lane = (int)threadIdx.x;
+    const int lane = (int)threadIdx.x % kWave;
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -896,113 +823,133 @@ __device__ __forceinline__ void flush_spikes(ResolveLds& sh, const Model& m, int
     __builtin_amdgcn_wave_barrier();
 }
 
-// Rounds over one step (see the section comment): lane l takes window
-// interval i0 + l if l < nlanes.  Each lane holds the deficit Dl at its
-// interval's start; an interval crosses iff Dl <= crit.  The spike-time
-// solve of a round runs wave-uniform on the crossing interval's data
-// (broadcast from its lane), so its iterations branch on scalars.
-__device__ __forceinline__ void resolve_step(ResolveLds& sh, const WinBuf& w, const Model& m, int i0, int nlanes,
-                                             Chain& ch, float* __restrict__ st, float* __restrict__ si,
-                                             int32_t* __restrict__ sk)
-{
-    const int lane = (int)threadIdx.x;
-    const int i = lane < nlanes ? i0 + lane : i0;
-    const double crit = w.crit[i];
-    const double t0 = w.t0[i];
-    double Dl = ch.ns > 0 ? ch.dref * exp(-(t0 - ch.tref) * m.inv_tm) : 0.0;
-    bool pend = lane < nlanes && crit >= 0.0 && Dl <= crit;
-    unsigned long long cm = __ballot(pend);
-    if (!cm) return;
-    const double2 s0 = w.s0[i];
-    const double hi = w.hi[i], fhi = w.fhi[i];
-    double ylo = 1.0;
-    for (;;) {
-        const int kl = __ffsll((long long)cm) - 1;
-        const double V0k = rl_double(s0.x, kl), I0k = rl_double(s0.y, kl), Dk = rl_double(Dl, kl);
-        const double t0k = rl_double(t0, kl), hik = rl_double(hi, kl), fhik = rl_double(fhi, kl);
-        const double ylok = rl_double(ylo, kl);
-        const double kI = m.kappa * I0k;
-        // after a spike inside the interval the raised deficit keeps F < 0
-        // on all of [0, u], so the general solver may bracket from the
-        // interval start; the polynomial solver starts from the spike (ylo)
-        const SpikeY sp = solve_spike_y(m, V0k - Dk + kI, kI, 0.0, ylok, V0k - m.th - Dk, hik, fhik - Dk);
-        if (lane == 0) {
-            sh.sp_t0[ch.ns % kWave] = t0k;
-            sh.sp_y[ch.ns % kWave] = sp.y;
-            sh.si[ch.ns % kWave] = (float)(I0k * (sp.E2 * sp.y));
-            sh.sk[ch.ns % kWave] = w.kev[i0 + kl];
-        }
-        // the deficit in interval kl's frame
-        const double Dnew = Dk + m.dth * sp.E1;
-        ++ch.ns;
-        ch.dref = Dnew;
-        ch.tref = t0k;
-        if (ch.ns % kWave == 0) flush_spikes(sh, m, ch.ns - kWave, ch.ns, st, si, sk);
-        if (ch.ns >= m.s_max) { ch.capped = true; return; }
-        // interval kl is tested again with the raised deficit (a second spike
-        // in it); later intervals take the new deficit; earlier ones are done
-        const double Dlater = Dnew * exp(-(t0 - t0k) * m.inv_tm);
-        Dl = lane == kl ? Dnew : Dlater;
-        ylo = lane == kl ? sp.y : ylo;
-        pend = pend && lane >= kl && Dl <= crit;
-        cm = __ballot(pend);
-        if (!cm) return;
-    }
-}
-
-// The staging wave's part of window c0 / kWinCand: its intervals' loads,
-// committed to buffer w, then the rebuild of its sub-blocks without a record.
-__device__ __forceinline__ void stage_window(const ResolveLds& sh, WinBuf& w, const Model& m, int c0, int tot,
-                                             int seg0, int b, int n, int nb, int S, int N, int C_in,
-                                             const float* __restrict__ tt, const int32_t* __restrict__ src,
-                                             const Decay* __restrict__ d, const float* __restrict__ WT,
-                                             const double2* __restrict__ ent, const Record* __restrict__ pool)
+// The spike in window interval i (the earliest crossing the search found):
+// the deficit at the interval start, the spike time (polynomial solve when
+// tau_m / tau_s is an integer plus one, else bracketed Newton on the
+// interval's closed-form maximum), the spike into the LDS buffer, and the
+// raised deficit in the interval's frame.  Returns false at s_max.
+template <int PI>
+__device__ bool spike_at(ResolveLds& sh, const WinBuf& w, const Model& m, int i, int wg, int c0, int seg0, int nb,
+                         Chain& ch, float* __restrict__ st, float* __restrict__ si, int32_t* __restrict__ sk)
 {
     const int lane = (int)threadIdx.x % kWave;
-    const int j = lane % kSub, r = lane / kSub;
-    StageIv nx[kIvPerLane];
-#pragma unroll
-    for (int h = 0; h < kIvPerLane; ++h) nx[h] = stage_load(sh, c0 + h * kStep + r, tot, seg0, nb, j, tt, pool);
-#pragma unroll
-    for (int h = 0; h < kIvPerLane; ++h) {
-        const int c = c0 + h * kStep + r;
-        const int i = h * kWave + lane;
-        const uint32_t cw = sh.cand[min(c, tot - 1)];
-        const int kq0 = (seg0 + (int)(cw >> 3)) * kSeg + (int)(cw & 7u) * kSub;
-        const bool valid = c < tot && kq0 + j < nb;
-        w.crit[i] = valid ? nx[h].crit : -1.0;
-        w.hi[i] = nx[h].hi;
-        w.fhi[i] = nx[h].fhi;
-        w.s0[i] = nx[h].s0;
-        w.t0[i] = kq0 + j > 0 ? (double)nx[h].tp : 0.0;
-        w.kev[i] = kq0 + j;
+    const double V0 = rl_double(w.v0[i], 0), I0 = rl_double(w.i0[i], 0);
+    const double t0 = (double)__builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, w.t0[i])));
+    const double Dk = ch.ns > 0 ? ch.dref * exp(-(t0 - ch.tref) * m.inv_tm) : 0.0;
+    const double ylo = (ch.ns > 0 && ch.lastw == wg && ch.lasti == i) ? ch.ylast : 1.0;
+    const double kI = m.kappa * I0, c0v = V0 - Dk + kI;
+    double y = 0.0, E1 = 0.0, E2 = 0.0;
+    bool ok = false;
+    if constexpr (PI > 0) {
+        ok = root_poly<PI>(m, c0v, kI, ylo, y);
+        if (ok) E2 = ipow<PI>(y);
     }
-    static_assert(kWinCand <= kWave, "one lane per candidate of the window");
-    if (__ballot(sh.slot[min(c0 + lane % kWinCand, tot - 1)] == kNoSlot))
-        rebuild_window(sh, w, m, c0, tot, seg0, b, n, nb, S, N, C_in, tt, src, d, WT, ent);
+    if (ok) {
+        E1 = rcp_refined(y);
+    } else {
+        // the exponential solve brackets the root in [0, hi] with the
+        // interval's closed-form maximum (interval_max)
+        const double L = i == kOpenIv ? sh.open_len : (double)w.t1[i] - t0;
+        double A = 0.0, D = 0.0, V1 = 0.0;
+        if (!isinf(L)) {
+            A = exp(-L * m.inv_tm);
+            D = exp(-L * m.inv_ts);
+            V1 = V0 * A + unit_kernel(m, L, A) * I0;
+        }
+        const IntervalMax im = interval_max(m, V0, I0, V1, L, A, D);
+        root_h(m, c0v, kI, 0.0, V0 - m.th - Dk, im.hi, im.Fhi - Dk, &E1, &E2, nullptr);
+        y = rcp_refined(E1);
+    }
+    int kev = nb;
+    if (i != kOpenIv) {
+        const uint32_t cw = sh.cand[c0 + i / kSub];
+        kev = (seg0 + (int)(cw >> 3)) * kSeg + (int)(cw & 7u) * kSub + i % kSub;
+    }
+    if (lane == 0) {
+        const int q = ch.ns % kWave;
+        sh.sp_t0[q] = t0;
+        sh.sp_y[q] = y;
+        sh.si[q] = (float)(I0 * (E2 * y));
+        sh.sk[q] = kev;
+    }
+    const double Dnew = Dk + m.dth * E1;
+    ch.dref = Dnew;
+    ch.tref = t0;
+    ch.K = log(Dnew) + t0 * m.inv_tm;
+    ch.ylast = y;
+    ch.lastw = wg;
+    ch.lasti = i;
+    ++ch.ns;
+    if (ch.ns % kWave == 0) flush_spikes(sh, m, ch.ns - kWave, ch.ns, st, si, sk);
+    if (ch.ns >= m.s_max) {
+        ch.capped = true;
+        return false;
+    }
+    return true;
+}
+
+// The chain wave's work on one window: its n_iv intervals (one per lane),
+// then (open_last) the open interval; one call site of the spike solve keeps
+// the kernel's code small.
+template <int PI>
+__device__ __forceinline__ void chain_window(ResolveLds& sh, const WinBuf& w, const Model& m, int wg, int c0, int n_iv,
+                                             bool open_last, int seg0, int nb, Chain& ch, float* __restrict__ st,
+                                             float* __restrict__ si, int32_t* __restrict__ sk)
+{
+    const int lane = (int)threadIdx.x % kWave;
+    const int nh = n_iv > 0 ? 1 : 0;
+    const int hend = open_last ? nh + 1 : nh;
+    const double kb = w.key[lane], ko = w.key[kOpenIv];
+    for (int h = 0; h < hend; ++h) {
+        const bool open = h == nh;
+        const double key = open ? ko : kb;
+        int from = 0;
+        for (;;) {
+            const unsigned long long cm = __ballot((open ? lane == 0 : lane >= from) && key >= ch.K);
+            if (cm == 0ull) break;
+            const int kl = __ffsll((long long)cm) - 1;
+            if (!spike_at<PI>(sh, w, m, open ? kOpenIv : h * kWave + kl, wg, c0, seg0, nb, ch, st, si, sk)) return;
+            from = kl;
+        }
+    }
 }
 
 // Both waves of the workgroup call this for the same neuron and pass the
-// same barriers (every loop bound is workgroup-uniform: candidate counts and
-// the capped flag are exchanged through LDS).  Returns the spike count on the
-// chain wave, 0 on the staging wave.
+// same barriers (one per chunk; candidate counts and the stop flag pass
+// through LDS).  Returns the spike count on the chain wave, 0 on the
+// staging wave.
+template <int PI>
 __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restrict__ ev_t,
                               const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
                               const float* __restrict__ WT, int C_in, int N, int E_pad, int S, const Model& m,
-                              const Decay* __restrict__ dec, const double2* __restrict__ ent,
-                              const uint2* __restrict__ mask, uint32_t pool_cap,
-                              const Record* __restrict__ pool, float* __restrict__ out_t, int32_t* __restrict__ out_n,
-                              float* __restrict__ out_i, int32_t* __restrict__ out_k)
+                              const Decay* __restrict__ dec, const double2* __restrict__ carry,
+                              const uint32_t* __restrict__ mask, uint32_t pool_cap, const double2* __restrict__ pool,
+                              float* __restrict__ out_t, int32_t* __restrict__ out_n, float* __restrict__ out_i,
+                              int32_t* __restrict__ out_k, int32_t* __restrict__ status)
 {
     const int lane = (int)threadIdx.x % kWave;
-    const bool chain = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)) == 0;   // wave-uniform
+    const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+    const bool chain = wv == 0;               // wave 0 resolves, waves 1.. stage (wave-uniform)
+    // the chain is the critical path: its instructions go first on its SIMD
+    if (chain) __builtin_amdgcn_s_setprio(3);
+    // a wait that does not end within kSpinLimit polls is an internal error:
+    // it is reported and the neuron is stopped instead of waiting for ever
+    auto give_up = [&]() {
+        if (lane == 0) atomicOr(&status[LIF_ST_FLAGS], LIF_WARN_INTERNAL);
+        lds_store(&sh.stop, 1);
+    };
+    if (threadIdx.x == 0) {
+        sh.consumed = 0;
+        sh.stop = 0;
+        for (int r = 0; r < kRing; ++r) sh.ready[r] = 0;
+    }
     // the first chunk's mask words are loaded together with the event count
     // (words past the sample's segments are dropped below)
-    uint2 mw[kSegPerLane];
+    uint32_t mw[kSegPerLane];
 #pragma unroll
     for (int h = 0; h < kSegPerLane; ++h) {
         const int sj = lane * kSegPerLane + h;
-        mw[h] = chain && sj < S ? mask[((size_t)b * S + sj) * N + n] : make_uint2(0u, 0u);
+        mw[h] = chain && sj < S ? mask[((size_t)b * S + sj) * N + n] : 0u;
     }
     const int nb = __builtin_amdgcn_readfirstlane(clamp_count(ev_n[b], E_max));
     const float* tt = ev_t + (size_t)b * E_max;
@@ -1014,10 +961,11 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
     int32_t* sk = out_k ? out_k + idx * (size_t)m.s_max : nullptr;
     const int Sb = (nb + kSeg - 1) / kSeg;
     const bool has_open = __builtin_amdgcn_readfirstlane(nb > 0 && m.t_end > (double)tt[max(nb - 1, 0)] ? 1 : 0) != 0;
+    __syncthreads();                          // the ring is reset
 
-    Chain ch{0, 0.0, 0.0, false};
+    Chain ch{0, 0.0, 0.0, -INFINITY, 1.0, -1, -1, false};
+    int wbase = 0;                            // windows of earlier chunks
     bool stop = false;
-
     for (int seg0 = 0; seg0 < Sb && !stop; seg0 += kChunkSeg) {
         // ---- this chunk's flagged sub-blocks as a time-ordered list, with
         // slots; lane l takes segments seg0 + kSegPerLane l + h
@@ -1027,23 +975,23 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
 #pragma unroll
             for (int h = 0; h < kSegPerLane; ++h) {
                 const int sj = seg0 + lane * kSegPerLane + h;
-                if (seg0 > 0) mw[h] = sj < Sb ? mask[((size_t)b * S + sj) * N + n] : make_uint2(0u, 0u);
-                mv[h] = sj < Sb ? mw[h].x : 0u;
+                if (seg0 > 0) mw[h] = sj < Sb ? mask[((size_t)b * S + sj) * N + n] : 0u;
+                mv[h] = sj < Sb ? (mw[h] & ((1u << kSubPerSeg) - 1u)) : 0u;
                 pc += __popc(mv[h]);
             }
             int ex = pc;
 #pragma unroll
             for (int off = 1; off < kWave; off <<= 1) {
-                int v = __shfl_up(ex, off, kWave);
+                const int v = __shfl_up(ex, off, kWave);
                 if (lane >= off) ex += v;
             }
             const int ctot = rl_int(ex, kWave - 1);
             ex -= pc;
-            // candidates and their record slots (consecutive per segment)
+            // candidates and their pool slots (consecutive per segment)
             int o = ex;
 #pragma unroll
             for (int h = 0; h < kSegPerLane; ++h) {
-                uint32_t mm = mv[h], rel = mw[h].y;
+                uint32_t mm = mv[h], rel = mw[h] >> kMaskBits;
                 while (mm) {
                     sh.cand[o] = ((uint32_t)(lane * kSegPerLane + h) << 3) | (uint32_t)__builtin_ctz(mm);
                     sh.slot[o] = rel < pool_cap ? (uint32_t)b * pool_cap + rel : kNoSlot;
@@ -1056,58 +1004,74 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
         }
         __syncthreads();
         const int tot = __builtin_amdgcn_readfirstlane(sh.ntot);
+        const int nwin = (tot + kWinCand - 1) / kWinCand;
         if (tot > 0) {
             // the open interval is taken after the window holding the sample's
             // last sub-block, when that sub-block is flagged (it is the last
             // candidate of the last chunk)
             const uint32_t cwl = (uint32_t)__builtin_amdgcn_readfirstlane((int)sh.cand[tot - 1]);
             const bool open_here = has_open && (seg0 + (int)(cwl >> 3)) * kSeg + (int)(cwl & 7u) * kSub + kSub >= nb;
-            const int nwin = (tot + kWinCand - 1) / kWinCand;
             if (!chain) {
-                if (open_here) {
-                    // the open interval's data, from the last candidate's
-                    // record, in slot kOpenIv of both buffers (the windows do
-                    // not overwrite it; a rebuild of the last sub-block does)
-                    const uint32_t slot = (uint32_t)__builtin_amdgcn_readfirstlane((int)sh.slot[tot - 1]);
-                    const int kq0 = (seg0 + (int)(cwl >> 3)) * kSeg + (int)(cwl & 7u) * kSub;
-                    const Record* rec = pool + (slot != kNoSlot ? slot : 0u);
-                    const double oc = rec->crit[kSub], oh = rec->hi[kSub], of = rec->fhi[kSub];
-                    const double2 os = rec->s[min(nb - kq0, kSub)];
-                    const double ot = (double)tt[nb - 1];
-                    if (lane < 2) {
-                        WinBuf& w = sh.win[lane];
-                        w.crit[kOpenIv] = slot != kNoSlot ? oc : -1.0;
-                        w.hi[kOpenIv] = oh;
-                        w.fhi[kOpenIv] = of;
-                        w.s0[kOpenIv] = os;
-                        w.t0[kOpenIv] = ot;
-                        w.kev[kOpenIv] = nb;
+                for (int wi = wv - 1; wi < nwin; wi += kResolveWaves - 1) {
+                    const int wg = wbase + wi, buf = wg % kRing;
+                    bool halt = false;
+                    for (int spin = 0;; ++spin) {
+                        halt = lds_load(&sh.stop) != 0;
+                        if (halt || lds_load(&sh.consumed) >= wg - kRing + 1) break;
+                        if (spin >= kSpinLimit) {
+                            give_up();
+                            halt = true;
+                            break;
+                        }
+                        __builtin_amdgcn_s_sleep(1);
+                    }
+                    if (halt) break;
+                    stage_window(sh, sh.win[buf], m, wi * kWinCand, tot, seg0, b, n, nb, S, N, C_in, tt, src, d, WT,
+                                 carry, pool, open_here && wi == nwin - 1, sh.kmax[buf]);
+                    lds_store(&sh.ready[buf], wg + 1);
+                }
+            } else {
+                for (int wi = 0; wi < nwin;) {
+                    const int wg = wbase + wi, buf = wg % kRing;
+                    bool late = false;
+                    for (int spin = 0; lds_load(&sh.ready[buf]) != wg + 1; ++spin) {
+                        if (spin >= kSpinLimit || lds_load(&sh.stop) != 0) {
+                            if (spin >= kSpinLimit) give_up();
+                            late = true;
+                            break;
+                        }
+                        __builtin_amdgcn_s_sleep(1);
+                    }
+                    if (late) break;
+                    // the run of windows wi, wi + 1, ... staged already (lane q
+                    // looks at window wi + q), and the first of them whose
+                    // largest key reaches the current deficit's key: the
+                    // windows before it hold no crossing and are passed over
+                    const int bq = (wg + lane) % kRing;
+                    const bool rdy = lane < kRing && wi + lane < nwin && lds_load(&sh.ready[bq]) == wg + lane + 1;
+                    const int nr = __builtin_ctzll(~__ballot(rdy));
+                    const unsigned long long hit = __ballot(lane < nr && sh.kmax[bq] >= ch.K);
+                    if (hit == 0ull) {
+                        wi += nr;
+                        lds_store(&sh.consumed, wg + nr);
+                        continue;
+                    }
+                    wi += __builtin_ctzll(hit);
+                    const int wh = wbase + wi, c0 = wi * kWinCand;
+                    chain_window<PI>(sh, sh.win[wh % kRing], m, wh, c0, min(kWinCand, tot - c0) * kSub,
+                                     open_here && wi == nwin - 1, seg0, nb, ch, st, si, sk);
+                    ++wi;
+                    lds_store(&sh.consumed, wh + 1);
+                    if (ch.capped) {
+                        lds_store(&sh.stop, 1);
+                        break;
                     }
                 }
-                stage_window(sh, sh.win[0], m, 0, tot, seg0, b, n, nb, S, N, C_in, tt, src, d, WT, ent, pool);
-            }
-            __syncthreads();
-            for (int wi = 0; wi < nwin; ++wi) {
-                if (!chain) {
-                    if (wi + 1 < nwin)
-                        stage_window(sh, sh.win[(wi + 1) & 1], m, (wi + 1) * kWinCand, tot, seg0, b, n, nb, S, N,
-                                     C_in, tt, src, d, WT, ent, pool);
-                } else {
-                    // the window's steps, then (last window) the open interval as one more
-                    const WinBuf& w = sh.win[wi & 1];
-                    const int c0 = wi * kWinCand;
-                    const int steps = min(kWinSteps, (tot - c0 + kStep - 1) / kStep);
-                    const int nsteps = steps + (wi == nwin - 1 && open_here ? 1 : 0);
-                    for (int g = 0; g < nsteps && !ch.capped; ++g)
-                        resolve_step(sh, w, m, g < steps ? g * kWave : kOpenIv, g < steps ? kWave : 1, ch, st, si, sk);
-                    if (lane == 0) sh.stop[wi & 1] = ch.capped ? 1 : 0;
-                }
-                __syncthreads();              // window wi + 1 staged, window wi free
-                stop = __builtin_amdgcn_readfirstlane(sh.stop[wi & 1]) != 0;
-                if (stop) break;
             }
         }
-        __syncthreads();                      // the list is rewritten by the next chunk
+        wbase += nwin;
+        __syncthreads();                      // both waves are done with the chunk's list
+        stop = __builtin_amdgcn_readfirstlane(lds_load(&sh.stop)) != 0;
     }
     if (!chain) return 0;
     flush_spikes(sh, m, ch.ns - ch.ns % kWave, ch.ns, st, si, sk);
@@ -1115,32 +1079,53 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
     return ch.ns;
 }
 
-// Work-list driven: the per-sample lists of neurons built by k_check are
-// taken as one concatenated list, entry w by workgroup w mod gridDim.x, so
-// that samples with many listed neurons spread over the whole grid.  Status
-// counts are added once per workgroup.
-__global__ __launch_bounds__(kWave * kResolveWaves) void k_resolve(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src,
-                                                   const int32_t* __restrict__ ev_n, int B, int E_max,
-                                                   const float* __restrict__ WT, int C_in, int N, int E_pad, int S,
-                                                   Model m, const Decay* __restrict__ dec,
-                                                   const double2* __restrict__ ent,
-                                                   const uint2* __restrict__ mask, uint32_t pool_cap,
-                                                   const Record* __restrict__ pool,
-                                                   const uint32_t* __restrict__ work, const uint32_t* __restrict__ nwork,
-                                                   float* __restrict__ out_t, int32_t* __restrict__ out_n,
-                                                   float* __restrict__ out_i, int32_t* __restrict__ out_k,
-                                                   int32_t* __restrict__ status)
+// Work-list driven: the per-sample lists of neurons built by the check pass
+// are taken as one concatenated list, entry w by workgroup w mod gridDim.x.
+// Status counts are added once per workgroup.
+template <int PI>
+__global__ __launch_bounds__(kWave * kResolveWaves) void k_resolve(
+    const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int B,
+    int E_max, const float* __restrict__ WT, int C_in, int N, int E_pad, int S, Model m,
+    const Decay* __restrict__ dec, const double2* __restrict__ carry, const uint32_t* __restrict__ mask,
+    uint32_t pool_cap, const double2* __restrict__ pool, const uint32_t* __restrict__ pool_count,
+    const uint32_t* __restrict__ work, const uint32_t* __restrict__ nwork, float* __restrict__ out_t,
+    int32_t* __restrict__ out_n, float* __restrict__ out_i, int32_t* __restrict__ out_k, int32_t* __restrict__ status)
 {
     __shared__ ResolveLds sh;
+    const int lane = (int)threadIdx.x % kWave;
+    if (blockIdx.x == gridDim.x - 1 && threadIdx.x >= blockDim.x - kWave) {
+        // status words fixed once the check pass has run (the only writer of
+        // these words in the call): events consumed, flagged sub-blocks,
+        // sub-blocks past the pool's capacity
+        unsigned long long ev = 0, fl = 0, fb = 0;
+        for (int bb = lane; bb < B; bb += kWave) {
+            ev += (unsigned long long)clamp_count(ev_n[bb], E_max);
+            const uint32_t pc = pool_count[(size_t)bb * kCtr];
+            fl += pc;
+            fb += pc > pool_cap ? pc - pool_cap : 0u;
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+            ev += __shfl_xor(ev, off, kWave);
+            fl += __shfl_xor(fl, off, kWave);
+            fb += __shfl_xor(fb, off, kWave);
+        }
+        if (lane == 0) {
+            auto sat = [](unsigned long long x) { return (int32_t)(x > 0x7fffffffull ? 0x7fffffffull : x); };
+            status[LIF_ST_EVENTS] = sat(ev);
+            status[LIF_ST_CAND_BLOCKS] = sat(fl);
+            status[LIF_ST_WALKED_BLOCKS] = sat(fl);
+            status[LIF_ST_POOL_FALLBACK] = sat(fb);
+        }
+    }
     // spikes and capped neurons of this workgroup's neurons, added to the
-    // status words once at its end (no-return atomics: the wave does not
-    // wait for them)
+    // status words once at its end
     unsigned long long spikes = 0;
     uint32_t capped = 0;
-    const int lane = (int)threadIdx.x % kWave;
-    // Both waves walk the list the same way.  Running sum of the list lengths over groups of 64 samples (one load
-    // per lane, a wave prefix sum): entry w of the concatenated lists belongs
-    // to the first sample whose running sum exceeds w.
+    // Both waves walk the list the same way.  Running sum of the list
+    // lengths over groups of 64 samples (one load per lane, a wave prefix
+    // sum): entry w of the concatenated lists belongs to the first sample
+    // whose running sum exceeds w.
     int b0 = 0;               // first sample of the current group
     uint32_t base = 0;        // entries of the samples before the group
     uint32_t incl = 0;        // running sum up to and including sample b0 + lane
@@ -1167,12 +1152,10 @@ __global__ __launch_bounds__(kWave * kResolveWaves) void k_resolve(const float* 
         const int b = b0 + l;
         if (b0 >= B || l >= kWave || b >= B) break;
         const uint32_t before = l > 0 ? (uint32_t)__shfl((int)incl, l - 1, kWave) : base;
-        // wave-uniform by construction; readfirstlane lets the compiler
-        // treat everything derived from it as uniform (scalar branches)
         const uint32_t bn = (uint32_t)__builtin_amdgcn_readfirstlane((int)work[(size_t)b * N + (w - before)]);
-        const int ns = resolve_neuron(sh, (int)(bn / (uint32_t)N), (int)(bn % (uint32_t)N), ev_t, ev_src, ev_n,
-                                      E_max, WT, C_in, N, E_pad, S, m, dec, ent, mask, pool_cap, pool, out_t, out_n,
-                                      out_i, out_k);
+        const int ns = resolve_neuron<PI>(sh, (int)(bn / (uint32_t)N), (int)(bn % (uint32_t)N), ev_t, ev_src, ev_n,
+                                      E_max, WT, C_in, N, E_pad, S, m, dec, carry, mask, pool_cap, pool, out_t, out_n,
+                                      out_i, out_k, status);
         spikes += (unsigned long long)ns;
         capped += ns >= m.s_max ? 1u : 0u;
     }
@@ -1193,7 +1176,7 @@ __global__ __launch_bounds__(kWave * kResolveWaves) void k_resolve(const float* 
 // spikes and capped neurons from the counts, events from the queue lengths.
 // Each workgroup adds its sums with one atomic per word (one workgroup per
 // kStatusPer counts); the status words start at zero (reset by k_prep).  The
-// parallel path fills the same words inside its record and resolve passes.
+// parallel path fills the same words inside its resolve pass.
 constexpr int kStatusThreads = 1024;
 constexpr int kStatusBatch = 8;
 constexpr int kStatusPer = kStatusThreads * kStatusBatch;
@@ -1353,28 +1336,34 @@ FwdLayout fwd_layout(int B, int E_max, int N, int pool_cap)
     const size_t BS = (size_t)B * L.S;
     L.dec = take((size_t)B * L.E_pad * sizeof(Decay));
     L.segm = take(BS * sizeof(double2));
-    L.agg = take(BS * N * sizeof(double2));
+    // segment aggregates, overwritten in place by the carried states
     L.carry = take(BS * N * sizeof(double2));
-    L.mask = take(BS * N * sizeof(uint2));
-    L.ent = take(BS * kSubPerSeg * N * sizeof(double2));
-    // per sample: record-pool use, work-list length
+    L.mask = take(BS * N * sizeof(uint32_t));
+    // per sample: pool use, work-list length
     L.n_counters = 2 * (size_t)B * kCtr;
     L.counters = take(L.n_counters * sizeof(uint32_t));
     L.listed = take((size_t)B * N * sizeof(uint32_t));
     L.work = take((size_t)B * N * sizeof(uint32_t));
-    // Record pool: one record per flagged (sub-block, neuron), in per-sample
-    // slices sized at a 16th of the dense bound (every sub-block of every
-    // neuron flagged), at least 4096 records (or the dense bound when
-    // smaller).  A full slice only sends the excess sub-blocks through a
-    // slower re-walk.  lif_params.pool_cap >= 0 sets the slice size (tests
-    // of the re-walk path).
+    // Pool of entering states: one 16-byte entry per flagged (sub-block,
+    // neuron), in per-sample slices sized at a quarter of the dense bound
+    // (every sub-block of every neuron flagged), at least 4096 entries (the
+    // dense bound when smaller), and at most 1 GiB in all unless that leaves
+    // fewer than 4096 per sample.  A full slice only sends the excess
+    // sub-blocks through a slower rebuild from the segment's carried state,
+    // with identical results.  lif_params.pool_cap >= 0 sets the slice size.
     const size_t dense = (size_t)L.S * kSubPerSeg * N;
-    size_t cap = dense / 16 > 4096 ? dense / 16 : (dense < 4096 ? dense : 4096);
+    size_t cap = dense / 4 > 4096 ? dense / 4 : (dense < 4096 ? dense : 4096);
+    const size_t budget = (size_t)1 << 30;
+    if (B > 0 && (size_t)B * cap * sizeof(double2) > budget) {
+        const size_t fit = budget / ((size_t)B * sizeof(double2));
+        const size_t floor_ = dense < 4096 ? dense : 4096;
+        cap = fit > floor_ ? fit : floor_;
+    }
     if (pool_cap >= 0) cap = (size_t)pool_cap;
     if (B > 0 && (size_t)B * cap > 0xfffffff0ull) cap = 0xfffffff0ull / (size_t)B;   // slot indices are 32-bit
     L.pool_cap = cap;
     const size_t recs = (size_t)B * cap;
-    L.pool = take((recs > 0 ? recs : 1) * sizeof(Record));   // at least one record (a safe load address)
+    L.pool = take((recs > 0 ? recs : 1) * sizeof(double2));   // at least one entry (a safe load address)
     L.total = off + 256;
     return L;
 }
@@ -1391,16 +1380,17 @@ static int pick_npl(const float* WT, int N)
 
 struct FwdPtrs {
     Decay* dec;
-    double2 *segm, *agg, *carry, *ent;
-    uint2* mask;
+    double2 *segm, *carry;
+    uint32_t* mask;
     uint32_t *counters, *pool_count, *nwork, *listed, *work;
-    Record* pool;
+    double2* pool;
 };
 
 template <int NPL>
 static void launch_walks(const FwdLayout& L, const FwdPtrs& P, const float* ev_t, const int32_t* ev_src,
                          const int32_t* ev_n, int B, int E_max, const float* WT, int C_in, int N, const Model& m,
-                         int32_t* status, bool validate, hipStream_t stream)
+                         int32_t* status, bool validate, int32_t* out_n, float* out_t, float* out_i, int32_t* out_k,
+                         hipStream_t stream)
 {
     const int tiles = (N + kWave * NPL - 1) / (kWave * NPL);
     const size_t items = (size_t)B * L.S * tiles;
@@ -1408,23 +1398,24 @@ static void launch_walks(const FwdLayout& L, const FwdPtrs& P, const float* ev_t
     // the aggregate pass also computes the decays and resets the counters and
     // status words (validation flags are ORed in after it)
     TIMED_LAUNCH("aggregate", k_aggregate<NPL>, dim3(blocks), dim3(kWave * kWalkWaves), 0, stream,
-                 ev_t, ev_src, ev_n, E_max, L.E_pad, WT, C_in, N, tiles, L.S, (int)items, m, P.dec, P.segm, P.agg,
-                 status, P.counters, L.n_counters, P.listed, (size_t)B * N);
+                 ev_t, ev_src, ev_n, E_max, L.E_pad, WT, C_in, N, tiles, L.S, (int)items, m, P.dec, P.segm,
+                 P.carry, status, P.counters, L.n_counters, P.listed, (size_t)B * N, out_n, out_t, out_i, out_k,
+                 (size_t)B * N * (size_t)m.s_max);
     if (validate)
         TIMED_LAUNCH("validate", k_validate, dim3((unsigned)(((size_t)B * E_max + 255) / 256)), dim3(256), 0,
                      stream, ev_t, ev_src, ev_n, B, E_max, C_in, status);
     const int ctiles = (N + kWave - 1) / kWave;
     TIMED_LAUNCH("carry", k_carry, dim3((unsigned)((size_t)B * ctiles)), dim3(kWave * kCarryWaves), 0, stream,
-                 ev_n, B, E_max, N, ctiles, L.S, P.segm, P.agg, P.carry);
+                 ev_n, B, E_max, N, ctiles, L.S, P.segm, P.carry, P.carry);
     // The check pass takes one neuron per lane whatever NPL the aggregate
-    // uses: its screen and record state make wider lanes cost occupancy
+    // uses: its screen and pool state make wider lanes cost occupancy
     // (about 200 VGPRs at four neurons per lane against under 80 at one).
     const int ctl = (N + kWave - 1) / kWave;
     const size_t citems = (size_t)B * L.S * ctl;
     const unsigned cblocks = (unsigned)((citems + kWalkWaves - 1) / kWalkWaves);
     TIMED_LAUNCH("check", k_check, dim3(cblocks), dim3(kWave * kWalkWaves), 0, stream,
-                 ev_t, ev_src, ev_n, E_max, L.E_pad, WT, C_in, N, ctl, L.S, (int)citems, m, P.dec, P.carry, P.ent,
-                 P.mask, P.pool, P.pool_count, (uint32_t)L.pool_cap, P.listed, P.work, P.nwork);
+                 ev_t, ev_src, ev_n, E_max, L.E_pad, WT, C_in, N, ctl, L.S, (int)citems, m, P.dec, P.carry, P.mask,
+                 P.pool, P.pool_count, (uint32_t)L.pool_cap, P.listed, P.work, P.nwork);
 }
 
 int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
@@ -1440,26 +1431,26 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     FwdPtrs P;
     P.dec = (Decay*)(base + L.dec);
     P.segm = (double2*)(base + L.segm);
-    P.agg = (double2*)(base + L.agg);
     P.carry = (double2*)(base + L.carry);
-    P.ent = (double2*)(base + L.ent);
-    P.mask = (uint2*)(base + L.mask);
+    P.mask = (uint32_t*)(base + L.mask);
     P.counters = (uint32_t*)(base + L.counters);
     P.pool_count = P.counters;
     P.nwork = P.counters + (size_t)B * kCtr;
     P.listed = (uint32_t*)(base + L.listed);
     P.work = (uint32_t*)(base + L.work);
-    P.pool = (Record*)(base + L.pool);
+    P.pool = (double2*)(base + L.pool);
 
     const size_t nev = (size_t)B * L.E_pad;
     const size_t nn = (size_t)B * N;
     const size_t items_max = (size_t)B * L.S * ((N + kWave - 1) / kWave);
     if (items_max > 0x7fffffff || nn > 0xffffffffull) return LIF_ERR_SIZE;
+    // mask words hold a per-sample pool offset in 28 bits
+    if ((size_t)L.S * kSubPerSeg * N >= ((size_t)1 << (32 - kMaskBits))) return LIF_ERR_SIZE;
     const size_t n_out = nn * (size_t)p->s_max;
     const bool validate = (p->flags & LIF_VALIDATE) && (size_t)B * E_max;
     if (sequential || items_max == 0) {
         // decays and resets in their own pass (the parallel path folds them
-        // into the aggregate and record passes)
+        // into the aggregate and carry passes)
         size_t work_items = nev > n_out ? nev : n_out;
         size_t blocks = (work_items + 255) / 256;
         if (blocks > 2048) blocks = 2048;
@@ -1482,26 +1473,30 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     }
     if (items_max == 0) return check_launch();
     switch (pick_npl(WT, N)) {
-    case 4: launch_walks<4>(L, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, status, validate, stream); break;
-    case 2: launch_walks<2>(L, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, status, validate, stream); break;
-    default: launch_walks<1>(L, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, status, validate, stream); break;
+    case 4: launch_walks<4>(L, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, status, validate, out_n, out_t, out_i,
+                            out_k, stream); break;
+    case 2: launch_walks<2>(L, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, status, validate, out_n, out_t, out_i,
+                            out_k, stream); break;
+    default: launch_walks<1>(L, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, status, validate, out_n, out_t,
+                             out_i, out_k, stream); break;
     }
-    {
-        // 16 blocks of 4 waves per sample (256 records per round), fewer
-        // when the pool slice is smaller; the blocks loop over the records
-        const size_t per = (L.pool_cap + 15) / 16;
-        const unsigned bx = (unsigned)(per < 1 ? 1 : (per > 16 ? 16 : per));
-        if (B > 0)
-            TIMED_LAUNCH("records", k_records, dim3(bx, (unsigned)B), dim3(256), 0, stream,
-                         ev_t, ev_src, ev_n, E_max, L.E_pad, L.S, WT, C_in, N, m, P.dec, P.ent, P.pool, P.pool_count,
-                         (uint32_t)L.pool_cap, out_n, nn, out_t, out_i, out_k, n_out, B, status);
+    // Four-wave workgroups (a chain wave and three staging waves) over the
+    // concatenated per-sample lists, as many as are resident at once; one
+    // kernel per spike-time solver (the polynomial degree)
+    const unsigned rgrid = (unsigned)(nn < 1024 ? nn : 1024);
+    auto resolve = [&](auto kern) {
+        TIMED_LAUNCH("resolve", kern, dim3(rgrid), dim3(kWave * kResolveWaves), 0, stream,
+                     ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, L.E_pad, L.S, m, P.dec, P.carry, P.mask,
+                     (uint32_t)L.pool_cap, P.pool, P.pool_count, P.work, P.nwork, out_t, out_n, out_i, out_k,
+                     status);
+    };
+    switch (m.p_int) {
+    case 1: resolve(k_resolve<1>); break;
+    case 2: resolve(k_resolve<2>); break;
+    case 3: resolve(k_resolve<3>); break;
+    case 4: resolve(k_resolve<4>); break;
+    default: resolve(k_resolve<0>); break;
     }
-    // Two-wave workgroups (chain and staging waves) over the concatenated
-    // per-sample lists.
-    const unsigned rgrid = (unsigned)(nn < 4096 ? nn : 4096);
-    TIMED_LAUNCH("resolve", k_resolve, dim3(rgrid), dim3(kWave * kResolveWaves), 0, stream,
-                 ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, L.E_pad, L.S, m, P.dec, P.ent, P.mask, (uint32_t)L.pool_cap,
-                 P.pool, P.work, P.nwork, out_t, out_n, out_i, out_k, status);
     return check_launch();
 }
 

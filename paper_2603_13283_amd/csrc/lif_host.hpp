@@ -16,9 +16,9 @@ namespace lif {
 struct FwdLayout {
     int S;                                   // segments per sample
     int E_pad;                               // S * kSeg: row length of the decay table
-    size_t dec, segm, agg, carry, mask, ent, counters, listed, work, pool, total;
+    size_t dec, segm, carry, mask, counters, listed, work, pool, total;
     size_t n_counters;                       // uint32 counters reset by every call
-    size_t pool_cap;                         // record slots per sample
+    size_t pool_cap;                         // pool entries per sample
 };
 FwdLayout fwd_layout(int B, int E_max, int N, int pool_cap);
 

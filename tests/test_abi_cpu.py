@@ -40,7 +40,7 @@ def test_version_and_workspace_sizes(lib):
     big = L.lif_layer_forward_workspace_size(32, 5200, 700, 256, p)
     assert 0 < small < big < 2 ** 31
     assert L.lif_layer_forward_workspace_size(-1, 10, 4, 8, p) == 0
-    # the record pool's slots per sample enter the workspace size
+    # the pool's entries per sample enter the workspace size
     p0, p9 = L.Params(pool_cap=0).c(), L.Params(pool_cap=9000).c()
     assert (L.lif_layer_forward_workspace_size(32, 5200, 700, 256, p0)
             < L.lif_layer_forward_workspace_size(32, 5200, 700, 256, p9))
@@ -127,3 +127,20 @@ def test_weight_matrix_size_limit(lib, fn):
     assert _fwd(fn, p, C=1 << 15, N=(1 << 14) - 1, ws_bytes=0) == L.LIF_ERR_WORKSPACE
     bargs = [F, F, F, 2, 10, F, 1 << 15, 1 << 14, ctypes.byref(p), F, F, F, F, F, F, F, F, 10 ** 9, None]
     assert L.lif_layer_backward(*bargs) == L.LIF_ERR_SIZE
+
+
+@pytest.mark.parametrize("B,E,C,N", [(32, 5383, 700, 256), (128, 11429, 700, 512), (64, 20327, 2312, 1024),
+                                     (16, 101617, 32768, 2048)])
+def test_forward_workspace_formula(lib, B, E, C, N):
+    """The forward workspace is the per-(sample, segment, neuron) carried
+    state and mask word (16 + 4 bytes), the per-event decays (32 bytes), a
+    few per-neuron and per-sample words, and the pool of entering states
+    (16 bytes each, a quarter of the dense bound per sample, at most 1 GiB
+    in all); every workload of the benchmark fits in 2 GB."""
+    p = L.Params().c()
+    ws = L.lif_layer_forward_workspace_size(B, E, C, N, p)
+    S = -(-E // 64)
+    dense = B * S * N * (16 + 4) + B * S * 64 * 32 + B * S * 16 + 2 * B * N * 4 + 2 * B * 32 * 4
+    pool = min(B * max(S * 4 * N // 4, 4096) * 16, 1 << 30)
+    assert dense + pool <= ws <= dense + pool + 16 * 256
+    assert ws <= 2e9

@@ -47,6 +47,7 @@ def check(env, ev, WT, label, s_max=64, both=True, **kw):
         st = out.status.cpu().numpy()
         s = compare_spikes(out.out_t.cpu().numpy(), out.out_n.cpu().numpy(), ref, out.out_i.cpu().numpy(),
                            label=f"{label}{' seq' if seq else ''}", out_k_gpu=out.out_k.cpu().numpy())
+        assert not st[0] & 64, "internal error flagged by the library"
         assert st[2] == out.out_n.cpu().numpy().sum()
         assert st[6] == int(ev.ev_n.sum())
         assert st[1] == int(ref.capped.sum())
@@ -221,13 +222,23 @@ def test_validation_flags(env):
 
 
 def test_record_pool_fallback(env):
-    """With a tiny record pool (lif_params.pool_cap) the overflowing
-    sub-blocks are resolved by the re-walk fallback; results are unchanged."""
+    """With a tiny pool of entering states (lif_params.pool_cap) the
+    overflowing sub-blocks are rebuilt from the segment's carried state; the
+    results match the oracle and are bit-identical to the default pool's."""
+    torch, lif = env
     cfg = W.random_small(9, B=3, C=30, N=130, n_events=600, T=0.4, gain=14.0)
     s = check(env, cfg.events, cfg.layers[0].WT, "pool5", both=False, pool_cap=5)
     assert s["par"]["status"][7] > 0
     s = check(env, cfg.events, cfg.layers[0].WT, "pool0", both=False, pool_cap=0)
     assert s["par"]["status"][7] >= s["par"]["status"][4] > 0   # every walked block fell back
+    ev = cfg.events
+    args = [_dev(torch, a) for a in (ev.ev_t, ev.ev_src, ev.ev_n, cfg.layers[0].WT)]
+    outs = [lif.forward(*args, lif.Params(pool_cap=pc)) for pc in (-1, 5, 0)]
+    torch.cuda.synchronize()
+    for o in outs[1:]:
+        assert torch.equal(o.out_n, outs[0].out_n) and torch.equal(o.out_k, outs[0].out_k)
+        assert torch.equal(o.out_t.view(torch.int32), outs[0].out_t.view(torch.int32))
+        assert torch.equal(o.out_i.view(torch.int32), outs[0].out_i.view(torch.int32))
 
 
 @pytest.mark.parametrize("N", [264, 266, 265])
