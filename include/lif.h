@@ -8,8 +8,9 @@
  *     allocates and owns every buffer (outputs and workspace included).  The
  *     library never allocates device memory, never synchronises the stream
  *     and keeps no state between calls (except the optional kernel timer,
- *     see lif_timer_*).  Every behaviour is set by the arguments (no
- *     environment variables are read).
+ *     see lif_timer_*, and the fixed workspace array of
+ *     lif_layer_forward_noalloc).  Every behaviour is set by the arguments
+ *     (no environment variables are read).
  *   - Work is enqueued on `stream` (a hipStream_t; NULL is the null stream)
  *     and the call returns at once.  Calls on different streams with
  *     distinct buffers may run concurrently.
@@ -151,6 +152,25 @@ int lif_layer_forward_sequential(const float* ev_t, const int32_t* ev_src, const
                                  int E_max, const float* WT, int C_in, int N_out, const lif_params* p,
                                  float* out_t, int32_t* out_n, float* out_i, int32_t* out_k,
                                  int32_t* status, void* ws, size_t ws_bytes, lif_stream_t stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * forward pass of lif_layer_forward, with the same arguments and results
+ * but no ws/ws_bytes.  Its workspace is a fixed array of
+ * lif_layer_forward_noalloc_max_bytes() bytes (64 MiB) in each GPU's
+ * memory, held from the library's load until the process ends; the call
+ * allocates nothing.  The default pool (pool_cap < 0) is cut to what the
+ * array holds (the blocks past it take the rebuild path: results are
+ * unchanged); LIF_ERR_SIZE when the layout without pool entries, or with a
+ * pool_cap the caller set, exceeds the array.  LIF_ERR_HIP when the array's
+ * device address cannot be obtained.  Every call on a GPU uses that GPU's
+ * one array: calls that overlap on one GPU (different streams, or several
+ * host threads) race, and the caller must order them. */
+int lif_layer_forward_noalloc(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
+                              const float* WT, int C_in, int N_out, const lif_params* p,
+                              float* out_t, int32_t* out_n, float* out_i, int32_t* out_k, int32_t* status,
+                              lif_stream_t stream);
+size_t lif_layer_forward_noalloc_max_bytes(void);
 
 /* --------------------------------------------------------------------- */
 /* Backward pass (paper Appendix D.3, Eq. ift_vjp, chained through the     */

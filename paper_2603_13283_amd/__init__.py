@@ -43,7 +43,8 @@ WARN_INTERNAL = 64
 LIF_MERGE_MAX = 16384
 
 EXPORTED = ["lif_version", "lif_layer_forward_workspace_size", "lif_layer_forward",
-            "lif_layer_forward_sequential", "lif_layer_backward_workspace_size", "lif_layer_backward",
+            "lif_layer_forward_sequential", "lif_layer_forward_noalloc", "lif_layer_forward_noalloc_max_bytes",
+            "lif_layer_backward_workspace_size", "lif_layer_backward",
             "lif_merge_workspace_size", "lif_merge_spikes", "lif_first_spike_ce", "lif_timer_enable",
             "lif_timer_read"]
 
@@ -113,6 +114,10 @@ def load(path: Optional[str] = None):
         f = getattr(lib, name)
         f.restype = _I
         f.argtypes = fwd_args
+    lib.lif_layer_forward_noalloc.restype = _I
+    lib.lif_layer_forward_noalloc.argtypes = fwd_args[:14] + [_P]
+    lib.lif_layer_forward_noalloc_max_bytes.restype = _SZ
+    lib.lif_layer_forward_noalloc_max_bytes.argtypes = []
     lib.lif_layer_backward.restype = _I
     lib.lif_layer_backward.argtypes = [_P, _P, _P, _I, _I, _P, _I, _I, _PP, _P, _P, _P, _P, _P, _P, _P, _P, _SZ,
                                        _P]
@@ -157,6 +162,14 @@ def lif_layer_forward(*args) -> int:
 
 def lif_layer_forward_sequential(*args) -> int:
     return load().lif_layer_forward_sequential(*args)
+
+
+def lif_layer_forward_noalloc(*args) -> int:
+    return load().lif_layer_forward_noalloc(*args)
+
+
+def lif_layer_forward_noalloc_max_bytes() -> int:
+    return int(load().lif_layer_forward_noalloc_max_bytes())
 
 
 def lif_layer_backward(*args) -> int:

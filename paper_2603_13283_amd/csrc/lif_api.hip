@@ -60,12 +60,12 @@ Model make_model(const lif_params& p)
 
 int validate_forward_args(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
                           const float* WT, int C_in, int N, const lif_params* p, const float* out_t,
-                          const int32_t* out_n, const int32_t* status, const void* ws)
+                          const int32_t* out_n, const int32_t* status)
 {
     int rc = check_params(p);
     if (rc) return rc;
     if (B < 0 || E_max < 0 || C_in < 1 || N < 1) return LIF_ERR_ARG;
-    if (!WT || !out_t || !out_n || !status || !ws) return LIF_ERR_ARG;
+    if (!WT || !out_t || !out_n || !status) return LIF_ERR_ARG;
     if (B > 0 && !ev_n) return LIF_ERR_ARG;
     if ((size_t)B * (size_t)E_max > 0 && (!ev_t || !ev_src)) return LIF_ERR_ARG;
     if ((size_t)B * (size_t)E_max >= ((size_t)1 << 40)) return LIF_ERR_SIZE;

@@ -1422,8 +1422,9 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
                  const float* WT, int C_in, int N, const lif_params* p, float* out_t, int32_t* out_n,
                  float* out_i, int32_t* out_k, int32_t* status, void* ws, size_t ws_bytes, hipStream_t stream)
 {
-    int rc = validate_forward_args(ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, p, out_t, out_n, status, ws);
+    int rc = validate_forward_args(ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, p, out_t, out_n, status);
     if (rc) return rc;
+    if (!ws) return LIF_ERR_ARG;
     FwdLayout L = fwd_layout(B, E_max, N, p->pool_cap);
     if (ws_bytes < L.total) return LIF_ERR_WORKSPACE;
     Model m = make_model(*p);
@@ -1525,4 +1526,72 @@ extern "C" int lif_layer_forward_sequential(const float* ev_t, const int32_t* ev
 {
     return lif::forward_impl(true, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, p, out_t, out_n, out_i, out_k,
                              status, ws, ws_bytes, (hipStream_t)stream);
+}
+
+// ---------------------------------------------------------------------------
+// Forward pass without a caller workspace: the workspace is a fixed array in
+// device memory, one per GPU, held from the library's load until the process
+// ends.  Its device address is looked up once per device (with that device
+// current) and kept; host code passes only that address to kernels.
+// ---------------------------------------------------------------------------
+#include <mutex>
+
+namespace lif {
+
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxDevices];
+
+// The current device's address of the scratch array.
+static int scratch_address(void** out)
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return LIF_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return LIF_ERR_HIP;
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return LIF_OK;
+}
+
+}  // namespace lif
+
+extern "C" size_t lif_layer_forward_noalloc_max_bytes(void) { return lif::kScratchBytes; }
+
+extern "C" int lif_layer_forward_noalloc(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B,
+                                         int E_max, const float* WT, int C_in, int N_out, const lif_params* p,
+                                         float* out_t, int32_t* out_n, float* out_i, int32_t* out_k,
+                                         int32_t* status, lif_stream_t stream)
+{
+    using namespace lif;
+    int rc = validate_forward_args(ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, p, out_t, out_n, status);
+    if (rc) return rc;
+    lif_params q = *p;
+    // the layout without pool entries must fit; the default pool is cut to
+    // what the array holds (sub-blocks past it take the rebuild path, with
+    // identical results), a pool size the caller set must fit as it is
+    if (fwd_layout(B, E_max, N_out, 0).total > kScratchBytes) return LIF_ERR_SIZE;
+    if (q.pool_cap < 0) {
+        size_t cap = fwd_layout(B, E_max, N_out, -1).pool_cap;
+        if (cap > 0x7fffffff) cap = 0x7fffffff;
+        size_t lo = 0, hi = cap;                      // largest fitting slice size
+        while (lo < hi) {
+            const size_t mid = hi - (hi - lo) / 2;
+            if (fwd_layout(B, E_max, N_out, (int)mid).total <= kScratchBytes) lo = mid;
+            else hi = mid - 1;
+        }
+        q.pool_cap = (int32_t)lo;
+    }
+    if (fwd_layout(B, E_max, N_out, q.pool_cap).total > kScratchBytes) return LIF_ERR_SIZE;
+    void* ws = nullptr;
+    rc = scratch_address(&ws);
+    if (rc) return rc;
+    return forward_impl(false, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, &q, out_t, out_n, out_i, out_k, status,
+                        ws, kScratchBytes, (hipStream_t)stream);
 }

@@ -26,7 +26,7 @@ int check_params(const lif_params* p);
 Model make_model(const lif_params& p);
 int validate_forward_args(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
                           const float* WT, int C_in, int N, const lif_params* p, const float* out_t,
-                          const int32_t* out_n, const int32_t* status, const void* ws);
+                          const int32_t* out_n, const int32_t* status);
 int check_launch();
 
 // Kernel timer (lif_timer_*): a HIP event pair per launch, recorded by the
