@@ -231,6 +231,50 @@ int lif_first_spike_ce(const float* out_t, const int32_t* out_n, int B, int N, i
                        float* loss, float* grad_out_t, lif_stream_t stream);
 
 /* --------------------------------------------------------------------- */
+/* Gradient of a merged queue's event times back to the spikes it was      */
+/* made of (the inverse of lif_merge_spikes' permutation): grad_out_t      */
+/* [B][N][s_max] gets grad_ev_t2[b][j] in slot perm[b][j] for the queue's  */
+/* events j < ev_n2[b], and 0 in every other slot.                         */
+/* --------------------------------------------------------------------- */
+int lif_merge_grad(const float* grad_ev_t2, const int32_t* perm, const int32_t* ev_n2, int B, int E2_max,
+                   int N, int s_max, float* grad_out_t, lif_stream_t stream);
+
+/* --------------------------------------------------------------------- */
+/* The paper's readout and classification loss (Sec. 3.3, Appendix C):    */
+/* one leaky integrator (LI) per class, with the LIF neuron's V/I dynamics */
+/* (Eq. mem_pot) and no spikes, fed by the last hidden layer's merged      */
+/* queue with weights W^T [C_in][N_cls]; its logit is                      */
+/*   z_c = integral over [0, tau_max] of e^{-t/tau_li} V_c(t) dt           */
+/* (Eq. weighted_leaky_integrator_full; tau_li = +INFINITY gives the       */
+/* unweighted integral of Eq. leaky_integrator), and the loss is the mean  */
+/* softmax cross-entropy of beta z (the fixed temperature multiplier of    */
+/* Appendix C).  Events at or after tau_max add nothing.                   */
+/*   logits    float [B][N_cls] z before the temperature; may be NULL      */
+/*   labels    int32 [B] in [0, N_cls) (clamped); NULL: logits only       */
+/*   loss      float [1] device; may be NULL                               */
+/*   grad_WT   float [C_in][N_cls] dL/dW^T, overwritten; may be NULL       */
+/*   grad_ev_t float [B][E_max] dL/d(event time), 0 on padding; may be     */
+/*             NULL (route it to the spikes with lif_merge_grad)           */
+/* Sums run in a fixed order (no floating-point atomics): results are      */
+/* bitwise reproducible.  Limit: N_cls <= LIF_LI_MAX_CLASSES.              */
+/* --------------------------------------------------------------------- */
+#define LIF_LI_MAX_CLASSES 64
+typedef struct lif_li_params {
+    double tau_mem;     /* tau_m of the LI neurons (s), > tau_syn            */
+    double tau_syn;     /* tau_s (s), > 0                                    */
+    double tau_li;      /* weighting time constant (s), > 0; +INFINITY: none */
+    double tau_max;     /* end of the integration window (s), > 0            */
+    double beta;        /* logit temperature multiplier                      */
+} lif_li_params;
+
+size_t lif_li_readout_workspace_size(int B, int E_max, int C_in, int N_cls);
+
+int lif_li_readout(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
+                   const float* WT, int C_in, int N_cls, const lif_li_params* q, const int32_t* labels,
+                   float* logits, float* loss, float* grad_WT, float* grad_ev_t, void* ws, size_t ws_bytes,
+                   lif_stream_t stream);
+
+/* --------------------------------------------------------------------- */
 /* Optional kernel timer (host-side state, off by default).  When enabled, */
 /* every kernel launched by this library is launched with a pair of HIP    */
 /* events that its own dispatch records (hipExtLaunchKernel), so each      */

@@ -45,8 +45,9 @@ LIF_MERGE_MAX = 16384
 EXPORTED = ["lif_version", "lif_layer_forward_workspace_size", "lif_layer_forward",
             "lif_layer_forward_sequential", "lif_layer_forward_noalloc", "lif_layer_forward_noalloc_max_bytes",
             "lif_layer_backward_workspace_size", "lif_layer_backward",
-            "lif_merge_workspace_size", "lif_merge_spikes", "lif_first_spike_ce", "lif_timer_enable",
-            "lif_timer_read"]
+            "lif_merge_workspace_size", "lif_merge_spikes", "lif_first_spike_ce", "lif_merge_grad",
+            "lif_li_readout_workspace_size", "lif_li_readout", "lif_timer_enable", "lif_timer_read"]
+LIF_LI_MAX_CLASSES = 64
 
 
 class LibraryMissing(RuntimeError):
@@ -85,6 +86,26 @@ class Params:
         flags = (LIF_VALIDATE if self.validate else 0) | (LIF_ROOT_GENERAL if self.root_general else 0)
         return lif_params(self.tau_mem, self.tau_syn, self.v_th, self.v_reset, self.t_end, int(self.s_max),
                           flags, self.solver_reg, int(self.pool_cap), 0)
+
+
+class lif_li_params(ctypes.Structure):
+    _fields_ = [("tau_mem", ctypes.c_double), ("tau_syn", ctypes.c_double), ("tau_li", ctypes.c_double),
+                ("tau_max", ctypes.c_double), ("beta", ctypes.c_double)]
+
+
+@dataclass
+class LiParams:
+    """Readout constants: LI time constants, the weighting constant tau_li
+    (inf: unweighted), the integration window tau_max and the logit
+    temperature multiplier beta."""
+    tau_mem: float = 0.02
+    tau_syn: float = 0.005
+    tau_li: float = 0.5
+    tau_max: float = 1.0
+    beta: float = 0.05
+
+    def c(self) -> lif_li_params:
+        return lif_li_params(self.tau_mem, self.tau_syn, self.tau_li, self.tau_max, self.beta)
 
 
 _lib = None
@@ -127,6 +148,13 @@ def load(path: Optional[str] = None):
     lib.lif_merge_spikes.argtypes = [_P, _P, _I, _I, _I, _P, _P, _P, _P, _I, _P, _P, _SZ, _P]
     lib.lif_first_spike_ce.restype = _I
     lib.lif_first_spike_ce.argtypes = [_P, _P, _I, _I, _I, _P, ctypes.c_double, ctypes.c_double, _P, _P, _P]
+    lib.lif_merge_grad.restype = _I
+    lib.lif_merge_grad.argtypes = [_P, _P, _P, _I, _I, _I, _I, _P, _P]
+    lib.lif_li_readout_workspace_size.restype = _SZ
+    lib.lif_li_readout_workspace_size.argtypes = [_I, _I, _I, _I]
+    lib.lif_li_readout.restype = _I
+    lib.lif_li_readout.argtypes = [_P, _P, _P, _I, _I, _P, _I, _I, ctypes.POINTER(lif_li_params), _P, _P, _P, _P,
+                                   _P, _P, _SZ, _P]
     lib.lif_timer_enable.restype = None
     lib.lif_timer_enable.argtypes = [_I]
     lib.lif_timer_read.restype = _I
@@ -178,6 +206,18 @@ def lif_layer_backward(*args) -> int:
 
 def lif_merge_spikes(*args) -> int:
     return load().lif_merge_spikes(*args)
+
+
+def lif_merge_grad(*args) -> int:
+    return load().lif_merge_grad(*args)
+
+
+def lif_li_readout_workspace_size(B, E_max, C_in, N_cls) -> int:
+    return int(load().lif_li_readout_workspace_size(B, E_max, C_in, N_cls))
+
+
+def lif_li_readout(*args) -> int:
+    return load().lif_li_readout(*args)
 
 
 def lif_first_spike_ce(*args) -> int:
@@ -316,3 +356,38 @@ def first_spike_ce(fwd: ForwardOut, labels, tau0: float, t_silent: float, stream
                             _ptr(loss), _ptr(g), _stream(stream))
     _check("lif_first_spike_ce", rc)
     return loss, g
+
+
+def merge_grad(grad_ev_t2, perm, ev_n2, N: int, s_max: int, stream=None):
+    """Run lif_merge_grad; returns grad_out_t [B, N, s_max]."""
+    torch = _torch()
+    B, E2 = grad_ev_t2.shape
+    g = torch.empty((B, N, s_max), dtype=torch.float32, device=grad_ev_t2.device)
+    rc = lif_merge_grad(_ptr(grad_ev_t2), _ptr(perm), _ptr(ev_n2), B, E2, N, s_max, _ptr(g), _stream(stream))
+    _check("lif_merge_grad", rc)
+    return g
+
+
+def li_readout(ev_t, ev_src, ev_n, WT, q: LiParams = LiParams(), labels=None, grads: bool = True, stream=None,
+               ws=None):
+    """Run lif_li_readout; returns (logits [B, N_cls], loss [1] or None,
+    grad_WT or None, grad_ev_t or None)."""
+    torch = _torch()
+    B, E, C, K = _dev_inputs(ev_t, ev_src, ev_n, WT)
+    dev = ev_t.device
+    logits = torch.empty((B, K), dtype=torch.float32, device=dev)
+    loss = gW = gT = lab = None
+    if labels is not None:
+        lab = labels.to(device=dev, dtype=torch.int32).contiguous()
+        loss = torch.empty(1, dtype=torch.float32, device=dev)
+        if grads:
+            gW = torch.empty((C, K), dtype=torch.float32, device=dev)
+            gT = torch.empty((B, E), dtype=torch.float32, device=dev)
+    need = lif_li_readout_workspace_size(B, E, C, K)
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    qc = q.c()
+    rc = lif_li_readout(_ptr(ev_t), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(WT), C, K, ctypes.byref(qc), _ptr(lab),
+                        _ptr(logits), _ptr(loss), _ptr(gW), _ptr(gT), _ptr(ws), ws.numel(), _stream(stream))
+    _check("lif_li_readout", rc)
+    return logits, loss, gW, gT

@@ -144,3 +144,30 @@ def test_forward_workspace_formula(lib, B, E, C, N):
     pool = min(B * max(S * 4 * N // 4, 4096) * 16, 1 << 30)
     assert dense + pool <= ws <= dense + pool + 16 * 256
     assert ws <= 2e9
+
+
+def test_readout_and_merge_grad_argument_errors(lib):
+    q = L.LiParams().c()
+    ws = 10 ** 9
+    # ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_cls, q, labels, logits, loss, grad_WT, grad_ev_t, ws, ws_bytes, stream
+    args = [F, F, F, 2, 10, F, 4, 8, ctypes.byref(q), F, F, F, F, F, F, ws, None]
+
+    def call(**kw):
+        a = list(args)
+        for i, v in kw.items():
+            a[int(i[1:])] = v
+        return L.lif_li_readout(*a)
+    assert call(a7=L.LIF_LI_MAX_CLASSES + 1) == L.LIF_ERR_SIZE
+    assert call(a7=0) == L.LIF_ERR_ARG
+    assert call(a9=None) == L.LIF_ERR_ARG              # a loss or gradient without labels
+    assert call(a14=None) == L.LIF_ERR_ARG             # no workspace
+    assert call(a15=10) == L.LIF_ERR_WORKSPACE
+    bad = L.LiParams(tau_mem=0.005, tau_syn=0.005).c()
+    assert call(a8=ctypes.byref(bad)) == L.LIF_ERR_TAU
+    bad = L.LiParams(tau_li=0.0).c()
+    assert call(a8=ctypes.byref(bad)) == L.LIF_ERR_TAU
+    bad = L.LiParams(tau_max=math.inf).c()
+    assert call(a8=ctypes.byref(bad)) == L.LIF_ERR_ARG
+    assert L.lif_li_readout_workspace_size(2, 10, 4, 8) > 0
+    assert L.lif_merge_grad(F, F, F, 2, 10, 0, 4, F, None) == L.LIF_ERR_ARG
+    assert L.lif_merge_grad(F, F, F, 2, 10, 8, 4, None, None) == L.LIF_ERR_ARG
