@@ -170,6 +170,40 @@ def run_workload(torch, lif, d, name, ev, WT, P, steps, warmup, seq_steps, backw
     return r
 
 
+def train_step(torch, lif, d, c3, steps, warmup):
+    """The paper's training step (two LIF layers, merges, weighted LI readout
+    with temperature cross-entropy, backward through both merges, Adam) at
+    config 3's shape with a 512 -> 20 readout, with the parallel layers and
+    with the sequential baseline in their place."""
+    from paper_2603_13283_amd.train import AdamParams, TwoLayerNet
+    ev = c3.events
+    rng = np.random.default_rng(11)
+    Wo = (rng.normal(0, 1, (512, 20)) * 4.0 / np.sqrt(512)).astype(np.float32)
+    labels = d(rng.integers(0, 20, ev.B).astype(np.int32))
+    inp = [d(ev.ev_t), d(ev.ev_src), d(ev.ev_n)]
+    out = {"workload": "700->512->512 LIF + 512->20 weighted LI readout, B=128, ~10k events; forward, "
+                       "cross-entropy, backward through both merges, Adam on all three weight matrices"}
+    for name, seq in (("parallel", False), ("sequential", True)):
+        net = TwoLayerNet(d(c3.layers[0].WT), d(c3.layers[1].WT), d(Wo), B=ev.B, E_max=ev.E_max,
+                          P1=lif.Params(s_max=128), P2=lif.Params(s_max=128),
+                          q=lif.LiParams(tau_li=0.5, tau_max=1.0, beta=0.05), adam=AdamParams(lr=1e-3))
+        r = net.step(*inp, labels, sequential=seq)
+        torch.cuda.synchronize()
+        ms, ev_ms = time_steps(torch, lambda: net.step(*inp, labels, sequential=seq), steps if not seq else 3,
+                               warmup if not seq else 1)
+        out[f"{name}_ms"] = ms
+        out[f"{name}_event_ms"] = stats_ms(ev_ms)
+        if not seq:
+            out["spikes_layer1"] = int(r.fwd1.out_n.sum().item())
+            out["spikes_layer2"] = int(r.fwd2.out_n.sum().item())
+            out["loss_first_step"] = float(r.loss.item())
+        del net, r
+    out["speedup_vs_sequential"] = out["sequential_ms"] / out["parallel_ms"]
+    log(f"[bench] training step: {out['parallel_ms']:.2f} ms parallel, {out['sequential_ms']:.2f} ms with the "
+        f"sequential layers ({out['speedup_vs_sequential']:.1f}x)")
+    return out
+
+
 def cpu_oracle(ev, WT, nthreads, seconds, n_samples, n_neurons):
     """The float64 oracle on a bounded sample of a workload (the first
     n_samples samples and n_neurons neurons), repeated for about `seconds`;
@@ -322,6 +356,7 @@ def main():
         W1d = (c5.layers[0].WT * 4.0).astype(np.float32)    # gain 16: the driven variant of the parity tests
         extras["c5_hidden_driven"] = run_workload(torch, lif, d, "32768->2048, B=16, ~100k events, gain 16",
                                                   c5.events, W1d, lif.Params(s_max=64), st, wu, 1, backward=True)
+        extras["train_step_c3"] = train_step(torch, lif, d, c3, st, wu)
         del c3, c4, c5, W1d
 
     # ---- float64 CPU oracle on the host cores (bounded samples)

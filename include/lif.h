@@ -275,6 +275,20 @@ int lif_li_readout(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n
                    lif_stream_t stream);
 
 /* --------------------------------------------------------------------- */
+/* Adam step (the optimiser the paper trains with, App. E): for each of    */
+/* the n parameters, m1 = b1 m1 + (1 - b1) g, m2 = b2 m2 + (1 - b2) g^2,   */
+/* p -= lr (m1 / (1 - b1^step)) / (sqrt(m2 / (1 - b2^step)) + eps), in     */
+/* float64, stored in float32.  step >= 1 counts the updates so far.       */
+/* param, m1, m2 are updated in place; the moments start at 0.            */
+/* --------------------------------------------------------------------- */
+typedef struct lif_adam_params {
+    double lr, beta1, beta2, eps;
+} lif_adam_params;
+
+int lif_adam_step(float* param, const float* grad, float* m1, float* m2, size_t n, const lif_adam_params* a,
+                  int step, lif_stream_t stream);
+
+/* --------------------------------------------------------------------- */
 /* Optional kernel timer (host-side state, off by default).  When enabled, */
 /* every kernel launched by this library is launched with a pair of HIP    */
 /* events that its own dispatch records (hipExtLaunchKernel), so each      */

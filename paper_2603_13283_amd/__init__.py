@@ -46,7 +46,8 @@ EXPORTED = ["lif_version", "lif_layer_forward_workspace_size", "lif_layer_forwar
             "lif_layer_forward_sequential", "lif_layer_forward_noalloc", "lif_layer_forward_noalloc_max_bytes",
             "lif_layer_backward_workspace_size", "lif_layer_backward",
             "lif_merge_workspace_size", "lif_merge_spikes", "lif_first_spike_ce", "lif_merge_grad",
-            "lif_li_readout_workspace_size", "lif_li_readout", "lif_timer_enable", "lif_timer_read"]
+            "lif_li_readout_workspace_size", "lif_li_readout", "lif_adam_step", "lif_timer_enable",
+            "lif_timer_read"]
 LIF_LI_MAX_CLASSES = 64
 
 
@@ -108,6 +109,11 @@ class LiParams:
         return lif_li_params(self.tau_mem, self.tau_syn, self.tau_li, self.tau_max, self.beta)
 
 
+class lif_adam_params(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_double), ("beta1", ctypes.c_double), ("beta2", ctypes.c_double),
+                ("eps", ctypes.c_double)]
+
+
 _lib = None
 _P = ctypes.c_void_p
 _I = ctypes.c_int
@@ -155,6 +161,8 @@ def load(path: Optional[str] = None):
     lib.lif_li_readout.restype = _I
     lib.lif_li_readout.argtypes = [_P, _P, _P, _I, _I, _P, _I, _I, ctypes.POINTER(lif_li_params), _P, _P, _P, _P,
                                    _P, _P, _SZ, _P]
+    lib.lif_adam_step.restype = _I
+    lib.lif_adam_step.argtypes = [_P, _P, _P, _P, _SZ, ctypes.POINTER(lif_adam_params), _I, _P]
     lib.lif_timer_enable.restype = None
     lib.lif_timer_enable.argtypes = [_I]
     lib.lif_timer_read.restype = _I
@@ -218,6 +226,10 @@ def lif_li_readout_workspace_size(B, E_max, C_in, N_cls) -> int:
 
 def lif_li_readout(*args) -> int:
     return load().lif_li_readout(*args)
+
+
+def lif_adam_step(*args) -> int:
+    return load().lif_adam_step(*args)
 
 
 def lif_first_spike_ce(*args) -> int:
@@ -391,3 +403,15 @@ def li_readout(ev_t, ev_src, ev_n, WT, q: LiParams = LiParams(), labels=None, gr
                         _ptr(logits), _ptr(loss), _ptr(gW), _ptr(gT), _ptr(ws), ws.numel(), _stream(stream))
     _check("lif_li_readout", rc)
     return logits, loss, gW, gT
+
+
+def adam_step(param, grad, m1, m2, step: int, lr: float = 1e-3, beta1: float = 0.9, beta2: float = 0.999,
+              eps: float = 1e-8, stream=None):
+    """Run lif_adam_step on contiguous float32 tensors of one shape (in place)."""
+    for t in (param, grad, m1, m2):
+        if not t.is_contiguous() or t.numel() != param.numel():
+            raise ValueError("adam_step needs contiguous tensors of one size")
+    a = lif_adam_params(lr, beta1, beta2, eps)
+    rc = lif_adam_step(_ptr(param), _ptr(grad), _ptr(m1), _ptr(m2), param.numel(), ctypes.byref(a), int(step),
+                       _stream(stream))
+    _check("lif_adam_step", rc)
