@@ -69,6 +69,11 @@ def _fwd_bwd(env, ev, WT, seed, s_max=64, reg=0.01, label="", **kw):
     rT, fT = compare_grad_e2e(gT.cpu().numpy()[okB], oT[okB], qT[okB], label=f"{label} grad_ev_t")
     hW, hT = lif.backward(*d, _dev_fwd(torch, lif, r32), _dev(torch, g), P)
     torch.cuda.synchronize()
+    # bitwise reproducible: the same call again gives the same bits
+    gW2, gT2 = lif.backward(*d, out, _dev(torch, g), P)
+    torch.cuda.synchronize()
+    assert torch.equal(gW.view(torch.int32), gW2.view(torch.int32))
+    assert torch.equal(gT.view(torch.int32), gT2.view(torch.int32))
     sW = compare_grad(hW.cpu().numpy(), qW, label=f"{label} grad_WT (same inputs)")
     sT = compare_grad(hT.cpu().numpy(), qT, label=f"{label} grad_ev_t (same inputs)")
     print(f"[case] {label} spikes={int(ref.out_n.sum())} flagged={st['flagged']} excused={st['excused']} "
@@ -193,3 +198,22 @@ def test_first_spike_ce(env):
     gg = g.cpu().numpy()
     assert np.allclose(gg[:, :, 0], rg, rtol=1e-5, atol=1e-6)
     assert np.all(gg[:, :, 1:] == 0)
+
+
+def test_backward_deterministic_full_size(env):
+    """Config 2 at its full batch: three backward calls give identical bits
+    (dL/dW is summed in 64-bit fixed point, dL/dt per tile in order)."""
+    torch, lif = env
+    cfg = W.config2()
+    P = lif.Params(v_th=0.5)
+    d = [_dev(torch, a) for a in (cfg.events.ev_t, cfg.events.ev_src, cfg.events.ev_n, cfg.layers[0].WT)]
+    out = lif.forward(*d, P)
+    rng = np.random.default_rng(27)
+    valid = np.isfinite(out.out_t.cpu().numpy())
+    g = _dev(torch, (rng.standard_normal(valid.shape) * valid).astype(np.float32))
+    runs = [lif.backward(*d, out, g, P) for _ in range(3)]
+    torch.cuda.synchronize()
+    assert int(out.out_n.sum()) > 1000
+    for gW, gT in runs[1:]:
+        assert torch.equal(gW.view(torch.int32), runs[0][0].view(torch.int32))
+        assert torch.equal(gT.view(torch.int32), runs[0][1].view(torch.int32))
