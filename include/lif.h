@@ -275,6 +275,31 @@ int lif_li_readout(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n
                    lif_stream_t stream);
 
 /* --------------------------------------------------------------------- */
+/* Spike-count regularisers (Appendix E.1, Eq. loss) of a layer, from its  */
+/* inputs and the forward's spikes.  For each (sample b, neuron i) and     */
+/* each input interval j (between events j - 1 and j, t_{-1} = 0, and the  */
+/* open interval after the last event up to t_end), V_max is the largest  */
+/* V of the interval's trajectory from its true start state (the resets of */
+/* earlier intervals applied, none inside it); interval j is spiking when  */
+/* a spike has out_k = j, else silent.                                     */
+/*   under[b][i] = mean over silent intervals of max(V_th - V_max, 0)       */
+/*   over[b][i]  = mean over spiking intervals of max(V_max - V_th, 0)      */
+/* (0 for an empty set), and with c = spike counts (out_n), the gates      */
+/* g_u = max(1 - mean_b c / c_target, 0), g_o = max(mean_b c / c_target - 1, 0): */
+/*   loss[0] = L_reg  = mean_i (g_u mean_b under + g_o mean_b over)         */
+/*   loss[1] = L_over = (1/N) sum_i sum_b max(c / c_target - 1, 0) over     */
+/* The caller weights them (lambda_reg, lambda_over-reg of Eq. loss).      */
+/*   under, over  float [B][N_out]; may be NULL                            */
+/* Sums run in a fixed order: results are bitwise reproducible.            */
+/* --------------------------------------------------------------------- */
+size_t lif_spike_count_reg_workspace_size(int B, int E_max, int C_in, int N_out);
+
+int lif_spike_count_reg(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
+                        const float* WT, int C_in, int N_out, const lif_params* p, const float* out_t,
+                        const int32_t* out_n, const int32_t* out_k, double c_target, float* loss, float* under,
+                        float* over, void* ws, size_t ws_bytes, lif_stream_t stream);
+
+/* --------------------------------------------------------------------- */
 /* Adam step (the optimiser the paper trains with, App. E): for each of    */
 /* the n parameters, m1 = b1 m1 + (1 - b1) g, m2 = b2 m2 + (1 - b2) g^2,   */
 /* p -= lr (m1 / (1 - b1^step)) / (sqrt(m2 / (1 - b2^step)) + eps), in     */

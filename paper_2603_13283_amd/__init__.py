@@ -46,8 +46,8 @@ EXPORTED = ["lif_version", "lif_layer_forward_workspace_size", "lif_layer_forwar
             "lif_layer_forward_sequential", "lif_layer_forward_noalloc", "lif_layer_forward_noalloc_max_bytes",
             "lif_layer_backward_workspace_size", "lif_layer_backward",
             "lif_merge_workspace_size", "lif_merge_spikes", "lif_first_spike_ce", "lif_merge_grad",
-            "lif_li_readout_workspace_size", "lif_li_readout", "lif_adam_step", "lif_timer_enable",
-            "lif_timer_read"]
+            "lif_li_readout_workspace_size", "lif_li_readout", "lif_adam_step", "lif_spike_count_reg_workspace_size",
+            "lif_spike_count_reg", "lif_timer_enable", "lif_timer_read"]
 LIF_LI_MAX_CLASSES = 64
 
 
@@ -161,6 +161,11 @@ def load(path: Optional[str] = None):
     lib.lif_li_readout.restype = _I
     lib.lif_li_readout.argtypes = [_P, _P, _P, _I, _I, _P, _I, _I, ctypes.POINTER(lif_li_params), _P, _P, _P, _P,
                                    _P, _P, _SZ, _P]
+    lib.lif_spike_count_reg_workspace_size.restype = _SZ
+    lib.lif_spike_count_reg_workspace_size.argtypes = [_I, _I, _I, _I]
+    lib.lif_spike_count_reg.restype = _I
+    lib.lif_spike_count_reg.argtypes = [_P, _P, _P, _I, _I, _P, _I, _I, _PP, _P, _P, _P, ctypes.c_double, _P, _P,
+                                        _P, _P, _SZ, _P]
     lib.lif_adam_step.restype = _I
     lib.lif_adam_step.argtypes = [_P, _P, _P, _P, _SZ, ctypes.POINTER(lif_adam_params), _I, _P]
     lib.lif_timer_enable.restype = None
@@ -226,6 +231,14 @@ def lif_li_readout_workspace_size(B, E_max, C_in, N_cls) -> int:
 
 def lif_li_readout(*args) -> int:
     return load().lif_li_readout(*args)
+
+
+def lif_spike_count_reg_workspace_size(B, E_max, C_in, N_out) -> int:
+    return int(load().lif_spike_count_reg_workspace_size(B, E_max, C_in, N_out))
+
+
+def lif_spike_count_reg(*args) -> int:
+    return load().lif_spike_count_reg(*args)
 
 
 def lif_adam_step(*args) -> int:
@@ -415,3 +428,24 @@ def adam_step(param, grad, m1, m2, step: int, lr: float = 1e-3, beta1: float = 0
     rc = lif_adam_step(_ptr(param), _ptr(grad), _ptr(m1), _ptr(m2), param.numel(), ctypes.byref(a), int(step),
                        _stream(stream))
     _check("lif_adam_step", rc)
+
+
+def spike_count_reg(ev_t, ev_src, ev_n, WT, fwd: ForwardOut, c_target: float, params: Params = Params(),
+                    stream=None, ws=None):
+    """Run lif_spike_count_reg; returns (loss [2] = (L_reg, L_over), under
+    [B, N], over [B, N])."""
+    torch = _torch()
+    B, E, C, N = _dev_inputs(ev_t, ev_src, ev_n, WT)
+    dev = ev_t.device
+    loss = torch.empty(2, dtype=torch.float32, device=dev)
+    under = torch.empty((B, N), dtype=torch.float32, device=dev)
+    over = torch.empty((B, N), dtype=torch.float32, device=dev)
+    need = lif_spike_count_reg_workspace_size(B, E, C, N)
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    p = params.c()
+    rc = lif_spike_count_reg(_ptr(ev_t), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(WT), C, N, ctypes.byref(p),
+                             _ptr(fwd.out_t), _ptr(fwd.out_n), _ptr(fwd.out_k), float(c_target), _ptr(loss),
+                             _ptr(under), _ptr(over), _ptr(ws), ws.numel(), _stream(stream))
+    _check("lif_spike_count_reg", rc)
+    return loss, under, over

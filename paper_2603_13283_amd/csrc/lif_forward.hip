@@ -221,13 +221,14 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_aggregate(
         for (size_t i = gt; i < n_counters; i += gs) counters[i] = 0u;
         for (size_t i = gt; i < nn; i += gs) {
             listed[i] = 0u;
-            out_n[i] = 0;
+            if (out_n) out_n[i] = 0;
         }
-        for (size_t i = gt; i < n_out; i += gs) {
-            out_t[i] = INFINITY;
-            if (out_i) out_i[i] = 0.0f;
-            if (out_k) out_k[i] = 0;
-        }
+        if (out_t)
+            for (size_t i = gt; i < n_out; i += gs) {
+                out_t[i] = INFINITY;
+                if (out_i) out_i[i] = 0.0f;
+                if (out_k) out_k[i] = 0;
+            }
     }
     __shared__ double2 s_ad[kWalkWaves][kSeg];
     WalkCoords c;
@@ -1390,7 +1391,7 @@ template <int NPL>
 static void launch_walks(const FwdLayout& L, const FwdPtrs& P, const float* ev_t, const int32_t* ev_src,
                          const int32_t* ev_n, int B, int E_max, const float* WT, int C_in, int N, const Model& m,
                          int32_t* status, bool validate, int32_t* out_n, float* out_t, float* out_i, int32_t* out_k,
-                         hipStream_t stream)
+                         hipStream_t stream, bool check = true)
 {
     const int tiles = (N + kWave * NPL - 1) / (kWave * NPL);
     const size_t items = (size_t)B * L.S * tiles;
@@ -1400,13 +1401,14 @@ static void launch_walks(const FwdLayout& L, const FwdPtrs& P, const float* ev_t
     TIMED_LAUNCH("aggregate", k_aggregate<NPL>, dim3(blocks), dim3(kWave * kWalkWaves), 0, stream,
                  ev_t, ev_src, ev_n, E_max, L.E_pad, WT, C_in, N, tiles, L.S, (int)items, m, P.dec, P.segm,
                  P.carry, status, P.counters, L.n_counters, P.listed, (size_t)B * N, out_n, out_t, out_i, out_k,
-                 (size_t)B * N * (size_t)m.s_max);
+                 out_t ? (size_t)B * N * (size_t)m.s_max : (size_t)0);
     if (validate)
         TIMED_LAUNCH("validate", k_validate, dim3((unsigned)(((size_t)B * E_max + 255) / 256)), dim3(256), 0,
                      stream, ev_t, ev_src, ev_n, B, E_max, C_in, status);
     const int ctiles = (N + kWave - 1) / kWave;
     TIMED_LAUNCH("carry", k_carry, dim3((unsigned)((size_t)B * ctiles)), dim3(kWave * kCarryWaves), 0, stream,
                  ev_n, B, E_max, N, ctiles, L.S, P.segm, P.carry, P.carry);
+    if (!check) return;
     // The check pass takes one neuron per lane whatever NPL the aggregate
     // uses: its screen and pool state make wider lanes cost occupancy
     // (about 200 VGPRs at four neurons per lane against under 80 at one).
@@ -1526,6 +1528,292 @@ extern "C" int lif_layer_forward_sequential(const float* ev_t, const int32_t* ev
 {
     return lif::forward_impl(true, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, p, out_t, out_n, out_i, out_k,
                              status, ws, ws_bytes, (hipStream_t)stream);
+}
+
+namespace lif {
+
+// ---------------------------------------------------------------------------
+// Spike-count regularisers (App. E.1, Eq. loss): for every (sample, neuron)
+// and every input interval j (between events j - 1 and j, and the open one
+// after the last event up to t_end), the largest V of the interval's
+// trajectory from its true start state (resets of earlier intervals
+// applied, none inside it), split into the intervals that hold a spike
+// (out_k = j) and the silent ones.  The no-reset state comes from the
+// forward's segment scan (k_aggregate, k_carry); the resets enter as the
+// decaying deficit (V_th - V_reset) e^{-(t - t_s)/tm} of each earlier spike.
+// ---------------------------------------------------------------------------
+
+// Largest V over [0, L] of the no-reset trajectory from (V0, I0): the start,
+// the end (L finite) and the stationary point of Eq. t_vmax when it lies
+// inside.
+__device__ __forceinline__ double reg_vmax(const Model& m, double V0, double I0, double L, double A, double Dd)
+{
+    double best = V0;
+    if (!isinf(L)) best = fmax(best, V0 * A + m.kappa * I0 * (A - Dd));
+    const double a = V0 + m.kappa * I0;
+    if (I0 > 0.0 && a > 0.0) {
+        const double ratio = m.kappa * I0 * m.tm / (a * m.ts);
+        if (ratio > 1.0) {
+            const double u = log(ratio) * m.c_tv;
+            if (u > 0.0 && u < L) {
+                const double em = exp(-u * m.inv_tm), es = exp(-u * m.inv_ts);
+                best = fmax(best, V0 * em + m.kappa * I0 * (em - es));
+            }
+        }
+    }
+    return best;
+}
+
+// Per (sample, segment, 64 neurons): the segment's intervals (and the open
+// one in the sample's last segment); per lane the sums of the hinge terms
+// and the interval counts, part = (sum under, silent count, sum over,
+// spiking count).
+__global__ __launch_bounds__(kWave * kWalkWaves) void k_reg_walk(
+    const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
+    int E_pad, const float* __restrict__ WT, int C_in, int N, int tiles, int S, int items, Model m,
+    const Decay* __restrict__ dec, const double2* __restrict__ carry, const float* __restrict__ out_t,
+    const int32_t* __restrict__ out_n, const int32_t* __restrict__ out_k, double4* __restrict__ part)
+{
+    __shared__ double2 s_ad[kWalkWaves][kSeg];
+    __shared__ float s_t[kWalkWaves][kSeg + 1];
+    WalkCoords c;
+    if (!walk_coords<1>(items, tiles, S, ev_n, E_max, N, c)) return;
+    const int lane = c.lane, wv = (int)threadIdx.x / kWave;
+    const int n = c.n0;
+    double2* lad = s_ad[wv];
+    float* lt = s_t[wv];
+    const float* tt = ev_t + (size_t)c.b * E_max;
+    const Stage st = stage_segment(c, ev_src + (size_t)c.b * E_max + c.k0, dec + (size_t)c.b * E_pad + c.k0, WT,
+                                   C_in, N, lad, nullptr, nullptr);
+    // lt[e] = start of interval k0 + e (the time of event k0 + e - 1, or 0)
+#pragma unroll
+    for (int h = 0; h < kSrcRegs; ++h) {
+        const int e = h * kWave + lane;
+        if (e < c.cnt) lt[e + 1] = tt[c.k0 + e];
+    }
+    if (lane == 0) lt[0] = c.k0 > 0 ? tt[c.k0 - 1] : 0.0f;
+    wave_lds_sync();
+    const double2 cs = carry[((size_t)c.b * S + c.seg) * N + n];
+    double U = cs.x, J = cs.y;
+    // the neuron's spikes: the deficit at the segment's start from those of
+    // earlier intervals, then the ones inside taken in order
+    const size_t base = ((size_t)c.b * N + n) * (size_t)m.s_max;
+    const float* ts = out_t + base;
+    const int32_t* ks = out_k + base;
+    const int ns = c.live ? min(out_n[(size_t)c.b * N + n], m.s_max) : 0;
+    const double t_start = (double)lt[0];
+    double Dft = 0.0;
+    int sp = 0;
+    while (sp < ns && ks[sp] < c.k0) {
+        Dft += m.dth * exp(-(t_start - (double)ts[sp]) * m.inv_tm);
+        ++sp;
+    }
+    double su = 0.0, so = 0.0;
+    int nsil = 0, nspk = 0;
+    auto take = [&](int j, double L, double A, double Dd, double t1) {
+        const double vmax = reg_vmax(m, v_of(m, U, J) - Dft, J, L, A, Dd);
+        const bool spiked = sp < ns && ks[sp] == j;
+        if (spiked) {
+            so += fmax(vmax - m.th, 0.0);
+            ++nspk;
+        } else {
+            su += fmax(m.th - vmax, 0.0);
+            ++nsil;
+        }
+        // the deficit at the interval's end, with the spikes inside it
+        Dft *= A;
+        while (sp < ns && ks[sp] == j) {
+            Dft += m.dth * exp(-(t1 - (double)ts[sp]) * m.inv_tm);
+            ++sp;
+        }
+    };
+    const int ng = (c.cnt + kGrp - 1) / kGrp;
+    float wa[kGrp][1], wb[kGrp][1];
+    load_grp<1>(st, 0, wa);
+    auto group = [&](int g, const float (&w)[kGrp][1]) {
+#pragma unroll
+        for (int jj = 0; jj < kGrp; ++jj) {
+            const int e = g * kGrp + jj;
+            if (e >= c.cnt) break;
+            const double2 ad = lad[e];
+            const double t0 = (double)lt[e], t1 = (double)lt[e + 1];
+            take(c.k0 + e, t1 - t0, ad.x, ad.y, t1);
+            step1(ad, w[jj][0], U, J);
+        }
+    };
+    for (int g = 0; g < ng; g += 2) {
+        if (g + 1 < ng) load_grp<1>(st, (g + 1) * kGrp, wb);
+        group(g, wa);
+        if (g + 1 >= ng) break;
+        if (g + 2 < ng) load_grp<1>(st, (g + 2) * kGrp, wa);
+        group(g + 1, wb);
+    }
+    if (c.k0 + c.cnt == c.nb) {
+        // the open interval after the sample's last event, up to t_end
+        const double t0 = (double)lt[c.cnt];
+        const double L = m.t_end - t0;
+        const double A = isinf(L) ? 0.0 : exp(-L * m.inv_tm), Dd = isinf(L) ? 0.0 : exp(-L * m.inv_ts);
+        take(c.nb, L, A, Dd, m.t_end);
+    }
+    if (c.live) part[((size_t)c.b * S + c.seg) * N + n] = make_double4(su, (double)nsil, so, (double)nspk);
+}
+
+// Per (sample, neuron): the sums over the segments in order, then the means
+// over the silent and the spiking intervals (0 for an empty set).
+__global__ __launch_bounds__(256) void k_reg_reduce(const double4* __restrict__ part, const int32_t* __restrict__ ev_n,
+                                                    int B, int E_max, int N, int S, double th, double* __restrict__ ub,
+                                                    double* __restrict__ ob, float* __restrict__ under,
+                                                    float* __restrict__ over)
+{
+    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (size_t)B * N) return;
+    const int b = (int)(i / (size_t)N), n = (int)(i % (size_t)N);
+    const int nb = clamp_count(ev_n[b], E_max);
+    const int Sb = (nb + kSeg - 1) / kSeg;
+    double su = 0.0, nsil = 0.0, so = 0.0, nspk = 0.0;
+    for (int s = 0; s < Sb; ++s) {
+        const double4 p = part[((size_t)b * S + s) * N + n];
+        su += p.x;
+        nsil += p.y;
+        so += p.z;
+        nspk += p.w;
+    }
+    if (Sb == 0) {             // no event: the one interval [0, t_end) at rest (V_max = 0)
+        su = th;
+        nsil = 1.0;
+    }
+    const double u = nsil > 0.0 ? su / nsil : 0.0;
+    const double o = nspk > 0.0 ? so / nspk : 0.0;
+    ub[i] = u;
+    ob[i] = o;
+    if (under) under[i] = (float)u;
+    if (over) over[i] = (float)o;
+}
+
+// The two loss terms (one workgroup): per neuron the batch means and the
+// gates of the mean spike count against the target, then the means over the
+// neurons, each sum in a fixed order.
+constexpr int kRegThreads = 256;
+
+__global__ __launch_bounds__(kRegThreads) void k_reg_loss(const double* __restrict__ ub, const double* __restrict__ ob,
+                                                          const int32_t* __restrict__ out_n, int B, int N, int s_max,
+                                                          double c_target, float* __restrict__ loss)
+{
+    __shared__ double s_reg[kRegThreads], s_over[kRegThreads];
+    double lr = 0.0, lo = 0.0;
+    for (int n = threadIdx.x; n < N; n += kRegThreads) {
+        double cb = 0.0, mu = 0.0, mo = 0.0, ov = 0.0;
+        for (int b = 0; b < B; ++b) {
+            const size_t i = (size_t)b * N + n;
+            const double cnt = (double)min(out_n[i], s_max);
+            cb += cnt;
+            mu += ub[i];
+            mo += ob[i];
+            ov += fmax(cnt / c_target - 1.0, 0.0) * ob[i];
+        }
+        cb /= (double)B;
+        lr += fmax(1.0 - cb / c_target, 0.0) * (mu / (double)B) + fmax(cb / c_target - 1.0, 0.0) * (mo / (double)B);
+        lo += ov;
+    }
+    s_reg[threadIdx.x] = lr;
+    s_over[threadIdx.x] = lo;
+    __syncthreads();
+    for (int off = kRegThreads / 2; off > 0; off >>= 1) {
+        if ((int)threadIdx.x < off) {
+            s_reg[threadIdx.x] += s_reg[threadIdx.x + off];
+            s_over[threadIdx.x] += s_over[threadIdx.x + off];
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        loss[0] = (float)(s_reg[0] / (double)N);
+        loss[1] = (float)(s_over[0] / (double)N);
+    }
+}
+
+struct RegLayout {
+    FwdLayout f;
+    size_t part, ub, ob, status, total;
+};
+
+static RegLayout reg_layout(int B, int E_max, int N)
+{
+    RegLayout R;
+    R.f = fwd_layout(B, E_max, N, 0);
+    size_t off = R.f.total;
+    auto take = [&](size_t bytes) { size_t o = off; off += (bytes + 255) & ~(size_t)255; return o; };
+    R.part = take((size_t)B * R.f.S * N * sizeof(double4));
+    R.ub = take((size_t)B * N * sizeof(double));
+    R.ob = take((size_t)B * N * sizeof(double));
+    R.status = take(LIF_STATUS_WORDS * sizeof(int32_t));
+    R.total = off + 256;
+    return R;
+}
+
+}  // namespace lif
+
+extern "C" size_t lif_spike_count_reg_workspace_size(int B, int E_max, int C_in, int N_out)
+{
+    (void)C_in;
+    if (B < 0 || E_max < 0 || N_out < 1) return 0;
+    return lif::reg_layout(B, E_max, N_out).total;
+}
+
+extern "C" int lif_spike_count_reg(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
+                                   const float* WT, int C_in, int N_out, const lif_params* p, const float* out_t,
+                                   const int32_t* out_n, const int32_t* out_k, double c_target, float* loss,
+                                   float* under, float* over, void* ws, size_t ws_bytes, lif_stream_t stream_)
+{
+    using namespace lif;
+    int rc = validate_forward_args(ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, p, out_t, out_n, out_n);
+    if (rc) return rc;
+    if (!out_k || !loss || !ws || !(c_target > 0.0) || !isfinite(c_target)) return LIF_ERR_ARG;
+    const RegLayout R = reg_layout(B, E_max, N_out);
+    if (ws_bytes < R.total) return LIF_ERR_WORKSPACE;
+    const size_t items_max = (size_t)B * R.f.S * ((N_out + kWave - 1) / kWave);
+    if (items_max > 0x7fffffff) return LIF_ERR_SIZE;
+    hipStream_t stream = (hipStream_t)stream_;
+    const Model m = make_model(*p);
+    char* base = (char*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
+    FwdPtrs P{};
+    P.dec = (Decay*)(base + R.f.dec);
+    P.segm = (double2*)(base + R.f.segm);
+    P.carry = (double2*)(base + R.f.carry);
+    P.mask = (uint32_t*)(base + R.f.mask);
+    P.counters = (uint32_t*)(base + R.f.counters);
+    P.pool_count = P.counters;
+    P.nwork = P.counters + (size_t)B * kCtr;
+    P.listed = (uint32_t*)(base + R.f.listed);
+    P.work = (uint32_t*)(base + R.f.work);
+    P.pool = (double2*)(base + R.f.pool);
+    double4* part = (double4*)(base + R.part);
+    double* ub = (double*)(base + R.ub);
+    double* ob = (double*)(base + R.ob);
+    int32_t* st = (int32_t*)(base + R.status);
+    const size_t nn = (size_t)B * N_out;
+    if (items_max > 0) {
+        // the no-reset state entering every segment (the forward's scan)
+        switch (pick_npl(WT, N_out)) {
+        case 4: launch_walks<4>(R.f, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, m, st, false, nullptr, nullptr,
+                                nullptr, nullptr, stream, false); break;
+        case 2: launch_walks<2>(R.f, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, m, st, false, nullptr, nullptr,
+                                nullptr, nullptr, stream, false); break;
+        default: launch_walks<1>(R.f, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, m, st, false, nullptr,
+                                 nullptr, nullptr, nullptr, stream, false); break;
+        }
+        const int tl = (N_out + kWave - 1) / kWave;
+        const size_t it = (size_t)B * R.f.S * tl;
+        TIMED_LAUNCH("reg_walk", k_reg_walk, dim3((unsigned)((it + kWalkWaves - 1) / kWalkWaves)),
+                     dim3(kWave * kWalkWaves), 0, stream, ev_t, ev_src, ev_n, E_max, R.f.E_pad, WT, C_in, N_out, tl,
+                     R.f.S, (int)it, m, P.dec, P.carry, out_t, out_n, out_k, part);
+    }
+    if (nn)
+        TIMED_LAUNCH("reg_reduce", k_reg_reduce, dim3((unsigned)((nn + 255) / 256)), dim3(256), 0, stream, part, ev_n,
+                     B, E_max, N_out, R.f.S, m.th, ub, ob, under, over);
+    if (B > 0)
+        TIMED_LAUNCH("reg_loss", k_reg_loss, dim3(1), dim3(kRegThreads), 0, stream, ub, ob, out_n, B, N_out, m.s_max,
+                     c_target, loss);
+    return check_launch();
 }
 
 // ---------------------------------------------------------------------------

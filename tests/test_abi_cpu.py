@@ -171,3 +171,21 @@ def test_readout_and_merge_grad_argument_errors(lib):
     assert L.lif_li_readout_workspace_size(2, 10, 4, 8) > 0
     assert L.lif_merge_grad(F, F, F, 2, 10, 0, 4, F, None) == L.LIF_ERR_ARG
     assert L.lif_merge_grad(F, F, F, 2, 10, 8, 4, None, None) == L.LIF_ERR_ARG
+
+
+def test_spike_count_reg_argument_errors(lib):
+    p = L.Params().c()
+    # ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, p, out_t, out_n, out_k, c_target, loss, under, over, ws, ws_bytes, s
+    base = [F, F, F, 2, 10, F, 4, 8, ctypes.byref(p), F, F, F, 4.0, F, None, None, F, 10 ** 9, None]
+
+    def call(i, v):
+        a = list(base)
+        a[i] = v
+        return L.lif_spike_count_reg(*a)
+    assert call(11, None) == L.LIF_ERR_ARG          # out_k required
+    assert call(13, None) == L.LIF_ERR_ARG          # loss required
+    assert call(12, 0.0) == L.LIF_ERR_ARG           # c_target > 0
+    assert call(17, 10) == L.LIF_ERR_WORKSPACE
+    bad = L.Params(tau_mem=0.001).c()
+    assert call(8, ctypes.byref(bad)) == L.LIF_ERR_TAU
+    assert L.lif_spike_count_reg_workspace_size(2, 10, 4, 8) > 0

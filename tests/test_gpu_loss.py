@@ -128,3 +128,54 @@ def test_readout_on_a_merged_hidden_layer(env):
         k = n2n[b]
         ref[b, pn[b, :k]] = gTn[b, :k]
     assert np.array_equal(go.reshape(B, -1), ref)
+
+
+def _reg_oracle(ev, WT, r, P, c_target):
+    """The oracle's interval tables from its own spike trains, and the
+    regulariser terms."""
+    B, N = r.out_n.shape
+    tables = []
+    for b in range(B):
+        n = int(ev.ev_n[b])
+        row = []
+        for i in range(N):
+            ns = int(r.out_n[b, i])
+            w = WT[ev.ev_src[b, :n], i]
+            row.append(OL.interval_table(ev.ev_t[b, :n], n, w, r.out_t[b, i, :ns], r.out_k[b, i, :ns], ns, P.tau_mem,
+                                         P.tau_syn, P.v_th, P.v_reset, P.t_end))
+        tables.append(row)
+    L_reg, L_over, _ = OL.spike_count_reg(tables, r.out_n, P.v_th, OL.RegParams(c_target=c_target))
+    under = np.array([[np.mean([max(P.v_th - x[4], 0.0) for x in t if not x[6]] or [0.0]) for t in row]
+                      for row in tables])
+    over = np.array([[np.mean([max(x[4] - P.v_th, 0.0) for x in t if x[6]] or [0.0]) for t in row]
+                     for row in tables])
+    return L_reg, L_over, under, over
+
+
+@pytest.mark.parametrize("t_end,vr", [(math.inf, 0.0), (0.5, -0.3)])
+def test_spike_count_regularisers(env, t_end, vr):
+    """App. E.1 on a driven layer with ragged queues and an empty sample: the
+    per-(sample, neuron) hinge means and both loss terms, from the oracle's
+    spike trains handed to both sides (rounded to float32 for the GPU)."""
+    torch, lif = env
+    cfg = W.random_small(51, B=4, C=40, N=70, n_events=600, T=0.4, gain=6.0)
+    ev, WT = cfg.events, cfg.layers[0].WT
+    ev.ev_n[2] = 0
+    P = oracle.LifParams(s_max=64, t_end=t_end, v_reset=vr)
+    r = oracle.forward(ev.ev_t, ev.ev_src, ev.ev_n, WT, P)
+    assert r.out_n.sum() > 100 and not r.capped.any()
+    print(f"[case] regularisers t_end={t_end} v_reset={vr} spikes={int(r.out_n.sum())}", flush=True)
+    L_reg, L_over, under, over = _reg_oracle(ev, WT, r, P, 4.0)
+    fwd = lif.ForwardOut(_dev(torch, r.out_t.astype(np.float32)), _dev(torch, r.out_n),
+                         _dev(torch, r.out_i.astype(np.float32)), None, _dev(torch, r.out_k))
+    args = [_dev(torch, a) for a in (ev.ev_t, ev.ev_src, ev.ev_n, WT)]
+    lp = lif.Params(s_max=64, t_end=t_end, v_reset=vr)
+    loss, gu, go = lif.spike_count_reg(*args, fwd, 4.0, lp)
+    loss2, _, _ = lif.spike_count_reg(*args, fwd, 4.0, lp)
+    torch.cuda.synchronize()
+    _close(gu.cpu().numpy(), under, 1e-5, "under")
+    _close(go.cpu().numpy(), over, 1e-5, "over")
+    assert (gu.cpu().numpy()[2] == P.v_th).all()            # the empty sample: V = 0 throughout
+    assert abs(loss[0].item() - L_reg) <= 1e-5 * abs(L_reg), (loss[0].item(), L_reg)
+    assert abs(loss[1].item() - L_over) <= 1e-5 * max(abs(L_over), 1e-12), (loss[1].item(), L_over)
+    assert torch.equal(loss.view(torch.int32), loss2.view(torch.int32))
