@@ -11,6 +11,11 @@ Two independent implementations live here:
   forward, backward (implicit differentiation through the resets) and the
   layer merge.  Wrapped below with ctypes + numpy.
 * ``ref.py``: the same definitions in pure Python loops for tiny inputs.
+* ``loss.py``: the paper's readout loss and spike-count regularisers
+  (numpy, float64).
+
+``lif_oracle.c`` also holds the chunk mode of Sec. 3.2.1 (K events per
+iteration, a budget of C iterations, work counters of Appendix G).
 
 Functions whose results cannot be pinned independently would say
 "parity unpinned" here; at present every output (spike times, counts, I at
@@ -62,6 +67,10 @@ def _load():
         _lib.or_forward.argtypes = [P, P, P, ctypes.c_int, ctypes.c_int, P, ctypes.c_int, ctypes.c_int,
                                     ctypes.POINTER(_Params), ctypes.c_int, P, P, P, P, P, P, P]
         _lib.or_forward.restype = ctypes.c_int
+        _lib.or_forward_chunked.argtypes = [P, P, P, ctypes.c_int, ctypes.c_int, P, ctypes.c_int, ctypes.c_int,
+                                            ctypes.POINTER(_Params), ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                            P, P, P, P, P, P, P, P, P]
+        _lib.or_forward_chunked.restype = ctypes.c_int
         _lib.or_backward.argtypes = [P, P, P, ctypes.c_int, ctypes.c_int, P, ctypes.c_int, ctypes.c_int,
                                      ctypes.POINTER(_Params), ctypes.c_int, P, P, P, P, P, P, P]
         _lib.or_backward.restype = ctypes.c_int
@@ -151,6 +160,38 @@ def forward(ev_t, ev_src, ev_n, WT, params: LifParams = LifParams(), nthreads: O
     if rc != 0:
         raise ValueError(f"oracle forward rejected its arguments (rc={rc})")
     return ForwardResult(out_t, out_i, out_n, capped, tie_t, min_gap, out_k)
+
+
+def forward_chunked(ev_t, ev_src, ev_n, WT, K: int, C: int, params: LifParams = LifParams(),
+                    nthreads: Optional[int] = None):
+    """Chunk-mode forward (K events per chunk iteration, at most C
+    iterations per neuron; Sec. 3.2.1 speculative execution and fixed
+    budget).  Returns (ForwardResult, consumed [B, N], processed [B, N])."""
+    lib = _load()
+    ev_t = np.ascontiguousarray(ev_t, dtype=np.float32)
+    ev_src = np.ascontiguousarray(ev_src, dtype=np.int32)
+    ev_n = np.ascontiguousarray(ev_n, dtype=np.int32)
+    WT = np.ascontiguousarray(WT, dtype=np.float32)
+    B, E = ev_t.shape
+    C_in, N = WT.shape
+    S = int(params.s_max)
+    out_t = np.empty((B, N, S), np.float64)
+    out_i = np.empty((B, N, S), np.float64)
+    out_k = np.empty((B, N, S), np.int32)
+    out_n = np.empty((B, N), np.int32)
+    capped = np.empty((B, N), np.int32)
+    tie_t = np.empty((B, N), np.float64)
+    min_gap = np.empty((B, N), np.float64)
+    consumed = np.empty((B, N), np.int32)
+    processed = np.empty((B, N), np.int32)
+    p = params.c()
+    rc = lib.or_forward_chunked(_ptr(ev_t), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(WT), C_in, N, ctypes.byref(p),
+                                int(K), int(C), _nthreads(nthreads), _ptr(out_t), _ptr(out_i), _ptr(out_k),
+                                _ptr(out_n), _ptr(capped), _ptr(tie_t), _ptr(min_gap), _ptr(consumed),
+                                _ptr(processed))
+    if rc != 0:
+        raise ValueError(f"oracle chunked forward rejected its arguments (rc={rc})")
+    return ForwardResult(out_t, out_i, out_n, capped, tie_t, min_gap, out_k), consumed, processed
 
 
 def backward(ev_t, ev_src, ev_n, WT, fwd: ForwardResult, grad_out_t, params: LifParams = LifParams(),

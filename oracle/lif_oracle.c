@@ -265,6 +265,130 @@ int or_forward(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, in
     return rc;
 }
 
+/* ---------------------------------------------------------------------- */
+/* Chunk mode (Sec. 3.2.1 "Speculative execution" and "Fixed compute        */
+/* budget", Appendix E.2): the neuron takes its queue K events at a time.   */
+/* Each chunk iteration tests the intervals closed by its events in order   */
+/* (and, in the chunk that holds the last event, the interval after it up   */
+/* to t_end); at the first crossing it commits one spike, hard-resets, and  */
+/* the next iteration starts at the spike time with the same pending event  */
+/* (the chunk's later events are processed but discarded); without a        */
+/* crossing all its events are consumed.  At most C iterations run and at   */
+/* most s_max spikes are kept.  Work counters (Appendix G): processed = the */
+/* events of every iteration's chunk (an event visited twice counts twice), */
+/* consumed = the events consumed when the neuron stops.                    */
+/* ---------------------------------------------------------------------- */
+static or_neuron_result simulate_neuron_chunked(const or_params* p, const float* ev_t, const int32_t* ev_src, int n,
+                                                const float* WT, int N, int i, int K, int C, double* st, double* si,
+                                                int32_t* sk, int32_t* consumed, int32_t* processed)
+{
+    or_neuron_result res = {0, 0, INFINITY, INFINITY};
+    double t_cur = 0.0, V = 0.0, I = 0.0;
+    int k = 0, chunks = 0;
+    long long work = 0;
+    int finished = 0;
+    while (!finished && !res.capped && chunks < C) {
+        ++chunks;
+        const int end = (k + K < n) ? k + K : n;
+        work += end - k;
+        for (;;) {
+            double t_hi;
+            if (k < end) t_hi = (double)ev_t[k];
+            else if (end == n) t_hi = p->t_end;      /* the interval after the last event */
+            else break;                              /* the chunk is consumed */
+            double len = t_hi - t_cur;
+            if (len > 0.0) {
+                or_check c = check_interval(p, V, I, len);
+                double gap = fabs(c.vmax - p->v_th);
+                if (gap < res.min_gap) res.min_gap = gap;
+                if (gap < p->tie_band && t_cur < res.tie_t) res.tie_t = t_cur;
+                if (c.crossing) {
+                    double tau = solve_root(p, V, I, c.hi);
+                    double Istar = i_at(p, I, tau);
+                    st[res.n_spikes] = t_cur + tau;
+                    si[res.n_spikes] = Istar;
+                    sk[res.n_spikes] = k;
+                    res.n_spikes++;
+                    if (res.n_spikes >= p->s_max) res.capped = 1;
+                    V = p->v_reset;
+                    I = Istar;
+                    t_cur = t_cur + tau;
+                    break;                           /* the next iteration restarts here */
+                }
+            }
+            if (k >= n) { finished = 1; break; }     /* the last interval holds no spike */
+            if (len > 0.0) {
+                double Vn = v_at(p, V, I, len);
+                I = i_at(p, I, len);
+                V = Vn;
+            }
+            I += (double)WT[(size_t)ev_src[k] * (size_t)N + (size_t)i];
+            t_cur = t_hi;
+            ++k;
+        }
+    }
+    *consumed = k;
+    *processed = (int32_t)work;
+    return res;
+}
+
+typedef struct {
+    fwd_job f;
+    int K, C;
+    int32_t* consumed; int32_t* processed;
+} chunk_job;
+
+static void* chunk_worker(void* arg)
+{
+    chunk_job* cj = (chunk_job*)arg;
+    fwd_job* j = &cj->f;
+    size_t total = (size_t)j->B * (size_t)j->N;
+    for (size_t item = (size_t)j->tid; item < total; item += (size_t)j->nthreads) {
+        int b = (int)(item / (size_t)j->N), i = (int)(item % (size_t)j->N);
+        size_t o = item * (size_t)j->p->s_max;
+        for (int s = 0; s < j->p->s_max; ++s) {
+            j->out_t[o + s] = INFINITY;
+            j->out_i[o + s] = 0.0;
+            j->out_k[o + s] = 0;
+        }
+        or_neuron_result r = simulate_neuron_chunked(j->p, j->ev_t + (size_t)b * j->E_max,
+                                                     j->ev_src + (size_t)b * j->E_max, j->ev_n[b], j->WT, j->N, i,
+                                                     cj->K, cj->C, j->out_t + o, j->out_i + o, j->out_k + o,
+                                                     cj->consumed + item, cj->processed + item);
+        j->out_n[item] = r.n_spikes;
+        j->capped[item] = r.capped;
+        j->tie_t[item] = r.tie_t;
+        j->min_gap[item] = r.min_gap;
+    }
+    return NULL;
+}
+
+/* Chunk-mode forward over a batch (outputs as or_forward, plus the
+ * per-(sample, neuron) consumed and processed event counts). */
+int or_forward_chunked(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
+                       const float* WT, int C_in, int N, const or_params* p, int K, int C, int nthreads,
+                       double* out_t, double* out_i, int32_t* out_k, int32_t* out_n, int32_t* capped,
+                       double* tie_t, double* min_gap, int32_t* consumed, int32_t* processed)
+{
+    if (!(p->tau_mem > p->tau_syn && p->tau_syn > 0.0) || !(p->v_reset < p->v_th) || p->s_max < 1 || K < 1 || C < 1)
+        return -1;
+    if (nthreads < 1) nthreads = 1;
+    chunk_job* jobs = (chunk_job*)calloc((size_t)nthreads, sizeof(chunk_job));
+    if (!jobs) return -2;
+    for (int t = 0; t < nthreads; ++t) {
+        fwd_job j = {p, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N,
+                     out_t, out_i, out_k, out_n, capped, tie_t, min_gap, t, nthreads};
+        jobs[t].f = j;
+        jobs[t].K = K;
+        jobs[t].C = C;
+        jobs[t].consumed = consumed;
+        jobs[t].processed = processed;
+    }
+    int rc = run_threads(chunk_worker, jobs, sizeof(chunk_job), nthreads);
+    free(jobs);
+    return rc;
+}
+
 /* Membrane trace of one neuron right after every input event (no spikes
  * beyond what the full forward finds); used by the closed-form pins.
  * V_after[k], I_after[k] are the true (reset-including) state just after
