@@ -204,6 +204,27 @@ def train_step(torch, lif, d, c3, steps, warmup):
     return out
 
 
+def chunk_study(torch, lif, d, ev, WT, steps, warmup, seq_ms):
+    """The paper's chunked scheme on the headline workload at chunk sizes 64,
+    128 and 256 with its budget rule: time per forward, work retained
+    (consumed / processed events) and speedup over the sequential loop."""
+    args = [d(ev.ev_t), d(ev.ev_src), d(ev.ev_n), d(WT)]
+    out = {"workload": "700->256, B=32, chunked forward (one wave per neuron, K events per iteration, "
+                       "budget ceil(E_max/K) + s_max iterations)"}
+    for K in (64, 128, 256):
+        run = lambda: lif.forward_chunked(*args, K=K, C=0)
+        o, cons, proc = run()
+        torch.cuda.synchronize()
+        ms, ev_ms = time_steps(torch, run, steps, warmup)
+        c, p = int(cons.sum().item()), int(proc.sum().item())
+        out[f"K{K}"] = {"ms": ms, "event_ms": stats_ms(ev_ms), "work_retained": c / max(p, 1),
+                        "consumed": c, "processed": p, "spikes": int(o.out_n.sum().item()),
+                        "speedup_vs_sequential": seq_ms / ms}
+        log(f"[bench] chunked K={K}: {ms * 1e3:.1f} us, work retained {c / max(p, 1):.3f}, "
+            f"{seq_ms / ms:.1f}x the sequential loop")
+    return out
+
+
 def cpu_oracle(ev, WT, nthreads, seconds, n_samples, n_neurons):
     """The float64 oracle on a bounded sample of a workload (the first
     n_samples samples and n_neurons neurons), repeated for about `seconds`;
@@ -357,6 +378,7 @@ def main():
         extras["c5_hidden_driven"] = run_workload(torch, lif, d, "32768->2048, B=16, ~100k events, gain 16",
                                                   c5.events, W1d, lif.Params(s_max=64), st, wu, 1, backward=True)
         extras["train_step_c3"] = train_step(torch, lif, d, c3, st, wu)
+        extras["chunk_mode_c2"] = chunk_study(torch, lif, d, ev, WT, st, wu, seq_ms)
         del c3, c4, c5, W1d
 
     # ---- float64 CPU oracle on the host cores (bounded samples)

@@ -172,6 +172,29 @@ int lif_layer_forward_noalloc(const float* ev_t, const int32_t* ev_src, const in
                               lif_stream_t stream);
 size_t lif_layer_forward_noalloc_max_bytes(void);
 
+/* The paper's own chunked scheme, for studies of the chunk size and the
+ * work retained (Sec. 3.2.1 "Speculative execution" and "Fixed compute
+ * budget", Appendix E.2, Appendix G): one wave per (sample, neuron) takes
+ * its queue K events at a time (K = 64, 128 or 256), scans the chunk's
+ * affine maps across the wave, tests every interval with the rule of
+ * Sec. 3.2.2 and commits only the first crossing (bracket of Appendix D.2,
+ * multisection to the smallest double with V >= V_th); the next iteration
+ * restarts at the spike with the same pending event.  At most C iterations
+ * run per neuron (C <= 0: ceil(E_max / K) + s_max, the paper's budget for
+ * an input layer) and at most s_max spikes are kept.  Outputs as
+ * lif_layer_forward (out_k included), and per (sample, neuron):
+ *   consumed  int32 [B][N_out] input events consumed when the neuron stopped
+ *   processed int32 [B][N_out] input events of all its chunk iterations (an
+ *             event visited twice counts twice); may be NULL, as consumed
+ * Status words: LIF_ST_CAND_BLOCKS counts chunk iterations and
+ * LIF_ST_WALKED_BLOCKS processed events; the others as the forward.
+ * With a budget that suffices, the spikes are those of lif_layer_forward.
+ * No workspace. */
+int lif_layer_forward_chunked(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
+                              const float* WT, int C_in, int N_out, const lif_params* p, int K, int C,
+                              float* out_t, int32_t* out_n, float* out_i, int32_t* out_k, int32_t* consumed,
+                              int32_t* processed, int32_t* status, lif_stream_t stream);
+
 /* --------------------------------------------------------------------- */
 /* Backward pass (paper Appendix D.3, Eq. ift_vjp, chained through the     */
 /* hard resets): given dL/dt for every output spike, returns dL/dW and     */

@@ -44,6 +44,7 @@ LIF_MERGE_MAX = 16384
 
 EXPORTED = ["lif_version", "lif_layer_forward_workspace_size", "lif_layer_forward",
             "lif_layer_forward_sequential", "lif_layer_forward_noalloc", "lif_layer_forward_noalloc_max_bytes",
+            "lif_layer_forward_chunked",
             "lif_layer_backward_workspace_size", "lif_layer_backward",
             "lif_merge_workspace_size", "lif_merge_spikes", "lif_first_spike_ce", "lif_merge_grad",
             "lif_li_readout_workspace_size", "lif_li_readout", "lif_adam_step", "lif_spike_count_reg_workspace_size",
@@ -141,6 +142,9 @@ def load(path: Optional[str] = None):
         f = getattr(lib, name)
         f.restype = _I
         f.argtypes = fwd_args
+    lib.lif_layer_forward_chunked.restype = _I
+    lib.lif_layer_forward_chunked.argtypes = [_P, _P, _P, _I, _I, _P, _I, _I, _PP, _I, _I, _P, _P, _P, _P, _P, _P, _P,
+                                              _P]
     lib.lif_layer_forward_noalloc.restype = _I
     lib.lif_layer_forward_noalloc.argtypes = fwd_args[:14] + [_P]
     lib.lif_layer_forward_noalloc_max_bytes.restype = _SZ
@@ -203,6 +207,10 @@ def lif_layer_forward(*args) -> int:
 
 def lif_layer_forward_sequential(*args) -> int:
     return load().lif_layer_forward_sequential(*args)
+
+
+def lif_layer_forward_chunked(*args) -> int:
+    return load().lif_layer_forward_chunked(*args)
 
 
 def lif_layer_forward_noalloc(*args) -> int:
@@ -449,3 +457,25 @@ def spike_count_reg(ev_t, ev_src, ev_n, WT, fwd: ForwardOut, c_target: float, pa
                              _ptr(under), _ptr(over), _ptr(ws), ws.numel(), _stream(stream))
     _check("lif_spike_count_reg", rc)
     return loss, under, over
+
+
+def forward_chunked(ev_t, ev_src, ev_n, WT, K: int = 128, C: int = 0, params: Params = Params(), stream=None):
+    """Run lif_layer_forward_chunked; returns (ForwardOut, consumed [B, N],
+    processed [B, N])."""
+    torch = _torch()
+    B, E, Cin, N = _dev_inputs(ev_t, ev_src, ev_n, WT)
+    dev = ev_t.device
+    p = params.c()
+    out = ForwardOut(torch.empty((B, N, params.s_max), dtype=torch.float32, device=dev),
+                     torch.empty((B, N), dtype=torch.int32, device=dev),
+                     torch.empty((B, N, params.s_max), dtype=torch.float32, device=dev),
+                     torch.empty(LIF_STATUS_WORDS, dtype=torch.int32, device=dev),
+                     torch.empty((B, N, params.s_max), dtype=torch.int32, device=dev))
+    consumed = torch.empty((B, N), dtype=torch.int32, device=dev)
+    processed = torch.empty((B, N), dtype=torch.int32, device=dev)
+    rc = lif_layer_forward_chunked(_ptr(ev_t), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(WT), Cin, N, ctypes.byref(p),
+                                   int(K), int(C), _ptr(out.out_t), _ptr(out.out_n), _ptr(out.out_i),
+                                   _ptr(out.out_k), _ptr(consumed), _ptr(processed), _ptr(out.status),
+                                   _stream(stream))
+    _check("lif_layer_forward_chunked", rc)
+    return out, consumed, processed
