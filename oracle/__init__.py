@@ -15,7 +15,9 @@ Two independent implementations live here:
   (numpy, float64).
 
 ``lif_oracle.c`` also holds the chunk mode of Sec. 3.2.1 (K events per
-iteration, a budget of C iterations, work counters of Appendix G).
+iteration, a budget of C iterations, work counters of Appendix G) and the
+layer with learnable synaptic delays (Sec. 3.1 Eq. spike_input: a queue per
+neuron ordered by arrival time, App. E.2).
 
 Functions whose results cannot be pinned independently would say
 "parity unpinned" here; at present every output (spike times, counts, I at
@@ -74,6 +76,14 @@ def _load():
         _lib.or_backward.argtypes = [P, P, P, ctypes.c_int, ctypes.c_int, P, ctypes.c_int, ctypes.c_int,
                                      ctypes.POINTER(_Params), ctypes.c_int, P, P, P, P, P, P, P]
         _lib.or_backward.restype = ctypes.c_int
+        _lib.or_delay_queues.argtypes = [P, P, P, ctypes.c_int, ctypes.c_int, P, ctypes.c_int, ctypes.c_int, P, P]
+        _lib.or_delay_queues.restype = ctypes.c_int
+        _lib.or_forward_delayed.argtypes = [P, P, P, ctypes.c_int, ctypes.c_int, P, P, ctypes.c_int, ctypes.c_int,
+                                            ctypes.POINTER(_Params), ctypes.c_int, P, P, P, P, P, P, P]
+        _lib.or_forward_delayed.restype = ctypes.c_int
+        _lib.or_backward_delayed.argtypes = [P, P, P, ctypes.c_int, ctypes.c_int, P, P, ctypes.c_int, ctypes.c_int,
+                                             ctypes.POINTER(_Params), ctypes.c_int, P, P, P, P, P, P, P, P]
+        _lib.or_backward_delayed.restype = ctypes.c_int
         _lib.or_trace.argtypes = [P, P, ctypes.c_int, P, ctypes.c_int, ctypes.c_int,
                                   ctypes.POINTER(_Params), P, P]
         _lib.or_trace.restype = ctypes.c_int
@@ -219,6 +229,83 @@ def backward(ev_t, ev_src, ev_n, WT, fwd: ForwardResult, grad_out_t, params: Lif
     if rc != 0:
         raise RuntimeError(f"oracle backward failed (rc={rc})")
     return gW, gT
+
+
+def _f32(a):
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def _i32(a):
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def delay_queues(ev_t, ev_src, ev_n, DT):
+    """Each neuron's queue of arrivals (Sec. 3.1 Eq. spike_input, App. E.2):
+    event k of sample b reaches neuron i at fl32(t_k + DT[src_k, i]), ordered
+    by (arrival, k).  Returns q_t float32 [B, N, E_max] and q_k int32 (the
+    sample's event index); entries past ev_n[b] are 0."""
+    ev_t, ev_src, ev_n, DT = _f32(ev_t), _i32(ev_src), _i32(ev_n), _f32(DT)
+    B, E = ev_t.shape
+    C, N = DT.shape
+    q_t = np.zeros((B, N, E), np.float32)
+    q_k = np.zeros((B, N, E), np.int32)
+    rc = _load().or_delay_queues(_ptr(ev_t), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(DT), C, N, _ptr(q_t), _ptr(q_k))
+    if rc != 0:
+        raise RuntimeError(f"oracle delay queues failed (rc={rc})")
+    return q_t, q_k
+
+
+def forward_delayed(ev_t, ev_src, ev_n, WT, DT, params: LifParams = LifParams(),
+                    nthreads: Optional[int] = None) -> ForwardResult:
+    """Serial float64 forward of a layer with synaptic delays DT [C_in, N]:
+    every neuron runs the serial simulation on its own arrival queue (out_k
+    counts events of that queue)."""
+    lib = _load()
+    ev_t, ev_src, ev_n, WT, DT = _f32(ev_t), _i32(ev_src), _i32(ev_n), _f32(WT), _f32(DT)
+    B, E = ev_t.shape
+    C, N = WT.shape
+    assert DT.shape == WT.shape
+    S = int(params.s_max)
+    out_t = np.empty((B, N, S), np.float64)
+    out_i = np.empty((B, N, S), np.float64)
+    out_k = np.empty((B, N, S), np.int32)
+    out_n = np.empty((B, N), np.int32)
+    capped = np.empty((B, N), np.int32)
+    tie_t = np.empty((B, N), np.float64)
+    min_gap = np.empty((B, N), np.float64)
+    p = params.c()
+    rc = lib.or_forward_delayed(_ptr(ev_t), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(WT), _ptr(DT), C, N,
+                                ctypes.byref(p), _nthreads(nthreads), _ptr(out_t), _ptr(out_i), _ptr(out_k),
+                                _ptr(out_n), _ptr(capped), _ptr(tie_t), _ptr(min_gap))
+    if rc != 0:
+        raise ValueError(f"oracle delayed forward rejected its arguments (rc={rc})")
+    return ForwardResult(out_t, out_i, out_n, capped, tie_t, min_gap, out_k)
+
+
+def backward_delayed(ev_t, ev_src, ev_n, WT, DT, fwd: ForwardResult, grad_out_t,
+                     params: LifParams = LifParams(), nthreads: Optional[int] = None):
+    """float64 gradients (grad_WT, grad_DT [C_in, N], grad_ev_t [B, E_max])
+    of L = sum grad_out_t * out_t for a layer with delays, through a delayed
+    forward result for the same inputs."""
+    lib = _load()
+    ev_t, ev_src, ev_n, WT, DT = _f32(ev_t), _i32(ev_src), _i32(ev_n), _f32(WT), _f32(DT)
+    B, E = ev_t.shape
+    C, N = WT.shape
+    g = np.ascontiguousarray(grad_out_t, dtype=np.float64)
+    gW = np.empty((C, N), np.float64)
+    gD = np.empty((C, N), np.float64)
+    gT = np.empty((B, E), np.float64)
+    p = params.c()
+    rc = lib.or_backward_delayed(_ptr(ev_t), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(WT), _ptr(DT), C, N,
+                                 ctypes.byref(p), _nthreads(nthreads),
+                                 _ptr(np.ascontiguousarray(fwd.out_t, dtype=np.float64)),
+                                 _ptr(np.ascontiguousarray(fwd.out_i, dtype=np.float64)),
+                                 _ptr(np.ascontiguousarray(fwd.out_k, dtype=np.int32)),
+                                 _ptr(np.ascontiguousarray(fwd.out_n, dtype=np.int32)),
+                                 _ptr(g), _ptr(gW), _ptr(gD), _ptr(gT))
+    if rc != 0:
+        raise RuntimeError(f"oracle delayed backward failed (rc={rc})")
+    return gW, gD, gT
 
 
 def trace(ev_t_row, ev_src_row, n, WT, i, params: LifParams = LifParams()):

@@ -600,3 +600,241 @@ double or_solve_root(const or_params* p, double V0, double I0, double hi)
 {
     return solve_root(p, V0, I0, hi);
 }
+
+/* ---------------------------------------------------------------------- */
+/* Learnable synaptic delays (Sec. 3.1 Eq. spike_input; App. E.2 event      */
+/* queues).  A spike of input channel j at t_k reaches neuron i at          */
+/* a = t_k + d_ij, so every neuron has its own queue: the sample's events   */
+/* ordered by arrival.  Readings: the arrival is the float32 sum            */
+/* fl(t_k + d_ij) (the same value on every side that builds the queue), and */
+/* equal arrivals keep the sample's event order (index k).  The neuron then */
+/* runs the serial simulation of simulate_neuron on its queue, with         */
+/* out_k counting events of its own queue.  Gradients: the arrival enters   */
+/* only through the event's time, so dL/dd_ij sums dL/da over the events of */
+/* channel j in neuron i's queue, and dL/dt_k sums dL/da over the neurons.  */
+/* ---------------------------------------------------------------------- */
+
+typedef struct { float a; int32_t k; } or_arrival;
+
+static int cmp_arrival(const void* x, const void* y)
+{
+    const or_arrival* p = (const or_arrival*)x;
+    const or_arrival* q = (const or_arrival*)y;
+    if (p->a < q->a) return -1;
+    if (p->a > q->a) return 1;
+    return (p->k > q->k) - (p->k < q->k);
+}
+
+/* Neuron i's queue of one sample: arrival times qa[r] and the sample's
+ * event index qk[r] of its r-th event, r = 0 .. n - 1. */
+static void build_queue(const float* ev_t, const int32_t* ev_src, int n, const float* DT, int N, int i,
+                        or_arrival* tmp, float* qa, int32_t* qk, int32_t* qsrc)
+{
+    for (int k = 0; k < n; ++k) {
+        volatile float a = ev_t[k] + DT[(size_t)ev_src[k] * (size_t)N + (size_t)i];
+        tmp[k].a = a;
+        tmp[k].k = k;
+    }
+    qsort(tmp, (size_t)n, sizeof(or_arrival), cmp_arrival);
+    for (int r = 0; r < n; ++r) {
+        qa[r] = tmp[r].a;
+        qk[r] = tmp[r].k;
+        qsrc[r] = ev_src[tmp[r].k];
+    }
+}
+
+/* The queues of a batch: q_t, q_k [B][N][E_max] (entries past ev_n[b] are
+ * left as they are). */
+int or_delay_queues(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
+                    const float* DT, int C_in, int N, float* q_t, int32_t* q_k)
+{
+    (void)C_in;
+    or_arrival* tmp = (or_arrival*)malloc(sizeof(or_arrival) * (size_t)(E_max > 0 ? E_max : 1));
+    int32_t* qs = (int32_t*)malloc(sizeof(int32_t) * (size_t)(E_max > 0 ? E_max : 1));
+    if (!tmp || !qs) { free(tmp); free(qs); return -2; }
+    for (int b = 0; b < B; ++b)
+        for (int i = 0; i < N; ++i) {
+            size_t o = ((size_t)b * (size_t)N + (size_t)i) * (size_t)E_max;
+            build_queue(ev_t + (size_t)b * E_max, ev_src + (size_t)b * E_max, ev_n[b], DT, N, i, tmp,
+                        q_t + o, q_k + o, qs);
+        }
+    free(tmp); free(qs);
+    return 0;
+}
+
+typedef struct {
+    const or_params* p;
+    const float* ev_t; const int32_t* ev_src; const int32_t* ev_n;
+    int B, E_max; const float* WT; const float* DT; int C_in, N;
+    double* out_t; double* out_i; int32_t* out_k; int32_t* out_n; int32_t* capped; double* tie_t;
+    double* min_gap;
+    int tid, nthreads;
+} dly_fwd_job;
+
+static void* dly_fwd_worker(void* arg)
+{
+    dly_fwd_job* j = (dly_fwd_job*)arg;
+    size_t E = (size_t)(j->E_max > 0 ? j->E_max : 1);
+    or_arrival* tmp = (or_arrival*)malloc(sizeof(or_arrival) * E);
+    float* qa = (float*)malloc(sizeof(float) * E);
+    int32_t* qk = (int32_t*)malloc(sizeof(int32_t) * E);
+    int32_t* qs = (int32_t*)malloc(sizeof(int32_t) * E);
+    size_t total = (size_t)j->B * (size_t)j->N;
+    for (size_t item = (size_t)j->tid; item < total; item += (size_t)j->nthreads) {
+        int b = (int)(item / (size_t)j->N), i = (int)(item % (size_t)j->N);
+        size_t o = item * (size_t)j->p->s_max;
+        for (int s = 0; s < j->p->s_max; ++s) {
+            j->out_t[o + s] = INFINITY;
+            j->out_i[o + s] = 0.0;
+            j->out_k[o + s] = 0;
+        }
+        int n = j->ev_n[b];
+        build_queue(j->ev_t + (size_t)b * j->E_max, j->ev_src + (size_t)b * j->E_max, n, j->DT, j->N, i, tmp,
+                    qa, qk, qs);
+        or_neuron_result r = simulate_neuron(j->p, qa, qs, n, j->WT, j->N, i, j->out_t + o, j->out_i + o,
+                                             j->out_k + o);
+        j->out_n[item] = r.n_spikes;
+        j->capped[item] = r.capped;
+        j->tie_t[item] = r.tie_t;
+        j->min_gap[item] = r.min_gap;
+    }
+    free(tmp); free(qa); free(qk); free(qs);
+    return NULL;
+}
+
+/* Forward of a layer with delays DT [C_in][N] (d_ij at DT[j*N + i]);
+ * outputs as or_forward, out_k counting events of the neuron's queue. */
+int or_forward_delayed(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
+                       const float* WT, const float* DT, int C_in, int N, const or_params* p, int nthreads,
+                       double* out_t, double* out_i, int32_t* out_k, int32_t* out_n, int32_t* capped,
+                       double* tie_t, double* min_gap)
+{
+    if (!(p->tau_mem > p->tau_syn && p->tau_syn > 0.0) || !(p->v_reset < p->v_th) || p->s_max < 1)
+        return -1;
+    if (nthreads < 1) nthreads = 1;
+    dly_fwd_job* jobs = (dly_fwd_job*)calloc((size_t)nthreads, sizeof(dly_fwd_job));
+    if (!jobs) return -2;
+    for (int t = 0; t < nthreads; ++t) {
+        dly_fwd_job j = {p, ev_t, ev_src, ev_n, B, E_max, WT, DT, C_in, N,
+                         out_t, out_i, out_k, out_n, capped, tie_t, min_gap, t, nthreads};
+        jobs[t] = j;
+    }
+    int rc = run_threads(dly_fwd_worker, jobs, sizeof(dly_fwd_job), nthreads);
+    free(jobs);
+    return rc;
+}
+
+typedef struct {
+    const or_params* p;
+    const float* ev_t; const int32_t* ev_src; const int32_t* ev_n;
+    int B, E_max; const float* WT; const float* DT; int C_in, N;
+    const double* out_t; const double* out_i; const int32_t* out_k; const int32_t* out_n;
+    const double* grad_out_t;
+    double* gW_part;   /* [nthreads][C_in][N] */
+    double* gD_part;   /* [nthreads][C_in][N] */
+    double* gT_part;   /* [nthreads][B][E_max] */
+    int tid, nthreads;
+} dly_bwd_job;
+
+static void* dly_bwd_worker(void* arg)
+{
+    dly_bwd_job* j = (dly_bwd_job*)arg;
+    const or_params* p = j->p;
+    const double tm = p->tau_mem, ts = p->tau_syn, ka = kappa(p);
+    const int smax = p->s_max;
+    size_t E = (size_t)(j->E_max > 0 ? j->E_max : 1);
+    double* mu = (double*)malloc(sizeof(double) * (size_t)smax);
+    or_arrival* tmp = (or_arrival*)malloc(sizeof(or_arrival) * E);
+    float* qa = (float*)malloc(sizeof(float) * E);
+    int32_t* qk = (int32_t*)malloc(sizeof(int32_t) * E);
+    int32_t* qs = (int32_t*)malloc(sizeof(int32_t) * E);
+    size_t wsz = (size_t)j->C_in * (size_t)j->N;
+    double* gW = j->gW_part + (size_t)j->tid * wsz;
+    double* gD = j->gD_part + (size_t)j->tid * wsz;
+    double* gT = j->gT_part + (size_t)j->tid * (size_t)j->B * (size_t)j->E_max;
+    size_t total = (size_t)j->B * (size_t)j->N;
+    for (size_t item = (size_t)j->tid; item < total; item += (size_t)j->nthreads) {
+        int b = (int)(item / (size_t)j->N), i = (int)(item % (size_t)j->N);
+        int ns = j->out_n[item];
+        if (ns <= 0) continue;
+        const double* ts_ = j->out_t + item * (size_t)smax;
+        const double* is_ = j->out_i + item * (size_t)smax;
+        const int32_t* ks_ = j->out_k + item * (size_t)smax;
+        const double* g = j->grad_out_t + item * (size_t)smax;
+        /* the adjoints of the spikes, as in bwd_worker */
+        for (int s = ns - 1; s >= 0; --s) {
+            double lam = g[s];
+            for (int s2 = s + 1; s2 < ns; ++s2)
+                lam -= (p->v_th - p->v_reset) / tm * mu[s2] * exp(-(ts_[s2] - ts_[s]) / tm);
+            double vp = dvdt(p, p->v_th, is_[s]);
+            if (vp < p->solver_reg) vp = p->solver_reg;
+            mu[s] = -lam / vp;
+        }
+        int n = j->ev_n[b];
+        build_queue(j->ev_t + (size_t)b * j->E_max, j->ev_src + (size_t)b * j->E_max, n, j->DT, j->N, i, tmp,
+                    qa, qk, qs);
+        /* each queue event before a spike: dF_s/dw = K(t_s - a_r),
+         * dF_s/da_r = -w K'(t_s - a_r) */
+        for (int r = 0; r < n; ++r) {
+            if (r >= ks_[ns - 1]) break;
+            double ar = (double)qa[r];
+            double a = 0.0, ad = 0.0;
+            for (int s = 0; s < ns; ++s) {
+                if (r >= ks_[s]) continue;
+                double u = ts_[s] - ar;
+                if (u < 0.0) u = 0.0;
+                double em = exp(-u / tm), es2 = exp(-u / ts);
+                a += mu[s] * ka * (em - es2);
+                ad += mu[s] * ka * (-em / tm + es2 / ts);
+            }
+            size_t wi = (size_t)qs[r] * (size_t)j->N + (size_t)i;
+            double w = (double)j->WT[wi];
+            gW[wi] += a;
+            gD[wi] += -w * ad;
+            gT[(size_t)b * j->E_max + qk[r]] += -w * ad;
+        }
+    }
+    free(mu); free(tmp); free(qa); free(qk); free(qs);
+    return NULL;
+}
+
+/* Backward of a layer with delays: grad_WT, grad_DT [C_in][N] and
+ * grad_ev_t [B][E_max] overwritten, from the delayed forward's outputs. */
+int or_backward_delayed(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
+                        const float* WT, const float* DT, int C_in, int N, const or_params* p, int nthreads,
+                        const double* out_t, const double* out_i, const int32_t* out_k, const int32_t* out_n,
+                        const double* grad_out_t, double* grad_WT, double* grad_DT, double* grad_ev_t)
+{
+    if (nthreads < 1) nthreads = 1;
+    size_t wsz = (size_t)C_in * (size_t)N, tsz = (size_t)B * (size_t)E_max;
+    double* gW_part = (double*)calloc(wsz * (size_t)nthreads, sizeof(double));
+    double* gD_part = (double*)calloc(wsz * (size_t)nthreads, sizeof(double));
+    double* gT_part = (double*)calloc(tsz * (size_t)nthreads + 1, sizeof(double));
+    dly_bwd_job* jobs = (dly_bwd_job*)calloc((size_t)nthreads, sizeof(dly_bwd_job));
+    if (!gW_part || !gD_part || !gT_part || !jobs) {
+        free(gW_part); free(gD_part); free(gT_part); free(jobs);
+        return -2;
+    }
+    for (int t = 0; t < nthreads; ++t) {
+        dly_bwd_job j = {p, ev_t, ev_src, ev_n, B, E_max, WT, DT, C_in, N, out_t, out_i, out_k, out_n, grad_out_t,
+                         gW_part, gD_part, gT_part, t, nthreads};
+        jobs[t] = j;
+    }
+    run_threads(dly_bwd_worker, jobs, sizeof(dly_bwd_job), nthreads);
+    for (size_t x = 0; x < wsz; ++x) {
+        double s = 0.0, sd = 0.0;
+        for (int t = 0; t < nthreads; ++t) {
+            s += gW_part[(size_t)t * wsz + x];
+            sd += gD_part[(size_t)t * wsz + x];
+        }
+        grad_WT[x] = s;
+        grad_DT[x] = sd;
+    }
+    for (size_t x = 0; x < tsz; ++x) {
+        double s = 0.0;
+        for (int t = 0; t < nthreads; ++t) s += gT_part[(size_t)t * tsz + x];
+        grad_ev_t[x] = s;
+    }
+    free(gW_part); free(gD_part); free(gT_part); free(jobs);
+    return 0;
+}

@@ -239,3 +239,11 @@ def random_small(seed: int, B: int, C: int, N: int, n_events: int, T: float, gai
         times.append(re.random(n) * T)
         srcs.append(re.integers(0, C, size=n))
     return Workload(f"small_s{seed}", pack_events(times, srcs), [Layer(WT)], T=T)
+
+
+def uniform_delays(seed: int, C_in: int, N: int, d_max: float = 0.1) -> np.ndarray:
+    """Synaptic delays d_ij ~ U[0, d_max) s as float32 [C_in, N] (the W^T
+    layout), the initialisation of App. E.5 (delay initialisation multiplier
+    0.1 s).  Drawn from the spare stream of the seed."""
+    rs = _rngs(seed)[3]
+    return (rs.random((C_in, N)) * d_max).astype(np.float32)
