@@ -225,6 +225,39 @@ def chunk_study(torch, lif, d, ev, WT, steps, warmup, seq_ms):
     return out
 
 
+def delay_study(torch, lif, d, ev, WT, steps, warmup, seq_steps):
+    """The layer with synaptic delays on the headline workload, delays drawn
+    U[0, 0.1) s (the paper's initialisation): queue build, forward (one wave
+    per neuron on its own queue), the sequential loop on the same queues, and
+    the backward (weights, delays, input times)."""
+    import workloads as W
+    C, N = WT.shape
+    DT = W.uniform_delays(2, C, N)
+    dt, ds, dn, dW, dD = d(ev.ev_t), d(ev.ev_src), d(ev.ev_n), d(WT), d(DT)
+    P = lif.Params(s_max=64)
+    qws = torch.empty(lif.lif_delay_queues_workspace_size(ev.B, ev.E_max, N), dtype=torch.uint8, device=dt.device)
+    q = lif.delay_queues(dt, ds, dn, dD, ws=qws)
+    q_ms, q_ev = time_steps(torch, lambda: lif.delay_queues(dt, ds, dn, dD, ws=qws), steps, warmup)
+    fwd = lambda: lif.forward_delayed(q, ds, dn, dW, P)
+    o = fwd()
+    torch.cuda.synchronize()
+    f_ms, f_ev = time_steps(torch, fwd, steps, warmup)
+    s_ms, _ = time_steps(torch, lambda: lif.forward_delayed(q, ds, dn, dW, P, sequential=True), seq_steps, 1)
+    g = torch.randn(o.out_t.shape, device=dt.device) * torch.isfinite(o.out_t)
+    bws = torch.empty(lif.lif_layer_backward_delayed_workspace_size(ev.B, ev.E_max, C, N, P.c()), dtype=torch.uint8,
+                      device=dt.device)
+    b_ms, b_ev = time_steps(torch, lambda: lif.backward_delayed(q, ds, dn, dW, o, g, P, ws=bws), steps, warmup)
+    ne = int(ev.ev_n.sum()) * N
+    spikes = int(o.out_n.sum().item())
+    log(f"[bench] delays: queues {q_ms * 1e3:.1f} us, forward {f_ms * 1e3:.1f} us ({ne / (f_ms * 1e-3):.3e} "
+        f"neuron-events/s), sequential {s_ms:.3f} ms ({s_ms / f_ms:.1f}x), backward {b_ms * 1e3:.1f} us, "
+        f"{spikes} spikes")
+    return {"workload": "700->256, B=32, ~5k events, delays U[0, 0.1) s: per-neuron queues, forward, backward",
+            "queues_ms": q_ms, "queues_event_ms": stats_ms(q_ev), "forward_ms": f_ms, "forward_event_ms": stats_ms(f_ev),
+            "neuron_events_per_s": ne / (f_ms * 1e-3), "sequential_ms": s_ms, "speedup_vs_sequential": s_ms / f_ms,
+            "backward_ms": b_ms, "backward_event_ms": stats_ms(b_ev), "spikes": spikes}
+
+
 def cpu_oracle(ev, WT, nthreads, seconds, n_samples, n_neurons):
     """The float64 oracle on a bounded sample of a workload (the first
     n_samples samples and n_neurons neurons), repeated for about `seconds`;
@@ -379,6 +412,7 @@ def main():
                                                   c5.events, W1d, lif.Params(s_max=64), st, wu, 1, backward=True)
         extras["train_step_c3"] = train_step(torch, lif, d, c3, st, wu)
         extras["chunk_mode_c2"] = chunk_study(torch, lif, d, ev, WT, st, wu, seq_ms)
+        extras["delays_c2"] = delay_study(torch, lif, d, ev, WT, st, wu, 1)
         del c3, c4, c5, W1d
 
     # ---- float64 CPU oracle on the host cores (bounded samples)

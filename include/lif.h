@@ -84,6 +84,8 @@ typedef struct ihipStream_t* lif_stream_t;
 #define LIF_WARN_BAD_COUNT  32  /* LIF_VALIDATE: ev_n[b] outside [0, E_max]  */
 #define LIF_WARN_INTERNAL   64  /* internal error: a cross-workgroup wait gave
                                    up (results are not valid)                */
+#define LIF_WARN_BAD_DELAY 128  /* lif_delay_queues: a delay is negative or
+                                   not finite (queue order unspecified)      */
 
 typedef struct lif_params {
     double   tau_mem;    /* tau_m (s); must exceed tau_syn (paper: 0.02)        */
@@ -194,6 +196,65 @@ int lif_layer_forward_chunked(const float* ev_t, const int32_t* ev_src, const in
                               const float* WT, int C_in, int N_out, const lif_params* p, int K, int C,
                               float* out_t, int32_t* out_n, float* out_i, int32_t* out_k, int32_t* consumed,
                               int32_t* processed, int32_t* status, lif_stream_t stream);
+
+/* A layer with learnable synaptic delays (Sec. 3.1 Eq. spike_input: a spike
+ * of input channel j at t_k reaches neuron i at t_k + d_ij; Appendix E.2:
+ * a sorted event queue per neuron).  Three calls: the queues, then the
+ * forward and the backward on them.
+ *
+ * lif_delay_queues: neuron i's queue of sample b lists the sample's events
+ * ordered by (arrival, k), with the arrival the float32 sum
+ * a = t_k + DT[src_k * N_out + i] (DT: delays d_ij >= 0 in seconds, W^T
+ * layout [C_in][N_out]).
+ *   q_t  float [B][N_out][E_max]  arrival time of each queue entry
+ *   q_k  int32 [B][N_out][E_max]  the sample's event index of each entry
+ * Entries past ev_n[b] are not written.  status (nullable) int32
+ * [LIF_STATUS_WORDS]: reset, then LIF_ST_EVENTS and LIF_WARN_BAD_DELAY in
+ * LIF_ST_FLAGS when some delay is negative or not finite (the queues are
+ * then in bounds, their order unspecified).  ws: at least
+ * lif_delay_queues_workspace_size(B, E_max, N_out) bytes (8 per queue entry).
+ * Errors: LIF_ERR_ARG, LIF_ERR_SIZE (B * N_out >= 2^31), LIF_ERR_WORKSPACE. */
+size_t lif_delay_queues_workspace_size(int B, int E_max, int N_out);
+int lif_delay_queues(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
+                     const float* DT, int C_in, int N_out, float* q_t, int32_t* q_k, int32_t* status,
+                     void* ws, size_t ws_bytes, lif_stream_t stream);
+
+/* Forward of the delayed layer on the queues of lif_delay_queues (the
+ * sample's ev_src/ev_n with them): every neuron runs the interval rule and
+ * spike solve of the layer on its own queue (the chunked walk of
+ * lif_layer_forward_chunked with K = 128 and no budget: the queue is
+ * consumed unless the neuron stops at s_max).  Outputs as
+ * lif_layer_forward; out_k counts events of the neuron's own queue.  Status
+ * words as lif_layer_forward_chunked.  No workspace. */
+int lif_layer_forward_delayed(const float* q_t, const int32_t* q_k, const int32_t* ev_src, const int32_t* ev_n,
+                              int B, int E_max, const float* WT, int C_in, int N_out, const lif_params* p,
+                              float* out_t, int32_t* out_n, float* out_i, int32_t* out_k, int32_t* status,
+                              lif_stream_t stream);
+
+/* The sequential baseline of the delayed layer (Appendix E.3): one thread
+ * per (sample, neuron) takes its queue one event at a time with the same
+ * interval rule and spike solve.  Same arguments and outputs as
+ * lif_layer_forward_delayed; status words as lif_layer_forward_sequential. */
+int lif_layer_forward_delayed_sequential(const float* q_t, const int32_t* q_k, const int32_t* ev_src,
+                                         const int32_t* ev_n, int B, int E_max, const float* WT, int C_in,
+                                         int N_out, const lif_params* p, float* out_t, int32_t* out_n,
+                                         float* out_i, int32_t* out_k, int32_t* status, lif_stream_t stream);
+
+/* Backward of the delayed layer (Appendix D.3 on each neuron's queue): for
+ * L = sum grad_out_t * out_t, from the delayed forward's outputs,
+ *   grad_WT    float [C_in][N_out]  dL/dw_ij, overwritten
+ *   grad_DT    float [C_in][N_out]  dL/dd_ij, overwritten (nullable)
+ *   grad_ev_t  float [B][E_max]     dL/dt_k summed over the neurons,
+ *                                   overwritten (nullable; 0 past ev_n[b])
+ * Bitwise reproducible (64-bit fixed-point sums).  ws: at least
+ * lif_layer_backward_delayed_workspace_size(...) bytes.  Errors as
+ * lif_layer_backward. */
+size_t lif_layer_backward_delayed_workspace_size(int B, int E_max, int C_in, int N_out, const lif_params* p);
+int lif_layer_backward_delayed(const float* q_t, const int32_t* q_k, const int32_t* ev_src, const int32_t* ev_n,
+                               int B, int E_max, const float* WT, int C_in, int N_out, const lif_params* p,
+                               const float* out_t, const int32_t* out_n, const float* out_i,
+                               const int32_t* out_k, const float* grad_out_t, float* grad_WT, float* grad_DT,
+                               float* grad_ev_t, void* ws, size_t ws_bytes, lif_stream_t stream);
 
 /* --------------------------------------------------------------------- */
 /* Backward pass (paper Appendix D.3, Eq. ift_vjp, chained through the     */

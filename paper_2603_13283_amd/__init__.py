@@ -40,6 +40,7 @@ LIF_STATUS_WORDS = 8
 ST_FLAGS, ST_CAPPED, ST_SPIKES, ST_CAND_BLOCKS, ST_WALKED_BLOCKS, ST_ROOT_SOLVES, ST_EVENTS, ST_POOL_FALLBACK = range(8)
 WARN_SPIKE_CAP, WARN_UNSORTED, WARN_BAD_SOURCE, WARN_NONFINITE, WARN_MERGE_FULL, WARN_BAD_COUNT = 1, 2, 4, 8, 16, 32
 WARN_INTERNAL = 64
+WARN_BAD_DELAY = 128
 LIF_MERGE_MAX = 16384
 
 EXPORTED = ["lif_version", "lif_layer_forward_workspace_size", "lif_layer_forward",
@@ -48,7 +49,10 @@ EXPORTED = ["lif_version", "lif_layer_forward_workspace_size", "lif_layer_forwar
             "lif_layer_backward_workspace_size", "lif_layer_backward",
             "lif_merge_workspace_size", "lif_merge_spikes", "lif_first_spike_ce", "lif_merge_grad",
             "lif_li_readout_workspace_size", "lif_li_readout", "lif_adam_step", "lif_spike_count_reg_workspace_size",
-            "lif_spike_count_reg", "lif_timer_enable", "lif_timer_read"]
+            "lif_spike_count_reg", "lif_delay_queues_workspace_size", "lif_delay_queues",
+            "lif_layer_forward_delayed", "lif_layer_forward_delayed_sequential",
+            "lif_layer_backward_delayed_workspace_size", "lif_layer_backward_delayed",
+            "lif_timer_enable", "lif_timer_read"]
 LIF_LI_MAX_CLASSES = 64
 
 
@@ -172,6 +176,19 @@ def load(path: Optional[str] = None):
                                         _P, _P, _SZ, _P]
     lib.lif_adam_step.restype = _I
     lib.lif_adam_step.argtypes = [_P, _P, _P, _P, _SZ, ctypes.POINTER(lif_adam_params), _I, _P]
+    lib.lif_delay_queues_workspace_size.restype = _SZ
+    lib.lif_delay_queues_workspace_size.argtypes = [_I, _I, _I]
+    lib.lif_delay_queues.restype = _I
+    lib.lif_delay_queues.argtypes = [_P, _P, _P, _I, _I, _P, _I, _I, _P, _P, _P, _P, _SZ, _P]
+    for name in ("lif_layer_forward_delayed", "lif_layer_forward_delayed_sequential"):
+        f = getattr(lib, name)
+        f.restype = _I
+        f.argtypes = [_P, _P, _P, _P, _I, _I, _P, _I, _I, _PP, _P, _P, _P, _P, _P, _P]
+    lib.lif_layer_backward_delayed_workspace_size.restype = _SZ
+    lib.lif_layer_backward_delayed_workspace_size.argtypes = [_I, _I, _I, _I, _PP]
+    lib.lif_layer_backward_delayed.restype = _I
+    lib.lif_layer_backward_delayed.argtypes = [_P, _P, _P, _P, _I, _I, _P, _I, _I, _PP, _P, _P, _P, _P, _P, _P, _P,
+                                               _P, _P, _SZ, _P]
     lib.lif_timer_enable.restype = None
     lib.lif_timer_enable.argtypes = [_I]
     lib.lif_timer_read.restype = _I
@@ -255,6 +272,30 @@ def lif_adam_step(*args) -> int:
 
 def lif_first_spike_ce(*args) -> int:
     return load().lif_first_spike_ce(*args)
+
+
+def lif_delay_queues_workspace_size(B, E_max, N_out) -> int:
+    return load().lif_delay_queues_workspace_size(B, E_max, N_out)
+
+
+def lif_delay_queues(*args) -> int:
+    return load().lif_delay_queues(*args)
+
+
+def lif_layer_forward_delayed(*args) -> int:
+    return load().lif_layer_forward_delayed(*args)
+
+
+def lif_layer_forward_delayed_sequential(*args) -> int:
+    return load().lif_layer_forward_delayed_sequential(*args)
+
+
+def lif_layer_backward_delayed_workspace_size(B, E_max, C_in, N_out, p: lif_params) -> int:
+    return load().lif_layer_backward_delayed_workspace_size(B, E_max, C_in, N_out, ctypes.byref(p))
+
+
+def lif_layer_backward_delayed(*args) -> int:
+    return load().lif_layer_backward_delayed(*args)
 
 
 def lif_timer_enable(on: bool) -> None:
@@ -479,3 +520,79 @@ def forward_chunked(ev_t, ev_src, ev_n, WT, K: int = 128, C: int = 0, params: Pa
                                    _stream(stream))
     _check("lif_layer_forward_chunked", rc)
     return out, consumed, processed
+
+
+@dataclass
+class DelayQueues:
+    q_t: "object"       # float32 [B, N, E_max]: arrival times, each neuron's queue in order
+    q_k: "object"       # int32 [B, N, E_max]: the sample's event index of each entry
+    status: "object"    # int32 [LIF_STATUS_WORDS]
+
+
+def delay_queues(ev_t, ev_src, ev_n, DT, stream=None, ws=None) -> DelayQueues:
+    """Run lif_delay_queues: each neuron's queue of arrivals t_k + DT[src_k, i]."""
+    torch = _torch()
+    B, E, C, N = _dev_inputs(ev_t, ev_src, ev_n, DT)
+    dev = ev_t.device
+    q = DelayQueues(torch.empty((B, N, E), dtype=torch.float32, device=dev),
+                    torch.empty((B, N, E), dtype=torch.int32, device=dev),
+                    torch.empty(LIF_STATUS_WORDS, dtype=torch.int32, device=dev))
+    need = lif_delay_queues_workspace_size(B, E, N)
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    rc = lif_delay_queues(_ptr(ev_t), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(DT), C, N, _ptr(q.q_t), _ptr(q.q_k),
+                          _ptr(q.status), _ptr(ws), ws.numel(), _stream(stream))
+    _check("lif_delay_queues", rc)
+    return q
+
+
+def _queue_inputs(q: DelayQueues, ev_src, ev_n, WT):
+    torch = _torch()
+    B, E, C, N = _dev_inputs(q.q_t.new_empty(ev_src.shape), ev_src, ev_n, WT)
+    for name, t, dt in (("q_t", q.q_t, torch.float32), ("q_k", q.q_k, torch.int32)):
+        if t.dtype != dt or not t.is_cuda or not t.is_contiguous() or tuple(t.shape) != (B, N, E):
+            raise ValueError(f"{name} must be a contiguous {dt} CUDA tensor [B, N_out, E_max]")
+    return B, E, C, N
+
+
+def forward_delayed(q: DelayQueues, ev_src, ev_n, WT, params: Params = Params(), sequential: bool = False,
+                    stream=None) -> ForwardOut:
+    """Run lif_layer_forward_delayed (or its sequential baseline) on the
+    queues of delay_queues."""
+    torch = _torch()
+    B, E, C, N = _queue_inputs(q, ev_src, ev_n, WT)
+    dev = WT.device
+    p = params.c()
+    out = ForwardOut(torch.empty((B, N, params.s_max), dtype=torch.float32, device=dev),
+                     torch.empty((B, N), dtype=torch.int32, device=dev),
+                     torch.empty((B, N, params.s_max), dtype=torch.float32, device=dev),
+                     torch.empty(LIF_STATUS_WORDS, dtype=torch.int32, device=dev),
+                     torch.empty((B, N, params.s_max), dtype=torch.int32, device=dev))
+    fn = lif_layer_forward_delayed_sequential if sequential else lif_layer_forward_delayed
+    rc = fn(_ptr(q.q_t), _ptr(q.q_k), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(WT), C, N, ctypes.byref(p),
+            _ptr(out.out_t), _ptr(out.out_n), _ptr(out.out_i), _ptr(out.out_k), _ptr(out.status), _stream(stream))
+    _check(fn.__name__, rc)
+    return out
+
+
+def backward_delayed(q: DelayQueues, ev_src, ev_n, WT, fwd: ForwardOut, grad_out_t, params: Params = Params(),
+                     stream=None, want_delay_grad: bool = True, want_time_grad: bool = True, ws=None):
+    """Run lif_layer_backward_delayed; returns (grad_WT, grad_DT or None,
+    grad_ev_t or None)."""
+    torch = _torch()
+    B, E, C, N = _queue_inputs(q, ev_src, ev_n, WT)
+    dev = WT.device
+    p = params.c()
+    gW = torch.empty((C, N), dtype=torch.float32, device=dev)
+    gD = torch.empty((C, N), dtype=torch.float32, device=dev) if want_delay_grad else None
+    gT = torch.empty((B, E), dtype=torch.float32, device=dev) if want_time_grad else None
+    need = lif_layer_backward_delayed_workspace_size(B, E, C, N, p)
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    g = grad_out_t.contiguous().to(torch.float32)
+    rc = lif_layer_backward_delayed(_ptr(q.q_t), _ptr(q.q_k), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(WT), C, N,
+                                    ctypes.byref(p), _ptr(fwd.out_t), _ptr(fwd.out_n), _ptr(fwd.out_i),
+                                    _ptr(fwd.out_k), _ptr(g), _ptr(gW), _ptr(gD), _ptr(gT), _ptr(ws), ws.numel(),
+                                    _stream(stream))
+    _check("lif_layer_backward_delayed", rc)
+    return gW, gD, gT

@@ -105,25 +105,11 @@ __global__ __launch_bounds__(256) void k_bwd_setup(const float* __restrict__ ev_
         dec[idx] = d;
     }
     const size_t nn = (size_t)B * (size_t)N;
-    const double jump = (m.th - m.vr) * m.inv_tm;
     for (size_t idx = gtid; idx < nn; idx += gs) {
         const int ns = min(out_n[idx], m.s_max);
-        const float* ts = out_t + idx * (size_t)m.s_max;
-        const float* is = out_i + idx * (size_t)m.s_max;
-        const float* g = grad_out_t + idx * (size_t)m.s_max;
-        double* mo = mu + idx * (size_t)m.s_max;
-        double Q = 0.0, mu_next = 0.0, asum = 0.0;
-        for (int s = ns - 1; s >= 0; --s) {
-            if (s + 1 < ns) Q = (Q + mu_next) * exp(-((double)ts[s + 1] - (double)ts[s]) * m.inv_tm);
-            const double lam = (double)g[s] - jump * Q;
-            const double vp = fmax(((double)is[s] - m.th) * m.inv_tm, m.reg);
-            const double mu_s = vp > 0.0 ? -lam / vp : 0.0;
-            mo[s] = mu_s;
-            mu_next = mu_s;
-            asum += fabs(mu_s);
-        }
-        klast[idx] = ns > 0 ? out_k[idx * (size_t)m.s_max + ns - 1] : 0;
-        musum[idx] = asum;
+        const size_t o = idx * (size_t)m.s_max;
+        musum[idx] = spike_adjoints(m, ns, out_t + o, out_i + o, grad_out_t + o, mu + o);
+        klast[idx] = ns > 0 ? out_k[o + ns - 1] : 0;
     }
 }
 

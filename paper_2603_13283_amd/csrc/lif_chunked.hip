@@ -21,6 +21,10 @@
 //     last event also tests the interval after it, up to t_end.
 // At most C iterations run per neuron and at most s_max spikes are kept; the
 // neuron's consumed and processed event counts give the work retention.
+// The same walk takes the per-neuron queues of a layer with synaptic delays
+// (QUEUE: neuron i's arrival times and the sample's event index of each
+// entry, built by lif_delay_queues); out_k then counts events of the
+// neuron's own queue.
 #include "lif_common.hpp"
 #include "lif_host.hpp"
 
@@ -76,10 +80,11 @@ struct LaneMap {
     double aU, bU, aJ, bJ;   // U_out = aU U_in + bU, J_out = aJ J_in + bJ
 };
 
-template <int M>
+template <int M, bool QUEUE>
 __global__ __launch_bounds__(kWave * kChunkWaves) void k_chunked(
-    const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int B,
-    int E_max, const float* __restrict__ WT, int C_in, int N, Model m, int C_budget, float* __restrict__ out_t,
+    const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n,
+    const int32_t* __restrict__ q_k, int B, int E_max, const float* __restrict__ WT, int C_in, int N, Model m,
+    int C_budget, float* __restrict__ out_t,
     int32_t* __restrict__ out_n, float* __restrict__ out_i, int32_t* __restrict__ out_k,
     int32_t* __restrict__ consumed, int32_t* __restrict__ processed, int32_t* __restrict__ status)
 {
@@ -89,8 +94,10 @@ __global__ __launch_bounds__(kWave * kChunkWaves) void k_chunked(
     if (item >= (size_t)B * N) return;
     const int b = (int)(item / (size_t)N), n = (int)(item % (size_t)N);
     const int nb = clamp_count(ev_n[b], E_max);
-    const float* tt = ev_t + (size_t)b * E_max;
+    // the neuron's queue: the sample's events, or (QUEUE) its own arrivals
+    const float* tt = ev_t + (QUEUE ? item : (size_t)b) * (size_t)E_max;
     const int32_t* src = ev_src + (size_t)b * E_max;
+    const int32_t* qk = QUEUE ? q_k + item * (size_t)E_max : nullptr;
     float* st = out_t + item * (size_t)m.s_max;
     float* si = out_i ? out_i + item * (size_t)m.s_max : nullptr;
     int32_t* sk = out_k ? out_k + item * (size_t)m.s_max : nullptr;
@@ -111,7 +118,8 @@ __global__ __launch_bounds__(kWave * kChunkWaves) void k_chunked(
             const int e = k + lane * M + j;
             valid[j] = e < end;
             te[j] = valid[j] ? (double)tt[e] : 0.0;
-            w[j] = valid[j] ? WT[(size_t)clamp_src(src[e], C_in) * (size_t)N + n] : 0.0f;
+            const int se = QUEUE ? min(max(valid[j] ? qk[e] : 0, 0), max(nb - 1, 0)) : e;
+            w[j] = valid[j] ? WT[(size_t)clamp_src(src[se], C_in) * (size_t)N + n] : 0.0f;
         }
         // the time before each event: the previous event's, t_cur for the
         // chunk's first
@@ -264,6 +272,36 @@ __global__ void k_chunked_status_reset(int32_t* __restrict__ status)
     if (threadIdx.x < LIF_STATUS_WORDS) status[threadIdx.x] = 0;
 }
 
+int launch_chunked_walk(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, const int32_t* q_k, int B,
+                        int E_max, const float* WT, int C_in, int N, const Model& m, int K, int C, float* out_t,
+                        int32_t* out_n, float* out_i, int32_t* out_k, int32_t* consumed, int32_t* processed,
+                        int32_t* status, hipStream_t stream)
+{
+    TIMED_LAUNCH("chunked_reset", k_chunked_status_reset, dim3(1), dim3(kWave), 0, stream, status);
+    const size_t waves = (size_t)B * N;
+    if (waves) {
+        const dim3 grid((unsigned)((waves + kChunkWaves - 1) / kChunkWaves)), block(kWave * kChunkWaves);
+#define LIF_CHUNKED(MM, QQ)                                                                                       \
+    TIMED_LAUNCH("chunked", (k_chunked<MM, QQ>), grid, block, 0, stream, ev_t, ev_src, ev_n, q_k, B, E_max, WT, \
+                 C_in, N, m, C, out_t, out_n, out_i, out_k, consumed, processed, status)
+        if (q_k) {
+            switch (K) {
+            case 64: LIF_CHUNKED(1, true); break;
+            case 128: LIF_CHUNKED(2, true); break;
+            default: LIF_CHUNKED(4, true); break;
+            }
+        } else {
+            switch (K) {
+            case 64: LIF_CHUNKED(1, false); break;
+            case 128: LIF_CHUNKED(2, false); break;
+            default: LIF_CHUNKED(4, false); break;
+            }
+        }
+#undef LIF_CHUNKED
+    }
+    return check_launch();
+}
+
 }  // namespace lif
 
 extern "C" int lif_layer_forward_chunked(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B,
@@ -278,20 +316,6 @@ extern "C" int lif_layer_forward_chunked(const float* ev_t, const int32_t* ev_sr
     if (K != 64 && K != 128 && K != 256) return LIF_ERR_ARG;
     if ((size_t)B * (size_t)N_out >= ((size_t)1 << 31)) return LIF_ERR_SIZE;
     if (C <= 0) C = (E_max + K - 1) / K + p->s_max;    // the paper's budget for an input layer (App. E.2)
-    hipStream_t stream = (hipStream_t)stream_;
-    const Model m = make_model(*p);
-    TIMED_LAUNCH("chunked_reset", k_chunked_status_reset, dim3(1), dim3(kWave), 0, stream, status);
-    const size_t waves = (size_t)B * N_out;
-    if (waves) {
-        const dim3 grid((unsigned)((waves + kChunkWaves - 1) / kChunkWaves)), block(kWave * kChunkWaves);
-        switch (K) {
-        case 64: TIMED_LAUNCH("chunked", k_chunked<1>, grid, block, 0, stream, ev_t, ev_src, ev_n, B, E_max, WT, C_in,
-                              N_out, m, C, out_t, out_n, out_i, out_k, consumed, processed, status); break;
-        case 128: TIMED_LAUNCH("chunked", k_chunked<2>, grid, block, 0, stream, ev_t, ev_src, ev_n, B, E_max, WT,
-                               C_in, N_out, m, C, out_t, out_n, out_i, out_k, consumed, processed, status); break;
-        default: TIMED_LAUNCH("chunked", k_chunked<4>, grid, block, 0, stream, ev_t, ev_src, ev_n, B, E_max, WT,
-                              C_in, N_out, m, C, out_t, out_n, out_i, out_k, consumed, processed, status); break;
-        }
-    }
-    return check_launch();
+    return launch_chunked_walk(ev_t, ev_src, ev_n, nullptr, B, E_max, WT, C_in, N_out, make_model(*p), K, C, out_t,
+                               out_n, out_i, out_k, consumed, processed, status, (hipStream_t)stream_);
 }

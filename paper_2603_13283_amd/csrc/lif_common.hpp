@@ -84,6 +84,30 @@ __device__ __forceinline__ int clamp_src(int s, int C_in) { return min(max(s, 0)
 // Event count of a sample, clamped into [0, E_max].
 __device__ __forceinline__ int clamp_count(int n, int E_max) { return min(max(n, 0), E_max); }
 
+// Adjoints of one neuron's spikes (Appendix D.3, Eq. ift_vjp, chained
+// through the hard resets), last spike first:
+//   lambda_s = g_s - ((V_th - V_reset)/tm) sum_{s'' > s} mu_s'' e^{-(t_s'' - t_s)/tm}
+//   mu_s     = -lambda_s / max(dV/dt(t_s), reg),  dV/dt(t_s) = (I_s - V_th)/tm
+// (mo[s] = mu_s).  Returns sum_s |mu_s|, which bounds the neuron's adjoint
+// sums P^m and P^s.
+__device__ inline double spike_adjoints(const Model& m, int ns, const float* __restrict__ ts,
+                                        const float* __restrict__ is, const float* __restrict__ g,
+                                        double* __restrict__ mo)
+{
+    const double jump = (m.th - m.vr) * m.inv_tm;
+    double Q = 0.0, mu_next = 0.0, asum = 0.0;
+    for (int s = ns - 1; s >= 0; --s) {
+        if (s + 1 < ns) Q = (Q + mu_next) * exp(-((double)ts[s + 1] - (double)ts[s]) * m.inv_tm);
+        const double lam = (double)g[s] - jump * Q;
+        const double vp = fmax(((double)is[s] - m.th) * m.inv_tm, m.reg);
+        const double mu_s = vp > 0.0 ? -lam / vp : 0.0;
+        mo[s] = mu_s;
+        mu_next = mu_s;
+        asum += fabs(mu_s);
+    }
+    return asum;
+}
+
 // Unit kernel K(u) = kappa (e^{-u/tm} - e^{-u/ts}) written with expm1 so that
 // tiny gaps do not cancel.
 __device__ __forceinline__ double unit_kernel(const Model& m, double u, double eA)

@@ -1,0 +1,485 @@
+// lif_delay.hip -- a layer with learnable synaptic delays (Sec. 3.1 Eq.
+// spike_input: a spike of input channel j at t_k reaches neuron i at
+// t_k + d_ij; Appendix E.2: a sorted event queue per neuron; Appendix E.5:
+// delays per layer, initialised uniformly in [0, 0.1] s).
+//
+// Delays break what the main forward is built on: the event maps are no
+// longer shared by the neurons of a sample, since every neuron sees its own
+// event order.  The delayed layer therefore runs per neuron:
+//   k_dly_queue    per (sample, neuron), one workgroup: the neuron's queue,
+//                  the sample's events ordered by (arrival, k) with the
+//                  arrival a = fl32(t_k + d_ij), by a bucket sort: arrivals
+//                  are binned by value into up to kQBins bins (a histogram
+//                  and a prefix sum in LDS), scattered into their bins, and
+//                  each event is then placed at its bin's start plus its
+//                  rank among the bin's keys.  Keys are unique 64-bit words
+//                  (arrival bits, then k), so the result does not depend on
+//                  the order in which the scatter's atomics land.
+//   forward        the chunked walk of lif_chunked.hip on these queues (one
+//                  wave per neuron, K = 128 events per iteration, no budget:
+//                  every event is consumed unless the neuron stops at s_max).
+//   k_dly_adjoint  per (sample, neuron) that fires: the adjoint sums
+//                  P^m_r = sum over the spikes s after queue event r of
+//                  mu_s e^{-(t_s - a_r)/tm} (P^s_r the same with ts), taken
+//                  64 queue events per step from the last one that feeds a
+//                  spike down to the first (lanes = events), from a carry of
+//                  the later spikes plus the spikes that fall inside the step;
+//                  for queue event r with channel j and sample index k:
+//                    dL/dw_ij += kappa (P^m_r - P^s_r)
+//                    dL/dd_ij += w_ij kappa (P^m_r / tm - P^s_r / ts)  (= dL/da_r)
+//                    dL/dt_k  += the same dL/da_r
+//                  added as 64-bit fixed-point integers (exact and order
+//                  free, so the gradients are bitwise reproducible) with
+//                  power-of-two scales that keep every sum below 2^62.
+#include "lif_common.hpp"
+#include "lif_host.hpp"
+
+namespace lif {
+
+constexpr int kQThreads = 256;
+constexpr int kQBins = 8192;            // most bins of one queue's bucket sort (32 KB of LDS)
+
+// Arrival of event k at neuron n: the float32 sum (no contraction is
+// possible in a single add); -0 becomes +0 so that the bits order like the
+// values for every non-negative arrival.
+__device__ __forceinline__ float arrival(const float* __restrict__ tt, const int32_t* __restrict__ src,
+                                         const float* __restrict__ DT, int C_in, int N, int n, int k)
+{
+    const float a = tt[k] + DT[(size_t)clamp_src(src[k], C_in) * (size_t)N + n];
+    return a + 0.0f;
+}
+
+// Bin of an arrival: floor(a * sc) clamped into [0, nbins - 1]; monotone
+// non-decreasing in a (a NaN or negative value goes to bin 0).
+__device__ __forceinline__ int bin_of(float a, float sc, int nbins)
+{
+    const float x = a * sc;
+    if (!(x >= 0.0f)) return 0;
+    return x < (float)(nbins - 1) ? (int)x : nbins - 1;
+}
+
+__global__ __launch_bounds__(kQThreads) void k_dly_queue(const float* __restrict__ ev_t,
+                                                        const int32_t* __restrict__ ev_src,
+                                                        const int32_t* __restrict__ ev_n, int E_max,
+                                                        const float* __restrict__ DT, int C_in, int N,
+                                                        unsigned long long* __restrict__ keys,
+                                                        float* __restrict__ q_t, int32_t* __restrict__ q_k)
+{
+    __shared__ int s_bin[kQBins];
+    __shared__ float s_red[kQThreads / kWave];
+    __shared__ int s_part[kQThreads];
+    const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    const size_t item = blockIdx.x;
+    const int b = (int)(item / (size_t)N), n = (int)(item % (size_t)N);
+    const int nb = clamp_count(ev_n[b], E_max);
+    if (nb == 0) return;
+    const float* tt = ev_t + (size_t)b * E_max;
+    const int32_t* src = ev_src + (size_t)b * E_max;
+    const size_t base = item * (size_t)E_max;
+    // the largest arrival
+    float mx = 0.0f;
+    for (int k = tid; k < nb; k += kQThreads) mx = fmaxf(mx, arrival(tt, src, DT, C_in, N, n, k));
+    for (int off = kWave / 2; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, kWave));
+    if (lane == 0) s_red[wave] = mx;
+    int nbins = 1;
+    while (nbins < nb && nbins < kQBins) nbins <<= 1;
+    for (int j = tid; j < nbins; j += kQThreads) s_bin[j] = 0;
+    __syncthreads();
+    float amax = s_red[0];
+    for (int w = 1; w < kQThreads / kWave; ++w) amax = fmaxf(amax, s_red[w]);
+    const float sc = amax > 0.0f && amax < INFINITY ? (float)nbins / amax : 0.0f;
+    // histogram
+    for (int k = tid; k < nb; k += kQThreads)
+        atomicAdd(&s_bin[bin_of(arrival(tt, src, DT, C_in, N, n, k), sc, nbins)], 1);
+    __syncthreads();
+    // exclusive prefix sum over the bins: each thread a contiguous range
+    const int per = (nbins + kQThreads - 1) / kQThreads;
+    const int j0 = min(tid * per, nbins), j1 = min(j0 + per, nbins);
+    int local = 0;
+    for (int j = j0; j < j1; ++j) local += s_bin[j];
+    s_part[tid] = local;
+    __syncthreads();
+    for (int off = 1; off < kQThreads; off <<= 1) {
+        const int x = tid >= off ? s_part[tid - off] : 0;
+        __syncthreads();
+        s_part[tid] += x;
+        __syncthreads();
+    }
+    int run = s_part[tid] - local;
+    for (int j = j0; j < j1; ++j) {
+        const int c = s_bin[j];
+        s_bin[j] = run;
+        run += c;
+    }
+    __syncthreads();
+    // scatter into the bins; s_bin[j] ends at the end of bin j
+    for (int k = tid; k < nb; k += kQThreads) {
+        const float a = arrival(tt, src, DT, C_in, N, n, k);
+        const int pos = atomicAdd(&s_bin[bin_of(a, sc, nbins)], 1);
+        if (pos < nb) keys[base + pos] = ((unsigned long long)__float_as_uint(a) << 32) | (unsigned)k;
+    }
+    __syncthreads();
+    // each key's place: its bin's start plus its rank among the bin's keys
+    for (int p = tid; p < nb; p += kQThreads) {
+        const unsigned long long key = keys[base + p];
+        const float a = __uint_as_float((unsigned)(key >> 32));
+        const int j = bin_of(a, sc, nbins);
+        const int lo = j > 0 ? s_bin[j - 1] : 0, hi = s_bin[j];
+        int rank = 0;
+        for (int q = lo; q < hi; ++q) rank += keys[base + q] < key;
+        if (lo + rank < nb) {                 // always: bins are recomputed bit for bit
+            q_t[base + lo + rank] = a;
+            q_k[base + lo + rank] = (int32_t)(key & 0xffffffffull);
+        }
+    }
+}
+
+// Status words of the queue build: events of the batch, and
+// LIF_WARN_BAD_DELAY when a delay is negative or not finite.
+__global__ __launch_bounds__(256) void k_dly_check(const float* __restrict__ DT, size_t nD,
+                                                  const int32_t* __restrict__ ev_n, int B, int E_max,
+                                                  int32_t* __restrict__ status)
+{
+    const size_t gtid = (size_t)blockIdx.x * blockDim.x + threadIdx.x, gs = (size_t)gridDim.x * blockDim.x;
+    bool bad = false;
+    for (size_t x = gtid; x < nD; x += gs) bad |= !(DT[x] >= 0.0f && DT[x] < INFINITY);
+    if (__ballot(bad) && threadIdx.x % kWave == 0) atomicOr(&status[LIF_ST_FLAGS], LIF_WARN_BAD_DELAY);
+    if (gtid == 0) {
+        int ev = 0;
+        for (int b = 0; b < B; ++b) ev += clamp_count(ev_n[b], E_max);
+        atomicAdd(&status[LIF_ST_EVENTS], ev);
+    }
+}
+
+__global__ void k_dly_status_reset(int32_t* __restrict__ status)
+{
+    if (threadIdx.x < LIF_STATUS_WORDS) status[threadIdx.x] = 0;
+}
+
+// ---------------------------------------------------------------------------
+// Backward
+// ---------------------------------------------------------------------------
+struct DlyBwdLayout {
+    size_t mu, musum, scale, wmax, gw, gd, gt, total;
+};
+
+static DlyBwdLayout dly_bwd_layout(int B, int E_max, int C_in, int N, int s_max)
+{
+    DlyBwdLayout L{};
+    size_t off = 0;
+    auto take = [&](size_t bytes) { size_t o = off; off += (bytes + 255) & ~(size_t)255; return o; };
+    L.mu = take((size_t)B * N * s_max * sizeof(double));
+    L.musum = take((size_t)B * N * sizeof(double));
+    L.scale = take(4 * sizeof(double));
+    L.wmax = take(sizeof(uint32_t));
+    L.gw = take((size_t)C_in * N * sizeof(long long));
+    L.gd = take((size_t)C_in * N * sizeof(long long));
+    L.gt = take((size_t)B * E_max * sizeof(long long));
+    L.total = off + 256;
+    return L;
+}
+
+// Zeroed accumulators and the spike adjoints of every (sample, neuron).
+__global__ __launch_bounds__(256) void k_dly_setup(size_t nW, size_t nT, long long* __restrict__ gw,
+                                                  long long* __restrict__ gd, long long* __restrict__ gt,
+                                                  uint32_t* __restrict__ wmax, size_t nn, Model m,
+                                                  const float* __restrict__ out_t, const int32_t* __restrict__ out_n,
+                                                  const float* __restrict__ out_i,
+                                                  const float* __restrict__ grad_out_t, double* __restrict__ mu,
+                                                  double* __restrict__ musum)
+{
+    const size_t gtid = (size_t)blockIdx.x * blockDim.x + threadIdx.x, gs = (size_t)gridDim.x * blockDim.x;
+    for (size_t x = gtid; x < nW; x += gs) {
+        gw[x] = 0;
+        gd[x] = 0;
+    }
+    for (size_t x = gtid; x < nT; x += gs) gt[x] = 0;
+    if (gtid == 0) *wmax = 0u;
+    for (size_t idx = gtid; idx < nn; idx += gs) {
+        const int ns = min(out_n[idx], m.s_max);
+        const size_t o = idx * (size_t)m.s_max;
+        musum[idx] = spike_adjoints(m, ns, out_t + o, out_i + o, grad_out_t + o, mu + o);
+    }
+}
+
+// max |w| over W^T: float bits of non-negative values order like the values,
+// so an integer atomicMax gives the (order-free) maximum.
+__global__ __launch_bounds__(256) void k_dly_wmax(const float* __restrict__ WT, size_t nW,
+                                                 uint32_t* __restrict__ wmax)
+{
+    const size_t gtid = (size_t)blockIdx.x * blockDim.x + threadIdx.x, gs = (size_t)gridDim.x * blockDim.x;
+    float mx = 0.0f;
+    for (size_t x = gtid; x < nW; x += gs) mx = fmaxf(mx, fabsf(WT[x]));
+    for (int off = kWave / 2; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, kWave));
+    if (threadIdx.x % kWave == 0) atomicMax(wmax, __float_as_uint(mx));
+}
+
+// Fixed-point scales (one workgroup).  With M = max over neurons of
+// sum_s |mu_s| (a bound of |P^m| and |P^s|, up to the e^{+ulp} of a spike
+// time rounded below an arrival, which the extra bit of headroom covers),
+// a contribution to dL/dw is at most 2 kappa M, one to dL/dd or dL/dt at most
+// |w|max kappa M (1/tm + 1/ts); an element of dL/dW or dL/dD sums at most one
+// per event of the batch, one of dL/dt one per neuron.  scale =
+// 2^(61 - ceil(log2 bound)).
+constexpr int kDlyScaleThreads = 1024;
+
+__global__ __launch_bounds__(kDlyScaleThreads) void k_dly_scale(const double* __restrict__ musum, size_t nn,
+                                                                const int32_t* __restrict__ ev_n, int B, int E_max,
+                                                                int N, Model m, const uint32_t* __restrict__ wmax,
+                                                                double* __restrict__ scale)
+{
+    __shared__ double s_max[kDlyScaleThreads];
+    __shared__ double s_ev[kDlyScaleThreads];
+    double mx = 0.0, ev = 0.0;
+    for (size_t i = threadIdx.x; i < nn; i += kDlyScaleThreads) mx = fmax(mx, musum[i]);
+    for (int b = threadIdx.x; b < B; b += kDlyScaleThreads) ev += (double)clamp_count(ev_n[b], E_max);
+    s_max[threadIdx.x] = mx;
+    s_ev[threadIdx.x] = ev;
+    __syncthreads();
+    for (int off = kDlyScaleThreads / 2; off > 0; off >>= 1) {
+        if ((int)threadIdx.x < off) {
+            s_max[threadIdx.x] = fmax(s_max[threadIdx.x], s_max[threadIdx.x + off]);
+            s_ev[threadIdx.x] += s_ev[threadIdx.x + off];
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        const double M = s_max[0], E = fmax(s_ev[0], 1.0), w = (double)__uint_as_float(*wmax);
+        const double bw = 2.0 * m.kappa * M * E;
+        const double bd = w * m.kappa * M * (m.inv_tm + m.inv_ts) * E;
+        const double bt = w * m.kappa * M * (m.inv_tm + m.inv_ts) * (double)N;
+        const double bounds[3] = {bw, bd, bt};
+        for (int q = 0; q < 3; ++q) {
+            int ex = 0;
+            if (bounds[q] > 0.0 && isfinite(bounds[q])) frexp(bounds[q], &ex);   // bound < 2^ex
+            scale[q] = ldexp(1.0, 61 - ex);
+        }
+    }
+}
+
+constexpr int kDlyWaves = 4;
+
+__device__ __forceinline__ void fx_add(long long* p, double v, double sc)
+{
+    atomicAdd((unsigned long long*)p, (unsigned long long)llrint(v * sc));
+}
+
+__global__ __launch_bounds__(kWave * kDlyWaves) void k_dly_adjoint(
+    const float* __restrict__ q_t, const int32_t* __restrict__ q_k, const int32_t* __restrict__ ev_src,
+    const int32_t* __restrict__ ev_n, int B, int E_max, const float* __restrict__ WT, int C_in, int N, Model m,
+    const float* __restrict__ out_t, const int32_t* __restrict__ out_n, const int32_t* __restrict__ out_k,
+    const double* __restrict__ mu, const double* __restrict__ scale, long long* __restrict__ gw,
+    long long* __restrict__ gd, long long* __restrict__ gt)
+{
+    const int lane = (int)threadIdx.x % kWave;
+    const size_t item = (size_t)blockIdx.x * kDlyWaves + threadIdx.x / kWave;
+    if (item >= (size_t)B * N) return;
+    const int ns = min(out_n[item], m.s_max);
+    if (ns <= 0) return;
+    const int b = (int)(item / (size_t)N), n = (int)(item % (size_t)N);
+    const int nb = clamp_count(ev_n[b], E_max);
+    const size_t so = item * (size_t)m.s_max;
+    const float* st = out_t + so;
+    const int32_t* sk = out_k + so;
+    const double* mo = mu + so;
+    const int klast = min(max(sk[ns - 1], 0), nb);      // queue events 0 .. klast - 1 feed a spike
+    if (klast <= 0) return;
+    const float* qa = q_t + item * (size_t)E_max;
+    const int32_t* qi = q_k + item * (size_t)E_max;
+    const int32_t* src = ev_src + (size_t)b * E_max;
+    const double sW = scale[0], sD = scale[1], sT = scale[2];
+    // the step holding queue event klast - 1, and the carry of the spikes
+    // after it (every spike with out_k = klast), referred to its arrival
+    int r_last = klast - 1;
+    int f = (r_last / kWave) * kWave;
+    double a_ref = (double)qa[r_last];
+    int s_hi = ns;
+    while (s_hi > 0 && sk[s_hi - 1] > r_last) --s_hi;
+    double Cm = 0.0, Cs = 0.0;
+    for (int s = s_hi + lane; s < ns; s += kWave) {
+        const double u = fmax((double)st[s] - a_ref, 0.0);
+        Cm += mo[s] * exp(-u * m.inv_tm);
+        Cs += mo[s] * exp(-u * m.inv_ts);
+    }
+    for (int off = 1; off < kWave; off <<= 1) {
+        Cm += __shfl_xor(Cm, off, kWave);
+        Cs += __shfl_xor(Cs, off, kWave);
+    }
+    for (;;) {
+        // spikes [s_lo, s_hi) have f < out_k <= r_last: after some event of the step
+        int s_lo = s_hi;
+        while (s_lo > 0 && sk[s_lo - 1] > f) --s_lo;
+        const int e = f + lane;
+        if (e <= r_last) {
+            const double a = (double)qa[e];
+            const int k = min(max(qi[e], 0), nb - 1);
+            const int j = clamp_src(src[k], C_in);
+            const double w = (double)WT[(size_t)j * N + n];
+            double Pm = Cm * exp(-(a_ref - a) * m.inv_tm), Ps = Cs * exp(-(a_ref - a) * m.inv_ts);
+            for (int s = s_lo; s < s_hi; ++s) {
+                if (e < sk[s]) {
+                    const double u = fmax((double)st[s] - a, 0.0);
+                    Pm += mo[s] * exp(-u * m.inv_tm);
+                    Ps += mo[s] * exp(-u * m.inv_ts);
+                }
+            }
+            const size_t wi = (size_t)j * N + n;
+            fx_add(&gw[wi], m.kappa * (Pm - Ps), sW);
+            const double ga = w * m.kappa * (Pm * m.inv_tm - Ps * m.inv_ts);
+            if (gd) fx_add(&gd[wi], ga, sD);
+            if (gt) fx_add(&gt[(size_t)b * E_max + k], ga, sT);
+        }
+        if (f == 0) break;
+        // the carry moved to the previous step's last event
+        const double a2 = (double)qa[f - 1];
+        Cm *= exp(-(a_ref - a2) * m.inv_tm);
+        Cs *= exp(-(a_ref - a2) * m.inv_ts);
+        for (int s = s_lo; s < s_hi; ++s) {
+            const double u = fmax((double)st[s] - a2, 0.0);
+            Cm += mo[s] * exp(-u * m.inv_tm);
+            Cs += mo[s] * exp(-u * m.inv_ts);
+        }
+        a_ref = a2;
+        r_last = f - 1;
+        f -= kWave;
+        s_hi = s_lo;
+    }
+}
+
+// Fixed point -> float32 gradients.
+__global__ __launch_bounds__(256) void k_dly_convert(const long long* __restrict__ gw,
+                                                    const long long* __restrict__ gd,
+                                                    const long long* __restrict__ gt,
+                                                    const double* __restrict__ scale, size_t nW, size_t nT,
+                                                    float* __restrict__ grad_WT, float* __restrict__ grad_DT,
+                                                    float* __restrict__ grad_ev_t)
+{
+    const size_t gtid = (size_t)blockIdx.x * blockDim.x + threadIdx.x, gs = (size_t)gridDim.x * blockDim.x;
+    const double iW = 1.0 / scale[0], iD = 1.0 / scale[1], iT = 1.0 / scale[2];
+    for (size_t x = gtid; x < nW; x += gs) {
+        grad_WT[x] = (float)((double)gw[x] * iW);
+        if (grad_DT) grad_DT[x] = (float)((double)gd[x] * iD);
+    }
+    if (grad_ev_t)
+        for (size_t x = gtid; x < nT; x += gs) grad_ev_t[x] = (float)((double)gt[x] * iT);
+}
+
+static unsigned grid_for(size_t work)
+{
+    size_t blocks = (work + 255) / 256;
+    if (blocks > 2048) blocks = 2048;
+    if (blocks < 1) blocks = 1;
+    return (unsigned)blocks;
+}
+
+}  // namespace lif
+
+extern "C" size_t lif_delay_queues_workspace_size(int B, int E_max, int N_out)
+{
+    if (B < 0 || E_max < 0 || N_out < 1) return 0;
+    return (size_t)B * (size_t)N_out * (size_t)E_max * sizeof(unsigned long long) + 256;
+}
+
+extern "C" int lif_delay_queues(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
+                                const float* DT, int C_in, int N_out, float* q_t, int32_t* q_k, int32_t* status,
+                                void* ws, size_t ws_bytes, lif_stream_t stream_)
+{
+    using namespace lif;
+    if (B < 0 || E_max < 0 || C_in < 1 || N_out < 1) return LIF_ERR_ARG;
+    if (B > 0 && E_max > 0 && (!ev_t || !ev_src || !ev_n || !DT || !q_t || !q_k || !ws)) return LIF_ERR_ARG;
+    if ((size_t)B * (size_t)N_out >= ((size_t)1 << 31)) return LIF_ERR_SIZE;
+    if (ws_bytes < lif_delay_queues_workspace_size(B, E_max, N_out)) return LIF_ERR_WORKSPACE;
+    hipStream_t stream = (hipStream_t)stream_;
+    if (status) {
+        TIMED_LAUNCH("dly_status_reset", k_dly_status_reset, dim3(1), dim3(kWave), 0, stream, status);
+        const size_t nD = (size_t)C_in * N_out;
+        TIMED_LAUNCH("dly_check", k_dly_check, dim3(grid_for(nD)), dim3(256), 0, stream, DT, nD, ev_n, B, E_max,
+                     status);
+    }
+    if (B > 0 && E_max > 0) {
+        unsigned long long* keys = (unsigned long long*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
+        TIMED_LAUNCH("dly_queue", k_dly_queue, dim3((unsigned)((size_t)B * N_out)), dim3(kQThreads), 0, stream,
+                     ev_t, ev_src, ev_n, E_max, DT, C_in, N_out, keys, q_t, q_k);
+    }
+    return check_launch();
+}
+
+extern "C" int lif_layer_forward_delayed(const float* q_t, const int32_t* q_k, const int32_t* ev_src,
+                                         const int32_t* ev_n, int B, int E_max, const float* WT, int C_in,
+                                         int N_out, const lif_params* p, float* out_t, int32_t* out_n, float* out_i,
+                                         int32_t* out_k, int32_t* status, lif_stream_t stream_)
+{
+    using namespace lif;
+    int rc = validate_forward_args(q_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, p, out_t, out_n, status);
+    if (rc) return rc;
+    if (B > 0 && E_max > 0 && !q_k) return LIF_ERR_ARG;
+    if ((size_t)B * (size_t)N_out >= ((size_t)1 << 31)) return LIF_ERR_SIZE;
+    // no budget: a neuron stops when its queue is consumed or at s_max spikes
+    return launch_chunked_walk(q_t, ev_src, ev_n, q_k, B, E_max, WT, C_in, N_out, make_model(*p), 128, 0x7fffffff,
+                               out_t, out_n, out_i, out_k, nullptr, nullptr, status, (hipStream_t)stream_);
+}
+
+extern "C" int lif_layer_forward_delayed_sequential(const float* q_t, const int32_t* q_k, const int32_t* ev_src,
+                                                    const int32_t* ev_n, int B, int E_max, const float* WT, int C_in,
+                                                    int N_out, const lif_params* p, float* out_t, int32_t* out_n,
+                                                    float* out_i, int32_t* out_k, int32_t* status,
+                                                    lif_stream_t stream_)
+{
+    using namespace lif;
+    int rc = validate_forward_args(q_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, p, out_t, out_n, status);
+    if (rc) return rc;
+    if (B > 0 && E_max > 0 && !q_k) return LIF_ERR_ARG;
+    if ((size_t)B * (size_t)N_out >= ((size_t)1 << 31)) return LIF_ERR_SIZE;
+    return launch_sequential_queue(q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N_out, make_model(*p), out_t, out_n,
+                                   out_i, out_k, status, (hipStream_t)stream_);
+}
+
+extern "C" size_t lif_layer_backward_delayed_workspace_size(int B, int E_max, int C_in, int N_out,
+                                                            const lif_params* p)
+{
+    if (B < 0 || E_max < 0 || C_in < 1 || N_out < 1 || !p || p->s_max < 1) return 0;
+    return lif::dly_bwd_layout(B, E_max, C_in, N_out, p->s_max).total;
+}
+
+extern "C" int lif_layer_backward_delayed(const float* q_t, const int32_t* q_k, const int32_t* ev_src,
+                                          const int32_t* ev_n, int B, int E_max, const float* WT, int C_in,
+                                          int N_out, const lif_params* p, const float* out_t, const int32_t* out_n,
+                                          const float* out_i, const int32_t* out_k, const float* grad_out_t,
+                                          float* grad_WT, float* grad_DT, float* grad_ev_t, void* ws,
+                                          size_t ws_bytes, lif_stream_t stream_)
+{
+    using namespace lif;
+    if (!p || !WT || !grad_WT || B < 0 || E_max < 0 || C_in < 1 || N_out < 1) return LIF_ERR_ARG;
+    int rc = check_params(p);
+    if (rc) return rc;
+    if (B > 0 && (!ev_n || !out_t || !out_n || !out_i || !out_k || !grad_out_t)) return LIF_ERR_ARG;
+    if (B > 0 && E_max > 0 && (!q_t || !q_k || !ev_src)) return LIF_ERR_ARG;
+    if ((size_t)B * (size_t)N_out >= ((size_t)1 << 31)) return LIF_ERR_SIZE;
+    const DlyBwdLayout L = dly_bwd_layout(B, E_max, C_in, N_out, p->s_max);
+    if (!ws || ws_bytes < L.total) return LIF_ERR_WORKSPACE;
+    hipStream_t stream = (hipStream_t)stream_;
+    const Model m = make_model(*p);
+    char* base = (char*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
+    double* mu = (double*)(base + L.mu);
+    double* musum = (double*)(base + L.musum);
+    double* scale = (double*)(base + L.scale);
+    uint32_t* wmax = (uint32_t*)(base + L.wmax);
+    long long* gw = (long long*)(base + L.gw);
+    long long* gd = (long long*)(base + L.gd);
+    long long* gt = (long long*)(base + L.gt);
+    const size_t nW = (size_t)C_in * N_out, nT = (size_t)B * E_max, nn = (size_t)B * N_out;
+    size_t work = nW > nT ? nW : nT;
+    if (nn > work) work = nn;
+    TIMED_LAUNCH("dly_setup", k_dly_setup, dim3(grid_for(work)), dim3(256), 0, stream, nW, nT, gw, gd, gt, wmax, nn,
+                 m, out_t, out_n, out_i, grad_out_t, mu, musum);
+    TIMED_LAUNCH("dly_wmax", k_dly_wmax, dim3(grid_for(nW)), dim3(256), 0, stream, WT, nW, wmax);
+    TIMED_LAUNCH("dly_scale", k_dly_scale, dim3(1), dim3(kDlyScaleThreads), 0, stream, musum, nn, ev_n, B, E_max,
+                 N_out, m, wmax, scale);
+    if (nn && E_max > 0)
+        TIMED_LAUNCH("dly_adjoint", k_dly_adjoint, dim3((unsigned)((nn + kDlyWaves - 1) / kDlyWaves)),
+                     dim3(kWave * kDlyWaves), 0, stream, q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N_out, m, out_t,
+                     out_n, out_k, mu, scale, gw, grad_DT ? gd : nullptr, grad_ev_t ? gt : nullptr);
+    TIMED_LAUNCH("dly_convert", k_dly_convert, dim3(grid_for(work)), dim3(256), 0, stream, gw, gd, gt, scale, nW, nT,
+                 grad_WT, grad_DT, grad_ev_t);
+    return check_launch();
+}

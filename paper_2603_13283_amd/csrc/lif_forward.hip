@@ -1247,21 +1247,26 @@ static unsigned status_blocks(int B, int N)
 // The state (V, I) is the true one, so each interval starts with deficit 0;
 // spikes inside it raise the deficit and the rest of the interval is
 // re-tested.
+// QUEUE: every neuron has its own queue (a layer with synaptic delays):
+// ev_t holds the arrival times [B][N][E_max], q_k the sample's event index of
+// each entry, and each thread computes its own decays (no shared table).
+template <bool QUEUE>
 __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src,
-                                                   const int32_t* __restrict__ ev_n, int B, int E_max,
-                                                   const float* __restrict__ WT, int C_in, int N, Model m,
-                                                   int E_pad, const Decay* __restrict__ dec, float* __restrict__ out_t,
-                                                   int32_t* __restrict__ out_n, float* __restrict__ out_i,
-                                                   int32_t* __restrict__ out_k)
+                                                   const int32_t* __restrict__ ev_n, const int32_t* __restrict__ q_k,
+                                                   int B, int E_max, const float* __restrict__ WT, int C_in, int N,
+                                                   Model m, int E_pad, const Decay* __restrict__ dec,
+                                                   float* __restrict__ out_t, int32_t* __restrict__ out_n,
+                                                   float* __restrict__ out_i, int32_t* __restrict__ out_k)
 {
     const size_t idx_raw = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     const bool live = idx_raw < (size_t)B * (size_t)N;
     const size_t idx = live ? idx_raw : 0;            // lanes past the end run neuron 0 and write nothing
     int b = (int)(idx / (size_t)N), n = (int)(idx % (size_t)N);
     int nb = clamp_count(ev_n[b], E_max);
-    const float* tt = ev_t + (size_t)b * E_max;
+    const float* tt = ev_t + (QUEUE ? idx : (size_t)b) * (size_t)E_max;
     const int32_t* src = ev_src + (size_t)b * E_max;
-    const Decay* d = dec + (size_t)b * E_pad;
+    const int32_t* qk = QUEUE ? q_k + idx * (size_t)E_max : nullptr;
+    const Decay* d = QUEUE ? nullptr : dec + (size_t)b * E_pad;
     float* st = out_t + idx * (size_t)m.s_max;
     float* si = out_i ? out_i + idx * (size_t)m.s_max : nullptr;
     int32_t* sk = out_k ? out_k + idx * (size_t)m.s_max : nullptr;
@@ -1271,7 +1276,7 @@ __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_
     for (int k = 0; k <= nb && !capped; ++k) {
         double L, A, C, Dd;
         if (k < nb) {
-            Decay e = d[k];
+            const Decay e = QUEUE ? make_decay(m, tt, k) : d[k];
             A = e.A; C = e.C; Dd = e.D;
             L = (double)tt[k] - t_prev;
         } else {
@@ -1310,7 +1315,8 @@ __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_
         }
         V = V1;
         if (k < nb) {
-            I = Dd * I + (double)WT[(size_t)clamp_src(src[k], C_in) * (size_t)N + n];
+            const int se = QUEUE ? min(max(qk[k], 0), nb - 1) : k;
+            I = Dd * I + (double)WT[(size_t)clamp_src(src[se], C_in) * (size_t)N + n];
             t_prev = (double)tt[k];
         }
     }
@@ -1322,6 +1328,25 @@ __global__ __launch_bounds__(64) void k_sequential(const float* __restrict__ ev_
             if (sk) sk[s] = 0;
         }
     }
+}
+
+__global__ void k_status_zero(int32_t* __restrict__ status)
+{
+    if (threadIdx.x < LIF_STATUS_WORDS) status[threadIdx.x] = 0;
+}
+
+int launch_sequential_queue(const float* q_t, const int32_t* q_k, const int32_t* ev_src, const int32_t* ev_n, int B,
+                            int E_max, const float* WT, int C_in, int N, const Model& m, float* out_t, int32_t* out_n,
+                            float* out_i, int32_t* out_k, int32_t* status, hipStream_t stream)
+{
+    const size_t nn = (size_t)B * N;
+    TIMED_LAUNCH("status_zero", k_status_zero, dim3(1), dim3(kWave), 0, stream, status);
+    if (nn)
+        TIMED_LAUNCH("sequential", k_sequential<true>, dim3((unsigned)((nn + 63) / 64)), dim3(64), 0, stream, q_t,
+                     ev_src, ev_n, q_k, B, E_max, WT, C_in, N, m, 0, nullptr, out_t, out_n, out_i, out_k);
+    TIMED_LAUNCH("status", k_status, dim3(status_blocks(B, N)), dim3(kStatusThreads), 0, stream, ev_n, B, E_max, N,
+                 m.s_max, out_n, status);
+    return check_launch();
 }
 
 // ---------------------------------------------------------------------------
@@ -1468,8 +1493,9 @@ int forward_impl(bool sequential, const float* ev_t, const int32_t* ev_src, cons
     }
     if (sequential) {
         if (nn)
-            TIMED_LAUNCH("sequential", k_sequential, dim3((unsigned)((nn + 63) / 64)), dim3(64), 0, stream,
-                         ev_t, ev_src, ev_n, B, E_max, WT, C_in, N, m, L.E_pad, P.dec, out_t, out_n, out_i, out_k);
+            TIMED_LAUNCH("sequential", k_sequential<false>, dim3((unsigned)((nn + 63) / 64)), dim3(64), 0, stream,
+                         ev_t, ev_src, ev_n, nullptr, B, E_max, WT, C_in, N, m, L.E_pad, P.dec, out_t, out_n, out_i,
+                         out_k);
         TIMED_LAUNCH("status", k_status, dim3(status_blocks(B, N)), dim3(kStatusThreads), 0, stream, ev_n, B, E_max, N, m.s_max, out_n,
                      status);
         return check_launch();

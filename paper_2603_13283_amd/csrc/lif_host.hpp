@@ -29,6 +29,20 @@ int validate_forward_args(const float* ev_t, const int32_t* ev_src, const int32_
                           const int32_t* out_n, const int32_t* status);
 int check_launch();
 
+// The sequential baseline (one thread per (sample, neuron), every event in
+// order) on per-neuron queues (lif_forward.hip).
+int launch_sequential_queue(const float* q_t, const int32_t* q_k, const int32_t* ev_src, const int32_t* ev_n, int B,
+                            int E_max, const float* WT, int C_in, int N, const Model& m, float* out_t, int32_t* out_n,
+                            float* out_i, int32_t* out_k, int32_t* status, hipStream_t stream);
+
+// The chunked walk of lif_layer_forward_chunked (lif_chunked.hip), on the
+// sample queues (q_k null) or on per-neuron queues (ev_t = arrival times
+// [B][N][E_max], q_k = the sample's event index of each entry).
+int launch_chunked_walk(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, const int32_t* q_k, int B,
+                        int E_max, const float* WT, int C_in, int N, const Model& m, int K, int C, float* out_t,
+                        int32_t* out_n, float* out_i, int32_t* out_k, int32_t* consumed, int32_t* processed,
+                        int32_t* status, hipStream_t stream);
+
 // Kernel timer (lif_timer_*): a HIP event pair per launch, recorded by the
 // dispatch of the kernel itself (hipExtLaunchKernelGGL), so that the elapsed
 // time is the kernel's own execution.

@@ -189,3 +189,44 @@ def test_spike_count_reg_argument_errors(lib):
     bad = L.Params(tau_mem=0.001).c()
     assert call(8, ctypes.byref(bad)) == L.LIF_ERR_TAU
     assert L.lif_spike_count_reg_workspace_size(2, 10, 4, 8) > 0
+
+
+def test_delay_argument_errors(lib):
+    p = L.Params().c()
+    # queues: ev_t, ev_src, ev_n, B, E_max, DT, C_in, N, q_t, q_k, status, ws, ws_bytes, stream
+    qb = [F, F, F, 2, 10, F, 4, 8, F, F, None, F, 10 ** 9, None]
+
+    def q(i, v):
+        a = list(qb)
+        a[i] = v
+        return L.lif_delay_queues(*a)
+    assert q(5, None) == L.LIF_ERR_ARG              # DT required
+    assert q(9, None) == L.LIF_ERR_ARG              # q_k required
+    assert q(12, 2 * 8 * 10 * 8 - 1) == L.LIF_ERR_WORKSPACE
+    assert L.lif_delay_queues_workspace_size(2, 10, 8) >= 2 * 8 * 10 * 8
+    assert L.lif_delay_queues_workspace_size(-1, 10, 8) == 0
+    # forward: q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N, p, out_t, out_n, out_i, out_k, status, stream
+    fb = [F, F, F, F, 2, 10, F, 4, 8, ctypes.byref(p), F, F, F, F, F, None]
+
+    def f(i, v):
+        a = list(fb)
+        a[i] = v
+        return L.lif_layer_forward_delayed(*a)
+    assert f(1, None) == L.LIF_ERR_ARG              # q_k required
+    assert f(6, None) == L.LIF_ERR_ARG              # WT required
+    bad = L.Params(v_th=0.0).c()
+    assert f(9, ctypes.byref(bad)) == L.LIF_ERR_THRESHOLD
+    # backward: q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N, p, out_t, out_n, out_i, out_k, g, gW, gD, gT,
+    # ws, ws_bytes, stream
+    bb = [F, F, F, F, 2, 10, F, 4, 8, ctypes.byref(p), F, F, F, F, F, F, None, None, F, 10 ** 9, None]
+
+    def b(i, v):
+        a = list(bb)
+        a[i] = v
+        return L.lif_layer_backward_delayed(*a)
+    assert b(15, None) == L.LIF_ERR_ARG             # grad_WT required
+    assert b(13, None) == L.LIF_ERR_ARG             # out_k required
+    need = L.lif_layer_backward_delayed_workspace_size(2, 10, 4, 8, p)
+    assert need > 0 and b(19, need - 1) == L.LIF_ERR_WORKSPACE
+    bad = L.Params(tau_mem=0.001).c()
+    assert b(9, ctypes.byref(bad)) == L.LIF_ERR_TAU

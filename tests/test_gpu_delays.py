@@ -1,0 +1,149 @@
+"""GPU parity of the layer with learnable synaptic delays (lif_delay_queues,
+lif_layer_forward_delayed, lif_layer_backward_delayed) against the delayed
+oracle on the same seeded inputs: the per-neuron queues bit for bit, the
+spike trains, and the weight, delay and input-time gradients."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from tests.parity import compare_grad, compare_spikes
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def env():
+    import torch
+    import paper_2603_13283_amd as lif
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    lif.load()
+    return torch, lif
+
+
+def _dev(torch, a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda:0")
+
+
+def run_case(env, ev, WT, DT, label, P=None, OP=None, grads=True, twice=True):
+    torch, lif = env
+    P = P or lif.Params()
+    OP = OP or oracle.LifParams()
+    print(f"[case] {label} B={ev.B} E_max={ev.E_max} C={WT.shape[0]} N={WT.shape[1]}", flush=True)
+    t, s, n, w, d = (_dev(torch, a) for a in (ev.ev_t, ev.ev_src, ev.ev_n, WT, DT))
+    q = lif.delay_queues(t, s, n, d)
+    out = lif.forward_delayed(q, s, n, w, P)
+    torch.cuda.synchronize()
+    # queues, bit for bit
+    rq_t, rq_k = oracle.delay_queues(ev.ev_t, ev.ev_src, ev.ev_n, DT)
+    gq_t, gq_k = q.q_t.cpu().numpy(), q.q_k.cpu().numpy()
+    for b in range(ev.B):
+        k = int(ev.ev_n[b])
+        assert np.array_equal(gq_k[b, :, :k], rq_k[b, :, :k]), f"{label}: queue order of sample {b}"
+        assert np.array_equal(gq_t[b, :, :k].view(np.uint32), rq_t[b, :, :k].view(np.uint32)), \
+            f"{label}: arrival times of sample {b}"
+    qs = q.status.cpu().numpy()
+    assert qs[0] == 0 and qs[6] == int(ev.ev_n.sum())
+    # spikes
+    ref = oracle.forward_delayed(ev.ev_t, ev.ev_src, ev.ev_n, WT, DT, OP)
+    st = compare_spikes(out.out_t.cpu().numpy(), out.out_n.cpu().numpy(), ref, out.out_i.cpu().numpy(), label=label,
+                        out_k_gpu=out.out_k.cpu().numpy())
+    status = out.status.cpu().numpy()
+    assert status[2] == int(out.out_n.cpu().numpy().sum()) and status[6] == int(ev.ev_n.sum())
+    assert not (status[0] & lif.WARN_INTERNAL)
+    # the sequential baseline on the same queues
+    seq = lif.forward_delayed(q, s, n, w, P, sequential=True)
+    torch.cuda.synchronize()
+    compare_spikes(seq.out_t.cpu().numpy(), seq.out_n.cpu().numpy(), ref, seq.out_i.cpu().numpy(),
+                   label=f"{label} (sequential)", out_k_gpu=seq.out_k.cpu().numpy())
+    ss = seq.status.cpu().numpy()
+    assert ss[2] == int(seq.out_n.cpu().numpy().sum()) and ss[6] == int(ev.ev_n.sum())
+    print(f"    spikes {st['spikes']} flagged {st['flagged']} excused {st['excused']}", flush=True)
+    if not grads:
+        return st
+    # gradients on identical inputs: the oracle's spikes in float32
+    rng = np.random.default_rng(5)
+    r32 = ref.rounded()
+    g = (rng.standard_normal(ref.out_t.shape) * np.isfinite(ref.out_t)).astype(np.float32)
+    fwd = lif.ForwardOut(_dev(torch, r32.out_t.astype(np.float32)), _dev(torch, ref.out_n),
+                         _dev(torch, r32.out_i.astype(np.float32)), None, _dev(torch, ref.out_k))
+    gW, gD, gT = lif.backward_delayed(q, s, n, w, fwd, _dev(torch, g), P)
+    torch.cuda.synchronize()
+    rW, rD, rT = oracle.backward_delayed(ev.ev_t, ev.ev_src, ev.ev_n, WT, DT, r32, g.astype(np.float64), OP)
+    ew = compare_grad(gW.cpu().numpy(), rW, label=f"{label} grad_W")
+    ed = compare_grad(gD.cpu().numpy(), rD, label=f"{label} grad_D")
+    et = compare_grad(gT.cpu().numpy(), rT, label=f"{label} grad_t")
+    assert (gT.cpu().numpy()[np.arange(ev.E_max)[None, :] >= ev.ev_n[:, None]] == 0).all()
+    print(f"    rel(gW) {ew:.2e} rel(gD) {ed:.2e} rel(gT) {et:.2e}", flush=True)
+    if twice:
+        gW2, gD2, gT2 = lif.backward_delayed(q, s, n, w, fwd, _dev(torch, g), P)
+        q2 = lif.delay_queues(t, s, n, d)
+        out2 = lif.forward_delayed(q2, s, n, w, P)
+        for a, b_ in ((gW, gW2), (gD, gD2), (gT, gT2), (out.out_t, out2.out_t)):
+            assert torch.equal(a.view(torch.int32), b_.view(torch.int32)), f"{label}: not reproducible"
+        k1, k2 = q.q_k.cpu().numpy(), q2.q_k.cpu().numpy()     # entries past ev_n are not written
+        for b in range(ev.B):
+            assert np.array_equal(k1[b, :, :ev.ev_n[b]], k2[b, :, :ev.ev_n[b]]), f"{label}: queues differ"
+    return st
+
+
+@pytest.mark.parametrize("N", [70, 64, 3])
+def test_delays_small_ragged(env, N):
+    cfg = W.random_small(81, B=5, C=40, N=N, n_events=600, T=0.5, gain=7.0)
+    ev = cfg.events
+    ev.ev_n[1] = 0
+    run_case(env, ev, cfg.layers[0].WT, W.uniform_delays(81, 40, N), f"ragged N={N}")
+
+
+def test_delays_reset_and_t_end(env):
+    torch, lif = env
+    cfg = W.random_small(82, B=3, C=30, N=50, n_events=500, T=0.4, gain=14.0)
+    P, OP = lif.Params(v_reset=-0.3, t_end=0.45), oracle.LifParams(v_reset=-0.3, t_end=0.45)
+    run_case(env, cfg.events, cfg.layers[0].WT, W.uniform_delays(82, 30, 50, d_max=0.05), "v_reset=-0.3 t_end=0.45",
+             P=P, OP=OP)
+
+
+def test_delays_zero_and_ties(env):
+    """Zero delays give the sample's queue (the layer's own spikes), and
+    equal arrivals keep the event order."""
+    torch, lif = env
+    rng = np.random.default_rng(83)
+    C, N, n = 16, 40, 400
+    t = (rng.integers(0, 64, n) / 128.0).astype(np.float32)          # many equal times
+    src = rng.integers(0, C, n).astype(np.int32)
+    ev = W.pack_events([t, t[: n // 2]], [src, src[: n // 2]])
+    WT = (rng.standard_normal((C, N)) * 5 / math.sqrt(C)).astype(np.float32)
+    DT = np.zeros((C, N), np.float32)
+    DT[: C // 2] = (rng.integers(0, 4, (C // 2, N)) / 128.0).astype(np.float32)   # equal arrivals across channels
+    run_case(env, ev, WT, DT, "ties")
+    run_case(env, ev, WT, np.zeros_like(WT), "zero delays", grads=False, twice=False)
+
+
+def test_delays_spike_cap(env):
+    torch, lif = env
+    cfg = W.random_small(84, B=2, C=20, N=30, n_events=800, T=0.3, gain=30.0)
+    P, OP = lif.Params(s_max=4), oracle.LifParams(s_max=4)
+    st = run_case(env, cfg.events, cfg.layers[0].WT, W.uniform_delays(84, 20, 30), "cap s_max=4", P=P, OP=OP,
+                  twice=False)
+    assert st["spikes"] > 0
+
+
+def test_bad_delay_reported(env):
+    torch, lif = env
+    cfg = W.random_small(85, B=2, C=10, N=8, n_events=50, T=0.2, gain=4.0)
+    ev = cfg.events
+    DT = W.uniform_delays(85, 10, 8)
+    DT[3, 5] = -0.01
+    q = lif.delay_queues(*(_dev(torch, a) for a in (ev.ev_t, ev.ev_src, ev.ev_n, DT)))
+    torch.cuda.synchronize()
+    assert q.status.cpu().numpy()[0] & lif.WARN_BAD_DELAY
+
+
+@pytest.mark.timeout(600)
+def test_delays_config2_shape(env):
+    """The 700 -> 256 layer at B = 32 (~5k events per sample) with the
+    paper's delay initialisation U[0, 0.1] s and a gain that makes it fire."""
+    cfg = W.config2(gain=6.0)
+    run_case(env, cfg.events, cfg.layers[0].WT, W.uniform_delays(2, 700, 256), "config-2 shape, gain 6")
