@@ -31,6 +31,7 @@
 namespace lif {
 
 constexpr int kChunkWaves = 4;
+constexpr int kChunkLdsC = 2048;        // weight-column entries staged in LDS per wave (8 KB)
 
 // V of the no-reset trajectory u after a state (V0, I0) (Eq. mem_pot).
 __device__ __forceinline__ double v_after(const Model& m, double V0, double I0, double u)
@@ -40,12 +41,18 @@ __device__ __forceinline__ double v_after(const Model& m, double V0, double I0, 
 }
 
 // The interval rule (Sec. 3.2.2) on an interval of length L > 0 from
-// (V0, I0): crossing when V(L) >= V_th or when the stationary point of Eq.
-// t_vmax lies inside with V >= V_th there; hi is the end of the root
-// bracket (the stationary point when it lies inside, else L).
-__device__ __forceinline__ bool interval_rule(const Model& m, double V0, double I0, double L, double& hi)
+// (V0, I0), A = e^{-L/tm}, D = e^{-L/ts}: crossing when V(L) >= V_th or when
+// the stationary point of Eq. t_vmax lies inside with V >= V_th there; hi is
+// the end of the root bracket (the stationary point when it lies inside,
+// else L).  Intervals that fail the no-crossing screen of screen_value
+// (V0 + max(I0 - V_th, 0) L / tm below the threshold) are rejected first:
+// they cannot cross, so the rule's outcome is unchanged.
+__device__ __forceinline__ bool interval_rule(const Model& m, double V0, double I0, double L, double A, double D,
+                                              double& hi)
 {
-    const double vend = v_after(m, V0, I0, L);
+    hi = L;
+    if (V0 + fmax(I0 - m.th, 0.0) * (L * m.inv_tm) < m.th_lo) return false;
+    const double vend = V0 * A + m.kappa * I0 * (A - D);
     const double Dm = V0 * (m.tm - m.ts) + I0 * m.ts;
     const bool has_max = I0 > V0 && Dm > 0.0;
     double tv = INFINITY;
@@ -89,18 +96,33 @@ __global__ __launch_bounds__(kWave * kChunkWaves) void k_chunked(
     int32_t* __restrict__ consumed, int32_t* __restrict__ processed, int32_t* __restrict__ status)
 {
     constexpr int K = kWave * M;
-    const int lane = (int)threadIdx.x % kWave;
-    const size_t item = (size_t)blockIdx.x * kChunkWaves + threadIdx.x / kWave;
+    __shared__ float s_w[kChunkWaves][kChunkLdsC];
+    const int lane = (int)threadIdx.x % kWave, wave = (int)threadIdx.x / kWave;
+    // waves in neuron-major order: the waves of a workgroup mostly share a
+    // neuron, so their loads of its weight column hit the same lines
+    const size_t item = (size_t)blockIdx.x * kChunkWaves + wave;
     if (item >= (size_t)B * N) return;
-    const int b = (int)(item / (size_t)N), n = (int)(item % (size_t)N);
+    const int n = (int)(item / (size_t)B), b = (int)(item % (size_t)B);
+    const size_t idx = (size_t)b * N + n;
     const int nb = clamp_count(ev_n[b], E_max);
     // the neuron's queue: the sample's events, or (QUEUE) its own arrivals
-    const float* tt = ev_t + (QUEUE ? item : (size_t)b) * (size_t)E_max;
+    const float* tt = ev_t + (QUEUE ? idx : (size_t)b) * (size_t)E_max;
     const int32_t* src = ev_src + (size_t)b * E_max;
-    const int32_t* qk = QUEUE ? q_k + item * (size_t)E_max : nullptr;
-    float* st = out_t + item * (size_t)m.s_max;
-    float* si = out_i ? out_i + item * (size_t)m.s_max : nullptr;
-    int32_t* sk = out_k ? out_k + item * (size_t)m.s_max : nullptr;
+    const int32_t* qk = QUEUE ? q_k + idx * (size_t)E_max : nullptr;
+    float* st = out_t + idx * (size_t)m.s_max;
+    float* si = out_i ? out_i + idx * (size_t)m.s_max : nullptr;
+    int32_t* sk = out_k ? out_k + idx * (size_t)m.s_max : nullptr;
+    // the neuron's weight column W^T[:, n] in the wave's LDS slice (lanes of
+    // one event chunk read random rows of it); from global memory when it
+    // does not fit.  Each wave writes and reads only its own slice, and LDS
+    // operations of one wave complete in order.
+    const bool lds_w = C_in <= kChunkLdsC;
+    if (lds_w) {
+        for (int c = lane; c < C_in; c += kWave) s_w[wave][c] = WT[(size_t)c * N + n];
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
     double t_cur = 0.0, V = 0.0, I = 0.0;
     int k = 0, chunks = 0, ns = 0;
     long long work = 0;
@@ -119,7 +141,8 @@ __global__ __launch_bounds__(kWave * kChunkWaves) void k_chunked(
             valid[j] = e < end;
             te[j] = valid[j] ? (double)tt[e] : 0.0;
             const int se = QUEUE ? min(max(valid[j] ? qk[e] : 0, 0), max(nb - 1, 0)) : e;
-            w[j] = valid[j] ? WT[(size_t)clamp_src(src[se], C_in) * (size_t)N + n] : 0.0f;
+            const int c = valid[j] ? clamp_src(src[se], C_in) : 0;
+            w[j] = valid[j] ? (lds_w ? s_w[wave][c] : WT[(size_t)c * N + n]) : 0.0f;
         }
         // the time before each event: the previous event's, t_cur for the
         // chunk's first
@@ -169,7 +192,7 @@ __global__ __launch_bounds__(kWave * kChunkWaves) void k_chunked(
             if (jc < 0 && L[j] > 0.0) {
                 double hi;
                 const double V0 = m.kappa * (U - J), I0 = J;
-                if (interval_rule(m, V0, I0, L[j], hi)) {
+                if (interval_rule(m, V0, I0, L[j], A[j], D[j], hi)) {
                     jc = j;
                     cV = V0;
                     cI = I0;
@@ -226,7 +249,7 @@ __global__ __launch_bounds__(kWave * kChunkWaves) void k_chunked(
             // the interval after the last event, up to t_end
             const double Lo = m.t_end - t_cur;
             double hi;
-            if (Lo > 0.0 && interval_rule(m, V, I, Lo, hi)) {
+            if (Lo > 0.0 && interval_rule(m, V, I, Lo, exp(-Lo * m.inv_tm), exp(-Lo * m.inv_ts), hi)) {
                 const double tau = spike_offset(m, V, I, hi);
                 const double Is = I * exp(-tau * m.inv_ts);
                 if (lane == 0) {
@@ -250,9 +273,9 @@ __global__ __launch_bounds__(kWave * kChunkWaves) void k_chunked(
         if (sk) sk[q] = 0;
     }
     if (lane == 0) {
-        out_n[item] = ns;
-        if (consumed) consumed[item] = k;
-        if (processed) processed[item] = (int32_t)min(work, 0x7fffffffll);
+        out_n[idx] = ns;
+        if (consumed) consumed[idx] = k;
+        if (processed) processed[idx] = (int32_t)min(work, 0x7fffffffll);
         if (ns) {
             atomicAdd(&status[LIF_ST_SPIKES], ns);
             atomicAdd(&status[LIF_ST_ROOT_SOLVES], ns);

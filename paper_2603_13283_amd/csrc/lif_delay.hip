@@ -6,15 +6,22 @@
 // Delays break what the main forward is built on: the event maps are no
 // longer shared by the neurons of a sample, since every neuron sees its own
 // event order.  The delayed layer therefore runs per neuron:
-//   k_dly_queue    per (sample, neuron), one workgroup: the neuron's queue,
-//                  the sample's events ordered by (arrival, k) with the
-//                  arrival a = fl32(t_k + d_ij), by a bucket sort: arrivals
-//                  are binned by value into up to kQBins bins (a histogram
-//                  and a prefix sum in LDS), scattered into their bins, and
-//                  each event is then placed at its bin's start plus its
-//                  rank among the bin's keys.  Keys are unique 64-bit words
-//                  (arrival bits, then k), so the result does not depend on
-//                  the order in which the scatter's atomics land.
+//   k_dly_arrival  per (sample, 64 events, 64 neurons): the arrivals
+//                  a = fl32(t_k + d_ij), with the delays read as coalesced
+//                  W^T-layout row slices (lanes = neurons) and written per
+//                  neuron through an LDS transpose (lanes = events), so both
+//                  sides are coalesced.
+//   k_dly_queue_lds / k_dly_queue
+//                  per (sample, neuron), one workgroup: the neuron's queue,
+//                  its events ordered by the key (arrival bits, then k), by a
+//                  bucket sort: arrivals are binned by value (a histogram and
+//                  a prefix sum in LDS), scattered into their bins, and each
+//                  key is then placed at its bin's start plus its rank among
+//                  the bin's keys.  Keys are unique, so the result does not
+//                  depend on the order in which the scatter's atomics land.
+//                  Queues of up to kQLdsMax events keep their keys in
+//                  registers and the binned keys in LDS (one read of the
+//                  arrivals); longer ones bin through global memory.
 //   forward        the chunked walk of lif_chunked.hip on these queues (one
 //                  wave per neuron, K = 128 events per iteration, no budget:
 //                  every event is consumed unless the neuron stops at s_max).
@@ -58,10 +65,161 @@ __device__ __forceinline__ int bin_of(float a, float sc, int nbins)
     return x < (float)(nbins - 1) ? (int)x : nbins - 1;
 }
 
-__global__ __launch_bounds__(kQThreads) void k_dly_queue(const float* __restrict__ ev_t,
-                                                        const int32_t* __restrict__ ev_src,
-                                                        const int32_t* __restrict__ ev_n, int E_max,
-                                                        const float* __restrict__ DT, int C_in, int N,
+constexpr int kArrTile = 64;            // events and neurons per k_dly_arrival workgroup
+
+__global__ __launch_bounds__(256) void k_dly_arrival(const float* __restrict__ ev_t,
+                                                    const int32_t* __restrict__ ev_src,
+                                                    const int32_t* __restrict__ ev_n, int E_max,
+                                                    const float* __restrict__ DT, int C_in, int N,
+                                                    float* __restrict__ arr)
+{
+    __shared__ float s_a[kArrTile][kArrTile + 1];      // [neuron][event]
+    const int lane = (int)threadIdx.x % kWave, wave = (int)threadIdx.x / kWave;
+    const int k0 = blockIdx.x * kArrTile, b = blockIdx.y, n0 = blockIdx.z * kArrTile;
+    const int nb = clamp_count(ev_n[b], E_max);
+    if (k0 >= nb) return;
+    const float* tt = ev_t + (size_t)b * E_max;
+    const int32_t* src = ev_src + (size_t)b * E_max;
+    const int n = n0 + lane;
+    for (int e = wave; e < kArrTile; e += 256 / kWave) {
+        const int k = k0 + e;
+        if (k < nb && n < N) s_a[lane][e] = arrival(tt, src, DT, C_in, N, n, k);
+    }
+    __syncthreads();
+    const int k = k0 + lane;
+    for (int q = wave; q < kArrTile; q += 256 / kWave) {
+        const int nn = n0 + q;
+        if (k < nb && nn < N) arr[((size_t)b * N + nn) * (size_t)E_max + k] = s_a[q][lane];
+    }
+}
+
+constexpr int kQLdsMax = 8192;          // longest queue sorted in registers and LDS
+constexpr int kQLdsBins = 2048;
+constexpr int kQLdsThreads = 512;
+constexpr int kQR = kQLdsMax / kQLdsThreads;
+
+__global__ __launch_bounds__(kQLdsThreads) void k_dly_queue_lds(const int32_t* __restrict__ ev_n, int E_max, int N,
+                                                               const float* __restrict__ arr,
+                                                               float* __restrict__ q_t, int32_t* __restrict__ q_k)
+{
+    __shared__ uint32_t s_at[kQLdsMax];        // binned arrivals (bits)
+    __shared__ uint16_t s_ak[kQLdsMax];        // and their event indices
+    __shared__ int s_bin[kQLdsBins];
+    __shared__ float s_red[kQLdsThreads / kWave];
+    __shared__ int s_part[kQLdsThreads];
+    const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    const size_t item = blockIdx.x;
+    const int b = (int)(item / (size_t)N);
+    const int nb = min(clamp_count(ev_n[b], E_max), kQLdsMax);
+    if (nb == 0) return;
+    const size_t base = item * (size_t)E_max;
+    // the thread's arrivals (event k = tid + r kQLdsThreads), all loads at once
+    uint32_t ab[kQR];
+#pragma unroll
+    for (int r = 0; r < kQR; ++r) {
+        const int k = tid + r * kQLdsThreads;
+        ab[r] = k < nb ? __float_as_uint(arr[base + k]) : 0u;
+    }
+    float mx = 0.0f;
+#pragma unroll
+    for (int r = 0; r < kQR; ++r) mx = fmaxf(mx, __uint_as_float(ab[r]));
+    for (int off = kWave / 2; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, kWave));
+    if (lane == 0) s_red[wave] = mx;
+    int nbins = 1;
+    while (nbins < nb && nbins < kQLdsBins) nbins <<= 1;
+    for (int j = tid; j < nbins; j += kQLdsThreads) s_bin[j] = 0;
+    __syncthreads();
+    float amax = s_red[0];
+    for (int w = 1; w < kQLdsThreads / kWave; ++w) amax = fmaxf(amax, s_red[w]);
+    const float sc = amax > 0.0f && amax < INFINITY ? (float)nbins / amax : 0.0f;
+    int bin[kQR];
+#pragma unroll
+    for (int r = 0; r < kQR; ++r) {
+        bin[r] = bin_of(__uint_as_float(ab[r]), sc, nbins);
+        if (tid + r * kQLdsThreads < nb) atomicAdd(&s_bin[bin[r]], 1);
+    }
+    __syncthreads();
+    // exclusive prefix sum over the bins: each thread a contiguous range
+    const int per = (nbins + kQLdsThreads - 1) / kQLdsThreads;
+    const int j0 = min(tid * per, nbins), j1 = min(j0 + per, nbins);
+    int local = 0;
+    for (int j = j0; j < j1; ++j) local += s_bin[j];
+    s_part[tid] = local;
+    __syncthreads();
+    for (int off = 1; off < kQLdsThreads; off <<= 1) {
+        const int x = tid >= off ? s_part[tid - off] : 0;
+        __syncthreads();
+        s_part[tid] += x;
+        __syncthreads();
+    }
+    int run = s_part[tid] - local;
+    for (int j = j0; j < j1; ++j) {
+        const int c = s_bin[j];
+        s_bin[j] = run;
+        run += c;
+    }
+    __syncthreads();
+    // scatter into the bins in LDS; s_bin[j] ends at the end of bin j
+#pragma unroll
+    for (int r = 0; r < kQR; ++r) {
+        const int k = tid + r * kQLdsThreads;
+        if (k < nb) {
+            const int pos = atomicAdd(&s_bin[bin[r]], 1);
+            if (pos < nb) {
+                s_at[pos] = ab[r];
+                s_ak[pos] = (uint16_t)k;
+            }
+        }
+    }
+    __syncthreads();
+    // each event's place: its bin's start plus its rank among the bin's
+    // keys, the thread's events stepping through their bins together
+    int lo[kQR], cnt[kQR], rank[kQR];
+    int mxc = 0;
+#pragma unroll
+    for (int r = 0; r < kQR; ++r) {
+        const bool v = tid + r * kQLdsThreads < nb;
+        lo[r] = bin[r] > 0 ? s_bin[bin[r] - 1] : 0;
+        cnt[r] = v ? s_bin[bin[r]] - lo[r] : 0;
+        rank[r] = 0;
+        mxc = max(mxc, cnt[r]);
+    }
+    for (int q = 0; q < mxc; ++q) {
+#pragma unroll
+        for (int r = 0; r < kQR; ++r) {
+            if (q < cnt[r]) {
+                const uint32_t o = s_at[lo[r] + q];
+                const int ok = s_ak[lo[r] + q];
+                rank[r] += o < ab[r] || (o == ab[r] && ok < tid + r * kQLdsThreads);
+            }
+        }
+    }
+    __syncthreads();
+    // the queue in order in LDS, then written out coalesced
+#pragma unroll
+    for (int r = 0; r < kQR; ++r) {
+        const int place = lo[r] + rank[r];
+        if (cnt[r] > 0 && place < nb) {         // always: a key's bin is the one it was scattered to
+            s_at[place] = ab[r];
+            s_ak[place] = (uint16_t)(tid + r * kQLdsThreads);
+        }
+    }
+    __syncthreads();
+    for (int i = tid; i < nb; i += kQLdsThreads) {
+        q_t[base + i] = __uint_as_float(s_at[i]);
+        q_k[base + i] = s_ak[i];
+    }
+}
+
+// 64-bit sort key of event k with arrival a: the arrival's bits (which order
+// like the values for non-negative arrivals), then k.
+__device__ __forceinline__ unsigned long long arrival_key(float a, int k)
+{
+    return ((unsigned long long)__float_as_uint(a) << 32) | (unsigned)k;
+}
+
+__global__ __launch_bounds__(kQThreads) void k_dly_queue(const int32_t* __restrict__ ev_n, int E_max, int N,
+                                                        const float* __restrict__ arr,
                                                         unsigned long long* __restrict__ keys,
                                                         float* __restrict__ q_t, int32_t* __restrict__ q_k)
 {
@@ -70,15 +228,15 @@ __global__ __launch_bounds__(kQThreads) void k_dly_queue(const float* __restrict
     __shared__ int s_part[kQThreads];
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
     const size_t item = blockIdx.x;
-    const int b = (int)(item / (size_t)N), n = (int)(item % (size_t)N);
+    const int b = (int)(item / (size_t)N);
     const int nb = clamp_count(ev_n[b], E_max);
     if (nb == 0) return;
-    const float* tt = ev_t + (size_t)b * E_max;
-    const int32_t* src = ev_src + (size_t)b * E_max;
     const size_t base = item * (size_t)E_max;
+    const float* ain = arr + base;
+    auto key_arrival = [](unsigned long long key) { return __uint_as_float((unsigned)(key >> 32)); };
     // the largest arrival
     float mx = 0.0f;
-    for (int k = tid; k < nb; k += kQThreads) mx = fmaxf(mx, arrival(tt, src, DT, C_in, N, n, k));
+    for (int k = tid; k < nb; k += kQThreads) mx = fmaxf(mx, ain[k]);
     for (int off = kWave / 2; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, kWave));
     if (lane == 0) s_red[wave] = mx;
     int nbins = 1;
@@ -89,8 +247,7 @@ __global__ __launch_bounds__(kQThreads) void k_dly_queue(const float* __restrict
     for (int w = 1; w < kQThreads / kWave; ++w) amax = fmaxf(amax, s_red[w]);
     const float sc = amax > 0.0f && amax < INFINITY ? (float)nbins / amax : 0.0f;
     // histogram
-    for (int k = tid; k < nb; k += kQThreads)
-        atomicAdd(&s_bin[bin_of(arrival(tt, src, DT, C_in, N, n, k), sc, nbins)], 1);
+    for (int k = tid; k < nb; k += kQThreads) atomicAdd(&s_bin[bin_of(ain[k], sc, nbins)], 1);
     __syncthreads();
     // exclusive prefix sum over the bins: each thread a contiguous range
     const int per = (nbins + kQThreads - 1) / kQThreads;
@@ -114,21 +271,20 @@ __global__ __launch_bounds__(kQThreads) void k_dly_queue(const float* __restrict
     __syncthreads();
     // scatter into the bins; s_bin[j] ends at the end of bin j
     for (int k = tid; k < nb; k += kQThreads) {
-        const float a = arrival(tt, src, DT, C_in, N, n, k);
+        const float a = ain[k];
         const int pos = atomicAdd(&s_bin[bin_of(a, sc, nbins)], 1);
-        if (pos < nb) keys[base + pos] = ((unsigned long long)__float_as_uint(a) << 32) | (unsigned)k;
+        if (pos < nb) keys[base + pos] = arrival_key(a, k);
     }
     __syncthreads();
     // each key's place: its bin's start plus its rank among the bin's keys
     for (int p = tid; p < nb; p += kQThreads) {
         const unsigned long long key = keys[base + p];
-        const float a = __uint_as_float((unsigned)(key >> 32));
-        const int j = bin_of(a, sc, nbins);
+        const int j = bin_of(key_arrival(key), sc, nbins);
         const int lo = j > 0 ? s_bin[j - 1] : 0, hi = s_bin[j];
         int rank = 0;
         for (int q = lo; q < hi; ++q) rank += keys[base + q] < key;
-        if (lo + rank < nb) {                 // always: bins are recomputed bit for bit
-            q_t[base + lo + rank] = a;
+        if (lo + rank < nb) {                 // always: a key's bin is the one it was scattered to
+            q_t[base + lo + rank] = key_arrival(key);
             q_k[base + lo + rank] = (int32_t)(key & 0xffffffffull);
         }
     }
@@ -374,10 +530,21 @@ static unsigned grid_for(size_t work)
 
 }  // namespace lif
 
+// Workspace of lif_delay_queues: the arrivals [B][N][E_max] (float), and
+// for queues longer than kQLdsMax the binned keys (64-bit).
+static void dly_queue_layout(int B, int E_max, int N, size_t& arr_bytes, size_t& key_bytes)
+{
+    const size_t n = (size_t)B * (size_t)N * (size_t)E_max;
+    arr_bytes = (n * sizeof(float) + 255) & ~(size_t)255;
+    key_bytes = E_max > lif::kQLdsMax ? (n * sizeof(unsigned long long) + 255) & ~(size_t)255 : 0;
+}
+
 extern "C" size_t lif_delay_queues_workspace_size(int B, int E_max, int N_out)
 {
     if (B < 0 || E_max < 0 || N_out < 1) return 0;
-    return (size_t)B * (size_t)N_out * (size_t)E_max * sizeof(unsigned long long) + 256;
+    size_t arr_bytes, key_bytes;
+    dly_queue_layout(B, E_max, N_out, arr_bytes, key_bytes);
+    return arr_bytes + key_bytes + 256;
 }
 
 extern "C" int lif_delay_queues(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
@@ -387,7 +554,7 @@ extern "C" int lif_delay_queues(const float* ev_t, const int32_t* ev_src, const 
     using namespace lif;
     if (B < 0 || E_max < 0 || C_in < 1 || N_out < 1) return LIF_ERR_ARG;
     if (B > 0 && E_max > 0 && (!ev_t || !ev_src || !ev_n || !DT || !q_t || !q_k || !ws)) return LIF_ERR_ARG;
-    if ((size_t)B * (size_t)N_out >= ((size_t)1 << 31)) return LIF_ERR_SIZE;
+    if ((size_t)B * (size_t)N_out >= ((size_t)1 << 31) || B > 65535) return LIF_ERR_SIZE;
     if (ws_bytes < lif_delay_queues_workspace_size(B, E_max, N_out)) return LIF_ERR_WORKSPACE;
     hipStream_t stream = (hipStream_t)stream_;
     if (status) {
@@ -397,9 +564,21 @@ extern "C" int lif_delay_queues(const float* ev_t, const int32_t* ev_src, const 
                      status);
     }
     if (B > 0 && E_max > 0) {
-        unsigned long long* keys = (unsigned long long*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
-        TIMED_LAUNCH("dly_queue", k_dly_queue, dim3((unsigned)((size_t)B * N_out)), dim3(kQThreads), 0, stream,
-                     ev_t, ev_src, ev_n, E_max, DT, C_in, N_out, keys, q_t, q_k);
+        size_t arr_bytes, key_bytes;
+        dly_queue_layout(B, E_max, N_out, arr_bytes, key_bytes);
+        float* arr = (float*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
+        unsigned long long* keys = (unsigned long long*)((char*)arr + arr_bytes);
+        const dim3 agrid((unsigned)((E_max + kArrTile - 1) / kArrTile), (unsigned)B,
+                         (unsigned)((N_out + kArrTile - 1) / kArrTile));
+        TIMED_LAUNCH("dly_arrival", k_dly_arrival, agrid, dim3(256), 0, stream, ev_t, ev_src, ev_n, E_max, DT, C_in,
+                     N_out, arr);
+        const dim3 qgrid((unsigned)((size_t)B * N_out));
+        if (E_max <= kQLdsMax)
+            TIMED_LAUNCH("dly_queue", k_dly_queue_lds, qgrid, dim3(kQLdsThreads), 0, stream, ev_n, E_max, N_out, arr,
+                         q_t, q_k);
+        else
+            TIMED_LAUNCH("dly_queue", k_dly_queue, qgrid, dim3(kQThreads), 0, stream, ev_n, E_max, N_out, arr, keys,
+                         q_t, q_k);
     }
     return check_launch();
 }

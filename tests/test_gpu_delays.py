@@ -141,6 +141,15 @@ def test_bad_delay_reported(env):
     assert q.status.cpu().numpy()[0] & lif.WARN_BAD_DELAY
 
 
+def test_delays_long_queues(env):
+    """Queues longer than the register/LDS sort (E_max > 8192) bin through
+    global memory."""
+    cfg = W.random_small(86, B=2, C=60, N=20, n_events=12000, T=2.0, gain=2.0)
+    ev = cfg.events
+    assert ev.E_max > 8192
+    run_case(env, ev, cfg.layers[0].WT, W.uniform_delays(86, 60, 20), "long queues E_max=12000")
+
+
 @pytest.mark.timeout(600)
 def test_delays_config2_shape(env):
     """The 700 -> 256 layer at B = 32 (~5k events per sample) with the
