@@ -251,3 +251,67 @@ def spike_count_reg(tables, counts, th, rp: RegParams):
             row.append(cs)
         coef.append(row)
     return L_reg, L_over, coef
+
+
+def spike_count_reg_grad(ev_t, ev_src, ev_n, WT, out_t, out_k, out_n, tm, ts, th, vr, t_end, rp: RegParams):
+    """Gradient of lam_reg L_reg + lam_over L_over (App. E.1, Eq. loss) with
+    the gates held constant (they are functions of the spike counts, which are
+    piecewise constant in the parameters).  Each V_max is the value of the
+    interval's trajectory at its argmax tau = t0 + u:
+        V(tau) = sum_{k < j} w_k K(tau - t_k) - (th - vr) sum_{s: out_k < j} e^{-(tau - t_s)/tm},
+    with K(u) = kappa (e^{-u/tm} - e^{-u/ts}).  Its derivative takes the
+    explicit dependence on the weights, the input times and the spike times
+    before the interval, plus V'(tau) times the motion of tau when the argmax
+    is an interval end that is an input time (zero at an interior maximum,
+    where V' = 0).  Returns (L_reg, L_over, gW_direct [C, N], gT_direct
+    [B, E_max], g_spike [B, N, s_max]); the full gradient adds the layer's
+    backward pass (App. D.3) of the upstream spike-time gradient g_spike."""
+    B, N = out_n.shape
+    C = WT.shape[0]
+    E = ev_t.shape[1]
+    S = out_t.shape[2]
+    ka = ts / (tm - ts)
+    tables = []
+    for b in range(B):
+        n = int(ev_n[b])
+        row = []
+        for i in range(N):
+            ns = int(out_n[b, i])
+            w = WT[ev_src[b, :n], i]
+            row.append(interval_table(ev_t[b, :n], n, w, out_t[b, i, :ns], out_k[b, i, :ns], ns, tm, ts, th, vr, t_end))
+        tables.append(row)
+    L_reg, L_over, coef = spike_count_reg(tables, out_n, th, rp)
+    gW = np.zeros((C, N))
+    gT = np.zeros((B, E))
+    gS = np.zeros((B, N, S))
+    for b in range(B):
+        n = int(ev_n[b])
+        t = np.asarray(ev_t[b, :n], np.float64)
+        src = np.asarray(ev_src[b, :n])
+        for i in range(N):
+            w = np.asarray(WT[src, i], np.float64)
+            ns = int(out_n[b, i])
+            st = np.asarray(out_t[b, i, :ns], np.float64)
+            sk = np.asarray(out_k[b, i, :ns])
+            for j, (t0, t1, V0, I0, vmax, u, spiked) in enumerate(tables[b][i]):
+                c = coef[b][i][j]
+                if c == 0.0:
+                    continue
+                tau = t0 + u
+                # the input events before the interval (k < j)
+                d = tau - t[:j]
+                em, es = np.exp(-d / tm), np.exp(-d / ts)
+                np.add.at(gW[:, i], src[:j], c * ka * (em - es))
+                gT[b, :j] += -c * w[:j] * ka * (-em / tm + es / ts)
+                # the spikes before the interval
+                before = sk < j
+                gS[b, i, :ns][before] += c * (-(th - vr) / tm) * np.exp(-(tau - st[before]) / tm)
+                # an argmax at an interval end that is an input time moves with it
+                L = t1 - t0
+                if u == 0.0 and j > 0:
+                    gT[b, j - 1] += c * (I0 - V0) / tm
+                elif j < n and u == L and L > 0.0:
+                    emL, esL = math.exp(-L / tm), math.exp(-L / ts)
+                    V1 = V0 * emL + ka * I0 * (emL - esL)
+                    gT[b, j] += c * (I0 * esL - V1) / tm
+    return L_reg, L_over, gW, gT, gS

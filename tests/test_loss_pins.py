@@ -11,6 +11,7 @@ import torch
 
 import oracle
 from oracle import loss as OL
+import workloads as W
 
 TM, TS = 0.02, 0.005
 KA = TS / (TM - TS)
@@ -225,3 +226,66 @@ def test_individual_over_firing_term_by_hand():
     over = (0.5 + 0.2 + 0.1) / 3
     assert abs(L_over - 0.5 * over) < 1e-15            # gate 3/2 - 1, one neuron
     assert abs(L_reg - 0.5 * over) < 1e-15             # batch of one: same gate
+
+
+def _reg_loss(ev, WT, P, rp):
+    """lam_reg L_reg + lam_over L_over of the layer's own forward at WT."""
+    r = oracle.forward(ev.ev_t, ev.ev_src, ev.ev_n, WT, P)
+    L_reg, L_over, _, _, _ = OL.spike_count_reg_grad(ev.ev_t, ev.ev_src, ev.ev_n, WT, r.out_t, r.out_k, r.out_n,
+                                                    P.tau_mem, P.tau_syn, P.v_th, P.v_reset, P.t_end, rp)
+    return rp.lam_reg * L_reg + rp.lam_over * L_over, r.out_n
+
+
+@pytest.mark.parametrize("vr", [0.0, -0.3])
+def test_regulariser_gradients_match_finite_differences(vr):
+    """App. E.1 regularisers: the direct V_max terms plus the layer's backward
+    pass of the spike-time terms against central differences of the loss
+    recomputed from a fresh forward (float64 weights and times; gates and
+    interval sets unchanged by the small steps)."""
+    cfg = W.random_small(51, B=3, C=12, N=6, n_events=60, T=0.15, gain=10.0)
+    ev = cfg.events
+    WT = cfg.layers[0].WT.astype(np.float64)
+    P = oracle.LifParams(solver_reg=0.0, v_reset=vr)
+    rp = OL.RegParams(c_target=3.0, lam_reg=0.7, lam_over=0.4)
+    r = oracle.forward(ev.ev_t, ev.ev_src, ev.ev_n, WT.astype(np.float32), P)
+    assert r.out_n.max() > 3 and (r.out_n.mean(axis=0) < 3).any() and (r.out_n.mean(axis=0) > 3).any()
+    L_reg, L_over, gWd, gTd, gS = OL.spike_count_reg_grad(ev.ev_t, ev.ev_src, ev.ev_n, WT.astype(np.float32),
+                                                         r.out_t, r.out_k, r.out_n, P.tau_mem, P.tau_syn, P.v_th,
+                                                         P.v_reset, P.t_end, rp)
+    gWs, gTs = oracle.backward(ev.ev_t, ev.ev_src, ev.ev_n, WT.astype(np.float32), r, gS, P)
+    gW, gT = gWd + gWs, gTd + gTs
+    assert np.abs(gW).max() > 0 and np.abs(gS).max() > 0
+    # weights: the oracle reads float32 weights, so perturb in a way float32 holds exactly
+    checked = 0
+    for c in range(WT.shape[0]):
+        for i in range(WT.shape[1]):
+            h = 2.0 ** -14
+            Wp, Wm = WT.copy(), WT.copy()
+            Wp[c, i] += h
+            Wm[c, i] -= h
+            lp, np_ = _reg_loss(ev, Wp.astype(np.float32), P, rp)
+            lm, nm = _reg_loss(ev, Wm.astype(np.float32), P, rp)
+            if not (np.array_equal(np_, r.out_n) and np.array_equal(nm, r.out_n)):
+                continue
+            fd = (lp - lm) / (2 * h)
+            assert abs(fd - gW[c, i]) <= 2e-4 * max(abs(fd), 1e-2 * np.abs(gW).max()), (c, i, fd, gW[c, i])
+            checked += 1
+    assert checked >= 50
+    # input times (float32 steps of 2^-20 s)
+    done = 0
+    for b in range(ev.B):
+        for k in range(0, int(ev.ev_n[b]), 7):
+            h = 2.0 ** -20
+            tp, tm_ = ev.ev_t.copy(), ev.ev_t.copy()
+            tp[b, k] += h
+            tm_[b, k] -= h
+            if (k + 1 < ev.ev_n[b] and tp[b, k] >= ev.ev_t[b, k + 1]) or (k > 0 and tm_[b, k] <= ev.ev_t[b, k - 1]):
+                continue
+            lp, np_ = _reg_loss(W.EventBatch(tp, ev.ev_src, ev.ev_n), WT.astype(np.float32), P, rp)
+            lm, nm = _reg_loss(W.EventBatch(tm_, ev.ev_src, ev.ev_n), WT.astype(np.float32), P, rp)
+            if not (np.array_equal(np_, r.out_n) and np.array_equal(nm, r.out_n)):
+                continue
+            fd = (lp - lm) / (2 * h)
+            assert abs(fd - gT[b, k]) <= 2e-3 * max(abs(fd), 1e-2 * np.abs(gT).max()), (b, k, fd, gT[b, k])
+            done += 1
+    assert done >= 10
