@@ -385,6 +385,32 @@ int lif_spike_count_reg(const float* ev_t, const int32_t* ev_src, const int32_t*
                         const int32_t* out_n, const int32_t* out_k, double c_target, float* loss, float* under,
                         float* over, void* ws, size_t ws_bytes, lif_stream_t stream);
 
+/* Gradient of lambda_reg L_reg + lambda_over L_over (the loss values of
+ * lif_spike_count_reg, also written to loss[2] when loss is not NULL), the
+ * gates held constant (they are functions of the spike counts).  Each V_max
+ * is the interval trajectory's value at its argmax, which depends on the
+ * weights and input times before the interval, on the spike times before it
+ * (through the resets), and, when the argmax is an interval end that is an
+ * input time, on that time.  Outputs:
+ *   grad_spike float [B][N_out][s_max]  the upstream gradient on the layer's
+ *              spike times, ADDED to what the array holds: run
+ *              lif_layer_backward with it (together with the downstream
+ *              loss's spike-time gradient) for the part through the spikes
+ *   grad_WT    float [C_in][N_out]      the direct part of dL/dW, overwritten
+ *   grad_ev_t  float [B][E_max]         the direct part of dL/dt_in,
+ *              overwritten (nullable; 0 past ev_n[b])
+ * The full gradient is the direct part plus that backward pass.  Bitwise
+ * reproducible.  ws: lif_spike_count_reg_backward_workspace_size(...) bytes
+ * (about 16 bytes per (sample, interval, neuron)).  Errors as
+ * lif_spike_count_reg, LIF_ERR_ARG also for a non-finite lambda. */
+size_t lif_spike_count_reg_backward_workspace_size(int B, int E_max, int C_in, int N_out);
+
+int lif_spike_count_reg_backward(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B, int E_max,
+                                 const float* WT, int C_in, int N_out, const lif_params* p, const float* out_t,
+                                 const int32_t* out_n, const int32_t* out_k, double c_target, double lam_reg,
+                                 double lam_over, float* loss, float* grad_spike, float* grad_WT, float* grad_ev_t,
+                                 void* ws, size_t ws_bytes, lif_stream_t stream);
+
 /* --------------------------------------------------------------------- */
 /* Adam step (the optimiser the paper trains with, App. E): for each of    */
 /* the n parameters, m1 = b1 m1 + (1 - b1) g, m2 = b2 m2 + (1 - b2) g^2,   */

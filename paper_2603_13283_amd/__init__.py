@@ -49,7 +49,8 @@ EXPORTED = ["lif_version", "lif_layer_forward_workspace_size", "lif_layer_forwar
             "lif_layer_backward_workspace_size", "lif_layer_backward",
             "lif_merge_workspace_size", "lif_merge_spikes", "lif_first_spike_ce", "lif_merge_grad",
             "lif_li_readout_workspace_size", "lif_li_readout", "lif_adam_step", "lif_spike_count_reg_workspace_size",
-            "lif_spike_count_reg", "lif_delay_queues_workspace_size", "lif_delay_queues",
+            "lif_spike_count_reg", "lif_spike_count_reg_backward_workspace_size", "lif_spike_count_reg_backward",
+            "lif_delay_queues_workspace_size", "lif_delay_queues",
             "lif_layer_forward_delayed", "lif_layer_forward_delayed_sequential",
             "lif_layer_backward_delayed_workspace_size", "lif_layer_backward_delayed",
             "lif_timer_enable", "lif_timer_read"]
@@ -176,6 +177,11 @@ def load(path: Optional[str] = None):
                                         _P, _P, _SZ, _P]
     lib.lif_adam_step.restype = _I
     lib.lif_adam_step.argtypes = [_P, _P, _P, _P, _SZ, ctypes.POINTER(lif_adam_params), _I, _P]
+    lib.lif_spike_count_reg_backward_workspace_size.restype = _SZ
+    lib.lif_spike_count_reg_backward_workspace_size.argtypes = [_I, _I, _I, _I]
+    lib.lif_spike_count_reg_backward.restype = _I
+    lib.lif_spike_count_reg_backward.argtypes = [_P, _P, _P, _I, _I, _P, _I, _I, _PP, _P, _P, _P, ctypes.c_double,
+                                                 ctypes.c_double, ctypes.c_double, _P, _P, _P, _P, _P, _SZ, _P]
     lib.lif_delay_queues_workspace_size.restype = _SZ
     lib.lif_delay_queues_workspace_size.argtypes = [_I, _I, _I]
     lib.lif_delay_queues.restype = _I
@@ -272,6 +278,14 @@ def lif_adam_step(*args) -> int:
 
 def lif_first_spike_ce(*args) -> int:
     return load().lif_first_spike_ce(*args)
+
+
+def lif_spike_count_reg_backward_workspace_size(B, E_max, C_in, N_out) -> int:
+    return load().lif_spike_count_reg_backward_workspace_size(B, E_max, C_in, N_out)
+
+
+def lif_spike_count_reg_backward(*args) -> int:
+    return load().lif_spike_count_reg_backward(*args)
 
 
 def lif_delay_queues_workspace_size(B, E_max, N_out) -> int:
@@ -596,3 +610,29 @@ def backward_delayed(q: DelayQueues, ev_src, ev_n, WT, fwd: ForwardOut, grad_out
                                     _stream(stream))
     _check("lif_layer_backward_delayed", rc)
     return gW, gD, gT
+
+
+def spike_count_reg_backward(ev_t, ev_src, ev_n, WT, fwd: ForwardOut, c_target: float, lam_reg: float = 1.0,
+                             lam_over: float = 1.0, params: Params = Params(), grad_spike=None,
+                             want_time_grad: bool = True, stream=None, ws=None):
+    """Run lif_spike_count_reg_backward; returns (loss [2], grad_spike
+    [B, N, s_max] (the given tensor, added to, or a new one), direct grad_WT,
+    direct grad_ev_t or None)."""
+    torch = _torch()
+    B, E, C, N = _dev_inputs(ev_t, ev_src, ev_n, WT)
+    dev = ev_t.device
+    p = params.c()
+    loss = torch.empty(2, dtype=torch.float32, device=dev)
+    if grad_spike is None:
+        grad_spike = torch.zeros((B, N, params.s_max), dtype=torch.float32, device=dev)
+    gW = torch.empty((C, N), dtype=torch.float32, device=dev)
+    gT = torch.empty((B, E), dtype=torch.float32, device=dev) if want_time_grad else None
+    need = lif_spike_count_reg_backward_workspace_size(B, E, C, N)
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    rc = lif_spike_count_reg_backward(_ptr(ev_t), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(WT), C, N, ctypes.byref(p),
+                                      _ptr(fwd.out_t), _ptr(fwd.out_n), _ptr(fwd.out_k), float(c_target),
+                                      float(lam_reg), float(lam_over), _ptr(loss), _ptr(grad_spike), _ptr(gW),
+                                      _ptr(gT), _ptr(ws), ws.numel(), _stream(stream))
+    _check("lif_spike_count_reg_backward", rc)
+    return loss, grad_spike, gW, gT

@@ -1571,11 +1571,21 @@ namespace lif {
 
 // Largest V over [0, L] of the no-reset trajectory from (V0, I0): the start,
 // the end (L finite) and the stationary point of Eq. t_vmax when it lies
-// inside.
-__device__ __forceinline__ double reg_vmax(const Model& m, double V0, double I0, double L, double A, double Dd)
+// inside, with the decays e^{-u/tm}, e^{-u/ts} at its argmax and
+// whether that is the interval's start or end (the first of equal values
+// wins: the start, then the end, then the stationary point).
+struct RegArg {
+    double vmax, em, es;
+    bool at_start, at_end;
+};
+
+__device__ __forceinline__ RegArg reg_vmax_arg(const Model& m, double V0, double I0, double L, double A, double Dd)
 {
-    double best = V0;
-    if (!isinf(L)) best = fmax(best, V0 * A + m.kappa * I0 * (A - Dd));
+    RegArg r{V0, 1.0, 1.0, true, false};
+    if (!isinf(L)) {
+        const double V1 = V0 * A + m.kappa * I0 * (A - Dd);
+        if (V1 > r.vmax) r = RegArg{V1, A, Dd, false, true};
+    }
     const double a = V0 + m.kappa * I0;
     if (I0 > 0.0 && a > 0.0) {
         const double ratio = m.kappa * I0 * m.tm / (a * m.ts);
@@ -1583,22 +1593,33 @@ __device__ __forceinline__ double reg_vmax(const Model& m, double V0, double I0,
             const double u = log(ratio) * m.c_tv;
             if (u > 0.0 && u < L) {
                 const double em = exp(-u * m.inv_tm), es = exp(-u * m.inv_ts);
-                best = fmax(best, V0 * em + m.kappa * I0 * (em - es));
+                const double Vu = V0 * em + m.kappa * I0 * (em - es);
+                if (Vu > r.vmax) r = RegArg{Vu, em, es, false, false};
             }
         }
     }
-    return best;
+    return r;
 }
+
+// Per-interval record for the regularisers' gradient (interval j of a
+// (sample, neuron), rec[(b (E_max + 1) + j) N + n]): the decays at the
+// argmax, the slope V' there when the argmax is an interval end that is an
+// input time (0 otherwise), and a code: 1 under-firing term active (silent,
+// V_max < V_th), 2 over-firing term active (spiked, V_max > V_th), 0 none,
+// plus 4 when the argmax is the start (input event j - 1) and 8 when it is
+// the end (input event j).
+constexpr int kRecUnder = 1, kRecOver = 2, kRecStart = 4, kRecEnd = 8;
 
 // Per (sample, segment, 64 neurons): the segment's intervals (and the open
 // one in the sample's last segment); per lane the sums of the hinge terms
 // and the interval counts, part = (sum under, silent count, sum over,
-// spiking count).
+// spiking count); with rec, the per-interval records.
 __global__ __launch_bounds__(kWave * kWalkWaves) void k_reg_walk(
     const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
     int E_pad, const float* __restrict__ WT, int C_in, int N, int tiles, int S, int items, Model m,
     const Decay* __restrict__ dec, const double2* __restrict__ carry, const float* __restrict__ out_t,
-    const int32_t* __restrict__ out_n, const int32_t* __restrict__ out_k, double4* __restrict__ part)
+    const int32_t* __restrict__ out_n, const int32_t* __restrict__ out_k, double4* __restrict__ part,
+    float4* __restrict__ rec)
 {
     __shared__ double2 s_ad[kWalkWaves][kSeg];
     __shared__ float s_t[kWalkWaves][kSeg + 1];
@@ -1636,8 +1657,11 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_reg_walk(
     }
     double su = 0.0, so = 0.0;
     int nsil = 0, nspk = 0;
+    float4* rb = rec ? rec + (size_t)c.b * (E_max + 1) * N + n : nullptr;
     auto take = [&](int j, double L, double A, double Dd, double t1) {
-        const double vmax = reg_vmax(m, v_of(m, U, J) - Dft, J, L, A, Dd);
+        const double V0 = v_of(m, U, J) - Dft;
+        const RegArg ra = reg_vmax_arg(m, V0, J, L, A, Dd);
+        const double vmax = ra.vmax;
         const bool spiked = sp < ns && ks[sp] == j;
         if (spiked) {
             so += fmax(vmax - m.th, 0.0);
@@ -1645,6 +1669,18 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_reg_walk(
         } else {
             su += fmax(m.th - vmax, 0.0);
             ++nsil;
+        }
+        if (rb && c.live) {
+            int code = spiked ? (vmax > m.th ? kRecOver : 0) : (vmax < m.th ? kRecUnder : 0);
+            double vp = 0.0;
+            if (code && ra.at_start && j > 0) {
+                code |= kRecStart;
+                vp = (J - V0) * m.inv_tm;
+            } else if (code && ra.at_end && j < c.nb) {
+                code |= kRecEnd;
+                vp = (J * Dd - ra.vmax) * m.inv_tm;
+            }
+            rb[(size_t)j * N] = make_float4((float)ra.em, (float)ra.es, (float)vp, (float)code);
         }
         // the deficit at the interval's end, with the spikes inside it
         Dft *= A;
@@ -1689,7 +1725,7 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_reg_walk(
 __global__ __launch_bounds__(256) void k_reg_reduce(const double4* __restrict__ part, const int32_t* __restrict__ ev_n,
                                                     int B, int E_max, int N, int S, double th, double* __restrict__ ub,
                                                     double* __restrict__ ob, float* __restrict__ under,
-                                                    float* __restrict__ over)
+                                                    float* __restrict__ over, double2* __restrict__ counts)
 {
     const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= (size_t)B * N) return;
@@ -1714,6 +1750,7 @@ __global__ __launch_bounds__(256) void k_reg_reduce(const double4* __restrict__ 
     ob[i] = o;
     if (under) under[i] = (float)u;
     if (over) over[i] = (float)o;
+    if (counts) counts[i] = make_double2(nsil, nspk);
 }
 
 // The two loss terms (one workgroup): per neuron the batch means and the
@@ -1723,7 +1760,8 @@ constexpr int kRegThreads = 256;
 
 __global__ __launch_bounds__(kRegThreads) void k_reg_loss(const double* __restrict__ ub, const double* __restrict__ ob,
                                                           const int32_t* __restrict__ out_n, int B, int N, int s_max,
-                                                          double c_target, float* __restrict__ loss)
+                                                          double c_target, float* __restrict__ loss,
+                                                          double2* __restrict__ gates)
 {
     __shared__ double s_reg[kRegThreads], s_over[kRegThreads];
     double lr = 0.0, lo = 0.0;
@@ -1738,8 +1776,10 @@ __global__ __launch_bounds__(kRegThreads) void k_reg_loss(const double* __restri
             ov += fmax(cnt / c_target - 1.0, 0.0) * ob[i];
         }
         cb /= (double)B;
-        lr += fmax(1.0 - cb / c_target, 0.0) * (mu / (double)B) + fmax(cb / c_target - 1.0, 0.0) * (mo / (double)B);
+        const double gu = fmax(1.0 - cb / c_target, 0.0), go = fmax(cb / c_target - 1.0, 0.0);
+        lr += gu * (mu / (double)B) + go * (mo / (double)B);
         lo += ov;
+        if (gates) gates[n] = make_double2(gu, go);
     }
     s_reg[threadIdx.x] = lr;
     s_over[threadIdx.x] = lo;
@@ -1751,7 +1791,7 @@ __global__ __launch_bounds__(kRegThreads) void k_reg_loss(const double* __restri
         }
         __syncthreads();
     }
-    if (threadIdx.x == 0) {
+    if (threadIdx.x == 0 && loss) {
         loss[0] = (float)(s_reg[0] / (double)N);
         loss[1] = (float)(s_over[0] / (double)N);
     }
@@ -1831,14 +1871,380 @@ extern "C" int lif_spike_count_reg(const float* ev_t, const int32_t* ev_src, con
         const size_t it = (size_t)B * R.f.S * tl;
         TIMED_LAUNCH("reg_walk", k_reg_walk, dim3((unsigned)((it + kWalkWaves - 1) / kWalkWaves)),
                      dim3(kWave * kWalkWaves), 0, stream, ev_t, ev_src, ev_n, E_max, R.f.E_pad, WT, C_in, N_out, tl,
-                     R.f.S, (int)it, m, P.dec, P.carry, out_t, out_n, out_k, part);
+                     R.f.S, (int)it, m, P.dec, P.carry, out_t, out_n, out_k, part, nullptr);
     }
     if (nn)
         TIMED_LAUNCH("reg_reduce", k_reg_reduce, dim3((unsigned)((nn + 255) / 256)), dim3(256), 0, stream, part, ev_n,
-                     B, E_max, N_out, R.f.S, m.th, ub, ob, under, over);
+                     B, E_max, N_out, R.f.S, m.th, ub, ob, under, over, nullptr);
     if (B > 0)
         TIMED_LAUNCH("reg_loss", k_reg_loss, dim3(1), dim3(kRegThreads), 0, stream, ub, ob, out_n, B, N_out, m.s_max,
-                     c_target, loss);
+                     c_target, loss, nullptr);
+    return check_launch();
+}
+
+// ---------------------------------------------------------------------------
+// Gradient of lam_reg L_reg + lam_over L_over (App. E.1, Eq. loss), the gates
+// held constant (functions of the spike counts).  Each V_max is the value of
+// its interval's trajectory at the argmax tau_j = t_{j-1} + u_j:
+//   V(tau) = sum_{k < j} w_k K(tau - t_k) - (V_th - V_reset) sum_{s: out_k < j} e^{-(tau - t_s)/tm},
+// so with mu_j = dL/dV_max of interval j (G_u for an active under-firing
+// interval, G_o for an active over-firing one, 0 otherwise) and
+//   P_k = sum_{j > k} mu_j e^{-(tau_j - t_k)/tm}    (Q_k the same with ts)
+// every input event k collects
+//   dL/dw_{i, src_k} += kappa (P_k - Q_k),   dL/dt_k += w kappa (P_k/tm - Q_k/ts)
+// (the adjoint sums of the layer's backward pass with a pseudo-spike at
+// each interval's argmax), an argmax at an interval end that is an input
+// time adds mu_j V'(tau_j) to that time's gradient, and spike s collects the
+// upstream spike-time gradient -((V_th - V_reset)/tm) P_{out_k} e^{-(t_{out_k} - t_s)/tm},
+// which the layer's backward pass carries to W and the input times.
+// P obeys P_{k-1} = A_k P_k + mu_k e^{-u_k/tm} (A_k the decay into event k),
+// a reverse affine scan: per segment a local sum from zero (k_regg_seg), a
+// reverse carry over segments (k_regg_carry), and the walk with the carry
+// (k_regg_walk).  dL/dW is added as 64-bit fixed-point integers (order
+// free); dL/dt per neuron tile, the tiles added in order.
+// ---------------------------------------------------------------------------
+namespace lif {
+
+__device__ __forceinline__ double rec_mu(const float4& r, const double2& G)
+{
+    const int code = (int)r.w;
+    return (code & kRecUnder) ? G.x : ((code & kRecOver) ? G.y : 0.0);
+}
+
+// Per (sample, neuron): G_u = -lam_reg gu / (N B nsil), G_o = (lam_reg go /
+// (N B) + lam_over gi / N) / nspk with gi = ReLU(c / c_target - 1) of its
+// spike count c, and |G_u| nsil + |G_o| nspk, a bound of its sums P and Q.
+__global__ __launch_bounds__(256) void k_regg_coef(const double2* __restrict__ counts,
+                                                   const double2* __restrict__ gates,
+                                                   const int32_t* __restrict__ out_n, int B, int N, int s_max,
+                                                   double c_target, double lam_reg, double lam_over,
+                                                   double2* __restrict__ coef, double* __restrict__ musum,
+                                                   long long* __restrict__ gw, size_t nW)
+{
+    const size_t gtid = (size_t)blockIdx.x * blockDim.x + threadIdx.x, gs = (size_t)gridDim.x * blockDim.x;
+    for (size_t x = gtid; x < nW; x += gs) gw[x] = 0;
+    const size_t nn = (size_t)B * N;
+    for (size_t i = gtid; i < nn; i += gs) {
+        const int n = (int)(i % (size_t)N);
+        const double2 cnt = counts[i], g = gates[n];
+        const double c = (double)min(out_n[i], s_max);
+        const double gi = fmax(c / c_target - 1.0, 0.0);
+        const double Gu = cnt.x > 0.0 ? -lam_reg * g.x / ((double)N * B) / cnt.x : 0.0;
+        const double Go = cnt.y > 0.0 ? (lam_reg * g.y / ((double)N * B) + lam_over * gi / (double)N) / cnt.y : 0.0;
+        coef[i] = make_double2(Gu, Go);
+        musum[i] = fabs(Gu) * cnt.x + fabs(Go) * cnt.y;
+    }
+}
+
+// Fixed-point scale of dL/dW (one workgroup): a contribution is at most
+// 2 kappa M (M = the largest bound of k_regg_coef; the float32 decays of the
+// records add far less than the bit of headroom), an element sums at most
+// one per event of the batch: scale = 2^(61 - ceil(log2(2 kappa M events))).
+__global__ __launch_bounds__(kRegThreads) void k_regg_scale(const double* __restrict__ musum, size_t nn,
+                                                            const int32_t* __restrict__ ev_n, int B, int E_max,
+                                                            double kappa, double* __restrict__ scale)
+{
+    __shared__ double s_max[kRegThreads], s_ev[kRegThreads];
+    double mx = 0.0, ev = 0.0;
+    for (size_t i = threadIdx.x; i < nn; i += kRegThreads) mx = fmax(mx, musum[i]);
+    for (int b = threadIdx.x; b < B; b += kRegThreads) ev += (double)clamp_count(ev_n[b], E_max);
+    s_max[threadIdx.x] = mx;
+    s_ev[threadIdx.x] = ev;
+    __syncthreads();
+    for (int off = kRegThreads / 2; off > 0; off >>= 1) {
+        if ((int)threadIdx.x < off) {
+            s_max[threadIdx.x] = fmax(s_max[threadIdx.x], s_max[threadIdx.x + off]);
+            s_ev[threadIdx.x] += s_ev[threadIdx.x + off];
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        const double bound = 2.0 * kappa * s_max[0] * fmax(s_ev[0], 1.0);
+        int ex = 0;
+        if (bound > 0.0 && isfinite(bound)) frexp(bound, &ex);
+        scale[0] = ldexp(1.0, 61 - ex);
+    }
+}
+
+// Per (sample, segment, 64 neurons): the segment's part of (P, Q) at its
+// first event k0 (the pseudo-spikes of intervals k0 + 1 .. k1 + 1, k1 the
+// segment's last event), and per (sample, segment) the decay from event
+// k1 + 1 back to k0.
+__global__ __launch_bounds__(kWave * kWalkWaves) void k_regg_seg(
+    const int32_t* __restrict__ ev_n, int E_max, int E_pad, int N, int tiles, int S, int items,
+    const Decay* __restrict__ dec, const float4* __restrict__ rec, const double2* __restrict__ coef,
+    double2* __restrict__ local, double2* __restrict__ factor)
+{
+    WalkCoords c;
+    if (!walk_coords<1>(items, tiles, S, ev_n, E_max, N, c)) return;
+    const int n = c.n0;
+    const Decay* d = dec + (size_t)c.b * E_pad;
+    const float4* rb = rec + (size_t)c.b * (E_max + 1) * N + n;
+    const double2 G = c.live ? coef[(size_t)c.b * N + n] : make_double2(0.0, 0.0);
+    const int k1 = c.k0 + c.cnt - 1;
+    double Pm = 0.0, Ps = 0.0, Fm = 1.0, Fs = 1.0;
+    for (int k = k1; k >= c.k0; --k) {
+        if (k < k1) {
+            const Decay e = d[k + 1];
+            Pm *= e.A;
+            Ps *= e.D;
+            Fm *= e.A;
+            Fs *= e.D;
+        }
+        const float4 r = rb[(size_t)(k + 1) * N];
+        const double mu = rec_mu(r, G);
+        Pm = fma(mu, (double)r.x, Pm);
+        Ps = fma(mu, (double)r.y, Ps);
+    }
+    if (k1 + 1 < c.nb) {
+        const Decay e = d[k1 + 1];
+        Fm *= e.A;
+        Fs *= e.D;
+    }
+    if (c.live) local[((size_t)c.b * S + c.seg) * N + n] = make_double2(Pm, Ps);
+    if (c.tile == 0 && c.lane == 0) factor[(size_t)c.b * S + c.seg] = make_double2(Fm, Fs);
+}
+
+// Per (sample, 64 neurons): the reverse carry over segments, cin[seg] =
+// (P, Q) at the first event of segment seg + 1 (0 for the last segment).
+__global__ __launch_bounds__(kWave) void k_regg_carry(const int32_t* __restrict__ ev_n, int E_max, int N, int S,
+                                                      const double2* __restrict__ factor,
+                                                      const double2* __restrict__ local, double2* __restrict__ cin)
+{
+    const int b = blockIdx.y, n = blockIdx.x * kWave + (int)threadIdx.x;
+    if (n >= N) return;
+    const int nb = clamp_count(ev_n[b], E_max);
+    const int Sb = (nb + kSeg - 1) / kSeg;
+    double Fm = 0.0, Fs = 0.0;
+#pragma unroll 8
+    for (int seg = Sb - 1; seg >= 0; --seg) {
+        const size_t at = ((size_t)b * S + seg) * N + n;
+        const double2 L = local[at], f = factor[(size_t)b * S + seg];
+        cin[at] = make_double2(Fm, Fs);
+        Fm = fma(f.x, Fm, L.x);
+        Fs = fma(f.y, Fs, L.y);
+    }
+}
+
+// Per (sample, segment, 64 neurons): (P_k, Q_k) from the segment's last
+// event down to its first, each event's contributions, and the upstream
+// gradient of the lane's spikes inside the segment.
+__global__ __launch_bounds__(kWave * kWalkWaves) void k_regg_walk(
+    const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int B,
+    int E_max, int E_pad, const float* __restrict__ WT, int C_in, int N, int tiles, int S, int items, Model m,
+    const Decay* __restrict__ dec, const float4* __restrict__ rec, const double2* __restrict__ coef,
+    const double2* __restrict__ cin, const float* __restrict__ out_t, const int32_t* __restrict__ out_n,
+    const int32_t* __restrict__ out_k, const double* __restrict__ scale, long long* __restrict__ gw,
+    double* __restrict__ gtp, float* __restrict__ grad_spike)
+{
+    WalkCoords c;
+    if (!walk_coords<1>(items, tiles, S, ev_n, E_max, N, c)) return;
+    const int n = c.n0;
+    const Decay* d = dec + (size_t)c.b * E_pad;
+    const float4* rb = rec + (size_t)c.b * (E_max + 1) * N + n;
+    const float* tt = ev_t + (size_t)c.b * E_max;
+    const int32_t* src = ev_src + (size_t)c.b * E_max;
+    const size_t bn = (size_t)c.b * N + n;
+    const double2 G = c.live ? coef[bn] : make_double2(0.0, 0.0);
+    const double sc = scale[0];
+    const int k1 = c.k0 + c.cnt - 1;
+    const double2 ci = cin[((size_t)c.b * S + c.seg) * N + n];
+    double Pm = ci.x, Ps = ci.y;
+    if (k1 + 1 < c.nb) {
+        const Decay e = d[k1 + 1];
+        Pm *= e.A;
+        Ps *= e.D;
+    }
+    float4 rn = rb[(size_t)(k1 + 1) * N];          // the interval after event k
+    double mun = rec_mu(rn, G);
+    Pm = fma(mun, (double)rn.x, Pm);
+    Ps = fma(mun, (double)rn.y, Ps);
+    // the lane's spikes in this segment, last first
+    const float* ts = out_t + bn * (size_t)m.s_max;
+    const int32_t* ks = out_k + bn * (size_t)m.s_max;
+    float* gsp = grad_spike + bn * (size_t)m.s_max;
+    int sp = c.live ? min(out_n[bn], m.s_max) : 0;
+    while (sp > 0 && ks[sp - 1] > k1) --sp;
+    double* gt = gtp + ((size_t)c.tile * B + c.b) * E_max;
+    for (int k = k1; k >= c.k0; --k) {
+        const float4 r = rb[(size_t)k * N];            // the interval that event k closes
+        const double mu = rec_mu(r, G);
+        const int j = clamp_src(src[k], C_in);
+        const double w = (double)WT[(size_t)j * N + n];
+        double g = w * m.kappa * (Pm * m.inv_tm - Ps * m.inv_ts);
+        if ((int)rn.w & kRecStart) g = fma(mun, (double)rn.z, g);
+        if ((int)r.w & kRecEnd) g = fma(mu, (double)r.z, g);
+        if (c.live) {
+            atomicAdd((unsigned long long*)&gw[(size_t)j * N + n],
+                      (unsigned long long)llrint(m.kappa * (Pm - Ps) * sc));
+            const double tk = (double)tt[k];
+            while (sp > 0 && ks[sp - 1] == k) {
+                --sp;
+                gsp[sp] += (float)(-(m.dth * m.inv_tm) * Pm * exp(-(tk - (double)ts[sp]) * m.inv_tm));
+            }
+        } else {
+            g = 0.0;
+        }
+        for (int off = kWave / 2; off > 0; off >>= 1) g += __shfl_xor(g, off, kWave);
+        if (c.lane == 0) gt[k] = g;
+        if (k > c.k0) {
+            const Decay e = d[k];
+            Pm = fma(mu, (double)r.x, Pm * e.A);
+            Ps = fma(mu, (double)r.y, Ps * e.D);
+        }
+        rn = r;
+        mun = mu;
+    }
+}
+
+// Fixed point -> float32 dL/dW; dL/dt summed over the tiles in order (0 past
+// each sample's last event).
+__global__ __launch_bounds__(256) void k_regg_convert(const long long* __restrict__ gw,
+                                                     const double* __restrict__ scale, size_t nW,
+                                                     float* __restrict__ grad_WT, const double* __restrict__ gtp,
+                                                     const int32_t* __restrict__ ev_n, int B, int E_max, int tiles,
+                                                     float* __restrict__ grad_ev_t)
+{
+    const size_t gtid = (size_t)blockIdx.x * blockDim.x + threadIdx.x, gs = (size_t)gridDim.x * blockDim.x;
+    const double inv = 1.0 / scale[0];
+    for (size_t x = gtid; x < nW; x += gs) grad_WT[x] = (float)((double)gw[x] * inv);
+    if (!grad_ev_t) return;
+    const size_t nT = (size_t)B * E_max;
+    for (size_t x = gtid; x < nT; x += gs) {
+        const int b = (int)(x / (size_t)E_max), k = (int)(x % (size_t)E_max);
+        double g = 0.0;
+        if (k < clamp_count(ev_n[b], E_max))
+            for (int t = 0; t < tiles; ++t) g += gtp[(size_t)t * nT + x];
+        grad_ev_t[x] = (float)g;
+    }
+}
+
+struct RegGradLayout {
+    RegLayout r;
+    size_t rec, counts, gates, coef, musum, scale, local, factor, cin, gw, gtp, total;
+};
+
+static RegGradLayout reg_grad_layout(int B, int E_max, int C_in, int N)
+{
+    RegGradLayout G;
+    G.r = reg_layout(B, E_max, N);
+    size_t off = G.r.total;
+    auto take = [&](size_t bytes) { size_t o = off; off += (bytes + 255) & ~(size_t)255; return o; };
+    const size_t BS = (size_t)B * G.r.f.S;
+    const int tiles = (N + kWave - 1) / kWave;
+    G.rec = take((size_t)B * ((size_t)E_max + 1) * N * sizeof(float4));
+    G.counts = take((size_t)B * N * sizeof(double2));
+    G.gates = take((size_t)N * sizeof(double2));
+    G.coef = take((size_t)B * N * sizeof(double2));
+    G.musum = take((size_t)B * N * sizeof(double));
+    G.scale = take(sizeof(double));
+    G.local = take(BS * N * sizeof(double2));
+    G.factor = take(BS * sizeof(double2));
+    G.cin = take(BS * N * sizeof(double2));
+    G.gw = take((size_t)C_in * N * sizeof(long long));
+    G.gtp = take((size_t)tiles * B * E_max * sizeof(double));
+    G.total = off + 256;
+    return G;
+}
+
+}  // namespace lif
+
+extern "C" size_t lif_spike_count_reg_backward_workspace_size(int B, int E_max, int C_in, int N_out)
+{
+    if (B < 0 || E_max < 0 || C_in < 1 || N_out < 1) return 0;
+    return lif::reg_grad_layout(B, E_max, C_in, N_out).total;
+}
+
+extern "C" int lif_spike_count_reg_backward(const float* ev_t, const int32_t* ev_src, const int32_t* ev_n, int B,
+                                            int E_max, const float* WT, int C_in, int N_out, const lif_params* p,
+                                            const float* out_t, const int32_t* out_n, const int32_t* out_k,
+                                            double c_target, double lam_reg, double lam_over, float* loss,
+                                            float* grad_spike, float* grad_WT, float* grad_ev_t, void* ws,
+                                            size_t ws_bytes, lif_stream_t stream_)
+{
+    using namespace lif;
+    int rc = validate_forward_args(ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, p, out_t, out_n, out_n);
+    if (rc) return rc;
+    if (!out_k || !grad_spike || !grad_WT || !ws || !(c_target > 0.0) || !isfinite(c_target) ||
+        !isfinite(lam_reg) || !isfinite(lam_over))
+        return LIF_ERR_ARG;
+    const RegGradLayout G = reg_grad_layout(B, E_max, C_in, N_out);
+    if (ws_bytes < G.total) return LIF_ERR_WORKSPACE;
+    const int tl = (N_out + kWave - 1) / kWave;
+    const size_t items_max = (size_t)B * G.r.f.S * tl;
+    if (items_max > 0x7fffffff || B > 65535) return LIF_ERR_SIZE;
+    hipStream_t stream = (hipStream_t)stream_;
+    const Model m = make_model(*p);
+    char* base = (char*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
+    const RegLayout& R = G.r;
+    FwdPtrs P{};
+    P.dec = (Decay*)(base + R.f.dec);
+    P.segm = (double2*)(base + R.f.segm);
+    P.carry = (double2*)(base + R.f.carry);
+    P.mask = (uint32_t*)(base + R.f.mask);
+    P.counters = (uint32_t*)(base + R.f.counters);
+    P.pool_count = P.counters;
+    P.nwork = P.counters + (size_t)B * kCtr;
+    P.listed = (uint32_t*)(base + R.f.listed);
+    P.work = (uint32_t*)(base + R.f.work);
+    P.pool = (double2*)(base + R.f.pool);
+    double4* part = (double4*)(base + R.part);
+    double* ub = (double*)(base + R.ub);
+    double* ob = (double*)(base + R.ob);
+    int32_t* st = (int32_t*)(base + R.status);
+    float4* rec = (float4*)(base + G.rec);
+    double2* counts = (double2*)(base + G.counts);
+    double2* gates = (double2*)(base + G.gates);
+    double2* coef = (double2*)(base + G.coef);
+    double* musum = (double*)(base + G.musum);
+    double* scale = (double*)(base + G.scale);
+    double2* local = (double2*)(base + G.local);
+    double2* factor = (double2*)(base + G.factor);
+    double2* cin = (double2*)(base + G.cin);
+    long long* gw = (long long*)(base + G.gw);
+    double* gtp = (double*)(base + G.gtp);
+    const size_t nn = (size_t)B * N_out, nW = (size_t)C_in * N_out;
+    const unsigned wblocks = (unsigned)((items_max + kWalkWaves - 1) / kWalkWaves);
+    if (items_max > 0) {
+        switch (pick_npl(WT, N_out)) {
+        case 4: launch_walks<4>(R.f, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, m, st, false, nullptr, nullptr,
+                                nullptr, nullptr, stream, false); break;
+        case 2: launch_walks<2>(R.f, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, m, st, false, nullptr, nullptr,
+                                nullptr, nullptr, stream, false); break;
+        default: launch_walks<1>(R.f, P, ev_t, ev_src, ev_n, B, E_max, WT, C_in, N_out, m, st, false, nullptr,
+                                 nullptr, nullptr, nullptr, stream, false); break;
+        }
+        TIMED_LAUNCH("reg_walk", k_reg_walk, dim3(wblocks), dim3(kWave * kWalkWaves), 0, stream, ev_t, ev_src, ev_n,
+                     E_max, R.f.E_pad, WT, C_in, N_out, tl, R.f.S, (int)items_max, m, P.dec, P.carry, out_t, out_n,
+                     out_k, part, rec);
+    }
+    if (nn)
+        TIMED_LAUNCH("reg_reduce", k_reg_reduce, dim3((unsigned)((nn + 255) / 256)), dim3(256), 0, stream, part, ev_n,
+                     B, E_max, N_out, R.f.S, m.th, ub, ob, nullptr, nullptr, counts);
+    if (B > 0)
+        TIMED_LAUNCH("reg_loss", k_reg_loss, dim3(1), dim3(kRegThreads), 0, stream, ub, ob, out_n, B, N_out, m.s_max,
+                     c_target, loss, gates);
+    size_t work = nW > nn ? nW : nn;
+    size_t blocks = (work + 255) / 256;
+    blocks = blocks < 1 ? 1 : (blocks > 2048 ? 2048 : blocks);
+    TIMED_LAUNCH("regg_coef", k_regg_coef, dim3((unsigned)blocks), dim3(256), 0, stream, counts, gates, out_n, B,
+                 N_out, m.s_max, c_target, lam_reg, lam_over, coef, musum, gw, nW);
+    TIMED_LAUNCH("regg_scale", k_regg_scale, dim3(1), dim3(kRegThreads), 0, stream, musum, nn, ev_n, B, E_max,
+                 m.kappa, scale);
+    if (items_max > 0) {
+        TIMED_LAUNCH("regg_seg", k_regg_seg, dim3(wblocks), dim3(kWave * kWalkWaves), 0, stream, ev_n, E_max,
+                     R.f.E_pad, N_out, tl, R.f.S, (int)items_max, P.dec, rec, coef, local, factor);
+        TIMED_LAUNCH("regg_carry", k_regg_carry, dim3((unsigned)tl, (unsigned)B), dim3(kWave), 0, stream, ev_n, E_max,
+                     N_out, R.f.S, factor, local, cin);
+        TIMED_LAUNCH("regg_walk", k_regg_walk, dim3(wblocks), dim3(kWave * kWalkWaves), 0, stream, ev_t, ev_src, ev_n,
+                     B, E_max, R.f.E_pad, WT, C_in, N_out, tl, R.f.S, (int)items_max, m, P.dec, rec, coef, cin, out_t,
+                     out_n, out_k, scale, gw, gtp, grad_spike);
+    }
+    work = nW > (size_t)B * E_max ? nW : (size_t)B * E_max;
+    blocks = (work + 255) / 256;
+    blocks = blocks < 1 ? 1 : (blocks > 2048 ? 2048 : blocks);
+    TIMED_LAUNCH("regg_convert", k_regg_convert, dim3((unsigned)blocks), dim3(256), 0, stream, gw, scale, nW, grad_WT,
+                 gtp, ev_n, B, E_max, tl, grad_ev_t);
     return check_launch();
 }
 

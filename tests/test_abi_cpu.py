@@ -232,3 +232,23 @@ def test_delay_argument_errors(lib):
     assert need > 0 and b(19, need - 1) == L.LIF_ERR_WORKSPACE
     bad = L.Params(tau_mem=0.001).c()
     assert b(9, ctypes.byref(bad)) == L.LIF_ERR_TAU
+
+
+def test_spike_count_reg_backward_argument_errors(lib):
+    p = L.Params().c()
+    # ev_t, ev_src, ev_n, B, E, WT, C, N, p, out_t, out_n, out_k, c_target, lam_reg, lam_over, loss, g_spike, gW, gT,
+    # ws, ws_bytes, stream
+    base = [F, F, F, 2, 10, F, 4, 8, ctypes.byref(p), F, F, F, 4.0, 1.0, 1.0, None, F, F, None, F, 10 ** 9, None]
+
+    def call(i, v):
+        a = list(base)
+        a[i] = v
+        return L.lif_spike_count_reg_backward(*a)
+    assert call(11, None) == L.LIF_ERR_ARG          # out_k required
+    assert call(16, None) == L.LIF_ERR_ARG          # grad_spike required
+    assert call(17, None) == L.LIF_ERR_ARG          # grad_WT required
+    assert call(12, -1.0) == L.LIF_ERR_ARG          # c_target > 0
+    assert call(13, math.inf) == L.LIF_ERR_ARG      # finite lambda
+    need = L.lif_spike_count_reg_backward_workspace_size(2, 10, 4, 8)
+    assert need > L.lif_spike_count_reg_workspace_size(2, 10, 4, 8)
+    assert call(20, need - 1) == L.LIF_ERR_WORKSPACE

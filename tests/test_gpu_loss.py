@@ -179,3 +179,52 @@ def test_spike_count_regularisers(env, t_end, vr):
     assert abs(loss[0].item() - L_reg) <= 1e-5 * abs(L_reg), (loss[0].item(), L_reg)
     assert abs(loss[1].item() - L_over) <= 1e-5 * max(abs(L_over), 1e-12), (loss[1].item(), L_over)
     assert torch.equal(loss.view(torch.int32), loss2.view(torch.int32))
+
+
+@pytest.mark.parametrize("t_end,vr", [(math.inf, 0.0), (0.5, -0.3)])
+def test_spike_count_regulariser_gradients(env, t_end, vr):
+    """The gradient of lam_reg L_reg + lam_over L_over: the loss values, the
+    upstream spike-time gradient and the direct weight and input-time parts
+    against the oracle on identical inputs (the oracle's spike trains in
+    float32), then the full weight and input-time gradients through the
+    layer's backward pass."""
+    from tests.parity import compare_grad
+    torch, lif = env
+    cfg = W.random_small(51, B=4, C=40, N=70, n_events=600, T=0.4, gain=6.0)
+    ev, WT = cfg.events, cfg.layers[0].WT
+    ev.ev_n[2] = 0
+    P = oracle.LifParams(s_max=64, t_end=t_end, v_reset=vr)
+    r = oracle.forward(ev.ev_t, ev.ev_src, ev.ev_n, WT, P)
+    assert r.out_n.sum() > 100 and not r.capped.any()
+    c_target = float(np.median(r.out_n.mean(axis=0))) + 0.5
+    rp = OL.RegParams(c_target=c_target, lam_reg=0.8, lam_over=0.3)
+    r32 = r.rounded()
+    print(f"[case] regulariser gradients t_end={t_end} v_reset={vr} spikes={int(r.out_n.sum())} "
+          f"c_target={c_target}", flush=True)
+    L_reg, L_over, gWd, gTd, gS = OL.spike_count_reg_grad(ev.ev_t, ev.ev_src, ev.ev_n, WT, r32.out_t, r.out_k,
+                                                         r.out_n, P.tau_mem, P.tau_syn, P.v_th, P.v_reset, P.t_end, rp)
+    gWs, gTs = oracle.backward(ev.ev_t, ev.ev_src, ev.ev_n, WT, r32, gS, P)
+    fwd = lif.ForwardOut(_dev(torch, r32.out_t.astype(np.float32)), _dev(torch, r.out_n),
+                         _dev(torch, r32.out_i.astype(np.float32)), None, _dev(torch, r.out_k))
+    args = [_dev(torch, a) for a in (ev.ev_t, ev.ev_src, ev.ev_n, WT)]
+    lp = lif.Params(s_max=64, t_end=t_end, v_reset=vr)
+    seed = torch.full((ev.B, WT.shape[1], 64), 0.25, device="cuda:0") * fwd.out_t.isfinite()
+    loss, gsp, gW, gT = lif.spike_count_reg_backward(*args, fwd, c_target, 0.8, 0.3, lp, grad_spike=seed.clone())
+    torch.cuda.synchronize()
+    assert abs(loss[0].item() - L_reg) <= 1e-5 * abs(L_reg) and abs(loss[1].item() - L_over) <= 1e-5 * max(
+        abs(L_over), 1e-12)
+    g_spike = (gsp - seed).cpu().numpy()
+    assert np.abs(gS).max() > 0 and np.abs(gWd).max() > 0
+    es = compare_grad(g_spike, gS, label="regulariser spike-time gradient")
+    ew = compare_grad(gW.cpu().numpy(), gWd, label="regulariser direct grad_W")
+    et = compare_grad(gT.cpu().numpy(), gTd, label="regulariser direct grad_t")
+    # the full gradient: direct part plus the layer's backward of the spike-time part
+    bW, bT = lif.backward(*args, fwd, gsp - seed, lp)
+    torch.cuda.synchronize()
+    fw = compare_grad((gW + bW).cpu().numpy(), gWd + gWs, label="regulariser grad_W")
+    ft = compare_grad((gT + bT).cpu().numpy(), gTd + gTs, label="regulariser grad_t")
+    print(f"    rel spike {es:.2e} direct W {ew:.2e} t {et:.2e}; full W {fw:.2e} t {ft:.2e}", flush=True)
+    # bitwise reproducible
+    loss2, gsp2, gW2, gT2 = lif.spike_count_reg_backward(*args, fwd, c_target, 0.8, 0.3, lp, grad_spike=seed.clone())
+    for a, b_ in ((loss, loss2), (gsp, gsp2), (gW, gW2), (gT, gT2)):
+        assert torch.equal(a.view(torch.int32), b_.view(torch.int32))
