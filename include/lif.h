@@ -425,6 +425,17 @@ typedef struct lif_adam_params {
 int lif_adam_step(float* param, const float* grad, float* m1, float* m2, size_t n, const lif_adam_params* a,
                   int step, lif_stream_t stream);
 
+/* Elementwise pieces of the training step.  lif_add: y[i] += x[i] (adds the
+ * direct part of a regulariser gradient to a layer's gradient).
+ * lif_softplus: d[i] = log(1 + e^{beta x[i]}) / beta, the delay activation
+ * of App. E.5 (beta = the softplus sharpness, > 0); lif_softplus_grad:
+ * grad_x[i] = grad_d[i] sigmoid(beta x[i]).  Computed in float64, stored in
+ * float32; LIF_ERR_ARG on a null pointer with n > 0 or beta <= 0. */
+int lif_add(float* y, const float* x, size_t n, lif_stream_t stream);
+int lif_softplus(const float* x, float* d, size_t n, double beta, lif_stream_t stream);
+int lif_softplus_grad(const float* x, const float* grad_d, float* grad_x, size_t n, double beta,
+                      lif_stream_t stream);
+
 /* --------------------------------------------------------------------- */
 /* Optional kernel timer (host-side state, off by default).  When enabled, */
 /* every kernel launched by this library is launched with a pair of HIP    */

@@ -53,7 +53,7 @@ EXPORTED = ["lif_version", "lif_layer_forward_workspace_size", "lif_layer_forwar
             "lif_delay_queues_workspace_size", "lif_delay_queues",
             "lif_layer_forward_delayed", "lif_layer_forward_delayed_sequential",
             "lif_layer_backward_delayed_workspace_size", "lif_layer_backward_delayed",
-            "lif_timer_enable", "lif_timer_read"]
+            "lif_add", "lif_softplus", "lif_softplus_grad", "lif_timer_enable", "lif_timer_read"]
 LIF_LI_MAX_CLASSES = 64
 
 
@@ -195,6 +195,12 @@ def load(path: Optional[str] = None):
     lib.lif_layer_backward_delayed.restype = _I
     lib.lif_layer_backward_delayed.argtypes = [_P, _P, _P, _P, _I, _I, _P, _I, _I, _PP, _P, _P, _P, _P, _P, _P, _P,
                                                _P, _P, _SZ, _P]
+    lib.lif_add.restype = _I
+    lib.lif_add.argtypes = [_P, _P, _SZ, _P]
+    lib.lif_softplus.restype = _I
+    lib.lif_softplus.argtypes = [_P, _P, _SZ, ctypes.c_double, _P]
+    lib.lif_softplus_grad.restype = _I
+    lib.lif_softplus_grad.argtypes = [_P, _P, _P, _SZ, ctypes.c_double, _P]
     lib.lif_timer_enable.restype = None
     lib.lif_timer_enable.argtypes = [_I]
     lib.lif_timer_read.restype = _I
@@ -312,6 +318,18 @@ def lif_layer_backward_delayed(*args) -> int:
     return load().lif_layer_backward_delayed(*args)
 
 
+def lif_add(*args) -> int:
+    return load().lif_add(*args)
+
+
+def lif_softplus(*args) -> int:
+    return load().lif_softplus(*args)
+
+
+def lif_softplus_grad(*args) -> int:
+    return load().lif_softplus_grad(*args)
+
+
 def lif_timer_enable(on: bool) -> None:
     load().lif_timer_enable(1 if on else 0)
 
@@ -368,6 +386,7 @@ class ForwardOut:
     out_i: "object"     # float32 [B, N, s_max]
     status: "object"    # int32 [LIF_STATUS_WORDS]
     out_k: "object" = None   # int32 [B, N, s_max]: input events consumed before each spike
+    queues: "object" = None  # the per-neuron queues of a layer with delays (DelayQueues), else None
 
 
 def forward(ev_t, ev_src, ev_n, WT, params: Params = Params(), sequential: bool = False, stream=None,
@@ -636,3 +655,26 @@ def spike_count_reg_backward(ev_t, ev_src, ev_n, WT, fwd: ForwardOut, c_target: 
                                       _ptr(gT), _ptr(ws), ws.numel(), _stream(stream))
     _check("lif_spike_count_reg_backward", rc)
     return loss, grad_spike, gW, gT
+
+
+def add_(y, x, stream=None):
+    """y += x on the device (lif_add); returns y."""
+    if y.shape != x.shape or y.dtype != x.dtype:
+        raise ValueError("add_: shapes and dtypes must match")
+    _check("lif_add", lif_add(_ptr(y), _ptr(x.contiguous()), y.numel(), _stream(stream)))
+    return y
+
+
+def softplus(x, beta: float, stream=None):
+    """d = softplus(x) = log(1 + e^{beta x}) / beta (lif_softplus)."""
+    d = _torch().empty_like(x)
+    _check("lif_softplus", lif_softplus(_ptr(x), _ptr(d), x.numel(), float(beta), _stream(stream)))
+    return d
+
+
+def softplus_grad(x, grad_d, beta: float, stream=None):
+    """grad_x = grad_d * sigmoid(beta x) (lif_softplus_grad)."""
+    gx = _torch().empty_like(x)
+    _check("lif_softplus_grad", lif_softplus_grad(_ptr(x), _ptr(grad_d), _ptr(gx), x.numel(), float(beta),
+                                                  _stream(stream)))
+    return gx
