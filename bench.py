@@ -170,23 +170,36 @@ def run_workload(torch, lif, d, name, ev, WT, P, steps, warmup, seq_steps, backw
     return r
 
 
-def train_step(torch, lif, d, c3, steps, warmup):
+def train_step(torch, lif, d, c3, steps, warmup, variant="plain"):
     """The paper's training step (two LIF layers, merges, weighted LI readout
     with temperature cross-entropy, backward through both merges, Adam) at
     config 3's shape with a 512 -> 20 readout, with the parallel layers and
-    with the sequential baseline in their place."""
-    from paper_2603_13283_amd.train import AdamParams, TwoLayerNet
+    with the sequential baseline in their place.  variant "reg" adds the
+    spike-count regularisers to both hidden layers (targets 14, lambda_reg
+    1e-3, lambda_over 5e-5, as the paper's SHD model), "delays" learnable
+    delays on both hidden layers (initial delays U[0, 0.1) s, softplus
+    sharpness 5)."""
+    from paper_2603_13283_amd.train import AdamParams, DelayConfig, RegConfig, TwoLayerNet
     ev = c3.events
     rng = np.random.default_rng(11)
     Wo = (rng.normal(0, 1, (512, 20)) * 4.0 / np.sqrt(512)).astype(np.float32)
     labels = d(rng.integers(0, 20, ev.B).astype(np.int32))
     inp = [d(ev.ev_t), d(ev.ev_src), d(ev.ev_n)]
+    extra = {"plain": "", "reg": " + spike-count regularisers on both hidden layers",
+             "delays": " + learnable delays on both hidden layers"}[variant]
     out = {"workload": "700->512->512 LIF + 512->20 weighted LI readout, B=128, ~10k events; forward, "
-                       "cross-entropy, backward through both merges, Adam on all three weight matrices"}
+                       "cross-entropy, backward through both merges, Adam on all parameters" + extra}
+    beta = 5.0
+    raw = lambda shape: d((np.log(np.expm1(beta * rng.uniform(1e-3, 0.1, shape))) / beta).astype(np.float32))
     for name, seq in (("parallel", False), ("sequential", True)):
+        kw = {}
+        if variant == "reg":
+            kw["reg"] = RegConfig(c_target=(14.0, 14.0), lam_reg=1e-3, lam_over=5e-5)
+        elif variant == "delays":
+            kw["delays"] = DelayConfig(raw((700, 512)), raw((512, 512)), beta=beta, adam=AdamParams(lr=1e-3))
         net = TwoLayerNet(d(c3.layers[0].WT), d(c3.layers[1].WT), d(Wo), B=ev.B, E_max=ev.E_max,
                           P1=lif.Params(s_max=128), P2=lif.Params(s_max=128),
-                          q=lif.LiParams(tau_li=0.5, tau_max=1.0, beta=0.05), adam=AdamParams(lr=1e-3))
+                          q=lif.LiParams(tau_li=0.5, tau_max=1.0, beta=0.05), adam=AdamParams(lr=1e-3), **kw)
         r = net.step(*inp, labels, sequential=seq)
         torch.cuda.synchronize()
         ms, ev_ms = time_steps(torch, lambda: net.step(*inp, labels, sequential=seq), steps if not seq else 3,
@@ -199,8 +212,8 @@ def train_step(torch, lif, d, c3, steps, warmup):
             out["loss_first_step"] = float(r.loss.item())
         del net, r
     out["speedup_vs_sequential"] = out["sequential_ms"] / out["parallel_ms"]
-    log(f"[bench] training step: {out['parallel_ms']:.2f} ms parallel, {out['sequential_ms']:.2f} ms with the "
-        f"sequential layers ({out['speedup_vs_sequential']:.1f}x)")
+    log(f"[bench] training step{extra}: {out['parallel_ms']:.2f} ms parallel, {out['sequential_ms']:.2f} ms with "
+        f"the sequential layers ({out['speedup_vs_sequential']:.1f}x)")
     return out
 
 
@@ -411,6 +424,8 @@ def main():
         extras["c5_hidden_driven"] = run_workload(torch, lif, d, "32768->2048, B=16, ~100k events, gain 16",
                                                   c5.events, W1d, lif.Params(s_max=64), st, wu, 1, backward=True)
         extras["train_step_c3"] = train_step(torch, lif, d, c3, st, wu)
+        extras["train_step_c3_reg"] = train_step(torch, lif, d, c3, st, wu, "reg")
+        extras["train_step_c3_delays"] = train_step(torch, lif, d, c3, st, wu, "delays")
         extras["chunk_mode_c2"] = chunk_study(torch, lif, d, ev, WT, st, wu, seq_ms)
         extras["delays_c2"] = delay_study(torch, lif, d, ev, WT, st, wu, 1)
         del c3, c4, c5, W1d
