@@ -1601,25 +1601,29 @@ __device__ __forceinline__ RegArg reg_vmax_arg(const Model& m, double V0, double
     return r;
 }
 
-// Per-interval record for the regularisers' gradient (interval j of a
-// (sample, neuron), rec[(b (E_max + 1) + j) N + n]): the decays at the
-// argmax, the slope V' there when the argmax is an interval end that is an
-// input time (0 otherwise), and a code: 1 under-firing term active (silent,
-// V_max < V_th), 2 over-firing term active (spiked, V_max > V_th), 0 none,
-// plus 4 when the argmax is the start (input event j - 1) and 8 when it is
-// the end (input event j).
-constexpr int kRecUnder = 1, kRecOver = 2, kRecStart = 4, kRecEnd = 8;
+// Per-interval record for the regularisers' gradient, interval j of a
+// (sample, neuron) at rec[(b (E_max + 1) + j) N + n], float2 {x, y}: the sign
+// of x is the active hinge (> 0 under-firing: silent with V_max < V_th;
+// < 0 over-firing: spiked with V_max > V_th; 0 none) and |x| the argmax:
+// e^{-u/tm} in (0, 1) for a stationary point inside (then y = e^{-u/ts}),
+// kRecStart for the interval's start, kRecEnd for its end (then y = the
+// slope V' there when that point is an input time, else 0; the decays of an
+// end are the interval's own).
+constexpr float kRecStart = 2.0f, kRecEnd = 3.0f;
 
 // Per (sample, segment, 64 neurons): the segment's intervals (and the open
 // one in the sample's last segment); per lane the sums of the hinge terms
 // and the interval counts, part = (sum under, silent count, sum over,
-// spiking count); with rec, the per-interval records.
+// spiking count); with rec, the per-interval records and, per (sample,
+// segment, neuron), the sums over the segment's active intervals of the
+// decays from the segment's start (the input event before it) to the
+// interval's argmax, local = (under: e^{-./tm}, e^{-./ts}; over: the same).
 __global__ __launch_bounds__(kWave * kWalkWaves) void k_reg_walk(
     const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int E_max,
     int E_pad, const float* __restrict__ WT, int C_in, int N, int tiles, int S, int items, Model m,
     const Decay* __restrict__ dec, const double2* __restrict__ carry, const float* __restrict__ out_t,
     const int32_t* __restrict__ out_n, const int32_t* __restrict__ out_k, double4* __restrict__ part,
-    float4* __restrict__ rec)
+    float2* __restrict__ rec, double4* __restrict__ local)
 {
     __shared__ double2 s_ad[kWalkWaves][kSeg];
     __shared__ float s_t[kWalkWaves][kSeg + 1];
@@ -1657,7 +1661,9 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_reg_walk(
     }
     double su = 0.0, so = 0.0;
     int nsil = 0, nspk = 0;
-    float4* rb = rec ? rec + (size_t)c.b * (E_max + 1) * N + n : nullptr;
+    float2* rb = rec ? rec + (size_t)c.b * (E_max + 1) * N + n : nullptr;
+    double cdm = 1.0, cds = 1.0;                 // decays from the segment's start to the interval's start
+    double4 loc = make_double4(0.0, 0.0, 0.0, 0.0);
     auto take = [&](int j, double L, double A, double Dd, double t1) {
         const double V0 = v_of(m, U, J) - Dft;
         const RegArg ra = reg_vmax_arg(m, V0, J, L, A, Dd);
@@ -1671,16 +1677,28 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_reg_walk(
             ++nsil;
         }
         if (rb && c.live) {
-            int code = spiked ? (vmax > m.th ? kRecOver : 0) : (vmax < m.th ? kRecUnder : 0);
-            double vp = 0.0;
-            if (code && ra.at_start && j > 0) {
-                code |= kRecStart;
-                vp = (J - V0) * m.inv_tm;
-            } else if (code && ra.at_end && j < c.nb) {
-                code |= kRecEnd;
-                vp = (J * Dd - ra.vmax) * m.inv_tm;
+            const float sgn = spiked ? (vmax > m.th ? -1.0f : 0.0f) : (vmax < m.th ? 1.0f : 0.0f);
+            float x, y;
+            if (ra.at_start) {
+                x = kRecStart;
+                y = j > 0 ? (float)((J - V0) * m.inv_tm) : 0.0f;
+            } else if (ra.at_end && j < c.nb) {
+                x = kRecEnd;
+                y = (float)((J * Dd - ra.vmax) * m.inv_tm);
+            } else {                             // inside, or the end t_end of the open interval
+                x = (float)ra.em;
+                y = (float)ra.es;
             }
-            rb[(size_t)j * N] = make_float4((float)ra.em, (float)ra.es, (float)vp, (float)code);
+            rb[(size_t)j * N] = make_float2(sgn * x, sgn != 0.0f ? y : 0.0f);
+            if (sgn > 0.0f) {
+                loc.x = fma(cdm, ra.em, loc.x);
+                loc.y = fma(cds, ra.es, loc.y);
+            } else if (sgn < 0.0f) {
+                loc.z = fma(cdm, ra.em, loc.z);
+                loc.w = fma(cds, ra.es, loc.w);
+            }
+            cdm *= A;
+            cds *= Dd;
         }
         // the deficit at the interval's end, with the spikes inside it
         Dft *= A;
@@ -1718,6 +1736,7 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_reg_walk(
         take(c.nb, L, A, Dd, m.t_end);
     }
     if (c.live) part[((size_t)c.b * S + c.seg) * N + n] = make_double4(su, (double)nsil, so, (double)nspk);
+    if (local && c.live) local[((size_t)c.b * S + c.seg) * N + n] = loc;
 }
 
 // Per (sample, neuron): the sums over the segments in order, then the means
@@ -1871,7 +1890,7 @@ extern "C" int lif_spike_count_reg(const float* ev_t, const int32_t* ev_src, con
         const size_t it = (size_t)B * R.f.S * tl;
         TIMED_LAUNCH("reg_walk", k_reg_walk, dim3((unsigned)((it + kWalkWaves - 1) / kWalkWaves)),
                      dim3(kWave * kWalkWaves), 0, stream, ev_t, ev_src, ev_n, E_max, R.f.E_pad, WT, C_in, N_out, tl,
-                     R.f.S, (int)it, m, P.dec, P.carry, out_t, out_n, out_k, part, nullptr);
+                     R.f.S, (int)it, m, P.dec, P.carry, out_t, out_n, out_k, part, nullptr, nullptr);
     }
     if (nn)
         TIMED_LAUNCH("reg_reduce", k_reg_reduce, dim3((unsigned)((nn + 255) / 256)), dim3(256), 0, stream, part, ev_n,
@@ -1898,17 +1917,45 @@ extern "C" int lif_spike_count_reg(const float* ev_t, const int32_t* ev_src, con
 // upstream spike-time gradient -((V_th - V_reset)/tm) P_{out_k} e^{-(t_{out_k} - t_s)/tm},
 // which the layer's backward pass carries to W and the input times.
 // P obeys P_{k-1} = A_k P_k + mu_k e^{-u_k/tm} (A_k the decay into event k),
-// a reverse affine scan: per segment a local sum from zero (k_regg_seg), a
-// reverse carry over segments (k_regg_carry), and the walk with the carry
+// a reverse affine scan: per segment the sums over its own intervals (taken
+// by k_reg_walk on its forward walk, split by hinge so that the multipliers,
+// known only once the whole batch is walked, enter later), a reverse carry
+// over segments (k_regg_carry), and the walk back with the carry
 // (k_regg_walk).  dL/dW is added as 64-bit fixed-point integers (order
 // free); dL/dt per neuron tile, the tiles added in order.
 // ---------------------------------------------------------------------------
 namespace lif {
 
-__device__ __forceinline__ double rec_mu(const float4& r, const double2& G)
+// A record decoded with the interval's own decays (A, D): the multiplier mu
+// of its pseudo-spike (dL/dV_max), the decays at its argmax, and its
+// end-point slope term: at the start (the input event before the interval)
+// or at the end (the event that closes it).
+struct RecTerm {
+    double mu, em, es, vp;
+    bool at_start, at_end;
+};
+
+__device__ __forceinline__ RecTerm rec_term(const float2& r, const double2& G, double A, double D)
 {
-    const int code = (int)r.w;
-    return (code & kRecUnder) ? G.x : ((code & kRecOver) ? G.y : 0.0);
+    RecTerm t{0.0, 0.0, 0.0, 0.0, false, false};
+    if (r.x == 0.0f) return t;
+    t.mu = r.x > 0.0f ? G.x : G.y;
+    const float a = fabsf(r.x);
+    if (a == kRecStart) {
+        t.em = 1.0;
+        t.es = 1.0;
+        t.vp = (double)r.y;
+        t.at_start = true;
+    } else if (a == kRecEnd) {
+        t.em = A;
+        t.es = D;
+        t.vp = (double)r.y;
+        t.at_end = true;
+    } else {
+        t.em = (double)a;
+        t.es = (double)r.y;
+    }
+    return t;
 }
 
 // Per (sample, neuron): G_u = -lam_reg gu / (N B nsil), G_o = (lam_reg go /
@@ -1966,63 +2013,30 @@ __global__ __launch_bounds__(kRegThreads) void k_regg_scale(const double* __rest
     }
 }
 
-// Per (sample, segment, 64 neurons): the segment's part of (P, Q) at its
-// first event k0 (the pseudo-spikes of intervals k0 + 1 .. k1 + 1, k1 the
-// segment's last event), and per (sample, segment) the decay from event
-// k1 + 1 back to k0.
-__global__ __launch_bounds__(kWave * kWalkWaves) void k_regg_seg(
-    const int32_t* __restrict__ ev_n, int E_max, int E_pad, int N, int tiles, int S, int items,
-    const Decay* __restrict__ dec, const float4* __restrict__ rec, const double2* __restrict__ coef,
-    double2* __restrict__ local, double2* __restrict__ factor)
-{
-    WalkCoords c;
-    if (!walk_coords<1>(items, tiles, S, ev_n, E_max, N, c)) return;
-    const int n = c.n0;
-    const Decay* d = dec + (size_t)c.b * E_pad;
-    const float4* rb = rec + (size_t)c.b * (E_max + 1) * N + n;
-    const double2 G = c.live ? coef[(size_t)c.b * N + n] : make_double2(0.0, 0.0);
-    const int k1 = c.k0 + c.cnt - 1;
-    double Pm = 0.0, Ps = 0.0, Fm = 1.0, Fs = 1.0;
-    for (int k = k1; k >= c.k0; --k) {
-        if (k < k1) {
-            const Decay e = d[k + 1];
-            Pm *= e.A;
-            Ps *= e.D;
-            Fm *= e.A;
-            Fs *= e.D;
-        }
-        const float4 r = rb[(size_t)(k + 1) * N];
-        const double mu = rec_mu(r, G);
-        Pm = fma(mu, (double)r.x, Pm);
-        Ps = fma(mu, (double)r.y, Ps);
-    }
-    if (k1 + 1 < c.nb) {
-        const Decay e = d[k1 + 1];
-        Fm *= e.A;
-        Fs *= e.D;
-    }
-    if (c.live) local[((size_t)c.b * S + c.seg) * N + n] = make_double2(Pm, Ps);
-    if (c.tile == 0 && c.lane == 0) factor[(size_t)c.b * S + c.seg] = make_double2(Fm, Fs);
-}
-
-// Per (sample, 64 neurons): the reverse carry over segments, cin[seg] =
-// (P, Q) at the first event of segment seg + 1 (0 for the last segment).
+// Per (sample, 64 neurons): the reverse carry over segments.  F(seg) =
+// (P, Q) at the input event before segment seg = its own part (local with the
+// neuron's G) plus the later segments' F decayed over the segment (its
+// composed decays segm); cin[seg] = F(seg + 1) = (P, Q) at the segment's last
+// event, 0 for the last segment (its walk adds the open interval itself).
 __global__ __launch_bounds__(kWave) void k_regg_carry(const int32_t* __restrict__ ev_n, int E_max, int N, int S,
-                                                      const double2* __restrict__ factor,
-                                                      const double2* __restrict__ local, double2* __restrict__ cin)
+                                                      const double2* __restrict__ segm,
+                                                      const double4* __restrict__ local,
+                                                      const double2* __restrict__ coef, double2* __restrict__ cin)
 {
     const int b = blockIdx.y, n = blockIdx.x * kWave + (int)threadIdx.x;
     if (n >= N) return;
     const int nb = clamp_count(ev_n[b], E_max);
     const int Sb = (nb + kSeg - 1) / kSeg;
+    const double2 G = coef[(size_t)b * N + n];
     double Fm = 0.0, Fs = 0.0;
 #pragma unroll 8
     for (int seg = Sb - 1; seg >= 0; --seg) {
         const size_t at = ((size_t)b * S + seg) * N + n;
-        const double2 L = local[at], f = factor[(size_t)b * S + seg];
+        const double4 L = local[at];
+        const double2 f = segm[(size_t)b * S + seg];
         cin[at] = make_double2(Fm, Fs);
-        Fm = fma(f.x, Fm, L.x);
-        Fs = fma(f.y, Fs, L.y);
+        Fm = fma(f.x, Fm, fma(G.x, L.x, G.y * L.z));
+        Fs = fma(f.y, Fs, fma(G.x, L.y, G.y * L.w));
     }
 }
 
@@ -2032,7 +2046,7 @@ __global__ __launch_bounds__(kWave) void k_regg_carry(const int32_t* __restrict_
 __global__ __launch_bounds__(kWave * kWalkWaves) void k_regg_walk(
     const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int B,
     int E_max, int E_pad, const float* __restrict__ WT, int C_in, int N, int tiles, int S, int items, Model m,
-    const Decay* __restrict__ dec, const float4* __restrict__ rec, const double2* __restrict__ coef,
+    const Decay* __restrict__ dec, const float2* __restrict__ rec, const double2* __restrict__ coef,
     const double2* __restrict__ cin, const float* __restrict__ out_t, const int32_t* __restrict__ out_n,
     const int32_t* __restrict__ out_k, const double* __restrict__ scale, long long* __restrict__ gw,
     double* __restrict__ gtp, float* __restrict__ grad_spike)
@@ -2041,24 +2055,24 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_regg_walk(
     if (!walk_coords<1>(items, tiles, S, ev_n, E_max, N, c)) return;
     const int n = c.n0;
     const Decay* d = dec + (size_t)c.b * E_pad;
-    const float4* rb = rec + (size_t)c.b * (E_max + 1) * N + n;
+    const float2* rb = rec + (size_t)c.b * (E_max + 1) * N + n;
     const float* tt = ev_t + (size_t)c.b * E_max;
     const int32_t* src = ev_src + (size_t)c.b * E_max;
     const size_t bn = (size_t)c.b * N + n;
     const double2 G = c.live ? coef[bn] : make_double2(0.0, 0.0);
     const double sc = scale[0];
     const int k1 = c.k0 + c.cnt - 1;
+    // (P, Q) at event k1: the later segments' part, and in the last segment
+    // the open interval after the sample's last event
     const double2 ci = cin[((size_t)c.b * S + c.seg) * N + n];
     double Pm = ci.x, Ps = ci.y;
-    if (k1 + 1 < c.nb) {
-        const Decay e = d[k1 + 1];
-        Pm *= e.A;
-        Ps *= e.D;
+    const bool last = k1 + 1 == c.nb;
+    const Decay en = last ? Decay{0.0, 0.0, 0.0, 0.0} : d[k1 + 1];
+    RecTerm tn = rec_term(rb[(size_t)(k1 + 1) * N], G, en.A, en.D);     // the interval after event k
+    if (last) {
+        Pm = fma(tn.mu, tn.em, Pm);
+        Ps = fma(tn.mu, tn.es, Ps);
     }
-    float4 rn = rb[(size_t)(k1 + 1) * N];          // the interval after event k
-    double mun = rec_mu(rn, G);
-    Pm = fma(mun, (double)rn.x, Pm);
-    Ps = fma(mun, (double)rn.y, Ps);
     // the lane's spikes in this segment, last first
     const float* ts = out_t + bn * (size_t)m.s_max;
     const int32_t* ks = out_k + bn * (size_t)m.s_max;
@@ -2067,13 +2081,13 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_regg_walk(
     while (sp > 0 && ks[sp - 1] > k1) --sp;
     double* gt = gtp + ((size_t)c.tile * B + c.b) * E_max;
     for (int k = k1; k >= c.k0; --k) {
-        const float4 r = rb[(size_t)k * N];            // the interval that event k closes
-        const double mu = rec_mu(r, G);
+        const Decay e = d[k];
+        const RecTerm t = rec_term(rb[(size_t)k * N], G, e.A, e.D);     // the interval that event k closes
         const int j = clamp_src(src[k], C_in);
         const double w = (double)WT[(size_t)j * N + n];
         double g = w * m.kappa * (Pm * m.inv_tm - Ps * m.inv_ts);
-        if ((int)rn.w & kRecStart) g = fma(mun, (double)rn.z, g);
-        if ((int)r.w & kRecEnd) g = fma(mu, (double)r.z, g);
+        if (tn.at_start) g = fma(tn.mu, tn.vp, g);
+        if (t.at_end) g = fma(t.mu, t.vp, g);
         if (c.live) {
             atomicAdd((unsigned long long*)&gw[(size_t)j * N + n],
                       (unsigned long long)llrint(m.kappa * (Pm - Ps) * sc));
@@ -2088,12 +2102,10 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_regg_walk(
         for (int off = kWave / 2; off > 0; off >>= 1) g += __shfl_xor(g, off, kWave);
         if (c.lane == 0) gt[k] = g;
         if (k > c.k0) {
-            const Decay e = d[k];
-            Pm = fma(mu, (double)r.x, Pm * e.A);
-            Ps = fma(mu, (double)r.y, Ps * e.D);
+            Pm = fma(t.mu, t.em, Pm * e.A);
+            Ps = fma(t.mu, t.es, Ps * e.D);
         }
-        rn = r;
-        mun = mu;
+        tn = t;
     }
 }
 
@@ -2121,7 +2133,7 @@ __global__ __launch_bounds__(256) void k_regg_convert(const long long* __restric
 
 struct RegGradLayout {
     RegLayout r;
-    size_t rec, counts, gates, coef, musum, scale, local, factor, cin, gw, gtp, total;
+    size_t rec, counts, gates, coef, musum, scale, local, cin, gw, gtp, total;
 };
 
 static RegGradLayout reg_grad_layout(int B, int E_max, int C_in, int N)
@@ -2132,14 +2144,13 @@ static RegGradLayout reg_grad_layout(int B, int E_max, int C_in, int N)
     auto take = [&](size_t bytes) { size_t o = off; off += (bytes + 255) & ~(size_t)255; return o; };
     const size_t BS = (size_t)B * G.r.f.S;
     const int tiles = (N + kWave - 1) / kWave;
-    G.rec = take((size_t)B * ((size_t)E_max + 1) * N * sizeof(float4));
+    G.rec = take((size_t)B * ((size_t)E_max + 1) * N * sizeof(float2));
     G.counts = take((size_t)B * N * sizeof(double2));
     G.gates = take((size_t)N * sizeof(double2));
     G.coef = take((size_t)B * N * sizeof(double2));
     G.musum = take((size_t)B * N * sizeof(double));
     G.scale = take(sizeof(double));
-    G.local = take(BS * N * sizeof(double2));
-    G.factor = take(BS * sizeof(double2));
+    G.local = take(BS * N * sizeof(double4));
     G.cin = take(BS * N * sizeof(double2));
     G.gw = take((size_t)C_in * N * sizeof(long long));
     G.gtp = take((size_t)tiles * B * E_max * sizeof(double));
@@ -2192,14 +2203,13 @@ extern "C" int lif_spike_count_reg_backward(const float* ev_t, const int32_t* ev
     double* ub = (double*)(base + R.ub);
     double* ob = (double*)(base + R.ob);
     int32_t* st = (int32_t*)(base + R.status);
-    float4* rec = (float4*)(base + G.rec);
+    float2* rec = (float2*)(base + G.rec);
     double2* counts = (double2*)(base + G.counts);
     double2* gates = (double2*)(base + G.gates);
     double2* coef = (double2*)(base + G.coef);
     double* musum = (double*)(base + G.musum);
     double* scale = (double*)(base + G.scale);
-    double2* local = (double2*)(base + G.local);
-    double2* factor = (double2*)(base + G.factor);
+    double4* local = (double4*)(base + G.local);
     double2* cin = (double2*)(base + G.cin);
     long long* gw = (long long*)(base + G.gw);
     double* gtp = (double*)(base + G.gtp);
@@ -2216,7 +2226,7 @@ extern "C" int lif_spike_count_reg_backward(const float* ev_t, const int32_t* ev
         }
         TIMED_LAUNCH("reg_walk", k_reg_walk, dim3(wblocks), dim3(kWave * kWalkWaves), 0, stream, ev_t, ev_src, ev_n,
                      E_max, R.f.E_pad, WT, C_in, N_out, tl, R.f.S, (int)items_max, m, P.dec, P.carry, out_t, out_n,
-                     out_k, part, rec);
+                     out_k, part, rec, local);
     }
     if (nn)
         TIMED_LAUNCH("reg_reduce", k_reg_reduce, dim3((unsigned)((nn + 255) / 256)), dim3(256), 0, stream, part, ev_n,
@@ -2232,10 +2242,8 @@ extern "C" int lif_spike_count_reg_backward(const float* ev_t, const int32_t* ev
     TIMED_LAUNCH("regg_scale", k_regg_scale, dim3(1), dim3(kRegThreads), 0, stream, musum, nn, ev_n, B, E_max,
                  m.kappa, scale);
     if (items_max > 0) {
-        TIMED_LAUNCH("regg_seg", k_regg_seg, dim3(wblocks), dim3(kWave * kWalkWaves), 0, stream, ev_n, E_max,
-                     R.f.E_pad, N_out, tl, R.f.S, (int)items_max, P.dec, rec, coef, local, factor);
         TIMED_LAUNCH("regg_carry", k_regg_carry, dim3((unsigned)tl, (unsigned)B), dim3(kWave), 0, stream, ev_n, E_max,
-                     N_out, R.f.S, factor, local, cin);
+                     N_out, R.f.S, P.segm, local, coef, cin);
         TIMED_LAUNCH("regg_walk", k_regg_walk, dim3(wblocks), dim3(kWave * kWalkWaves), 0, stream, ev_t, ev_src, ev_n,
                      B, E_max, R.f.E_pad, WT, C_in, N_out, tl, R.f.S, (int)items_max, m, P.dec, rec, coef, cin, out_t,
                      out_n, out_k, scale, gw, gtp, grad_spike);
