@@ -107,21 +107,25 @@ class Dev:
 
 
 def time_steps(torch, fn, steps, warmup):
-    """Warm up, then time `steps` calls: wall clock over the whole loop
-    (bracketed by device synchronisations) and HIP events around every call
-    on the current stream (the library launches on it).  Returns (ms per
-    step by wall clock, per-step event durations in ms)."""
+    """Warm up, then time `steps` calls twice: a plain loop by wall clock
+    (bracketed by device synchronisations, nothing else enqueued between
+    the calls), then a loop with HIP events around every call on the current
+    stream (the library launches on it) for per-step statistics.  Returns
+    (ms per step by wall clock, per-step event durations in ms)."""
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     t0 = time.perf_counter()
+    for _ in range(steps):
+        fn()
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps * 1e3
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     for a, b in ev:
         a.record()
         fn()
         b.record()
     torch.cuda.synchronize()
-    wall = (time.perf_counter() - t0) / steps * 1e3
     return wall, [a.elapsed_time(b) for a, b in ev]
 
 
