@@ -653,6 +653,7 @@ struct ResolveLds {
     double kmax[kRing];                          // largest key of each buffer's window (NaN keys left out)
     int consumed;                                // windows the chain has finished
     int stop;                                    // the chain reached s_max
+    unsigned long long kpub;                     // bits of the chain's current deficit key K
 };
 
 __device__ __forceinline__ int lds_load(const int* p)
@@ -707,54 +708,113 @@ __device__ __forceinline__ double row_bcast(double v)
     return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
 
-// Step E of a sub-block walk: lane j takes its interval's start state before
-// event E = j, and steps the state through event E while E <= j (event E's
-// weight and decays come from lane E of the row).
-template <int E>
-__device__ __forceinline__ void walk_from(const Model& m, int j, float wv, double2 ad, double& U, double& J,
-                                          double& V0, double& I0)
+// The value of lane j - Dist of the calling lane's row of 16 lanes (DPP
+// row shift); lanes j < Dist get fill.
+template <int Dist>
+__device__ __forceinline__ double row_shr(double v, double fill)
 {
-    const float w = __builtin_bit_cast(float, row_bcast<E>(__builtin_bit_cast(int, wv)));
-    const double A = row_bcast<E>(ad.x), D = row_bcast<E>(ad.y);
-    if (E == j) {
-        V0 = v_of(m, U, J);
-        I0 = J;
-    }
-    if (E <= j) step1(make_double2(A, D), w, U, J);
-    if constexpr (E + 1 < kSub) walk_from<E + 1>(m, j, wv, ad, U, J, V0, I0);
+    const unsigned long long u = (unsigned long long)__double_as_longlong(v);
+    const unsigned long long f = (unsigned long long)__double_as_longlong(fill);
+    const unsigned lo = (unsigned)__builtin_amdgcn_update_dpp((int)(unsigned)f, (int)(unsigned)u, 0x110 + Dist, 0xf,
+                                                              0xf, false);
+    const unsigned hi = (unsigned)__builtin_amdgcn_update_dpp((int)(unsigned)(f >> 32), (int)(unsigned)(u >> 32),
+                                                              0x110 + Dist, 0xf, 0xf, false);
+    return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+
+// One step of the row's inclusive scan of event maps in (U, J): lane j's map
+// (a, b) (x -> a x + b) composed after the map of lane j - Dist.
+template <int Dist>
+__device__ __forceinline__ void scan_step(double& aU, double& bU, double& aJ, double& bJ)
+{
+    const double paU = row_shr<Dist>(aU, 1.0), pbU = row_shr<Dist>(bU, 0.0);
+    const double paJ = row_shr<Dist>(aJ, 1.0), pbJ = row_shr<Dist>(bJ, 0.0);
+    bU = fma(aU, pbU, bU);
+    aU *= paU;
+    bJ = fma(aJ, pbJ, bJ);
+    aJ *= paJ;
+}
+
+// The no-reset states of a sub-block's intervals from its entering state u0
+// (one row of 16 lanes, lane j holding event j of the sub-block with decays
+// (A, D) and weight w): the maps of events 0 .. j composed by a log-depth
+// scan within the row (App. B: the maps form a semigroup), so lane j gets
+// the state at the start of its interval (after event j - 1) and after its
+// event.
+__device__ __forceinline__ void row_states(double2 u0, double A, double D, float w, double& U0, double& J0,
+                                           double& U1, double& J1)
+{
+    double aU = A, bU = (double)w, aJ = D, bJ = (double)w;
+    scan_step<1>(aU, bU, aJ, bJ);
+    scan_step<2>(aU, bU, aJ, bJ);
+    scan_step<4>(aU, bU, aJ, bJ);
+    scan_step<8>(aU, bU, aJ, bJ);
+    U1 = fma(aU, u0.x, bU);
+    J1 = fma(aJ, u0.y, bJ);
+    U0 = fma(row_shr<1>(aU, 1.0), u0.x, row_shr<1>(bU, 0.0));
+    J0 = fma(row_shr<1>(aJ, 1.0), u0.y, row_shr<1>(bJ, 0.0));
 }
 
 // A staging wave's window: candidates c0 .. c0 + kWinCand - 1 of the chunk,
 // lane l taking interval j = l % kSub of candidate c0 + l / kSub.  Every lane
 // loads its own interval's closing event (source, decays, times) and its
-// candidate's entering state, then its weight; the 16 lanes of a candidate
-// (one row) walk the sub-block together, lane j taking the no-reset state at
-// its interval's start (after event j - 1) and end, and the interval's
-// crossing key.  Candidates past the pool's capacity take their entering
-// state from rebuild_entry.  open_last: the window holds the sample's last
-// sub-block, and the open interval after its last event is staged too.
-__device__ __forceinline__ void stage_window(ResolveLds& sh, WinBuf& w, const Model& m, int c0, int tot, int seg0,
-                                             int b, int n, int nb, int S, int N, int C_in,
-                                             const float* __restrict__ tt, const int32_t* __restrict__ src,
-                                             const Decay* __restrict__ d, const float* __restrict__ WT,
-                                             const double2* __restrict__ carry, const double2* __restrict__ pool,
-                                             bool open_last, double& kmax)
+// candidate's entering state (stage_load, issued before the wait for the
+// window's buffer), then its weight; the 16
+// lanes of a candidate (one row) take the no-reset states of the sub-block by
+// a scan of its event maps (row_states), lane j the state at its interval's
+// start (after event j - 1) and end, and the interval's crossing key.  Candidates past the pool's capacity take
+// their entering state from rebuild_entry.  open_last: the window holds the
+// sample's last sub-block, and the open interval after its last event is
+// staged too.
+struct StageIn {
+    int k, sc;
+    bool ok;
+    uint32_t slot;
+    double A, D;
+    float ta, tb;
+    double2 u0;
+};
+
+__device__ __forceinline__ StageIn stage_load(const ResolveLds& sh, int c0, int tot, int seg0, int nb,
+                                              const float* __restrict__ tt, const int32_t* __restrict__ src,
+                                              const Decay* __restrict__ d, const double2* __restrict__ pool)
 {
     const int lane = (int)threadIdx.x % kWave;
     const int j = lane % kSub, r = lane / kSub;
     const int c = c0 + r;
     const int cc = min(c, tot - 1);
-    const uint32_t cw = sh.cand[cc], slot = sh.slot[cc];
+    const uint32_t cw = sh.cand[cc];
+    StageIn in;
+    in.slot = sh.slot[cc];
     const int kq = (seg0 + (int)(cw >> 3)) * kSeg + (int)(cw & 7u) * kSub;
-    const bool ok = c < tot && kq + j < nb;
-    const int k = min(kq + j, nb - 1);
-    const int sc = src[k];
-    const Decay dk = d[k];
-    const double2 ad = make_double2(dk.A, dk.D);
-    const float ta = tt[max(k - 1, 0)], tb = tt[k];
-    double2 u0 = pool[slot != kNoSlot ? slot : 0u];    // the pool holds at least one entry
+    in.ok = c < tot && kq + j < nb;
+    in.k = min(kq + j, nb - 1);
+    in.sc = src[in.k];
+    const Decay dk = d[in.k];
+    in.A = dk.A;
+    in.D = dk.D;
+    in.ta = tt[max(in.k - 1, 0)];
+    in.tb = tt[in.k];
+    in.u0 = pool[in.slot != kNoSlot ? in.slot : 0u];    // the pool holds at least one entry
+    return in;
+}
+
+__device__ __forceinline__ void stage_window(ResolveLds& sh, WinBuf& w, const Model& m, const StageIn& in, int c0,
+                                             int tot, int seg0, int b, int n, int nb, int S, int N, int C_in,
+                                             const int32_t* __restrict__ src, const Decay* __restrict__ d,
+                                             const float* __restrict__ WT, const double2* __restrict__ carry,
+                                             bool open_last, double& kmax)
+{
+    const int lane = (int)threadIdx.x % kWave;
+    const int j = lane % kSub, r = lane / kSub;
+    const int c = c0 + r;
+    const int k = in.k, sc = in.sc;
+    const bool ok = in.ok;
+    const double2 ad = make_double2(in.A, in.D);
+    const float ta = in.ta, tb = in.tb;
+    double2 u0 = in.u0;
     const float wv = WT[(size_t)clamp_src(sc, C_in) * (size_t)N + n];
-    if (__ballot(c < tot && slot == kNoSlot)) {
+    if (__ballot(c < tot && in.slot == kNoSlot)) {
         const int nc = min(kWinCand, tot - c0);
         for (int x = 0; x < nc; ++x) {
             if (sh.slot[c0 + x] != kNoSlot) continue;
@@ -766,13 +826,28 @@ __device__ __forceinline__ void stage_window(ResolveLds& sh, WinBuf& w, const Mo
             if (x == r) u0 = e;
         }
     }
-    double U = u0.x, J = u0.y, V0 = 0.0, I0 = 0.0;
-    walk_from<0>(m, j, wv, ad, U, J, V0, I0);
+    double U0, J0, U, J;
+    row_states(u0, ad.x, ad.y, wv, U0, J0, U, J);
+    const double V0 = v_of(m, U0, J0), I0 = J0;
     const double V1 = v_of(m, U, J);
     const double t0 = k > 0 ? (double)ta : 0.0, t1 = (double)tb;
+    // The deficit of the spikes the chain has found so far, decayed to the
+    // interval's start, bounds the true deficit there from below (the chain
+    // works on earlier windows, and later spikes only add to it), so the
+    // no-crossing screen of the true state is safe with it.  Most intervals of
+    // a neuron that has fired fail it; the crossing key is computed only when
+    // some lane passes.
+    const double Kp = __longlong_as_double((long long)__hip_atomic_load(&sh.kpub, __ATOMIC_RELAXED,
+                                                                        __HIP_MEMORY_SCOPE_WORKGROUP));
+    const double L = t1 - t0;
+    const bool maybe = ok && L > 0.0 &&
+                       (V0 - exp(Kp - t0 * m.inv_tm)) + (I0 > m.th ? (I0 - m.th) * (L * m.inv_tm) : 0.0) >= m.th_lo;
+    double key = __builtin_nan("");
     double crit, hi, fhi;
-    crossing_data(m, V0, I0, V1, t1 - t0, ad.x, ad.y, crit, hi, fhi);
-    const double key = ok ? crossing_key(m, crit, t0) : __builtin_nan("");
+    if (__ballot(maybe)) {
+        crossing_data(m, V0, I0, V1, L, ad.x, ad.y, crit, hi, fhi);
+        if (maybe) key = crossing_key(m, crit, t0);
+    }
     w.key[lane] = key;
     double km = key;
     w.v0[lane] = V0;
@@ -780,9 +855,16 @@ __device__ __forceinline__ void stage_window(ResolveLds& sh, WinBuf& w, const Mo
     w.t0[lane] = k > 0 ? ta : 0.0f;
     w.t1[lane] = tb;
     if (open_last && ok && k == nb - 1) {
-        // the open interval after the sample's last event
-        open_interval_data(m, V1, J, m.t_end - t1, crit, hi, fhi);
-        w.key[kOpenIv] = crossing_key(m, crit, t1);
+        // the open interval after the sample's last event (the same screen)
+        const double Lo = m.t_end - t1;
+        const bool mo = Lo > 0.0 &&
+                        (V1 - exp(Kp - t1 * m.inv_tm)) + (J > m.th ? (J - m.th) * (Lo * m.inv_tm) : 0.0) >= m.th_lo;
+        double ko = __builtin_nan("");
+        if (mo) {
+            open_interval_data(m, V1, J, Lo, crit, hi, fhi);
+            ko = crossing_key(m, crit, t1);
+        }
+        w.key[kOpenIv] = ko;
         w.v0[kOpenIv] = V1;
         w.i0[kOpenIv] = J;
         w.t0[kOpenIv] = tb;
@@ -877,6 +959,9 @@ __device__ bool spike_at(ResolveLds& sh, const WinBuf& w, const Model& m, int i,
     ch.dref = Dnew;
     ch.tref = t0;
     ch.K = log(Dnew) + t0 * m.inv_tm;
+    if (lane == 0)
+        __hip_atomic_store(&sh.kpub, (unsigned long long)__double_as_longlong(ch.K), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_WORKGROUP);
     ch.ylast = y;
     ch.lastw = wg;
     ch.lasti = i;
@@ -942,6 +1027,7 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
     if (threadIdx.x == 0) {
         sh.consumed = 0;
         sh.stop = 0;
+        sh.kpub = (unsigned long long)__double_as_longlong(-INFINITY);
         for (int r = 0; r < kRing; ++r) sh.ready[r] = 0;
     }
     // the first chunk's mask words are loaded together with the event count
@@ -1015,6 +1101,8 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
             if (!chain) {
                 for (int wi = wv - 1; wi < nwin; wi += kResolveWaves - 1) {
                     const int wg = wbase + wi, buf = wg % kRing;
+                    // this window's loads go out before the wait for its buffer
+                    const StageIn cur = stage_load(sh, wi * kWinCand, tot, seg0, nb, tt, src, d, pool);
                     bool halt = false;
                     for (int spin = 0;; ++spin) {
                         halt = lds_load(&sh.stop) != 0;
@@ -1027,8 +1115,8 @@ __device__ int resolve_neuron(ResolveLds& sh, int b, int n, const float* __restr
                         __builtin_amdgcn_s_sleep(1);
                     }
                     if (halt) break;
-                    stage_window(sh, sh.win[buf], m, wi * kWinCand, tot, seg0, b, n, nb, S, N, C_in, tt, src, d, WT,
-                                 carry, pool, open_here && wi == nwin - 1, sh.kmax[buf]);
+                    stage_window(sh, sh.win[buf], m, cur, wi * kWinCand, tot, seg0, b, n, nb, S, N, C_in, src, d,
+                                 WT, carry, open_here && wi == nwin - 1, sh.kmax[buf]);
                     lds_store(&sh.ready[buf], wg + 1);
                 }
             } else {
