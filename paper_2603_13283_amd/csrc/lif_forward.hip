@@ -755,6 +755,15 @@ __device__ __forceinline__ void row_states(double2 u0, double A, double D, float
     J0 = fma(row_shr<1>(aJ, 1.0), u0.y, row_shr<1>(bJ, 0.0));
 }
 
+// A value <= e^x for the staging screen: the float exponential (relative
+// error below 2^-16 for |x| <= 88, argument rounding included) scaled by
+// 1 - 2^-10; 0 below the float range and at most FLT_MAX above it (beyond
+// it the deficit exceeds any state the screen could pass).
+__device__ __forceinline__ double exp_lower(double x)
+{
+    return (1.0 - 0x1p-10) * (double)fminf(__expf((float)x), 3.0e38f);
+}
+
 // A staging wave's window: candidates c0 .. c0 + kWinCand - 1 of the chunk,
 // lane l taking interval j = l % kSub of candidate c0 + l / kSub.  Every lane
 // loads its own interval's closing event (source, decays, times) and its
@@ -806,7 +815,7 @@ __device__ __forceinline__ void stage_window(ResolveLds& sh, WinBuf& w, const Mo
                                              bool open_last, double& kmax)
 {
     const int lane = (int)threadIdx.x % kWave;
-    const int j = lane % kSub, r = lane / kSub;
+    const int r = lane / kSub;
     const int c = c0 + r;
     const int k = in.k, sc = in.sc;
     const bool ok = in.ok;
@@ -834,14 +843,15 @@ __device__ __forceinline__ void stage_window(ResolveLds& sh, WinBuf& w, const Mo
     // The deficit of the spikes the chain has found so far, decayed to the
     // interval's start, bounds the true deficit there from below (the chain
     // works on earlier windows, and later spikes only add to it), so the
-    // no-crossing screen of the true state is safe with it.  Most intervals of
-    // a neuron that has fired fail it; the crossing key is computed only when
-    // some lane passes.
+    // no-crossing screen of the true state is safe with it (with a lower
+    // bound of that deficit, exp_lower).  Most intervals of a neuron that has
+    // fired fail it; the crossing key is computed only when some lane passes.
     const double Kp = __longlong_as_double((long long)__hip_atomic_load(&sh.kpub, __ATOMIC_RELAXED,
                                                                         __HIP_MEMORY_SCOPE_WORKGROUP));
     const double L = t1 - t0;
     const bool maybe = ok && L > 0.0 &&
-                       (V0 - exp(Kp - t0 * m.inv_tm)) + (I0 > m.th ? (I0 - m.th) * (L * m.inv_tm) : 0.0) >= m.th_lo;
+                       (V0 - exp_lower(Kp - t0 * m.inv_tm)) + (I0 > m.th ? (I0 - m.th) * (L * m.inv_tm) : 0.0) >=
+                           m.th_lo;
     double key = __builtin_nan("");
     double crit, hi, fhi;
     if (__ballot(maybe)) {
@@ -858,7 +868,8 @@ __device__ __forceinline__ void stage_window(ResolveLds& sh, WinBuf& w, const Mo
         // the open interval after the sample's last event (the same screen)
         const double Lo = m.t_end - t1;
         const bool mo = Lo > 0.0 &&
-                        (V1 - exp(Kp - t1 * m.inv_tm)) + (J > m.th ? (J - m.th) * (Lo * m.inv_tm) : 0.0) >= m.th_lo;
+                        (V1 - exp_lower(Kp - t1 * m.inv_tm)) + (J > m.th ? (J - m.th) * (Lo * m.inv_tm) : 0.0) >=
+                            m.th_lo;
         double ko = __builtin_nan("");
         if (mo) {
             open_interval_data(m, V1, J, Lo, crit, hi, fhi);
