@@ -201,28 +201,6 @@ __global__ __launch_bounds__(256) void k_bwd_convert(const long long* __restrict
         }
 }
 
-__device__ __forceinline__ double group_sum8(const double (&v)[kGrp], int lane)
-{
-    const bool u32 = (lane & 32) != 0, u16 = (lane & 16) != 0, u8 = (lane & 8) != 0;
-    double r4[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const double keep = u32 ? v[q + 4] : v[q], send = u32 ? v[q] : v[q + 4];
-        r4[q] = keep + __shfl_xor(send, 32, kWave);
-    }
-    double r2[2];
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
-        const double keep = u16 ? r4[q + 2] : r4[q], send = u16 ? r4[q] : r4[q + 2];
-        r2[q] = keep + __shfl_xor(send, 16, kWave);
-    }
-    double r = (u8 ? r2[1] : r2[0]) + __shfl_xor(u8 ? r2[0] : r2[1], 8, kWave);
-    r += __shfl_xor(r, 4, kWave);
-    r += __shfl_xor(r, 2, kWave);
-    r += __shfl_xor(r, 1, kWave);
-    return r;
-}
-
 // One wave per (sample, segment, chunk of 64 firing neurons), walking the
 // segment's events backwards: at event k, dL/dw += kappa (P^m - P^s) (one
 // fixed-point integer atomic per live lane) and the chunk's part of dL/dt_k,

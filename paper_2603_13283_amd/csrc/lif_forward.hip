@@ -40,6 +40,7 @@
 #include "lif_common.hpp"
 #include "lif_host.hpp"
 #include "lif_walk.hpp"
+#include <type_traits>
 
 namespace lif {
 
@@ -1685,13 +1686,26 @@ __device__ __forceinline__ RegArg reg_vmax_arg(const Model& m, double V0, double
         const double V1 = V0 * A + m.kappa * I0 * (A - Dd);
         if (V1 > r.vmax) r = RegArg{V1, A, Dd, false, true};
     }
+    // The logarithm and the decays of the stationary point in float32
+    // arithmetic (relative errors near 2^-22; the records keep the decays in
+    // float32 anyway), with e^{-u/ts} = (e^{-u/tm})^(p+1) when tau_m / tau_s
+    // = p + 1; a ratio past the float32 range takes the float64 logarithm.
     const double a = V0 + m.kappa * I0;
     if (I0 > 0.0 && a > 0.0) {
         const double ratio = m.kappa * I0 * m.tm / (a * m.ts);
         if (ratio > 1.0) {
-            const double u = log(ratio) * m.c_tv;
+            const double u = (ratio < 1.0e38 ? (double)__logf((float)ratio) : log(ratio)) * m.c_tv;
             if (u > 0.0 && u < L) {
-                const double em = exp(-u * m.inv_tm), es = exp(-u * m.inv_ts);
+                const float emf = __expf((float)(-u * m.inv_tm));
+                float esf;
+                switch (m.p_int) {
+                case 1: esf = emf * emf; break;
+                case 2: esf = emf * emf * emf; break;
+                case 3: { const float e2 = emf * emf; esf = e2 * e2; } break;
+                case 4: { const float e2 = emf * emf; esf = e2 * e2 * emf; } break;
+                default: esf = __expf((float)(-u * m.inv_ts)); break;
+                }
+                const double em = (double)emf, es = (double)esf;
                 const double Vu = V0 * em + m.kappa * I0 * (em - es);
                 if (Vu > r.vmax) r = RegArg{Vu, em, es, false, false};
             }
@@ -2026,34 +2040,25 @@ extern "C" int lif_spike_count_reg(const float* ev_t, const int32_t* ev_src, con
 namespace lif {
 
 // A record decoded with the interval's own decays (A, D): the multiplier mu
-// of its pseudo-spike (dL/dV_max), the decays at its argmax, and its
-// end-point slope term: at the start (the input event before the interval)
-// or at the end (the event that closes it).
+// of its pseudo-spike (dL/dV_max; 0 for an inactive record, whose fields are
+// all 0), the decays at its argmax, and its end-point slope terms: vs when
+// the argmax is the start (the input event before the interval), ve when it
+// is the end (the event that closes it), 0 otherwise.  Selects only, so
+// that the walk over a group has no branches.
 struct RecTerm {
-    double mu, em, es, vp;
-    bool at_start, at_end;
+    double mu, em, es, vs, ve;
 };
 
 __device__ __forceinline__ RecTerm rec_term(const float2& r, const double2& G, double A, double D)
 {
-    RecTerm t{0.0, 0.0, 0.0, 0.0, false, false};
-    if (r.x == 0.0f) return t;
-    t.mu = r.x > 0.0f ? G.x : G.y;
     const float a = fabsf(r.x);
-    if (a == kRecStart) {
-        t.em = 1.0;
-        t.es = 1.0;
-        t.vp = (double)r.y;
-        t.at_start = true;
-    } else if (a == kRecEnd) {
-        t.em = A;
-        t.es = D;
-        t.vp = (double)r.y;
-        t.at_end = true;
-    } else {
-        t.em = (double)a;
-        t.es = (double)r.y;
-    }
+    const bool st = a == kRecStart, en = a == kRecEnd;
+    RecTerm t;
+    t.mu = r.x > 0.0f ? G.x : (r.x < 0.0f ? G.y : 0.0);
+    t.em = st ? 1.0 : (en ? A : (double)a);
+    t.es = st ? 1.0 : (en ? D : (double)r.y);
+    t.vs = st ? (double)r.y : 0.0;
+    t.ve = en ? (double)r.y : 0.0;
     return t;
 }
 
@@ -2141,7 +2146,14 @@ __global__ __launch_bounds__(kWave) void k_regg_carry(const int32_t* __restrict_
 
 // Per (sample, segment, 64 neurons): (P_k, Q_k) from the segment's last
 // event down to its first, each event's contributions, and the upstream
-// gradient of the lane's spikes inside the segment.
+// gradient of the lane's spikes inside the segment.  The segment is staged
+// as in the forward walks (sources in registers, decays and times in LDS);
+// groups of kGrp events are walked from the last backwards with the next
+// group's weights and records in flight, the dL/dW terms of a group added
+// after its walk and its dL/dt terms summed over the lanes together
+// (group_sum8).
+constexpr int kRegPre = 4;
+
 __global__ __launch_bounds__(kWave * kWalkWaves) void k_regg_walk(
     const float* __restrict__ ev_t, const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n, int B,
     int E_max, int E_pad, const float* __restrict__ WT, int C_in, int N, int tiles, int S, int items, Model m,
@@ -2150,13 +2162,24 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_regg_walk(
     const int32_t* __restrict__ out_k, const double* __restrict__ scale, long long* __restrict__ gw,
     double* __restrict__ gtp, float* __restrict__ grad_spike)
 {
+    __shared__ double2 s_ad[kWalkWaves][kSeg];
+    __shared__ float s_t[kWalkWaves][kSeg];
     WalkCoords c;
     if (!walk_coords<1>(items, tiles, S, ev_n, E_max, N, c)) return;
-    const int n = c.n0;
+    const int n = c.n0, lane = c.lane, wv = (int)threadIdx.x / kWave;
+    double2* lad = s_ad[wv];
+    float* lt = s_t[wv];
     const Decay* d = dec + (size_t)c.b * E_pad;
     const float2* rb = rec + (size_t)c.b * (E_max + 1) * N + n;
     const float* tt = ev_t + (size_t)c.b * E_max;
-    const int32_t* src = ev_src + (size_t)c.b * E_max;
+    const Stage st = stage_segment(c, ev_src + (size_t)c.b * E_max + c.k0, d + c.k0, WT, C_in, N, lad, nullptr,
+                                   nullptr);
+#pragma unroll
+    for (int h = 0; h < kSrcRegs; ++h) {
+        const int e = h * kWave + lane;
+        if (e < c.cnt) lt[e] = tt[c.k0 + e];
+    }
+    wave_lds_sync();
     const size_t bn = (size_t)c.b * N + n;
     const double2 G = c.live ? coef[bn] : make_double2(0.0, 0.0);
     const double sc = scale[0];
@@ -2167,44 +2190,143 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_regg_walk(
     double Pm = ci.x, Ps = ci.y;
     const bool last = k1 + 1 == c.nb;
     const Decay en = last ? Decay{0.0, 0.0, 0.0, 0.0} : d[k1 + 1];
-    RecTerm tn = rec_term(rb[(size_t)(k1 + 1) * N], G, en.A, en.D);     // the interval after event k
+    RecTerm tn = rec_term(rb[(size_t)(k1 + 1) * N], G, en.A, en.D);     // the interval after event k1
     if (last) {
         Pm = fma(tn.mu, tn.em, Pm);
         Ps = fma(tn.mu, tn.es, Ps);
     }
-    // the lane's spikes in this segment, last first
+    // the lane's spikes in this segment (out_k in [k0, k1]), last first; the
+    // first kRegPre of them and their upstream gradients are held in
+    // registers and written back after the walk, so that the walk itself
+    // loads nothing but the next group's weights and records.  A wave where
+    // some lane has more spikes in the segment (a burst) reads and updates
+    // them in the walk instead.
     const float* ts = out_t + bn * (size_t)m.s_max;
     const int32_t* ks = out_k + bn * (size_t)m.s_max;
     float* gsp = grad_spike + bn * (size_t)m.s_max;
-    int sp = c.live ? min(out_n[bn], m.s_max) : 0;
-    while (sp > 0 && ks[sp - 1] > k1) --sp;
-    double* gt = gtp + ((size_t)c.tile * B + c.b) * E_max;
-    for (int k = k1; k >= c.k0; --k) {
-        const Decay e = d[k];
-        const RecTerm t = rec_term(rb[(size_t)k * N], G, e.A, e.D);     // the interval that event k closes
-        const int j = clamp_src(src[k], C_in);
-        const double w = (double)WT[(size_t)j * N + n];
-        double g = w * m.kappa * (Pm * m.inv_tm - Ps * m.inv_ts);
-        if (tn.at_start) g = fma(tn.mu, tn.vp, g);
-        if (t.at_end) g = fma(t.mu, t.vp, g);
-        if (c.live) {
-            atomicAdd((unsigned long long*)&gw[(size_t)j * N + n],
-                      (unsigned long long)llrint(m.kappa * (Pm - Ps) * sc));
-            const double tk = (double)tt[k];
-            while (sp > 0 && ks[sp - 1] == k) {
-                --sp;
-                gsp[sp] += (float)(-(m.dth * m.inv_tm) * Pm * exp(-(tk - (double)ts[sp]) * m.inv_tm));
+    int sp = 0;                                   // spikes with out_k <= k1 (out_k is non-decreasing)
+    {
+        int hi = c.live ? min(out_n[bn], m.s_max) : 0;
+        while (sp < hi) {
+            const int mid = (sp + hi) >> 1;
+            if (ks[mid] <= k1) sp = mid + 1; else hi = mid;
+        }
+    }
+    int pk[kRegPre];
+    float pt[kRegPre], pg[kRegPre];
+#pragma unroll
+    for (int u = 0; u < kRegPre; ++u) {
+        const int q = sp - 1 - u;
+        const int kq = q >= 0 ? ks[q] : -1;
+        const bool in = kq >= c.k0;
+        pk[u] = in ? kq : -1;
+        pt[u] = in ? ts[q] : 0.0f;
+        pg[u] = in ? gsp[q] : 0.0f;
+    }
+    const int qx = sp - 1 - kRegPre;
+    const bool burst = __ballot(qx >= 0 && ks[max(qx, 0)] >= c.k0) != 0ull;
+    double* gt = gtp + ((size_t)c.tile * B + c.b) * E_max + c.k0;
+    const double kap = m.kappa, sk = -(m.dth * m.inv_tm);
+    auto load_rec = [&](int g, float2 (&r)[kGrp]) {
+#pragma unroll
+        for (int jj = 0; jj < kGrp; ++jj) r[jj] = rb[(size_t)(c.k0 + min(g * kGrp + jj, c.cnt - 1)) * N];
+    };
+    auto walk = [&](auto burst_tag) {
+        constexpr bool kBurst = decltype(burst_tag)::value;
+        int knext = kBurst && sp > 0 ? ks[sp - 1] : -1;
+        // the walk of group g (its dL/dt terms ca and fixed-point dL/dW terms ga)
+        auto group = [&](int g, const float (&w)[kGrp][1], const float2 (&r)[kGrp], double (&ca)[kGrp],
+                         long long (&ga)[kGrp]) {
+#pragma unroll
+            for (int jj = kGrp - 1; jj >= 0; --jj) {
+                const int e = g * kGrp + jj;
+                ca[jj] = 0.0;
+                ga[jj] = 0;
+                if (e >= c.cnt) continue;
+                const int k = c.k0 + e;
+                const double2 ad = lad[e];
+                const RecTerm t = rec_term(r[jj], G, ad.x, ad.y);        // the interval that event e closes
+                double gk = (double)w[jj][0] * kap * (Pm * m.inv_tm - Ps * m.inv_ts);
+                gk = fma(tn.mu, tn.vs, gk);              // adds 0 unless the argmax is that end
+                gk = fma(t.mu, t.ve, gk);
+                const long long gq = llrint(kap * (Pm - Ps) * sc);
+                ca[jj] = c.live ? gk : 0.0;
+                ga[jj] = c.live ? gq : 0ll;
+                // spikes between events k - 1 and k: their upstream gradient
+                // from P at event k
+                if constexpr (kBurst) {
+                    if (c.live && knext == k) {
+                        const double tk = (double)lt[e];
+                        while (sp > 0 && ks[sp - 1] == k) {
+                            --sp;
+                            gsp[sp] += (float)(sk * Pm * exp(-(tk - (double)ts[sp]) * m.inv_tm));
+                        }
+                        knext = sp > 0 ? ks[sp - 1] : -1;
+                    }
+                } else {
+                    bool hit = false;
+#pragma unroll
+                    for (int u = 0; u < kRegPre; ++u) hit |= pk[u] == k;
+                    if (__ballot(hit)) {
+                        const double tk = (double)lt[e];
+#pragma unroll
+                        for (int u = 0; u < kRegPre; ++u)
+                            if (pk[u] == k) pg[u] += (float)(sk * Pm * exp(-(tk - (double)pt[u]) * m.inv_tm));
+                    }
+                }
+                if (e > 0) {
+                    Pm = fma(t.mu, t.em, Pm * ad.x);
+                    Ps = fma(t.mu, t.es, Ps * ad.y);
+                }
+                tn = t;
             }
-        } else {
-            g = 0.0;
+        };
+        // group g's dL/dW terms (zero terms included, so that every group
+        // issues the same memory operations) and its dL/dt sums
+        auto flush = [&](int g, const double (&ca)[kGrp], const long long (&ga)[kGrp]) {
+            const int oreg = g * kGrp < kWave ? st.off[0] : st.off[kSrcRegs - 1];
+#pragma unroll
+            for (int jj = 0; jj < kGrp; ++jj) {
+                const int roff = __builtin_amdgcn_readlane(oreg, (g * kGrp + jj) & (kWave - 1));
+                atomicAdd((unsigned long long*)&gw[(size_t)(roff >> 2) + (size_t)n], (unsigned long long)ga[jj]);
+            }
+            const double sum = group_sum8(ca, lane);
+            const int j = ((lane >> 5) & 1) * 4 + ((lane >> 4) & 1) * 2 + ((lane >> 3) & 1);
+            if ((lane & 7) == 0 && g * kGrp + j < c.cnt) gt[g * kGrp + j] = sum;
+        };
+        // Groups from the last backwards with two groups' weights and records
+        // in flight; a group's loads are issued before the atomics of the
+        // group walked just before, so that no wait for loads waits for
+        // atomics (the memory counter is in order).  Loads past the first
+        // group re-read it.
+        const int ng = (c.cnt + kGrp - 1) / kGrp;
+        float wa[kGrp][1], wb[kGrp][1];
+        float2 ra[kGrp], rbuf[kGrp];
+        double ca[kGrp];
+        long long ga[kGrp];
+        load_grp<1>(st, (ng - 1) * kGrp, wa);
+        load_rec(ng - 1, ra);
+        load_grp<1>(st, max(ng - 2, 0) * kGrp, wb);
+        load_rec(max(ng - 2, 0), rbuf);
+        for (int g = ng - 1; g >= 0; g -= 2) {
+            group(g, wa, ra, ca, ga);
+            load_grp<1>(st, max(g - 2, 0) * kGrp, wa);
+            load_rec(max(g - 2, 0), ra);
+            flush(g, ca, ga);
+            if (g < 1) break;
+            group(g - 1, wb, rbuf, ca, ga);
+            load_grp<1>(st, max(g - 3, 0) * kGrp, wb);
+            load_rec(max(g - 3, 0), rbuf);
+            flush(g - 1, ca, ga);
         }
-        for (int off = kWave / 2; off > 0; off >>= 1) g += __shfl_xor(g, off, kWave);
-        if (c.lane == 0) gt[k] = g;
-        if (k > c.k0) {
-            Pm = fma(t.mu, t.em, Pm * e.A);
-            Ps = fma(t.mu, t.es, Ps * e.D);
-        }
-        tn = t;
+    };
+    if (burst) {
+        walk(std::true_type{});
+    } else {
+        walk(std::false_type{});
+#pragma unroll
+        for (int u = 0; u < kRegPre; ++u)
+            if (pk[u] >= 0) gsp[sp - 1 - u] = pg[u];
     }
 }
 

@@ -158,4 +158,30 @@ __device__ __forceinline__ void load_grp(const Stage& st, int e0, float (&w)[kGr
     for (int j = 0; j < kGrp; ++j) load_w<NPL>(st, __builtin_amdgcn_readlane(oreg, (e0 + j) & (kWave - 1)), w[j]);
 }
 
+// Sums over the 64 lanes of v[0..7] (one value per event of a group):
+// lane l ends with the sum of v[j] for j = 4 b5 + 2 b4 + b3 (b5, b4, b3 the
+// bits 5, 4, 3 of l), by a halving exchange (4 + 2 + 1 shuffles) and a
+// butterfly over the lane's 8-lane row (3 shuffles).
+__device__ __forceinline__ double group_sum8(const double (&v)[kGrp], int lane)
+{
+    const bool u32 = (lane & 32) != 0, u16 = (lane & 16) != 0, u8 = (lane & 8) != 0;
+    double r4[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const double keep = u32 ? v[q + 4] : v[q], send = u32 ? v[q] : v[q + 4];
+        r4[q] = keep + __shfl_xor(send, 32, kWave);
+    }
+    double r2[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const double keep = u16 ? r4[q + 2] : r4[q], send = u16 ? r4[q] : r4[q + 2];
+        r2[q] = keep + __shfl_xor(send, 16, kWave);
+    }
+    double r = (u8 ? r2[1] : r2[0]) + __shfl_xor(u8 ? r2[0] : r2[1], 8, kWave);
+    r += __shfl_xor(r, 4, kWave);
+    r += __shfl_xor(r, 2, kWave);
+    r += __shfl_xor(r, 1, kWave);
+    return r;
+}
+
 }  // namespace lif
