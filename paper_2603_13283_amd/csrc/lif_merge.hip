@@ -7,7 +7,9 @@
 // time order; the workgroup gathers them into LDS as 64-bit keys (float bits
 // of the time, which order like the times since spike times are positive,
 // then i * s_max + s, which orders equal times by neuron) and sorts them
-// with a bitonic network in LDS.  When a sample has more spikes than the
+// with a bitonic network in LDS, over the smallest power of two holding its
+// keys (the LDS array is sized for the most a sample can hold).  When a
+// sample has more spikes than the
 // sort holds, the K = min(total, E2_max) earliest are found first: the
 // K-th smallest time t_K by bisection on its float bits (each neuron's
 // spikes are sorted, so counting the spikes at or before a time is a binary
@@ -69,7 +71,11 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(const float* __restrict
     int total = 0;
     int pos = block_exclusive_scan(local, s_scan, total);
     const int kept = min(total, E2_max);
-    for (int e = tid; e < cap; e += kMergeThreads) keys[e] = ~0ull;
+    // keys sorted: every spike when they fit, else the kept earliest
+    const int held = total <= cap ? total : kept;
+    int n2 = 2;
+    while (n2 < held) n2 <<= 1;
+    for (int e = tid; e < n2; e += kMergeThreads) keys[e] = ~0ull;
     __syncthreads();
     if (total <= cap) {
         // every spike fits: gather all of them
@@ -123,10 +129,10 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(const float* __restrict
         }
     }
     __syncthreads();
-    // Bitonic sort of cap keys.
-    for (int size = 2; size <= cap; size <<= 1) {
+    // Bitonic sort of the n2 keys.
+    for (int size = 2; size <= n2; size <<= 1) {
         for (int stride = size >> 1; stride > 0; stride >>= 1) {
-            for (int e = tid; e < cap; e += kMergeThreads) {
+            for (int e = tid; e < n2; e += kMergeThreads) {
                 int partner = e ^ stride;
                 if (partner > e) {
                     bool up = (e & size) == 0;
