@@ -93,31 +93,34 @@ __global__ __launch_bounds__(256) void k_dly_arrival(const float* __restrict__ e
     }
 }
 
-constexpr int kQLdsMax = 8192;          // longest queue sorted in registers and LDS
-constexpr int kQLdsBins = 2048;
-constexpr int kQLdsThreads = 512;
-constexpr int kQR = kQLdsMax / kQLdsThreads;
+// Queues of up to kMax events are sorted in registers and LDS by kThreads
+// threads (kMax / kThreads arrivals each, kMax / 4 bins at most): 8192 by 512
+// threads (two workgroups per CU), 16384 by 1024 (116 KB of LDS, one).
+constexpr int kQLdsMax = 16384;         // longest queue sorted in registers and LDS
 
-__global__ __launch_bounds__(kQLdsThreads) void k_dly_queue_lds(const int32_t* __restrict__ ev_n, int E_max, int N,
+template <int kMax, int kThreads>
+__global__ __launch_bounds__(kThreads) void k_dly_queue_lds(const int32_t* __restrict__ ev_n, int E_max, int N,
                                                                const float* __restrict__ arr,
                                                                float* __restrict__ q_t, int32_t* __restrict__ q_k)
 {
-    __shared__ uint32_t s_at[kQLdsMax];        // binned arrivals (bits)
-    __shared__ uint16_t s_ak[kQLdsMax];        // and their event indices
+    constexpr int kQLdsBins = kMax / 4;
+    constexpr int kQR = kMax / kThreads;
+    __shared__ uint32_t s_at[kMax];        // binned arrivals (bits)
+    __shared__ uint16_t s_ak[kMax];        // and their event indices
     __shared__ int s_bin[kQLdsBins];
-    __shared__ float s_red[kQLdsThreads / kWave];
-    __shared__ int s_part[kQLdsThreads];
+    __shared__ float s_red[kThreads / kWave];
+    __shared__ int s_part[kThreads];
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
     const size_t item = blockIdx.x;
     const int b = (int)(item / (size_t)N);
-    const int nb = min(clamp_count(ev_n[b], E_max), kQLdsMax);
+    const int nb = min(clamp_count(ev_n[b], E_max), kMax);
     if (nb == 0) return;
     const size_t base = item * (size_t)E_max;
-    // the thread's arrivals (event k = tid + r kQLdsThreads), all loads at once
+    // the thread's arrivals (event k = tid + r kThreads), all loads at once
     uint32_t ab[kQR];
 #pragma unroll
     for (int r = 0; r < kQR; ++r) {
-        const int k = tid + r * kQLdsThreads;
+        const int k = tid + r * kThreads;
         ab[r] = k < nb ? __float_as_uint(arr[base + k]) : 0u;
     }
     float mx = 0.0f;
@@ -127,26 +130,26 @@ __global__ __launch_bounds__(kQLdsThreads) void k_dly_queue_lds(const int32_t* _
     if (lane == 0) s_red[wave] = mx;
     int nbins = 1;
     while (nbins < nb && nbins < kQLdsBins) nbins <<= 1;
-    for (int j = tid; j < nbins; j += kQLdsThreads) s_bin[j] = 0;
+    for (int j = tid; j < nbins; j += kThreads) s_bin[j] = 0;
     __syncthreads();
     float amax = s_red[0];
-    for (int w = 1; w < kQLdsThreads / kWave; ++w) amax = fmaxf(amax, s_red[w]);
+    for (int w = 1; w < kThreads / kWave; ++w) amax = fmaxf(amax, s_red[w]);
     const float sc = amax > 0.0f && amax < INFINITY ? (float)nbins / amax : 0.0f;
     int bin[kQR];
 #pragma unroll
     for (int r = 0; r < kQR; ++r) {
         bin[r] = bin_of(__uint_as_float(ab[r]), sc, nbins);
-        if (tid + r * kQLdsThreads < nb) atomicAdd(&s_bin[bin[r]], 1);
+        if (tid + r * kThreads < nb) atomicAdd(&s_bin[bin[r]], 1);
     }
     __syncthreads();
     // exclusive prefix sum over the bins: each thread a contiguous range
-    const int per = (nbins + kQLdsThreads - 1) / kQLdsThreads;
+    const int per = (nbins + kThreads - 1) / kThreads;
     const int j0 = min(tid * per, nbins), j1 = min(j0 + per, nbins);
     int local = 0;
     for (int j = j0; j < j1; ++j) local += s_bin[j];
     s_part[tid] = local;
     __syncthreads();
-    for (int off = 1; off < kQLdsThreads; off <<= 1) {
+    for (int off = 1; off < kThreads; off <<= 1) {
         const int x = tid >= off ? s_part[tid - off] : 0;
         __syncthreads();
         s_part[tid] += x;
@@ -162,7 +165,7 @@ __global__ __launch_bounds__(kQLdsThreads) void k_dly_queue_lds(const int32_t* _
     // scatter into the bins in LDS; s_bin[j] ends at the end of bin j
 #pragma unroll
     for (int r = 0; r < kQR; ++r) {
-        const int k = tid + r * kQLdsThreads;
+        const int k = tid + r * kThreads;
         if (k < nb) {
             const int pos = atomicAdd(&s_bin[bin[r]], 1);
             if (pos < nb) {
@@ -178,7 +181,7 @@ __global__ __launch_bounds__(kQLdsThreads) void k_dly_queue_lds(const int32_t* _
     int mxc = 0;
 #pragma unroll
     for (int r = 0; r < kQR; ++r) {
-        const bool v = tid + r * kQLdsThreads < nb;
+        const bool v = tid + r * kThreads < nb;
         lo[r] = bin[r] > 0 ? s_bin[bin[r] - 1] : 0;
         cnt[r] = v ? s_bin[bin[r]] - lo[r] : 0;
         rank[r] = 0;
@@ -190,7 +193,7 @@ __global__ __launch_bounds__(kQLdsThreads) void k_dly_queue_lds(const int32_t* _
             if (q < cnt[r]) {
                 const uint32_t o = s_at[lo[r] + q];
                 const int ok = s_ak[lo[r] + q];
-                rank[r] += o < ab[r] || (o == ab[r] && ok < tid + r * kQLdsThreads);
+                rank[r] += o < ab[r] || (o == ab[r] && ok < tid + r * kThreads);
             }
         }
     }
@@ -201,11 +204,11 @@ __global__ __launch_bounds__(kQLdsThreads) void k_dly_queue_lds(const int32_t* _
         const int place = lo[r] + rank[r];
         if (cnt[r] > 0 && place < nb) {         // always: a key's bin is the one it was scattered to
             s_at[place] = ab[r];
-            s_ak[place] = (uint16_t)(tid + r * kQLdsThreads);
+            s_ak[place] = (uint16_t)(tid + r * kThreads);
         }
     }
     __syncthreads();
-    for (int i = tid; i < nb; i += kQLdsThreads) {
+    for (int i = tid; i < nb; i += kThreads) {
         q_t[base + i] = __uint_as_float(s_at[i]);
         q_k[base + i] = s_ak[i];
     }
@@ -573,9 +576,12 @@ extern "C" int lif_delay_queues(const float* ev_t, const int32_t* ev_src, const 
         TIMED_LAUNCH("dly_arrival", k_dly_arrival, agrid, dim3(256), 0, stream, ev_t, ev_src, ev_n, E_max, DT, C_in,
                      N_out, arr);
         const dim3 qgrid((unsigned)((size_t)B * N_out));
-        if (E_max <= kQLdsMax)
-            TIMED_LAUNCH("dly_queue", k_dly_queue_lds, qgrid, dim3(kQLdsThreads), 0, stream, ev_n, E_max, N_out, arr,
-                         q_t, q_k);
+        if (E_max <= 8192)
+            TIMED_LAUNCH("dly_queue", (k_dly_queue_lds<8192, 512>), qgrid, dim3(512), 0, stream, ev_n, E_max, N_out,
+                         arr, q_t, q_k);
+        else if (E_max <= kQLdsMax)
+            TIMED_LAUNCH("dly_queue", (k_dly_queue_lds<kQLdsMax, 1024>), qgrid, dim3(1024), 0, stream, ev_n, E_max,
+                         N_out, arr, q_t, q_k);
         else
             TIMED_LAUNCH("dly_queue", k_dly_queue, qgrid, dim3(kQThreads), 0, stream, ev_n, E_max, N_out, arr, keys,
                          q_t, q_k);

@@ -141,13 +141,14 @@ def test_bad_delay_reported(env):
     assert q.status.cpu().numpy()[0] & lif.WARN_BAD_DELAY
 
 
-def test_delays_long_queues(env):
-    """Queues longer than the register/LDS sort (E_max > 8192) bin through
-    global memory."""
-    cfg = W.random_small(86, B=2, C=60, N=20, n_events=12000, T=2.0, gain=2.0)
+@pytest.mark.parametrize("n_events,gain", [(12000, 2.0), (17000, 1.4)])
+def test_delays_long_queues(env, n_events, gain):
+    """Queues past the 512-thread register/LDS sort (E_max > 8192) take the
+    1024-thread one; past 16384 they bin through global memory."""
+    cfg = W.random_small(86, B=2, C=60, N=20, n_events=n_events, T=2.0 * n_events / 12000, gain=gain)
     ev = cfg.events
-    assert ev.E_max > 8192
-    run_case(env, ev, cfg.layers[0].WT, W.uniform_delays(86, 60, 20), "long queues E_max=12000")
+    assert ev.E_max > 8192 and (n_events < 16384 or ev.E_max > 16384)
+    run_case(env, ev, cfg.layers[0].WT, W.uniform_delays(86, 60, 20), f"long queues E_max={ev.E_max}")
 
 
 @pytest.mark.timeout(600)
