@@ -423,16 +423,17 @@ __device__ __forceinline__ void fx_add(long long* p, double v, double sc)
     atomicAdd((unsigned long long*)p, (unsigned long long)llrint(v * sc));
 }
 
-__global__ __launch_bounds__(kWave * kDlyWaves) void k_dly_adjoint(
-    const float* __restrict__ q_t, const int32_t* __restrict__ q_k, const int32_t* __restrict__ ev_src,
-    const int32_t* __restrict__ ev_n, int B, int E_max, const float* __restrict__ WT, int C_in, int N, Model m,
-    const float* __restrict__ out_t, const int32_t* __restrict__ out_n, const int32_t* __restrict__ out_k,
-    const double* __restrict__ mu, const double* __restrict__ scale, long long* __restrict__ gw,
-    long long* __restrict__ gd, long long* __restrict__ gt)
+// The walk of one (sample, neuron) item; add_wd(j, dL/dw_j, dL/dd_j) takes
+// the weight and delay terms of an event from input channel j.
+template <class AddWD>
+__device__ __forceinline__ void dly_walk(size_t item, const float* __restrict__ q_t, const int32_t* __restrict__ q_k,
+                                         const int32_t* __restrict__ ev_src, const int32_t* __restrict__ ev_n,
+                                         int E_max, const float* __restrict__ WT, int C_in, int N, const Model& m,
+                                         const float* __restrict__ out_t, const int32_t* __restrict__ out_n,
+                                         const int32_t* __restrict__ out_k, const double* __restrict__ mu,
+                                         const double* __restrict__ scale, AddWD add_wd, long long* __restrict__ gt)
 {
     const int lane = (int)threadIdx.x % kWave;
-    const size_t item = (size_t)blockIdx.x * kDlyWaves + threadIdx.x / kWave;
-    if (item >= (size_t)B * N) return;
     const int ns = min(out_n[item], m.s_max);
     if (ns <= 0) return;
     const int b = (int)(item / (size_t)N), n = (int)(item % (size_t)N);
@@ -446,7 +447,7 @@ __global__ __launch_bounds__(kWave * kDlyWaves) void k_dly_adjoint(
     const float* qa = q_t + item * (size_t)E_max;
     const int32_t* qi = q_k + item * (size_t)E_max;
     const int32_t* src = ev_src + (size_t)b * E_max;
-    const double sW = scale[0], sD = scale[1], sT = scale[2];
+    const double sT = scale[2];
     // the step holding queue event klast - 1, and the carry of the spikes
     // after it (every spike with out_k = klast), referred to its arrival
     int r_last = klast - 1;
@@ -482,10 +483,8 @@ __global__ __launch_bounds__(kWave * kDlyWaves) void k_dly_adjoint(
                     Ps += mo[s] * exp(-u * m.inv_ts);
                 }
             }
-            const size_t wi = (size_t)j * N + n;
-            fx_add(&gw[wi], m.kappa * (Pm - Ps), sW);
             const double ga = w * m.kappa * (Pm * m.inv_tm - Ps * m.inv_ts);
-            if (gd) fx_add(&gd[wi], ga, sD);
+            add_wd(j, m.kappa * (Pm - Ps), ga);
             if (gt) fx_add(&gt[(size_t)b * E_max + k], ga, sT);
         }
         if (f == 0) break;
@@ -502,6 +501,70 @@ __global__ __launch_bounds__(kWave * kDlyWaves) void k_dly_adjoint(
         r_last = f - 1;
         f -= kWave;
         s_hi = s_lo;
+    }
+}
+
+// One wave per (sample, neuron); dL/dW and dL/dD added to global memory.
+__global__ __launch_bounds__(kWave * kDlyWaves) void k_dly_adjoint(
+    const float* __restrict__ q_t, const int32_t* __restrict__ q_k, const int32_t* __restrict__ ev_src,
+    const int32_t* __restrict__ ev_n, int B, int E_max, const float* __restrict__ WT, int C_in, int N, Model m,
+    const float* __restrict__ out_t, const int32_t* __restrict__ out_n, const int32_t* __restrict__ out_k,
+    const double* __restrict__ mu, const double* __restrict__ scale, long long* __restrict__ gw,
+    long long* __restrict__ gd, long long* __restrict__ gt)
+{
+    const size_t item = (size_t)blockIdx.x * kDlyWaves + threadIdx.x / kWave;
+    if (item >= (size_t)B * N) return;
+    const int n = (int)(item % (size_t)N);
+    const double sW = scale[0], sD = scale[1];
+    auto add_wd = [&](int j, double vw, double vd) {
+        const size_t wi = (size_t)j * N + n;
+        fx_add(&gw[wi], vw, sW);
+        if (gd) fx_add(&gd[wi], vd, sD);
+    };
+    dly_walk(item, q_t, q_k, ev_src, ev_n, E_max, WT, C_in, N, m, out_t, out_n, out_k, mu, scale, add_wd, gt);
+}
+
+// For C_in <= kDlyLdsMaxC: one workgroup per (neuron, kDlyLdsWaves samples),
+// a wave per sample; the neuron's dL/dW and dL/dD column is summed in LDS
+// (2 C_in 64-bit fixed-point sums, order free) and added to global memory
+// once per workgroup, nonzero entries only.
+constexpr int kDlyLdsWaves = 8;
+constexpr int kDlyLdsMaxC = 4096;
+
+__global__ __launch_bounds__(kWave * kDlyLdsWaves) void k_dly_adjoint_lds(
+    const float* __restrict__ q_t, const int32_t* __restrict__ q_k, const int32_t* __restrict__ ev_src,
+    const int32_t* __restrict__ ev_n, int B, int E_max, const float* __restrict__ WT, int C_in, int N, Model m,
+    const float* __restrict__ out_t, const int32_t* __restrict__ out_n, const int32_t* __restrict__ out_k,
+    const double* __restrict__ mu, const double* __restrict__ scale, long long* __restrict__ gw,
+    long long* __restrict__ gd, long long* __restrict__ gt, int nbg)
+{
+    extern __shared__ long long s_wd[];            // [C_in] dL/dW sums, then [C_in] dL/dD sums
+    long long* s_w = s_wd;
+    long long* s_d = s_wd + C_in;
+    const int n = (int)(blockIdx.x / (unsigned)nbg), bg = (int)(blockIdx.x % (unsigned)nbg);
+    const int tid = (int)threadIdx.x;
+    for (int j = tid; j < C_in; j += (int)blockDim.x) {
+        s_w[j] = 0;
+        s_d[j] = 0;
+    }
+    __syncthreads();
+    const int b = bg * kDlyLdsWaves + tid / kWave;
+    if (b < B) {
+        const double sW = scale[0], sD = scale[1];
+        const bool want_d = gd != nullptr;
+        auto add_wd = [&](int j, double vw, double vd) {
+            atomicAdd((unsigned long long*)&s_w[j], (unsigned long long)llrint(vw * sW));
+            if (want_d) atomicAdd((unsigned long long*)&s_d[j], (unsigned long long)llrint(vd * sD));
+        };
+        dly_walk((size_t)b * N + n, q_t, q_k, ev_src, ev_n, E_max, WT, C_in, N, m, out_t, out_n, out_k, mu, scale,
+                 add_wd, gt);
+    }
+    __syncthreads();
+    for (int j = tid; j < C_in; j += (int)blockDim.x) {
+        const size_t wi = (size_t)j * N + n;
+        const long long vw = s_w[j], vd = s_d[j];
+        if (vw) atomicAdd((unsigned long long*)&gw[wi], (unsigned long long)vw);
+        if (gd && vd) atomicAdd((unsigned long long*)&gd[wi], (unsigned long long)vd);
     }
 }
 
@@ -660,10 +723,18 @@ extern "C" int lif_layer_backward_delayed(const float* q_t, const int32_t* q_k, 
     TIMED_LAUNCH("dly_wmax", k_dly_wmax, dim3(grid_for(nW)), dim3(256), 0, stream, WT, nW, wmax);
     TIMED_LAUNCH("dly_scale", k_dly_scale, dim3(1), dim3(kDlyScaleThreads), 0, stream, musum, nn, ev_n, B, E_max,
                  N_out, m, wmax, scale);
-    if (nn && E_max > 0)
-        TIMED_LAUNCH("dly_adjoint", k_dly_adjoint, dim3((unsigned)((nn + kDlyWaves - 1) / kDlyWaves)),
-                     dim3(kWave * kDlyWaves), 0, stream, q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N_out, m, out_t,
-                     out_n, out_k, mu, scale, gw, grad_DT ? gd : nullptr, grad_ev_t ? gt : nullptr);
+    if (nn && E_max > 0) {
+        if (C_in <= kDlyLdsMaxC) {
+            const int nbg = (B + kDlyLdsWaves - 1) / kDlyLdsWaves;
+            TIMED_LAUNCH("dly_adjoint", k_dly_adjoint_lds, dim3((unsigned)((size_t)N_out * nbg)),
+                         dim3(kWave * kDlyLdsWaves), (size_t)2 * C_in * sizeof(long long), stream, q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N_out, m,
+                         out_t, out_n, out_k, mu, scale, gw, grad_DT ? gd : nullptr, grad_ev_t ? gt : nullptr, nbg);
+        } else {
+            TIMED_LAUNCH("dly_adjoint", k_dly_adjoint, dim3((unsigned)((nn + kDlyWaves - 1) / kDlyWaves)),
+                         dim3(kWave * kDlyWaves), 0, stream, q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N_out, m,
+                         out_t, out_n, out_k, mu, scale, gw, grad_DT ? gd : nullptr, grad_ev_t ? gt : nullptr);
+        }
+    }
     TIMED_LAUNCH("dly_convert", k_dly_convert, dim3(grid_for(work)), dim3(256), 0, stream, gw, gd, gt, scale, nW, nT,
                  grad_WT, grad_DT, grad_ev_t);
     return check_launch();

@@ -141,6 +141,15 @@ def test_bad_delay_reported(env):
     assert q.status.cpu().numpy()[0] & lif.WARN_BAD_DELAY
 
 
+def test_delays_wide_input(env):
+    """More input channels than the LDS column sums of the backward hold
+    (C_in > 4096): dL/dW and dL/dD go straight to global memory."""
+    cfg = W.random_small(87, B=3, C=4500, N=12, n_events=900, T=0.5, gain=60.0)
+    ev = cfg.events
+    st = run_case(env, ev, cfg.layers[0].WT, W.uniform_delays(87, 4500, 12), "wide input C_in=4500")
+    assert st["spikes"] > 0
+
+
 @pytest.mark.parametrize("n_events,gain", [(12000, 2.0), (17000, 1.4)])
 def test_delays_long_queues(env, n_events, gain):
     """Queues past the 512-thread register/LDS sort (E_max > 8192) take the
