@@ -315,3 +315,84 @@ def spike_count_reg_grad(ev_t, ev_src, ev_n, WT, out_t, out_k, out_n, tm, ts, th
                     V1 = V0 * emL + ka * I0 * (emL - esL)
                     gT[b, j] += c * (I0 * esL - V1) / tm
     return L_reg, L_over, gW, gT, gS
+
+
+# ---------------------------------------------------------------------------
+# The same regularisers on a layer with synaptic delays
+# ---------------------------------------------------------------------------
+
+def delayed_interval_tables(ev_src, ev_n, WT, q_t, q_k, out_t, out_k, out_n, tm, ts, th, vr, t_end):
+    """interval_table of every (sample, neuron) of a layer with synaptic
+    delays (Sec. 3.1 Eq. spike_input): a neuron's input sequence is its own
+    arrival queue q_t[b, i], q_k[b, i] (App. E.2; oracle.delay_queues), so its
+    intervals lie between consecutive arrivals and out_k counts queue events.
+    Returns tables[b][i]."""
+    B, N = out_n.shape
+    tables = []
+    for b in range(B):
+        n = int(ev_n[b])
+        row = []
+        for i in range(N):
+            ns = int(out_n[b, i])
+            k = np.asarray(q_k[b, i, :n])
+            w = WT[np.asarray(ev_src[b])[k], i]
+            row.append(interval_table(q_t[b, i, :n], n, w, out_t[b, i, :ns], out_k[b, i, :ns], ns, tm, ts, th, vr,
+                                      t_end))
+        tables.append(row)
+    return tables
+
+
+def spike_count_reg_delayed_grad(ev_t, ev_src, ev_n, WT, q_t, q_k, out_t, out_k, out_n, tm, ts, th, vr, t_end,
+                                 rp: RegParams):
+    """spike_count_reg_grad for a layer with synaptic delays: every input
+    time of a neuron is its arrival a = t_k + d_{src_k, i} (its queue,
+    q_t / q_k), so a term of dL/da goes both to dL/dt_k and to
+    dL/dd_{src_k, i} (d a / d t_k = d a / d d = 1).  Returns (L_reg, L_over,
+    gW_direct [C, N], gD_direct [C, N], gT_direct [B, E_max], g_spike
+    [B, N, s_max])."""
+    B, N = out_n.shape
+    C = WT.shape[0]
+    E = ev_t.shape[1]
+    S = out_t.shape[2]
+    ka = ts / (tm - ts)
+    tables = delayed_interval_tables(ev_src, ev_n, WT, q_t, q_k, out_t, out_k, out_n, tm, ts, th, vr, t_end)
+    L_reg, L_over, coef = spike_count_reg(tables, out_n, th, rp)
+    gW = np.zeros((C, N))
+    gD = np.zeros((C, N))
+    gT = np.zeros((B, E))
+    gS = np.zeros((B, N, S))
+    for b in range(B):
+        n = int(ev_n[b])
+        for i in range(N):
+            k = np.asarray(q_k[b, i, :n], np.int64)
+            a = np.asarray(q_t[b, i, :n], np.float64)
+            src = np.asarray(ev_src[b], np.int64)[k]
+            w = np.asarray(WT[src, i], np.float64)
+            ns = int(out_n[b, i])
+            st = np.asarray(out_t[b, i, :ns], np.float64)
+            sk = np.asarray(out_k[b, i, :ns])
+            ga = np.zeros(n)                       # dL/da of each queue event
+            for j, (t0, t1, V0, I0, vmax, u, spiked) in enumerate(tables[b][i]):
+                c = coef[b][i][j]
+                if c == 0.0:
+                    continue
+                tau = t0 + u
+                # the arrivals before the interval (queue events r < j)
+                d = tau - a[:j]
+                em, es = np.exp(-d / tm), np.exp(-d / ts)
+                np.add.at(gW[:, i], src[:j], c * ka * (em - es))
+                ga[:j] += -c * w[:j] * ka * (-em / tm + es / ts)
+                # the spikes before the interval
+                before = sk < j
+                gS[b, i, :ns][before] += c * (-(th - vr) / tm) * np.exp(-(tau - st[before]) / tm)
+                # an argmax at an interval end that is an arrival moves with it
+                L = t1 - t0
+                if u == 0.0 and j > 0:
+                    ga[j - 1] += c * (I0 - V0) / tm
+                elif j < n and u == L and L > 0.0:
+                    emL, esL = math.exp(-L / tm), math.exp(-L / ts)
+                    V1 = V0 * emL + ka * I0 * (emL - esL)
+                    ga[j] += c * (I0 * esL - V1) / tm
+            np.add.at(gT[b], k, ga)
+            np.add.at(gD[:, i], src, ga)
+    return L_reg, L_over, gW, gD, gT, gS

@@ -289,3 +289,103 @@ def test_regulariser_gradients_match_finite_differences(vr):
             assert abs(fd - gT[b, k]) <= 2e-3 * max(abs(fd), 1e-2 * np.abs(gT).max()), (b, k, fd, gT[b, k])
             done += 1
     assert done >= 10
+
+
+def _dreg_loss(ev, WT, DT, P, rp):
+    """lam_reg L_reg + lam_over L_over of a delayed layer's own forward."""
+    r = oracle.forward_delayed(ev.ev_t, ev.ev_src, ev.ev_n, WT, DT, P)
+    q_t, q_k = oracle.delay_queues(ev.ev_t, ev.ev_src, ev.ev_n, DT)
+    tables = OL.delayed_interval_tables(ev.ev_src, ev.ev_n, WT, q_t, q_k, r.out_t, r.out_k, r.out_n, P.tau_mem,
+                                        P.tau_syn, P.v_th, P.v_reset, P.t_end)
+    L_reg, L_over, _ = OL.spike_count_reg(tables, r.out_n, P.v_th, rp)
+    return rp.lam_reg * L_reg + rp.lam_over * L_over, r.out_n, q_k
+
+
+def test_delayed_regulariser_tables_reduce_to_the_plain_ones():
+    """With zero delays every neuron's queue is the sample's own event order
+    (arrivals t_k, ties by k), so the delayed tables are the plain ones."""
+    cfg = W.random_small(53, B=2, C=10, N=5, n_events=50, T=0.15, gain=10.0)
+    ev = cfg.events
+    WT = cfg.layers[0].WT
+    P = oracle.LifParams(v_reset=-0.3)
+    r = oracle.forward(ev.ev_t, ev.ev_src, ev.ev_n, WT, P)
+    q_t, q_k = oracle.delay_queues(ev.ev_t, ev.ev_src, ev.ev_n, np.zeros_like(WT))
+    tab_d = OL.delayed_interval_tables(ev.ev_src, ev.ev_n, WT, q_t, q_k, r.out_t, r.out_k, r.out_n, P.tau_mem,
+                                       P.tau_syn, P.v_th, P.v_reset, P.t_end)
+    rp = OL.RegParams(c_target=3.0, lam_reg=0.7, lam_over=0.4)
+    a = OL.spike_count_reg_grad(ev.ev_t, ev.ev_src, ev.ev_n, WT, r.out_t, r.out_k, r.out_n, P.tau_mem, P.tau_syn,
+                                P.v_th, P.v_reset, P.t_end, rp)
+    d = OL.spike_count_reg_delayed_grad(ev.ev_t, ev.ev_src, ev.ev_n, WT, q_t, q_k, r.out_t, r.out_k, r.out_n,
+                                        P.tau_mem, P.tau_syn, P.v_th, P.v_reset, P.t_end, rp)
+    for b in range(ev.B):
+        for i in range(WT.shape[1]):
+            n = int(ev.ev_n[b])
+            plain = OL.interval_table(ev.ev_t[b, :n], n, WT[ev.ev_src[b, :n], i], r.out_t[b, i], r.out_k[b, i],
+                                      int(r.out_n[b, i]), P.tau_mem, P.tau_syn, P.v_th, P.v_reset, P.t_end)
+            assert tab_d[b][i] == plain
+    assert d[0] == a[0] and d[1] == a[1]
+    assert np.allclose(d[2], a[2], rtol=1e-12, atol=0) and np.allclose(d[4], a[3], rtol=1e-12, atol=1e-300)
+    assert np.array_equal(d[5], a[4])
+    # with zero delays dL/dd_{j,i} sums the arrival terms of channel j's events at neuron i
+    assert np.abs(d[3]).max() > 0
+
+
+@pytest.mark.parametrize("vr", [0.0, -0.3])
+def test_delayed_regulariser_gradients_match_finite_differences(vr):
+    """The regularisers of a layer with synaptic delays: the direct terms plus
+    the delayed layer's backward pass of the spike-time terms against central
+    differences of the loss from a fresh delayed forward, for weights, delays
+    and input times (steps float32 holds exactly; cases whose spike counts or
+    queue order the step changes are skipped)."""
+    cfg = W.random_small(52, B=3, C=12, N=6, n_events=60, T=0.15, gain=10.0)
+    ev = cfg.events
+    WT = cfg.layers[0].WT.astype(np.float32)
+    DT = W.uniform_delays(52, 12, 6, d_max=0.03)
+    P = oracle.LifParams(solver_reg=0.0, v_reset=vr)
+    rp = OL.RegParams(c_target=3.0, lam_reg=0.7, lam_over=0.4)
+    r = oracle.forward_delayed(ev.ev_t, ev.ev_src, ev.ev_n, WT, DT, P)
+    assert r.out_n.max() > 3 and (r.out_n.mean(axis=0) < 3).any() and (r.out_n.mean(axis=0) > 3).any()
+    q_t, q_k = oracle.delay_queues(ev.ev_t, ev.ev_src, ev.ev_n, DT)
+    L_reg, L_over, gWd, gDd, gTd, gS = OL.spike_count_reg_delayed_grad(
+        ev.ev_t, ev.ev_src, ev.ev_n, WT, q_t, q_k, r.out_t, r.out_k, r.out_n, P.tau_mem, P.tau_syn, P.v_th,
+        P.v_reset, P.t_end, rp)
+    gWs, gDs, gTs = oracle.backward_delayed(ev.ev_t, ev.ev_src, ev.ev_n, WT, DT, r, gS, P)
+    gW, gD, gT = gWd + gWs, gDd + gDs, gTd + gTs
+    assert np.abs(gW).max() > 0 and np.abs(gD).max() > 0 and np.abs(gS).max() > 0
+
+    def same(res):
+        return np.array_equal(res[1], r.out_n) and np.array_equal(res[2], q_k)
+
+    checked = {"W": 0, "D": 0, "t": 0}
+    for c in range(WT.shape[0]):
+        for i in range(WT.shape[1]):
+            for name, base, h, g in (("W", WT, 2.0 ** -14, gW), ("D", DT, 2.0 ** -20, gD)):
+                xp, xm = base.copy(), base.copy()
+                xp[c, i] += np.float32(h)
+                xm[c, i] -= np.float32(h)
+                if name == "D" and xm[c, i] < 0:
+                    continue
+                rp_ = _dreg_loss(ev, xp, DT, P, rp) if name == "W" else _dreg_loss(ev, WT, xp, P, rp)
+                rm_ = _dreg_loss(ev, xm, DT, P, rp) if name == "W" else _dreg_loss(ev, WT, xm, P, rp)
+                if not (same(rp_) and same(rm_)):
+                    continue
+                fd = (rp_[0] - rm_[0]) / (2 * h)
+                tol = 2e-4 if name == "W" else 2e-3
+                assert abs(fd - g[c, i]) <= tol * max(abs(fd), 1e-2 * np.abs(g).max()), (name, c, i, fd, g[c, i])
+                checked[name] += 1
+    for b in range(ev.B):
+        for k in range(0, int(ev.ev_n[b]), 5):
+            h = 2.0 ** -20
+            tp, tm_ = ev.ev_t.copy(), ev.ev_t.copy()
+            tp[b, k] += h
+            tm_[b, k] -= h
+            if (k + 1 < ev.ev_n[b] and tp[b, k] >= ev.ev_t[b, k + 1]) or (k > 0 and tm_[b, k] <= ev.ev_t[b, k - 1]):
+                continue
+            rp_ = _dreg_loss(W.EventBatch(tp, ev.ev_src, ev.ev_n), WT, DT, P, rp)
+            rm_ = _dreg_loss(W.EventBatch(tm_, ev.ev_src, ev.ev_n), WT, DT, P, rp)
+            if not (same(rp_) and same(rm_)):
+                continue
+            fd = (rp_[0] - rm_[0]) / (2 * h)
+            assert abs(fd - gT[b, k]) <= 2e-3 * max(abs(fd), 1e-2 * np.abs(gT).max()), (b, k, fd, gT[b, k])
+            checked["t"] += 1
+    assert checked["W"] >= 40 and checked["D"] >= 30 and checked["t"] >= 10, checked
