@@ -204,8 +204,9 @@ def test_delay_argument_errors(lib):
     assert q(9, None) == L.LIF_ERR_ARG              # q_k required
     need = L.lif_delay_queues_workspace_size(2, 10, 8)
     assert need >= 2 * 8 * 10 * 4 and q(12, need - 1) == L.LIF_ERR_WORKSPACE
-    # queues longer than the LDS sort take 64-bit keys as well
-    assert L.lif_delay_queues_workspace_size(2, 9000, 8) >= 2 * 8 * 9000 * 12
+    # queues up to 16384 events are sorted in LDS (arrivals only); longer ones take 64-bit keys as well
+    assert 2 * 8 * 16384 * 4 <= L.lif_delay_queues_workspace_size(2, 16384, 8) < 2 * 8 * 16384 * 12
+    assert L.lif_delay_queues_workspace_size(2, 16385, 8) >= 2 * 8 * 16385 * 12
     assert L.lif_delay_queues_workspace_size(-1, 10, 8) == 0
     # forward: q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N, p, out_t, out_n, out_i, out_k, status, stream
     fb = [F, F, F, F, 2, 10, F, 4, 8, ctypes.byref(p), F, F, F, F, F, None]
@@ -252,3 +253,35 @@ def test_spike_count_reg_backward_argument_errors(lib):
     need = L.lif_spike_count_reg_backward_workspace_size(2, 10, 4, 8)
     assert need > L.lif_spike_count_reg_workspace_size(2, 10, 4, 8)
     assert call(20, need - 1) == L.LIF_ERR_WORKSPACE
+
+
+def test_spike_count_reg_delayed_argument_errors(lib):
+    p = L.Params().c()
+    # q_t, q_k, ev_src, ev_n, B, E, WT, C, N, p, out_t, out_n, out_k, c_target, loss, under, over, ws, ws_bytes,
+    # stream
+    fb = [F, F, F, F, 2, 10, F, 4, 8, ctypes.byref(p), F, F, F, 4.0, None, None, None, F, 10 ** 9, None]
+
+    def f(i, v):
+        a = list(fb)
+        a[i] = v
+        return L.lif_spike_count_reg_delayed(*a)
+    assert f(1, None) == L.LIF_ERR_ARG              # q_k required
+    assert f(12, None) == L.LIF_ERR_ARG             # out_k required
+    assert f(13, 0.0) == L.LIF_ERR_ARG              # c_target > 0
+    bad = L.Params(v_th=0.0).c()
+    assert f(9, ctypes.byref(bad)) == L.LIF_ERR_THRESHOLD
+    need = L.lif_spike_count_reg_delayed_workspace_size(2, 10, 4, 8)
+    assert need >= 2 * 8 * 11 * 8 and f(18, 256) == L.LIF_ERR_WORKSPACE
+    assert L.lif_spike_count_reg_delayed_workspace_size(-1, 10, 4, 8) == 0
+    # backward: ... c_target, lam_reg, lam_over, loss, g_spike, gW, gD, gT, ws, ws_bytes, stream
+    bb = [F, F, F, F, 2, 10, F, 4, 8, ctypes.byref(p), F, F, F, 4.0, 1.0, 1.0, None, F, F, None, None, F, 10 ** 9,
+          None]
+
+    def b(i, v):
+        a = list(bb)
+        a[i] = v
+        return L.lif_spike_count_reg_delayed_backward(*a)
+    assert b(17, None) == L.LIF_ERR_ARG             # grad_spike required
+    assert b(18, None) == L.LIF_ERR_ARG             # grad_WT required
+    assert b(14, math.nan) == L.LIF_ERR_ARG         # finite lambda
+    assert b(22, need - 1) == L.LIF_ERR_WORKSPACE
