@@ -411,6 +411,43 @@ int lif_spike_count_reg_backward(const float* ev_t, const int32_t* ev_src, const
                                  double lam_over, float* loss, float* grad_spike, float* grad_WT, float* grad_ev_t,
                                  void* ws, size_t ws_bytes, lif_stream_t stream);
 
+/* Spike-count regularisers of a layer with synaptic delays: the same terms */
+/* as lif_spike_count_reg with each neuron's intervals lying between        */
+/* consecutive arrivals of its own queue (Sec. 3.1 Eq. spike_input, App.    */
+/* E.2): interval r of neuron i ends at its queue event r, interval ev_n[b] */
+/* is the open one up to t_end, and a spike belongs to interval out_k (the  */
+/* queue events consumed before it, as lif_layer_forward_delayed counts).   */
+/*   q_t, q_k   the queues of lif_delay_queues ([B][N_out][E_max])          */
+/*   out_*      lif_layer_forward_delayed's outputs for them                */
+/*   loss, under, over  as lif_spike_count_reg (all nullable)               */
+/* ws: lif_spike_count_reg_delayed_workspace_size(...) bytes (the same size */
+/* serves the backward below).  Bitwise reproducible.  Errors as            */
+/* lif_spike_count_reg.                                                     */
+/* Backward: the gradient of lambda_reg L_reg + lambda_over L_over with the */
+/* gates held constant, an arrival's term going to both its input time and  */
+/* its delay (d a / d t = d a / d d = 1):                                   */
+/*   grad_spike float [B][N_out][s_max]  ADDED to (run                      */
+/*              lif_layer_backward_delayed with it for the part through     */
+/*              the spikes)                                                 */
+/*   grad_WT, grad_DT float [C_in][N_out], grad_ev_t float [B][E_max]: the  */
+/*              direct parts, overwritten (grad_DT, grad_ev_t nullable)     */
+/* about 8 bytes per (sample, neuron, queue event) of workspace.            */
+/* --------------------------------------------------------------------- */
+size_t lif_spike_count_reg_delayed_workspace_size(int B, int E_max, int C_in, int N_out);
+
+int lif_spike_count_reg_delayed(const float* q_t, const int32_t* q_k, const int32_t* ev_src, const int32_t* ev_n,
+                                int B, int E_max, const float* WT, int C_in, int N_out, const lif_params* p,
+                                const float* out_t, const int32_t* out_n, const int32_t* out_k, double c_target,
+                                float* loss, float* under, float* over, void* ws, size_t ws_bytes,
+                                lif_stream_t stream);
+
+int lif_spike_count_reg_delayed_backward(const float* q_t, const int32_t* q_k, const int32_t* ev_src,
+                                         const int32_t* ev_n, int B, int E_max, const float* WT, int C_in,
+                                         int N_out, const lif_params* p, const float* out_t, const int32_t* out_n,
+                                         const int32_t* out_k, double c_target, double lam_reg, double lam_over,
+                                         float* loss, float* grad_spike, float* grad_WT, float* grad_DT,
+                                         float* grad_ev_t, void* ws, size_t ws_bytes, lif_stream_t stream);
+
 /* --------------------------------------------------------------------- */
 /* Adam step (the optimiser the paper trains with, App. E): for each of    */
 /* the n parameters, m1 = b1 m1 + (1 - b1) g, m2 = b2 m2 + (1 - b2) g^2,   */

@@ -53,6 +53,8 @@ EXPORTED = ["lif_version", "lif_layer_forward_workspace_size", "lif_layer_forwar
             "lif_delay_queues_workspace_size", "lif_delay_queues",
             "lif_layer_forward_delayed", "lif_layer_forward_delayed_sequential",
             "lif_layer_backward_delayed_workspace_size", "lif_layer_backward_delayed",
+            "lif_spike_count_reg_delayed_workspace_size", "lif_spike_count_reg_delayed",
+            "lif_spike_count_reg_delayed_backward",
             "lif_add", "lif_softplus", "lif_softplus_grad", "lif_timer_enable", "lif_timer_read"]
 LIF_LI_MAX_CLASSES = 64
 
@@ -182,6 +184,15 @@ def load(path: Optional[str] = None):
     lib.lif_spike_count_reg_backward.restype = _I
     lib.lif_spike_count_reg_backward.argtypes = [_P, _P, _P, _I, _I, _P, _I, _I, _PP, _P, _P, _P, ctypes.c_double,
                                                  ctypes.c_double, ctypes.c_double, _P, _P, _P, _P, _P, _SZ, _P]
+    lib.lif_spike_count_reg_delayed_workspace_size.restype = _SZ
+    lib.lif_spike_count_reg_delayed_workspace_size.argtypes = [_I, _I, _I, _I]
+    lib.lif_spike_count_reg_delayed.restype = _I
+    lib.lif_spike_count_reg_delayed.argtypes = [_P, _P, _P, _P, _I, _I, _P, _I, _I, _PP, _P, _P, _P, ctypes.c_double,
+                                                _P, _P, _P, _P, _SZ, _P]
+    lib.lif_spike_count_reg_delayed_backward.restype = _I
+    lib.lif_spike_count_reg_delayed_backward.argtypes = [_P, _P, _P, _P, _I, _I, _P, _I, _I, _PP, _P, _P, _P,
+                                                         ctypes.c_double, ctypes.c_double, ctypes.c_double, _P, _P,
+                                                         _P, _P, _P, _P, _SZ, _P]
     lib.lif_delay_queues_workspace_size.restype = _SZ
     lib.lif_delay_queues_workspace_size.argtypes = [_I, _I, _I]
     lib.lif_delay_queues.restype = _I
@@ -316,6 +327,18 @@ def lif_layer_backward_delayed_workspace_size(B, E_max, C_in, N_out, p: lif_para
 
 def lif_layer_backward_delayed(*args) -> int:
     return load().lif_layer_backward_delayed(*args)
+
+
+def lif_spike_count_reg_delayed_workspace_size(B, E_max, C_in, N_out) -> int:
+    return load().lif_spike_count_reg_delayed_workspace_size(B, E_max, C_in, N_out)
+
+
+def lif_spike_count_reg_delayed(*args) -> int:
+    return load().lif_spike_count_reg_delayed(*args)
+
+
+def lif_spike_count_reg_delayed_backward(*args) -> int:
+    return load().lif_spike_count_reg_delayed_backward(*args)
 
 
 def lif_add(*args) -> int:
@@ -655,6 +678,57 @@ def spike_count_reg_backward(ev_t, ev_src, ev_n, WT, fwd: ForwardOut, c_target: 
                                       _ptr(gT), _ptr(ws), ws.numel(), _stream(stream))
     _check("lif_spike_count_reg_backward", rc)
     return loss, grad_spike, gW, gT
+
+
+def spike_count_reg_delayed(q: DelayQueues, ev_src, ev_n, WT, fwd: ForwardOut, c_target: float,
+                            params: Params = Params(), stream=None, ws=None):
+    """Run lif_spike_count_reg_delayed on the queues of delay_queues and the
+    delayed forward's outputs; returns (loss [2], under [B, N], over [B, N])."""
+    torch = _torch()
+    B, E, C, N = _queue_inputs(q, ev_src, ev_n, WT)
+    dev = WT.device
+    p = params.c()
+    loss = torch.empty(2, dtype=torch.float32, device=dev)
+    under = torch.empty((B, N), dtype=torch.float32, device=dev)
+    over = torch.empty((B, N), dtype=torch.float32, device=dev)
+    need = lif_spike_count_reg_delayed_workspace_size(B, E, C, N)
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    rc = lif_spike_count_reg_delayed(_ptr(q.q_t), _ptr(q.q_k), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(WT), C, N,
+                                     ctypes.byref(p), _ptr(fwd.out_t), _ptr(fwd.out_n), _ptr(fwd.out_k),
+                                     float(c_target), _ptr(loss), _ptr(under), _ptr(over), _ptr(ws), ws.numel(),
+                                     _stream(stream))
+    _check("lif_spike_count_reg_delayed", rc)
+    return loss, under, over
+
+
+def spike_count_reg_delayed_backward(q: DelayQueues, ev_src, ev_n, WT, fwd: ForwardOut, c_target: float,
+                                     lam_reg: float = 1.0, lam_over: float = 1.0, params: Params = Params(),
+                                     grad_spike=None, want_delay_grad: bool = True, want_time_grad: bool = True,
+                                     stream=None, ws=None):
+    """Run lif_spike_count_reg_delayed_backward; returns (loss [2],
+    grad_spike [B, N, s_max] (the given tensor, added to, or a new one),
+    direct grad_WT, direct grad_DT or None, direct grad_ev_t or None)."""
+    torch = _torch()
+    B, E, C, N = _queue_inputs(q, ev_src, ev_n, WT)
+    dev = WT.device
+    p = params.c()
+    loss = torch.empty(2, dtype=torch.float32, device=dev)
+    if grad_spike is None:
+        grad_spike = torch.zeros((B, N, params.s_max), dtype=torch.float32, device=dev)
+    gW = torch.empty((C, N), dtype=torch.float32, device=dev)
+    gD = torch.empty((C, N), dtype=torch.float32, device=dev) if want_delay_grad else None
+    gT = torch.empty((B, E), dtype=torch.float32, device=dev) if want_time_grad else None
+    need = lif_spike_count_reg_delayed_workspace_size(B, E, C, N)
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    rc = lif_spike_count_reg_delayed_backward(_ptr(q.q_t), _ptr(q.q_k), _ptr(ev_src), _ptr(ev_n), B, E, _ptr(WT), C,
+                                              N, ctypes.byref(p), _ptr(fwd.out_t), _ptr(fwd.out_n), _ptr(fwd.out_k),
+                                              float(c_target), float(lam_reg), float(lam_over), _ptr(loss),
+                                              _ptr(grad_spike), _ptr(gW), _ptr(gD), _ptr(gT), _ptr(ws), ws.numel(),
+                                              _stream(stream))
+    _check("lif_spike_count_reg_delayed_backward", rc)
+    return loss, grad_spike, gW, gD, gT
 
 
 def add_(y, x, stream=None):

@@ -40,6 +40,7 @@
 //                  power-of-two scales that keep every sum below 2^62.
 #include "lif_common.hpp"
 #include "lif_host.hpp"
+#include "lif_reg.hpp"
 
 namespace lif {
 
@@ -586,6 +587,404 @@ __global__ __launch_bounds__(256) void k_dly_convert(const long long* __restrict
         for (size_t x = gtid; x < nT; x += gs) grad_ev_t[x] = (float)((double)gt[x] * iT);
 }
 
+// ---------------------------------------------------------------------------
+// Spike-count regularisers (App. E.1) of a layer with synaptic delays.  A
+// neuron's input intervals lie between consecutive arrivals of its own queue
+// (interval r ends at queue event r; interval nb is the open one up to
+// t_end), so the walks run per (sample, neuron), one wave each, 64 queue
+// events per step with lane l on event f + l and the interval it closes.
+//   k_dreg_walk   forward: the event maps (decays from the arrival gaps, the
+//                 weight jump) composed across the lanes by a log-depth scan
+//                 give each interval's no-reset start state from the step's
+//                 carried state; the reset deficit of the neuron's spikes is
+//                 the carried deficit decayed by the same products plus the
+//                 spikes of the step; V_max (reg_vmax_arg), the hinge sums and
+//                 counts, and the per-interval record.
+//   k_dregg_walk  backward: P_r = sum of the pseudo-spikes of the intervals
+//                 after event r (mu e^{-(argmax - a_r)/tm}, and with ts), by
+//                 P_{r-1} = A_r P_r + mu_r e^{-u_r/tm}: a suffix scan across
+//                 the lanes from the carried P at the step's last event.  Per
+//                 event dL/dw += kappa (P^m - P^s), dL/da = w kappa (P^m/tm -
+//                 P^s/ts) plus the end-point slope terms, added to dL/dd and
+//                 dL/dt; each spike's upstream gradient
+//                 -((th - vr)/tm) P^m e^{-(a_r - t_s)/tm} at the event r that
+//                 closes its interval.
+// ---------------------------------------------------------------------------
+constexpr int kDRegWaves = 4;
+
+// Inclusive scan across the wave of affine maps x -> a x + b, composed in
+// lane order (lane l: the maps of lanes 0 .. l, lane 0's applied first).
+__device__ __forceinline__ void scan_maps_up(double& a, double& b, int lane)
+{
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const double pa = __shfl_up(a, off, kWave), pb = __shfl_up(b, off, kWave);
+        if (lane >= off) {
+            b = fma(a, pb, b);
+            a *= pa;
+        }
+    }
+}
+
+// The same from the top (lane l: the maps of lanes 63 .. l, lane 63's
+// applied first).
+__device__ __forceinline__ void scan_maps_down(double& a, double& b, int lane)
+{
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const double pa = __shfl_down(a, off, kWave), pb = __shfl_down(b, off, kWave);
+        if (lane + off < kWave) {
+            b = fma(a, pb, b);
+            a *= pa;
+        }
+    }
+}
+
+__global__ __launch_bounds__(kWave * kDRegWaves) void k_dreg_walk(
+    const float* __restrict__ q_t, const int32_t* __restrict__ q_k, const int32_t* __restrict__ ev_src,
+    const int32_t* __restrict__ ev_n, int B, int E_max, const float* __restrict__ WT, int C_in, int N, Model m,
+    const float* __restrict__ out_t, const int32_t* __restrict__ out_n, const int32_t* __restrict__ out_k,
+    double* __restrict__ ub, double* __restrict__ ob, float* __restrict__ under, float* __restrict__ over,
+    double2* __restrict__ counts, double* __restrict__ vpmax, float2* __restrict__ rec)
+{
+    const int lane = (int)threadIdx.x % kWave;
+    const size_t item = (size_t)blockIdx.x * kDRegWaves + threadIdx.x / kWave;
+    if (item >= (size_t)B * N) return;
+    const int b = (int)(item / (size_t)N), n = (int)(item % (size_t)N);
+    const int nb = clamp_count(ev_n[b], E_max);
+    const float* qa = q_t + item * (size_t)E_max;
+    const int32_t* qi = q_k + item * (size_t)E_max;
+    const int32_t* src = ev_src + (size_t)b * E_max;
+    const int ns = max(min(out_n[item], m.s_max), 0);
+    const float* st = out_t + item * (size_t)m.s_max;
+    const int32_t* sk = out_k + item * (size_t)m.s_max;
+    float2* rb = rec ? rec + item * ((size_t)E_max + 1) : nullptr;
+    double su = 0.0, so = 0.0, nsil = 0.0, nspk = 0.0, vpm = 0.0;
+    auto take = [&](int j, double V0, double I0, double L, double A, double D, bool spiked, bool end_input) {
+        const RegArg ra = reg_vmax_arg(m, V0, I0, L, A, D);
+        const double vmax = ra.vmax;
+        if (spiked) {
+            so += fmax(vmax - m.th, 0.0);
+            nspk += 1.0;
+        } else {
+            su += fmax(m.th - vmax, 0.0);
+            nsil += 1.0;
+        }
+        if (rb) {
+            const float sgn = spiked ? (vmax > m.th ? -1.0f : 0.0f) : (vmax < m.th ? 1.0f : 0.0f);
+            double slope = 0.0;
+            if (ra.at_start) {
+                slope = j > 0 ? (I0 - V0) * m.inv_tm : 0.0;
+                rb[j] = make_record(sgn, kRecStart, 1.0, 1.0, slope);
+            } else if (ra.at_end && end_input) {
+                slope = (I0 * D - vmax) * m.inv_tm;
+                rb[j] = make_record(sgn, kRecEnd, A, D, slope);
+            } else {                             // inside, or the end t_end of the open interval
+                rb[j] = make_record(sgn, kRecInside, ra.em, ra.es, 0.0);
+            }
+            if (sgn != 0.0f) vpm = fmax(vpm, fabs(slope));
+        }
+    };
+    double U = 0.0, J = 0.0;       // no-reset state after event f - 1
+    double Dc = 0.0;               // reset deficit there, of the spikes with out_k < f
+    double a_prev = 0.0;           // arrival of event f - 1 (0 before the first)
+    int sp = 0;                    // first spike with out_k >= f
+    for (int f = 0; f < nb; f += kWave) {
+        const int r = f + lane;
+        const bool ok = r < nb;
+        const int lv = min(kWave - 1, nb - 1 - f);          // the step's last event (lane)
+        const float af = ok ? qa[r] : 0.0f;
+        const int k = ok ? min(max(qi[r], 0), nb - 1) : 0;
+        const float w = ok ? WT[(size_t)clamp_src(src[k], C_in) * (size_t)N + n] : 0.0f;
+        double ap = __shfl_up((double)af, 1, kWave);         // arrival of event r - 1
+        if (lane == 0) ap = a_prev;
+        const double a = (double)af;
+        const double L = a - ap;
+        double A = 1.0, D = 1.0;
+        if (ok) {
+            A = exp(-L * m.inv_tm);
+            D = exp(-L * m.inv_ts);
+        }
+        double aU = A, bU = ok ? (double)w : 0.0, aJ = D, bJ = bU;
+        scan_maps_up(aU, bU, lane);
+        scan_maps_up(aJ, bJ, lane);
+        double eaU = __shfl_up(aU, 1, kWave), ebU = __shfl_up(bU, 1, kWave);
+        double eaJ = __shfl_up(aJ, 1, kWave), ebJ = __shfl_up(bJ, 1, kWave);
+        if (lane == 0) {
+            eaU = 1.0;
+            ebU = 0.0;
+            eaJ = 1.0;
+            ebJ = 0.0;
+        }
+        const double U0 = fma(eaU, U, ebU), J0 = fma(eaJ, J, ebJ);     // at interval r's start
+        // the deficit at interval r's start: the carried one decayed over
+        // events f .. r - 1 (the product eaU), plus the spikes of intervals
+        // f .. r - 1
+        double Dft = Dc * eaU;
+        bool spiked = false;
+        for (int s = sp; s < ns && sk[s] < f + kWave; ++s) {
+            const int ks = sk[s];
+            if (ks < r) Dft += m.dth * exp(-(ap - (double)st[s]) * m.inv_tm);
+            spiked |= ks == r;
+        }
+        if (ok) take(r, v_of(m, U0, J0) - Dft, J0, L, A, D, spiked, true);
+        // the carry: the state after the step's last event, its arrival and
+        // the deficit there
+        const double Un = fma(aU, U, bU), Jn = fma(aJ, J, bJ);
+        const double a_last = __shfl(a, lv, kWave);
+        double Dn = Dc * __shfl(aU, lv, kWave);
+        while (sp < ns && sk[sp] <= f + lv) {
+            Dn += m.dth * exp(-(a_last - (double)st[sp]) * m.inv_tm);
+            ++sp;
+        }
+        U = __shfl(Un, lv, kWave);
+        J = __shfl(Jn, lv, kWave);
+        Dc = Dn;
+        a_prev = a_last;
+    }
+    {
+        // the open interval after the last arrival, up to t_end
+        const double L = m.t_end - a_prev;
+        const double A = isinf(L) ? 0.0 : exp(-L * m.inv_tm), D = isinf(L) ? 0.0 : exp(-L * m.inv_ts);
+        bool spiked = false;
+        for (int s = sp; s < ns; ++s) spiked |= sk[s] == nb;
+        if (lane == 0) take(nb, v_of(m, U, J) - Dc, J, L, A, D, spiked, false);
+    }
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        su += __shfl_xor(su, off, kWave);
+        so += __shfl_xor(so, off, kWave);
+        nsil += __shfl_xor(nsil, off, kWave);
+        nspk += __shfl_xor(nspk, off, kWave);
+        vpm = fmax(vpm, __shfl_xor(vpm, off, kWave));
+    }
+    if (lane == 0) {
+        const double u = nsil > 0.0 ? su / nsil : 0.0;
+        const double o = nspk > 0.0 ? so / nspk : 0.0;
+        ub[item] = u;
+        ob[item] = o;
+        if (under) under[item] = (float)u;
+        if (over) over[item] = (float)o;
+        if (counts) counts[item] = make_double2(nsil, nspk);
+        if (vpmax) vpmax[item] = vpm;
+    }
+}
+
+// Fixed-point scales of the delayed regularisers' gradient (one workgroup):
+// M = the largest |G_u| nsil + |G_o| nspk (a bound of |P|), Gm the largest
+// |G|, Vp the largest end-point slope of an active record.  A dL/dw term is
+// at most 2 kappa M; a dL/da term at most w_max kappa M (1/tm + 1/ts) +
+// 2 Gm Vp; dL/dW and dL/dD sum at most one term per event of the batch, dL/dt
+// one per neuron: scale = 2^(61 - ceil(log2(bound))) each.
+__global__ __launch_bounds__(kDlyScaleThreads) void k_dregg_scale(const double* __restrict__ musum,
+                                                                const double2* __restrict__ coef,
+                                                                const double* __restrict__ vpmax, size_t nn,
+                                                                const int32_t* __restrict__ ev_n, int B, int E_max,
+                                                                int N, Model m, const uint32_t* __restrict__ wmax,
+                                                                double* __restrict__ scale)
+{
+    __shared__ double s_m[kDlyScaleThreads], s_g[kDlyScaleThreads], s_v[kDlyScaleThreads], s_e[kDlyScaleThreads];
+    double M = 0.0, Gm = 0.0, Vp = 0.0, ev = 0.0;
+    for (size_t i = threadIdx.x; i < nn; i += kDlyScaleThreads) {
+        M = fmax(M, musum[i]);
+        Gm = fmax(Gm, fmax(fabs(coef[i].x), fabs(coef[i].y)));
+        Vp = fmax(Vp, vpmax[i]);
+    }
+    for (int b = threadIdx.x; b < B; b += kDlyScaleThreads) ev += (double)clamp_count(ev_n[b], E_max);
+    s_m[threadIdx.x] = M;
+    s_g[threadIdx.x] = Gm;
+    s_v[threadIdx.x] = Vp;
+    s_e[threadIdx.x] = ev;
+    __syncthreads();
+    for (int off = kDlyScaleThreads / 2; off > 0; off >>= 1) {
+        if ((int)threadIdx.x < off) {
+            s_m[threadIdx.x] = fmax(s_m[threadIdx.x], s_m[threadIdx.x + off]);
+            s_g[threadIdx.x] = fmax(s_g[threadIdx.x], s_g[threadIdx.x + off]);
+            s_v[threadIdx.x] = fmax(s_v[threadIdx.x], s_v[threadIdx.x + off]);
+            s_e[threadIdx.x] += s_e[threadIdx.x + off];
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        const double E = fmax(s_e[0], 1.0), w = (double)__uint_as_float(*wmax);
+        const double term = w * m.kappa * s_m[0] * (m.inv_tm + m.inv_ts) + 2.0 * s_g[0] * s_v[0];
+        const double bounds[3] = {2.0 * m.kappa * s_m[0] * E, term * E, term * (double)N};
+        for (int q = 0; q < 3; ++q) {
+            int ex = 0;
+            if (bounds[q] > 0.0 && isfinite(bounds[q])) frexp(bounds[q], &ex);   // bound < 2^ex
+            scale[q] = ldexp(1.0, 61 - ex);
+        }
+    }
+}
+
+// The backward walk of one (sample, neuron) item; add_wd(j, dL/dw_j,
+// dL/dd_j) takes the weight and delay terms of an event from channel j.
+template <class AddWD>
+__device__ __forceinline__ void dregg_walk(size_t item, const float* __restrict__ q_t,
+                                           const int32_t* __restrict__ q_k, const int32_t* __restrict__ ev_src,
+                                           const int32_t* __restrict__ ev_n, int E_max, const float* __restrict__ WT,
+                                           int C_in, int N, const Model& m, const float* __restrict__ out_t,
+                                           const int32_t* __restrict__ out_n, const int32_t* __restrict__ out_k,
+                                           const float2* __restrict__ rec, const double2* __restrict__ coef,
+                                           const double* __restrict__ scale, AddWD add_wd,
+                                           long long* __restrict__ gt, float* __restrict__ grad_spike)
+{
+    const int lane = (int)threadIdx.x % kWave;
+    const int b = (int)(item / (size_t)N), n = (int)(item % (size_t)N);
+    const int nb = clamp_count(ev_n[b], E_max);
+    const double2 G = coef[item];
+    if (nb == 0 || (G.x == 0.0 && G.y == 0.0)) return;
+    const float* qa = q_t + item * (size_t)E_max;
+    const int32_t* qi = q_k + item * (size_t)E_max;
+    const int32_t* src = ev_src + (size_t)b * E_max;
+    const int ns = max(min(out_n[item], m.s_max), 0);
+    const float* st = out_t + item * (size_t)m.s_max;
+    const int32_t* sk = out_k + item * (size_t)m.s_max;
+    float* gsp = grad_spike + item * (size_t)m.s_max;
+    const float2* rb = rec + item * ((size_t)E_max + 1);
+    const double sT = scale[2], kap = m.kappa, skp = -(m.dth * m.inv_tm);
+    // P at event nb - 1: the open interval's pseudo-spike; tn: that interval
+    RecTerm tn = rec_term(rb[nb], G, 0.0, 0.0);
+    double Pm = tn.mu * tn.em, Ps = tn.mu * tn.es;
+    int s_hi = ns;                                        // spikes with out_k <= the step's last event
+    while (s_hi > 0 && sk[s_hi - 1] > nb - 1) --s_hi;
+    for (int f = ((nb - 1) / kWave) * kWave; f >= 0; f -= kWave) {
+        const int r = f + lane;
+        const bool ok = r < nb;
+        const int hi = min(f + kWave - 1, nb - 1);
+        const float af = ok ? qa[r] : 0.0f;
+        const int k = ok ? min(max(qi[r], 0), nb - 1) : 0;
+        const int j = clamp_src(src[k], C_in);
+        const double w = ok ? (double)WT[(size_t)j * N + n] : 0.0;
+        double ap = __shfl_up((double)af, 1, kWave);
+        if (lane == 0) ap = f > 0 ? (double)qa[f - 1] : 0.0;
+        const double a = (double)af;
+        double A = 1.0, D = 1.0;
+        RecTerm t{0.0, 0.0, 0.0, 0.0, 0.0};
+        if (ok) {
+            const double L = a - ap;
+            A = exp(-L * m.inv_tm);
+            D = exp(-L * m.inv_ts);
+            t = rec_term(rb[r], G, A, D);                 // interval r, closed by event r
+        }
+        // the record after event r: lane r + 1's, or the carried one at the top
+        RecTerm tx;
+        tx.mu = __shfl_down(t.mu, 1, kWave);
+        tx.vs = __shfl_down(t.vs, 1, kWave);
+        if (r == hi) {
+            tx.mu = tn.mu;
+            tx.vs = tn.vs;
+        }
+        // P at event r: the maps of lanes r + 1 .. hi applied to P at event hi
+        double am = A, bm = t.mu * t.em, as = D, bs = t.mu * t.es;
+        scan_maps_down(am, bm, lane);
+        scan_maps_down(as, bs, lane);
+        double xam = __shfl_down(am, 1, kWave), xbm = __shfl_down(bm, 1, kWave);
+        double xas = __shfl_down(as, 1, kWave), xbs = __shfl_down(bs, 1, kWave);
+        if (lane == kWave - 1) {
+            xam = 1.0;
+            xbm = 0.0;
+            xas = 1.0;
+            xbs = 0.0;
+        }
+        const double Pmr = fma(xam, Pm, xbm), Psr = fma(xas, Ps, xbs);
+        if (ok) {
+            double ga = w * kap * (Pmr * m.inv_tm - Psr * m.inv_ts);
+            ga = fma(tx.mu, tx.vs, ga);                   // 0 unless that argmax is the interval's start
+            ga = fma(t.mu, t.ve, ga);                     // 0 unless this argmax is the interval's end
+            add_wd(j, kap * (Pmr - Psr), ga);
+            if (gt) atomicAdd((unsigned long long*)&gt[(size_t)b * E_max + k], (unsigned long long)llrint(ga * sT));
+        }
+        // the spikes of intervals f .. hi: upstream gradient from P at the
+        // event that closes their interval
+        int s_lo = s_hi;
+        while (s_lo > 0 && sk[s_lo - 1] >= f) --s_lo;
+        for (int s = s_lo; s < s_hi; ++s)
+            if (sk[s] == r) gsp[s] += (float)(skp * Pmr * exp(-(a - (double)st[s]) * m.inv_tm));
+        // the carry: P at event f - 1 and the record of interval f
+        Pm = __shfl(fma(am, Pm, bm), 0, kWave);
+        Ps = __shfl(fma(as, Ps, bs), 0, kWave);
+        tn.mu = __shfl(t.mu, 0, kWave);
+        tn.vs = __shfl(t.vs, 0, kWave);
+        s_hi = s_lo;
+    }
+}
+
+// dL/dW and dL/dD to global memory (C_in > kDlyLdsMaxC).
+__global__ __launch_bounds__(kWave * kDRegWaves) void k_dregg_walk(
+    const float* __restrict__ q_t, const int32_t* __restrict__ q_k, const int32_t* __restrict__ ev_src,
+    const int32_t* __restrict__ ev_n, int B, int E_max, const float* __restrict__ WT, int C_in, int N, Model m,
+    const float* __restrict__ out_t, const int32_t* __restrict__ out_n, const int32_t* __restrict__ out_k,
+    const float2* __restrict__ rec, const double2* __restrict__ coef, const double* __restrict__ scale,
+    long long* __restrict__ gw, long long* __restrict__ gd, long long* __restrict__ gt,
+    float* __restrict__ grad_spike)
+{
+    const size_t item = (size_t)blockIdx.x * kDRegWaves + threadIdx.x / kWave;
+    if (item >= (size_t)B * N) return;
+    const int n = (int)(item % (size_t)N);
+    const double sW = scale[0], sD = scale[1];
+    auto add_wd = [&](int j, double vw, double vd) {
+        const size_t wi = (size_t)j * N + n;
+        fx_add(&gw[wi], vw, sW);
+        if (gd) fx_add(&gd[wi], vd, sD);
+    };
+    dregg_walk(item, q_t, q_k, ev_src, ev_n, E_max, WT, C_in, N, m, out_t, out_n, out_k, rec, coef, scale, add_wd,
+               gt, grad_spike);
+}
+
+// C_in <= kDlyLdsMaxC: one workgroup per (neuron, kDlyLdsWaves samples), the
+// neuron's dL/dW and dL/dD column summed in LDS as in k_dly_adjoint_lds.
+__global__ __launch_bounds__(kWave * kDlyLdsWaves) void k_dregg_walk_lds(
+    const float* __restrict__ q_t, const int32_t* __restrict__ q_k, const int32_t* __restrict__ ev_src,
+    const int32_t* __restrict__ ev_n, int B, int E_max, const float* __restrict__ WT, int C_in, int N, Model m,
+    const float* __restrict__ out_t, const int32_t* __restrict__ out_n, const int32_t* __restrict__ out_k,
+    const float2* __restrict__ rec, const double2* __restrict__ coef, const double* __restrict__ scale,
+    long long* __restrict__ gw, long long* __restrict__ gd, long long* __restrict__ gt,
+    float* __restrict__ grad_spike, int nbg)
+{
+    extern __shared__ long long s_wd[];            // [C_in] dL/dW sums, then [C_in] dL/dD sums
+    long long* s_w = s_wd;
+    long long* s_d = s_wd + C_in;
+    const int n = (int)(blockIdx.x / (unsigned)nbg), bg = (int)(blockIdx.x % (unsigned)nbg);
+    const int tid = (int)threadIdx.x;
+    for (int j = tid; j < C_in; j += (int)blockDim.x) {
+        s_w[j] = 0;
+        s_d[j] = 0;
+    }
+    __syncthreads();
+    const int b = bg * kDlyLdsWaves + tid / kWave;
+    if (b < B) {
+        const double sW = scale[0], sD = scale[1];
+        const bool want_d = gd != nullptr;
+        auto add_wd = [&](int j, double vw, double vd) {
+            atomicAdd((unsigned long long*)&s_w[j], (unsigned long long)llrint(vw * sW));
+            if (want_d) atomicAdd((unsigned long long*)&s_d[j], (unsigned long long)llrint(vd * sD));
+        };
+        dregg_walk((size_t)b * N + n, q_t, q_k, ev_src, ev_n, E_max, WT, C_in, N, m, out_t, out_n, out_k, rec, coef,
+                   scale, add_wd, gt, grad_spike);
+    }
+    __syncthreads();
+    for (int j = tid; j < C_in; j += (int)blockDim.x) {
+        const size_t wi = (size_t)j * N + n;
+        const long long vw = s_w[j], vd = s_d[j];
+        if (vw) atomicAdd((unsigned long long*)&gw[wi], (unsigned long long)vw);
+        if (gd && vd) atomicAdd((unsigned long long*)&gd[wi], (unsigned long long)vd);
+    }
+}
+
+__global__ __launch_bounds__(256) void k_dregg_zero(size_t nW, size_t nT, long long* __restrict__ gw,
+                                                   long long* __restrict__ gd, long long* __restrict__ gt,
+                                                   uint32_t* __restrict__ wmax)
+{
+    const size_t gtid = (size_t)blockIdx.x * blockDim.x + threadIdx.x, gs = (size_t)gridDim.x * blockDim.x;
+    for (size_t x = gtid; x < nW; x += gs) {
+        gw[x] = 0;
+        gd[x] = 0;
+    }
+    for (size_t x = gtid; x < nT; x += gs) gt[x] = 0;
+    if (gtid == 0) *wmax = 0u;
+}
+
 static unsigned grid_for(size_t work)
 {
     size_t blocks = (work + 255) / 256;
@@ -734,6 +1133,160 @@ extern "C" int lif_layer_backward_delayed(const float* q_t, const int32_t* q_k, 
                          dim3(kWave * kDlyWaves), 0, stream, q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N_out, m,
                          out_t, out_n, out_k, mu, scale, gw, grad_DT ? gd : nullptr, grad_ev_t ? gt : nullptr);
         }
+    }
+    TIMED_LAUNCH("dly_convert", k_dly_convert, dim3(grid_for(work)), dim3(256), 0, stream, gw, gd, gt, scale, nW, nT,
+                 grad_WT, grad_DT, grad_ev_t);
+    return check_launch();
+}
+
+// ---------------------------------------------------------------------------
+// Spike-count regularisers of a layer with synaptic delays
+// ---------------------------------------------------------------------------
+namespace lif {
+
+struct DRegLayout {
+    size_t ub, ob, counts, gates, coef, musum, vpmax, rec, wmax, scale, gw, gd, gt, total;
+};
+
+static DRegLayout dreg_layout(int B, int E_max, int C_in, int N, bool grad)
+{
+    DRegLayout L{};
+    size_t off = 0;
+    auto take = [&](size_t bytes) { size_t o = off; off += (bytes + 255) & ~(size_t)255; return o; };
+    const size_t nn = (size_t)B * N;
+    L.ub = take(nn * sizeof(double));
+    L.ob = take(nn * sizeof(double));
+    L.counts = take(nn * sizeof(double2));
+    L.gates = take((size_t)N * sizeof(double2));
+    if (grad) {
+        L.coef = take(nn * sizeof(double2));
+        L.musum = take(nn * sizeof(double));
+        L.vpmax = take(nn * sizeof(double));
+        L.rec = take(nn * ((size_t)E_max + 1) * sizeof(float2));
+        L.wmax = take(sizeof(uint32_t));
+        L.scale = take(4 * sizeof(double));
+        L.gw = take((size_t)C_in * N * sizeof(long long));
+        L.gd = take((size_t)C_in * N * sizeof(long long));
+        L.gt = take((size_t)B * E_max * sizeof(long long));
+    }
+    L.total = off + 256;
+    return L;
+}
+
+static int dreg_check(const float* q_t, const int32_t* q_k, const int32_t* ev_src, const int32_t* ev_n, int B,
+                      int E_max, const float* WT, int C_in, int N_out, const lif_params* p, const float* out_t,
+                      const int32_t* out_n, const int32_t* out_k, double c_target)
+{
+    if (!p || !WT || B < 0 || E_max < 0 || C_in < 1 || N_out < 1) return LIF_ERR_ARG;
+    int rc = check_params(p);
+    if (rc) return rc;
+    if (B > 0 && (!ev_n || !out_t || !out_n || !out_k)) return LIF_ERR_ARG;
+    if (B > 0 && E_max > 0 && (!q_t || !q_k || !ev_src)) return LIF_ERR_ARG;
+    if (!(c_target > 0.0) || !isfinite(c_target)) return LIF_ERR_ARG;
+    if ((size_t)B * (size_t)N_out >= ((size_t)1 << 31) || B > 65535) return LIF_ERR_SIZE;
+    return LIF_OK;
+}
+
+static void launch_dreg_walk(const float* q_t, const int32_t* q_k, const int32_t* ev_src, const int32_t* ev_n, int B,
+                             int E_max, const float* WT, int C_in, int N, const Model& m, const float* out_t,
+                             const int32_t* out_n, const int32_t* out_k, double* ub, double* ob, float* under,
+                             float* over, double2* counts, double* vpmax, float2* rec, hipStream_t stream)
+{
+    const size_t nn = (size_t)B * N;
+    if (nn == 0) return;
+    TIMED_LAUNCH("dreg_walk", k_dreg_walk, dim3((unsigned)((nn + kDRegWaves - 1) / kDRegWaves)),
+                 dim3(kWave * kDRegWaves), 0, stream, q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N, m, out_t, out_n,
+                 out_k, ub, ob, under, over, counts, vpmax, rec);
+}
+
+}  // namespace lif
+
+extern "C" size_t lif_spike_count_reg_delayed_workspace_size(int B, int E_max, int C_in, int N_out)
+{
+    if (B < 0 || E_max < 0 || C_in < 1 || N_out < 1) return 0;
+    return lif::dreg_layout(B, E_max, C_in, N_out, true).total;
+}
+
+extern "C" int lif_spike_count_reg_delayed(const float* q_t, const int32_t* q_k, const int32_t* ev_src,
+                                           const int32_t* ev_n, int B, int E_max, const float* WT, int C_in,
+                                           int N_out, const lif_params* p, const float* out_t, const int32_t* out_n,
+                                           const int32_t* out_k, double c_target, float* loss, float* under,
+                                           float* over, void* ws, size_t ws_bytes, lif_stream_t stream_)
+{
+    using namespace lif;
+    int rc = dreg_check(q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N_out, p, out_t, out_n, out_k, c_target);
+    if (rc) return rc;
+    const DRegLayout L = dreg_layout(B, E_max, C_in, N_out, false);
+    if (!ws || ws_bytes < L.total) return LIF_ERR_WORKSPACE;
+    hipStream_t stream = (hipStream_t)stream_;
+    const Model m = make_model(*p);
+    char* base = (char*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
+    double* ub = (double*)(base + L.ub);
+    double* ob = (double*)(base + L.ob);
+    launch_dreg_walk(q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N_out, m, out_t, out_n, out_k, ub, ob, under, over,
+                     nullptr, nullptr, nullptr, stream);
+    if (B > 0) launch_reg_loss(ub, ob, out_n, B, N_out, m.s_max, c_target, loss, nullptr, stream);
+    return check_launch();
+}
+
+extern "C" int lif_spike_count_reg_delayed_backward(const float* q_t, const int32_t* q_k, const int32_t* ev_src,
+                                                    const int32_t* ev_n, int B, int E_max, const float* WT, int C_in,
+                                                    int N_out, const lif_params* p, const float* out_t,
+                                                    const int32_t* out_n, const int32_t* out_k, double c_target,
+                                                    double lam_reg, double lam_over, float* loss, float* grad_spike,
+                                                    float* grad_WT, float* grad_DT, float* grad_ev_t, void* ws,
+                                                    size_t ws_bytes, lif_stream_t stream_)
+{
+    using namespace lif;
+    int rc = dreg_check(q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N_out, p, out_t, out_n, out_k, c_target);
+    if (rc) return rc;
+    if (!grad_WT || (B > 0 && !grad_spike) || !isfinite(lam_reg) || !isfinite(lam_over)) return LIF_ERR_ARG;
+    const DRegLayout L = dreg_layout(B, E_max, C_in, N_out, true);
+    if (!ws || ws_bytes < L.total) return LIF_ERR_WORKSPACE;
+    hipStream_t stream = (hipStream_t)stream_;
+    const Model m = make_model(*p);
+    char* base = (char*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
+    double* ub = (double*)(base + L.ub);
+    double* ob = (double*)(base + L.ob);
+    double2* counts = (double2*)(base + L.counts);
+    double2* gates = (double2*)(base + L.gates);
+    double2* coef = (double2*)(base + L.coef);
+    double* musum = (double*)(base + L.musum);
+    double* vpmax = (double*)(base + L.vpmax);
+    float2* rec = (float2*)(base + L.rec);
+    uint32_t* wmax = (uint32_t*)(base + L.wmax);
+    double* scale = (double*)(base + L.scale);
+    long long* gw = (long long*)(base + L.gw);
+    long long* gd = (long long*)(base + L.gd);
+    long long* gt = (long long*)(base + L.gt);
+    const size_t nW = (size_t)C_in * N_out, nT = (size_t)B * E_max, nn = (size_t)B * N_out;
+    const size_t work = nW > nT ? nW : nT;
+    TIMED_LAUNCH("dregg_zero", k_dregg_zero, dim3(grid_for(work)), dim3(256), 0, stream, nW, nT, gw, gd, gt, wmax);
+    TIMED_LAUNCH("dly_wmax", k_dly_wmax, dim3(grid_for(nW)), dim3(256), 0, stream, WT, nW, wmax);
+    launch_dreg_walk(q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N_out, m, out_t, out_n, out_k, ub, ob, nullptr,
+                     nullptr, counts, vpmax, rec, stream);
+    if (B > 0) {
+        launch_reg_loss(ub, ob, out_n, B, N_out, m.s_max, c_target, loss, gates, stream);
+        launch_regg_coef(counts, gates, out_n, B, N_out, m.s_max, c_target, lam_reg, lam_over, coef, musum, stream);
+        TIMED_LAUNCH("dregg_scale", k_dregg_scale, dim3(1), dim3(kDlyScaleThreads), 0, stream, musum, coef, vpmax, nn,
+                     ev_n, B, E_max, N_out, m, wmax, scale);
+        if (E_max > 0) {
+            if (C_in <= kDlyLdsMaxC) {
+                const int nbg = (B + kDlyLdsWaves - 1) / kDlyLdsWaves;
+                TIMED_LAUNCH("dregg_walk", k_dregg_walk_lds, dim3((unsigned)((size_t)N_out * nbg)),
+                             dim3(kWave * kDlyLdsWaves), (size_t)2 * C_in * sizeof(long long), stream, q_t, q_k,
+                             ev_src, ev_n, B, E_max, WT, C_in, N_out, m, out_t, out_n, out_k, rec, coef, scale, gw,
+                             grad_DT ? gd : nullptr, grad_ev_t ? gt : nullptr, grad_spike, nbg);
+            } else {
+                TIMED_LAUNCH("dregg_walk", k_dregg_walk, dim3((unsigned)((nn + kDRegWaves - 1) / kDRegWaves)),
+                             dim3(kWave * kDRegWaves), 0, stream, q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N_out, m,
+                             out_t, out_n, out_k, rec, coef, scale, gw, grad_DT ? gd : nullptr,
+                             grad_ev_t ? gt : nullptr, grad_spike);
+            }
+        }
+    } else {
+        TIMED_LAUNCH("dregg_scale", k_dregg_scale, dim3(1), dim3(kDlyScaleThreads), 0, stream, musum, coef, vpmax,
+                     (size_t)0, ev_n, 0, E_max, N_out, m, wmax, scale);
     }
     TIMED_LAUNCH("dly_convert", k_dly_convert, dim3(grid_for(work)), dim3(256), 0, stream, gw, gd, gt, scale, nW, nT,
                  grad_WT, grad_DT, grad_ev_t);

@@ -40,6 +40,7 @@
 #include "lif_common.hpp"
 #include "lif_host.hpp"
 #include "lif_walk.hpp"
+#include "lif_reg.hpp"
 #include <type_traits>
 
 namespace lif {
@@ -1669,60 +1670,6 @@ namespace lif {
 // decaying deficit (V_th - V_reset) e^{-(t - t_s)/tm} of each earlier spike.
 // ---------------------------------------------------------------------------
 
-// Largest V over [0, L] of the no-reset trajectory from (V0, I0): the start,
-// the end (L finite) and the stationary point of Eq. t_vmax when it lies
-// inside, with the decays e^{-u/tm}, e^{-u/ts} at its argmax and
-// whether that is the interval's start or end (the first of equal values
-// wins: the start, then the end, then the stationary point).
-struct RegArg {
-    double vmax, em, es;
-    bool at_start, at_end;
-};
-
-__device__ __forceinline__ RegArg reg_vmax_arg(const Model& m, double V0, double I0, double L, double A, double Dd)
-{
-    RegArg r{V0, 1.0, 1.0, true, false};
-    if (!isinf(L)) {
-        const double V1 = V0 * A + m.kappa * I0 * (A - Dd);
-        if (V1 > r.vmax) r = RegArg{V1, A, Dd, false, true};
-    }
-    // The logarithm and the decays of the stationary point in float32
-    // arithmetic (relative errors near 2^-22; the records keep the decays in
-    // float32 anyway), with e^{-u/ts} = (e^{-u/tm})^(p+1) when tau_m / tau_s
-    // = p + 1; a ratio past the float32 range takes the float64 logarithm.
-    const double a = V0 + m.kappa * I0;
-    if (I0 > 0.0 && a > 0.0) {
-        const double ratio = m.kappa * I0 * m.tm / (a * m.ts);
-        if (ratio > 1.0) {
-            const double u = (ratio < 1.0e38 ? (double)__logf((float)ratio) : log(ratio)) * m.c_tv;
-            if (u > 0.0 && u < L) {
-                const float emf = __expf((float)(-u * m.inv_tm));
-                float esf;
-                switch (m.p_int) {
-                case 1: esf = emf * emf; break;
-                case 2: esf = emf * emf * emf; break;
-                case 3: { const float e2 = emf * emf; esf = e2 * e2; } break;
-                case 4: { const float e2 = emf * emf; esf = e2 * e2 * emf; } break;
-                default: esf = __expf((float)(-u * m.inv_ts)); break;
-                }
-                const double em = (double)emf, es = (double)esf;
-                const double Vu = V0 * em + m.kappa * I0 * (em - es);
-                if (Vu > r.vmax) r = RegArg{Vu, em, es, false, false};
-            }
-        }
-    }
-    return r;
-}
-
-// Per-interval record for the regularisers' gradient, interval j of a
-// (sample, neuron) at rec[(b (E_max + 1) + j) N + n], float2 {x, y}: the sign
-// of x is the active hinge (> 0 under-firing: silent with V_max < V_th;
-// < 0 over-firing: spiked with V_max > V_th; 0 none) and |x| the argmax:
-// e^{-u/tm} in (0, 1) for a stationary point inside (then y = e^{-u/ts}),
-// kRecStart for the interval's start, kRecEnd for its end (then y = the
-// slope V' there when that point is an input time, else 0; the decays of an
-// end are the interval's own).
-constexpr float kRecStart = 2.0f, kRecEnd = 3.0f;
 
 // Per (sample, segment, 64 neurons): the segment's intervals (and the open
 // one in the sample's last segment); per lane the sums of the hinge terms
@@ -1791,18 +1738,12 @@ __global__ __launch_bounds__(kWave * kWalkWaves) void k_reg_walk(
         }
         if (rb && c.live) {
             const float sgn = spiked ? (vmax > m.th ? -1.0f : 0.0f) : (vmax < m.th ? 1.0f : 0.0f);
-            float x, y;
-            if (ra.at_start) {
-                x = kRecStart;
-                y = j > 0 ? (float)((J - V0) * m.inv_tm) : 0.0f;
-            } else if (ra.at_end && j < c.nb) {
-                x = kRecEnd;
-                y = (float)((J * Dd - ra.vmax) * m.inv_tm);
-            } else {                             // inside, or the end t_end of the open interval
-                x = (float)ra.em;
-                y = (float)ra.es;
-            }
-            rb[(size_t)j * N] = make_float2(sgn * x, sgn != 0.0f ? y : 0.0f);
+            if (ra.at_start)
+                rb[(size_t)j * N] = make_record(sgn, kRecStart, 1.0, 1.0, j > 0 ? (J - V0) * m.inv_tm : 0.0);
+            else if (ra.at_end && j < c.nb)
+                rb[(size_t)j * N] = make_record(sgn, kRecEnd, A, Dd, (J * Dd - ra.vmax) * m.inv_tm);
+            else                                 // inside, or the end t_end of the open interval
+                rb[(size_t)j * N] = make_record(sgn, kRecInside, ra.em, ra.es, 0.0);
             if (sgn > 0.0f) {
                 loc.x = fma(cdm, ra.em, loc.x);
                 loc.y = fma(cds, ra.es, loc.y);
@@ -1929,6 +1870,13 @@ __global__ __launch_bounds__(kRegThreads) void k_reg_loss(const double* __restri
     }
 }
 
+void launch_reg_loss(const double* ub, const double* ob, const int32_t* out_n, int B, int N, int s_max,
+                     double c_target, float* loss, double2* gates, hipStream_t stream)
+{
+    TIMED_LAUNCH("reg_loss", k_reg_loss, dim3(1), dim3(kRegThreads), 0, stream, ub, ob, out_n, B, N, s_max, c_target,
+                 loss, gates);
+}
+
 struct RegLayout {
     FwdLayout f;
     size_t part, ub, ob, status, total;
@@ -2039,28 +1987,6 @@ extern "C" int lif_spike_count_reg(const float* ev_t, const int32_t* ev_src, con
 // ---------------------------------------------------------------------------
 namespace lif {
 
-// A record decoded with the interval's own decays (A, D): the multiplier mu
-// of its pseudo-spike (dL/dV_max; 0 for an inactive record, whose fields are
-// all 0), the decays at its argmax, and its end-point slope terms: vs when
-// the argmax is the start (the input event before the interval), ve when it
-// is the end (the event that closes it), 0 otherwise.  Selects only, so
-// that the walk over a group has no branches.
-struct RecTerm {
-    double mu, em, es, vs, ve;
-};
-
-__device__ __forceinline__ RecTerm rec_term(const float2& r, const double2& G, double A, double D)
-{
-    const float a = fabsf(r.x);
-    const bool st = a == kRecStart, en = a == kRecEnd;
-    RecTerm t;
-    t.mu = r.x > 0.0f ? G.x : (r.x < 0.0f ? G.y : 0.0);
-    t.em = st ? 1.0 : (en ? A : (double)a);
-    t.es = st ? 1.0 : (en ? D : (double)r.y);
-    t.vs = st ? (double)r.y : 0.0;
-    t.ve = en ? (double)r.y : 0.0;
-    return t;
-}
 
 // Per (sample, neuron): G_u = -lam_reg gu / (N B nsil), G_o = (lam_reg go /
 // (N B) + lam_over gi / N) / nspk with gi = ReLU(c / c_target - 1) of its
@@ -2085,6 +2011,17 @@ __global__ __launch_bounds__(256) void k_regg_coef(const double2* __restrict__ c
         coef[i] = make_double2(Gu, Go);
         musum[i] = fabs(Gu) * cnt.x + fabs(Go) * cnt.y;
     }
+}
+
+void launch_regg_coef(const double2* counts, const double2* gates, const int32_t* out_n, int B, int N, int s_max,
+                      double c_target, double lam_reg, double lam_over, double2* coef, double* musum,
+                      hipStream_t stream)
+{
+    const size_t nn = (size_t)B * N;
+    size_t blocks = (nn + 255) / 256;
+    blocks = blocks < 1 ? 1 : (blocks > 2048 ? 2048 : blocks);
+    TIMED_LAUNCH("regg_coef", k_regg_coef, dim3((unsigned)blocks), dim3(256), 0, stream, counts, gates, out_n, B, N,
+                 s_max, c_target, lam_reg, lam_over, coef, musum, (long long*)nullptr, (size_t)0);
 }
 
 // Fixed-point scale of dL/dW (one workgroup): a contribution is at most

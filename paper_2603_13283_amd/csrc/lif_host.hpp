@@ -43,6 +43,17 @@ int launch_chunked_walk(const float* ev_t, const int32_t* ev_src, const int32_t*
                         int32_t* out_n, float* out_i, int32_t* out_k, int32_t* consumed, int32_t* processed,
                         int32_t* status, hipStream_t stream);
 
+// The regularisers' batch terms (lif_forward.hip), shared by the plain and
+// the delayed layer: from the per-(sample, neuron) hinge means ub, ob the
+// two loss terms (loss nullable) and the per-neuron gates; from the interval
+// counts and the gates the per-(sample, neuron) multipliers coef = (G_u, G_o)
+// of the active intervals and their bound musum = |G_u| nsil + |G_o| nspk.
+void launch_reg_loss(const double* ub, const double* ob, const int32_t* out_n, int B, int N, int s_max,
+                     double c_target, float* loss, double2* gates, hipStream_t stream);
+void launch_regg_coef(const double2* counts, const double2* gates, const int32_t* out_n, int B, int N, int s_max,
+                      double c_target, double lam_reg, double lam_over, double2* coef, double* musum,
+                      hipStream_t stream);
+
 // Kernel timer (lif_timer_*): a HIP event pair per launch, recorded by the
 // dispatch of the kernel itself (hipExtLaunchKernelGGL), so that the elapsed
 // time is the kernel's own execution.

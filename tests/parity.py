@@ -157,3 +157,37 @@ def compare_grad_e2e(g_gpu, g_or, g_or32, label=""):
         w = float((np.abs(g_gpu - g_or32) / den32)[ill].max())
         assert w <= GRAD_RTOL, f"{label}: element-wise relative error {w:.3e} against the float32 hand-over"
     return rel, float(ill.mean())
+
+
+def compare_grad_band(g_gpu, g_or, g_or64, label=""):
+    """Regulariser gradient check on a spike train handed over in float32:
+    norm-wise and element-wise (floored) against g_or, the oracle at those
+    float32 spike times, except where the rounding of the hand-over itself
+    moves the oracle's gradient (g_or64: at its exact spike times) by more
+    than COND_RTOL; there the element must lie within GRAD_RTOL of the band
+    between g_or and g_or64.  The GPU takes the reset of a spike at a float32
+    time as the decaying deficit of a threshold crossing there, the oracle as
+    V set to V_reset there; the two agree to that rounding, to which such an
+    element is sensitive.  Returns (norm-wise error, ill-conditioned
+    fraction)."""
+    g_gpu = np.asarray(g_gpu, dtype=np.float64)
+    g_or = np.asarray(g_or, dtype=np.float64)
+    g_or64 = np.asarray(g_or64, dtype=np.float64)
+    nrm = np.linalg.norm(g_or)
+    if nrm == 0:
+        assert np.all(g_gpu == 0), f"{label}: oracle gradient is zero, GPU's is not"
+        return 0.0, 0.0
+    rel = float(np.linalg.norm(g_gpu - g_or) / nrm)
+    assert rel <= GRAD_RTOL, f"{label}: norm-wise relative error {rel:.3e}"
+    den = np.maximum(np.abs(g_or), 1e-3 * np.abs(g_or).max())
+    ill = np.abs(g_or64 - g_or) / den > COND_RTOL
+    e = np.abs(g_gpu - g_or) / den
+    if (~ill).any():
+        w = float(e[~ill].max())
+        assert w <= GRAD_RTOL, f"{label}: element-wise relative error {w:.3e} (well-conditioned entries)"
+    if ill.any():
+        lo, hi = np.minimum(g_or, g_or64), np.maximum(g_or, g_or64)
+        out = np.maximum(lo - g_gpu, 0.0) + np.maximum(g_gpu - hi, 0.0)
+        w = float((out / den)[ill].max())
+        assert w <= GRAD_RTOL, f"{label}: element-wise relative error {w:.3e} outside the hand-over band"
+    return rel, float(ill.mean())

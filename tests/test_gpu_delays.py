@@ -166,3 +166,111 @@ def test_delays_config2_shape(env):
     paper's delay initialisation U[0, 0.1] s and a gain that makes it fire."""
     cfg = W.config2(gain=6.0)
     run_case(env, cfg.events, cfg.layers[0].WT, W.uniform_delays(2, 700, 256), "config-2 shape, gain 6")
+
+
+@pytest.mark.parametrize("t_end,vr", [(math.inf, 0.0), (0.5, -0.3)])
+def test_delayed_regularisers(env, t_end, vr):
+    """Spike-count regularisers of a layer with delays (each neuron's
+    intervals between its own arrivals): the hinge means and loss values,
+    then the upstream spike-time gradient and the direct weight, delay and
+    input-time parts against the oracle on identical inputs (the oracle's
+    spike trains in float32), the full gradients through the delayed
+    backward, and bitwise reproducibility."""
+    from oracle import loss as OL
+    from tests.parity import compare_grad_band
+    torch, lif = env
+    cfg = W.random_small(54, B=4, C=40, N=70, n_events=600, T=0.4, gain=7.0)
+    ev, WT = cfg.events, cfg.layers[0].WT
+    ev.ev_n[2] = 0
+    DT = W.uniform_delays(54, 40, 70, d_max=0.05)
+    P = oracle.LifParams(s_max=64, t_end=t_end, v_reset=vr)
+    r = oracle.forward_delayed(ev.ev_t, ev.ev_src, ev.ev_n, WT, DT, P)
+    assert r.out_n.sum() > 100 and not r.capped.any()
+    c_target = float(np.median(r.out_n.mean(axis=0))) + 0.5
+    rp = OL.RegParams(c_target=c_target, lam_reg=0.8, lam_over=0.3)
+    r32 = r.rounded()
+    q_t, q_k = oracle.delay_queues(ev.ev_t, ev.ev_src, ev.ev_n, DT)
+    print(f"[case] delayed regularisers t_end={t_end} v_reset={vr} spikes={int(r.out_n.sum())} "
+          f"c_target={c_target}", flush=True)
+    tables = OL.delayed_interval_tables(ev.ev_src, ev.ev_n, WT, q_t, q_k, r32.out_t, r.out_k, r.out_n, P.tau_mem,
+                                        P.tau_syn, P.v_th, P.v_reset, P.t_end)
+    under = np.array([[np.mean([max(P.v_th - x[4], 0.0) for x in t if not x[6]] or [0.0]) for t in row]
+                      for row in tables])
+    over = np.array([[np.mean([max(x[4] - P.v_th, 0.0) for x in t if x[6]] or [0.0]) for t in row]
+                     for row in tables])
+    L_reg, L_over, gWd, gDd, gTd, gS = OL.spike_count_reg_delayed_grad(
+        ev.ev_t, ev.ev_src, ev.ev_n, WT, q_t, q_k, r32.out_t, r.out_k, r.out_n, P.tau_mem, P.tau_syn, P.v_th,
+        P.v_reset, P.t_end, rp)
+    gWs, gDs, gTs = oracle.backward_delayed(ev.ev_t, ev.ev_src, ev.ev_n, WT, DT, r32, gS, P)
+    # the oracle at its exact spike times (the band of the float32 hand-over)
+    _, _, hWd, hDd, hTd, hS = OL.spike_count_reg_delayed_grad(
+        ev.ev_t, ev.ev_src, ev.ev_n, WT, q_t, q_k, r.out_t, r.out_k, r.out_n, P.tau_mem, P.tau_syn, P.v_th,
+        P.v_reset, P.t_end, rp)
+    hWs, hDs, hTs = oracle.backward_delayed(ev.ev_t, ev.ev_src, ev.ev_n, WT, DT, r, hS, P)
+    t, s, n, w, d = (_dev(torch, a) for a in (ev.ev_t, ev.ev_src, ev.ev_n, WT, DT))
+    q = lif.delay_queues(t, s, n, d)
+    fwd = lif.ForwardOut(_dev(torch, r32.out_t.astype(np.float32)), _dev(torch, r.out_n),
+                         _dev(torch, r32.out_i.astype(np.float32)), None, _dev(torch, r.out_k))
+    lp = lif.Params(s_max=64, t_end=t_end, v_reset=vr)
+    loss, gu, go = lif.spike_count_reg_delayed(q, s, n, w, fwd, c_target, lp)
+    torch.cuda.synchronize()
+    for got, ref, label in ((gu.cpu().numpy(), under, "under"), (go.cpu().numpy(), over, "over")):
+        err = np.abs(got - ref) - 1e-5 * np.abs(ref)
+        assert (err <= 1e-7 * max(np.abs(ref).max(), 1e-30)).all(), label
+    assert (gu.cpu().numpy()[2] == P.v_th).all()            # the empty sample: V = 0 throughout
+    assert abs(loss[0].item() - L_reg) <= 1e-5 * abs(L_reg)
+    assert abs(loss[1].item() - L_over) <= 1e-5 * max(abs(L_over), 1e-12)
+    seed = torch.full((ev.B, WT.shape[1], 64), 0.25, device="cuda:0") * fwd.out_t.isfinite()
+    loss2, gsp, gW, gD, gT = lif.spike_count_reg_delayed_backward(q, s, n, w, fwd, c_target, 0.8, 0.3, lp,
+                                                                  grad_spike=seed.clone())
+    torch.cuda.synchronize()
+    assert torch.equal(loss.view(torch.int32), loss2.view(torch.int32))
+    g_spike = (gsp - seed).cpu().numpy()
+    assert np.abs(gS).max() > 0 and np.abs(gWd).max() > 0 and np.abs(gDd).max() > 0
+    res = [compare_grad_band(g_spike, gS, hS, label="delayed regulariser spike-time gradient"),
+           compare_grad_band(gW.cpu().numpy(), gWd, hWd, label="delayed regulariser direct grad_W"),
+           compare_grad_band(gD.cpu().numpy(), gDd, hDd, label="delayed regulariser direct grad_D"),
+           compare_grad_band(gT.cpu().numpy(), gTd, hTd, label="delayed regulariser direct grad_t")]
+    bW, bD, bT = lif.backward_delayed(q, s, n, w, fwd, gsp - seed, lp)
+    torch.cuda.synchronize()
+    res += [compare_grad_band((gW + bW).cpu().numpy(), gWd + gWs, hWd + hWs, label="delayed regulariser grad_W"),
+            compare_grad_band((gD + bD).cpu().numpy(), gDd + gDs, hDd + hDs, label="delayed regulariser grad_D"),
+            compare_grad_band((gT + bT).cpu().numpy(), gTd + gTs, hTd + hTs, label="delayed regulariser grad_t")]
+    print("    norm-wise errors (ill-conditioned fractions): spike, direct W D t, full W D t: " +
+          ", ".join(f"{e:.1e} ({f:.3f})" for e, f in res), flush=True)
+    loss3, gsp3, gW3, gD3, gT3 = lif.spike_count_reg_delayed_backward(q, s, n, w, fwd, c_target, 0.8, 0.3, lp,
+                                                                      grad_spike=seed.clone())
+    for a, b_ in ((gsp, gsp3), (gW, gW3), (gD, gD3), (gT, gT3)):
+        assert torch.equal(a.view(torch.int32), b_.view(torch.int32)), "not reproducible"
+
+
+def test_delayed_regularisers_wide_input(env):
+    """C_in > 4096: the regulariser gradient's dL/dW and dL/dD go straight to
+    global memory; direct parts against the oracle."""
+    from oracle import loss as OL
+    from tests.parity import compare_grad
+    torch, lif = env
+    cfg = W.random_small(88, B=3, C=4500, N=12, n_events=900, T=0.5, gain=60.0)
+    ev, WT = cfg.events, cfg.layers[0].WT
+    DT = W.uniform_delays(88, 4500, 12)
+    P = oracle.LifParams()
+    r = oracle.forward_delayed(ev.ev_t, ev.ev_src, ev.ev_n, WT, DT, P)
+    assert r.out_n.sum() > 20
+    r32 = r.rounded()
+    rp = OL.RegParams(c_target=2.0, lam_reg=0.8, lam_over=0.3)
+    q_t, q_k = oracle.delay_queues(ev.ev_t, ev.ev_src, ev.ev_n, DT)
+    L_reg, L_over, gWd, gDd, gTd, gS = OL.spike_count_reg_delayed_grad(
+        ev.ev_t, ev.ev_src, ev.ev_n, WT, q_t, q_k, r32.out_t, r.out_k, r.out_n, P.tau_mem, P.tau_syn, P.v_th,
+        P.v_reset, P.t_end, rp)
+    print(f"[case] delayed regularisers C_in=4500 spikes={int(r.out_n.sum())}", flush=True)
+    t, s, n, w, d = (_dev(torch, a) for a in (ev.ev_t, ev.ev_src, ev.ev_n, WT, DT))
+    q = lif.delay_queues(t, s, n, d)
+    fwd = lif.ForwardOut(_dev(torch, r32.out_t.astype(np.float32)), _dev(torch, r.out_n),
+                         _dev(torch, r32.out_i.astype(np.float32)), None, _dev(torch, r.out_k))
+    loss, gsp, gW, gD, gT = lif.spike_count_reg_delayed_backward(q, s, n, w, fwd, 2.0, 0.8, 0.3, lif.Params())
+    torch.cuda.synchronize()
+    assert abs(loss[0].item() - L_reg) <= 1e-5 * abs(L_reg)
+    compare_grad(gsp.cpu().numpy(), gS, label="wide spike-time gradient")
+    compare_grad(gW.cpu().numpy(), gWd, label="wide direct grad_W")
+    compare_grad(gD.cpu().numpy(), gDd, label="wide direct grad_D")
+    compare_grad(gT.cpu().numpy(), gTd, label="wide direct grad_t")
