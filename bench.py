@@ -182,7 +182,7 @@ def train_step(torch, lif, d, c3, steps, warmup, variant="plain"):
     spike-count regularisers to both hidden layers (targets 14, lambda_reg
     1e-3, lambda_over 5e-5, as the paper's SHD model), "delays" learnable
     delays on both hidden layers (initial delays U[0, 0.1) s, softplus
-    sharpness 5)."""
+    sharpness 5), "reg_delays" both."""
     from paper_2603_13283_amd.train import AdamParams, DelayConfig, RegConfig, TwoLayerNet
     ev = c3.events
     rng = np.random.default_rng(11)
@@ -190,16 +190,17 @@ def train_step(torch, lif, d, c3, steps, warmup, variant="plain"):
     labels = d(rng.integers(0, 20, ev.B).astype(np.int32))
     inp = [d(ev.ev_t), d(ev.ev_src), d(ev.ev_n)]
     extra = {"plain": "", "reg": " + spike-count regularisers on both hidden layers",
-             "delays": " + learnable delays on both hidden layers"}[variant]
+             "delays": " + learnable delays on both hidden layers",
+             "reg_delays": " + learnable delays and spike-count regularisers on both hidden layers"}[variant]
     out = {"workload": "700->512->512 LIF + 512->20 weighted LI readout, B=128, ~10k events; forward, "
                        "cross-entropy, backward through both merges, Adam on all parameters" + extra}
     beta = 5.0
     raw = lambda shape: d((np.log(np.expm1(beta * rng.uniform(1e-3, 0.1, shape))) / beta).astype(np.float32))
     for name, seq in (("parallel", False), ("sequential", True)):
         kw = {}
-        if variant == "reg":
+        if variant in ("reg", "reg_delays"):
             kw["reg"] = RegConfig(c_target=(14.0, 14.0), lam_reg=1e-3, lam_over=5e-5)
-        elif variant == "delays":
+        if variant in ("delays", "reg_delays"):
             kw["delays"] = DelayConfig(raw((700, 512)), raw((512, 512)), beta=beta, adam=AdamParams(lr=1e-3))
         net = TwoLayerNet(d(c3.layers[0].WT), d(c3.layers[1].WT), d(Wo), B=ev.B, E_max=ev.E_max,
                           P1=lif.Params(s_max=128), P2=lif.Params(s_max=128),
@@ -430,6 +431,7 @@ def main():
         extras["train_step_c3"] = train_step(torch, lif, d, c3, st, wu)
         extras["train_step_c3_reg"] = train_step(torch, lif, d, c3, st, wu, "reg")
         extras["train_step_c3_delays"] = train_step(torch, lif, d, c3, st, wu, "delays")
+        extras["train_step_c3_reg_delays"] = train_step(torch, lif, d, c3, st, wu, "reg_delays")
         extras["chunk_mode_c2"] = chunk_study(torch, lif, d, ev, WT, st, wu, seq_ms)
         extras["delays_c2"] = delay_study(torch, lif, d, ev, WT, st, wu, 1)
         del c3, c4, c5, W1d

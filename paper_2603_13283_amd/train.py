@@ -4,8 +4,9 @@ integrator readout with temperature cross-entropy (Sec. 3.3, App. C), the
 backward pass chained through both merges (App. D.3), and an Adam update of
 the weight matrices.  Options the paper's models use (App. E.5
 hyperparameter table): spike-count regularisers on both hidden layers (App.
-E.1, Eq. loss), or learnable synaptic delays on both hidden layers (Sec.
-3.1 Eq. spike_input, softplus activation, their own Adam learning rate).
+E.1, Eq. loss) and learnable synaptic delays on both hidden layers (Sec.
+3.1 Eq. spike_input, softplus activation, their own Adam learning rate),
+each alone or both together.
 Every step is a call of liblif.so; this module only holds the device buffers
 and orders the calls on one stream."""
 from __future__ import annotations
@@ -15,8 +16,10 @@ from typing import Optional, Sequence
 
 from . import (LiParams, Params, adam_step, add_, backward, backward_delayed, delay_queues, forward,
                forward_delayed, li_readout, merge, merge_grad, softplus, softplus_grad, spike_count_reg_backward,
-               lif_layer_forward_workspace_size, lif_layer_backward_workspace_size, lif_li_readout_workspace_size,
-               lif_spike_count_reg_backward_workspace_size, LIF_MERGE_MAX, _torch)
+               spike_count_reg_delayed_backward, lif_layer_forward_workspace_size,
+               lif_layer_backward_workspace_size, lif_li_readout_workspace_size,
+               lif_spike_count_reg_backward_workspace_size, lif_spike_count_reg_delayed_workspace_size,
+               LIF_MERGE_MAX, _torch)
 
 
 @dataclass
@@ -71,8 +74,6 @@ class TwoLayerNet:
                  q: LiParams = LiParams(), adam: AdamParams = AdamParams(), E2_max: int = LIF_MERGE_MAX,
                  E3_max: int = LIF_MERGE_MAX, reg: Optional[RegConfig] = None, delays: Optional[DelayConfig] = None):
         torch = _torch()
-        if reg is not None and delays is not None:
-            raise ValueError("the regularisers of a layer with delays are not built: use one or the other")
         self.W = [W1, W2, Wo]
         self.m1 = [torch.zeros_like(w) for w in self.W]
         self.m2 = [torch.zeros_like(w) for w in self.W]
@@ -93,8 +94,10 @@ class TwoLayerNet:
         self.ws_b2 = u8(lif_layer_backward_workspace_size(B, E2_max, N1, N2, P2.c()))
         self.ws_ro = u8(lif_li_readout_workspace_size(B, E3_max, N2, K))
         if reg is not None:
-            self.ws_r1 = u8(lif_spike_count_reg_backward_workspace_size(B, E_max, C, N1))
-            self.ws_r2 = u8(lif_spike_count_reg_backward_workspace_size(B, E2_max, N1, N2))
+            size = lif_spike_count_reg_delayed_workspace_size if delays is not None else \
+                lif_spike_count_reg_backward_workspace_size
+            self.ws_r1 = u8(size(B, E_max, C, N1))
+            self.ws_r2 = u8(size(B, E2_max, N1, N2))
 
     def _layer(self, l, ev_t, ev_src, ev_n, W, P, sequential, stream, ws):
         """Forward of hidden layer l (0 or 1); with delays also its queues."""
@@ -115,13 +118,24 @@ class TwoLayerNet:
         if self.reg is not None:
             n_all = self.W[0].shape[1] + self.W[1].shape[1]
             share = W.shape[1] / n_all
-            reg_loss, g, gWd, gTd = spike_count_reg_backward(
-                ev_t, ev_src, ev_n, W, out, self.reg.c_target[l], self.reg.lam_reg * share,
-                self.reg.lam_over * share, P, grad_spike=g, want_time_grad=want_time_grad, stream=stream, ws=ws_reg)
+            c, lr, lo = self.reg.c_target[l], self.reg.lam_reg * share, self.reg.lam_over * share
+            if self.delays is not None:
+                reg_loss, g, gWd, gDd, gTd = spike_count_reg_delayed_backward(
+                    out.queues, ev_src, ev_n, W, out, c, lr, lo, P, grad_spike=g, want_time_grad=want_time_grad,
+                    stream=stream, ws=ws_reg)
+            else:
+                reg_loss, g, gWd, gTd = spike_count_reg_backward(
+                    ev_t, ev_src, ev_n, W, out, c, lr, lo, P, grad_spike=g, want_time_grad=want_time_grad,
+                    stream=stream, ws=ws_reg)
         if self.delays is not None:
             qs, X = out.queues, (self.delays.X1, self.delays.X2)[l]
             gW, gD, gT = backward_delayed(qs, ev_src, ev_n, W, out, g, P, stream=stream, want_time_grad=want_time_grad)
-            return gW, gT, softplus_grad(X, gD, self.delays.beta, stream=stream), None
+            if self.reg is not None:
+                add_(gW, gWd, stream=stream)
+                add_(gD, gDd, stream=stream)
+                if want_time_grad:
+                    add_(gT, gTd, stream=stream)
+            return gW, gT, softplus_grad(X, gD, self.delays.beta, stream=stream), reg_loss
         gW, gT = backward(ev_t, ev_src, ev_n, W, out, g, P, stream=stream, want_time_grad=want_time_grad, ws=ws)
         if self.reg is not None:
             add_(gW, gWd, stream=stream)

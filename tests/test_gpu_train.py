@@ -11,7 +11,7 @@ import pytest
 import oracle
 import workloads as W
 from oracle import loss as OL
-from tests.parity import compare_grad, compare_spikes
+from tests.parity import compare_grad, compare_grad_band, compare_spikes
 
 pytestmark = pytest.mark.gpu
 
@@ -263,3 +263,87 @@ def test_training_step_with_delays(env):
     for x0, x1, k in zip(before, dX, ("X1", "X2")):
         g = res.grads[k].cpu().numpy().astype(np.float64)
         assert np.allclose(x1.cpu().numpy(), _adam(x0, g, 1, 1e-3, 0.9, 0.999, 1e-8), rtol=1e-6, atol=1e-7), k
+
+
+def test_training_step_with_regularisers_and_delays(env):
+    """Both options together: learnable delays on both hidden layers and the
+    spike-count regularisers of those delayed layers (each neuron's intervals
+    between its own arrivals); the regulariser's delay terms join the
+    layer's delay gradient before the softplus."""
+    torch, lif = env
+    from paper_2603_13283_amd.train import AdamParams, DelayConfig, RegConfig, TwoLayerNet
+    ev, W1, W2, Wo, labels, rng = _net_case(23, gain2=4.8)
+    B = ev.B
+    beta = 5.0
+    d1 = rng.uniform(0.005, 0.05, W1.shape)
+    d2 = rng.uniform(0.005, 0.05, W2.shape)
+    X1 = (np.log(np.expm1(beta * d1)) / beta).astype(np.float32)
+    X2 = (np.log(np.expm1(beta * d2)) / beta).astype(np.float32)
+    D1, D2 = _softplus(X1, beta), _softplus(X2, beta)
+    OP = oracle.LifParams(s_max=64)
+    q = OL.LiParams(tau_li=0.5, tau_max=0.7, beta=0.2)
+    E2, E3 = 4096, 4096
+    r1 = oracle.forward_delayed(ev.ev_t, ev.ev_src, ev.ev_n, W1, D1, OP)
+    q2 = oracle.merge(r1.out_t.astype(np.float32), r1.out_n, E2)
+    r2 = oracle.forward_delayed(q2[0], q2[1], q2[2], W2, D2, OP)
+    q3 = oracle.merge(r2.out_t.astype(np.float32), r2.out_n, E3)
+    assert r1.out_n.sum() > 50 and r2.out_n.sum() > 50 and not r1.capped.any() and not r2.capped.any()
+    c1 = float(np.median(r1.out_n.mean(axis=0))) + 0.5
+    c2 = float(np.median(r2.out_n.mean(axis=0))) + 0.5
+    lam_reg, lam_over = 0.05, 0.02
+    n_all = W1.shape[1] + W2.shape[1]
+    print(f"[case] train step with delays and regularisers B={B} c_target=({c1}, {c2})", flush=True)
+    z = OL.li_readout(q3[0], q3[1], q3[2], Wo, q)
+    loss, dz = OL.ce_with_temperature(z, labels, q.beta)
+    gWo, gT3 = OL.li_readout_grad(q3[0], q3[1], q3[2], Wo, q, dz)
+    qt2, qk2 = oracle.delay_queues(q2[0], q2[1], q2[2], D2)
+    qt1, qk1 = oracle.delay_queues(ev.ev_t, ev.ev_src, ev.ev_n, D1)
+    rp2 = OL.RegParams(c_target=c2, lam_reg=lam_reg * W2.shape[1] / n_all, lam_over=lam_over * W2.shape[1] / n_all)
+    rp1 = OL.RegParams(c_target=c1, lam_reg=lam_reg * W1.shape[1] / n_all, lam_over=lam_over * W1.shape[1] / n_all)
+    sig = lambda x: 1.0 / (1.0 + np.exp(-beta * x.astype(np.float64)))
+
+    def chain(s1, s2):
+        """The oracle's backward chain from the hidden spike trains s1, s2
+        (float32-rounded, as handed to the GPU, or exact)."""
+        g2 = _scatter(gT3.astype(np.float32), q3[3], q3[2], r2.out_t.shape)
+        _, _, gW2d, gD2d, gT2d, gS2 = OL.spike_count_reg_delayed_grad(
+            q2[0], q2[1], q2[2], W2, qt2, qk2, s2.out_t, r2.out_k, r2.out_n, OP.tau_mem, OP.tau_syn, OP.v_th,
+            OP.v_reset, OP.t_end, rp2)
+        g2 = (g2 + gS2).astype(np.float32).astype(np.float64)
+        gW2, gD2, gT2 = oracle.backward_delayed(q2[0], q2[1], q2[2], W2, D2, s2, g2, OP)
+        gW2, gD2, gT2 = gW2 + gW2d, gD2 + gD2d, gT2 + gT2d
+        g1 = _scatter(gT2.astype(np.float32), q2[3], q2[2], r1.out_t.shape)
+        _, _, gW1d, gD1d, _, gS1 = OL.spike_count_reg_delayed_grad(
+            ev.ev_t, ev.ev_src, ev.ev_n, W1, qt1, qk1, s1.out_t, r1.out_k, r1.out_n, OP.tau_mem, OP.tau_syn,
+            OP.v_th, OP.v_reset, OP.t_end, rp1)
+        g1 = (g1 + gS1).astype(np.float32).astype(np.float64)
+        gW1, gD1, _ = oracle.backward_delayed(ev.ev_t, ev.ev_src, ev.ev_n, W1, D1, s1, g1, OP)
+        return {"W2": gW2, "W1": gW1 + gW1d, "X2": gD2 * sig(X2), "X1": (gD1 + gD1d) * sig(X1), "D1d": gD1d,
+                "D1": gD1 + gD1d}
+
+    ref32, ref64 = chain(r1.rounded(), r2.rounded()), chain(r1, r2)
+    # the GPU step
+    dW = [_dev(torch, w) for w in (W1, W2, Wo)]
+    dX = [_dev(torch, x) for x in (X1, X2)]
+    lq = lif.LiParams(q.tau_mem, q.tau_syn, q.tau_li, q.tau_max, q.beta)
+    net = TwoLayerNet(*dW, B=B, E_max=ev.E_max, P1=lif.Params(s_max=64), P2=lif.Params(s_max=64), q=lq,
+                      adam=AdamParams(lr=1e-3), E2_max=E2, E3_max=E3,
+                      reg=RegConfig(c_target=(c1, c2), lam_reg=lam_reg, lam_over=lam_over),
+                      delays=DelayConfig(dX[0], dX[1], beta=beta, adam=AdamParams(lr=1e-3)))
+    inp = [_dev(torch, a) for a in (ev.ev_t, ev.ev_src, ev.ev_n)]
+    res = net.step(*inp, _dev(torch, labels), update=False)
+    torch.cuda.synchronize()
+    s1 = compare_spikes(res.fwd1.out_t.cpu().numpy(), res.fwd1.out_n.cpu().numpy(), r1, res.fwd1.out_i.cpu().numpy(),
+                        label="reg+delays l1", out_k_gpu=res.fwd1.out_k.cpu().numpy())
+    s2 = compare_spikes(res.fwd2.out_t.cpu().numpy(), res.fwd2.out_n.cpu().numpy(), r2, res.fwd2.out_i.cpu().numpy(),
+                        label="reg+delays l2", out_k_gpu=res.fwd2.out_k.cpu().numpy())
+    assert s1["flagged"] == 0 and s2["flagged"] == 0
+    assert abs(res.loss.item() - loss) <= 1e-5 * abs(loss)
+    assert len(res.reg_losses) == 2
+    compare_grad(res.grads["Wo"].cpu().numpy(), gWo, label="train+reg+delays grad Wo")
+    for k in ("W2", "W1", "X2", "X1"):
+        rel, ill = compare_grad_band(res.grads[k].cpu().numpy(), ref32[k], ref64[k],
+                                     label=f"train+reg+delays grad {k}")
+        print(f"    grad {k} rel {rel:.2e} (hand-over sensitive {ill:.3f})", flush=True)
+    # the regulariser terms changed the delay gradients
+    assert np.linalg.norm(ref32["D1d"]) > 1e-3 * np.linalg.norm(ref32["D1"])
