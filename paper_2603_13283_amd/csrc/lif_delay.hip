@@ -648,7 +648,9 @@ __global__ __launch_bounds__(kWave * kDRegWaves) void k_dreg_walk(
     double2* __restrict__ counts, double* __restrict__ vpmax, float2* __restrict__ rec)
 {
     const int lane = (int)threadIdx.x % kWave;
-    const size_t item = (size_t)blockIdx.x * kDRegWaves + threadIdx.x / kWave;
+    // wave-uniform (scalar registers): the neuron's spike list is read with
+    // scalar loads, which do not wait behind the queue loads in flight
+    const size_t item = (size_t)__builtin_amdgcn_readfirstlane((int)(blockIdx.x * kDRegWaves + threadIdx.x / kWave));
     if (item >= (size_t)B * N) return;
     const int b = (int)(item / (size_t)N), n = (int)(item % (size_t)N);
     const int nb = clamp_count(ev_n[b], E_max);
@@ -689,13 +691,43 @@ __global__ __launch_bounds__(kWave * kDRegWaves) void k_dreg_walk(
     double Dc = 0.0;               // reset deficit there, of the spikes with out_k < f
     double a_prev = 0.0;           // arrival of event f - 1 (0 before the first)
     int sp = 0;                    // first spike with out_k >= f
+    // The queue's loads run ahead of the walk: at step f the weights of step
+    // f + 64 (their sources loaded a step earlier), the sources of step
+    // f + 128 and the arrivals and event indices of step f + 192 are issued
+    // before the step's work.
+    auto ld_q = [&](int ff, float& a_, int& k_) {
+        const int rr = ff + lane;
+        const bool o = rr < nb;
+        a_ = o ? qa[rr] : 0.0f;
+        k_ = o ? min(max(qi[rr], 0), nb - 1) : 0;
+    };
+    auto ld_j = [&](int k_) { return clamp_src(src[k_], C_in); };
+    auto ld_w = [&](int ff, int j_) { return ff + lane < nb ? WT[(size_t)j_ * (size_t)N + n] : 0.0f; };
+    float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, w0 = 0.0f;
+    int k0 = 0, k1 = 0, k2 = 0, j1 = 0;
+    if (nb > 0) {
+        ld_q(0, a0, k0);
+        w0 = ld_w(0, ld_j(k0));
+        ld_q(kWave, a1, k1);
+        j1 = ld_j(k1);
+        ld_q(2 * kWave, a2, k2);
+    }
     for (int f = 0; f < nb; f += kWave) {
         const int r = f + lane;
         const bool ok = r < nb;
         const int lv = min(kWave - 1, nb - 1 - f);          // the step's last event (lane)
-        const float af = ok ? qa[r] : 0.0f;
-        const int k = ok ? min(max(qi[r], 0), nb - 1) : 0;
-        const float w = ok ? WT[(size_t)clamp_src(src[k], C_in) * (size_t)N + n] : 0.0f;
+        const float w1 = ld_w(f + kWave, j1);
+        const int j2 = ld_j(k2);
+        float a3;
+        int k3;
+        ld_q(f + 3 * kWave, a3, k3);
+        const float af = a0, w = w0;
+        a0 = a1;
+        w0 = w1;
+        a1 = a2;
+        j1 = j2;
+        a2 = a3;
+        k2 = k3;
         double ap = __shfl_up((double)af, 1, kWave);         // arrival of event r - 1
         if (lane == 0) ap = a_prev;
         const double a = (double)af;
@@ -848,16 +880,50 @@ __device__ __forceinline__ void dregg_walk(size_t item, const float* __restrict_
     double Pm = tn.mu * tn.em, Ps = tn.mu * tn.es;
     int s_hi = ns;                                        // spikes with out_k <= the step's last event
     while (s_hi > 0 && sk[s_hi - 1] > nb - 1) --s_hi;
-    for (int f = ((nb - 1) / kWave) * kWave; f >= 0; f -= kWave) {
+    // The queue's loads run ahead of the walk (steps going down): at step f
+    // the weights of step f - 64 (their sources loaded a step earlier), the
+    // sources of step f - 128 and the arrivals, event indices and records of
+    // step f - 192 are issued before the step's work.
+    auto ld_q = [&](int ff, float& a_, int& k_, float2& rc_) {
+        const int rr = ff + lane;
+        const bool o = ff >= 0 && rr < nb;
+        a_ = o ? qa[rr] : 0.0f;
+        k_ = o ? min(max(qi[rr], 0), nb - 1) : 0;
+        rc_ = o ? rb[rr] : make_float2(0.0f, 0.0f);
+    };
+    auto ld_j = [&](int k_) { return clamp_src(src[k_], C_in); };
+    auto ld_w = [&](int ff, int j_) { return ff >= 0 && ff + lane < nb ? WT[(size_t)j_ * (size_t)N + n] : 0.0f; };
+    const int ftop = ((nb - 1) / kWave) * kWave;
+    float a0, a1, a2, w0;
+    int k0, k1, k2, j0, j1;
+    float2 c0, c1, c2;
+    ld_q(ftop, a0, k0, c0);
+    j0 = ld_j(k0);
+    w0 = ld_w(ftop, j0);
+    ld_q(ftop - kWave, a1, k1, c1);
+    j1 = ld_j(k1);
+    ld_q(ftop - 2 * kWave, a2, k2, c2);
+    for (int f = ftop; f >= 0; f -= kWave) {
         const int r = f + lane;
         const bool ok = r < nb;
         const int hi = min(f + kWave - 1, nb - 1);
-        const float af = ok ? qa[r] : 0.0f;
-        const int k = ok ? min(max(qi[r], 0), nb - 1) : 0;
-        const int j = clamp_src(src[k], C_in);
-        const double w = ok ? (double)WT[(size_t)j * N + n] : 0.0;
+        const float w1 = ld_w(f - kWave, j1);
+        const int j2 = ld_j(k2);
+        float a3;
+        int k3;
+        float2 c3;
+        ld_q(f - 3 * kWave, a3, k3, c3);
+        const float af = a0;
+        const int k = k0, j = j0;
+        const double w = ok ? (double)w0 : 0.0;
+        const float2 rc = c0;
+        // the arrival before each event: the lane below, or the step below's last
         double ap = __shfl_up((double)af, 1, kWave);
-        if (lane == 0) ap = f > 0 ? (double)qa[f - 1] : 0.0;
+        const double a_below = __shfl((double)a1, kWave - 1, kWave);
+        if (lane == 0) ap = f > 0 ? a_below : 0.0;
+        a0 = a1; k0 = k1; j0 = j1; w0 = w1; c0 = c1;
+        a1 = a2; k1 = k2; j1 = j2; c1 = c2;
+        a2 = a3; k2 = k3; c2 = c3;
         const double a = (double)af;
         double A = 1.0, D = 1.0;
         RecTerm t{0.0, 0.0, 0.0, 0.0, 0.0};
@@ -865,7 +931,7 @@ __device__ __forceinline__ void dregg_walk(size_t item, const float* __restrict_
             const double L = a - ap;
             A = exp(-L * m.inv_tm);
             D = exp(-L * m.inv_ts);
-            t = rec_term(rb[r], G, A, D);                 // interval r, closed by event r
+            t = rec_term(rc, G, A, D);                    // interval r, closed by event r
         }
         // the record after event r: lane r + 1's, or the carried one at the top
         RecTerm tx;
@@ -919,7 +985,7 @@ __global__ __launch_bounds__(kWave * kDRegWaves) void k_dregg_walk(
     long long* __restrict__ gw, long long* __restrict__ gd, long long* __restrict__ gt,
     float* __restrict__ grad_spike)
 {
-    const size_t item = (size_t)blockIdx.x * kDRegWaves + threadIdx.x / kWave;
+    const size_t item = (size_t)__builtin_amdgcn_readfirstlane((int)(blockIdx.x * kDRegWaves + threadIdx.x / kWave));
     if (item >= (size_t)B * N) return;
     const int n = (int)(item % (size_t)N);
     const double sW = scale[0], sD = scale[1];
@@ -952,7 +1018,7 @@ __global__ __launch_bounds__(kWave * kDlyLdsWaves) void k_dregg_walk_lds(
         s_d[j] = 0;
     }
     __syncthreads();
-    const int b = bg * kDlyLdsWaves + tid / kWave;
+    const int b = __builtin_amdgcn_readfirstlane(bg * kDlyLdsWaves + tid / kWave);
     if (b < B) {
         const double sW = scale[0], sD = scale[1];
         const bool want_d = gd != nullptr;
