@@ -249,7 +249,9 @@ int lif_layer_forward_delayed_sequential(const float* q_t, const int32_t* q_k, c
  *   grad_ev_t  float [B][E_max]     dL/dt_k summed over the neurons,
  *                                   overwritten (nullable; 0 past ev_n[b])
  * Bitwise reproducible (64-bit fixed-point sums).  ws: at least
- * lif_layer_backward_delayed_workspace_size(...) bytes.  Errors as
+ * lif_layer_backward_delayed_workspace_size(...) bytes, which include 8
+ * bytes per (sample, neuron, queue event) for the dL/dt terms: with
+ * grad_ev_t NULL, B * N_out * E_max * 8 bytes less suffice.  Errors as
  * lif_layer_backward. */
 size_t lif_layer_backward_delayed_workspace_size(int B, int E_max, int C_in, int N_out, const lif_params* p);
 int lif_layer_backward_delayed(const float* q_t, const int32_t* q_k, const int32_t* ev_src, const int32_t* ev_n,

@@ -643,6 +643,8 @@ def backward_delayed(q: DelayQueues, ev_src, ev_n, WT, fwd: ForwardOut, grad_out
     gD = torch.empty((C, N), dtype=torch.float32, device=dev) if want_delay_grad else None
     gT = torch.empty((B, E), dtype=torch.float32, device=dev) if want_time_grad else None
     need = lif_layer_backward_delayed_workspace_size(B, E, C, N, p)
+    if not want_time_grad:
+        need -= B * N * E * 8          # no per-event dL/dt terms are stored
     if ws is None or ws.numel() < need:
         ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     g = grad_out_t.contiguous().to(torch.float32)

@@ -320,10 +320,12 @@ __global__ void k_dly_status_reset(int32_t* __restrict__ status)
 // Backward
 // ---------------------------------------------------------------------------
 struct DlyBwdLayout {
-    size_t mu, musum, scale, wmax, gw, gd, gt, total;
+    size_t mu, musum, scale, wmax, gw, gd, gt, tcnt, tq, total;
 };
 
-static DlyBwdLayout dly_bwd_layout(int B, int E_max, int C_in, int N, int s_max)
+// tq (the walks' per-queue-event dL/dt terms) comes last and only with
+// want_t, so that a call without dL/dt can take B N E_max 8 bytes less.
+static DlyBwdLayout dly_bwd_layout(int B, int E_max, int C_in, int N, int s_max, bool want_t)
 {
     DlyBwdLayout L{};
     size_t off = 0;
@@ -335,6 +337,8 @@ static DlyBwdLayout dly_bwd_layout(int B, int E_max, int C_in, int N, int s_max)
     L.gw = take((size_t)C_in * N * sizeof(long long));
     L.gd = take((size_t)C_in * N * sizeof(long long));
     L.gt = take((size_t)B * E_max * sizeof(long long));
+    L.tcnt = take((size_t)B * N * sizeof(int32_t));
+    L.tq = take(want_t ? (size_t)B * N * (size_t)E_max * sizeof(long long) : 0);
     L.total = off + 256;
     return L;
 }
@@ -432,19 +436,21 @@ __device__ __forceinline__ void dly_walk(size_t item, const float* __restrict__ 
                                          int E_max, const float* __restrict__ WT, int C_in, int N, const Model& m,
                                          const float* __restrict__ out_t, const int32_t* __restrict__ out_n,
                                          const int32_t* __restrict__ out_k, const double* __restrict__ mu,
-                                         const double* __restrict__ scale, AddWD add_wd, long long* __restrict__ gt)
+                                         const double* __restrict__ scale, AddWD add_wd, long long* __restrict__ tq,
+                                         int32_t* __restrict__ tcnt)
 {
     const int lane = (int)threadIdx.x % kWave;
     const int ns = min(out_n[item], m.s_max);
-    if (ns <= 0) return;
     const int b = (int)(item / (size_t)N), n = (int)(item % (size_t)N);
     const int nb = clamp_count(ev_n[b], E_max);
     const size_t so = item * (size_t)m.s_max;
     const float* st = out_t + so;
     const int32_t* sk = out_k + so;
     const double* mo = mu + so;
-    const int klast = min(max(sk[ns - 1], 0), nb);      // queue events 0 .. klast - 1 feed a spike
+    const int klast = ns > 0 ? min(max(sk[ns - 1], 0), nb) : 0;   // queue events 0 .. klast - 1 feed a spike
+    if (tcnt && lane == 0) tcnt[item] = klast;          // and get a dL/dt term in tq
     if (klast <= 0) return;
+    long long* tqr = tq ? tq + item * (size_t)E_max : nullptr;
     const float* qa = q_t + item * (size_t)E_max;
     const int32_t* qi = q_k + item * (size_t)E_max;
     const int32_t* src = ev_src + (size_t)b * E_max;
@@ -486,7 +492,7 @@ __device__ __forceinline__ void dly_walk(size_t item, const float* __restrict__ 
             }
             const double ga = w * m.kappa * (Pm * m.inv_tm - Ps * m.inv_ts);
             add_wd(j, m.kappa * (Pm - Ps), ga);
-            if (gt) fx_add(&gt[(size_t)b * E_max + k], ga, sT);
+            if (tqr) tqr[e] = llrint(ga * sT);
         }
         if (f == 0) break;
         // the carry moved to the previous step's last event
@@ -511,7 +517,7 @@ __global__ __launch_bounds__(kWave * kDlyWaves) void k_dly_adjoint(
     const int32_t* __restrict__ ev_n, int B, int E_max, const float* __restrict__ WT, int C_in, int N, Model m,
     const float* __restrict__ out_t, const int32_t* __restrict__ out_n, const int32_t* __restrict__ out_k,
     const double* __restrict__ mu, const double* __restrict__ scale, long long* __restrict__ gw,
-    long long* __restrict__ gd, long long* __restrict__ gt)
+    long long* __restrict__ gd, long long* __restrict__ tq, int32_t* __restrict__ tcnt)
 {
     const size_t item = (size_t)blockIdx.x * kDlyWaves + threadIdx.x / kWave;
     if (item >= (size_t)B * N) return;
@@ -522,7 +528,7 @@ __global__ __launch_bounds__(kWave * kDlyWaves) void k_dly_adjoint(
         fx_add(&gw[wi], vw, sW);
         if (gd) fx_add(&gd[wi], vd, sD);
     };
-    dly_walk(item, q_t, q_k, ev_src, ev_n, E_max, WT, C_in, N, m, out_t, out_n, out_k, mu, scale, add_wd, gt);
+    dly_walk(item, q_t, q_k, ev_src, ev_n, E_max, WT, C_in, N, m, out_t, out_n, out_k, mu, scale, add_wd, tq, tcnt);
 }
 
 // For C_in <= kDlyLdsMaxC: one workgroup per (neuron, kDlyLdsWaves samples),
@@ -537,7 +543,7 @@ __global__ __launch_bounds__(kWave * kDlyLdsWaves) void k_dly_adjoint_lds(
     const int32_t* __restrict__ ev_n, int B, int E_max, const float* __restrict__ WT, int C_in, int N, Model m,
     const float* __restrict__ out_t, const int32_t* __restrict__ out_n, const int32_t* __restrict__ out_k,
     const double* __restrict__ mu, const double* __restrict__ scale, long long* __restrict__ gw,
-    long long* __restrict__ gd, long long* __restrict__ gt, int nbg)
+    long long* __restrict__ gd, long long* __restrict__ tq, int32_t* __restrict__ tcnt, int nbg)
 {
     extern __shared__ long long s_wd[];            // [C_in] dL/dW sums, then [C_in] dL/dD sums
     long long* s_w = s_wd;
@@ -558,7 +564,7 @@ __global__ __launch_bounds__(kWave * kDlyLdsWaves) void k_dly_adjoint_lds(
             if (want_d) atomicAdd((unsigned long long*)&s_d[j], (unsigned long long)llrint(vd * sD));
         };
         dly_walk((size_t)b * N + n, q_t, q_k, ev_src, ev_n, E_max, WT, C_in, N, m, out_t, out_n, out_k, mu, scale,
-                 add_wd, gt);
+                 add_wd, tq, tcnt);
     }
     __syncthreads();
     for (int j = tid; j < C_in; j += (int)blockDim.x) {
@@ -585,6 +591,83 @@ __global__ __launch_bounds__(256) void k_dly_convert(const long long* __restrict
     }
     if (grad_ev_t)
         for (size_t x = gtid; x < nT; x += gs) grad_ev_t[x] = (float)((double)gt[x] * iT);
+}
+
+// dL/dt from the walks' per-event terms.  A walk stores the 64-bit
+// fixed-point dL/dt term of each of its first tcnt[item] queue events at
+// tq[item * stride + r] instead of adding it to dL/dt_k itself (every neuron
+// of a sample adds to the same k, which makes those adds the walk's
+// bottleneck).  One workgroup per (sample, group of neurons, range of kChunk
+// event indices) sums its group's terms into LDS by event index (integer adds,
+// order free) and adds each nonzero sum to gt once.
+constexpr int kGtTargetBlocks = 1024;   // workgroups the neuron groups aim for
+
+template <int kChunk, int kThreads>
+__global__ __launch_bounds__(kThreads) void k_gt_gather(const int32_t* __restrict__ q_k,
+                                                       const int32_t* __restrict__ ev_n,
+                                                       const int32_t* __restrict__ tcnt, const long long* tq,
+                                                       size_t stride, int E_max, int N, int ng, int nck,
+                                                       long long* __restrict__ gt)
+{
+    __shared__ long long s_gt[kChunk];
+    constexpr int kU = 4;                   // entries per thread in flight
+    const int tid = (int)threadIdx.x;
+    const int ck = (int)(blockIdx.x % (unsigned)nck);
+    const int g = (int)((blockIdx.x / (unsigned)nck) % (unsigned)ng);
+    const int b = (int)(blockIdx.x / ((unsigned)nck * (unsigned)ng));
+    const int nb = clamp_count(ev_n[b], E_max);
+    const int k0 = ck * kChunk, k1 = min(k0 + kChunk, nb);
+    if (k0 >= k1) return;
+    for (int i = tid; i < k1 - k0; i += kThreads) s_gt[i] = 0;
+    __syncthreads();
+    const int per = (N + ng - 1) / ng, n0 = g * per, n1 = min(N, n0 + per);
+    for (int n = n0; n < n1; ++n) {
+        const size_t item = (size_t)b * N + n;
+        const int c = min(max(tcnt[item], 0), nb);
+        const int32_t* qk = q_k + item * (size_t)E_max;
+        const long long* tv = tq + item * stride;
+        for (int r0 = 0; r0 < c; r0 += kU * kThreads) {
+            int kk[kU];
+            long long vv[kU];
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                const int r = r0 + u * kThreads + tid;
+                const bool o = r < c;
+                kk[u] = o ? min(max(qk[r], 0), nb - 1) : -1;
+                vv[u] = o ? tv[r] : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < kU; ++u)
+                if (vv[u] != 0 && kk[u] >= k0 && kk[u] < k1)
+                    atomicAdd((unsigned long long*)&s_gt[kk[u] - k0], (unsigned long long)vv[u]);
+        }
+    }
+    __syncthreads();
+    for (int i = tid; i < k1 - k0; i += kThreads) {
+        const long long v = s_gt[i];
+        if (v) atomicAdd((unsigned long long*)&gt[(size_t)b * E_max + k0 + i], (unsigned long long)v);
+    }
+}
+
+static void launch_gt_gather(const int32_t* q_k, const int32_t* ev_n, const int32_t* tcnt, const long long* tq,
+                             size_t stride, int B, int E_max, int N, long long* gt, hipStream_t stream)
+{
+    if (B <= 0 || E_max <= 0) return;
+    auto groups = [&](int nck) {
+        const long long per_b = (long long)B * nck;
+        long long ng = (kGtTargetBlocks + per_b - 1) / per_b;
+        return (int)(ng < 1 ? 1 : (ng > N ? N : ng));
+    };
+    if (E_max <= 4096) {
+        const int ng = groups(1);
+        TIMED_LAUNCH("gt_gather", (k_gt_gather<4096, 256>), dim3((unsigned)((size_t)B * ng)), dim3(256), 0, stream,
+                     q_k, ev_n, tcnt, tq, stride, E_max, N, ng, 1, gt);
+    } else {
+        const int nck = (E_max + 16383) / 16384;
+        const int ng = groups(nck);
+        TIMED_LAUNCH("gt_gather", (k_gt_gather<16384, 1024>), dim3((unsigned)((size_t)B * ng * nck)), dim3(1024), 0,
+                     stream, q_k, ev_n, tcnt, tq, stride, E_max, N, ng, nck, gt);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -857,15 +940,17 @@ __device__ __forceinline__ void dregg_walk(size_t item, const float* __restrict_
                                            const int32_t* __restrict__ ev_n, int E_max, const float* __restrict__ WT,
                                            int C_in, int N, const Model& m, const float* __restrict__ out_t,
                                            const int32_t* __restrict__ out_n, const int32_t* __restrict__ out_k,
-                                           const float2* __restrict__ rec, const double2* __restrict__ coef,
+                                           float2* rec, const double2* __restrict__ coef,
                                            const double* __restrict__ scale, AddWD add_wd,
-                                           long long* __restrict__ gt, float* __restrict__ grad_spike)
+                                           int32_t* __restrict__ tcnt, float* __restrict__ grad_spike)
 {
     const int lane = (int)threadIdx.x % kWave;
     const int b = (int)(item / (size_t)N), n = (int)(item % (size_t)N);
     const int nb = clamp_count(ev_n[b], E_max);
     const double2 G = coef[item];
-    if (nb == 0 || (G.x == 0.0 && G.y == 0.0)) return;
+    const bool live = nb > 0 && (G.x != 0.0 || G.y != 0.0);
+    if (tcnt && lane == 0) tcnt[item] = live ? nb : 0;  // queue events with a dL/dt term
+    if (!live) return;
     const float* qa = q_t + item * (size_t)E_max;
     const int32_t* qi = q_k + item * (size_t)E_max;
     const int32_t* src = ev_src + (size_t)b * E_max;
@@ -873,7 +958,10 @@ __device__ __forceinline__ void dregg_walk(size_t item, const float* __restrict_
     const float* st = out_t + item * (size_t)m.s_max;
     const int32_t* sk = out_k + item * (size_t)m.s_max;
     float* gsp = grad_spike + item * (size_t)m.s_max;
-    const float2* rb = rec + item * ((size_t)E_max + 1);
+    // the item's records; with tcnt, record r is overwritten by the 64-bit
+    // fixed-point dL/dt term of queue event r once the walk has read it
+    // (three steps before), stored as a float2 of the same bits
+    float2* rb = rec + item * ((size_t)E_max + 1);
     const double sT = scale[2], kap = m.kappa, skp = -(m.dth * m.inv_tm);
     // P at event nb - 1: the open interval's pseudo-spike; tn: that interval
     RecTerm tn = rec_term(rb[nb], G, 0.0, 0.0);
@@ -914,7 +1002,7 @@ __device__ __forceinline__ void dregg_walk(size_t item, const float* __restrict_
         float2 c3;
         ld_q(f - 3 * kWave, a3, k3, c3);
         const float af = a0;
-        const int k = k0, j = j0;
+        const int j = j0;
         const double w = ok ? (double)w0 : 0.0;
         const float2 rc = c0;
         // the arrival before each event: the lane below, or the step below's last
@@ -959,7 +1047,7 @@ __device__ __forceinline__ void dregg_walk(size_t item, const float* __restrict_
             ga = fma(tx.mu, tx.vs, ga);                   // 0 unless that argmax is the interval's start
             ga = fma(t.mu, t.ve, ga);                     // 0 unless this argmax is the interval's end
             add_wd(j, kap * (Pmr - Psr), ga);
-            if (gt) atomicAdd((unsigned long long*)&gt[(size_t)b * E_max + k], (unsigned long long)llrint(ga * sT));
+            if (tcnt) rb[r] = __builtin_bit_cast(float2, (long long)llrint(ga * sT));
         }
         // the spikes of intervals f .. hi: upstream gradient from P at the
         // event that closes their interval
@@ -981,8 +1069,8 @@ __global__ __launch_bounds__(kWave * kDRegWaves) void k_dregg_walk(
     const float* __restrict__ q_t, const int32_t* __restrict__ q_k, const int32_t* __restrict__ ev_src,
     const int32_t* __restrict__ ev_n, int B, int E_max, const float* __restrict__ WT, int C_in, int N, Model m,
     const float* __restrict__ out_t, const int32_t* __restrict__ out_n, const int32_t* __restrict__ out_k,
-    const float2* __restrict__ rec, const double2* __restrict__ coef, const double* __restrict__ scale,
-    long long* __restrict__ gw, long long* __restrict__ gd, long long* __restrict__ gt,
+    float2* rec, const double2* __restrict__ coef, const double* __restrict__ scale,
+    long long* __restrict__ gw, long long* __restrict__ gd, int32_t* __restrict__ tcnt,
     float* __restrict__ grad_spike)
 {
     const size_t item = (size_t)__builtin_amdgcn_readfirstlane((int)(blockIdx.x * kDRegWaves + threadIdx.x / kWave));
@@ -995,7 +1083,7 @@ __global__ __launch_bounds__(kWave * kDRegWaves) void k_dregg_walk(
         if (gd) fx_add(&gd[wi], vd, sD);
     };
     dregg_walk(item, q_t, q_k, ev_src, ev_n, E_max, WT, C_in, N, m, out_t, out_n, out_k, rec, coef, scale, add_wd,
-               gt, grad_spike);
+               tcnt, grad_spike);
 }
 
 // C_in <= kDlyLdsMaxC: one workgroup per (neuron, kDlyLdsWaves samples), the
@@ -1004,8 +1092,8 @@ __global__ __launch_bounds__(kWave * kDlyLdsWaves) void k_dregg_walk_lds(
     const float* __restrict__ q_t, const int32_t* __restrict__ q_k, const int32_t* __restrict__ ev_src,
     const int32_t* __restrict__ ev_n, int B, int E_max, const float* __restrict__ WT, int C_in, int N, Model m,
     const float* __restrict__ out_t, const int32_t* __restrict__ out_n, const int32_t* __restrict__ out_k,
-    const float2* __restrict__ rec, const double2* __restrict__ coef, const double* __restrict__ scale,
-    long long* __restrict__ gw, long long* __restrict__ gd, long long* __restrict__ gt,
+    float2* rec, const double2* __restrict__ coef, const double* __restrict__ scale,
+    long long* __restrict__ gw, long long* __restrict__ gd, int32_t* __restrict__ tcnt,
     float* __restrict__ grad_spike, int nbg)
 {
     extern __shared__ long long s_wd[];            // [C_in] dL/dW sums, then [C_in] dL/dD sums
@@ -1027,7 +1115,7 @@ __global__ __launch_bounds__(kWave * kDlyLdsWaves) void k_dregg_walk_lds(
             if (want_d) atomicAdd((unsigned long long*)&s_d[j], (unsigned long long)llrint(vd * sD));
         };
         dregg_walk((size_t)b * N + n, q_t, q_k, ev_src, ev_n, E_max, WT, C_in, N, m, out_t, out_n, out_k, rec, coef,
-                   scale, add_wd, gt, grad_spike);
+                   scale, add_wd, tcnt, grad_spike);
     }
     __syncthreads();
     for (int j = tid; j < C_in; j += (int)blockDim.x) {
@@ -1151,7 +1239,7 @@ extern "C" size_t lif_layer_backward_delayed_workspace_size(int B, int E_max, in
                                                             const lif_params* p)
 {
     if (B < 0 || E_max < 0 || C_in < 1 || N_out < 1 || !p || p->s_max < 1) return 0;
-    return lif::dly_bwd_layout(B, E_max, C_in, N_out, p->s_max).total;
+    return lif::dly_bwd_layout(B, E_max, C_in, N_out, p->s_max, true).total;
 }
 
 extern "C" int lif_layer_backward_delayed(const float* q_t, const int32_t* q_k, const int32_t* ev_src,
@@ -1168,7 +1256,7 @@ extern "C" int lif_layer_backward_delayed(const float* q_t, const int32_t* q_k, 
     if (B > 0 && (!ev_n || !out_t || !out_n || !out_i || !out_k || !grad_out_t)) return LIF_ERR_ARG;
     if (B > 0 && E_max > 0 && (!q_t || !q_k || !ev_src)) return LIF_ERR_ARG;
     if ((size_t)B * (size_t)N_out >= ((size_t)1 << 31)) return LIF_ERR_SIZE;
-    const DlyBwdLayout L = dly_bwd_layout(B, E_max, C_in, N_out, p->s_max);
+    const DlyBwdLayout L = dly_bwd_layout(B, E_max, C_in, N_out, p->s_max, grad_ev_t != nullptr);
     if (!ws || ws_bytes < L.total) return LIF_ERR_WORKSPACE;
     hipStream_t stream = (hipStream_t)stream_;
     const Model m = make_model(*p);
@@ -1180,6 +1268,8 @@ extern "C" int lif_layer_backward_delayed(const float* q_t, const int32_t* q_k, 
     long long* gw = (long long*)(base + L.gw);
     long long* gd = (long long*)(base + L.gd);
     long long* gt = (long long*)(base + L.gt);
+    int32_t* tcnt = grad_ev_t ? (int32_t*)(base + L.tcnt) : nullptr;
+    long long* tq = grad_ev_t ? (long long*)(base + L.tq) : nullptr;
     const size_t nW = (size_t)C_in * N_out, nT = (size_t)B * E_max, nn = (size_t)B * N_out;
     size_t work = nW > nT ? nW : nT;
     if (nn > work) work = nn;
@@ -1193,12 +1283,13 @@ extern "C" int lif_layer_backward_delayed(const float* q_t, const int32_t* q_k, 
             const int nbg = (B + kDlyLdsWaves - 1) / kDlyLdsWaves;
             TIMED_LAUNCH("dly_adjoint", k_dly_adjoint_lds, dim3((unsigned)((size_t)N_out * nbg)),
                          dim3(kWave * kDlyLdsWaves), (size_t)2 * C_in * sizeof(long long), stream, q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N_out, m,
-                         out_t, out_n, out_k, mu, scale, gw, grad_DT ? gd : nullptr, grad_ev_t ? gt : nullptr, nbg);
+                         out_t, out_n, out_k, mu, scale, gw, grad_DT ? gd : nullptr, tq, tcnt, nbg);
         } else {
             TIMED_LAUNCH("dly_adjoint", k_dly_adjoint, dim3((unsigned)((nn + kDlyWaves - 1) / kDlyWaves)),
                          dim3(kWave * kDlyWaves), 0, stream, q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N_out, m,
-                         out_t, out_n, out_k, mu, scale, gw, grad_DT ? gd : nullptr, grad_ev_t ? gt : nullptr);
+                         out_t, out_n, out_k, mu, scale, gw, grad_DT ? gd : nullptr, tq, tcnt);
         }
+        if (grad_ev_t) launch_gt_gather(q_k, ev_n, tcnt, tq, (size_t)E_max, B, E_max, N_out, gt, stream);
     }
     TIMED_LAUNCH("dly_convert", k_dly_convert, dim3(grid_for(work)), dim3(256), 0, stream, gw, gd, gt, scale, nW, nT,
                  grad_WT, grad_DT, grad_ev_t);
@@ -1211,7 +1302,7 @@ extern "C" int lif_layer_backward_delayed(const float* q_t, const int32_t* q_k, 
 namespace lif {
 
 struct DRegLayout {
-    size_t ub, ob, counts, gates, coef, musum, vpmax, rec, wmax, scale, gw, gd, gt, total;
+    size_t ub, ob, counts, gates, coef, musum, vpmax, rec, wmax, scale, gw, gd, gt, tcnt, total;
 };
 
 static DRegLayout dreg_layout(int B, int E_max, int C_in, int N, bool grad)
@@ -1234,6 +1325,7 @@ static DRegLayout dreg_layout(int B, int E_max, int C_in, int N, bool grad)
         L.gw = take((size_t)C_in * N * sizeof(long long));
         L.gd = take((size_t)C_in * N * sizeof(long long));
         L.gt = take((size_t)B * E_max * sizeof(long long));
+        L.tcnt = take(nn * sizeof(int32_t));
     }
     L.total = off + 256;
     return L;
@@ -1325,6 +1417,7 @@ extern "C" int lif_spike_count_reg_delayed_backward(const float* q_t, const int3
     long long* gw = (long long*)(base + L.gw);
     long long* gd = (long long*)(base + L.gd);
     long long* gt = (long long*)(base + L.gt);
+    int32_t* tcnt = grad_ev_t ? (int32_t*)(base + L.tcnt) : nullptr;
     const size_t nW = (size_t)C_in * N_out, nT = (size_t)B * E_max, nn = (size_t)B * N_out;
     const size_t work = nW > nT ? nW : nT;
     TIMED_LAUNCH("dregg_zero", k_dregg_zero, dim3(grid_for(work)), dim3(256), 0, stream, nW, nT, gw, gd, gt, wmax);
@@ -1342,13 +1435,16 @@ extern "C" int lif_spike_count_reg_delayed_backward(const float* q_t, const int3
                 TIMED_LAUNCH("dregg_walk", k_dregg_walk_lds, dim3((unsigned)((size_t)N_out * nbg)),
                              dim3(kWave * kDlyLdsWaves), (size_t)2 * C_in * sizeof(long long), stream, q_t, q_k,
                              ev_src, ev_n, B, E_max, WT, C_in, N_out, m, out_t, out_n, out_k, rec, coef, scale, gw,
-                             grad_DT ? gd : nullptr, grad_ev_t ? gt : nullptr, grad_spike, nbg);
+                             grad_DT ? gd : nullptr, tcnt, grad_spike, nbg);
             } else {
                 TIMED_LAUNCH("dregg_walk", k_dregg_walk, dim3((unsigned)((nn + kDRegWaves - 1) / kDRegWaves)),
                              dim3(kWave * kDRegWaves), 0, stream, q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N_out, m,
-                             out_t, out_n, out_k, rec, coef, scale, gw, grad_DT ? gd : nullptr,
-                             grad_ev_t ? gt : nullptr, grad_spike);
+                             out_t, out_n, out_k, rec, coef, scale, gw, grad_DT ? gd : nullptr, tcnt,
+                             grad_spike);
             }
+            if (grad_ev_t)
+                launch_gt_gather(q_k, ev_n, tcnt, (const long long*)rec, (size_t)E_max + 1, B, E_max, N_out, gt,
+                                 stream);
         }
     } else {
         TIMED_LAUNCH("dregg_scale", k_dregg_scale, dim3(1), dim3(kDlyScaleThreads), 0, stream, musum, coef, vpmax,

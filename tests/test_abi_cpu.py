@@ -230,7 +230,11 @@ def test_delay_argument_errors(lib):
     assert b(15, None) == L.LIF_ERR_ARG             # grad_WT required
     assert b(13, None) == L.LIF_ERR_ARG             # out_k required
     need = L.lif_layer_backward_delayed_workspace_size(2, 10, 4, 8, p)
-    assert need > 0 and b(19, need - 1) == L.LIF_ERR_WORKSPACE
+    with_t = list(bb)
+    with_t[17], with_t[19] = F, need - 1          # with grad_ev_t: the full size
+    assert need > 0 and L.lif_layer_backward_delayed(*with_t) == L.LIF_ERR_WORKSPACE
+    # without grad_ev_t the per-event dL/dt terms (B N E_max 8 bytes) are not stored
+    assert b(19, need - 2 * 8 * 10 * 8 - 1) == L.LIF_ERR_WORKSPACE
     bad = L.Params(tau_mem=0.001).c()
     assert b(9, ctypes.byref(bad)) == L.LIF_ERR_TAU
 

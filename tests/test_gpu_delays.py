@@ -274,3 +274,48 @@ def test_delayed_regularisers_wide_input(env):
     compare_grad(gW.cpu().numpy(), gWd, label="wide direct grad_W")
     compare_grad(gD.cpu().numpy(), gDd, label="wide direct grad_D")
     compare_grad(gT.cpu().numpy(), gTd, label="wide direct grad_t")
+
+
+def test_delayed_regularisers_long_queues(env):
+    """E_max > 16384: the per-event dL/dt terms are summed over two ranges of
+    event indices; every output against the oracle at the float32 spike
+    times (with the hand-over band of the oracle at its exact ones), and
+    bitwise reproducible."""
+    from oracle import loss as OL
+    from tests.parity import compare_grad_band
+    torch, lif = env
+    cfg = W.random_small(91, B=2, C=60, N=6, n_events=17000, T=2.0 * 17000 / 12000, gain=1.0)
+    ev, WT = cfg.events, cfg.layers[0].WT
+    assert ev.E_max > 16384
+    DT = W.uniform_delays(91, 60, 6)
+    P = oracle.LifParams()
+    r = oracle.forward_delayed(ev.ev_t, ev.ev_src, ev.ev_n, WT, DT, P)
+    assert r.out_n.sum() > 10 and not r.capped.any()
+    r32 = r.rounded()
+    c_target = float(np.median(r.out_n.mean(axis=0))) + 0.5
+    rp = OL.RegParams(c_target=c_target, lam_reg=0.8, lam_over=0.3)
+    q_t, q_k = oracle.delay_queues(ev.ev_t, ev.ev_src, ev.ev_n, DT)
+    at32, at64 = (OL.spike_count_reg_delayed_grad(ev.ev_t, ev.ev_src, ev.ev_n, WT, q_t, q_k, x.out_t, r.out_k,
+                                                  r.out_n, P.tau_mem, P.tau_syn, P.v_th, P.v_reset, P.t_end, rp)
+                  for x in (r32, r))
+    print(f"[case] delayed regularisers E_max={ev.E_max} spikes={int(r.out_n.sum())}", flush=True)
+    t, s, n, w, d = (_dev(torch, a) for a in (ev.ev_t, ev.ev_src, ev.ev_n, WT, DT))
+    q = lif.delay_queues(t, s, n, d)
+    fwd = lif.ForwardOut(_dev(torch, r32.out_t.astype(np.float32)), _dev(torch, r.out_n),
+                         _dev(torch, r32.out_i.astype(np.float32)), None, _dev(torch, r.out_k))
+    outs = []
+    for _ in range(2):
+        loss, gsp, gW, gD, gT = lif.spike_count_reg_delayed_backward(q, s, n, w, fwd, c_target, 0.8, 0.3,
+                                                                     lif.Params())
+        torch.cuda.synchronize()
+        outs.append([x.cpu().numpy() for x in (loss, gsp, gW, gD, gT)])
+    loss, gsp, gW, gD, gT = outs[0]
+    for i in range(2):                        # L_reg, L_over: inside the band, 1e-5 relative
+        lo, hi = sorted((at32[i], at64[i]))
+        assert lo - 1e-5 * abs(lo) <= loss[i] <= hi + 1e-5 * abs(hi), (i, loss[i], at32[i], at64[i])
+    for got, j, label in ((gsp, 5, "spike-time gradient"), (gW, 2, "direct grad_W"), (gD, 3, "direct grad_D"),
+                          (gT, 4, "direct grad_t")):
+        compare_grad_band(got, at32[j], at64[j], label=f"long-queue {label}")
+    assert (gT[np.arange(ev.E_max)[None, :] >= ev.ev_n[:, None]] == 0).all()
+    for a, b_ in zip(outs[0], outs[1]):
+        assert np.array_equal(a.view(np.uint32), b_.view(np.uint32)), "not reproducible"
