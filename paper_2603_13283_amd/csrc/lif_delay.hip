@@ -95,22 +95,24 @@ __global__ __launch_bounds__(256) void k_dly_arrival(const float* __restrict__ e
 }
 
 // Queues of up to kMax events are sorted in registers and LDS by kThreads
-// threads (kMax / kThreads arrivals each, kMax / 4 bins at most): 8192 by 512
-// threads (two workgroups per CU), 16384 by 1024 (116 KB of LDS, one).
+// threads (kMax / kThreads arrivals each, kBins bins at most): 8192 by 512
+// threads and 11520 by 768 (two workgroups per CU), 16384 by 1024 (112 KB of
+// LDS, one).
 constexpr int kQLdsMax = 16384;         // longest queue sorted in registers and LDS
 
-template <int kMax, int kThreads>
-__global__ __launch_bounds__(kThreads) void k_dly_queue_lds(const int32_t* __restrict__ ev_n, int E_max, int N,
+template <int kMax, int kThreads, int kBins, int kWavesPerEU>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kWavesPerEU))) void k_dly_queue_lds(const int32_t* __restrict__ ev_n, int E_max, int N,
                                                                const float* __restrict__ arr,
                                                                float* __restrict__ q_t, int32_t* __restrict__ q_k)
 {
-    constexpr int kQLdsBins = kMax / 4;
+    constexpr int kQLdsBins = kBins;
     constexpr int kQR = kMax / kThreads;
+    static_assert(kQR * kThreads == kMax && (kBins & (kBins - 1)) == 0 && kMax < 32768, "queue sort shape");
     __shared__ uint32_t s_at[kMax];        // binned arrivals (bits)
     __shared__ uint16_t s_ak[kMax];        // and their event indices
     __shared__ int s_bin[kQLdsBins];
     __shared__ float s_red[kThreads / kWave];
-    __shared__ int s_part[kThreads];
+    __shared__ int s_wsum[kThreads / kWave];
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
     const size_t item = blockIdx.x;
     const int b = (int)(item / (size_t)N);
@@ -143,20 +145,21 @@ __global__ __launch_bounds__(kThreads) void k_dly_queue_lds(const int32_t* __res
         if (tid + r * kThreads < nb) atomicAdd(&s_bin[bin[r]], 1);
     }
     __syncthreads();
-    // exclusive prefix sum over the bins: each thread a contiguous range
+    // exclusive prefix sum over the bins: each thread a contiguous range,
+    // the ranges' sums scanned across each wave, then over the waves
     const int per = (nbins + kThreads - 1) / kThreads;
     const int j0 = min(tid * per, nbins), j1 = min(j0 + per, nbins);
     int local = 0;
     for (int j = j0; j < j1; ++j) local += s_bin[j];
-    s_part[tid] = local;
-    __syncthreads();
-    for (int off = 1; off < kThreads; off <<= 1) {
-        const int x = tid >= off ? s_part[tid - off] : 0;
-        __syncthreads();
-        s_part[tid] += x;
-        __syncthreads();
+    int incl = local;
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int x = __shfl_up(incl, off, kWave);
+        if (lane >= off) incl += x;
     }
-    int run = s_part[tid] - local;
+    if (lane == kWave - 1) s_wsum[wave] = incl;
+    __syncthreads();
+    int run = incl - local;
+    for (int w = 0; w < wave; ++w) run += s_wsum[w];
     for (int j = j0; j < j1; ++j) {
         const int c = s_bin[j];
         s_bin[j] = run;
@@ -178,22 +181,25 @@ __global__ __launch_bounds__(kThreads) void k_dly_queue_lds(const int32_t* __res
     __syncthreads();
     // each event's place: its bin's start plus its rank among the bin's
     // keys, the thread's events stepping through their bins together
-    int lo[kQR], cnt[kQR], rank[kQR];
+    // (a bin's start and size packed as start | size << 16: both <= kMax < 2^15)
+    int lc[kQR], rank[kQR];
     int mxc = 0;
 #pragma unroll
     for (int r = 0; r < kQR; ++r) {
         const bool v = tid + r * kThreads < nb;
-        lo[r] = bin[r] > 0 ? s_bin[bin[r] - 1] : 0;
-        cnt[r] = v ? s_bin[bin[r]] - lo[r] : 0;
+        const int lo = bin[r] > 0 ? s_bin[bin[r] - 1] : 0;
+        const int cnt = v ? s_bin[bin[r]] - lo : 0;
+        lc[r] = lo | (cnt << 16);
         rank[r] = 0;
-        mxc = max(mxc, cnt[r]);
+        mxc = max(mxc, cnt);
     }
     for (int q = 0; q < mxc; ++q) {
 #pragma unroll
         for (int r = 0; r < kQR; ++r) {
-            if (q < cnt[r]) {
-                const uint32_t o = s_at[lo[r] + q];
-                const int ok = s_ak[lo[r] + q];
+            if (q < (lc[r] >> 16)) {
+                const int at = (lc[r] & 0xffff) + q;
+                const uint32_t o = s_at[at];
+                const int ok = s_ak[at];
                 rank[r] += o < ab[r] || (o == ab[r] && ok < tid + r * kThreads);
             }
         }
@@ -202,8 +208,8 @@ __global__ __launch_bounds__(kThreads) void k_dly_queue_lds(const int32_t* __res
     // the queue in order in LDS, then written out coalesced
 #pragma unroll
     for (int r = 0; r < kQR; ++r) {
-        const int place = lo[r] + rank[r];
-        if (cnt[r] > 0 && place < nb) {         // always: a key's bin is the one it was scattered to
+        const int place = (lc[r] & 0xffff) + rank[r];
+        if ((lc[r] >> 16) > 0 && place < nb) {  // always: a key's bin is the one it was scattered to
             s_at[place] = ab[r];
             s_ak[place] = (uint16_t)(tid + r * kThreads);
         }
@@ -1193,11 +1199,14 @@ extern "C" int lif_delay_queues(const float* ev_t, const int32_t* ev_src, const 
                      N_out, arr);
         const dim3 qgrid((unsigned)((size_t)B * N_out));
         if (E_max <= 8192)
-            TIMED_LAUNCH("dly_queue", (k_dly_queue_lds<8192, 512>), qgrid, dim3(512), 0, stream, ev_n, E_max, N_out,
-                         arr, q_t, q_k);
-        else if (E_max <= kQLdsMax)
-            TIMED_LAUNCH("dly_queue", (k_dly_queue_lds<kQLdsMax, 1024>), qgrid, dim3(1024), 0, stream, ev_n, E_max,
+            TIMED_LAUNCH("dly_queue", (k_dly_queue_lds<8192, 512, 2048, 4>), qgrid, dim3(512), 0, stream, ev_n, E_max,
                          N_out, arr, q_t, q_k);
+        else if (E_max <= 11520)
+            TIMED_LAUNCH("dly_queue", (k_dly_queue_lds<11520, 768, 2048, 6>), qgrid, dim3(768), 0, stream, ev_n, E_max,
+                         N_out, arr, q_t, q_k);
+        else if (E_max <= kQLdsMax)
+            TIMED_LAUNCH("dly_queue", (k_dly_queue_lds<kQLdsMax, 1024, 4096, 4>), qgrid, dim3(1024), 0, stream, ev_n,
+                         E_max, N_out, arr, q_t, q_k);
         else
             TIMED_LAUNCH("dly_queue", k_dly_queue, qgrid, dim3(kQThreads), 0, stream, ev_n, E_max, N_out, arr, keys,
                          q_t, q_k);

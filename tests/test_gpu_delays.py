@@ -150,10 +150,11 @@ def test_delays_wide_input(env):
     assert st["spikes"] > 0
 
 
-@pytest.mark.parametrize("n_events,gain", [(12000, 2.0), (17000, 1.4)])
+@pytest.mark.parametrize("n_events,gain", [(10000, 2.0), (12000, 2.0), (17000, 1.4)])
 def test_delays_long_queues(env, n_events, gain):
     """Queues past the 512-thread register/LDS sort (E_max > 8192) take the
-    1024-thread one; past 16384 they bin through global memory."""
+    768-thread one up to 11520 and the 1024-thread one up to 16384; past
+    16384 they bin through global memory."""
     cfg = W.random_small(86, B=2, C=60, N=20, n_events=n_events, T=2.0 * n_events / 12000, gain=gain)
     ev = cfg.events
     assert ev.E_max > 8192 and (n_events < 16384 or ev.E_max > 16384)
