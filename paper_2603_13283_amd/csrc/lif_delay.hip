@@ -41,6 +41,7 @@
 #include "lif_common.hpp"
 #include "lif_host.hpp"
 #include "lif_reg.hpp"
+#include "lif_scan.hpp"
 
 namespace lif {
 
@@ -700,34 +701,6 @@ static void launch_gt_gather(const int32_t* q_k, const int32_t* ev_n, const int3
 //                 closes its interval.
 // ---------------------------------------------------------------------------
 constexpr int kDRegWaves = 4;
-
-// Inclusive scan across the wave of affine maps x -> a x + b, composed in
-// lane order (lane l: the maps of lanes 0 .. l, lane 0's applied first).
-__device__ __forceinline__ void scan_maps_up(double& a, double& b, int lane)
-{
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-        const double pa = __shfl_up(a, off, kWave), pb = __shfl_up(b, off, kWave);
-        if (lane >= off) {
-            b = fma(a, pb, b);
-            a *= pa;
-        }
-    }
-}
-
-// The same from the top (lane l: the maps of lanes 63 .. l, lane 63's
-// applied first).
-__device__ __forceinline__ void scan_maps_down(double& a, double& b, int lane)
-{
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-        const double pa = __shfl_down(a, off, kWave), pb = __shfl_down(b, off, kWave);
-        if (lane + off < kWave) {
-            b = fma(a, pb, b);
-            a *= pa;
-        }
-    }
-}
 
 __global__ __launch_bounds__(kWave * kDRegWaves) void k_dreg_walk(
     const float* __restrict__ q_t, const int32_t* __restrict__ q_k, const int32_t* __restrict__ ev_src,
