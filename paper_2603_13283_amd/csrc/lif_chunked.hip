@@ -26,6 +26,7 @@
 // entry, built by lif_delay_queues); out_k then counts events of the
 // neuron's own queue.
 #include "lif_common.hpp"
+#include "lif_scan.hpp"
 #include "lif_host.hpp"
 
 namespace lif {
@@ -166,18 +167,8 @@ __global__ __launch_bounds__(kWave * kChunkWaves) void k_chunked(
             f.bJ = fma(D[j], f.bJ, x);
         }
         LaneMap inc = f;                      // inclusive scan: maps of lanes 0 .. l
-#pragma unroll
-        for (int off = 1; off < kWave; off <<= 1) {
-            const double aU = __shfl_up(inc.aU, off, kWave), bU = __shfl_up(inc.bU, off, kWave);
-            const double aJ = __shfl_up(inc.aJ, off, kWave), bJ = __shfl_up(inc.bJ, off, kWave);
-            if (lane >= off) {
-                // inc <- inc o earlier: apply the earlier lanes' map first
-                inc.bU = fma(inc.aU, bU, inc.bU);
-                inc.aU *= aU;
-                inc.bJ = fma(inc.aJ, bJ, inc.bJ);
-                inc.aJ *= aJ;
-            }
-        }
+        scan_maps_up(inc.aU, inc.bU, lane);
+        scan_maps_up(inc.aJ, inc.bJ, lane);
         LaneMap ex{__shfl_up(inc.aU, 1, kWave), __shfl_up(inc.bU, 1, kWave), __shfl_up(inc.aJ, 1, kWave),
                    __shfl_up(inc.bJ, 1, kWave)};
         if (lane == 0) ex = LaneMap{1.0, 0.0, 1.0, 0.0};
