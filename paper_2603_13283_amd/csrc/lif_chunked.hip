@@ -147,10 +147,10 @@ __global__ __launch_bounds__(kWave * kChunkWaves) void k_chunked(
         }
         // the time before each event: the previous event's, t_cur for the
         // chunk's first
-        const double prev_last = __shfl_up(te[M - 1], 1, kWave);
+        const double prev_last = wave_shr1(te[M - 1], t_cur);
 #pragma unroll
         for (int j = 0; j < M; ++j) {
-            const double tp = j > 0 ? te[j - 1] : (lane > 0 ? prev_last : t_cur);
+            const double tp = j > 0 ? te[j - 1] : prev_last;
             L[j] = valid[j] ? te[j] - tp : 0.0;
             A[j] = exp(-L[j] * m.inv_tm);
             D[j] = exp(-L[j] * m.inv_ts);
@@ -169,9 +169,8 @@ __global__ __launch_bounds__(kWave * kChunkWaves) void k_chunked(
         LaneMap inc = f;                      // inclusive scan: maps of lanes 0 .. l
         scan_maps_up(inc.aU, inc.bU, lane);
         scan_maps_up(inc.aJ, inc.bJ, lane);
-        LaneMap ex{__shfl_up(inc.aU, 1, kWave), __shfl_up(inc.bU, 1, kWave), __shfl_up(inc.aJ, 1, kWave),
-                   __shfl_up(inc.bJ, 1, kWave)};
-        if (lane == 0) ex = LaneMap{1.0, 0.0, 1.0, 0.0};
+        const LaneMap ex{wave_shr1(inc.aU, 1.0), wave_shr1(inc.bU, 0.0), wave_shr1(inc.aJ, 1.0),
+                         wave_shr1(inc.bJ, 0.0)};
         const double U0 = V / m.kappa + I, J0 = I;
         double U = fma(ex.aU, U0, ex.bU), J = fma(ex.aJ, J0, ex.bJ);
         // the lane's intervals in order; the first crossing's data kept

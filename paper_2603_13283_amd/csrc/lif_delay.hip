@@ -985,9 +985,7 @@ __device__ __forceinline__ void dregg_walk(size_t item, const float* __restrict_
         const double w = ok ? (double)w0 : 0.0;
         const float2 rc = c0;
         // the arrival before each event: the lane below, or the step below's last
-        double ap = __shfl_up((double)af, 1, kWave);
-        const double a_below = __shfl((double)a1, kWave - 1, kWave);
-        if (lane == 0) ap = f > 0 ? a_below : 0.0;
+        const double ap = wave_shr1((double)af, f > 0 ? read_lane_double((double)a1, kWave - 1) : 0.0);
         a0 = a1; k0 = k1; j0 = j1; w0 = w1; c0 = c1;
         a1 = a2; k1 = k2; j1 = j2; c1 = c2;
         a2 = a3; k2 = k3; c2 = c3;
@@ -1002,8 +1000,8 @@ __device__ __forceinline__ void dregg_walk(size_t item, const float* __restrict_
         }
         // the record after event r: lane r + 1's, or the carried one at the top
         RecTerm tx;
-        tx.mu = __shfl_down(t.mu, 1, kWave);
-        tx.vs = __shfl_down(t.vs, 1, kWave);
+        tx.mu = wave_shl1(t.mu, 0.0);
+        tx.vs = wave_shl1(t.vs, 0.0);
         if (r == hi) {
             tx.mu = tn.mu;
             tx.vs = tn.vs;
@@ -1012,14 +1010,8 @@ __device__ __forceinline__ void dregg_walk(size_t item, const float* __restrict_
         double am = A, bm = t.mu * t.em, as = D, bs = t.mu * t.es;
         scan_maps_down(am, bm, lane);
         scan_maps_down(as, bs, lane);
-        double xam = __shfl_down(am, 1, kWave), xbm = __shfl_down(bm, 1, kWave);
-        double xas = __shfl_down(as, 1, kWave), xbs = __shfl_down(bs, 1, kWave);
-        if (lane == kWave - 1) {
-            xam = 1.0;
-            xbm = 0.0;
-            xas = 1.0;
-            xbs = 0.0;
-        }
+        const double xam = wave_shl1(am, 1.0), xbm = wave_shl1(bm, 0.0);
+        const double xas = wave_shl1(as, 1.0), xbs = wave_shl1(bs, 0.0);
         const double Pmr = fma(xam, Pm, xbm), Psr = fma(xas, Ps, xbs);
         if (ok) {
             double ga = w * kap * (Pmr * m.inv_tm - Psr * m.inv_ts);
@@ -1035,10 +1027,10 @@ __device__ __forceinline__ void dregg_walk(size_t item, const float* __restrict_
         for (int s = s_lo; s < s_hi; ++s)
             if (sk[s] == r) gsp[s] += (float)(skp * Pmr * exp(-(a - (double)st[s]) * m.inv_tm));
         // the carry: P at event f - 1 and the record of interval f
-        Pm = __shfl(fma(am, Pm, bm), 0, kWave);
-        Ps = __shfl(fma(as, Ps, bs), 0, kWave);
-        tn.mu = __shfl(t.mu, 0, kWave);
-        tn.vs = __shfl(t.vs, 0, kWave);
+        Pm = read_lane_double(fma(am, Pm, bm), 0);
+        Ps = read_lane_double(fma(as, Ps, bs), 0);
+        tn.mu = read_lane_double(t.mu, 0);
+        tn.vs = read_lane_double(t.vs, 0);
         s_hi = s_lo;
     }
 }

@@ -22,6 +22,12 @@ __device__ __forceinline__ double dpp_double(double v, double fill)
     return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
 
+// v of lane j - 1 (lane 0: fill) / of lane j + 1 (lane 63: fill) across the
+// whole wave (DPP wave shifts).
+__device__ __forceinline__ double wave_shr1(double v, double fill) { return dpp_double<0x138>(v, fill); }
+__device__ __forceinline__ double wave_shl1(double v, double fill) { return dpp_double<0x130>(v, fill); }
+
+// v of lane l (l wave-uniform).
 __device__ __forceinline__ double read_lane_double(double v, int l)
 {
     const unsigned long long u = (unsigned long long)__double_as_longlong(v);
