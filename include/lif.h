@@ -213,7 +213,7 @@ int lif_layer_forward_chunked(const float* ev_t, const int32_t* ev_src, const in
  * LIF_ST_FLAGS when some delay is negative or not finite (the queues are
  * then in bounds, their order unspecified).  ws: at least
  * lif_delay_queues_workspace_size(B, E_max, N_out) bytes (4 per queue entry, 12
- * when E_max > 8192).
+ * when E_max > 16384).
  * Errors: LIF_ERR_ARG, LIF_ERR_SIZE (B * N_out >= 2^31 or B > 65535),
  * LIF_ERR_WORKSPACE. */
 size_t lif_delay_queues_workspace_size(int B, int E_max, int N_out);

@@ -98,10 +98,13 @@ __global__ __launch_bounds__(256) void k_dly_arrival(const float* __restrict__ e
 // Queues of up to kMax events are sorted in registers and LDS by kThreads
 // threads (kMax / kThreads arrivals each, kBins bins at most): 8192 by 512
 // threads and 11520 by 768 (two workgroups per CU), 16384 by 1024 (112 KB of
-// LDS, one).
+// LDS, one).  Each sort is launched over every (sample, neuron) for which E_max
+// allows a queue in its range and takes those whose queue length (the
+// sample's event count) is above kMin and at most kMax, so that short queues
+// get the sort with the most workgroups per CU whatever E_max is.
 constexpr int kQLdsMax = 16384;         // longest queue sorted in registers and LDS
 
-template <int kMax, int kThreads, int kBins, int kWavesPerEU>
+template <int kMin, int kMax, int kThreads, int kBins, int kWavesPerEU>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kWavesPerEU))) void k_dly_queue_lds(const int32_t* __restrict__ ev_n, int E_max, int N,
                                                                const float* __restrict__ arr,
                                                                float* __restrict__ q_t, int32_t* __restrict__ q_k)
@@ -117,8 +120,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kWaves
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
     const size_t item = blockIdx.x;
     const int b = (int)(item / (size_t)N);
-    const int nb = min(clamp_count(ev_n[b], E_max), kMax);
-    if (nb == 0) return;
+    const int nb = clamp_count(ev_n[b], E_max);
+    if (nb <= kMin || nb > kMax) return;      // empty, or another sort's range
     const size_t base = item * (size_t)E_max;
     // the thread's arrivals (event k = tid + r kThreads), all loads at once
     uint32_t ab[kQR];
@@ -241,7 +244,7 @@ __global__ __launch_bounds__(kQThreads) void k_dly_queue(const int32_t* __restri
     const size_t item = blockIdx.x;
     const int b = (int)(item / (size_t)N);
     const int nb = clamp_count(ev_n[b], E_max);
-    if (nb == 0) return;
+    if (nb <= kQLdsMax) return;               // sorted in LDS
     const size_t base = item * (size_t)E_max;
     const float* ain = arr + base;
     auto key_arrival = [](unsigned long long key) { return __uint_as_float((unsigned)(key >> 32)); };
@@ -1163,16 +1166,15 @@ extern "C" int lif_delay_queues(const float* ev_t, const int32_t* ev_src, const 
         TIMED_LAUNCH("dly_arrival", k_dly_arrival, agrid, dim3(256), 0, stream, ev_t, ev_src, ev_n, E_max, DT, C_in,
                      N_out, arr);
         const dim3 qgrid((unsigned)((size_t)B * N_out));
-        if (E_max <= 8192)
-            TIMED_LAUNCH("dly_queue", (k_dly_queue_lds<8192, 512, 2048, 4>), qgrid, dim3(512), 0, stream, ev_n, E_max,
-                         N_out, arr, q_t, q_k);
-        else if (E_max <= 11520)
-            TIMED_LAUNCH("dly_queue", (k_dly_queue_lds<11520, 768, 2048, 6>), qgrid, dim3(768), 0, stream, ev_n, E_max,
-                         N_out, arr, q_t, q_k);
-        else if (E_max <= kQLdsMax)
-            TIMED_LAUNCH("dly_queue", (k_dly_queue_lds<kQLdsMax, 1024, 4096, 4>), qgrid, dim3(1024), 0, stream, ev_n,
-                         E_max, N_out, arr, q_t, q_k);
-        else
+        TIMED_LAUNCH("dly_queue", (k_dly_queue_lds<0, 8192, 512, 2048, 4>), qgrid, dim3(512), 0, stream, ev_n, E_max,
+                     N_out, arr, q_t, q_k);
+        if (E_max > 8192)
+            TIMED_LAUNCH("dly_queue", (k_dly_queue_lds<8192, 11520, 768, 2048, 6>), qgrid, dim3(768), 0, stream,
+                         ev_n, E_max, N_out, arr, q_t, q_k);
+        if (E_max > 11520)
+            TIMED_LAUNCH("dly_queue", (k_dly_queue_lds<11520, kQLdsMax, 1024, 4096, 4>), qgrid, dim3(1024), 0,
+                         stream, ev_n, E_max, N_out, arr, q_t, q_k);
+        if (E_max > kQLdsMax)
             TIMED_LAUNCH("dly_queue", k_dly_queue, qgrid, dim3(kQThreads), 0, stream, ev_n, E_max, N_out, arr, keys,
                          q_t, q_k);
     }
