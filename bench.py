@@ -303,6 +303,8 @@ def main():
     ap.add_argument("--seq-steps", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true", help="time the headline workload only")
+    ap.add_argument("--extras", default="", metavar="NAMES",
+                    help="comma-separated subset of the other workloads (keys of other_workloads); default all")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="CPU oracle baseline: repeat the bounded sample until this much time has passed")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
@@ -415,26 +417,42 @@ def main():
     extras = {}
     if not args.no_extras:
         st, wu = max(3, args.steps // 10), 2
-        c3 = W.config3()
-        extras["c3_layer1"] = run_workload(torch, lif, d, "700->512 layer 1 of 700->512->512, B=128, ~10k events",
-                                           c3.events, c3.layers[0].WT, lif.Params(s_max=128), st, wu, 1)
-        c4 = W.config4()
-        extras["c4"] = run_workload(torch, lif, d, "2312->1024, B=64, ~20k events in 3 bursts", c4.events,
-                                    c4.layers[0].WT, lif.Params(s_max=64), st, wu, 1)
-        c5 = W.config5()
-        extras["c5_hidden"] = run_workload(torch, lif, d, "32768->2048, B=16, ~100k events (stated gain 4)",
-                                           c5.events, c5.layers[0].WT, lif.Params(s_max=64), st, wu, 1,
-                                           backward=True)
-        W1d = (c5.layers[0].WT * 4.0).astype(np.float32)    # gain 16: the driven variant of the parity tests
-        extras["c5_hidden_driven"] = run_workload(torch, lif, d, "32768->2048, B=16, ~100k events, gain 16",
-                                                  c5.events, W1d, lif.Params(s_max=64), st, wu, 1, backward=True)
-        extras["train_step_c3"] = train_step(torch, lif, d, c3, st, wu)
-        extras["train_step_c3_reg"] = train_step(torch, lif, d, c3, st, wu, "reg")
-        extras["train_step_c3_delays"] = train_step(torch, lif, d, c3, st, wu, "delays")
-        extras["train_step_c3_reg_delays"] = train_step(torch, lif, d, c3, st, wu, "reg_delays")
-        extras["chunk_mode_c2"] = chunk_study(torch, lif, d, ev, WT, st, wu, seq_ms)
-        extras["delays_c2"] = delay_study(torch, lif, d, ev, WT, st, wu, 1)
-        del c3, c4, c5, W1d
+        made = {}
+
+        def cfg(name):                                       # each config built once, when first needed
+            if name not in made:
+                made[name] = getattr(W, name)()
+            return made[name]
+        c3 = cfg("config3")
+        jobs = {
+            "c3_layer1": lambda: run_workload(torch, lif, d, "700->512 layer 1 of 700->512->512, B=128, ~10k events",
+                                              c3.events, c3.layers[0].WT, lif.Params(s_max=128), st, wu, 1),
+            "c4": lambda: run_workload(torch, lif, d, "2312->1024, B=64, ~20k events in 3 bursts",
+                                       cfg("config4").events, cfg("config4").layers[0].WT, lif.Params(s_max=64), st,
+                                       wu, 1),
+            "c5_hidden": lambda: run_workload(torch, lif, d, "32768->2048, B=16, ~100k events (stated gain 4)",
+                                              cfg("config5").events, cfg("config5").layers[0].WT,
+                                              lif.Params(s_max=64), st, wu, 1, backward=True),
+            # gain 16: the driven variant of the parity tests
+            "c5_hidden_driven": lambda: run_workload(torch, lif, d, "32768->2048, B=16, ~100k events, gain 16",
+                                                     cfg("config5").events,
+                                                     (cfg("config5").layers[0].WT * 4.0).astype(np.float32),
+                                                     lif.Params(s_max=64), st, wu, 1, backward=True),
+            "train_step_c3": lambda: train_step(torch, lif, d, c3, st, wu),
+            "train_step_c3_reg": lambda: train_step(torch, lif, d, c3, st, wu, "reg"),
+            "train_step_c3_delays": lambda: train_step(torch, lif, d, c3, st, wu, "delays"),
+            "train_step_c3_reg_delays": lambda: train_step(torch, lif, d, c3, st, wu, "reg_delays"),
+            "chunk_mode_c2": lambda: chunk_study(torch, lif, d, ev, WT, st, wu, seq_ms),
+            "delays_c2": lambda: delay_study(torch, lif, d, ev, WT, st, wu, 1),
+        }
+        pick = [x for x in args.extras.split(",") if x] or list(jobs)
+        unknown = [x for x in pick if x not in jobs]
+        if unknown:
+            print(f"bench.py: unknown --extras {unknown}; known: {list(jobs)}", file=sys.stderr)
+            sys.exit(2)
+        for name in pick:
+            extras[name] = jobs[name]()
+        del c3, made, jobs
 
     # ---- float64 CPU oracle on the host cores (bounded samples)
     cpu = None
