@@ -108,8 +108,11 @@ __global__ __launch_bounds__(256) void k_bwd_setup(const float* __restrict__ ev_
     for (size_t idx = gtid; idx < nn; idx += gs) {
         const int ns = min(out_n[idx], m.s_max);
         const size_t o = idx * (size_t)m.s_max;
-        musum[idx] = spike_adjoints(m, ns, out_t + o, out_i + o, grad_out_t + o, mu + o);
-        klast[idx] = ns > 0 ? out_k[o + ns - 1] : 0;
+        const double ms = spike_adjoints(m, ns, out_t + o, out_i + o, grad_out_t + o, mu + o);
+        musum[idx] = ms;
+        // a neuron whose spikes all have mu = 0 adds exactly 0 everywhere, so
+        // it is not walked (a NaN sum keeps it)
+        klast[idx] = ns > 0 && ms != 0.0 ? out_k[o + ns - 1] : 0;
     }
 }
 

@@ -446,11 +446,13 @@ __device__ __forceinline__ void dly_walk(size_t item, const float* __restrict__ 
                                          int E_max, const float* __restrict__ WT, int C_in, int N, const Model& m,
                                          const float* __restrict__ out_t, const int32_t* __restrict__ out_n,
                                          const int32_t* __restrict__ out_k, const double* __restrict__ mu,
-                                         const double* __restrict__ scale, AddWD add_wd, long long* __restrict__ tq,
-                                         int32_t* __restrict__ tcnt)
+                                         const double* __restrict__ musum, const double* __restrict__ scale,
+                                         AddWD add_wd, long long* __restrict__ tq, int32_t* __restrict__ tcnt)
 {
     const int lane = (int)threadIdx.x % kWave;
-    const int ns = min(out_n[item], m.s_max);
+    // spikes whose adjoints are all 0 add exactly 0 everywhere: not walked
+    // (a NaN sum keeps them)
+    const int ns = musum[item] == 0.0 ? 0 : min(out_n[item], m.s_max);
     const int b = (int)(item / (size_t)N), n = (int)(item % (size_t)N);
     const int nb = clamp_count(ev_n[b], E_max);
     const size_t so = item * (size_t)m.s_max;
@@ -526,8 +528,8 @@ __global__ __launch_bounds__(kWave * kDlyWaves) void k_dly_adjoint(
     const float* __restrict__ q_t, const int32_t* __restrict__ q_k, const int32_t* __restrict__ ev_src,
     const int32_t* __restrict__ ev_n, int B, int E_max, const float* __restrict__ WT, int C_in, int N, Model m,
     const float* __restrict__ out_t, const int32_t* __restrict__ out_n, const int32_t* __restrict__ out_k,
-    const double* __restrict__ mu, const double* __restrict__ scale, long long* __restrict__ gw,
-    long long* __restrict__ gd, long long* __restrict__ tq, int32_t* __restrict__ tcnt)
+    const double* __restrict__ mu, const double* __restrict__ musum, const double* __restrict__ scale,
+    long long* __restrict__ gw, long long* __restrict__ gd, long long* __restrict__ tq, int32_t* __restrict__ tcnt)
 {
     const size_t item = (size_t)blockIdx.x * kDlyWaves + threadIdx.x / kWave;
     if (item >= (size_t)B * N) return;
@@ -538,7 +540,8 @@ __global__ __launch_bounds__(kWave * kDlyWaves) void k_dly_adjoint(
         fx_add(&gw[wi], vw, sW);
         if (gd) fx_add(&gd[wi], vd, sD);
     };
-    dly_walk(item, q_t, q_k, ev_src, ev_n, E_max, WT, C_in, N, m, out_t, out_n, out_k, mu, scale, add_wd, tq, tcnt);
+    dly_walk(item, q_t, q_k, ev_src, ev_n, E_max, WT, C_in, N, m, out_t, out_n, out_k, mu, musum, scale, add_wd, tq,
+             tcnt);
 }
 
 // For C_in <= kDlyLdsMaxC: one workgroup per (neuron, kDlyLdsWaves samples),
@@ -552,8 +555,9 @@ __global__ __launch_bounds__(kWave * kDlyLdsWaves) void k_dly_adjoint_lds(
     const float* __restrict__ q_t, const int32_t* __restrict__ q_k, const int32_t* __restrict__ ev_src,
     const int32_t* __restrict__ ev_n, int B, int E_max, const float* __restrict__ WT, int C_in, int N, Model m,
     const float* __restrict__ out_t, const int32_t* __restrict__ out_n, const int32_t* __restrict__ out_k,
-    const double* __restrict__ mu, const double* __restrict__ scale, long long* __restrict__ gw,
-    long long* __restrict__ gd, long long* __restrict__ tq, int32_t* __restrict__ tcnt, int nbg)
+    const double* __restrict__ mu, const double* __restrict__ musum, const double* __restrict__ scale,
+    long long* __restrict__ gw, long long* __restrict__ gd, long long* __restrict__ tq, int32_t* __restrict__ tcnt,
+    int nbg)
 {
     extern __shared__ long long s_wd[];            // [C_in] dL/dW sums, then [C_in] dL/dD sums
     long long* s_w = s_wd;
@@ -573,8 +577,8 @@ __global__ __launch_bounds__(kWave * kDlyLdsWaves) void k_dly_adjoint_lds(
             atomicAdd((unsigned long long*)&s_w[j], (unsigned long long)llrint(vw * sW));
             if (want_d) atomicAdd((unsigned long long*)&s_d[j], (unsigned long long)llrint(vd * sD));
         };
-        dly_walk((size_t)b * N + n, q_t, q_k, ev_src, ev_n, E_max, WT, C_in, N, m, out_t, out_n, out_k, mu, scale,
-                 add_wd, tq, tcnt);
+        dly_walk((size_t)b * N + n, q_t, q_k, ev_src, ev_n, E_max, WT, C_in, N, m, out_t, out_n, out_k, mu, musum,
+                 scale, add_wd, tq, tcnt);
     }
     __syncthreads();
     for (int j = tid; j < C_in; j += (int)blockDim.x) {
@@ -1259,11 +1263,11 @@ extern "C" int lif_layer_backward_delayed(const float* q_t, const int32_t* q_k, 
             const int nbg = (B + kDlyLdsWaves - 1) / kDlyLdsWaves;
             TIMED_LAUNCH("dly_adjoint", k_dly_adjoint_lds, dim3((unsigned)((size_t)N_out * nbg)),
                          dim3(kWave * kDlyLdsWaves), (size_t)2 * C_in * sizeof(long long), stream, q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N_out, m,
-                         out_t, out_n, out_k, mu, scale, gw, grad_DT ? gd : nullptr, tq, tcnt, nbg);
+                         out_t, out_n, out_k, mu, musum, scale, gw, grad_DT ? gd : nullptr, tq, tcnt, nbg);
         } else {
             TIMED_LAUNCH("dly_adjoint", k_dly_adjoint, dim3((unsigned)((nn + kDlyWaves - 1) / kDlyWaves)),
                          dim3(kWave * kDlyWaves), 0, stream, q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N_out, m,
-                         out_t, out_n, out_k, mu, scale, gw, grad_DT ? gd : nullptr, tq, tcnt);
+                         out_t, out_n, out_k, mu, musum, scale, gw, grad_DT ? gd : nullptr, tq, tcnt);
         }
         if (grad_ev_t) launch_gt_gather(q_k, ev_n, tcnt, tq, (size_t)E_max, B, E_max, N_out, gt, stream);
     }
