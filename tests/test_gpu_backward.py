@@ -217,3 +217,39 @@ def test_backward_deterministic_full_size(env):
     for gW, gT in runs[1:]:
         assert torch.equal(gW.view(torch.int32), runs[0][0].view(torch.int32))
         assert torch.equal(gT.view(torch.int32), runs[0][1].view(torch.int32))
+
+
+@pytest.mark.parametrize("delayed", [False, True])
+def test_backward_neurons_without_gradient(env, delayed):
+    """Upstream gradients on every other neuron only (the others' spikes
+    get 0, so the walks leave them out): dL/dW, dL/dt (and dL/dD) against
+    the oracle on identical inputs, the zero columns exactly zero."""
+    torch, lif = env
+    cfg = W.random_small(24, B=3, C=30, N=40, n_events=500, T=0.4, gain=3.0)
+    ev, WT = cfg.events, cfg.layers[0].WT
+    OP = oracle.LifParams(s_max=64)
+    P = lif.Params(s_max=64)
+    DT = W.uniform_delays(24, 30, 40, d_max=0.05) if delayed else None
+    ref = (oracle.forward_delayed(ev.ev_t, ev.ev_src, ev.ev_n, WT, DT, OP) if delayed
+           else oracle.forward(ev.ev_t, ev.ev_src, ev.ev_n, WT, OP))
+    assert ref.out_n[:, 0::2].sum() > 10 and ref.out_n[:, 1::2].sum() > 10
+    r32 = ref.rounded()
+    rng = np.random.default_rng(24)
+    g = (rng.standard_normal(ref.out_t.shape) * np.isfinite(ref.out_t)).astype(np.float32)
+    g[:, 1::2, :] = 0.0
+    d = [_dev(torch, a) for a in (ev.ev_t, ev.ev_src, ev.ev_n, WT)]
+    fwd = _dev_fwd(torch, lif, r32)
+    if delayed:
+        q = lif.delay_queues(d[0], d[1], d[2], _dev(torch, DT))
+        hW, hD, hT = lif.backward_delayed(q, d[1], d[2], d[3], fwd, _dev(torch, g), P)
+        qW, qD, qT = oracle.backward_delayed(ev.ev_t, ev.ev_src, ev.ev_n, WT, DT, r32, g.astype(np.float64), OP)
+        compare_grad(hD.cpu().numpy(), qD, label="grad_DT, half the neurons without gradient")
+        assert (hD.cpu().numpy()[:, 1::2] == 0).all()
+    else:
+        hW, hT = lif.backward(*d, fwd, _dev(torch, g), P)
+        qW, qT = oracle.backward(ev.ev_t, ev.ev_src, ev.ev_n, WT, r32, g.astype(np.float64), OP)
+    torch.cuda.synchronize()
+    compare_grad(hW.cpu().numpy(), qW, label="grad_WT, half the neurons without gradient")
+    compare_grad(hT.cpu().numpy(), qT, label="grad_ev_t, half the neurons without gradient")
+    assert (hW.cpu().numpy()[:, 1::2] == 0).all()
+    print(f"[case] delayed={delayed} spikes={int(ref.out_n.sum())}", flush=True)
