@@ -377,15 +377,24 @@ __global__ __launch_bounds__(256) void k_dly_setup(size_t nW, size_t nT, long lo
 }
 
 // max |w| over W^T: float bits of non-negative values order like the values,
-// so an integer atomicMax gives the (order-free) maximum.
+// so an integer atomicMax gives the (order-free) maximum; one per workgroup
+// (a few hundred workgroups at most), the waves' maxima joined in LDS.
+constexpr int kWmaxBlocks = 256;
+
 __global__ __launch_bounds__(256) void k_dly_wmax(const float* __restrict__ WT, size_t nW,
                                                  uint32_t* __restrict__ wmax)
 {
+    __shared__ float s_m[256 / kWave];
     const size_t gtid = (size_t)blockIdx.x * blockDim.x + threadIdx.x, gs = (size_t)gridDim.x * blockDim.x;
     float mx = 0.0f;
     for (size_t x = gtid; x < nW; x += gs) mx = fmaxf(mx, fabsf(WT[x]));
     for (int off = kWave / 2; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, kWave));
-    if (threadIdx.x % kWave == 0) atomicMax(wmax, __float_as_uint(mx));
+    if (threadIdx.x % kWave == 0) s_m[threadIdx.x / kWave] = mx;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < 256 / kWave; ++w) mx = fmaxf(mx, s_m[w]);
+        atomicMax(wmax, __float_as_uint(mx));
+    }
 }
 
 // Fixed-point scales (one workgroup).  With M = max over neurons of
@@ -1255,7 +1264,8 @@ extern "C" int lif_layer_backward_delayed(const float* q_t, const int32_t* q_k, 
     if (nn > work) work = nn;
     TIMED_LAUNCH("dly_setup", k_dly_setup, dim3(grid_for(work)), dim3(256), 0, stream, nW, nT, gw, gd, gt, wmax, nn,
                  m, out_t, out_n, out_i, grad_out_t, mu, musum);
-    TIMED_LAUNCH("dly_wmax", k_dly_wmax, dim3(grid_for(nW)), dim3(256), 0, stream, WT, nW, wmax);
+    TIMED_LAUNCH("dly_wmax", k_dly_wmax, dim3(std::min(grid_for(nW), (unsigned)kWmaxBlocks)), dim3(256), 0, stream,
+                 WT, nW, wmax);
     TIMED_LAUNCH("dly_scale", k_dly_scale, dim3(1), dim3(kDlyScaleThreads), 0, stream, musum, nn, ev_n, B, E_max,
                  N_out, m, wmax, scale);
     if (nn && E_max > 0) {
@@ -1401,7 +1411,8 @@ extern "C" int lif_spike_count_reg_delayed_backward(const float* q_t, const int3
     const size_t nW = (size_t)C_in * N_out, nT = (size_t)B * E_max, nn = (size_t)B * N_out;
     const size_t work = nW > nT ? nW : nT;
     TIMED_LAUNCH("dregg_zero", k_dregg_zero, dim3(grid_for(work)), dim3(256), 0, stream, nW, nT, gw, gd, gt, wmax);
-    TIMED_LAUNCH("dly_wmax", k_dly_wmax, dim3(grid_for(nW)), dim3(256), 0, stream, WT, nW, wmax);
+    TIMED_LAUNCH("dly_wmax", k_dly_wmax, dim3(std::min(grid_for(nW), (unsigned)kWmaxBlocks)), dim3(256), 0, stream,
+                 WT, nW, wmax);
     launch_dreg_walk(q_t, q_k, ev_src, ev_n, B, E_max, WT, C_in, N_out, m, out_t, out_n, out_k, ub, ob, nullptr,
                      nullptr, counts, vpmax, rec, stream);
     if (B > 0) {
